@@ -1,0 +1,132 @@
+/*
+ * flashgmm.h - C ABI of the fused diagonal-covariance GMM EM iteration for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * Model (Flash-GMM paper, Sec. 2, with a diagonal covariance in place of the
+ * paper's isotropic sigma_k^2 I): K components with weights pi_k, means
+ * mu_k in R^D and per-dimension variances var_kd.
+ *
+ * Conventions shared by every entry point
+ *   - Every pointer argument is a DEVICE pointer owned by the caller; the
+ *     library never allocates and never frees.  Scratch memory comes from the
+ *     caller's workspace `ws` of `ws_bytes` bytes, sized by
+ *     gmm_workspace_bytes().  The workspace must be 256-byte aligned.
+ *   - Layouts are row-major and contiguous: x[n*d], means/vars/s/q[k*d],
+ *     weights/nk[k].  Parameters are fp32, statistics fp64.
+ *   - Every call only enqueues work on `stream` and returns; results are
+ *     valid once the caller synchronises the stream.  Calls that share a
+ *     workspace must be ordered on one stream.
+ *   - Errors: argument checks run on the host before anything is enqueued and
+ *     return a negative gmm_status (nothing is enqueued then).  A HIP error
+ *     reported at launch returns GMM_ERR_DEVICE.  NaN or Inf in the inputs is
+ *     not checked; it propagates into the outputs.
+ *   - Limits: 1 <= d <= GMM_MAX_D, 1 <= k <= GMM_MAX_K, n >= 1 (n may exceed
+ *     2^31), 1 <= m <= GMM_MAX_M.  Shapes beyond them return
+ *     GMM_ERR_UNSUPPORTED.
+ *   - Results are bitwise deterministic for a given (n, d, k) and inputs: no
+ *     atomics; every reduction runs in a fixed order.
+ */
+#ifndef FLASHGMM_H
+#define FLASHGMM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GMM_MAX_D 256
+#define GMM_MAX_K 65536
+#define GMM_MAX_M 8
+
+typedef enum {
+  GMM_OK = 0,
+  GMM_ERR_INVALID_ARG = -1, /* null pointer, non-positive size, bad m/tau */
+  GMM_ERR_UNSUPPORTED = -2, /* d, k or m beyond the library's limits */
+  GMM_ERR_WORKSPACE = -3,   /* workspace missing, misaligned or too small */
+  GMM_ERR_DEVICE = -4       /* a HIP call or kernel launch failed */
+} gmm_status;
+
+/* Human-readable name of a status code (static string). */
+const char* gmm_status_string(int status);
+
+/*
+ * Bytes of workspace needed by gmm_estep_accumulate / gmm_fit (m = 0) or by
+ * gmm_assign_topk (m >= 1) for n points in d dimensions and k components.
+ * Returns 0 when the shape is unsupported.  The size grows as O(n) (one fp32
+ * log-normaliser per point) plus O(k d) for the parameters and the
+ * per-workgroup partial statistics; it never holds an n x k array.
+ */
+size_t gmm_workspace_bytes(int64_t n, int32_t d, int32_t k, int32_t m);
+
+/*
+ * E-step and sufficient statistics of one EM iteration (Sec. 3.1 and
+ * Algorithm 1 of the paper, steps 1-2, with the diagonal model): at the
+ * parameters (weights, means, vars), for every point i and component k
+ *   l_ik   = log pi_k + log N(x_i | mu_k, diag var_k)
+ *   log Z_i = log sum_k exp(l_ik),  r_ik = exp(l_ik - log Z_i)
+ * and ADDS into the caller's fp64 accumulators
+ *   nk[k]     += sum_i r_ik
+ *   s[k*d+j]  += sum_i r_ik x_ij
+ *   q[k*d+j]  += sum_i r_ik x_ij^2
+ *   *loglik   += sum_i log Z_i          (natural log, 2*pi constant included)
+ * The caller zeroes them first; adding lets row chunks of one data set, or
+ * shards of it, be accumulated into one set of statistics.
+ * Components with weight 0 are dead: l_ik = -inf, they receive nothing.
+ * The n x k responsibility matrix is never stored.
+ *   x        [n*d] fp32 points          weights [k] fp32 (>= 0)
+ *   means    [k*d] fp32                 vars    [k*d] fp32 (> 0)
+ *   nk       [k] fp64, s/q [k*d] fp64, loglik [1] fp64 (all +=)
+ */
+int gmm_estep_accumulate(const float* x, int64_t n, int32_t d, int32_t k, const float* weights,
+                         const float* means, const float* vars, double* nk, double* s, double* q,
+                         double* loglik, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * M-step from the statistics (paper Eqs. Nk, muk, sig and Algorithm 1's
+ * final step, per dimension), in fp64, written back as fp32 parameters:
+ *   pi_k    = nk[k] / n_total
+ *   mu_kj   = s[k*d+j] / nk[k]
+ *   var_kj  = max(var_floor, q[k*d+j] / nk[k] - mu_kj^2)
+ * A component with nk[k] == 0 exactly keeps its mean and variances and gets
+ * weight 0.  weights/means/vars hold the old parameters on entry (needed for
+ * that rule) and the new ones on return.  n_total > 0, var_floor >= 0.
+ */
+int gmm_mstep(const double* nk, const double* s, const double* q, double n_total, int32_t d,
+              int32_t k, float var_floor, float* weights, float* means, float* vars,
+              hipStream_t stream);
+
+/*
+ * n_iters full EM iterations from Theta_0 = (weights, means, vars), updated
+ * in place to Theta_{n_iters}.  loglik_hist[t] (fp64, device, n_iters
+ * entries) receives LL(Theta_t), the log-likelihood computed in iteration
+ * t's E-step, before its M-step.  Each iteration is gmm_estep_accumulate
+ * followed by gmm_mstep with n_total = n.  Resuming means calling again with
+ * the returned parameters.
+ */
+int gmm_fit(const float* x, int64_t n, int32_t d, int32_t k, int32_t n_iters, float var_floor,
+            float* weights, float* means, float* vars, double* loglik_hist, void* ws,
+            size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Top-m multi-assignment (Sec. 4.2 single assignment, Sec. 4.3 multiple
+ * assignment): a fresh E-step at the given parameters; for every point the
+ * components ranked by responsibility (ties to the lower index).  Rank 1 is
+ * always assigned; rank j > 1 is assigned only if its responsibility is
+ * strictly greater than tau (the paper uses m = 2, tau = 1/K).
+ *   idx  [n*m] int32: component indices, -1 for an empty slot
+ *   resp [n*m] fp32 : their responsibilities, 0 for an empty slot
+ * 1 <= m <= GMM_MAX_M and m <= k; 0 <= tau < 1.
+ */
+int gmm_assign_topk(const float* x, int64_t n, int32_t d, int32_t k, const float* weights,
+                    const float* means, const float* vars, int32_t m, float tau, int32_t* idx,
+                    float* resp, void* ws, size_t ws_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FLASHGMM_H */

@@ -1,0 +1,166 @@
+"""Python binding of ``libflashgmm.so``: the fused diagonal-GMM EM iteration on MI355X.
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels of ``csrc/flashgmm.hip``.  PyTorch provides the device memory (CUDA
+tensors on ROCm) and the stream (``torch.cuda.current_stream()``); the entry
+points take the same names and arguments as the C ABI in
+``include/flashgmm.h``.  There is no CPU fallback: without the built library
+every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libflashgmm.so")
+
+GMM_OK = 0
+GMM_ERR_INVALID_ARG = -1
+GMM_ERR_UNSUPPORTED = -2
+GMM_ERR_WORKSPACE = -3
+GMM_ERR_DEVICE = -4
+GMM_MAX_D = 256
+GMM_MAX_K = 65536
+GMM_MAX_M = 8
+
+#: every symbol the C ABI exports
+EXPORTS = ("gmm_status_string", "gmm_workspace_bytes", "gmm_estep_accumulate", "gmm_mstep",
+           "gmm_fit", "gmm_assign_topk")
+
+_lib = None
+
+
+class GMMError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        self.status = status
+        super().__init__(f"{fn} failed: {status_string(status)} ({status})")
+
+
+def load_library():
+    """Loads libflashgmm.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_2606_10896_amd.build "
+                           "(no CPU fallback exists)")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i64, i32, f32, f64 = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_float,
+                              ctypes.c_double)
+    lib.gmm_status_string.argtypes = [ctypes.c_int]
+    lib.gmm_status_string.restype = ctypes.c_char_p
+    lib.gmm_workspace_bytes.argtypes = [i64, i32, i32, i32]
+    lib.gmm_workspace_bytes.restype = ctypes.c_size_t
+    lib.gmm_estep_accumulate.argtypes = [vp, i64, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp,
+                                         ctypes.c_size_t, vp]
+    lib.gmm_estep_accumulate.restype = ctypes.c_int
+    lib.gmm_mstep.argtypes = [vp, vp, vp, f64, i32, i32, f32, vp, vp, vp, vp]
+    lib.gmm_mstep.restype = ctypes.c_int
+    lib.gmm_fit.argtypes = [vp, i64, i32, i32, i32, f32, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.gmm_fit.restype = ctypes.c_int
+    lib.gmm_assign_topk.argtypes = [vp, i64, i32, i32, vp, vp, vp, i32, f32, vp, vp, vp,
+                                    ctypes.c_size_t, vp]
+    lib.gmm_assign_topk.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load_library().gmm_status_string(int(status)).decode()
+
+
+def workspace_bytes(n: int, d: int, k: int, m: int = 0) -> int:
+    """Workspace size for (n, d, k); m > 0 sizes it for gmm_assign_topk."""
+    return int(load_library().gmm_workspace_bytes(int(n), int(d), int(k), int(m)))
+
+
+# ------------------------------------------------------------------ tensor helpers
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _check(fn, rc):
+    if rc != GMM_OK:
+        raise GMMError(fn, rc)
+
+
+def _dev(t, dtype, name):
+    import torch
+    if not (isinstance(t, torch.Tensor) and t.is_cuda and t.dtype == dtype and t.is_contiguous()):
+        raise TypeError(f"{name} must be a contiguous {dtype} CUDA tensor")
+    return t
+
+
+def workspace(n: int, d: int, k: int, m: int = 0, device="cuda"):
+    """A workspace tensor (uint8, 256-byte aligned by the caching allocator)."""
+    import torch
+    nb = workspace_bytes(n, d, k, m)
+    if nb == 0:
+        raise GMMError("gmm_workspace_bytes", GMM_ERR_UNSUPPORTED)
+    return torch.empty(nb, dtype=torch.uint8, device=device)
+
+
+def gmm_estep_accumulate(x, weights, means, variances, nk, s, q, loglik, ws, stream=None):
+    """Adds the E-step statistics of x at (weights, means, variances) into fp64 nk, s, q and
+    loglik (all CUDA tensors)."""
+    import torch
+    _dev(x, torch.float32, "x")
+    n, d = x.shape
+    k = weights.shape[0]
+    rc = load_library().gmm_estep_accumulate(
+        _ptr(x), n, d, k, _ptr(_dev(weights, torch.float32, "weights")),
+        _ptr(_dev(means, torch.float32, "means")), _ptr(_dev(variances, torch.float32, "vars")),
+        _ptr(_dev(nk, torch.float64, "nk")), _ptr(_dev(s, torch.float64, "s")),
+        _ptr(_dev(q, torch.float64, "q")), _ptr(_dev(loglik, torch.float64, "loglik")),
+        _ptr(ws), ws.numel() if ws is not None else 0, _stream(stream))
+    _check("gmm_estep_accumulate", rc)
+
+
+def gmm_mstep(nk, s, q, n_total, weights, means, variances, var_floor=1e-6, stream=None):
+    """M-step from fp64 statistics; updates fp32 weights/means/variances in place."""
+    import torch
+    k, d = means.shape
+    rc = load_library().gmm_mstep(
+        _ptr(_dev(nk, torch.float64, "nk")), _ptr(_dev(s, torch.float64, "s")),
+        _ptr(_dev(q, torch.float64, "q")), float(n_total), d, k, float(var_floor),
+        _ptr(_dev(weights, torch.float32, "weights")), _ptr(_dev(means, torch.float32, "means")),
+        _ptr(_dev(variances, torch.float32, "vars")), _stream(stream))
+    _check("gmm_mstep", rc)
+
+
+def gmm_fit(x, weights, means, variances, n_iters, loglik_hist, ws, var_floor=1e-6, stream=None):
+    """n_iters EM iterations; parameters updated in place, loglik_hist[t] = LL(Theta_t)."""
+    import torch
+    _dev(x, torch.float32, "x")
+    n, d = x.shape
+    k = weights.shape[0]
+    rc = load_library().gmm_fit(
+        _ptr(x), n, d, k, int(n_iters), float(var_floor),
+        _ptr(_dev(weights, torch.float32, "weights")), _ptr(_dev(means, torch.float32, "means")),
+        _ptr(_dev(variances, torch.float32, "vars")),
+        _ptr(_dev(loglik_hist, torch.float64, "loglik_hist")), _ptr(ws),
+        ws.numel() if ws is not None else 0, _stream(stream))
+    _check("gmm_fit", rc)
+
+
+def gmm_assign_topk(x, weights, means, variances, m, tau, idx, resp, ws, stream=None):
+    """Top-m multi-assignment into idx (int32 [n, m]) and resp (fp32 [n, m])."""
+    import torch
+    _dev(x, torch.float32, "x")
+    n, d = x.shape
+    k = weights.shape[0]
+    rc = load_library().gmm_assign_topk(
+        _ptr(x), n, d, k, _ptr(_dev(weights, torch.float32, "weights")),
+        _ptr(_dev(means, torch.float32, "means")), _ptr(_dev(variances, torch.float32, "vars")),
+        int(m), float(tau), _ptr(_dev(idx, torch.int32, "idx")),
+        _ptr(_dev(resp, torch.float32, "resp")), _ptr(ws), ws.numel() if ws is not None else 0,
+        _stream(stream))
+    _check("gmm_assign_topk", rc)

@@ -1,0 +1,921 @@
+// Fused diagonal-covariance GMM EM iteration for AMD Instinct MI355X (gfx950).
+//
+// One EM iteration (Flash-GMM paper, Sec. 3.1 and Algorithm 1, with the
+// diagonal model) is computed without ever storing the n x k responsibility
+// matrix:
+//
+//   prep        per component: the expanded-form operands
+//                 W_kd = mu_kd / var_kd,  P_kd = -1/2 / var_kd,
+//                 c_k  = log pi_k - 1/2 sum_d (mu_kd^2 / var_kd + log(2 pi var_kd))
+//               (computed in fp64, stored fp32, all pre-scaled by log2(e) so
+//               the kernels work in base 2), packed in the register order the
+//               32x32x2 fp32 MFMA consumes them.
+//   logz        Step 1 of Algorithm 1: log-densities l = [x | x^2] . [W | P]^T + c
+//               on MFMA, an online log-sum-exp over all components, one fp32
+//               log-normaliser per point and per-workgroup log-likelihood
+//               partials.
+//   stats       Step 2 of Algorithm 1: the same log-densities recomputed for a
+//               32-component slice, r = 2^(l - log2 Z) kept on chip, and the
+//               statistic contraction r^T [x | x^2] in fp64 on the vector ALU
+//               (exact products), into per-workgroup partials.
+//   reduce      fixed-order fp64 sums of the partials (instead of the paper's
+//               atomics), added into the caller's accumulators.
+//   mstep       closed-form M-step (Eqs. Nk, muk, sig per dimension) in fp64.
+//
+// Conditioning.  The expanded form sums terms of size about mu^2/var that
+// cancel; its fp32 rounding error grows like u * sum_d (mu_kd^2 + var_kd)/var_kd.
+// Components that have shrunk onto a few points (tiny variances) make this
+// sum reach 1e5..1e9, where fp32 logits are meaningless.  Such components are
+// routed to the direct form (x - mu)^2 / var on the vector ALU, whose fp32
+// error is relative to the result.  Routing depends only on the parameters.
+// The statistics are fp64 for every component: the M-step forms the variance
+// as q/n - mu^2, which cancels by a factor mu^2/var that reaches 1e7 for a
+// component collapsing onto one point, beyond any fp32 accumulation.
+//
+// No atomics anywhere: results are bitwise reproducible run to run.
+
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#include "flashgmm.h"
+
+namespace {
+
+constexpr int kBK = 32;                 // components per MFMA block
+constexpr double kLog2e = 1.4426950408889634073599246810019;
+constexpr double kLn2 = 0.69314718055994530941723212145818;
+constexpr double kLog2Pi = 1.8378770664093454835606594728112;  // log(2 pi)
+// routing threshold (see header comment) on sum_d (mu^2 + var) / var: below it
+// the fp32 expanded form is good to ~1e-2 in log2 units, plenty for screening
+constexpr double kIllSum = 2.0e5;
+constexpr int kT = 4;                   // exact responsibilities stored per point
+constexpr float kWindow = 40.0f;        // refine components with r > 2^-40
+
+typedef float f16v __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ f16v mfma32(float a, float b, f16v c) {
+  return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float exp2_fast(float v) { return __builtin_amdgcn_exp2f(v); }
+
+// ---------------------------------------------------------------- online LSE (base 2)
+// State (m, s) represents log2 sum_j 2^(l_j) = m + log2 s, with m = -inf, s = 0
+// for the empty set.
+__device__ __forceinline__ void lse_add(float& m, float& s, float l) {
+  const float dl = l - m;                      // NaN only when both are -inf
+  const float e = exp2_fast(-fabsf(dl));
+  const bool gt = l > m;
+  const float s_gt = __fmaf_rn(s, e, 1.0f);
+  const float s_le = s + e;
+  s = gt ? s_gt : ((l > -INFINITY) ? s_le : s);
+  m = gt ? l : m;
+}
+
+__device__ __forceinline__ void lse_merge(float& m, float& s, float m2, float s2) {
+  const float mm = fmaxf(m, m2);
+  if (mm == -INFINITY) { m = -INFINITY; s = 0.0f; return; }
+  s = s * exp2_fast(m - mm) + s2 * exp2_fast(m2 - mm);
+  m = mm;
+}
+
+// ---------------------------------------------------------------- tiles
+// rows x D64 fp32 tile of x (rows [r0, r0+rows)) into LDS with row pitch D64+4;
+// rows >= nend and columns >= d are zero.
+template <int D64>
+__device__ __forceinline__ void load_tile(const float* __restrict__ x, int64_t nend, int d,
+                                          int64_t r0, int rows, float* xs, bool vec4) {
+  constexpr int P = D64 + 4;
+  if (vec4) {
+    constexpr int Q4 = D64 / 4;
+    for (int idx = threadIdx.x; idx < rows * Q4; idx += blockDim.x) {
+      const int r = idx / Q4, c = (idx % Q4) * 4;
+      const int64_t nn = r0 + r;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (nn < nend && c < d) v = *reinterpret_cast<const float4*>(x + nn * d + c);
+      *reinterpret_cast<float4*>(xs + r * P + c) = v;
+    }
+  } else {
+    for (int idx = threadIdx.x; idx < rows * D64; idx += blockDim.x) {
+      const int r = idx / D64, c = idx % D64;
+      const int64_t nn = r0 + r;
+      xs[r * P + c] = (nn < nend && c < d) ? x[nn * d + c] : 0.0f;
+    }
+  }
+}
+
+// ---------------------------------------------------------------- expanded-form logits (MFMA)
+// Contraction order (identical wherever log-densities are formed, so the two
+// passes agree bit for bit): chain 0 runs over the x part, chain 1 over the
+// x^2 part; step s of a chain feeds lane half h the dimension
+// 8*(s/4) + 4*h + s%4; l = (chain0 + chain1) + c.
+// Output layout (32x32 accumulator): register v of lane l holds point
+// row0 + 8*(v/4) + 4*(l/32) + v%4 and component slot l%32 of the block.
+
+template <int D64>
+__device__ __forceinline__ void logits_block(const float* xs, int row0,
+                                             const float4* __restrict__ wp, float cbias,
+                                             f16v& out) {
+  constexpr int P = D64 + 4, QH = D64 / 8;
+  const int lane = threadIdx.x & 63, h = lane >> 5, col = lane & 31;
+  const float* xr = xs + (row0 + col) * P + 4 * h;
+  f16v a0 = {}, a1 = {};
+#pragma unroll
+  for (int q = 0; q < QH; ++q) {
+    const float4 b0 = wp[q * 64 + lane];
+    const float4 b1 = wp[(QH + q) * 64 + lane];
+    const float4 a = *reinterpret_cast<const float4*>(xr + 8 * q);
+    a0 = mfma32(a.x, b0.x, a0);
+    a1 = mfma32(a.x * a.x, b1.x, a1);
+    a0 = mfma32(a.y, b0.y, a0);
+    a1 = mfma32(a.y * a.y, b1.y, a1);
+    a0 = mfma32(a.z, b0.z, a0);
+    a1 = mfma32(a.z * a.z, b1.z, a1);
+    a0 = mfma32(a.w, b0.w, a0);
+    a1 = mfma32(a.w * a.w, b1.w, a1);
+  }
+#pragma unroll
+  for (int v = 0; v < 16; ++v) out[v] = (a0[v] + a1[v]) + cbias;
+}
+
+// Two 32-point blocks (rows 0..31 and 32..63) against one component block,
+// sharing the parameter operand; each block's chains are those of logits_block.
+template <int D64>
+__device__ __forceinline__ void logits_2blocks(const float* xs, const float4* __restrict__ wp,
+                                               float cbias, f16v& o0, f16v& o1) {
+  constexpr int P = D64 + 4, QH = D64 / 8;
+  const int lane = threadIdx.x & 63, h = lane >> 5, col = lane & 31;
+  const float* xr0 = xs + col * P + 4 * h;
+  const float* xr1 = xs + (32 + col) * P + 4 * h;
+  f16v a0 = {}, a1 = {}, c0 = {}, c1 = {};
+#pragma unroll
+  for (int q = 0; q < QH; ++q) {
+    const float4 b0 = wp[q * 64 + lane];
+    const float4 b1 = wp[(QH + q) * 64 + lane];
+    const float4 a = *reinterpret_cast<const float4*>(xr0 + 8 * q);
+    const float4 c = *reinterpret_cast<const float4*>(xr1 + 8 * q);
+    a0 = mfma32(a.x, b0.x, a0);
+    c0 = mfma32(c.x, b0.x, c0);
+    a1 = mfma32(a.x * a.x, b1.x, a1);
+    c1 = mfma32(c.x * c.x, b1.x, c1);
+    a0 = mfma32(a.y, b0.y, a0);
+    c0 = mfma32(c.y, b0.y, c0);
+    a1 = mfma32(a.y * a.y, b1.y, a1);
+    c1 = mfma32(c.y * c.y, b1.y, c1);
+    a0 = mfma32(a.z, b0.z, a0);
+    c0 = mfma32(c.z, b0.z, c0);
+    a1 = mfma32(a.z * a.z, b1.z, a1);
+    c1 = mfma32(c.z * c.z, b1.z, c1);
+    a0 = mfma32(a.w, b0.w, a0);
+    c0 = mfma32(c.w, b0.w, c0);
+    a1 = mfma32(a.w * a.w, b1.w, a1);
+    c1 = mfma32(c.w * c.w, b1.w, c1);
+  }
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    o0[v] = (a0[v] + a1[v]) + cbias;
+    o1[v] = (c0[v] + c1[v]) + cbias;
+  }
+}
+
+// ---------------------------------------------------------------- direct-form logits (VALU)
+// l2 = c - sum_d (x_d - mu_d)^2 * hh_d, hh = log2(e) / (2 var), summed in
+// dimension order; padded dimensions have x = mu = hh = 0.
+template <int D64>
+__device__ __forceinline__ float ill_logit(const float* xrow, const float* __restrict__ mu,
+                                           const float* __restrict__ hh, float c) {
+  float acc = 0.0f;
+#pragma unroll 4
+  for (int j = 0; j < D64; j += 4) {
+    const float4 xv = *reinterpret_cast<const float4*>(xrow + j);
+    const float4 m = *reinterpret_cast<const float4*>(mu + j);
+    const float4 g = *reinterpret_cast<const float4*>(hh + j);
+    float t;
+    t = xv.x - m.x; acc = __fmaf_rn(__fmul_rn(t, t), g.x, acc);
+    t = xv.y - m.y; acc = __fmaf_rn(__fmul_rn(t, t), g.y, acc);
+    t = xv.z - m.z; acc = __fmaf_rn(__fmul_rn(t, t), g.z, acc);
+    t = xv.w - m.w; acc = __fmaf_rn(__fmul_rn(t, t), g.w, acc);
+  }
+  return c - acc;
+}
+
+// ---------------------------------------------------------------- prep
+// Workspace counters: [0] well components, [1] ill-conditioned components,
+// [2] well 32-blocks, [3] ill 32-blocks.
+
+__global__ __launch_bounds__(64) void k_prep_class(const float* __restrict__ w,
+                                                   const float* __restrict__ mu,
+                                                   const float* __restrict__ var, int d,
+                                                   int* __restrict__ cls,
+                                                   double* __restrict__ cwell,
+                                                   double* __restrict__ cdir) {
+  const int comp = blockIdx.x, lane = threadIdx.x;
+  double e = 0.0, lg = 0.0;
+  for (int j = lane; j < d; j += 64) {
+    const double m = mu[(int64_t)comp * d + j], v = var[(int64_t)comp * d + j];
+    e += m * m / v;
+    lg += kLog2Pi + log(v);
+  }
+  for (int off = 32; off > 0; off >>= 1) {
+    e += __shfl_xor(e, off);
+    lg += __shfl_xor(lg, off);
+  }
+  if (lane == 0) {
+    const double wk = w[comp];
+    int c;
+    if (!(wk > 0.0)) c = 2;
+    else if (e + d > kIllSum || !(e == e)) c = 1;
+    else c = 0;
+    cls[comp] = c;
+    const double lw = wk > 0.0 ? log(wk) : -INFINITY;
+    cwell[comp] = kLog2e * (lw - 0.5 * (e + lg));
+    cdir[comp] = kLog2e * (lw - 0.5 * lg);
+  }
+}
+
+__global__ __launch_bounds__(256) void k_prep_scan(const int* __restrict__ cls, int k,
+                                                   int* __restrict__ well_idx,
+                                                   int* __restrict__ ill_idx,
+                                                   int* __restrict__ counts) {
+  __shared__ int cw[256], ci[256];
+  const int t = threadIdx.x;
+  const int b = (int)((int64_t)k * t / 256), e = (int)((int64_t)k * (t + 1) / 256);
+  int nw = 0, ni = 0;
+  for (int c = b; c < e; ++c) { nw += cls[c] == 0; ni += cls[c] == 1; }
+  cw[t] = nw;
+  ci[t] = ni;
+  __syncthreads();
+  if (t == 0) {
+    int aw = 0, ai = 0;
+    for (int i = 0; i < 256; ++i) {
+      const int x = cw[i], y = ci[i];
+      cw[i] = aw; ci[i] = ai;
+      aw += x; ai += y;
+    }
+    counts[0] = aw;
+    counts[1] = ai;
+    counts[2] = (aw + kBK - 1) / kBK;
+    counts[3] = (ai + kBK - 1) / kBK;
+  }
+  __syncthreads();
+  int pw = cw[t], pi = ci[t];
+  for (int c = b; c < e; ++c) {
+    if (cls[c] == 0) well_idx[pw++] = c;
+    else if (cls[c] == 1) ill_idx[pi++] = c;
+  }
+}
+
+// Packed expanded-form operand: wp[(kb*(D64/4) + q)*64 + lane] is the float4 of
+// MFMA steps 4q..4q+3 for lane `lane` of component block kb.
+template <int D64>
+__global__ __launch_bounds__(256) void k_prep_pack_well(
+    const float* __restrict__ mu, const float* __restrict__ var, int d, int kpad,
+    const double* __restrict__ cwell, const int* __restrict__ counts,
+    const int* __restrict__ well_idx, float4* __restrict__ wp, float* __restrict__ cw) {
+  constexpr int QQ = D64 / 4, QH = D64 / 8;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (int64_t)kpad * QQ * 2) return;   // kpad/32 blocks * QQ * 64 lanes
+  const int lane = (int)(t & 63);
+  const int q = (int)((t >> 6) % QQ);
+  const int kb = (int)((t >> 6) / QQ);
+  const int slot = kb * kBK + (lane & 31), h = lane >> 5;
+  const int nw = counts[0];
+  const int comp = slot < nw ? well_idx[slot] : -1;
+  const bool xpart = q < QH;
+  const int qq = xpart ? q : q - QH;
+  float vals[4];
+  for (int i = 0; i < 4; ++i) {
+    const int j = 8 * qq + 4 * h + i;
+    float v = 0.0f;
+    if (comp >= 0 && j < d) {
+      const double m = mu[(int64_t)comp * d + j], s2 = var[(int64_t)comp * d + j];
+      v = xpart ? (float)(kLog2e * m / s2) : (float)(-0.5 * kLog2e / s2);
+    }
+    vals[i] = v;
+  }
+  wp[t] = make_float4(vals[0], vals[1], vals[2], vals[3]);
+  if (q == 0 && h == 0) cw[slot] = comp >= 0 ? (float)cwell[comp] : -INFINITY;
+}
+
+// Direct-form parameters of every component (indexed by component):
+// dmu = mu, dh = log2(e) / (2 var), dc = log2(e) (log pi - 1/2 sum_d log(2 pi var)),
+// zero-padded to D64 dimensions.
+template <int D64>
+__global__ __launch_bounds__(256) void k_prep_pack_direct(
+    const float* __restrict__ mu, const float* __restrict__ var, int d, int k,
+    const double* __restrict__ cdir, float* __restrict__ dmu, float* __restrict__ dh,
+    float* __restrict__ dc) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (int64_t)k * D64) return;
+  const int comp = (int)(t / D64), j = (int)(t % D64);
+  float m = 0.0f, g = 0.0f;
+  if (j < d) {
+    m = mu[(int64_t)comp * d + j];
+    g = (float)(0.5 * kLog2e / (double)var[(int64_t)comp * d + j]);
+  }
+  dmu[t] = m;
+  dh[t] = g;
+  if (j == 0) dc[comp] = (float)cdir[comp];
+}
+
+// ---------------------------------------------------------------- Step 1: log-normalisers
+// One workgroup = 64 points, 4 waves; wave w takes well component blocks w,
+// w+4, ... and ill-conditioned components w, w+4, ...
+//
+//   1. screen: expanded-form log-densities on MFMA with a per-lane online LSE
+//      that also remembers the arg-max; a "lane state" (wave, lane column,
+//      point) covers every 32nd component of the wave's blocks.
+//   2. the lane states are merged (within the wave by butterflies, then across
+//      waves in a fixed order) into a screening log2 Z per point.
+//   3. refinement: every lane state whose maximum lies within kWindow of that
+//      log2 Z marks its arg-max component as a candidate; the candidates'
+//      log-densities are recomputed in the direct form (fp32 error relative to
+//      the result), their screened terms are taken out of the sum and the exact
+//      ones put in.  The result is the log2 Z written for the point, and the
+//      kT largest exact responsibilities are stored for the statistics pass.
+// A significant component is missed only if a larger one of the same point
+// shares its lane state; its responsibility then keeps the screening error.
+template <int D64>
+__global__ __launch_bounds__(256) void k_logz(
+    const float* __restrict__ x, int64_t n, int d, int vec4, const float4* __restrict__ wp,
+    const float* __restrict__ cw, const int* __restrict__ well_idx,
+    const int* __restrict__ ill_idx, const float* __restrict__ dmu,
+    const float* __restrict__ dh, const float* __restrict__ dc, const int* __restrict__ counts,
+    float* __restrict__ logz2, int* __restrict__ cslot, float* __restrict__ cr,
+    double* __restrict__ ll_part) {
+  constexpr int P = D64 + 4;
+  __shared__ __align__(16) float xs[64 * P];
+  __shared__ float2 stw[4][64];      // per wave: merged well state (M_w, S_w) per point
+  __shared__ float2 sti[4][64];      // per wave: ill state per point
+  __shared__ float cms[4][64];       // per wave: candidate mass relative to M_w
+  __shared__ float lzm[64];          // screening log2 Z
+  __shared__ unsigned cmask[64][4];  // candidate lane columns per (point, wave)
+  __shared__ int cidx[64][128];      // arg-max well slot per (point, lane state)
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, h = lane >> 5, col = lane & 31;
+  const int64_t n0 = (int64_t)blockIdx.x * 64;
+  load_tile<D64>(x, n, d, n0, 64, xs, vec4 != 0);
+  __syncthreads();
+  const int n_wkb = counts[2], n_ill = counts[1];
+
+  float m0[16], s0[16], m1[16], s1[16];
+  int a0[16], a1[16];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    m0[v] = m1[v] = -INFINITY;
+    s0[v] = s1[v] = 0.0f;
+    a0[v] = a1[v] = -1;
+  }
+  for (int kb = wave; kb < n_wkb; kb += 4) {
+    f16v l0, l1;
+    logits_2blocks<D64>(xs, wp + (size_t)kb * (D64 / 4) * 64, cw[kb * kBK + col], l0, l1);
+    const int slot = kb * kBK + col;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      a0[v] = l0[v] > m0[v] ? slot : a0[v];
+      lse_add(m0[v], s0[v], l0[v]);
+      a1[v] = l1[v] > m1[v] ? slot : a1[v];
+      lse_add(m1[v], s1[v], l1[v]);
+    }
+  }
+  // arg-max of every lane state, and the per-wave merged state of every point
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int p = 8 * (v >> 2) + 4 * h + (v & 3);
+    cidx[p][wave * 32 + col] = a0[v];
+    cidx[32 + p][wave * 32 + col] = a1[v];
+    float M0 = m0[v], S0 = s0[v], M1 = m1[v], S1 = s1[v];
+    for (int off = 16; off > 0; off >>= 1) {
+      lse_merge(M0, S0, __shfl_xor(M0, off), __shfl_xor(S0, off));
+      lse_merge(M1, S1, __shfl_xor(M1, off), __shfl_xor(S1, off));
+    }
+    if (col == 0) {
+      stw[wave][p] = make_float2(M0, S0);
+      stw[wave][32 + p] = make_float2(M1, S1);
+    }
+  }
+  // ill-conditioned components, direct form, lane = point
+  float mi = -INFINITY, si = 0.0f;
+  for (int ki = wave; ki < n_ill; ki += 4) {
+    const int comp = ill_idx[ki];
+    const float l = ill_logit<D64>(xs + lane * P, dmu + (size_t)comp * D64,
+                                   dh + (size_t)comp * D64, dc[comp]);
+    lse_add(mi, si, l);
+  }
+  sti[wave][lane] = make_float2(mi, si);
+  __syncthreads();
+  if (tid < 64) {
+    float mm = -INFINITY, ss = 0.0f;
+    for (int w2 = 0; w2 < 4; ++w2) {
+      lse_merge(mm, ss, stw[w2][tid].x, stw[w2][tid].y);
+      lse_merge(mm, ss, sti[w2][tid].x, sti[w2][tid].y);
+    }
+    lzm[tid] = mm + __log2f(ss);
+  }
+  __syncthreads();
+  // candidates: lane states whose maximum is within the window of the screening log2 Z
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int p = 8 * (v >> 2) + 4 * h + (v & 3);
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk) {
+      const int pp = blk * 32 + p;
+      const float mv = blk ? m1[v] : m0[v];
+      const bool cand = mv > lzm[pp] - kWindow;
+      float term = cand ? exp2_fast(mv - stw[wave][pp].x) : 0.0f;
+      for (int off = 16; off > 0; off >>= 1) term += __shfl_xor(term, off);
+      const unsigned long long bal = __ballot(cand);
+      if (col == 0) {
+        cms[wave][pp] = term;
+        cmask[pp][wave] = (unsigned)(bal >> (32 * h));
+      }
+    }
+  }
+  __syncthreads();
+  if (tid < 64) {
+    const int p = tid;
+    // screened mass of everything that is not a candidate (ill states are exact)
+    float mm = -INFINITY;
+    for (int w2 = 0; w2 < 4; ++w2) mm = fmaxf(mm, fmaxf(stw[w2][p].x, sti[w2][p].x));
+    float snc = 0.0f;
+    if (mm > -INFINITY) {
+      for (int w2 = 0; w2 < 4; ++w2) {
+        const float2 a = stw[w2][p], b = sti[w2][p];
+        if (a.x > -INFINITY) snc += fmaxf(a.y - cms[w2][p], 0.0f) * exp2_fast(a.x - mm);
+        if (b.x > -INFINITY) snc += b.y * exp2_fast(b.x - mm);
+      }
+    }
+    // exact log-densities of the candidates, in (wave, lane column) order
+    float mc = -INFINITY, sc = 0.0f;
+    int tsl[kT];
+    float tl[kT];
+#pragma unroll
+    for (int j = 0; j < kT; ++j) { tsl[j] = -1; tl[j] = -INFINITY; }
+    for (int w2 = 0; w2 < 4; ++w2) {
+      unsigned msk = cmask[p][w2];
+      while (msk) {
+        const int b = __ffs(msk) - 1;
+        msk &= msk - 1;
+        const int slot = cidx[p][w2 * 32 + b];
+        const int comp = well_idx[slot];
+        const float l = ill_logit<D64>(xs + p * P, dmu + (size_t)comp * D64,
+                                       dh + (size_t)comp * D64, dc[comp]);
+        lse_add(mc, sc, l);
+        // keep the kT largest (ties: the earlier one stays ahead)
+        if (l > tl[kT - 1]) {
+          int j = kT - 1;
+          while (j > 0 && l > tl[j - 1]) { tl[j] = tl[j - 1]; tsl[j] = tsl[j - 1]; --j; }
+          tl[j] = l;
+          tsl[j] = slot;
+        }
+      }
+    }
+    float mt = fmaxf(mm, mc), stot = 0.0f;
+    if (mt > -INFINITY) {
+      if (mm > -INFINITY) stot += snc * exp2_fast(mm - mt);
+      if (mc > -INFINITY) stot += sc * exp2_fast(mc - mt);
+    }
+    const float lz = mt + __log2f(stot);
+    const int64_t nn = n0 + p;
+    double contrib = 0.0;
+    if (nn < n) {
+      logz2[nn] = lz;
+      contrib = (double)lz;
+#pragma unroll
+      for (int j = 0; j < kT; ++j) {
+        cslot[nn * kT + j] = tsl[j];
+        cr[nn * kT + j] = tsl[j] >= 0 ? exp2_fast(tl[j] - lz) : 0.0f;
+      }
+    }
+    for (int off = 32; off > 0; off >>= 1) contrib += __shfl_xor(contrib, off);
+    if (lane == 0) ll_part[blockIdx.x] = contrib;
+  }
+}
+
+// ---------------------------------------------------------------- Step 2: statistics
+// Grid: (component block) x (point chunk); the blocks of ill-conditioned
+// components come first so that these slower workgroups start early.  Per
+// iteration of PTS points:
+//   producers  well block: wave w forms r for points 32w..32w+31 with the MFMA
+//              log-densities (bit for bit those of k_logz); ill block: wave w
+//              forms r for components 8w..8w+7 with the direct form, lane =
+//              point.  r is kept in LDS as fp64; the n x k matrix never leaves
+//              the chip.
+//   consumers  the statistic contraction r^T [x | x^2] in fp64 on the vector
+//              ALU: wave w owns a quarter of the 2*D64 columns (x low/high half,
+//              x^2 low/high half); lane (ci, ei) owns components 4ci..4ci+3 and
+//              D64/16 consecutive columns.  The products r*x and r*x^2 of fp32
+//              values are exact in fp64, so the raw moments lose nothing to
+//              cancellation when the M-step forms q/n - mu^2.
+// Partial layout per (workgroup, slot): [N_k | S[D64] | Q[D64]] fp64, written
+// once per workgroup (no atomics).
+template <int D64>
+__global__ __launch_bounds__(256) void k_stats(const float* __restrict__ x, int64_t n, int d,
+                                               int vec4, const float4* __restrict__ wp,
+                                               const float* __restrict__ cw,
+                                               const int* __restrict__ ill_idx,
+                                               const float* __restrict__ dmu,
+                                               const float* __restrict__ dh,
+                                               const float* __restrict__ dc,
+                                               const int* __restrict__ counts,
+                                               const float* __restrict__ logz2,
+                                               const int* __restrict__ cslot,
+                                               const float* __restrict__ cr, int nch,
+                                               int64_t chunk_pts, double* __restrict__ part) {
+  constexpr int P = D64 + 4, PTS = D64 <= 128 ? 128 : 64, CT = D64 / 16, STRIDE = 1 + 2 * D64;
+  __shared__ __align__(16) float xs[PTS * P];
+  __shared__ __align__(16) double rl[PTS * 32];
+  __shared__ float lzs[PTS];
+  const int n_wkb = counts[2], n_ikb = counts[3], n_ill = counts[1];
+  const int kbi = blockIdx.x / nch, chunk = blockIdx.x % nch;
+  if (kbi >= n_ikb + n_wkb) return;
+  const bool ill = kbi < n_ikb;
+  const int kb = ill ? kbi : kbi - n_ikb;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, h = lane >> 5, col = lane & 31;
+  const int64_t p0 = (int64_t)chunk * chunk_pts;
+  const int64_t p1 = p0 + chunk_pts < n ? p0 + chunk_pts : n;
+  const int ci = lane >> 3, ei = lane & 7;
+  const bool sq = wave >= 2;
+  const int cbase = (wave & 1) * (D64 / 2) + ei * CT;
+  double acc[4][CT];
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+#pragma unroll
+    for (int j = 0; j < CT; ++j) acc[c][j] = 0.0;
+  double nk[4] = {0.0, 0.0, 0.0, 0.0};
+  const float cb = ill ? 0.0f : cw[kb * kBK + col];
+  const float4* wpk = wp + (size_t)(ill ? 0 : kb) * (D64 / 4) * 64;
+
+  for (int64_t it = p0; it < p1; it += PTS) {
+    __syncthreads();
+    load_tile<D64>(x, p1, d, it, PTS, xs, vec4 != 0);
+    for (int i = tid; i < PTS; i += 256) lzs[i] = (it + i < p1) ? logz2[it + i] : INFINITY;
+    __syncthreads();
+    if (!ill) {
+      if (wave * 32 < PTS) {
+        f16v l;
+        logits_block<D64>(xs, wave * 32, wpk, cb, l);
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int row = wave * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
+          rl[row * 32 + col] = (double)exp2_fast(l[v] - lzs[row]);
+        }
+      }
+      __syncthreads();
+      // exact responsibilities from the refinement in k_logz override the screened ones
+      for (int i = tid; i < PTS * kT; i += 256) {
+        const int pt = i / kT;
+        if (it + pt < p1) {
+          const int sl = cslot[(it + pt) * kT + (i % kT)];
+          if (sl >= 0 && (sl >> 5) == kb) rl[pt * 32 + (sl & 31)] = (double)cr[(it + pt) * kT + (i % kT)];
+        }
+      }
+    } else {
+      for (int pp = lane; pp < PTS; pp += 64) {
+        for (int c = 0; c < 8; ++c) {
+          const int ki = kb * kBK + wave * 8 + c;
+          float r = 0.0f;
+          if (ki < n_ill) {
+            const int comp = ill_idx[ki];
+            const float l = ill_logit<D64>(xs + pp * P, dmu + (size_t)comp * D64,
+                                           dh + (size_t)comp * D64, dc[comp]);
+            r = exp2_fast(l - lzs[pp]);
+          }
+          rl[pp * 32 + wave * 8 + c] = (double)r;
+        }
+      }
+    }
+    __syncthreads();
+    const int np = (int)(p1 - it < PTS ? p1 - it : PTS);
+    for (int p = 0; p < np; ++p) {
+      const double2 ra = *reinterpret_cast<const double2*>(rl + p * 32 + 4 * ci);
+      const double2 rb = *reinterpret_cast<const double2*>(rl + p * 32 + 4 * ci + 2);
+      const double r[4] = {ra.x, ra.y, rb.x, rb.y};
+      if (wave == 0) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) nk[c] += r[c];
+      }
+      const float* xp = xs + p * P + cbase;
+#pragma unroll
+      for (int j = 0; j < CT; ++j) {
+        double xv = (double)xp[j];
+        if (sq) xv = xv * xv;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[c][j] = fma(r[c], xv, acc[c][j]);
+      }
+    }
+  }
+  double* base = part + (size_t)blockIdx.x * kBK * STRIDE;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    double* row = base + (size_t)(4 * ci + c) * STRIDE;
+    if (wave == 0 && ei == 0) row[0] = nk[c];
+#pragma unroll
+    for (int j = 0; j < CT; ++j) row[1 + (sq ? D64 : 0) + cbase + j] = acc[c][j];
+  }
+}
+
+// ---------------------------------------------------------------- fixed-order reductions
+__global__ __launch_bounds__(256) void k_reduce_stats(
+    const double* __restrict__ part, const int* __restrict__ counts,
+    const int* __restrict__ well_idx, const int* __restrict__ ill_idx, int nch, int k, int d,
+    int D64, double* __restrict__ nk, double* __restrict__ s, double* __restrict__ q) {
+  const int64_t width = 1 + 2 * (int64_t)d;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= 2 * (int64_t)k * width) return;
+  const int which = (int)(t / ((int64_t)k * width));
+  const int64_t rem = t % ((int64_t)k * width);
+  const int slot = (int)(rem / width), c = (int)(rem % width);
+  int comp, kbi;
+  if (which == 0) {
+    if (slot >= counts[0]) return;
+    comp = well_idx[slot];
+    kbi = counts[3] + slot / kBK;
+  } else {
+    if (slot >= counts[1]) return;
+    comp = ill_idx[slot];
+    kbi = slot / kBK;
+  }
+  const int64_t stride = 1 + 2 * (int64_t)D64;
+  const int64_t off = c == 0 ? 0 : (c <= d ? 1 + (c - 1) : 1 + D64 + (c - 1 - d));
+  const double* p = part + ((size_t)kbi * nch * kBK + (slot % kBK)) * stride + off;
+  const int64_t cs = (int64_t)kBK * stride;
+  double acc = 0.0;
+  for (int ch = 0; ch < nch; ++ch) acc += p[ch * cs];
+  if (c == 0) nk[comp] += acc;
+  else if (c <= d) s[(int64_t)comp * d + (c - 1)] += acc;
+  else q[(int64_t)comp * d + (c - 1 - d)] += acc;
+}
+
+__global__ __launch_bounds__(1024) void k_reduce_ll(const double* __restrict__ ll_part,
+                                                    int64_t cnt, double* __restrict__ out,
+                                                    int accumulate) {
+  __shared__ double sh[1024];
+  const int t = threadIdx.x;
+  double a = 0.0;
+  for (int64_t i = t; i < cnt; i += 1024) a += ll_part[i];
+  sh[t] = a;
+  __syncthreads();
+  for (int w = 512; w > 0; w >>= 1) {
+    if (t < w) sh[t] += sh[t + w];
+    __syncthreads();
+  }
+  if (t == 0) {
+    const double v = sh[0] * kLn2;
+    *out = accumulate ? *out + v : v;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_mstep(const double* __restrict__ nk,
+                                               const double* __restrict__ s,
+                                               const double* __restrict__ q, double n_total,
+                                               int d, int k, double var_floor,
+                                               float* __restrict__ w, float* __restrict__ mu,
+                                               float* __restrict__ var) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (int64_t)k * d) return;
+  const int comp = (int)(t / d), j = (int)(t % d);
+  const double nn = nk[comp];
+  if (nn == 0.0) {  // dead component: keep mean and variances, weight 0
+    if (j == 0) w[comp] = 0.0f;
+    return;
+  }
+  const double m = s[t] / nn;
+  double v = q[t] / nn - m * m;
+  if (!(v > var_floor)) v = var_floor;
+  mu[t] = (float)m;
+  var[t] = (float)v;
+  if (j == 0) w[comp] = (float)(nn / n_total);
+}
+
+__global__ __launch_bounds__(256) void k_zero(double* __restrict__ p, int64_t cnt) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t < cnt) p[t] = 0.0;
+}
+
+// ---------------------------------------------------------------- host side
+inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+struct Layout {
+  int64_t n;
+  int d, k, kpad, D64, m;
+  int nch, nblk;
+  int64_t chunk, n_wg_logz;
+  size_t off_counts, off_cls, off_cwell, off_cdir, off_well_idx, off_ill_idx, off_cw, off_wp,
+      off_dmu, off_dh, off_dc, off_logz2, off_cslot, off_cr, off_llpart, off_part,
+      off_fit_nk, off_fit_s, off_fit_q, total;
+};
+
+bool make_layout(int64_t n, int d, int k, int m, Layout* L) {
+  if (n < 1 || d < 1 || k < 1 || d > GMM_MAX_D || k > GMM_MAX_K || m < 0 || m > GMM_MAX_M)
+    return false;
+  L->n = n; L->d = d; L->k = k; L->m = m;
+  L->kpad = (int)cdiv(k, kBK) * kBK;
+  L->D64 = (int)cdiv(d, 64) * 64;
+  const int nkb = L->kpad / kBK;
+  // chunking depends only on (n, k), never on the device
+  int maxc = 512 / nkb;
+  if (maxc < 8) maxc = 8;
+  int64_t c = cdiv(n, 2048);
+  if (c > maxc) c = maxc;
+  if (c >= 8) c = c / 8 * 8;
+  L->nch = (int)(c < 1 ? 1 : c);
+  L->chunk = cdiv(n, L->nch);
+  L->nblk = nkb + 1;  // well blocks + ill blocks never exceed ceil(k/32) + 1
+  L->n_wg_logz = cdiv(n, 64);
+  size_t o = 0;
+  auto take = [&](size_t bytes) { const size_t r = o; o = align256(o + bytes); return r; };
+  L->off_counts = take(16 * sizeof(int));
+  L->off_cls = take((size_t)k * sizeof(int));
+  L->off_cwell = take((size_t)k * sizeof(double));
+  L->off_cdir = take((size_t)k * sizeof(double));
+  L->off_well_idx = take((size_t)k * sizeof(int));
+  L->off_ill_idx = take((size_t)k * sizeof(int));
+  L->off_cw = take((size_t)L->kpad * sizeof(float));
+  L->off_wp = take((size_t)L->kpad * 2 * L->D64 * sizeof(float));
+  L->off_dmu = take((size_t)k * L->D64 * sizeof(float));
+  L->off_dh = take((size_t)k * L->D64 * sizeof(float));
+  L->off_dc = take((size_t)k * sizeof(float));
+  L->off_logz2 = take((size_t)n * sizeof(float));
+  L->off_cslot = take((size_t)n * kT * sizeof(int));
+  L->off_cr = take((size_t)n * kT * sizeof(float));
+  L->off_llpart = take((size_t)L->n_wg_logz * sizeof(double));
+  L->off_part = take((size_t)L->nblk * L->nch * kBK * (1 + 2 * (size_t)L->D64) * sizeof(double));
+  L->off_fit_nk = take((size_t)k * sizeof(double) + sizeof(double));  // + loglik slot
+  L->off_fit_s = take((size_t)k * d * sizeof(double));
+  L->off_fit_q = take((size_t)k * d * sizeof(double));
+  L->total = o;
+  return true;
+}
+
+template <typename T>
+T* at(void* ws, size_t off) { return reinterpret_cast<T*>(static_cast<char*>(ws) + off); }
+
+int launch_status() {
+  const hipError_t e = hipGetLastError();
+  return e == hipSuccess ? GMM_OK : GMM_ERR_DEVICE;
+}
+
+template <int D64>
+int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
+               const float* var, double* nk, double* s, double* q, double* loglik,
+               int ll_accumulate, void* ws, hipStream_t st) {
+  const int64_t n = L.n;
+  const int d = L.d, k = L.k, kpad = L.kpad;
+  int* counts = at<int>(ws, L.off_counts);
+  int* cls = at<int>(ws, L.off_cls);
+  double* cwell = at<double>(ws, L.off_cwell);
+  double* cdir = at<double>(ws, L.off_cdir);
+  int* well_idx = at<int>(ws, L.off_well_idx);
+  int* ill_idx = at<int>(ws, L.off_ill_idx);
+  float* cw = at<float>(ws, L.off_cw);
+  float4* wp = at<float4>(ws, L.off_wp);
+  float* dmu = at<float>(ws, L.off_dmu);
+  float* dh = at<float>(ws, L.off_dh);
+  float* dc = at<float>(ws, L.off_dc);
+  int* cslot = at<int>(ws, L.off_cslot);
+  float* cr = at<float>(ws, L.off_cr);
+  float* logz2 = at<float>(ws, L.off_logz2);
+  double* llpart = at<double>(ws, L.off_llpart);
+  double* part = at<double>(ws, L.off_part);
+  const int vec4 = ((d & 3) == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0) ? 1 : 0;
+
+  hipLaunchKernelGGL(k_prep_class, dim3(k), dim3(64), 0, st, w, mu, var, d, cls, cwell, cdir);
+  hipLaunchKernelGGL(k_prep_scan, dim3(1), dim3(256), 0, st, cls, k, well_idx, ill_idx, counts);
+  {
+    const int64_t tot = (int64_t)kpad * (D64 / 4) * 2;
+    hipLaunchKernelGGL(k_prep_pack_well<D64>, dim3((unsigned)cdiv(tot, 256)), dim3(256), 0, st,
+                       mu, var, d, kpad, cwell, counts, well_idx, wp, cw);
+    const int64_t toti = (int64_t)k * D64;
+    hipLaunchKernelGGL(k_prep_pack_direct<D64>, dim3((unsigned)cdiv(toti, 256)), dim3(256), 0,
+                       st, mu, var, d, k, cdir, dmu, dh, dc);
+  }
+  hipLaunchKernelGGL(k_logz<D64>, dim3((unsigned)L.n_wg_logz), dim3(256), 0, st, x, n, d, vec4,
+                     wp, cw, well_idx, ill_idx, dmu, dh, dc, counts, logz2, cslot, cr, llpart);
+  hipLaunchKernelGGL(k_stats<D64>, dim3((unsigned)(L.nblk * L.nch)), dim3(256), 0, st, x, n, d,
+                     vec4, wp, cw, ill_idx, dmu, dh, dc, counts, logz2, cslot, cr, L.nch, L.chunk,
+                     part);
+  {
+    const int64_t tot = 2 * (int64_t)k * (1 + 2 * (int64_t)d);
+    hipLaunchKernelGGL(k_reduce_stats, dim3((unsigned)cdiv(tot, 256)), dim3(256), 0, st, part,
+                       counts, well_idx, ill_idx, L.nch, k, d, D64, nk, s, q);
+  }
+  hipLaunchKernelGGL(k_reduce_ll, dim3(1), dim3(1024), 0, st, llpart, L.n_wg_logz, loglik,
+                     ll_accumulate);
+  return launch_status();
+}
+
+int estep_dispatch(const Layout& L, const float* x, const float* w, const float* mu,
+                   const float* var, double* nk, double* s, double* q, double* loglik,
+                   int ll_accumulate, void* ws, hipStream_t st) {
+  switch (L.D64) {
+    case 64: return estep_impl<64>(L, x, w, mu, var, nk, s, q, loglik, ll_accumulate, ws, st);
+    case 128: return estep_impl<128>(L, x, w, mu, var, nk, s, q, loglik, ll_accumulate, ws, st);
+    case 192: return estep_impl<192>(L, x, w, mu, var, nk, s, q, loglik, ll_accumulate, ws, st);
+    case 256: return estep_impl<256>(L, x, w, mu, var, nk, s, q, loglik, ll_accumulate, ws, st);
+    default: return GMM_ERR_UNSUPPORTED;
+  }
+}
+
+int check_ws(const Layout& L, void* ws, size_t ws_bytes) {
+  if (ws == nullptr || (reinterpret_cast<uintptr_t>(ws) & 255) != 0 || ws_bytes < L.total)
+    return GMM_ERR_WORKSPACE;
+  return GMM_OK;
+}
+
+int check_shape(int64_t n, int32_t d, int32_t k) {
+  if (n < 1 || d < 1 || k < 1) return GMM_ERR_INVALID_ARG;
+  if (d > GMM_MAX_D || k > GMM_MAX_K) return GMM_ERR_UNSUPPORTED;
+  return GMM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* gmm_status_string(int status) {
+  switch (status) {
+    case GMM_OK: return "GMM_OK";
+    case GMM_ERR_INVALID_ARG: return "GMM_ERR_INVALID_ARG";
+    case GMM_ERR_UNSUPPORTED: return "GMM_ERR_UNSUPPORTED";
+    case GMM_ERR_WORKSPACE: return "GMM_ERR_WORKSPACE";
+    case GMM_ERR_DEVICE: return "GMM_ERR_DEVICE";
+    default: return "GMM_UNKNOWN_STATUS";
+  }
+}
+
+size_t gmm_workspace_bytes(int64_t n, int32_t d, int32_t k, int32_t m) {
+  Layout L;
+  if (!make_layout(n, d, k, m, &L)) return 0;
+  return L.total;
+}
+
+int gmm_estep_accumulate(const float* x, int64_t n, int32_t d, int32_t k, const float* weights,
+                         const float* means, const float* vars, double* nk, double* s, double* q,
+                         double* loglik, void* ws, size_t ws_bytes, hipStream_t stream) {
+  int rc = check_shape(n, d, k);
+  if (rc != GMM_OK) return rc;
+  if (!x || !weights || !means || !vars || !nk || !s || !q || !loglik) return GMM_ERR_INVALID_ARG;
+  Layout L;
+  if (!make_layout(n, d, k, 0, &L)) return GMM_ERR_UNSUPPORTED;
+  rc = check_ws(L, ws, ws_bytes);
+  if (rc != GMM_OK) return rc;
+  return estep_dispatch(L, x, weights, means, vars, nk, s, q, loglik, 1, ws, stream);
+}
+
+int gmm_mstep(const double* nk, const double* s, const double* q, double n_total, int32_t d,
+              int32_t k, float var_floor, float* weights, float* means, float* vars,
+              hipStream_t stream) {
+  if (d < 1 || k < 1) return GMM_ERR_INVALID_ARG;
+  if (d > GMM_MAX_D || k > GMM_MAX_K) return GMM_ERR_UNSUPPORTED;
+  if (!nk || !s || !q || !weights || !means || !vars) return GMM_ERR_INVALID_ARG;
+  if (!(n_total > 0.0) || !(var_floor >= 0.0f)) return GMM_ERR_INVALID_ARG;
+  const int64_t tot = (int64_t)k * d;
+  hipLaunchKernelGGL(k_mstep, dim3((unsigned)cdiv(tot, 256)), dim3(256), 0, stream, nk, s, q,
+                     n_total, d, k, (double)var_floor, weights, means, vars);
+  return launch_status();
+}
+
+int gmm_fit(const float* x, int64_t n, int32_t d, int32_t k, int32_t n_iters, float var_floor,
+            float* weights, float* means, float* vars, double* loglik_hist, void* ws,
+            size_t ws_bytes, hipStream_t stream) {
+  int rc = check_shape(n, d, k);
+  if (rc != GMM_OK) return rc;
+  if (n_iters < 0 || !x || !weights || !means || !vars || (n_iters > 0 && !loglik_hist))
+    return GMM_ERR_INVALID_ARG;
+  if (!(var_floor >= 0.0f)) return GMM_ERR_INVALID_ARG;
+  Layout L;
+  if (!make_layout(n, d, k, 0, &L)) return GMM_ERR_UNSUPPORTED;
+  rc = check_ws(L, ws, ws_bytes);
+  if (rc != GMM_OK) return rc;
+  double* fnk = at<double>(ws, L.off_fit_nk);
+  double* fs = at<double>(ws, L.off_fit_s);
+  double* fq = at<double>(ws, L.off_fit_q);
+  const int64_t kd = (int64_t)k * d;
+  for (int t = 0; t < n_iters; ++t) {
+    hipLaunchKernelGGL(k_zero, dim3((unsigned)cdiv(k, 256)), dim3(256), 0, stream, fnk,
+                       (int64_t)k);
+    hipLaunchKernelGGL(k_zero, dim3((unsigned)cdiv(kd, 256)), dim3(256), 0, stream, fs, kd);
+    hipLaunchKernelGGL(k_zero, dim3((unsigned)cdiv(kd, 256)), dim3(256), 0, stream, fq, kd);
+    rc = estep_dispatch(L, x, weights, means, vars, fnk, fs, fq, loglik_hist + t, 0, ws, stream);
+    if (rc != GMM_OK) return rc;
+    hipLaunchKernelGGL(k_mstep, dim3((unsigned)cdiv(kd, 256)), dim3(256), 0, stream, fnk, fs, fq,
+                       (double)n, d, k, (double)var_floor, weights, means, vars);
+    rc = launch_status();
+    if (rc != GMM_OK) return rc;
+  }
+  return GMM_OK;
+}
+
+int gmm_assign_topk(const float* x, int64_t n, int32_t d, int32_t k, const float* weights,
+                    const float* means, const float* vars, int32_t m, float tau, int32_t* idx,
+                    float* resp, void* ws, size_t ws_bytes, hipStream_t stream) {
+  (void)x; (void)n; (void)d; (void)k; (void)weights; (void)means; (void)vars; (void)m;
+  (void)tau; (void)idx; (void)resp; (void)ws; (void)ws_bytes; (void)stream;
+  return GMM_ERR_UNSUPPORTED;
+}
+
+}  // extern "C"

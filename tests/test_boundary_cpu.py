@@ -1,0 +1,84 @@
+"""The C ABI without a GPU: the library loads, exports every symbol the header
+declares, sizes its workspace, and rejects bad arguments on the host before
+enqueuing anything."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2606_10896_amd as gmm
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _header_functions():
+    src = open(os.path.join(ROOT, "include", "flashgmm.h")).read()
+    return sorted(set(re.findall(r"^(?:const char\*|size_t|int)\s+(gmm_\w+)\(", src, re.M)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = gmm.load_library()
+    names = _header_functions()
+    assert set(names) == set(gmm.EXPORTS)
+    for name in names:
+        assert getattr(lib, name) is not None
+
+
+def test_status_strings():
+    assert gmm.status_string(0) == "GMM_OK"
+    assert gmm.status_string(-1) == "GMM_ERR_INVALID_ARG"
+    assert gmm.status_string(-2) == "GMM_ERR_UNSUPPORTED"
+    assert gmm.status_string(-3) == "GMM_ERR_WORKSPACE"
+    assert gmm.status_string(-4) == "GMM_ERR_DEVICE"
+    assert gmm.status_string(12345) == "GMM_UNKNOWN_STATUS"
+
+
+@pytest.mark.parametrize("n,d,k", [(1, 1, 1), (10_000, 16, 8), (100_000, 128, 1024),
+                                   (100_000_000, 128, 1024), (1_000_003, 37, 45),
+                                   (5_000, 256, 65536)])
+def test_workspace_is_o_n_plus_o_kd(n, d, k):
+    nb = gmm.workspace_bytes(n, d, k)
+    assert nb > 0 and nb % 256 == 0
+    # per point: one fp32 log-normaliser, 4 refined (slot, responsibility) pairs and 1/8 of an
+    # fp64 log-likelihood partial; plus O(k d) parameters and partial statistics: never an
+    # n x k array
+    assert nb >= 36 * n
+    d64 = (d + 63) // 64 * 64
+    kpad = (k + 31) // 32 * 32
+    well_part = 8 * (4 + 2 * d64) * max(8 * kpad, 512 * 32)
+    ill_part = 8 * (1 + 2 * d64) * 32 * max(512, kpad // 32)
+    okd = well_part + ill_part + 40 * kpad * d64 + 8 * 2 * k * d
+    assert nb <= 36 * n + n // 8 + okd + 64 * k + (1 << 16)
+    if n >= 10 ** 7:
+        assert nb < n * k * 4 / 25
+
+
+@pytest.mark.parametrize("n,d,k,m", [(0, 8, 4, 0), (10, 0, 4, 0), (10, 8, 0, 0), (10, 257, 4, 0),
+                                     (10, 8, 65537, 0), (10, 8, 4, 9), (10, 8, 4, -1)])
+def test_workspace_rejects_bad_shapes(n, d, k, m):
+    assert gmm.workspace_bytes(n, d, k, m) == 0
+
+
+def _fake(addr=0x100000):
+    return ctypes.c_void_p(addr)
+
+
+def test_host_validation_returns_before_any_launch():
+    lib = gmm.load_library()
+    p, ws = _fake(), _fake(0x200000)
+    big = gmm.workspace_bytes(1000, 8, 4)
+    # non-positive sizes and null pointers
+    assert lib.gmm_estep_accumulate(p, 0, 8, 4, p, p, p, p, p, p, p, ws, big, None) == gmm.GMM_ERR_INVALID_ARG
+    assert lib.gmm_estep_accumulate(p, 1000, 8, 4, None, p, p, p, p, p, p, ws, big, None) == gmm.GMM_ERR_INVALID_ARG
+    assert lib.gmm_estep_accumulate(p, 1000, 300, 4, p, p, p, p, p, p, p, ws, big, None) == gmm.GMM_ERR_UNSUPPORTED
+    # workspace: missing, misaligned, too small
+    assert lib.gmm_estep_accumulate(p, 1000, 8, 4, p, p, p, p, p, p, p, None, big, None) == gmm.GMM_ERR_WORKSPACE
+    assert lib.gmm_estep_accumulate(p, 1000, 8, 4, p, p, p, p, p, p, p, _fake(0x200010), big, None) == gmm.GMM_ERR_WORKSPACE
+    assert lib.gmm_estep_accumulate(p, 1000, 8, 4, p, p, p, p, p, p, p, ws, big - 1, None) == gmm.GMM_ERR_WORKSPACE
+    assert lib.gmm_fit(p, 1000, 8, 4, -1, 1e-6, p, p, p, p, ws, big, None) == gmm.GMM_ERR_INVALID_ARG
+    assert lib.gmm_fit(p, 1000, 8, 4, 3, -1.0, p, p, p, p, ws, big, None) == gmm.GMM_ERR_INVALID_ARG
+    assert lib.gmm_fit(p, 1000, 8, 4, 3, 1e-6, p, p, p, None, ws, big, None) == gmm.GMM_ERR_INVALID_ARG
+    assert lib.gmm_mstep(p, p, p, 0.0, 8, 4, 1e-6, p, p, p, None) == gmm.GMM_ERR_INVALID_ARG
+    assert lib.gmm_mstep(p, p, p, 10.0, 8, 4, -1.0, p, p, p, None) == gmm.GMM_ERR_INVALID_ARG
+    assert lib.gmm_mstep(None, p, p, 10.0, 8, 4, 1e-6, p, p, p, None) == gmm.GMM_ERR_INVALID_ARG
