@@ -123,7 +123,7 @@ __device__ __forceinline__ void logits_block(const float* xs, int row0,
   const int lane = threadIdx.x & 63, h = lane >> 5, col = lane & 31;
   const float* xr = xs + (row0 + col) * P + 4 * h;
   f16v a0 = {}, a1 = {};
-#pragma unroll
+#pragma unroll 2
   for (int q = 0; q < QH; ++q) {
     const float4 b0 = wp[q * 64 + lane];
     const float4 b1 = wp[(QH + q) * 64 + lane];
@@ -151,7 +151,7 @@ __device__ __forceinline__ void logits_2blocks(const float* xs, const float4* __
   const float* xr0 = xs + col * P + 4 * h;
   const float* xr1 = xs + (32 + col) * P + 4 * h;
   f16v a0 = {}, a1 = {}, c0 = {}, c1 = {};
-#pragma unroll
+#pragma unroll 2
   for (int q = 0; q < QH; ++q) {
     const float4 b0 = wp[q * 64 + lane];
     const float4 b1 = wp[(QH + q) * 64 + lane];
@@ -494,156 +494,317 @@ __global__ __launch_bounds__(256) void k_logz(
   }
 }
 
-// ---------------------------------------------------------------- Step 2: statistics
-// Grid: (component block) x (point chunk); the blocks of ill-conditioned
-// components come first so that these slower workgroups start early.  Per
-// iteration of PTS points:
-//   producers  well block: wave w forms r for points 32w..32w+31 with the MFMA
-//              log-densities (bit for bit those of k_logz); ill block: wave w
-//              forms r for components 8w..8w+7 with the direct form, lane =
-//              point.  r is kept in LDS as fp64; the n x k matrix never leaves
-//              the chip.
-//   consumers  the statistic contraction r^T [x | x^2] in fp64 on the vector
-//              ALU: wave w owns a quarter of the 2*D64 columns (x low/high half,
-//              x^2 low/high half); lane (ci, ei) owns components 4ci..4ci+3 and
-//              D64/16 consecutive columns.  The products r*x and r*x^2 of fp32
-//              values are exact in fp64, so the raw moments lose nothing to
-//              cancellation when the M-step forms q/n - mu^2.
-// Partial layout per (workgroup, slot): [N_k | S[D64] | Q[D64]] fp64, written
-// once per workgroup (no atomics).
+// ---------------------------------------------------------------- Step 2: statistics, well set
+// Grid: (component block kb, column half, point chunk).  Every 128-point
+// iteration:
+//   load      X tile and log2 Z into LDS; the refined (point, component)
+//             pairs of this block, taken from k_logz's per-point lists, are
+//             compacted in (point, rank) order and flagged per point.
+//   dense     wave w: MFMA log-densities of points 32w..32w+31 against the
+//             block, r = 2^(l - log2 Z) kept in registers with the refined pairs
+//             set to 0, then the statistic contraction r^T [x | x^2] on MFMA
+//             straight from those registers (the accumulator layout of the
+//             log-density MFMA is the operand layout of the statistic MFMA).
+//             fp32 accumulators are folded into fp64 every 16 iterations.
+//   sparse    the refined pairs (at most kT per point, the only ones that can
+//             carry a large share of a component) in fp64: exact products
+//             r * x and r * x^2, so q/n - mu^2 loses nothing to cancellation.
+// A column half covers 128 dimensions of x and the same of x^2; d <= 128 needs
+// one half, larger d two (the log-densities are then formed once per half).
 template <int D64>
-__global__ __launch_bounds__(256) void k_stats(const float* __restrict__ x, int64_t n, int d,
-                                               int vec4, const float4* __restrict__ wp,
-                                               const float* __restrict__ cw,
-                                               const int* __restrict__ ill_idx,
-                                               const float* __restrict__ dmu,
-                                               const float* __restrict__ dh,
-                                               const float* __restrict__ dc,
-                                               const int* __restrict__ counts,
-                                               const float* __restrict__ logz2,
-                                               const int* __restrict__ cslot,
-                                               const float* __restrict__ cr, int nch,
-                                               int64_t chunk_pts, double* __restrict__ part) {
-  constexpr int P = D64 + 4, PTS = D64 <= 128 ? 128 : 64, CT = D64 / 16, STRIDE = 1 + 2 * D64;
-  __shared__ __align__(16) float xs[PTS * P];
-  __shared__ __align__(16) double rl[PTS * 32];
-  __shared__ float lzs[PTS];
-  const int n_wkb = counts[2], n_ikb = counts[3], n_ill = counts[1];
-  const int kbi = blockIdx.x / nch, chunk = blockIdx.x % nch;
-  if (kbi >= n_ikb + n_wkb) return;
-  const bool ill = kbi < n_ikb;
-  const int kb = ill ? kbi : kbi - n_ikb;
+__global__ __launch_bounds__(256) void k_stats_well(
+    const float* __restrict__ x, int64_t n, int d, int vec4, const float4* __restrict__ wp,
+    const float* __restrict__ cw, const int* __restrict__ counts,
+    const float* __restrict__ logz2, const int* __restrict__ cslot,
+    const float* __restrict__ cr, int nch, int64_t chunk_pts, double* __restrict__ part) {
+  constexpr int P = D64 + 4;
+  constexpr int CW = D64 < 128 ? D64 : 128;     // x dimensions per column half
+  constexpr int NE = CW / 32;                   // 32-column MFMA blocks per part
+  constexpr int NH = D64 / CW;                  // column halves
+  constexpr int STRIDE = 1 + 2 * D64;
+  constexpr int NLC = 1 + 2 * CW;               // sparse columns: N_k, x dims, x^2 dims
+  constexpr int NSC = (NLC + 7) / 8;
+  __shared__ __align__(16) float xs[128 * P];
+  __shared__ float lzs[128];
+  __shared__ unsigned rbits[128];
+  __shared__ int2 ent[128 * kT];
+  __shared__ int ecnt;
+  const int kb = blockIdx.x / (NH * nch);
+  const int hh = (blockIdx.x / nch) % NH;
+  const int chunk = blockIdx.x % nch;
+  if (kb >= counts[2]) return;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, h = lane >> 5, col = lane & 31;
   const int64_t p0 = (int64_t)chunk * chunk_pts;
   const int64_t p1 = p0 + chunk_pts < n ? p0 + chunk_pts : n;
-  const int ci = lane >> 3, ei = lane & 7;
-  const bool sq = wave >= 2;
-  const int cbase = (wave & 1) * (D64 / 2) + ei * CT;
-  double acc[4][CT];
-#pragma unroll
-  for (int c = 0; c < 4; ++c)
-#pragma unroll
-    for (int j = 0; j < CT; ++j) acc[c][j] = 0.0;
-  double nk[4] = {0.0, 0.0, 0.0, 0.0};
-  const float cb = ill ? 0.0f : cw[kb * kBK + col];
-  const float4* wpk = wp + (size_t)(ill ? 0 : kb) * (D64 / 4) * 64;
+  const float cb = cw[kb * kBK + col];
+  const float4* wpk = wp + (size_t)kb * (D64 / 4) * 64;
+  const int c0 = hh * CW;                       // first x dimension of this half
+  double* pk = part + (size_t)blockIdx.x * 4 * kBK * STRIDE;
 
-  for (int64_t it = p0; it < p1; it += PTS) {
-    __syncthreads();
-    load_tile<D64>(x, p1, d, it, PTS, xs, vec4 != 0);
-    for (int i = tid; i < PTS; i += 256) lzs[i] = (it + i < p1) ? logz2[it + i] : INFINITY;
-    __syncthreads();
-    if (!ill) {
-      if (wave * 32 < PTS) {
-        f16v l;
-        logits_block<D64>(xs, wave * 32, wpk, cb, l);
+  f16v acc[2 * NE];
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int row = wave * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
-          rl[row * 32 + col] = (double)exp2_fast(l[v] - lzs[row]);
-        }
+  for (int e = 0; e < 2 * NE; ++e) acc[e] = f16v{};
+  float nkacc = 0.0f;
+  double sacc[NSC];
+#pragma unroll
+  for (int i = 0; i < NSC; ++i) sacc[i] = 0.0;
+  const int sc = tid >> 3, sg = tid & 7;        // sparse lane: component, column group
+  bool first = true;
+  int iter = 0;
+
+  // each wave accumulates its own point tiles into its own partial region
+  double* pw = pk + (size_t)wave * kBK * STRIDE;
+  auto flush = [&]() {
+    const float nk2 = nkacc + __shfl_xor(nkacc, 32);
+    double* pc = pw + (size_t)col * STRIDE;
+    if (h == 0 && hh == 0) pc[0] = first ? (double)nk2 : pc[0] + (double)nk2;
+#pragma unroll
+    for (int e = 0; e < NE; ++e) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int i = 8 * (v >> 2) + 4 * h + (v & 3);
+        const int dim = c0 + NE * i + e;
+        double* ds = pc + 1 + dim;
+        double* dq = pc + 1 + D64 + dim;
+        *ds = first ? (double)acc[e][v] : *ds + (double)acc[e][v];
+        *dq = first ? (double)acc[NE + e][v] : *dq + (double)acc[NE + e][v];
+        acc[e][v] = 0.0f;
+        acc[NE + e][v] = 0.0f;
       }
-      __syncthreads();
-      // exact responsibilities from the refinement in k_logz override the screened ones
-      for (int i = tid; i < PTS * kT; i += 256) {
-        const int pt = i / kT;
+    }
+    nkacc = 0.0f;
+    first = false;
+  };
+
+  for (int64_t it = p0; it < p1; it += 128, ++iter) {
+    __syncthreads();
+    load_tile<D64>(x, p1, d, it, 128, xs, vec4 != 0);
+    if (tid < 128) {
+      lzs[tid] = (it + tid < p1) ? logz2[it + tid] : INFINITY;
+      rbits[tid] = 0u;
+    }
+    __syncthreads();
+    if (wave == 0) {
+      // compact the refined pairs of this block, in (point, rank) order
+      int cnt = 0;
+      for (int q = 0; q < 128 * kT / 64; ++q) {
+        const int e = q * 64 + lane, pt = e / kT, j = e % kT;
+        int sl = -1;
+        float rv = 0.0f;
         if (it + pt < p1) {
-          const int sl = cslot[(it + pt) * kT + (i % kT)];
-          if (sl >= 0 && (sl >> 5) == kb) rl[pt * 32 + (sl & 31)] = (double)cr[(it + pt) * kT + (i % kT)];
+          sl = cslot[(it + pt) * kT + j];
+          rv = cr[(it + pt) * kT + j];
         }
+        const bool mine = sl >= 0 && (sl >> 5) == kb;
+        const unsigned long long bal = __ballot(mine);
+        if (mine) {
+          const int pos = cnt + __popcll(bal & ((1ull << lane) - 1ull));
+          ent[pos] = make_int2((pt << 5) | (sl & 31), __float_as_int(rv));
+          atomicOr(&rbits[pt], 1u << (sl & 31));
+        }
+        cnt += __popcll(bal);
       }
-    } else {
-      for (int pp = lane; pp < PTS; pp += 64) {
-        for (int c = 0; c < 8; ++c) {
-          const int ki = kb * kBK + wave * 8 + c;
-          float r = 0.0f;
-          if (ki < n_ill) {
-            const int comp = ill_idx[ki];
-            const float l = ill_logit<D64>(xs + pp * P, dmu + (size_t)comp * D64,
-                                           dh + (size_t)comp * D64, dc[comp]);
-            r = exp2_fast(l - lzs[pp]);
-          }
-          rl[pp * 32 + wave * 8 + c] = (double)r;
+      if (lane == 0) ecnt = cnt;
+    }
+    __syncthreads();
+    // dense part: log-densities, responsibilities and statistics of tile `wave`
+    {
+      f16v l;
+      logits_block<D64>(xs, wave * 32, wpk, cb, l);
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = wave * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
+        float r = exp2_fast(l[v] - lzs[row]);
+        r = ((rbits[row] >> col) & 1u) ? 0.0f : r;
+        nkacc += r;
+        l[v] = r;
+      }
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = wave * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
+        const float* xp = xs + row * P + c0 + NE * col;
+        float a[NE];
+        if constexpr (NE == 4) {
+          const float4 t = *reinterpret_cast<const float4*>(xp);
+          a[0] = t.x; a[1] = t.y; a[2] = t.z; a[3] = t.w;
+        } else if constexpr (NE == 2) {
+          const float2 t = *reinterpret_cast<const float2*>(xp);
+          a[0] = t.x; a[1] = t.y;
+        } else {
+#pragma unroll
+          for (int e = 0; e < NE; ++e) a[e] = xp[e];
+        }
+#pragma unroll
+        for (int e = 0; e < NE; ++e) {
+          acc[e] = mfma32(a[e], l[v], acc[e]);
+          acc[NE + e] = mfma32(a[e] * a[e], l[v], acc[NE + e]);
         }
       }
     }
-    __syncthreads();
-    const int np = (int)(p1 - it < PTS ? p1 - it : PTS);
-    for (int p = 0; p < np; ++p) {
-      const double2 ra = *reinterpret_cast<const double2*>(rl + p * 32 + 4 * ci);
-      const double2 rb = *reinterpret_cast<const double2*>(rl + p * 32 + 4 * ci + 2);
-      const double r[4] = {ra.x, ra.y, rb.x, rb.y};
-      if (wave == 0) {
+    // sparse part: refined pairs in fp64 (lane = component sc, column group sg)
+    {
+      const int ne = ecnt;
+      for (int e = 0; e < ne; ++e) {
+        const int2 en = ent[e];
+        const int comp = en.x & 31;
+        if ((comp >> 3) != wave) continue;          // wave-uniform
+        if (comp == sc) {
+          const int pt = en.x >> 5;
+          const double r = (double)__int_as_float(en.y);
+          const float* xr = xs + pt * P + c0;
 #pragma unroll
-        for (int c = 0; c < 4; ++c) nk[c] += r[c];
+          for (int i = 0; i < NSC; ++i) {
+            const int lc = sg + 8 * i;
+            if (lc < NLC) {
+              double y = 1.0;
+              if (lc > 0 && lc <= CW) y = (double)xr[lc - 1];
+              else if (lc > CW) { const double xv = (double)xr[lc - 1 - CW]; y = xv * xv; }
+              sacc[i] = fma(r, y, sacc[i]);
+            }
+          }
+        }
       }
-      const float* xp = xs + p * P + cbase;
+    }
+    if ((iter % 16) == 15) flush();
+  }
+  if (first || (iter % 16) != 0) flush();
+  __syncthreads();
+  // add the sparse fp64 part into the region of the wave that owns the component
+  // (lane sc's wave), after that wave's last dense flush
+  {
+    double* pc = pk + ((size_t)wave * kBK + sc) * STRIDE;
 #pragma unroll
-      for (int j = 0; j < CT; ++j) {
-        double xv = (double)xp[j];
-        if (sq) xv = xv * xv;
-#pragma unroll
-        for (int c = 0; c < 4; ++c) acc[c][j] = fma(r[c], xv, acc[c][j]);
+    for (int i = 0; i < NSC; ++i) {
+      const int lc = sg + 8 * i;
+      if (lc < NLC) {
+        int off;
+        if (lc == 0) off = hh == 0 ? 0 : -1;
+        else if (lc <= CW) off = 1 + c0 + (lc - 1);
+        else off = 1 + D64 + c0 + (lc - 1 - CW);
+        if (off >= 0) pc[off] += sacc[i];
       }
     }
   }
-  double* base = part + (size_t)blockIdx.x * kBK * STRIDE;
+}
+
+// ---------------------------------------------------------------- Step 2: statistics, ill set
+// Ill-conditioned components (few).  Grid of fixed size; each of the n_ikb
+// blocks of 32 such components gets grid/n_ikb point chunks.  Per 64-point
+// iteration wave w forms r for components 8w..8w+7 of the block with the
+// direct form (lane = point), then accumulates the statistics of those
+// components in fp64 (lane = column).
+__host__ __device__ inline int ill_chunks(int grid, int n_ikb, int64_t n) {
+  int c = grid / (n_ikb > 0 ? n_ikb : 1);
+  const int64_t cap = (n + 63) / 64;
+  if (c > cap) c = (int)cap;
+  return c < 1 ? 1 : c;
+}
+
+template <int D64>
+__global__ __launch_bounds__(256) void k_stats_ill(
+    const float* __restrict__ x, int64_t n, int d, int vec4, const int* __restrict__ ill_idx,
+    const float* __restrict__ dmu, const float* __restrict__ dh, const float* __restrict__ dc,
+    const int* __restrict__ counts, const float* __restrict__ logz2,
+    double* __restrict__ part) {
+  constexpr int P = D64 + 4, NJ = D64 / 64, STRIDE = 1 + 2 * D64;
+  __shared__ __align__(16) float xs[64 * P];
+  __shared__ float rs[32 * 64];
+  __shared__ float lzs[64];
+  const int n_ikb = counts[3];
+  if (n_ikb == 0) return;
+  const int nchk = ill_chunks(gridDim.x, n_ikb, n);
+  const int kb = blockIdx.x / nchk, chunk = blockIdx.x % nchk;
+  if (kb >= n_ikb) return;
+  const int64_t chunk_pts = (n + nchk - 1) / nchk;
+  const int n_ill = counts[1];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int64_t p0 = (int64_t)chunk * chunk_pts;
+  const int64_t p1 = p0 + chunk_pts < n ? p0 + chunk_pts : n;
+  double S[8][NJ], Q[8][NJ], NK[8];
 #pragma unroll
-  for (int c = 0; c < 4; ++c) {
-    double* row = base + (size_t)(4 * ci + c) * STRIDE;
-    if (wave == 0 && ei == 0) row[0] = nk[c];
+  for (int c = 0; c < 8; ++c) {
+    NK[c] = 0.0;
 #pragma unroll
-    for (int j = 0; j < CT; ++j) row[1 + (sq ? D64 : 0) + cbase + j] = acc[c][j];
+    for (int j = 0; j < NJ; ++j) S[c][j] = Q[c][j] = 0.0;
+  }
+  for (int64_t it = p0; it < p1; it += 64) {
+    __syncthreads();
+    load_tile<D64>(x, p1, d, it, 64, xs, vec4 != 0);
+    if (tid < 64) lzs[tid] = (it + tid < p1) ? logz2[it + tid] : INFINITY;
+    __syncthreads();
+    for (int c = 0; c < 8; ++c) {
+      const int ki = kb * kBK + wave * 8 + c;
+      float r = 0.0f;
+      if (ki < n_ill) {
+        const int comp = ill_idx[ki];
+        const float l = ill_logit<D64>(xs + lane * P, dmu + (size_t)comp * D64,
+                                       dh + (size_t)comp * D64, dc[comp]);
+        r = exp2_fast(l - lzs[lane]);
+      }
+      rs[(wave * 8 + c) * 64 + lane] = r;
+    }
+    __syncthreads();
+    const int np = (int)(p1 - it < 64 ? p1 - it : 64);
+    for (int p = 0; p < np; ++p) {
+      double xv[NJ];
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) xv[j] = (double)xs[p * P + lane + 64 * j];
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        const double r = (double)rs[(wave * 8 + c) * 64 + p];
+        NK[c] += r;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+          const double rx = r * xv[j];
+          S[c][j] += rx;
+          Q[c][j] = fma(rx, xv[j], Q[c][j]);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    double* base = part + ((size_t)blockIdx.x * kBK + wave * 8 + c) * STRIDE;
+    if (lane == 0) base[0] = NK[c];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      base[1 + lane + 64 * j] = S[c][j];
+      base[1 + D64 + lane + 64 * j] = Q[c][j];
+    }
   }
 }
 
 // ---------------------------------------------------------------- fixed-order reductions
 __global__ __launch_bounds__(256) void k_reduce_stats(
-    const double* __restrict__ part, const int* __restrict__ counts,
-    const int* __restrict__ well_idx, const int* __restrict__ ill_idx, int nch, int k, int d,
-    int D64, double* __restrict__ nk, double* __restrict__ s, double* __restrict__ q) {
+    const double* __restrict__ part_w, const double* __restrict__ part_i,
+    const int* __restrict__ counts, const int* __restrict__ well_idx,
+    const int* __restrict__ ill_idx, int nch, int grid_i, int64_t n, int k, int d, int D64,
+    double* __restrict__ nk, double* __restrict__ s, double* __restrict__ q) {
   const int64_t width = 1 + 2 * (int64_t)d;
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= 2 * (int64_t)k * width) return;
   const int which = (int)(t / ((int64_t)k * width));
   const int64_t rem = t % ((int64_t)k * width);
   const int slot = (int)(rem / width), c = (int)(rem % width);
-  int comp, kbi;
+  const int64_t stride = 1 + 2 * (int64_t)D64;
+  const int64_t off = c == 0 ? 0 : (c <= d ? 1 + (c - 1) : 1 + D64 + (c - 1 - d));
+  const int dim = c == 0 ? 0 : (c <= d ? c - 1 : c - 1 - d);
+  double acc = 0.0;
+  int comp;
   if (which == 0) {
     if (slot >= counts[0]) return;
     comp = well_idx[slot];
-    kbi = counts[3] + slot / kBK;
+    const int cw = D64 < 128 ? D64 : 128, nh = D64 / cw, hh = dim / cw;
+    const double* p = part_w + ((size_t)((slot / kBK) * nh + hh) * nch * 4 * kBK + (slot % kBK)) * stride + off;
+    for (int ch = 0; ch < nch; ++ch)
+      for (int w = 0; w < 4; ++w) acc += p[((size_t)ch * 4 + w) * kBK * stride];
   } else {
     if (slot >= counts[1]) return;
     comp = ill_idx[slot];
-    kbi = slot / kBK;
+    const int nchk = ill_chunks(grid_i, counts[3], n);
+    const double* p = part_i + ((size_t)(slot / kBK) * nchk * kBK + (slot % kBK)) * stride + off;
+    for (int ch = 0; ch < nchk; ++ch) acc += p[(size_t)ch * kBK * stride];
   }
-  const int64_t stride = 1 + 2 * (int64_t)D64;
-  const int64_t off = c == 0 ? 0 : (c <= d ? 1 + (c - 1) : 1 + D64 + (c - 1 - d));
-  const double* p = part + ((size_t)kbi * nch * kBK + (slot % kBK)) * stride + off;
-  const int64_t cs = (int64_t)kBK * stride;
-  double acc = 0.0;
-  for (int ch = 0; ch < nch; ++ch) acc += p[ch * cs];
   if (c == 0) nk[comp] += acc;
   else if (c <= d) s[(int64_t)comp * d + (c - 1)] += acc;
   else q[(int64_t)comp * d + (c - 1 - d)] += acc;
@@ -702,10 +863,10 @@ inline size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 struct Layout {
   int64_t n;
   int d, k, kpad, D64, m;
-  int nch, nblk;
+  int nch, nh, grid_i;
   int64_t chunk, n_wg_logz;
   size_t off_counts, off_cls, off_cwell, off_cdir, off_well_idx, off_ill_idx, off_cw, off_wp,
-      off_dmu, off_dh, off_dc, off_logz2, off_cslot, off_cr, off_llpart, off_part,
+      off_dmu, off_dh, off_dc, off_logz2, off_cslot, off_cr, off_llpart, off_part_w, off_part_i,
       off_fit_nk, off_fit_s, off_fit_q, total;
 };
 
@@ -724,7 +885,8 @@ bool make_layout(int64_t n, int d, int k, int m, Layout* L) {
   if (c >= 8) c = c / 8 * 8;
   L->nch = (int)(c < 1 ? 1 : c);
   L->chunk = cdiv(n, L->nch);
-  L->nblk = nkb + 1;  // well blocks + ill blocks never exceed ceil(k/32) + 1
+  L->nh = L->D64 <= 128 ? 1 : L->D64 / 128;
+  L->grid_i = nkb > 512 ? nkb : 512;
   L->n_wg_logz = cdiv(n, 64);
   size_t o = 0;
   auto take = [&](size_t bytes) { const size_t r = o; o = align256(o + bytes); return r; };
@@ -743,7 +905,8 @@ bool make_layout(int64_t n, int d, int k, int m, Layout* L) {
   L->off_cslot = take((size_t)n * kT * sizeof(int));
   L->off_cr = take((size_t)n * kT * sizeof(float));
   L->off_llpart = take((size_t)L->n_wg_logz * sizeof(double));
-  L->off_part = take((size_t)L->nblk * L->nch * kBK * (1 + 2 * (size_t)L->D64) * sizeof(double));
+  L->off_part_w = take((size_t)nkb * L->nh * L->nch * 4 * kBK * (1 + 2 * (size_t)L->D64) * sizeof(double));
+  L->off_part_i = take((size_t)L->grid_i * kBK * (1 + 2 * (size_t)L->D64) * sizeof(double));
   L->off_fit_nk = take((size_t)k * sizeof(double) + sizeof(double));  // + loglik slot
   L->off_fit_s = take((size_t)k * d * sizeof(double));
   L->off_fit_q = take((size_t)k * d * sizeof(double));
@@ -780,7 +943,8 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
   float* cr = at<float>(ws, L.off_cr);
   float* logz2 = at<float>(ws, L.off_logz2);
   double* llpart = at<double>(ws, L.off_llpart);
-  double* part = at<double>(ws, L.off_part);
+  double* part_w = at<double>(ws, L.off_part_w);
+  double* part_i = at<double>(ws, L.off_part_i);
   const int vec4 = ((d & 3) == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0) ? 1 : 0;
 
   hipLaunchKernelGGL(k_prep_class, dim3(k), dim3(64), 0, st, w, mu, var, d, cls, cwell, cdir);
@@ -795,13 +959,15 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
   }
   hipLaunchKernelGGL(k_logz<D64>, dim3((unsigned)L.n_wg_logz), dim3(256), 0, st, x, n, d, vec4,
                      wp, cw, well_idx, ill_idx, dmu, dh, dc, counts, logz2, cslot, cr, llpart);
-  hipLaunchKernelGGL(k_stats<D64>, dim3((unsigned)(L.nblk * L.nch)), dim3(256), 0, st, x, n, d,
-                     vec4, wp, cw, ill_idx, dmu, dh, dc, counts, logz2, cslot, cr, L.nch, L.chunk,
-                     part);
+  hipLaunchKernelGGL(k_stats_well<D64>, dim3((unsigned)((kpad / kBK) * L.nh * L.nch)), dim3(256),
+                     0, st, x, n, d, vec4, wp, cw, counts, logz2, cslot, cr, L.nch, L.chunk,
+                     part_w);
+  hipLaunchKernelGGL(k_stats_ill<D64>, dim3((unsigned)L.grid_i), dim3(256), 0, st, x, n, d, vec4,
+                     ill_idx, dmu, dh, dc, counts, logz2, part_i);
   {
     const int64_t tot = 2 * (int64_t)k * (1 + 2 * (int64_t)d);
-    hipLaunchKernelGGL(k_reduce_stats, dim3((unsigned)cdiv(tot, 256)), dim3(256), 0, st, part,
-                       counts, well_idx, ill_idx, L.nch, k, d, D64, nk, s, q);
+    hipLaunchKernelGGL(k_reduce_stats, dim3((unsigned)cdiv(tot, 256)), dim3(256), 0, st, part_w,
+                       part_i, counts, well_idx, ill_idx, L.nch, L.grid_i, n, k, d, D64, nk, s, q);
   }
   hipLaunchKernelGGL(k_reduce_ll, dim3(1), dim3(1024), 0, st, llpart, L.n_wg_logz, loglik,
                      ll_accumulate);
