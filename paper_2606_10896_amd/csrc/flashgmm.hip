@@ -52,6 +52,7 @@ constexpr double kLog2Pi = 1.8378770664093454835606594728112;  // log(2 pi)
 // the fp32 expanded form is good to ~1e-2 in log2 units, plenty for screening
 constexpr double kIllSum = 2.0e5;
 constexpr int kT = 4;                   // exact responsibilities stored per point
+constexpr int kFlush = 64;              // k_stats_well: fp32 -> fp64 every 64 iterations
 constexpr float kWindow = 40.0f;        // refine components with r > 2^-40
 
 typedef float f16v __attribute__((ext_vector_type(16)));
@@ -123,10 +124,17 @@ __device__ __forceinline__ void logits_block(const float* xs, int row0,
   const int lane = threadIdx.x & 63, h = lane >> 5, col = lane & 31;
   const float* xr = xs + (row0 + col) * P + 4 * h;
   f16v a0 = {}, a1 = {};
+  // parameter operands are loaded two steps ahead of their use
+  float4 n0 = wp[lane], n1 = wp[QH * 64 + lane];
+  float4 m0 = wp[64 + lane], m1 = wp[(QH + 1) * 64 + lane];
 #pragma unroll 2
   for (int q = 0; q < QH; ++q) {
-    const float4 b0 = wp[q * 64 + lane];
-    const float4 b1 = wp[(QH + q) * 64 + lane];
+    const float4 b0 = n0, b1 = n1;
+    n0 = m0; n1 = m1;
+    if (q + 2 < QH) {
+      m0 = wp[(q + 2) * 64 + lane];
+      m1 = wp[(QH + q + 2) * 64 + lane];
+    }
     const float4 a = *reinterpret_cast<const float4*>(xr + 8 * q);
     a0 = mfma32(a.x, b0.x, a0);
     a1 = mfma32(a.x * a.x, b1.x, a1);
@@ -151,10 +159,16 @@ __device__ __forceinline__ void logits_2blocks(const float* xs, const float4* __
   const float* xr0 = xs + col * P + 4 * h;
   const float* xr1 = xs + (32 + col) * P + 4 * h;
   f16v a0 = {}, a1 = {}, c0 = {}, c1 = {};
+  float4 n0 = wp[lane], n1 = wp[QH * 64 + lane];
+  float4 m0 = wp[64 + lane], m1 = wp[(QH + 1) * 64 + lane];
 #pragma unroll 2
   for (int q = 0; q < QH; ++q) {
-    const float4 b0 = wp[q * 64 + lane];
-    const float4 b1 = wp[(QH + q) * 64 + lane];
+    const float4 b0 = n0, b1 = n1;
+    n0 = m0; n1 = m1;
+    if (q + 2 < QH) {
+      m0 = wp[(q + 2) * 64 + lane];
+      m1 = wp[(QH + q + 2) * 64 + lane];
+    }
     const float4 a = *reinterpret_cast<const float4*>(xr0 + 8 * q);
     const float4 c = *reinterpret_cast<const float4*>(xr1 + 8 * q);
     a0 = mfma32(a.x, b0.x, a0);
@@ -495,20 +509,24 @@ __global__ __launch_bounds__(256) void k_logz(
 }
 
 // ---------------------------------------------------------------- Step 2: statistics, well set
-// Grid: (component block kb, column half, point chunk).  Every 128-point
-// iteration:
-//   load      X tile and log2 Z into LDS; the refined (point, component)
-//             pairs of this block, taken from k_logz's per-point lists, are
-//             compacted in (point, rank) order and flagged per point.
-//   dense     wave w: MFMA log-densities of points 32w..32w+31 against the
-//             block, r = 2^(l - log2 Z) kept in registers with the refined pairs
-//             set to 0, then the statistic contraction r^T [x | x^2] on MFMA
-//             straight from those registers (the accumulator layout of the
-//             log-density MFMA is the operand layout of the statistic MFMA).
-//             fp32 accumulators are folded into fp64 every 16 iterations.
-//   sparse    the refined pairs (at most kT per point, the only ones that can
-//             carry a large share of a component) in fp64: exact products
-//             r * x and r * x^2, so q/n - mu^2 loses nothing to cancellation.
+// Grid: (component block kb, column half, point chunk).  The block's packed
+// MFMA operand is copied to LDS once.  Every 128-point iteration:
+//   the tile prefetched into registers during the previous iteration (X,
+//   log2 Z, the refined lists) is stored to LDS, and the next tile's loads are
+//   issued so that they overlap this tile's MFMA work;
+//   each wave compacts the refined pairs of its 32 points that fall in this
+//   block (in (point, rank) order) and flags them;
+//   dense: wave w forms the MFMA log-densities of points 32w..32w+31,
+//   r = 2^(l - log2 Z) with the refined pairs set to 0, and contracts
+//   r^T [x | x^2] on MFMA straight from those registers (the accumulator layout
+//   of the log-density MFMA is the operand layout of the statistic MFMA); the
+//   fp32 accumulators, which only carry responsibilities outside the refined
+//   set, are folded into fp64 every kFlush iterations;
+//   sparse: the refined pairs (at most kT per point, the only ones that can
+//   carry a large share of a component) are accumulated in fp64 with exact
+//   products r * x and r * x^2, so q/n - mu^2 loses nothing to cancellation.
+// Each wave owns a partial region; the sparse sums of component c go to the
+// region of wave c/8, the wave whose lanes accumulate them.
 // A column half covers 128 dimensions of x and the same of x^2; d <= 128 needs
 // one half, larger d two (the log-densities are then formed once per half).
 template <int D64>
@@ -523,12 +541,21 @@ __global__ __launch_bounds__(256) void k_stats_well(
   constexpr int NH = D64 / CW;                  // column halves
   constexpr int STRIDE = 1 + 2 * D64;
   constexpr int NLC = 1 + 2 * CW;               // sparse columns: N_k, x dims, x^2 dims
+  constexpr int Q4 = D64 / 4;                   // float4 per row
+  constexpr int PTS = D64 <= 128 ? 128 : 64;    // points per iteration (LDS budget)
+  constexpr int NT = PTS / 32;                  // 32-point tiles per iteration
+  constexpr int LD = PTS * Q4 / 256;            // float4 per thread per tile
+  static_assert(kT == 4, "refined lists are loaded as int4/float4");
+  constexpr bool WLDS = D64 <= 128;             // packed operand copied to LDS
   constexpr int NSC = (NLC + 7) / 8;
-  __shared__ __align__(16) float xs[128 * P];
-  __shared__ float lzs[128];
-  __shared__ unsigned rbits[128];
-  __shared__ int2 ent[128 * kT];
-  __shared__ int ecnt;
+  __shared__ __align__(16) float xs[PTS * P];
+  __shared__ __align__(16) float4 wps[WLDS ? Q4 * 64 : 1];
+  __shared__ float lzs[PTS];
+  __shared__ unsigned rbits[PTS];
+  __shared__ __align__(16) int4 lsl[PTS];
+  __shared__ __align__(16) float4 lrr[PTS];
+  __shared__ int2 ent[4][32 * kT];
+  __shared__ int ecnt[4];
   const int kb = blockIdx.x / (NH * nch);
   const int hh = (blockIdx.x / nch) % NH;
   const int chunk = blockIdx.x % nch;
@@ -537,23 +564,64 @@ __global__ __launch_bounds__(256) void k_stats_well(
   const int64_t p0 = (int64_t)chunk * chunk_pts;
   const int64_t p1 = p0 + chunk_pts < n ? p0 + chunk_pts : n;
   const float cb = cw[kb * kBK + col];
-  const float4* wpk = wp + (size_t)kb * (D64 / 4) * 64;
+  const float4* wpk = wp + (size_t)kb * Q4 * 64;
+  if constexpr (WLDS) {
+    for (int i = tid; i < Q4 * 64; i += 256) wps[i] = wpk[i];
+  }
+  const float4* wsrc = WLDS ? wps : wpk;
+  double sacc[NSC];                             // refined-pair sums of component sc, fp64
+#pragma unroll
+  for (int i = 0; i < NSC; ++i) sacc[i] = 0.0;
   const int c0 = hh * CW;                       // first x dimension of this half
   double* pk = part + (size_t)blockIdx.x * 4 * kBK * STRIDE;
+  double* pw = pk + (size_t)wave * kBK * STRIDE;
 
   f16v acc[2 * NE];
 #pragma unroll
   for (int e = 0; e < 2 * NE; ++e) acc[e] = f16v{};
   float nkacc = 0.0f;
-  double sacc[NSC];
-#pragma unroll
-  for (int i = 0; i < NSC; ++i) sacc[i] = 0.0;
   const int sc = tid >> 3, sg = tid & 7;        // sparse lane: component, column group
   bool first = true;
   int iter = 0;
 
-  // each wave accumulates its own point tiles into its own partial region
-  double* pw = pk + (size_t)wave * kBK * STRIDE;
+  // register prefetch of one tile
+  float4 px[LD];
+  float plz = INFINITY;
+  int4 psl = make_int4(-1, -1, -1, -1);
+  float4 prr = make_float4(0.f, 0.f, 0.f, 0.f);
+  auto prefetch = [&](int64_t it) {
+#pragma unroll
+    for (int j = 0; j < LD; ++j) {
+      const int idx = tid + 256 * j, r = idx / Q4, c = (idx % Q4) * 4;
+      const int64_t nn = it + r;
+      float4 v;
+      if (vec4) {
+        // branch-free: out-of-range lanes read row 0 and are zeroed
+        const bool ok = nn < p1 && c < d;
+        v = *reinterpret_cast<const float4*>(x + (ok ? nn * d + c : 0));
+        if (!ok) v = make_float4(0.f, 0.f, 0.f, 0.f);
+      } else {
+        v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (nn < p1) {
+          const float* xr = x + nn * d;
+          v.x = c < d ? xr[c] : 0.f;
+          v.y = c + 1 < d ? xr[c + 1] : 0.f;
+          v.z = c + 2 < d ? xr[c + 2] : 0.f;
+          v.w = c + 3 < d ? xr[c + 3] : 0.f;
+        }
+      }
+      px[j] = v;
+    }
+    if (tid < PTS) {
+      const int64_t nn = it + tid;
+      plz = nn < p1 ? logz2[nn] : INFINITY;
+      psl = nn < p1 ? *reinterpret_cast<const int4*>(cslot + nn * kT) : make_int4(-1, -1, -1, -1);
+      prr = nn < p1 ? *reinterpret_cast<const float4*>(cr + nn * kT) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  };
+
+  // fold the fp32 accumulators into this wave's fp64 partial; all loads of a
+  // 32-column block are issued before its stores so their latency is paid once
   auto flush = [&]() {
     const float nk2 = nkacc + __shfl_xor(nkacc, 32);
     double* pc = pw + (size_t)col * STRIDE;
@@ -561,56 +629,71 @@ __global__ __launch_bounds__(256) void k_stats_well(
 #pragma unroll
     for (int e = 0; e < NE; ++e) {
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int i = 8 * (v >> 2) + 4 * h + (v & 3);
-        const int dim = c0 + NE * i + e;
-        double* ds = pc + 1 + dim;
-        double* dq = pc + 1 + D64 + dim;
-        *ds = first ? (double)acc[e][v] : *ds + (double)acc[e][v];
-        *dq = first ? (double)acc[NE + e][v] : *dq + (double)acc[NE + e][v];
-        acc[e][v] = 0.0f;
-        acc[NE + e][v] = 0.0f;
+      for (int v0 = 0; v0 < 16; v0 += 8) {
+        double os[8], oq[8];
+#pragma unroll
+        for (int v = v0; v < v0 + 8; ++v) {
+          const int dim = c0 + NE * (8 * (v >> 2) + 4 * h + (v & 3)) + e;
+          os[v - v0] = first ? 0.0 : pc[1 + dim];
+          oq[v - v0] = first ? 0.0 : pc[1 + D64 + dim];
+        }
+#pragma unroll
+        for (int v = v0; v < v0 + 8; ++v) {
+          const int dim = c0 + NE * (8 * (v >> 2) + 4 * h + (v & 3)) + e;
+          pc[1 + dim] = os[v - v0] + (double)acc[e][v];
+          pc[1 + D64 + dim] = oq[v - v0] + (double)acc[NE + e][v];
+          acc[e][v] = 0.0f;
+          acc[NE + e][v] = 0.0f;
+        }
       }
     }
     nkacc = 0.0f;
     first = false;
   };
 
-  for (int64_t it = p0; it < p1; it += 128, ++iter) {
-    __syncthreads();
-    load_tile<D64>(x, p1, d, it, 128, xs, vec4 != 0);
-    if (tid < 128) {
-      lzs[tid] = (it + tid < p1) ? logz2[it + tid] : INFINITY;
+  if (p0 < p1) prefetch(p0);
+  for (int64_t it = p0; it < p1; it += PTS, ++iter) {
+    __syncthreads();   // every read of the previous tile is done
+#pragma unroll
+    for (int j = 0; j < LD; ++j) {
+      const int idx = tid + 256 * j, r = idx / Q4, c = (idx % Q4) * 4;
+      *reinterpret_cast<float4*>(xs + r * P + c) = px[j];
+    }
+    if (tid < PTS) {
+      lzs[tid] = plz;
       rbits[tid] = 0u;
+      lsl[tid] = psl;
+      lrr[tid] = prr;
     }
     __syncthreads();
-    if (wave == 0) {
-      // compact the refined pairs of this block, in (point, rank) order
+    if (it + PTS < p1) prefetch(it + PTS);
+    // refined pairs of this wave's points that fall in this block
+    if (wave < NT) {
       int cnt = 0;
-      for (int q = 0; q < 128 * kT / 64; ++q) {
-        const int e = q * 64 + lane, pt = e / kT, j = e % kT;
-        int sl = -1;
-        float rv = 0.0f;
-        if (it + pt < p1) {
-          sl = cslot[(it + pt) * kT + j];
-          rv = cr[(it + pt) * kT + j];
-        }
+#pragma unroll
+      for (int q = 0; q < 32 * kT / 64; ++q) {
+        const int e = q * 64 + lane, pt = wave * 32 + e / kT, j = e % kT;
+        const int4 sl4 = lsl[pt];
+        const float4 rr4 = lrr[pt];
+        const int sl = j == 0 ? sl4.x : (j == 1 ? sl4.y : (j == 2 ? sl4.z : sl4.w));
+        const float rv = j == 0 ? rr4.x : (j == 1 ? rr4.y : (j == 2 ? rr4.z : rr4.w));
         const bool mine = sl >= 0 && (sl >> 5) == kb;
         const unsigned long long bal = __ballot(mine);
         if (mine) {
           const int pos = cnt + __popcll(bal & ((1ull << lane) - 1ull));
-          ent[pos] = make_int2((pt << 5) | (sl & 31), __float_as_int(rv));
+          ent[wave][pos] = make_int2((pt << 5) | (sl & 31), __float_as_int(rv));
           atomicOr(&rbits[pt], 1u << (sl & 31));
         }
         cnt += __popcll(bal);
       }
-      if (lane == 0) ecnt = cnt;
+      if (lane == 0) ecnt[wave] = cnt;
+    } else if (lane == 0) {
+      ecnt[wave] = 0;
     }
-    __syncthreads();
     // dense part: log-densities, responsibilities and statistics of tile `wave`
-    {
+    if (wave < NT) {
       f16v l;
-      logits_block<D64>(xs, wave * 32, wpk, cb, l);
+      logits_block<D64>(xs, wave * 32, wsrc, cb, l);
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int row = wave * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
@@ -641,11 +724,12 @@ __global__ __launch_bounds__(256) void k_stats_well(
         }
       }
     }
+    __syncthreads();   // every wave's refined list is complete
     // sparse part: refined pairs in fp64 (lane = component sc, column group sg)
-    {
-      const int ne = ecnt;
+    for (int w2 = 0; w2 < 4; ++w2) {
+      const int ne = ecnt[w2];
       for (int e = 0; e < ne; ++e) {
-        const int2 en = ent[e];
+        const int2 en = ent[w2][e];
         const int comp = en.x & 31;
         if ((comp >> 3) != wave) continue;          // wave-uniform
         if (comp == sc) {
@@ -665,24 +749,35 @@ __global__ __launch_bounds__(256) void k_stats_well(
         }
       }
     }
-    if ((iter % 16) == 15) flush();
+    if ((iter % kFlush) == kFlush - 1) flush();
   }
-  if (first || (iter % 16) != 0) flush();
+  if (first || (iter % kFlush) != 0) flush();
   __syncthreads();
   // add the sparse fp64 part into the region of the wave that owns the component
-  // (lane sc's wave), after that wave's last dense flush
   {
     double* pc = pk + ((size_t)wave * kBK + sc) * STRIDE;
+    double old[NSC];
 #pragma unroll
     for (int i = 0; i < NSC; ++i) {
       const int lc = sg + 8 * i;
+      int off = -1;
       if (lc < NLC) {
-        int off;
         if (lc == 0) off = hh == 0 ? 0 : -1;
         else if (lc <= CW) off = 1 + c0 + (lc - 1);
         else off = 1 + D64 + c0 + (lc - 1 - CW);
-        if (off >= 0) pc[off] += sacc[i];
       }
+      old[i] = off >= 0 ? pc[off] : 0.0;
+    }
+#pragma unroll
+    for (int i = 0; i < NSC; ++i) {
+      const int lc = sg + 8 * i;
+      int off = -1;
+      if (lc < NLC) {
+        if (lc == 0) off = hh == 0 ? 0 : -1;
+        else if (lc <= CW) off = 1 + c0 + (lc - 1);
+        else off = 1 + D64 + c0 + (lc - 1 - CW);
+      }
+      if (off >= 0) pc[off] = old[i] + sacc[i];
     }
   }
 }
