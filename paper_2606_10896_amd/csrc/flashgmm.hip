@@ -509,53 +509,75 @@ __global__ __launch_bounds__(256) void k_logz(
 }
 
 // ---------------------------------------------------------------- Step 2: statistics, well set
-// Grid: (component block kb, column half, point chunk).  The block's packed
-// MFMA operand is copied to LDS once.  Every 128-point iteration:
+// Grid: (component block kb, column part, point chunk); two workgroups share a
+// CU (about 58 KB of LDS and at most 256 registers per wave), so each SIMD
+// interleaves two waves.  Every 64-point iteration (two 32-point tiles):
 //   the tile prefetched into registers during the previous iteration (X,
-//   log2 Z, the refined lists) is stored to LDS, and the next tile's loads are
-//   issued so that they overlap this tile's MFMA work;
-//   each wave compacts the refined pairs of its 32 points that fall in this
+//   log2 Z, the refined lists) is stored to LDS;
+//   wave w compacts the refined pairs of points 16w..16w+15 that fall in this
 //   block (in (point, rank) order) and flags them;
-//   dense: wave w forms the MFMA log-densities of points 32w..32w+31,
-//   r = 2^(l - log2 Z) with the refined pairs set to 0, and contracts
-//   r^T [x | x^2] on MFMA straight from those registers (the accumulator layout
-//   of the log-density MFMA is the operand layout of the statistic MFMA); the
-//   fp32 accumulators, which only carry responsibilities outside the refined
-//   set, are folded into fp64 every kFlush iterations;
+//   producers: waves 2t and 2t+1 form the x and x^2 chains of the log-density
+//   MFMA of tile t (the contraction order of k_logz), wave 2t adds them and
+//   the bias, takes r = 2^(l - log2 Z) with the refined pairs set to 0, and
+//   writes the r tile to LDS;
+//   consumers: wave w owns a quarter of the statistic columns (x low/high
+//   half, x^2 low/high half of the column part) and contracts r^T [x | x^2]
+//   over both r tiles on MFMA; the fp32 accumulators, which only carry
+//   responsibilities outside the refined set, are folded into fp64 every
+//   kFlush iterations;
 //   sparse: the refined pairs (at most kT per point, the only ones that can
 //   carry a large share of a component) are accumulated in fp64 with exact
 //   products r * x and r * x^2, so q/n - mu^2 loses nothing to cancellation.
-// Each wave owns a partial region; the sparse sums of component c go to the
-// region of wave c/8, the wave whose lanes accumulate them.
-// A column half covers 128 dimensions of x and the same of x^2; d <= 128 needs
-// one half, larger d two (the log-densities are then formed once per half).
+// The next tile's loads are issued after the producers, so their latency
+// overlaps the consumer MFMAs.  Each wave owns a partial region: its
+// statistic columns, the N_k of its producer tile (waves 0 and 2), and the
+// refined sums of components 8w..8w+7; everything else in it is zero.
 template <int D64>
-__global__ __launch_bounds__(256) void k_stats_well(
+__device__ __forceinline__ void logits_chain(const float* xs, int row0, bool xsq,
+                                             const float4* __restrict__ wpc, f16v& acc) {
+  constexpr int P = D64 + 4, QH = D64 / 8;
+  const int lane = threadIdx.x & 63, h = lane >> 5, col = lane & 31;
+  const float* xr = xs + (row0 + col) * P + 4 * h;
+  f16v a = {};
+  float4 n0 = wpc[lane], m0 = wpc[64 + lane];
+#pragma unroll 4
+  for (int q = 0; q < QH; ++q) {
+    const float4 b = n0;
+    n0 = m0;
+    if (q + 2 < QH) m0 = wpc[(q + 2) * 64 + lane];
+    float4 v = *reinterpret_cast<const float4*>(xr + 8 * q);
+    if (xsq) { v.x *= v.x; v.y *= v.y; v.z *= v.z; v.w *= v.w; }
+    a = mfma32(v.x, b.x, a);
+    a = mfma32(v.y, b.y, a);
+    a = mfma32(v.z, b.z, a);
+    a = mfma32(v.w, b.w, a);
+  }
+  acc = a;
+}
+
+template <int D64>
+__global__ __launch_bounds__(256, 2) void k_stats_well(
     const float* __restrict__ x, int64_t n, int d, int vec4, const float4* __restrict__ wp,
     const float* __restrict__ cw, const int* __restrict__ counts,
-    const float* __restrict__ logz2, const int* __restrict__ cslot,
-    const float* __restrict__ cr, int nch, int64_t chunk_pts, double* __restrict__ part) {
+    const float* __restrict__ logz2, const int* __restrict__ cslot, int nch,
+    int64_t chunk_pts, double* __restrict__ part) {
   constexpr int P = D64 + 4;
-  constexpr int CW = D64 < 128 ? D64 : 128;     // x dimensions per column half
-  constexpr int NE = CW / 32;                   // 32-column MFMA blocks per part
-  constexpr int NH = D64 / CW;                  // column halves
+  constexpr int CW = D64 % 128 == 0 ? 128 : 64;  // x dimensions per column part
+  constexpr int NH = D64 / CW;                  // column parts
+  constexpr int NE = CW / 64;                   // 32-column MFMA blocks per consumer wave
   constexpr int STRIDE = 1 + 2 * D64;
-  constexpr int NLC = 1 + 2 * CW;               // sparse columns: N_k, x dims, x^2 dims
   constexpr int Q4 = D64 / 4;                   // float4 per row
-  constexpr int PTS = D64 <= 128 ? 128 : 64;    // points per iteration (LDS budget)
-  constexpr int NT = PTS / 32;                  // 32-point tiles per iteration
+  constexpr int QH = D64 / 8;
+  constexpr int PTS = 64;                       // points per iteration
   constexpr int LD = PTS * Q4 / 256;            // float4 per thread per tile
+  constexpr int RP = 20;                        // r / partial tile lane pitch (floats)
   static_assert(kT == 4, "refined lists are loaded as int4/float4");
-  constexpr bool WLDS = D64 <= 128;             // packed operand copied to LDS
-  constexpr int NSC = (NLC + 7) / 8;
   __shared__ __align__(16) float xs[PTS * P];
-  __shared__ __align__(16) float4 wps[WLDS ? Q4 * 64 : 1];
+  __shared__ __align__(16) float rt[2 * 64 * RP];
+  __shared__ __align__(16) float pl[2 * 64 * RP];
   __shared__ float lzs[PTS];
   __shared__ unsigned rbits[PTS];
   __shared__ __align__(16) int4 lsl[PTS];
-  __shared__ __align__(16) float4 lrr[PTS];
-  __shared__ int2 ent[4][32 * kT];
-  __shared__ int ecnt[4];
   const int kb = blockIdx.x / (NH * nch);
   const int hh = (blockIdx.x / nch) % NH;
   const int chunk = blockIdx.x % nch;
@@ -564,31 +586,24 @@ __global__ __launch_bounds__(256) void k_stats_well(
   const int64_t p0 = (int64_t)chunk * chunk_pts;
   const int64_t p1 = p0 + chunk_pts < n ? p0 + chunk_pts : n;
   const float cb = cw[kb * kBK + col];
-  const float4* wpk = wp + (size_t)kb * Q4 * 64;
-  if constexpr (WLDS) {
-    for (int i = tid; i < Q4 * 64; i += 256) wps[i] = wpk[i];
-  }
-  const float4* wsrc = WLDS ? wps : wpk;
-  double sacc[NSC];                             // refined-pair sums of component sc, fp64
-#pragma unroll
-  for (int i = 0; i < NSC; ++i) sacc[i] = 0.0;
-  const int c0 = hh * CW;                       // first x dimension of this half
-  double* pk = part + (size_t)blockIdx.x * 4 * kBK * STRIDE;
-  double* pw = pk + (size_t)wave * kBK * STRIDE;
+  const int ptile = wave >> 1;                  // producer: tile
+  const bool pxsq = (wave & 1) != 0;            // producer: x^2 chain
+  const float4* wpc = wp + ((size_t)kb * Q4 + (pxsq ? QH : 0)) * 64;
+  const int c0 = hh * CW;                       // first x dimension of this part
+  const bool sq = wave >= 2;                    // consumer: x^2 columns
+  const int cdim = c0 + (wave & 1) * (CW / 2);  // consumer: first dimension
+  double* pw = part + ((size_t)blockIdx.x * 4 + wave) * kBK * STRIDE;
 
-  f16v acc[2 * NE];
+  f16v acc[NE];
 #pragma unroll
-  for (int e = 0; e < 2 * NE; ++e) acc[e] = f16v{};
+  for (int e = 0; e < NE; ++e) acc[e] = f16v{};
   float nkacc = 0.0f;
-  const int sc = tid >> 3, sg = tid & 7;        // sparse lane: component, column group
   bool first = true;
   int iter = 0;
 
-  // register prefetch of one tile
   float4 px[LD];
   float plz = INFINITY;
   int4 psl = make_int4(-1, -1, -1, -1);
-  float4 prr = make_float4(0.f, 0.f, 0.f, 0.f);
   auto prefetch = [&](int64_t it) {
 #pragma unroll
     for (int j = 0; j < LD; ++j) {
@@ -596,7 +611,6 @@ __global__ __launch_bounds__(256) void k_stats_well(
       const int64_t nn = it + r;
       float4 v;
       if (vec4) {
-        // branch-free: out-of-range lanes read row 0 and are zeroed
         const bool ok = nn < p1 && c < d;
         v = *reinterpret_cast<const float4*>(x + (ok ? nn * d + c : 0));
         if (!ok) v = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -614,36 +628,40 @@ __global__ __launch_bounds__(256) void k_stats_well(
     }
     if (tid < PTS) {
       const int64_t nn = it + tid;
-      plz = nn < p1 ? logz2[nn] : INFINITY;
-      psl = nn < p1 ? *reinterpret_cast<const int4*>(cslot + nn * kT) : make_int4(-1, -1, -1, -1);
-      prr = nn < p1 ? *reinterpret_cast<const float4*>(cr + nn * kT) : make_float4(0.f, 0.f, 0.f, 0.f);
+      const bool ok = nn < p1;
+      const int64_t src = ok ? nn : 0;
+      plz = ok ? logz2[src] : INFINITY;
+      psl = *reinterpret_cast<const int4*>(cslot + src * kT);
+      if (!ok) psl = make_int4(-1, -1, -1, -1);
     }
   };
 
-  // fold the fp32 accumulators into this wave's fp64 partial; all loads of a
-  // 32-column block are issued before its stores so their latency is paid once
   auto flush = [&]() {
     const float nk2 = nkacc + __shfl_xor(nkacc, 32);
-    double* pc = pw + (size_t)col * STRIDE;
-    if (h == 0 && hh == 0) pc[0] = first ? (double)nk2 : pc[0] + (double)nk2;
+    if (first) {
+      for (int i = lane; i < kBK * STRIDE; i += 64) pw[i] = 0.0;
+    }
+    if (h == 0 && hh == 0 && !pxsq) {
+      double* dst = pw + (size_t)col * STRIDE;
+      dst[0] = first ? (double)nk2 : dst[0] + (double)nk2;
+    }
 #pragma unroll
     for (int e = 0; e < NE; ++e) {
 #pragma unroll
       for (int v0 = 0; v0 < 16; v0 += 8) {
-        double os[8], oq[8];
+        double o[8];
 #pragma unroll
         for (int v = v0; v < v0 + 8; ++v) {
-          const int dim = c0 + NE * (8 * (v >> 2) + 4 * h + (v & 3)) + e;
-          os[v - v0] = first ? 0.0 : pc[1 + dim];
-          oq[v - v0] = first ? 0.0 : pc[1 + D64 + dim];
+          const int i = 8 * (v >> 2) + 4 * h + (v & 3);
+          const int dim = cdim + NE * i + e;
+          o[v - v0] = first ? 0.0 : pw[(size_t)col * STRIDE + 1 + (sq ? D64 : 0) + dim];
         }
 #pragma unroll
         for (int v = v0; v < v0 + 8; ++v) {
-          const int dim = c0 + NE * (8 * (v >> 2) + 4 * h + (v & 3)) + e;
-          pc[1 + dim] = os[v - v0] + (double)acc[e][v];
-          pc[1 + D64 + dim] = oq[v - v0] + (double)acc[NE + e][v];
+          const int i = 8 * (v >> 2) + 4 * h + (v & 3);
+          const int dim = cdim + NE * i + e;
+          pw[(size_t)col * STRIDE + 1 + (sq ? D64 : 0) + dim] = o[v - v0] + (double)acc[e][v];
           acc[e][v] = 0.0f;
-          acc[NE + e][v] = 0.0f;
         }
       }
     }
@@ -663,121 +681,208 @@ __global__ __launch_bounds__(256) void k_stats_well(
       lzs[tid] = plz;
       rbits[tid] = 0u;
       lsl[tid] = psl;
-      lrr[tid] = prr;
     }
     __syncthreads();
-    if (it + PTS < p1) prefetch(it + PTS);
-    // refined pairs of this wave's points that fall in this block
-    if (wave < NT) {
-      int cnt = 0;
-#pragma unroll
-      for (int q = 0; q < 32 * kT / 64; ++q) {
-        const int e = q * 64 + lane, pt = wave * 32 + e / kT, j = e % kT;
-        const int4 sl4 = lsl[pt];
-        const float4 rr4 = lrr[pt];
-        const int sl = j == 0 ? sl4.x : (j == 1 ? sl4.y : (j == 2 ? sl4.z : sl4.w));
-        const float rv = j == 0 ? rr4.x : (j == 1 ? rr4.y : (j == 2 ? rr4.z : rr4.w));
-        const bool mine = sl >= 0 && (sl >> 5) == kb;
-        const unsigned long long bal = __ballot(mine);
-        if (mine) {
-          const int pos = cnt + __popcll(bal & ((1ull << lane) - 1ull));
-          ent[wave][pos] = make_int2((pt << 5) | (sl & 31), __float_as_int(rv));
-          atomicOr(&rbits[pt], 1u << (sl & 31));
-        }
-        cnt += __popcll(bal);
-      }
-      if (lane == 0) ecnt[wave] = cnt;
-    } else if (lane == 0) {
-      ecnt[wave] = 0;
+    {
+      // flag the refined pairs of points 16w..16w+15 that fall in this block
+      const int pt = wave * 16 + lane / kT, j = lane % kT;
+      const int4 sl4 = lsl[pt];
+      const int sl = j == 0 ? sl4.x : (j == 1 ? sl4.y : (j == 2 ? sl4.z : sl4.w));
+      if (sl >= 0 && (sl >> 5) == kb) atomicOr(&rbits[pt], 1u << (sl & 31));
     }
-    // dense part: log-densities, responsibilities and statistics of tile `wave`
-    if (wave < NT) {
-      f16v l;
-      logits_block<D64>(xs, wave * 32, wsrc, cb, l);
+    // producers: one chain of tile `ptile`
+    {
+      f16v a;
+      logits_chain<D64>(xs, ptile * 32, pxsq, wpc, a);
+      if (pxsq) {
+        float* dst = pl + (ptile * 64 + lane) * RP;
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = wave * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
-        float r = exp2_fast(l[v] - lzs[row]);
-        r = ((rbits[row] >> col) & 1u) ? 0.0f : r;
-        nkacc += r;
-        l[v] = r;
+        for (int v = 0; v < 16; v += 4)
+          *reinterpret_cast<float4*>(dst + v) = make_float4(a[v], a[v + 1], a[v + 2], a[v + 3]);
+      }
+      __syncthreads();   // x^2 chains and refined flags complete
+      if (!pxsq) {
+        const float* srcp = pl + (ptile * 64 + lane) * RP;
+        float* dst = rt + (ptile * 64 + lane) * RP;
+#pragma unroll
+        for (int v = 0; v < 16; v += 4) {
+          const float4 b = *reinterpret_cast<const float4*>(srcp + v);
+          const float bb[4] = {b.x, b.y, b.z, b.w};
+          float rr[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int vv = v + u;
+            const int row = ptile * 32 + 8 * (vv >> 2) + 4 * h + (vv & 3);
+            const float l = (a[vv] + bb[u]) + cb;
+            float r = exp2_fast(l - lzs[row]);
+            r = ((rbits[row] >> col) & 1u) ? 0.0f : r;
+            nkacc += r;
+            rr[u] = r;
+          }
+          *reinterpret_cast<float4*>(dst + v) = make_float4(rr[0], rr[1], rr[2], rr[3]);
+        }
+      }
+    }
+    __syncthreads();   // r tiles complete
+    if (it + PTS < p1) prefetch(it + PTS);
+    // consumers: statistic contraction for this wave's columns over both tiles
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const float* src = rt + (t * 64 + lane) * RP;
+      float rb[16];
+#pragma unroll
+      for (int v = 0; v < 16; v += 4) {
+        const float4 q4 = *reinterpret_cast<const float4*>(src + v);
+        rb[v] = q4.x; rb[v + 1] = q4.y; rb[v + 2] = q4.z; rb[v + 3] = q4.w;
       }
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const int row = wave * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
-        const float* xp = xs + row * P + c0 + NE * col;
+        const int row = t * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
+        const float* xp = xs + row * P + cdim + NE * col;
         float a[NE];
-        if constexpr (NE == 4) {
-          const float4 t = *reinterpret_cast<const float4*>(xp);
-          a[0] = t.x; a[1] = t.y; a[2] = t.z; a[3] = t.w;
-        } else if constexpr (NE == 2) {
-          const float2 t = *reinterpret_cast<const float2*>(xp);
-          a[0] = t.x; a[1] = t.y;
+        if constexpr (NE == 2) {
+          const float2 q2 = *reinterpret_cast<const float2*>(xp);
+          a[0] = q2.x; a[1] = q2.y;
         } else {
 #pragma unroll
           for (int e = 0; e < NE; ++e) a[e] = xp[e];
         }
 #pragma unroll
-        for (int e = 0; e < NE; ++e) {
-          acc[e] = mfma32(a[e], l[v], acc[e]);
-          acc[NE + e] = mfma32(a[e] * a[e], l[v], acc[NE + e]);
-        }
-      }
-    }
-    __syncthreads();   // every wave's refined list is complete
-    // sparse part: refined pairs in fp64 (lane = component sc, column group sg)
-    for (int w2 = 0; w2 < 4; ++w2) {
-      const int ne = ecnt[w2];
-      for (int e = 0; e < ne; ++e) {
-        const int2 en = ent[w2][e];
-        const int comp = en.x & 31;
-        if ((comp >> 3) != wave) continue;          // wave-uniform
-        if (comp == sc) {
-          const int pt = en.x >> 5;
-          const double r = (double)__int_as_float(en.y);
-          const float* xr = xs + pt * P + c0;
-#pragma unroll
-          for (int i = 0; i < NSC; ++i) {
-            const int lc = sg + 8 * i;
-            if (lc < NLC) {
-              double y = 1.0;
-              if (lc > 0 && lc <= CW) y = (double)xr[lc - 1];
-              else if (lc > CW) { const double xv = (double)xr[lc - 1 - CW]; y = xv * xv; }
-              sacc[i] = fma(r, y, sacc[i]);
-            }
-          }
-        }
+        for (int e = 0; e < NE; ++e) acc[e] = mfma32(sq ? a[e] * a[e] : a[e], rb[v], acc[e]);
       }
     }
     if ((iter % kFlush) == kFlush - 1) flush();
   }
   if (first || (iter % kFlush) != 0) flush();
-  __syncthreads();
-  // add the sparse fp64 part into the region of the wave that owns the component
-  {
-    double* pc = pk + ((size_t)wave * kBK + sc) * STRIDE;
-    double old[NSC];
+}
+
+// Refined pairs of a well block, in fp64.  Grid: (block, sparse chunk).  The
+// chunk's refined lists are scanned 1024 points at a time (the next group's
+// lists are loaded while the current one is processed); the pairs that fall in
+// this block are compacted in (point, rank) order and their rows gathered into
+// LDS in batches.  Wave w owns components 8w .. 8w+7 of the block; lane l owns
+// columns l, l + 64, ... of [1 | x | x^2] and adds r, r * x, r * x^2 (exact
+// products of fp32 values) in that order, in registers.
+template <int D64>
+__global__ __launch_bounds__(256) void k_stats_sparse(
+    const float* __restrict__ x, int64_t n, int d, const int* __restrict__ counts,
+    const int* __restrict__ cslot, const float* __restrict__ cr, int nch, int64_t chunk_pts,
+    double* __restrict__ part) {
+  constexpr int STRIDE = 1 + 2 * D64, NCI = (STRIDE + 63) / 64, NB = D64 <= 128 ? 64 : 32;
+  constexpr int P = D64 + 1;
+  constexpr int G = 4;                          // 256-point groups per scan step
+  __shared__ float xb[NB * P];
+  __shared__ int2 stage[G * 256 * kT];
+  __shared__ int wcnt[4];
+  const int kb = blockIdx.x / nch, chunk = blockIdx.x % nch;
+  if (kb >= counts[2]) return;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int64_t p0 = (int64_t)chunk * chunk_pts;
+  const int64_t p1 = p0 + chunk_pts < n ? p0 + chunk_pts : n;
+  double acc[8][NCI];
 #pragma unroll
-    for (int i = 0; i < NSC; ++i) {
-      const int lc = sg + 8 * i;
-      int off = -1;
-      if (lc < NLC) {
-        if (lc == 0) off = hh == 0 ? 0 : -1;
-        else if (lc <= CW) off = 1 + c0 + (lc - 1);
-        else off = 1 + D64 + c0 + (lc - 1 - CW);
+  for (int j = 0; j < 8; ++j)
+#pragma unroll
+    for (int i = 0; i < NCI; ++i) acc[j][i] = 0.0;
+  int4 sl[G];
+  float4 rr[G];
+  auto load_lists = [&](int64_t base) {
+#pragma unroll
+    for (int u = 0; u < G; ++u) {
+      const int64_t nn = base + u * 256 + tid;
+      if (nn < p1) {
+        sl[u] = *reinterpret_cast<const int4*>(cslot + nn * kT);
+        rr[u] = *reinterpret_cast<const float4*>(cr + nn * kT);
+      } else {
+        sl[u] = make_int4(-1, -1, -1, -1);
+        rr[u] = make_float4(0.f, 0.f, 0.f, 0.f);
       }
-      old[i] = off >= 0 ? pc[off] : 0.0;
+    }
+  };
+  auto in_block = [&](int v) { return v >= 0 && (v >> 5) == kb; };
+  if (p0 < p1) load_lists(p0);
+  for (int64_t base = p0; base < p1; base += G * 256) {
+    int mine[G];
+#pragma unroll
+    for (int u = 0; u < G; ++u) {
+      mine[u] = (int)in_block(sl[u].x) + (int)in_block(sl[u].y) + (int)in_block(sl[u].z) +
+                (int)in_block(sl[u].w);
+    }
+    // entries are staged in (group, thread, rank) order, i.e. in point order
+    int total = 0, pos[G];
+#pragma unroll
+    for (int u = 0; u < G; ++u) {
+      int inc = mine[u];
+      for (int off = 1; off < 64; off <<= 1) {
+        const int v = __shfl_up(inc, off);
+        if (lane >= off) inc += v;
+      }
+      __syncthreads();                          // wcnt free / previous batch consumed
+      if (lane == 63) wcnt[wave] = inc;
+      __syncthreads();
+      int before = 0, all = 0;
+      for (int w2 = 0; w2 < 4; ++w2) {
+        const int c2 = wcnt[w2];
+        if (w2 < wave) before += c2;
+        all += c2;
+      }
+      pos[u] = total + before + inc - mine[u];
+      total += all;
     }
 #pragma unroll
-    for (int i = 0; i < NSC; ++i) {
-      const int lc = sg + 8 * i;
-      int off = -1;
-      if (lc < NLC) {
-        if (lc == 0) off = hh == 0 ? 0 : -1;
-        else if (lc <= CW) off = 1 + c0 + (lc - 1);
-        else off = 1 + D64 + c0 + (lc - 1 - CW);
+    for (int u = 0; u < G; ++u) {
+      const int vs[4] = {sl[u].x, sl[u].y, sl[u].z, sl[u].w};
+      const float rs[4] = {rr[u].x, rr[u].y, rr[u].z, rr[u].w};
+      int q = pos[u];
+#pragma unroll
+      for (int j = 0; j < kT; ++j) {
+        if (in_block(vs[j]))
+          stage[q++] = make_int2(((u * 256 + tid) << 5) | (vs[j] & 31), __float_as_int(rs[j]));
       }
-      if (off >= 0) pc[off] = old[i] + sacc[i];
+    }
+    if (base + G * 256 < p1) load_lists(base + G * 256);
+    for (int b0 = 0; b0 < total; b0 += NB) {
+      const int nb = total - b0 < NB ? total - b0 : NB;
+      __syncthreads();                          // stage written / previous rows consumed
+      for (int i = tid; i < nb * D64; i += 256) {
+        const int e = i / D64, c = i % D64;
+        const int64_t row = base + (stage[b0 + e].x >> 5);
+        xb[e * P + c] = c < d ? x[row * d + c] : 0.0f;
+      }
+      __syncthreads();
+      for (int e = 0; e < nb; ++e) {
+        const int2 en = stage[b0 + e];
+        const int cl = (en.x & 31) - 8 * wave;
+        if (cl < 0 || cl >= 8) continue;
+        const double r = (double)__int_as_float(en.y);
+        const float* xr = xb + e * P;
+        double y[NCI];
+#pragma unroll
+        for (int i = 0; i < NCI; ++i) {
+          const int c = lane + 64 * i;
+          double v = 0.0;
+          if (c == 0) v = 1.0;
+          else if (c <= D64) v = (double)xr[c - 1];
+          else if (c < STRIDE) { const double xv = (double)xr[c - 1 - D64]; v = xv * xv; }
+          y[i] = v;
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          if (cl == j) {
+#pragma unroll
+            for (int i = 0; i < NCI; ++i) acc[j][i] = fma(r, y[i], acc[j][i]);
+          }
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    double* out = part + ((size_t)blockIdx.x * kBK + 8 * wave + j) * STRIDE;
+#pragma unroll
+    for (int i = 0; i < NCI; ++i) {
+      const int c = lane + 64 * i;
+      if (c < STRIDE) out[c] = acc[j][i];
     }
   }
 }
@@ -871,10 +976,11 @@ __global__ __launch_bounds__(256) void k_stats_ill(
 
 // ---------------------------------------------------------------- fixed-order reductions
 __global__ __launch_bounds__(256) void k_reduce_stats(
-    const double* __restrict__ part_w, const double* __restrict__ part_i,
+    const double* __restrict__ part_w, const double* __restrict__ part_s,
+    const double* __restrict__ part_i,
     const int* __restrict__ counts, const int* __restrict__ well_idx,
-    const int* __restrict__ ill_idx, int nch, int grid_i, int64_t n, int k, int d, int D64,
-    double* __restrict__ nk, double* __restrict__ s, double* __restrict__ q) {
+    const int* __restrict__ ill_idx, int nch, int nch_s, int grid_i, int64_t n, int k, int d,
+    int D64, double* __restrict__ nk, double* __restrict__ s, double* __restrict__ q) {
   const int64_t width = 1 + 2 * (int64_t)d;
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= 2 * (int64_t)k * width) return;
@@ -889,10 +995,12 @@ __global__ __launch_bounds__(256) void k_reduce_stats(
   if (which == 0) {
     if (slot >= counts[0]) return;
     comp = well_idx[slot];
-    const int cw = D64 < 128 ? D64 : 128, nh = D64 / cw, hh = dim / cw;
+    const int cw = D64 % 128 == 0 ? 128 : 64, nh = D64 / cw, hh = dim / cw;
     const double* p = part_w + ((size_t)((slot / kBK) * nh + hh) * nch * 4 * kBK + (slot % kBK)) * stride + off;
     for (int ch = 0; ch < nch; ++ch)
       for (int w = 0; w < 4; ++w) acc += p[((size_t)ch * 4 + w) * kBK * stride];
+    const double* ps = part_s + ((size_t)(slot / kBK) * nch_s * kBK + (slot % kBK)) * stride + off;
+    for (int ch = 0; ch < nch_s; ++ch) acc += ps[(size_t)ch * kBK * stride];
   } else {
     if (slot >= counts[1]) return;
     comp = ill_idx[slot];
@@ -958,10 +1066,11 @@ inline size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 struct Layout {
   int64_t n;
   int d, k, kpad, D64, m;
-  int nch, nh, grid_i;
+  int nch, nh, grid_i, nch_s;
+  int64_t chunk_s;
   int64_t chunk, n_wg_logz;
   size_t off_counts, off_cls, off_cwell, off_cdir, off_well_idx, off_ill_idx, off_cw, off_wp,
-      off_dmu, off_dh, off_dc, off_logz2, off_cslot, off_cr, off_llpart, off_part_w, off_part_i,
+      off_dmu, off_dh, off_dc, off_logz2, off_cslot, off_cr, off_llpart, off_part_w, off_part_s, off_part_i,
       off_fit_nk, off_fit_s, off_fit_q, total;
 };
 
@@ -980,7 +1089,15 @@ bool make_layout(int64_t n, int d, int k, int m, Layout* L) {
   if (c >= 8) c = c / 8 * 8;
   L->nch = (int)(c < 1 ? 1 : c);
   L->chunk = cdiv(n, L->nch);
-  L->nh = L->D64 <= 128 ? 1 : L->D64 / 128;
+  L->nh = L->D64 / (L->D64 % 128 == 0 ? 128 : 64);
+  {
+    int maxs = 2048 / nkb;
+    if (maxs < 8) maxs = 8;
+    int64_t cs = cdiv(n, 4096);
+    if (cs > maxs) cs = maxs;
+    L->nch_s = (int)(cs < 1 ? 1 : cs);
+    L->chunk_s = cdiv(n, L->nch_s);
+  }
   L->grid_i = nkb > 512 ? nkb : 512;
   L->n_wg_logz = cdiv(n, 64);
   size_t o = 0;
@@ -1001,6 +1118,7 @@ bool make_layout(int64_t n, int d, int k, int m, Layout* L) {
   L->off_cr = take((size_t)n * kT * sizeof(float));
   L->off_llpart = take((size_t)L->n_wg_logz * sizeof(double));
   L->off_part_w = take((size_t)nkb * L->nh * L->nch * 4 * kBK * (1 + 2 * (size_t)L->D64) * sizeof(double));
+  L->off_part_s = take((size_t)nkb * L->nch_s * kBK * (1 + 2 * (size_t)L->D64) * sizeof(double));
   L->off_part_i = take((size_t)L->grid_i * kBK * (1 + 2 * (size_t)L->D64) * sizeof(double));
   L->off_fit_nk = take((size_t)k * sizeof(double) + sizeof(double));  // + loglik slot
   L->off_fit_s = take((size_t)k * d * sizeof(double));
@@ -1039,6 +1157,7 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
   float* logz2 = at<float>(ws, L.off_logz2);
   double* llpart = at<double>(ws, L.off_llpart);
   double* part_w = at<double>(ws, L.off_part_w);
+  double* part_s = at<double>(ws, L.off_part_s);
   double* part_i = at<double>(ws, L.off_part_i);
   const int vec4 = ((d & 3) == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0) ? 1 : 0;
 
@@ -1055,14 +1174,16 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
   hipLaunchKernelGGL(k_logz<D64>, dim3((unsigned)L.n_wg_logz), dim3(256), 0, st, x, n, d, vec4,
                      wp, cw, well_idx, ill_idx, dmu, dh, dc, counts, logz2, cslot, cr, llpart);
   hipLaunchKernelGGL(k_stats_well<D64>, dim3((unsigned)((kpad / kBK) * L.nh * L.nch)), dim3(256),
-                     0, st, x, n, d, vec4, wp, cw, counts, logz2, cslot, cr, L.nch, L.chunk,
-                     part_w);
+                     0, st, x, n, d, vec4, wp, cw, counts, logz2, cslot, L.nch, L.chunk, part_w);
+  hipLaunchKernelGGL(k_stats_sparse<D64>, dim3((unsigned)((kpad / kBK) * L.nch_s)), dim3(256), 0,
+                     st, x, n, d, counts, cslot, cr, L.nch_s, L.chunk_s, part_s);
   hipLaunchKernelGGL(k_stats_ill<D64>, dim3((unsigned)L.grid_i), dim3(256), 0, st, x, n, d, vec4,
                      ill_idx, dmu, dh, dc, counts, logz2, part_i);
   {
     const int64_t tot = 2 * (int64_t)k * (1 + 2 * (int64_t)d);
     hipLaunchKernelGGL(k_reduce_stats, dim3((unsigned)cdiv(tot, 256)), dim3(256), 0, st, part_w,
-                       part_i, counts, well_idx, ill_idx, L.nch, L.grid_i, n, k, d, D64, nk, s, q);
+                       part_s, part_i, counts, well_idx, ill_idx, L.nch, L.nch_s, L.grid_i, n, k, d,
+                       D64, nk, s, q);
   }
   hipLaunchKernelGGL(k_reduce_ll, dim3(1), dim3(1024), 0, st, llpart, L.n_wg_logz, loglik,
                      ll_accumulate);

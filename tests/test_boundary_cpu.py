@@ -48,7 +48,8 @@ def test_workspace_is_o_n_plus_o_kd(n, d, k):
     kpad = (k + 31) // 32 * 32
     well_part = 8 * (1 + 2 * d64) * 4 * max(8 * kpad, 512 * 32) * max(1, d64 // 128)
     ill_part = 8 * (1 + 2 * d64) * 32 * max(512, kpad // 32)
-    okd = well_part + ill_part + 40 * kpad * d64 + 8 * 2 * k * d
+    sparse_part = 8 * (1 + 2 * d64) * max(8 * kpad, 2048 * 32)
+    okd = well_part + sparse_part + ill_part + 40 * kpad * d64 + 8 * 2 * k * d
     assert nb <= 36 * n + n // 8 + okd + 64 * k + (1 << 16)
     if n >= 10 ** 7:
         assert nb < n * k * 4 / 25
