@@ -53,7 +53,16 @@ constexpr double kLog2Pi = 1.8378770664093454835606594728112;  // log(2 pi)
 constexpr double kIllSum = 2.0e5;
 constexpr int kT = 4;                   // exact responsibilities stored per point
 constexpr int kFlush = 64;              // k_stats_well: fp32 -> fp64 every 64 iterations
-constexpr float kWindow = 40.0f;        // refine components with r > 2^-40
+// Refinement rule of k_logz.  A screened term r (relative to the screening
+// normaliser) is recomputed exactly when r > 2^-window, with window = 40 for
+// components whose fp32 expanded-form error bound (about 4 u log2(e) (e + d),
+// e = sum mu^2 / var) exceeds 2^-12 log2 units, and window = 10 for the others,
+// whose screened terms are already good to that bound.  Tight components need
+// the wide window: far points with small r still carry a measurable share of
+// their variance.
+constexpr double kWideWindow = 40.0;
+constexpr double kNarrowWindow = 10.0;
+constexpr double kLooseBound = -12.0;
 
 typedef float f16v __attribute__((ext_vector_type(16)));
 
@@ -83,6 +92,38 @@ __device__ __forceinline__ void lse_merge(float& m, float& s, float m2, float s2
   m = mm;
 }
 
+// Lane-state update of k_logz: the state starts at m = kEmpty (finite, below any
+// log-density), s = 0, a = -1, so l = -inf (a dead or padded component) adds
+// exactly 0 and no NaN can arise.  a tracks the arg-max slot.
+constexpr float kEmpty = -3.0e38f;
+__device__ __forceinline__ void lse_add_arg(float& m, float& s, int& a, float l, int slot) {
+  const float dl = l - m;
+  const float e = exp2_fast(-fabsf(dl));
+  const bool gt = dl > 0.0f;
+  s = gt ? __fmaf_rn(s, e, 1.0f) : s + e;
+  m = gt ? l : m;
+  a = gt ? slot : a;
+}
+
+// Inserts (l, slot) into the descending list tl/tsl of length kT; an entry
+// equal to an existing one goes after it.  Static indexing only.
+__device__ __forceinline__ void topk_insert(float* tl, int* tsl, float l, int slot) {
+#pragma unroll
+  for (int j = kT - 1; j > 0; --j) {
+    if (l > tl[j - 1]) {
+      tl[j] = tl[j - 1];
+      tsl[j] = tsl[j - 1];
+    } else if (l > tl[j]) {
+      tl[j] = l;
+      tsl[j] = slot;
+    }
+  }
+  if (l > tl[0]) {
+    tl[0] = l;
+    tsl[0] = slot;
+  }
+}
+
 // ---------------------------------------------------------------- tiles
 // rows x D64 fp32 tile of x (rows [r0, r0+rows)) into LDS with row pitch D64+4;
 // rows >= nend and columns >= d are zero.
@@ -109,91 +150,12 @@ __device__ __forceinline__ void load_tile(const float* __restrict__ x, int64_t n
 }
 
 // ---------------------------------------------------------------- expanded-form logits (MFMA)
-// Contraction order (identical wherever log-densities are formed, so the two
-// passes agree bit for bit): chain 0 runs over the x part, chain 1 over the
-// x^2 part; step s of a chain feeds lane half h the dimension
-// 8*(s/4) + 4*h + s%4; l = (chain0 + chain1) + c.
-// Output layout (32x32 accumulator): register v of lane l holds point
-// row0 + 8*(v/4) + 4*(l/32) + v%4 and component slot l%32 of the block.
-
-template <int D64>
-__device__ __forceinline__ void logits_block(const float* xs, int row0,
-                                             const float4* __restrict__ wp, float cbias,
-                                             f16v& out) {
-  constexpr int P = D64 + 4, QH = D64 / 8;
-  const int lane = threadIdx.x & 63, h = lane >> 5, col = lane & 31;
-  const float* xr = xs + (row0 + col) * P + 4 * h;
-  f16v a0 = {}, a1 = {};
-  // parameter operands are loaded two steps ahead of their use
-  float4 n0 = wp[lane], n1 = wp[QH * 64 + lane];
-  float4 m0 = wp[64 + lane], m1 = wp[(QH + 1) * 64 + lane];
-#pragma unroll 2
-  for (int q = 0; q < QH; ++q) {
-    const float4 b0 = n0, b1 = n1;
-    n0 = m0; n1 = m1;
-    if (q + 2 < QH) {
-      m0 = wp[(q + 2) * 64 + lane];
-      m1 = wp[(QH + q + 2) * 64 + lane];
-    }
-    const float4 a = *reinterpret_cast<const float4*>(xr + 8 * q);
-    a0 = mfma32(a.x, b0.x, a0);
-    a1 = mfma32(a.x * a.x, b1.x, a1);
-    a0 = mfma32(a.y, b0.y, a0);
-    a1 = mfma32(a.y * a.y, b1.y, a1);
-    a0 = mfma32(a.z, b0.z, a0);
-    a1 = mfma32(a.z * a.z, b1.z, a1);
-    a0 = mfma32(a.w, b0.w, a0);
-    a1 = mfma32(a.w * a.w, b1.w, a1);
-  }
-#pragma unroll
-  for (int v = 0; v < 16; ++v) out[v] = (a0[v] + a1[v]) + cbias;
-}
-
-// Two 32-point blocks (rows 0..31 and 32..63) against one component block,
-// sharing the parameter operand; each block's chains are those of logits_block.
-template <int D64>
-__device__ __forceinline__ void logits_2blocks(const float* xs, const float4* __restrict__ wp,
-                                               float cbias, f16v& o0, f16v& o1) {
-  constexpr int P = D64 + 4, QH = D64 / 8;
-  const int lane = threadIdx.x & 63, h = lane >> 5, col = lane & 31;
-  const float* xr0 = xs + col * P + 4 * h;
-  const float* xr1 = xs + (32 + col) * P + 4 * h;
-  f16v a0 = {}, a1 = {}, c0 = {}, c1 = {};
-  float4 n0 = wp[lane], n1 = wp[QH * 64 + lane];
-  float4 m0 = wp[64 + lane], m1 = wp[(QH + 1) * 64 + lane];
-#pragma unroll 2
-  for (int q = 0; q < QH; ++q) {
-    const float4 b0 = n0, b1 = n1;
-    n0 = m0; n1 = m1;
-    if (q + 2 < QH) {
-      m0 = wp[(q + 2) * 64 + lane];
-      m1 = wp[(QH + q + 2) * 64 + lane];
-    }
-    const float4 a = *reinterpret_cast<const float4*>(xr0 + 8 * q);
-    const float4 c = *reinterpret_cast<const float4*>(xr1 + 8 * q);
-    a0 = mfma32(a.x, b0.x, a0);
-    c0 = mfma32(c.x, b0.x, c0);
-    a1 = mfma32(a.x * a.x, b1.x, a1);
-    c1 = mfma32(c.x * c.x, b1.x, c1);
-    a0 = mfma32(a.y, b0.y, a0);
-    c0 = mfma32(c.y, b0.y, c0);
-    a1 = mfma32(a.y * a.y, b1.y, a1);
-    c1 = mfma32(c.y * c.y, b1.y, c1);
-    a0 = mfma32(a.z, b0.z, a0);
-    c0 = mfma32(c.z, b0.z, c0);
-    a1 = mfma32(a.z * a.z, b1.z, a1);
-    c1 = mfma32(c.z * c.z, b1.z, c1);
-    a0 = mfma32(a.w, b0.w, a0);
-    c0 = mfma32(c.w, b0.w, c0);
-    a1 = mfma32(a.w * a.w, b1.w, a1);
-    c1 = mfma32(c.w * c.w, b1.w, c1);
-  }
-#pragma unroll
-  for (int v = 0; v < 16; ++v) {
-    o0[v] = (a0[v] + a1[v]) + cbias;
-    o1[v] = (c0[v] + c1[v]) + cbias;
-  }
-}
+// Step s of a contraction over the x (or x^2) part feeds lane half h the
+// dimension 8*(s/4) + 4*h + s%4.  Accumulator layout (32x32): register v of
+// lane l holds point row0 + 8*(v/4) + 4*(l/32) + v%4 and component slot l%32
+// of the block.  k_logz and k_stats_well form the same log-densities with
+// different summation orders; they agree to fp32 rounding, far inside the
+// screening error that both passes tolerate.
 
 // ---------------------------------------------------------------- direct-form logits (VALU)
 // l2 = c - sum_d (x_d - mu_d)^2 * hh_d, hh = log2(e) / (2 var), summed in
@@ -225,7 +187,8 @@ __global__ __launch_bounds__(64) void k_prep_class(const float* __restrict__ w,
                                                    const float* __restrict__ var, int d,
                                                    int* __restrict__ cls,
                                                    double* __restrict__ cwell,
-                                                   double* __restrict__ cdir) {
+                                                   double* __restrict__ cdir,
+                                                   float* __restrict__ cthr) {
   const int comp = blockIdx.x, lane = threadIdx.x;
   double e = 0.0, lg = 0.0;
   for (int j = lane; j < d; j += 64) {
@@ -247,6 +210,10 @@ __global__ __launch_bounds__(64) void k_prep_class(const float* __restrict__ w,
     const double lw = wk > 0.0 ? log(wk) : -INFINITY;
     cwell[comp] = kLog2e * (lw - 0.5 * (e + lg));
     cdir[comp] = kLog2e * (lw - 0.5 * lg);
+    // screening error bound: about u * sum of |terms|, the terms of size
+    // log2(e) * (mu^2 + x^2) / var for x near mu; taken as 4 u log2(e) (e + d)
+    const double ldelta = -22.0 + log2(kLog2e * (e + d));
+    cthr[comp] = (float)(ldelta > kLooseBound ? -kWideWindow : -kNarrowWindow);
   }
 }
 
@@ -287,8 +254,9 @@ __global__ __launch_bounds__(256) void k_prep_scan(const int* __restrict__ cls, 
 template <int D64>
 __global__ __launch_bounds__(256) void k_prep_pack_well(
     const float* __restrict__ mu, const float* __restrict__ var, int d, int kpad,
-    const double* __restrict__ cwell, const int* __restrict__ counts,
-    const int* __restrict__ well_idx, float4* __restrict__ wp, float* __restrict__ cw) {
+    const double* __restrict__ cwell, const float* __restrict__ cthr,
+    const int* __restrict__ counts, const int* __restrict__ well_idx, float4* __restrict__ wp,
+    float* __restrict__ cw, float* __restrict__ thr) {
   constexpr int QQ = D64 / 4, QH = D64 / 8;
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= (int64_t)kpad * QQ * 2) return;   // kpad/32 blocks * QQ * 64 lanes
@@ -311,7 +279,10 @@ __global__ __launch_bounds__(256) void k_prep_pack_well(
     vals[i] = v;
   }
   wp[t] = make_float4(vals[0], vals[1], vals[2], vals[3]);
-  if (q == 0 && h == 0) cw[slot] = comp >= 0 ? (float)cwell[comp] : -INFINITY;
+  if (q == 0 && h == 0) {
+    cw[slot] = comp >= 0 ? (float)cwell[comp] : -INFINITY;
+    thr[slot] = comp >= 0 ? cthr[comp] : 0.0f;
+  }
 }
 
 // Direct-form parameters of every component (indexed by component):
@@ -336,6 +307,70 @@ __global__ __launch_bounds__(256) void k_prep_pack_direct(
 }
 
 // ---------------------------------------------------------------- Step 1: log-normalisers
+// One software-pipelined step of k_logz for one wave: when MF, the log-densities
+// of 64 points (two 32-point tiles) against component block wpb are formed on
+// MFMA into n0, n1, one chain per tile: bias first, then for every group of 8
+// dimensions the four x steps and the four x^2 steps.  When EPI, the lane
+// states take in the previous block's log-densities c0, c1 (slot = its
+// component slot of this lane), spread over the contraction so that the vector
+// ALU work overlaps the matrix work.
+template <int D64, bool MF, bool EPI>
+__device__ __forceinline__ void logz_step(const float* xs, const float4* __restrict__ wpb,
+                                          float cb, f16v& n0, f16v& n1, const f16v& c0,
+                                          const f16v& c1, int slot, float* m0, float* s0,
+                                          int* a0, float* m1, float* s1, int* a1) {
+  constexpr int P = D64 + 4, QH = D64 / 8;
+  const int lane = threadIdx.x & 63, h = lane >> 5, col = lane & 31;
+  const float* xr0 = xs + col * P + 4 * h;
+  const float* xr1 = xs + (32 + col) * P + 4 * h;
+  float4 bw[3], bp[3];
+  if (MF) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) { n0[v] = cb; n1[v] = cb; }
+    bw[0] = wpb[lane];
+    bp[0] = wpb[QH * 64 + lane];
+    bw[1] = wpb[64 + lane];
+    bp[1] = wpb[(QH + 1) * 64 + lane];
+  }
+#pragma unroll
+  for (int q = 0; q < QH; ++q) {
+    if (MF) {
+      if (q + 2 < QH) {
+        bw[(q + 2) % 3] = wpb[(q + 2) * 64 + lane];
+        bp[(q + 2) % 3] = wpb[(QH + q + 2) * 64 + lane];
+      }
+      const float4 a = *reinterpret_cast<const float4*>(xr0 + 8 * q);
+      const float4 c = *reinterpret_cast<const float4*>(xr1 + 8 * q);
+      const float4 w = bw[q % 3], pp = bp[q % 3];
+      n0 = mfma32(a.x, w.x, n0);
+      n1 = mfma32(c.x, w.x, n1);
+      n0 = mfma32(a.y, w.y, n0);
+      n1 = mfma32(c.y, w.y, n1);
+      n0 = mfma32(a.z, w.z, n0);
+      n1 = mfma32(c.z, w.z, n1);
+      n0 = mfma32(a.w, w.w, n0);
+      n1 = mfma32(c.w, w.w, n1);
+      n0 = mfma32(a.x * a.x, pp.x, n0);
+      n1 = mfma32(c.x * c.x, pp.x, n1);
+      n0 = mfma32(a.y * a.y, pp.y, n0);
+      n1 = mfma32(c.y * c.y, pp.y, n1);
+      n0 = mfma32(a.z * a.z, pp.z, n0);
+      n1 = mfma32(c.z * c.z, pp.z, n1);
+      n0 = mfma32(a.w * a.w, pp.w, n0);
+      n1 = mfma32(c.w * c.w, pp.w, n1);
+    }
+    if (EPI) {
+#pragma unroll
+      for (int v = q * 16 / QH; v < (q + 1) * 16 / QH; ++v) {
+        lse_add_arg(m0[v], s0[v], a0[v], c0[v], slot);
+        lse_add_arg(m1[v], s1[v], a1[v], c1[v], slot);
+      }
+    }
+    // keep each step's loads in their step (unbounded hoisting exhausts registers)
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
 // One workgroup = 64 points, 4 waves; wave w takes well component blocks w,
 // w+4, ... and ill-conditioned components w, w+4, ...
 //
@@ -344,22 +379,25 @@ __global__ __launch_bounds__(256) void k_prep_pack_direct(
 //      point) covers every 32nd component of the wave's blocks.
 //   2. the lane states are merged (within the wave by butterflies, then across
 //      waves in a fixed order) into a screening log2 Z per point.
-//   3. refinement: every lane state whose maximum lies within kWindow of that
-//      log2 Z marks its arg-max component as a candidate; the candidates'
-//      log-densities are recomputed in the direct form (fp32 error relative to
-//      the result), their screened terms are taken out of the sum and the exact
-//      ones put in.  The result is the log2 Z written for the point, and the
-//      kT largest exact responsibilities are stored for the statistics pass.
+//   3. refinement: a lane state whose maximum, relative to that log2 Z, passes
+//      its arg-max component's threshold (kWideWindow / kNarrowWindow) marks that
+//      component as a candidate; the candidates' log-densities are recomputed
+//      in the direct form (fp32 error relative to the result), thread (wave w,
+//      point p) taking the candidates of wave w's lane states; their screened
+//      terms are taken out of the sum and the exact ones put in, merged over
+//      waves in a fixed order.  The result is the log2 Z written for the point,
+//      and the kT largest exact responsibilities are stored for the statistics
+//      pass.
 // A significant component is missed only if a larger one of the same point
 // shares its lane state; its responsibility then keeps the screening error.
 template <int D64>
-__global__ __launch_bounds__(256) void k_logz(
+__global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_logz(
     const float* __restrict__ x, int64_t n, int d, int vec4, const float4* __restrict__ wp,
-    const float* __restrict__ cw, const int* __restrict__ well_idx,
-    const int* __restrict__ ill_idx, const float* __restrict__ dmu,
-    const float* __restrict__ dh, const float* __restrict__ dc, const int* __restrict__ counts,
-    float* __restrict__ logz2, int* __restrict__ cslot, float* __restrict__ cr,
-    double* __restrict__ ll_part) {
+    const float* __restrict__ cw, const float* __restrict__ thr,
+    const int* __restrict__ well_idx, const int* __restrict__ ill_idx,
+    const float* __restrict__ dmu, const float* __restrict__ dh, const float* __restrict__ dc,
+    const int* __restrict__ counts, float* __restrict__ logz2, int* __restrict__ cslot,
+    float* __restrict__ cr, double* __restrict__ ll_part) {
   constexpr int P = D64 + 4;
   __shared__ __align__(16) float xs[64 * P];
   __shared__ float2 stw[4][64];      // per wave: merged well state (M_w, S_w) per point
@@ -367,7 +405,10 @@ __global__ __launch_bounds__(256) void k_logz(
   __shared__ float cms[4][64];       // per wave: candidate mass relative to M_w
   __shared__ float lzm[64];          // screening log2 Z
   __shared__ unsigned cmask[64][4];  // candidate lane columns per (point, wave)
-  __shared__ int cidx[64][128];      // arg-max well slot per (point, lane state)
+  __shared__ unsigned short cidx[64][128];  // arg-max well slot per (point, lane state)
+  __shared__ float2 rmc[4][64];      // per (wave, point): exact candidate LSE state
+  __shared__ int rts[4][kT][64];     // per (wave, point): largest exact candidates
+  __shared__ float rtl[4][kT][64];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, h = lane >> 5, col = lane & 31;
   const int64_t n0 = (int64_t)blockIdx.x * 64;
   load_tile<D64>(x, n, d, n0, 64, xs, vec4 != 0);
@@ -378,28 +419,39 @@ __global__ __launch_bounds__(256) void k_logz(
   int a0[16], a1[16];
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
-    m0[v] = m1[v] = -INFINITY;
+    m0[v] = m1[v] = kEmpty;
     s0[v] = s1[v] = 0.0f;
     a0[v] = a1[v] = -1;
   }
-  for (int kb = wave; kb < n_wkb; kb += 4) {
-    f16v l0, l1;
-    logits_2blocks<D64>(xs, wp + (size_t)kb * (D64 / 4) * 64, cw[kb * kBK + col], l0, l1);
-    const int slot = kb * kBK + col;
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      a0[v] = l0[v] > m0[v] ? slot : a0[v];
-      lse_add(m0[v], s0[v], l0[v]);
-      a1[v] = l1[v] > m1[v] ? slot : a1[v];
-      lse_add(m1[v], s1[v], l1[v]);
+  {
+    // wave w takes blocks w, w+4, ...: the MFMAs of block i+1 run while the
+    // lane states take in block i
+    const int nb = n_wkb > wave ? (n_wkb - wave + 3) / 4 : 0;
+    constexpr size_t BS = (size_t)(D64 / 4) * 64;
+    f16v c0, c1, x0, x1;
+    if (nb > 0) {
+      logz_step<D64, true, false>(xs, wp + (size_t)wave * BS, cw[wave * kBK + col], c0, c1, x0,
+                                  x1, 0, m0, s0, a0, m1, s1, a1);
+      float cbn = nb > 1 ? cw[(wave + 4) * kBK + col] : 0.0f;
+      for (int i = 0; i + 1 < nb; ++i) {
+        const int kb = wave + 4 * i;
+        const float cb = cbn;
+        if (i + 2 < nb) cbn = cw[(kb + 8) * kBK + col];
+        logz_step<D64, true, true>(xs, wp + (size_t)(kb + 4) * BS, cb, x0, x1, c0, c1,
+                                   kb * kBK + col, m0, s0, a0, m1, s1, a1);
+        c0 = x0;
+        c1 = x1;
+      }
+      logz_step<D64, false, true>(xs, wp, 0.0f, x0, x1, c0, c1,
+                                  (wave + 4 * (nb - 1)) * kBK + col, m0, s0, a0, m1, s1, a1);
     }
   }
   // arg-max of every lane state, and the per-wave merged state of every point
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
     const int p = 8 * (v >> 2) + 4 * h + (v & 3);
-    cidx[p][wave * 32 + col] = a0[v];
-    cidx[32 + p][wave * 32 + col] = a1[v];
+    cidx[p][wave * 32 + col] = (unsigned short)a0[v];
+    cidx[32 + p][wave * 32 + col] = (unsigned short)a1[v];
     float M0 = m0[v], S0 = s0[v], M1 = m1[v], S1 = s1[v];
     for (int off = 16; off > 0; off >>= 1) {
       lse_merge(M0, S0, __shfl_xor(M0, off), __shfl_xor(S0, off));
@@ -437,7 +489,8 @@ __global__ __launch_bounds__(256) void k_logz(
     for (int blk = 0; blk < 2; ++blk) {
       const int pp = blk * 32 + p;
       const float mv = blk ? m1[v] : m0[v];
-      const bool cand = mv > lzm[pp] - kWindow;
+      const int av = blk ? a1[v] : a0[v];
+      const bool cand = av >= 0 && mv - lzm[pp] > thr[av];
       float term = cand ? exp2_fast(mv - stw[wave][pp].x) : 0.0f;
       for (int off = 16; off > 0; off >>= 1) term += __shfl_xor(term, off);
       const unsigned long long bal = __ballot(cand);
@@ -445,6 +498,33 @@ __global__ __launch_bounds__(256) void k_logz(
         cms[wave][pp] = term;
         cmask[pp][wave] = (unsigned)(bal >> (32 * h));
       }
+    }
+  }
+  __syncthreads();
+  {
+    // exact log-densities of wave w's candidates of point p, in lane column order
+    const int p = lane, w2 = wave;
+    float mc = -INFINITY, sc = 0.0f;
+    int tsl[kT];
+    float tl[kT];
+#pragma unroll
+    for (int j = 0; j < kT; ++j) { tsl[j] = -1; tl[j] = -INFINITY; }
+    unsigned msk = cmask[p][w2];
+    while (msk) {
+      const int b = __ffs(msk) - 1;
+      msk &= msk - 1;
+      const int slot = cidx[p][w2 * 32 + b];
+      const int comp = well_idx[slot];
+      const float l = ill_logit<D64>(xs + p * P, dmu + (size_t)comp * D64,
+                                     dh + (size_t)comp * D64, dc[comp]);
+      lse_add(mc, sc, l);
+      topk_insert(tl, tsl, l, slot);
+    }
+    rmc[w2][p] = make_float2(mc, sc);
+#pragma unroll
+    for (int j = 0; j < kT; ++j) {
+      rts[w2][j][p] = tsl[j];
+      rtl[w2][j][p] = tl[j];
     }
   }
   __syncthreads();
@@ -461,29 +541,19 @@ __global__ __launch_bounds__(256) void k_logz(
         if (b.x > -INFINITY) snc += b.y * exp2_fast(b.x - mm);
       }
     }
-    // exact log-densities of the candidates, in (wave, lane column) order
+    // merge the per-wave exact candidates in wave order
     float mc = -INFINITY, sc = 0.0f;
     int tsl[kT];
     float tl[kT];
 #pragma unroll
     for (int j = 0; j < kT; ++j) { tsl[j] = -1; tl[j] = -INFINITY; }
     for (int w2 = 0; w2 < 4; ++w2) {
-      unsigned msk = cmask[p][w2];
-      while (msk) {
-        const int b = __ffs(msk) - 1;
-        msk &= msk - 1;
-        const int slot = cidx[p][w2 * 32 + b];
-        const int comp = well_idx[slot];
-        const float l = ill_logit<D64>(xs + p * P, dmu + (size_t)comp * D64,
-                                       dh + (size_t)comp * D64, dc[comp]);
-        lse_add(mc, sc, l);
-        // keep the kT largest (ties: the earlier one stays ahead)
-        if (l > tl[kT - 1]) {
-          int j = kT - 1;
-          while (j > 0 && l > tl[j - 1]) { tl[j] = tl[j - 1]; tsl[j] = tsl[j - 1]; --j; }
-          tl[j] = l;
-          tsl[j] = slot;
-        }
+      const float2 st2 = rmc[w2][p];
+      lse_merge(mc, sc, st2.x, st2.y);
+      for (int j2 = 0; j2 < kT; ++j2) {
+        const int sl2 = rts[w2][j2][p];
+        const float l = rtl[w2][j2][p];
+        if (sl2 >= 0) topk_insert(tl, tsl, l, sl2);
       }
     }
     float mt = fmaxf(mm, mc), stot = 0.0f;
@@ -1069,7 +1139,8 @@ struct Layout {
   int nch, nh, grid_i, nch_s;
   int64_t chunk_s;
   int64_t chunk, n_wg_logz;
-  size_t off_counts, off_cls, off_cwell, off_cdir, off_well_idx, off_ill_idx, off_cw, off_wp,
+  size_t off_counts, off_cls, off_cwell, off_cdir, off_cthr, off_thr, off_well_idx, off_ill_idx,
+      off_cw, off_wp,
       off_dmu, off_dh, off_dc, off_logz2, off_cslot, off_cr, off_llpart, off_part_w, off_part_s, off_part_i,
       off_fit_nk, off_fit_s, off_fit_q, total;
 };
@@ -1109,6 +1180,8 @@ bool make_layout(int64_t n, int d, int k, int m, Layout* L) {
   L->off_well_idx = take((size_t)k * sizeof(int));
   L->off_ill_idx = take((size_t)k * sizeof(int));
   L->off_cw = take((size_t)L->kpad * sizeof(float));
+  L->off_cthr = take((size_t)k * sizeof(float));
+  L->off_thr = take((size_t)L->kpad * sizeof(float));
   L->off_wp = take((size_t)L->kpad * 2 * L->D64 * sizeof(float));
   L->off_dmu = take((size_t)k * L->D64 * sizeof(float));
   L->off_dh = take((size_t)k * L->D64 * sizeof(float));
@@ -1148,6 +1221,8 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
   int* well_idx = at<int>(ws, L.off_well_idx);
   int* ill_idx = at<int>(ws, L.off_ill_idx);
   float* cw = at<float>(ws, L.off_cw);
+  float* cthr = at<float>(ws, L.off_cthr);
+  float* thr = at<float>(ws, L.off_thr);
   float4* wp = at<float4>(ws, L.off_wp);
   float* dmu = at<float>(ws, L.off_dmu);
   float* dh = at<float>(ws, L.off_dh);
@@ -1161,18 +1236,20 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
   double* part_i = at<double>(ws, L.off_part_i);
   const int vec4 = ((d & 3) == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0) ? 1 : 0;
 
-  hipLaunchKernelGGL(k_prep_class, dim3(k), dim3(64), 0, st, w, mu, var, d, cls, cwell, cdir);
+  hipLaunchKernelGGL(k_prep_class, dim3(k), dim3(64), 0, st, w, mu, var, d, cls, cwell, cdir,
+                     cthr);
   hipLaunchKernelGGL(k_prep_scan, dim3(1), dim3(256), 0, st, cls, k, well_idx, ill_idx, counts);
   {
     const int64_t tot = (int64_t)kpad * (D64 / 4) * 2;
     hipLaunchKernelGGL(k_prep_pack_well<D64>, dim3((unsigned)cdiv(tot, 256)), dim3(256), 0, st,
-                       mu, var, d, kpad, cwell, counts, well_idx, wp, cw);
+                       mu, var, d, kpad, cwell, cthr, counts, well_idx, wp, cw, thr);
     const int64_t toti = (int64_t)k * D64;
     hipLaunchKernelGGL(k_prep_pack_direct<D64>, dim3((unsigned)cdiv(toti, 256)), dim3(256), 0,
                        st, mu, var, d, k, cdir, dmu, dh, dc);
   }
   hipLaunchKernelGGL(k_logz<D64>, dim3((unsigned)L.n_wg_logz), dim3(256), 0, st, x, n, d, vec4,
-                     wp, cw, well_idx, ill_idx, dmu, dh, dc, counts, logz2, cslot, cr, llpart);
+                     wp, cw, thr, well_idx, ill_idx, dmu, dh, dc, counts, logz2, cslot, cr,
+                     llpart);
   hipLaunchKernelGGL(k_stats_well<D64>, dim3((unsigned)((kpad / kBK) * L.nh * L.nch)), dim3(256),
                      0, st, x, n, d, vec4, wp, cw, counts, logz2, cslot, L.nch, L.chunk, part_w);
   hipLaunchKernelGGL(k_stats_sparse<D64>, dim3((unsigned)((kpad / kBK) * L.nch_s)), dim3(256), 0,
