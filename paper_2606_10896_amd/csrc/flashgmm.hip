@@ -827,21 +827,22 @@ __global__ __launch_bounds__(256, 2) void k_stats_well(
 }
 
 // Refined pairs of a well block, in fp64.  Grid: (block, sparse chunk).  The
-// chunk's refined lists are scanned 1024 points at a time (the next group's
+// chunk's refined lists are scanned G*256 points at a time (the next group's
 // lists are loaded while the current one is processed); the pairs that fall in
-// this block are compacted in (point, rank) order and their rows gathered into
-// LDS in batches.  Wave w owns components 8w .. 8w+7 of the block; lane l owns
-// columns l, l + 64, ... of [1 | x | x^2] and adds r, r * x, r * x^2 (exact
-// products of fp32 values) in that order, in registers.
+// this block are compacted in (point, rank) order.  Their rows are gathered in
+// batches of NB through registers into a double-buffered LDS tile, the next
+// batch's loads in flight while the current one is consumed.  Wave w owns
+// components 8w .. 8w+7 of the block and picks its pairs out of a batch with a
+// ballot; lane l owns columns l, l + 64, ... of [1 | x | x^2] and adds r,
+// r * x, r * x^2 (exact products of fp32 values) in pair order, in registers.
 template <int D64>
 __global__ __launch_bounds__(256) void k_stats_sparse(
     const float* __restrict__ x, int64_t n, int d, const int* __restrict__ counts,
     const int* __restrict__ cslot, const float* __restrict__ cr, int nch, int64_t chunk_pts,
     double* __restrict__ part) {
-  constexpr int STRIDE = 1 + 2 * D64, NCI = (STRIDE + 63) / 64, NB = D64 <= 128 ? 64 : 32;
-  constexpr int P = D64 + 1;
-  constexpr int G = 4;                          // 256-point groups per scan step
-  __shared__ float xb[NB * P];
+  constexpr int STRIDE = 1 + 2 * D64, NCI = (STRIDE + 63) / 64, NB = 32, G = 2;
+  constexpr int GL = NB * D64 / 256;            // gathered values per thread and batch
+  __shared__ float xb[2][NB * D64];
   __shared__ int2 stage[G * 256 * kT];
   __shared__ int wcnt[4];
   const int kb = blockIdx.x / nch, chunk = blockIdx.x % nch;
@@ -870,7 +871,20 @@ __global__ __launch_bounds__(256) void k_stats_sparse(
     }
   };
   auto in_block = [&](int v) { return v >= 0 && (v >> 5) == kb; };
+  float gv[GL];
+  // rows of the staged pairs b0 .. b0+nb-1 into registers (column c of pair e
+  // is value i = e * D64 + c, thread tid takes i = tid + 256 j)
+  auto gather = [&](int64_t base, int b0, int nb) {
+#pragma unroll
+    for (int j = 0; j < GL; ++j) {
+      const int i = tid + 256 * j, e = i / D64, c = i % D64;
+      float v = 0.0f;
+      if (e < nb && c < d) v = x[(base + (stage[b0 + e].x >> 5)) * d + c];
+      gv[j] = v;
+    }
+  };
   if (p0 < p1) load_lists(p0);
+  int buf = 0;
   for (int64_t base = p0; base < p1; base += G * 256) {
     int mine[G];
 #pragma unroll
@@ -887,7 +901,7 @@ __global__ __launch_bounds__(256) void k_stats_sparse(
         const int v = __shfl_up(inc, off);
         if (lane >= off) inc += v;
       }
-      __syncthreads();                          // wcnt free / previous batch consumed
+      __syncthreads();                          // wcnt free / previous stage consumed
       if (lane == 63) wcnt[wave] = inc;
       __syncthreads();
       int before = 0, all = 0;
@@ -911,21 +925,28 @@ __global__ __launch_bounds__(256) void k_stats_sparse(
       }
     }
     if (base + G * 256 < p1) load_lists(base + G * 256);
+    if (total == 0) continue;
+    __syncthreads();                            // stage complete
+    gather(base, 0, total < NB ? total : NB);
     for (int b0 = 0; b0 < total; b0 += NB) {
       const int nb = total - b0 < NB ? total - b0 : NB;
-      __syncthreads();                          // stage written / previous rows consumed
-      for (int i = tid; i < nb * D64; i += 256) {
-        const int e = i / D64, c = i % D64;
-        const int64_t row = base + (stage[b0 + e].x >> 5);
-        xb[e * P + c] = c < d ? x[row * d + c] : 0.0f;
-      }
-      __syncthreads();
-      for (int e = 0; e < nb; ++e) {
-        const int2 en = stage[b0 + e];
-        const int cl = (en.x & 31) - 8 * wave;
-        if (cl < 0 || cl >= 8) continue;
-        const double r = (double)__int_as_float(en.y);
-        const float* xr = xb + e * P;
+#pragma unroll
+      for (int j = 0; j < GL; ++j) xb[buf][tid + 256 * j] = gv[j];
+      __syncthreads();                          // batch b0 in xb[buf]
+      if (b0 + NB < total) gather(base, b0 + NB, total - b0 - NB < NB ? total - b0 - NB : NB);
+      // this wave's pairs of the batch
+      int2 en = make_int2(0, 0);
+      if (lane < nb) en = stage[b0 + lane];
+      const int cl = (en.x & 31) - 8 * wave;
+      unsigned long long own = __ballot(lane < nb && cl >= 0 && cl < 8);
+      while (own) {
+        const int e = __ffsll(own) - 1;
+        own &= own - 1;
+        const int ex = __builtin_amdgcn_readlane(en.x, e);
+        const int ey = __builtin_amdgcn_readlane(en.y, e);
+        const int jc = (ex & 31) - 8 * wave;
+        const double r = (double)__int_as_float(ey);
+        const float* xr = xb[buf] + e * D64;
         double y[NCI];
 #pragma unroll
         for (int i = 0; i < NCI; ++i) {
@@ -938,12 +959,13 @@ __global__ __launch_bounds__(256) void k_stats_sparse(
         }
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          if (cl == j) {
+          if (jc == j) {
 #pragma unroll
             for (int i = 0; i < NCI; ++i) acc[j][i] = fma(r, y[i], acc[j][i]);
           }
         }
       }
+      buf ^= 1;
     }
   }
 #pragma unroll
@@ -1002,6 +1024,9 @@ __global__ __launch_bounds__(256) void k_stats_ill(
     load_tile<D64>(x, p1, d, it, 64, xs, vec4 != 0);
     if (tid < 64) lzs[tid] = (it + tid < p1) ? logz2[it + tid] : INFINITY;
     __syncthreads();
+    // nz[c]: the points of this tile with r > 0 for component c (wave-uniform)
+    unsigned long long nz[8];
+#pragma unroll
     for (int c = 0; c < 8; ++c) {
       const int ki = kb * kBK + wave * 8 + c;
       float r = 0.0f;
@@ -1012,22 +1037,25 @@ __global__ __launch_bounds__(256) void k_stats_ill(
         r = exp2_fast(l - lzs[lane]);
       }
       rs[(wave * 8 + c) * 64 + lane] = r;
+      nz[c] = __ballot(r > 0.0f);
     }
     __syncthreads();
-    const int np = (int)(p1 - it < 64 ? p1 - it : 64);
-    for (int p = 0; p < np; ++p) {
-      double xv[NJ];
+    // pairs with r == 0 add exactly nothing and are skipped; per component the
+    // points are still taken in increasing order
 #pragma unroll
-      for (int j = 0; j < NJ; ++j) xv[j] = (double)xs[p * P + lane + 64 * j];
-#pragma unroll
-      for (int c = 0; c < 8; ++c) {
+    for (int c = 0; c < 8; ++c) {
+      unsigned long long msk = nz[c];
+      while (msk) {
+        const int p = __ffsll(msk) - 1;
+        msk &= msk - 1;
         const double r = (double)rs[(wave * 8 + c) * 64 + p];
         NK[c] += r;
 #pragma unroll
         for (int j = 0; j < NJ; ++j) {
-          const double rx = r * xv[j];
+          const double xv = (double)xs[p * P + lane + 64 * j];
+          const double rx = r * xv;
           S[c][j] += rx;
-          Q[c][j] = fma(rx, xv[j], Q[c][j]);
+          Q[c][j] = fma(rx, xv, Q[c][j]);
         }
       }
     }
