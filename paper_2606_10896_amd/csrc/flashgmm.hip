@@ -44,7 +44,8 @@
 
 namespace {
 
-constexpr int kBK = 32;                 // components per MFMA block
+constexpr int kBK = 32;                 // components per MFMA block (log-normalisers, sparse)
+constexpr int kWB = 64;                 // components per workgroup of k_stats_well
 constexpr double kLog2e = 1.4426950408889634073599246810019;
 constexpr double kLn2 = 0.69314718055994530941723212145818;
 constexpr double kLog2Pi = 1.8378770664093454835606594728112;  // log(2 pi)
@@ -283,6 +284,33 @@ __global__ __launch_bounds__(256) void k_prep_pack_well(
     cw[slot] = comp >= 0 ? (float)cwell[comp] : -INFINITY;
     thr[slot] = comp >= 0 ? cthr[comp] : 0.0f;
   }
+}
+
+// Packed 16x16x4 operand of k_stats_well: wq[(g * D64/2 + s) * 64 + lane] is,
+// for 16-component group g and lane l, component slot 16g + l%16 at step s:
+// W of dimension 16(s/4) + 4(l/16) + s%4 for s < D64/4, P of that dimension
+// (s - D64/4 in place of s) above.  Same fp64 -> fp32 values as wp.
+template <int D64>
+__global__ __launch_bounds__(256) void k_prep_pack_w16(
+    const float* __restrict__ mu, const float* __restrict__ var, int d, int kpad,
+    const int* __restrict__ counts, const int* __restrict__ well_idx, float* __restrict__ wq) {
+  constexpr int NS = D64 / 4;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (int64_t)kpad * 2 * D64) return;     // (kpad/16) groups * 2NS steps * 64 lanes
+  const int lane = (int)(t & 63);
+  const int s = (int)((t >> 6) % (2 * NS));
+  const int g = (int)((t >> 6) / (2 * NS));
+  const int slot = g * 16 + (lane & 15);
+  const int comp = slot < counts[0] ? well_idx[slot] : -1;
+  const bool xpart = s < NS;
+  const int ss = xpart ? s : s - NS;
+  const int j = 16 * (ss / 4) + 4 * (lane >> 4) + ss % 4;
+  float v = 0.0f;
+  if (comp >= 0 && j < d) {
+    const double m = mu[(int64_t)comp * d + j], s2 = var[(int64_t)comp * d + j];
+    v = xpart ? (float)(kLog2e * m / s2) : (float)(-0.5 * kLog2e / s2);
+  }
+  wq[t] = v;
 }
 
 // Direct-form parameters of every component (indexed by component):
@@ -579,251 +607,213 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_logz(
 }
 
 // ---------------------------------------------------------------- Step 2: statistics, well set
-// Grid: (component block kb, column part, point chunk); two workgroups share a
-// CU (about 58 KB of LDS and at most 256 registers per wave), so each SIMD
-// interleaves two waves.  Every 64-point iteration (two 32-point tiles):
-//   the tile prefetched into registers during the previous iteration (X,
-//   log2 Z, the refined lists) is stored to LDS;
-//   wave w compacts the refined pairs of points 16w..16w+15 that fall in this
-//   block (in (point, rank) order) and flags them;
-//   producers: waves 2t and 2t+1 form the x and x^2 chains of the log-density
-//   MFMA of tile t (the contraction order of k_logz), wave 2t adds them and
-//   the bias, takes r = 2^(l - log2 Z) with the refined pairs set to 0, and
-//   writes the r tile to LDS;
-//   consumers: wave w owns a quarter of the statistic columns (x low/high
-//   half, x^2 low/high half of the column part) and contracts r^T [x | x^2]
-//   over both r tiles on MFMA; the fp32 accumulators, which only carry
-//   responsibilities outside the refined set, are folded into fp64 every
-//   kFlush iterations;
-//   sparse: the refined pairs (at most kT per point, the only ones that can
-//   carry a large share of a component) are accumulated in fp64 with exact
-//   products r * x and r * x^2, so q/n - mu^2 loses nothing to cancellation.
-// The next tile's loads are issued after the producers, so their latency
-// overlaps the consumer MFMAs.  Each wave owns a partial region: its
-// statistic columns, the N_k of its producer tile (waves 0 and 2), and the
-// refined sums of components 8w..8w+7; everything else in it is zero.
-template <int D64>
-__device__ __forceinline__ void logits_chain(const float* xs, int row0, bool xsq,
-                                             const float4* __restrict__ wpc, f16v& acc) {
-  constexpr int P = D64 + 4, QH = D64 / 8;
-  const int lane = threadIdx.x & 63, h = lane >> 5, col = lane & 31;
-  const float* xr = xs + (row0 + col) * P + 4 * h;
-  f16v a = {};
-  float4 n0 = wpc[lane], m0 = wpc[64 + lane];
-#pragma unroll 4
-  for (int q = 0; q < QH; ++q) {
-    const float4 b = n0;
-    n0 = m0;
-    if (q + 2 < QH) m0 = wpc[(q + 2) * 64 + lane];
-    float4 v = *reinterpret_cast<const float4*>(xr + 8 * q);
-    if (xsq) { v.x *= v.x; v.y *= v.y; v.z *= v.z; v.w *= v.w; }
-    a = mfma32(v.x, b.x, a);
-    a = mfma32(v.y, b.y, a);
-    a = mfma32(v.z, b.z, a);
-    a = mfma32(v.w, b.w, a);
-  }
-  acc = a;
+// Grid: (64-component block, point chunk), 16x16x4 fp32 MFMA.  Wave w owns the
+// 16 components 16w .. 16w+15 of the block and works on its own: its
+// log-density operand (W and P of its components, 2 * D64 values per lane in
+// the MFMA B-operand order of the packed array wq) stays in registers for the
+// whole chunk; for every 16-point tile it forms the log-densities of its
+// components (one chain: bias, x steps, x^2 steps), takes r = 2^(l - log2 Z)
+// with the refined pairs set to 0 (k_stats_sparse sums those exactly), and
+// contracts r^T [x | x^2] into fp32 accumulators (its 16 components x 2 D64
+// columns) that are folded into the workgroup's fp64 partial every kFlush
+// iterations; N_k is summed on the vector ALU.  The log-density accumulator
+// layout (point 4(l/16)+v, component l%16) is the B-operand layout of the
+// statistic MFMA, so r stays in registers.  The waves share only the X tile:
+// 32 points per iteration, double-buffered in LDS and loaded one iteration
+// ahead, one barrier per iteration.
+//
+// Orders.  Log-density step s (< D64/4) of lane l uses dimension
+// 16(s/4) + 4(l/16) + s%4, so a lane reads 4 dimensions with one float4.
+// Statistic column block c = 4g + e (x part; the x^2 part likewise) row i is
+// dimension 64g + 4i + e, so a lane reads the 4 blocks of a group with one
+// float4 too.
+typedef float f4v __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ f4v mfma16(float a, float b, f4v c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
 template <int D64>
-__global__ __launch_bounds__(256, 2) void k_stats_well(
-    const float* __restrict__ x, int64_t n, int d, int vec4, const float4* __restrict__ wp,
+__global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
+    const float* __restrict__ x, int64_t n, int d, int vec4, const float* __restrict__ wq,
     const float* __restrict__ cw, const int* __restrict__ counts,
     const float* __restrict__ logz2, const int* __restrict__ cslot, int nch,
     int64_t chunk_pts, double* __restrict__ part) {
   constexpr int P = D64 + 4;
-  constexpr int CW = D64 % 128 == 0 ? 128 : 64;  // x dimensions per column part
-  constexpr int NH = D64 / CW;                  // column parts
-  constexpr int NE = CW / 64;                   // 32-column MFMA blocks per consumer wave
+  constexpr int NS = D64 / 4;                   // MFMA steps per chain
+  constexpr int NG = D64 / 64;                  // float4 column groups per part
+  constexpr int NB = D64 / 16;                  // 16-column blocks per part
+  constexpr int PTS = 32;                       // points per iteration (two tiles)
+  constexpr int Q4 = D64 / 4;
+  constexpr int LD = PTS * Q4 / 256;            // float4 per thread per X tile
   constexpr int STRIDE = 1 + 2 * D64;
-  constexpr int Q4 = D64 / 4;                   // float4 per row
-  constexpr int QH = D64 / 8;
-  constexpr int PTS = 64;                       // points per iteration
-  constexpr int LD = PTS * Q4 / 256;            // float4 per thread per tile
-  constexpr int RP = 20;                        // r / partial tile lane pitch (floats)
-  static_assert(kT == 4, "refined lists are loaded as int4/float4");
-  __shared__ __align__(16) float xs[PTS * P];
-  __shared__ __align__(16) float rt[2 * 64 * RP];
-  __shared__ __align__(16) float pl[2 * 64 * RP];
-  __shared__ float lzs[PTS];
-  __shared__ unsigned rbits[PTS];
-  __shared__ __align__(16) int4 lsl[PTS];
-  const int kb = blockIdx.x / (NH * nch);
-  const int hh = (blockIdx.x / nch) % NH;
-  const int chunk = blockIdx.x % nch;
-  if (kb >= counts[2]) return;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, h = lane >> 5, col = lane & 31;
+  static_assert(kT == 4, "refined lists are loaded as int4");
+  static_assert(LD >= 1 && PTS * Q4 % 256 == 0, "tile split");
+  __shared__ __align__(16) float xs[2][PTS * P];
+  __shared__ float lzb[2][PTS];
+  __shared__ unsigned long long rbb[2][PTS];
+  const int kb = blockIdx.x / nch, chunk = blockIdx.x % nch;
+  if (2 * kb >= counts[2]) return;              // counts[2]: well blocks of 32
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int i16 = lane & 15, k4 = lane >> 4;
   const int64_t p0 = (int64_t)chunk * chunk_pts;
   const int64_t p1 = p0 + chunk_pts < n ? p0 + chunk_pts : n;
-  const float cb = cw[kb * kBK + col];
-  const int ptile = wave >> 1;                  // producer: tile
-  const bool pxsq = (wave & 1) != 0;            // producer: x^2 chain
-  const float4* wpc = wp + ((size_t)kb * Q4 + (pxsq ? QH : 0)) * 64;
-  const int c0 = hh * CW;                       // first x dimension of this part
-  const bool sq = wave >= 2;                    // consumer: x^2 columns
-  const int cdim = c0 + (wave & 1) * (CW / 2);  // consumer: first dimension
-  double* pw = part + ((size_t)blockIdx.x * 4 + wave) * kBK * STRIDE;
-
-  f16v acc[NE];
+  double* pw = part + (size_t)blockIdx.x * kWB * STRIDE;
+  if (p0 >= p1) {
+    for (int i = tid; i < kWB * STRIDE; i += 256) pw[i] = 0.0;
+    return;
+  }
+  const int niter = (int)((p1 - p0 + PTS - 1) / PTS);
+  const int grp = kb * 4 + wave;                // 16-component group
+  const float cb = cw[grp * 16 + i16];
+  float wb[2 * NS];
 #pragma unroll
-  for (int e = 0; e < NE; ++e) acc[e] = f16v{};
-  float nkacc = 0.0f;
-  bool first = true;
-  int iter = 0;
+  for (int s2 = 0; s2 < 2 * NS; ++s2) wb[s2] = wq[((size_t)grp * 2 * NS + s2) * 64 + lane];
 
+  // ---- X tile: global -> registers -> LDS
   float4 px[LD];
   float plz = INFINITY;
-  int4 psl = make_int4(-1, -1, -1, -1);
-  auto prefetch = [&](int64_t it) {
+  unsigned long long prb = 0ull;
+  auto load_regs = [&](int i) {
+    const int64_t it = p0 + (int64_t)i * PTS;
 #pragma unroll
     for (int j = 0; j < LD; ++j) {
       const int idx = tid + 256 * j, r = idx / Q4, c = (idx % Q4) * 4;
       const int64_t nn = it + r;
-      float4 v;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
       if (vec4) {
-        const bool ok = nn < p1 && c < d;
-        v = *reinterpret_cast<const float4*>(x + (ok ? nn * d + c : 0));
-        if (!ok) v = make_float4(0.f, 0.f, 0.f, 0.f);
-      } else {
-        v = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (nn < p1) {
-          const float* xr = x + nn * d;
-          v.x = c < d ? xr[c] : 0.f;
-          v.y = c + 1 < d ? xr[c + 1] : 0.f;
-          v.z = c + 2 < d ? xr[c + 2] : 0.f;
-          v.w = c + 3 < d ? xr[c + 3] : 0.f;
-        }
+        if (nn < p1 && c < d) v = *reinterpret_cast<const float4*>(x + nn * d + c);
+      } else if (nn < p1) {
+        const float* xr = x + nn * d;
+        v.x = c < d ? xr[c] : 0.f;
+        v.y = c + 1 < d ? xr[c + 1] : 0.f;
+        v.z = c + 2 < d ? xr[c + 2] : 0.f;
+        v.w = c + 3 < d ? xr[c + 3] : 0.f;
       }
       px[j] = v;
     }
     if (tid < PTS) {
       const int64_t nn = it + tid;
-      const bool ok = nn < p1;
-      const int64_t src = ok ? nn : 0;
-      plz = ok ? logz2[src] : INFINITY;
-      psl = *reinterpret_cast<const int4*>(cslot + src * kT);
-      if (!ok) psl = make_int4(-1, -1, -1, -1);
+      plz = INFINITY;
+      prb = 0ull;
+      if (nn < p1) {
+        plz = logz2[nn];
+        const int4 sl = *reinterpret_cast<const int4*>(cslot + nn * kT);
+        const int v4[4] = {sl.x, sl.y, sl.z, sl.w};
+#pragma unroll
+        for (int j = 0; j < kT; ++j)
+          if (v4[j] >= 0 && v4[j] / kWB == kb) prb |= 1ull << (v4[j] % kWB);
+      }
+    }
+  };
+  auto store_regs = [&](int buf) {
+#pragma unroll
+    for (int j = 0; j < LD; ++j) {
+      const int idx = tid + 256 * j, r = idx / Q4, c = (idx % Q4) * 4;
+      *reinterpret_cast<float4*>(&xs[buf][r * P + c]) = px[j];
+    }
+    if (tid < PTS) {
+      lzb[buf][tid] = plz;
+      rbb[buf][tid] = prb;
     }
   };
 
+  f4v acc[2 * NB];
+#pragma unroll
+  for (int c = 0; c < 2 * NB; ++c) acc[c] = f4v{0.f, 0.f, 0.f, 0.f};
+  float nkacc = 0.0f;
+  bool first = true;
+  const int myc = wave * 16 + i16;              // this lane's component in the block
+
+  // fp32 accumulators -> fp64 partial.  Register v of block c at lane l is
+  // column 4(l/16) + v of the block: dimension 64 (c/4 % NG) + 4 (4 k4 + v) + c % 4.
   auto flush = [&]() {
-    const float nk2 = nkacc + __shfl_xor(nkacc, 32);
-    if (first) {
-      for (int i = lane; i < kBK * STRIDE; i += 64) pw[i] = 0.0;
-    }
-    if (h == 0 && hh == 0 && !pxsq) {
-      double* dst = pw + (size_t)col * STRIDE;
-      dst[0] = first ? (double)nk2 : dst[0] + (double)nk2;
-    }
+    float nk2 = nkacc + __shfl_xor(nkacc, 16);
+    nk2 += __shfl_xor(nk2, 32);
+    double* row = pw + (size_t)myc * STRIDE;
+    if (k4 == 0) row[0] = first ? (double)nk2 : row[0] + (double)nk2;
 #pragma unroll
-    for (int e = 0; e < NE; ++e) {
+    for (int part2 = 0; part2 < 2; ++part2) {
 #pragma unroll
-      for (int v0 = 0; v0 < 16; v0 += 8) {
-        double o[8];
+      for (int g = 0; g < NG; ++g) {
+        double o[16];
 #pragma unroll
-        for (int v = v0; v < v0 + 8; ++v) {
-          const int i = 8 * (v >> 2) + 4 * h + (v & 3);
-          const int dim = cdim + NE * i + e;
-          o[v - v0] = first ? 0.0 : pw[(size_t)col * STRIDE + 1 + (sq ? D64 : 0) + dim];
-        }
+        for (int e = 0; e < 4; ++e)
 #pragma unroll
-        for (int v = v0; v < v0 + 8; ++v) {
-          const int i = 8 * (v >> 2) + 4 * h + (v & 3);
-          const int dim = cdim + NE * i + e;
-          pw[(size_t)col * STRIDE + 1 + (sq ? D64 : 0) + dim] = o[v - v0] + (double)acc[e][v];
-          acc[e][v] = 0.0f;
-        }
+          for (int v = 0; v < 4; ++v) {
+            const int dim = 64 * g + 4 * (4 * k4 + v) + e;
+            o[4 * e + v] = first ? 0.0 : row[1 + part2 * D64 + dim];
+          }
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int dim = 64 * g + 4 * (4 * k4 + v) + e;
+            const int c = part2 * NB + 4 * g + e;
+            row[1 + part2 * D64 + dim] = o[4 * e + v] + (double)acc[c][v];
+            acc[c][v] = 0.0f;
+          }
       }
     }
     nkacc = 0.0f;
     first = false;
   };
 
-  if (p0 < p1) prefetch(p0);
-  for (int64_t it = p0; it < p1; it += PTS, ++iter) {
-    __syncthreads();   // every read of the previous tile is done
-#pragma unroll
-    for (int j = 0; j < LD; ++j) {
-      const int idx = tid + 256 * j, r = idx / Q4, c = (idx % Q4) * 4;
-      *reinterpret_cast<float4*>(xs + r * P + c) = px[j];
-    }
-    if (tid < PTS) {
-      lzs[tid] = plz;
-      rbits[tid] = 0u;
-      lsl[tid] = psl;
-    }
-    __syncthreads();
-    {
-      // flag the refined pairs of points 16w..16w+15 that fall in this block
-      const int pt = wave * 16 + lane / kT, j = lane % kT;
-      const int4 sl4 = lsl[pt];
-      const int sl = j == 0 ? sl4.x : (j == 1 ? sl4.y : (j == 2 ? sl4.z : sl4.w));
-      if (sl >= 0 && (sl >> 5) == kb) atomicOr(&rbits[pt], 1u << (sl & 31));
-    }
-    // producers: one chain of tile `ptile`
-    {
-      f16v a;
-      logits_chain<D64>(xs, ptile * 32, pxsq, wpc, a);
-      if (pxsq) {
-        float* dst = pl + (ptile * 64 + lane) * RP;
-#pragma unroll
-        for (int v = 0; v < 16; v += 4)
-          *reinterpret_cast<float4*>(dst + v) = make_float4(a[v], a[v + 1], a[v + 2], a[v + 3]);
-      }
-      __syncthreads();   // x^2 chains and refined flags complete
-      if (!pxsq) {
-        const float* srcp = pl + (ptile * 64 + lane) * RP;
-        float* dst = rt + (ptile * 64 + lane) * RP;
-#pragma unroll
-        for (int v = 0; v < 16; v += 4) {
-          const float4 b = *reinterpret_cast<const float4*>(srcp + v);
-          const float bb[4] = {b.x, b.y, b.z, b.w};
-          float rr[4];
-#pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            const int vv = v + u;
-            const int row = ptile * 32 + 8 * (vv >> 2) + 4 * h + (vv & 3);
-            const float l = (a[vv] + bb[u]) + cb;
-            float r = exp2_fast(l - lzs[row]);
-            r = ((rbits[row] >> col) & 1u) ? 0.0f : r;
-            nkacc += r;
-            rr[u] = r;
-          }
-          *reinterpret_cast<float4*>(dst + v) = make_float4(rr[0], rr[1], rr[2], rr[3]);
-        }
-      }
-    }
-    __syncthreads();   // r tiles complete
-    if (it + PTS < p1) prefetch(it + PTS);
-    // consumers: statistic contraction for this wave's columns over both tiles
+  load_regs(0);
+  store_regs(0);
+  for (int i = 0; i < niter; ++i) {
+    const int cur = i & 1;
+    __syncthreads();                            // tile i in xs[cur]; xs[cur ^ 1] free
+    if (i + 1 < niter) load_regs(i + 1);
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
-      const float* src = rt + (t * 64 + lane) * RP;
-      float rb[16];
+      // log-densities of points t*16 .. t*16+15 against this wave's components
+      f4v la = {cb, cb, cb, cb};
+      const float* xr = &xs[cur][(t * 16 + i16) * P + 4 * k4];
 #pragma unroll
-      for (int v = 0; v < 16; v += 4) {
-        const float4 q4 = *reinterpret_cast<const float4*>(src + v);
-        rb[v] = q4.x; rb[v + 1] = q4.y; rb[v + 2] = q4.z; rb[v + 3] = q4.w;
+      for (int j = 0; j < NS / 4; ++j) {
+        const float4 u = *reinterpret_cast<const float4*>(xr + 16 * j);
+        la = mfma16(u.x, wb[4 * j], la);
+        la = mfma16(u.y, wb[4 * j + 1], la);
+        la = mfma16(u.z, wb[4 * j + 2], la);
+        la = mfma16(u.w, wb[4 * j + 3], la);
       }
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = t * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
-        const float* xp = xs + row * P + cdim + NE * col;
-        float a[NE];
-        if constexpr (NE == 2) {
-          const float2 q2 = *reinterpret_cast<const float2*>(xp);
-          a[0] = q2.x; a[1] = q2.y;
-        } else {
+      for (int j = 0; j < NS / 4; ++j) {
+        const float4 u = *reinterpret_cast<const float4*>(xr + 16 * j);
+        la = mfma16(u.x * u.x, wb[NS + 4 * j], la);
+        la = mfma16(u.y * u.y, wb[NS + 4 * j + 1], la);
+        la = mfma16(u.z * u.z, wb[NS + 4 * j + 2], la);
+        la = mfma16(u.w * u.w, wb[NS + 4 * j + 3], la);
+      }
+      float r[4];
 #pragma unroll
-          for (int e = 0; e < NE; ++e) a[e] = xp[e];
+      for (int v = 0; v < 4; ++v) {
+        const int pt = t * 16 + 4 * k4 + v;
+        const float e = exp2_fast(la[v] - lzb[cur][pt]);
+        r[v] = ((rbb[cur][pt] >> myc) & 1ull) ? 0.0f : e;
+        nkacc += r[v];
+      }
+      // statistics: step v contracts points t*16 + 4k + v (k = 0..3)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const float* yr = &xs[cur][(t * 16 + 4 * k4 + v) * P + 4 * i16];
+#pragma unroll
+        for (int g = 0; g < NG; ++g) {
+          const float4 y = *reinterpret_cast<const float4*>(yr + 64 * g);
+          acc[4 * g + 0] = mfma16(y.x, r[v], acc[4 * g + 0]);
+          acc[4 * g + 1] = mfma16(y.y, r[v], acc[4 * g + 1]);
+          acc[4 * g + 2] = mfma16(y.z, r[v], acc[4 * g + 2]);
+          acc[4 * g + 3] = mfma16(y.w, r[v], acc[4 * g + 3]);
+          acc[NB + 4 * g + 0] = mfma16(y.x * y.x, r[v], acc[NB + 4 * g + 0]);
+          acc[NB + 4 * g + 1] = mfma16(y.y * y.y, r[v], acc[NB + 4 * g + 1]);
+          acc[NB + 4 * g + 2] = mfma16(y.z * y.z, r[v], acc[NB + 4 * g + 2]);
+          acc[NB + 4 * g + 3] = mfma16(y.w * y.w, r[v], acc[NB + 4 * g + 3]);
         }
-#pragma unroll
-        for (int e = 0; e < NE; ++e) acc[e] = mfma32(sq ? a[e] * a[e] : a[e], rb[v], acc[e]);
       }
     }
-    if ((iter % kFlush) == kFlush - 1) flush();
+    if (i + 1 < niter) store_regs(cur ^ 1);
+    if ((i % kFlush) == kFlush - 1 || i + 1 == niter) flush();
   }
-  if (first || (iter % kFlush) != 0) flush();
 }
 
 // Refined pairs of a well block, in fp64.  Grid: (block, sparse chunk).  The
@@ -1093,10 +1083,8 @@ __global__ __launch_bounds__(256) void k_reduce_stats(
   if (which == 0) {
     if (slot >= counts[0]) return;
     comp = well_idx[slot];
-    const int cw = D64 % 128 == 0 ? 128 : 64, nh = D64 / cw, hh = dim / cw;
-    const double* p = part_w + ((size_t)((slot / kBK) * nh + hh) * nch * 4 * kBK + (slot % kBK)) * stride + off;
-    for (int ch = 0; ch < nch; ++ch)
-      for (int w = 0; w < 4; ++w) acc += p[((size_t)ch * 4 + w) * kBK * stride];
+    const double* p = part_w + ((size_t)(slot / kWB) * nch * kWB + (slot % kWB)) * stride + off;
+    for (int ch = 0; ch < nch; ++ch) acc += p[(size_t)ch * kWB * stride];
     const double* ps = part_s + ((size_t)(slot / kBK) * nch_s * kBK + (slot % kBK)) * stride + off;
     for (int ch = 0; ch < nch_s; ++ch) acc += ps[(size_t)ch * kBK * stride];
   } else {
@@ -1164,11 +1152,11 @@ inline size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 struct Layout {
   int64_t n;
   int d, k, kpad, D64, m;
-  int nch, nh, grid_i, nch_s;
+  int nch, grid_i, nch_s;   // nch: chunks of k_stats_well (64-component blocks)
   int64_t chunk_s;
   int64_t chunk, n_wg_logz;
   size_t off_counts, off_cls, off_cwell, off_cdir, off_cthr, off_thr, off_well_idx, off_ill_idx,
-      off_cw, off_wp,
+      off_cw, off_wp, off_wq,
       off_dmu, off_dh, off_dc, off_logz2, off_cslot, off_cr, off_llpart, off_part_w, off_part_s, off_part_i,
       off_fit_nk, off_fit_s, off_fit_q, total;
 };
@@ -1177,18 +1165,19 @@ bool make_layout(int64_t n, int d, int k, int m, Layout* L) {
   if (n < 1 || d < 1 || k < 1 || d > GMM_MAX_D || k > GMM_MAX_K || m < 0 || m > GMM_MAX_M)
     return false;
   L->n = n; L->d = d; L->k = k; L->m = m;
-  L->kpad = (int)cdiv(k, kBK) * kBK;
+  L->kpad = (int)cdiv(k, kWB) * kWB;
   L->D64 = (int)cdiv(d, 64) * 64;
   const int nkb = L->kpad / kBK;
-  // chunking depends only on (n, k), never on the device
-  int maxc = 512 / nkb;
+  const int nwb = L->kpad / kWB;
+  // chunking depends only on (n, k), never on the device: about 512
+  // workgroups (two per CU) for k_stats_well
+  int maxc = 512 / nwb;
   if (maxc < 8) maxc = 8;
-  int64_t c = cdiv(n, 2048);
+  int64_t c = cdiv(n, 1024);
   if (c > maxc) c = maxc;
   if (c >= 8) c = c / 8 * 8;
   L->nch = (int)(c < 1 ? 1 : c);
   L->chunk = cdiv(n, L->nch);
-  L->nh = L->D64 / (L->D64 % 128 == 0 ? 128 : 64);
   {
     int maxs = 2048 / nkb;
     if (maxs < 8) maxs = 8;
@@ -1211,6 +1200,7 @@ bool make_layout(int64_t n, int d, int k, int m, Layout* L) {
   L->off_cthr = take((size_t)k * sizeof(float));
   L->off_thr = take((size_t)L->kpad * sizeof(float));
   L->off_wp = take((size_t)L->kpad * 2 * L->D64 * sizeof(float));
+  L->off_wq = take((size_t)L->kpad * 2 * L->D64 * sizeof(float));
   L->off_dmu = take((size_t)k * L->D64 * sizeof(float));
   L->off_dh = take((size_t)k * L->D64 * sizeof(float));
   L->off_dc = take((size_t)k * sizeof(float));
@@ -1218,7 +1208,7 @@ bool make_layout(int64_t n, int d, int k, int m, Layout* L) {
   L->off_cslot = take((size_t)n * kT * sizeof(int));
   L->off_cr = take((size_t)n * kT * sizeof(float));
   L->off_llpart = take((size_t)L->n_wg_logz * sizeof(double));
-  L->off_part_w = take((size_t)nkb * L->nh * L->nch * 4 * kBK * (1 + 2 * (size_t)L->D64) * sizeof(double));
+  L->off_part_w = take((size_t)nwb * L->nch * kWB * (1 + 2 * (size_t)L->D64) * sizeof(double));
   L->off_part_s = take((size_t)nkb * L->nch_s * kBK * (1 + 2 * (size_t)L->D64) * sizeof(double));
   L->off_part_i = take((size_t)L->grid_i * kBK * (1 + 2 * (size_t)L->D64) * sizeof(double));
   L->off_fit_nk = take((size_t)k * sizeof(double) + sizeof(double));  // + loglik slot
@@ -1252,6 +1242,7 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
   float* cthr = at<float>(ws, L.off_cthr);
   float* thr = at<float>(ws, L.off_thr);
   float4* wp = at<float4>(ws, L.off_wp);
+  float* wq = at<float>(ws, L.off_wq);
   float* dmu = at<float>(ws, L.off_dmu);
   float* dh = at<float>(ws, L.off_dh);
   float* dc = at<float>(ws, L.off_dc);
@@ -1271,6 +1262,8 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
     const int64_t tot = (int64_t)kpad * (D64 / 4) * 2;
     hipLaunchKernelGGL(k_prep_pack_well<D64>, dim3((unsigned)cdiv(tot, 256)), dim3(256), 0, st,
                        mu, var, d, kpad, cwell, cthr, counts, well_idx, wp, cw, thr);
+    hipLaunchKernelGGL(k_prep_pack_w16<D64>, dim3((unsigned)cdiv((int64_t)kpad * 2 * D64, 256)),
+                       dim3(256), 0, st, mu, var, d, kpad, counts, well_idx, wq);
     const int64_t toti = (int64_t)k * D64;
     hipLaunchKernelGGL(k_prep_pack_direct<D64>, dim3((unsigned)cdiv(toti, 256)), dim3(256), 0,
                        st, mu, var, d, k, cdir, dmu, dh, dc);
@@ -1278,8 +1271,8 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
   hipLaunchKernelGGL(k_logz<D64>, dim3((unsigned)L.n_wg_logz), dim3(256), 0, st, x, n, d, vec4,
                      wp, cw, thr, well_idx, ill_idx, dmu, dh, dc, counts, logz2, cslot, cr,
                      llpart);
-  hipLaunchKernelGGL(k_stats_well<D64>, dim3((unsigned)((kpad / kBK) * L.nh * L.nch)), dim3(256),
-                     0, st, x, n, d, vec4, wp, cw, counts, logz2, cslot, L.nch, L.chunk, part_w);
+  hipLaunchKernelGGL(k_stats_well<D64>, dim3((unsigned)((kpad / kWB) * L.nch)), dim3(256),
+                     0, st, x, n, d, vec4, wq, cw, counts, logz2, cslot, L.nch, L.chunk, part_w);
   hipLaunchKernelGGL(k_stats_sparse<D64>, dim3((unsigned)((kpad / kBK) * L.nch_s)), dim3(256), 0,
                      st, x, n, d, counts, cslot, cr, L.nch_s, L.chunk_s, part_s);
   hipLaunchKernelGGL(k_stats_ill<D64>, dim3((unsigned)L.grid_i), dim3(256), 0, st, x, n, d, vec4,
