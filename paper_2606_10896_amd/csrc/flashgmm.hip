@@ -125,6 +125,15 @@ __device__ __forceinline__ void topk_insert(float* tl, int* tsl, float l, int sl
   }
 }
 
+// Lane-state update without arg-max (same kEmpty convention).
+__device__ __forceinline__ void lse_add_e(float& m, float& s, float l) {
+  const float dl = l - m;
+  const float e = exp2_fast(-fabsf(dl));
+  const bool gt = dl > 0.0f;
+  s = gt ? __fmaf_rn(s, e, 1.0f) : s + e;
+  m = gt ? l : m;
+}
+
 // ---------------------------------------------------------------- tiles
 // rows x D64 fp32 tile of x (rows [r0, r0+rows)) into LDS with row pitch D64+4;
 // rows >= nend and columns >= d are zero.
@@ -335,18 +344,17 @@ __global__ __launch_bounds__(256) void k_prep_pack_direct(
 }
 
 // ---------------------------------------------------------------- Step 1: log-normalisers
-// One software-pipelined step of k_logz for one wave: when MF, the log-densities
-// of 64 points (two 32-point tiles) against component block wpb are formed on
-// MFMA into n0, n1, one chain per tile: bias first, then for every group of 8
-// dimensions the four x steps and the four x^2 steps.  When EPI, the lane
-// states take in the previous block's log-densities c0, c1 (slot = its
-// component slot of this lane), spread over the contraction so that the vector
-// ALU work overlaps the matrix work.
-template <int D64, bool MF, bool EPI>
+// One software-pipelined step of a screening pass for one wave: when MF, the
+// log-densities of 64 points (two 32-point tiles) against component block wpb
+// are formed on MFMA into n0, n1, one chain per tile: bias first, then for
+// every group of 8 dimensions the four x steps and the four x^2 steps.  When
+// EPI, epi(v, c0[v], c1[v]) takes in the previous block's log-densities,
+// spread over the contraction so that the vector ALU work overlaps the matrix
+// work.
+template <int D64, bool MF, bool EPI, class Epi>
 __device__ __forceinline__ void logz_step(const float* xs, const float4* __restrict__ wpb,
                                           float cb, f16v& n0, f16v& n1, const f16v& c0,
-                                          const f16v& c1, int slot, float* m0, float* s0,
-                                          int* a0, float* m1, float* s1, int* a1) {
+                                          const f16v& c1, Epi&& epi) {
   constexpr int P = D64 + 4, QH = D64 / 8;
   const int lane = threadIdx.x & 63, h = lane >> 5, col = lane & 31;
   const float* xr0 = xs + col * P + 4 * h;
@@ -389,10 +397,7 @@ __device__ __forceinline__ void logz_step(const float* xs, const float4* __restr
     }
     if (EPI) {
 #pragma unroll
-      for (int v = q * 16 / QH; v < (q + 1) * 16 / QH; ++v) {
-        lse_add_arg(m0[v], s0[v], a0[v], c0[v], slot);
-        lse_add_arg(m1[v], s1[v], a1[v], c1[v], slot);
-      }
+      for (int v = q * 16 / QH; v < (q + 1) * 16 / QH; ++v) epi(v, c0[v], c1[v]);
     }
     // keep each step's loads in their step (unbounded hoisting exhausts registers)
     __builtin_amdgcn_sched_barrier(0);
@@ -457,21 +462,26 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_logz(
     const int nb = n_wkb > wave ? (n_wkb - wave + 3) / 4 : 0;
     constexpr size_t BS = (size_t)(D64 / 4) * 64;
     f16v c0, c1, x0, x1;
+    int slot = 0;
+    auto epi = [&](int v, float l0, float l1) {
+      lse_add_arg(m0[v], s0[v], a0[v], l0, slot);
+      lse_add_arg(m1[v], s1[v], a1[v], l1, slot);
+    };
     if (nb > 0) {
       logz_step<D64, true, false>(xs, wp + (size_t)wave * BS, cw[wave * kBK + col], c0, c1, x0,
-                                  x1, 0, m0, s0, a0, m1, s1, a1);
+                                  x1, epi);
       float cbn = nb > 1 ? cw[(wave + 4) * kBK + col] : 0.0f;
       for (int i = 0; i + 1 < nb; ++i) {
         const int kb = wave + 4 * i;
         const float cb = cbn;
         if (i + 2 < nb) cbn = cw[(kb + 8) * kBK + col];
-        logz_step<D64, true, true>(xs, wp + (size_t)(kb + 4) * BS, cb, x0, x1, c0, c1,
-                                   kb * kBK + col, m0, s0, a0, m1, s1, a1);
+        slot = kb * kBK + col;
+        logz_step<D64, true, true>(xs, wp + (size_t)(kb + 4) * BS, cb, x0, x1, c0, c1, epi);
         c0 = x0;
         c1 = x1;
       }
-      logz_step<D64, false, true>(xs, wp, 0.0f, x0, x1, c0, c1,
-                                  (wave + 4 * (nb - 1)) * kBK + col, m0, s0, a0, m1, s1, a1);
+      slot = (wave + 4 * (nb - 1)) * kBK + col;
+      logz_step<D64, false, true>(xs, wp, 0.0f, x0, x1, c0, c1, epi);
     }
   }
   // arg-max of every lane state, and the per-wave merged state of every point
@@ -769,21 +779,30 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
       // log-densities of points t*16 .. t*16+15 against this wave's components
       f4v la = {cb, cb, cb, cb};
       const float* xr = &xs[cur][(t * 16 + i16) * P + 4 * k4];
+      // wide D: keep each group's operand load one group ahead and no further
+      // (hoisting all of them exhausts the registers)
+      constexpr bool kPin = D64 > 128;
+      float4 un = *reinterpret_cast<const float4*>(xr);
 #pragma unroll
       for (int j = 0; j < NS / 4; ++j) {
-        const float4 u = *reinterpret_cast<const float4*>(xr + 16 * j);
+        const float4 u = un;
+        if (j + 1 < NS / 4) un = *reinterpret_cast<const float4*>(xr + 16 * (j + 1));
         la = mfma16(u.x, wb[4 * j], la);
         la = mfma16(u.y, wb[4 * j + 1], la);
         la = mfma16(u.z, wb[4 * j + 2], la);
         la = mfma16(u.w, wb[4 * j + 3], la);
+        if constexpr (kPin) __builtin_amdgcn_sched_barrier(0);
       }
+      un = *reinterpret_cast<const float4*>(xr);
 #pragma unroll
       for (int j = 0; j < NS / 4; ++j) {
-        const float4 u = *reinterpret_cast<const float4*>(xr + 16 * j);
+        const float4 u = un;
+        if (j + 1 < NS / 4) un = *reinterpret_cast<const float4*>(xr + 16 * (j + 1));
         la = mfma16(u.x * u.x, wb[NS + 4 * j], la);
         la = mfma16(u.y * u.y, wb[NS + 4 * j + 1], la);
         la = mfma16(u.z * u.z, wb[NS + 4 * j + 2], la);
         la = mfma16(u.w * u.w, wb[NS + 4 * j + 3], la);
+        if constexpr (kPin) __builtin_amdgcn_sched_barrier(0);
       }
       float r[4];
 #pragma unroll
@@ -808,6 +827,7 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
           acc[NB + 4 * g + 1] = mfma16(y.y * y.y, r[v], acc[NB + 4 * g + 1]);
           acc[NB + 4 * g + 2] = mfma16(y.z * y.z, r[v], acc[NB + 4 * g + 2]);
           acc[NB + 4 * g + 3] = mfma16(y.w * y.w, r[v], acc[NB + 4 * g + 3]);
+          if constexpr (kPin) __builtin_amdgcn_sched_barrier(0);
         }
       }
     }
@@ -1062,6 +1082,361 @@ __global__ __launch_bounds__(256) void k_stats_ill(
   }
 }
 
+// ---------------------------------------------------------------- assignment (Sec. 4.2, 4.3)
+// Top-m multi-assignment at the given parameters, exact in the component order:
+//   1. k_assign_theta: the screened log-densities of every point (the MFMA
+//      pass of k_logz) give the T-th largest of its 128 lane-state maxima,
+//      S_T (T = m + 2).  At least T components have a screened log-density
+//      >= S_T, so the T-th largest exact one is >= S_T - slack, and every
+//      component among the T largest has a screened log-density >= theta =
+//      S_T - 2 slack, slack = kScreenSlack >= the screening error (log2 units).
+//   2. k_assign_collect: a second screening pass keeps every component with a
+//      screened log-density >= theta as a candidate (at most kACap per point)
+//      and sums all others in a log-sum-exp; the candidates' log-densities are
+//      recomputed in fp64 (direct form), ranked (ties to the lower index), and
+//      normalised with log Z = log(sum over candidates of exp(exact) + the
+//      screened sum of the others).  Rank 1 is always assigned, rank j > 1
+//      only if its responsibility is > tau.
+//   3. k_assign_fallback: points with more than kACap candidates are done
+//      exactly over all components in fp64.
+constexpr int kACap = 32;
+constexpr float kScreenSlack = 1.0f;
+constexpr int kTMax = GMM_MAX_M + 2;
+
+// fp64 direct-form log-density (natural log) of component comp at point xr
+// (fp32 row in LDS), from the caller's fp32 parameters and the fp64 constant
+// cdir (log2 units).
+__device__ __forceinline__ double ell64(const float* xr, const float* __restrict__ mu,
+                                        const float* __restrict__ var, double cdir_k, int d) {
+  double acc = 0.0;
+  for (int j = 0; j < d; ++j) {
+    const double t = (double)xr[j] - (double)mu[j];
+    acc += t * t / (double)var[j];
+  }
+  return cdir_k * kLn2 - 0.5 * acc;
+}
+
+template <int D64>
+__global__ __launch_bounds__(256) void k_assign_theta(
+    const float* __restrict__ x, int64_t n, int d, int vec4, const float4* __restrict__ wp,
+    const float* __restrict__ cw, const int* __restrict__ counts, int tsel,
+    float* __restrict__ theta) {
+  constexpr int P = D64 + 4;
+  __shared__ __align__(16) float xs[64 * P];
+  __shared__ float lmax[64][129];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, h = lane >> 5, col = lane & 31;
+  const int64_t n0 = (int64_t)blockIdx.x * 64;
+  load_tile<D64>(x, n, d, n0, 64, xs, vec4 != 0);
+  __syncthreads();
+  const int n_wkb = counts[2];
+  float m0[16], m1[16];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) m0[v] = m1[v] = kEmpty;
+  {
+    const int nb = n_wkb > wave ? (n_wkb - wave + 3) / 4 : 0;
+    constexpr size_t BS = (size_t)(D64 / 4) * 64;
+    f16v c0, c1, x0, x1;
+    auto epi = [&](int v, float l0, float l1) {
+      m0[v] = fmaxf(m0[v], l0);
+      m1[v] = fmaxf(m1[v], l1);
+    };
+    if (nb > 0) {
+      logz_step<D64, true, false>(xs, wp + (size_t)wave * BS, cw[wave * kBK + col], c0, c1, x0,
+                                  x1, epi);
+      for (int i = 0; i + 1 < nb; ++i) {
+        const int kb = wave + 4 * i;
+        logz_step<D64, true, true>(xs, wp + (size_t)(kb + 4) * BS, cw[(kb + 4) * kBK + col], x0,
+                                   x1, c0, c1, epi);
+        c0 = x0;
+        c1 = x1;
+      }
+      logz_step<D64, false, true>(xs, wp, 0.0f, x0, x1, c0, c1, epi);
+    }
+  }
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int p = 8 * (v >> 2) + 4 * h + (v & 3);
+    lmax[p][wave * 32 + col] = m0[v];
+    lmax[32 + p][wave * 32 + col] = m1[v];
+  }
+  __syncthreads();
+  if (tid < 64 && n0 + tid < n) {
+    float tl[kTMax];
+#pragma unroll
+    for (int j = 0; j < kTMax; ++j) tl[j] = -INFINITY;
+    for (int c = 0; c < 128; ++c) {
+      const float v = lmax[tid][c];
+      if (!(v > 0.5f * kEmpty)) continue;      // empty lane state
+#pragma unroll
+      for (int j = kTMax - 1; j > 0; --j) {
+        if (v > tl[j - 1]) tl[j] = tl[j - 1];
+        else if (v > tl[j]) tl[j] = v;
+      }
+      if (v > tl[0]) tl[0] = v;
+    }
+    float st = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < kTMax; ++j)
+      if (j == tsel - 1) st = tl[j];
+    theta[n0 + tid] = st - 2.0f * kScreenSlack;
+  }
+}
+
+template <int D64>
+__global__ __launch_bounds__(256) void k_assign_collect(
+    const float* __restrict__ x, int64_t n, int d, int vec4, const float4* __restrict__ wp,
+    const float* __restrict__ cw, const int* __restrict__ well_idx,
+    const int* __restrict__ ill_idx, const float* __restrict__ dmu,
+    const float* __restrict__ dh, const float* __restrict__ dc, const int* __restrict__ counts,
+    const float* __restrict__ theta, const float* __restrict__ mu,
+    const float* __restrict__ var, const double* __restrict__ cdir, int m, float tau,
+    int* __restrict__ idx, float* __restrict__ resp, int* __restrict__ ovf) {
+  constexpr int P = D64 + 4;
+  __shared__ __align__(16) float xs[64 * P];
+  __shared__ int ccnt[64];
+  __shared__ int cand[64][kACap];          // well slot s >= 0, or -(ill component + 1)
+  __shared__ double cl[64][kACap];
+  __shared__ float2 stw[4][64];
+  __shared__ float2 sti[4][64];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, h = lane >> 5, col = lane & 31;
+  const int64_t n0 = (int64_t)blockIdx.x * 64;
+  load_tile<D64>(x, n, d, n0, 64, xs, vec4 != 0);
+  if (tid < 64) ccnt[tid] = 0;
+  __syncthreads();
+  const int n_wkb = counts[2], n_ill = counts[1];
+  float th0[16], th1[16], m0[16], s0[16], m1[16], s1[16];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int p = 8 * (v >> 2) + 4 * h + (v & 3);
+    th0[v] = n0 + p < n ? theta[n0 + p] : INFINITY;
+    th1[v] = n0 + 32 + p < n ? theta[n0 + 32 + p] : INFINITY;
+    m0[v] = m1[v] = kEmpty;
+    s0[v] = s1[v] = 0.0f;
+  }
+  {
+    const int nb = n_wkb > wave ? (n_wkb - wave + 3) / 4 : 0;
+    constexpr size_t BS = (size_t)(D64 / 4) * 64;
+    f16v c0, c1, x0, x1;
+    int slot = 0;
+    auto epi = [&](int v, float l0, float l1) {
+      const int p = 8 * (v >> 2) + 4 * h + (v & 3);
+      if (l0 >= th0[v] && l0 > -INFINITY) {
+        const int pos = atomicAdd(&ccnt[p], 1);
+        if (pos < kACap) cand[p][pos] = slot;
+      } else {
+        lse_add_e(m0[v], s0[v], l0);
+      }
+      if (l1 >= th1[v] && l1 > -INFINITY) {
+        const int pos = atomicAdd(&ccnt[32 + p], 1);
+        if (pos < kACap) cand[32 + p][pos] = slot;
+      } else {
+        lse_add_e(m1[v], s1[v], l1);
+      }
+    };
+    if (nb > 0) {
+      logz_step<D64, true, false>(xs, wp + (size_t)wave * BS, cw[wave * kBK + col], c0, c1, x0,
+                                  x1, epi);
+      for (int i = 0; i + 1 < nb; ++i) {
+        const int kb = wave + 4 * i;
+        slot = kb * kBK + col;
+        logz_step<D64, true, true>(xs, wp + (size_t)(kb + 4) * BS, cw[(kb + 4) * kBK + col], x0,
+                                   x1, c0, c1, epi);
+        c0 = x0;
+        c1 = x1;
+      }
+      slot = (wave + 4 * (nb - 1)) * kBK + col;
+      logz_step<D64, false, true>(xs, wp, 0.0f, x0, x1, c0, c1, epi);
+    }
+  }
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int p = 8 * (v >> 2) + 4 * h + (v & 3);
+    float M0 = m0[v], S0 = s0[v], M1 = m1[v], S1 = s1[v];
+    for (int off = 16; off > 0; off >>= 1) {
+      lse_merge(M0, S0, __shfl_xor(M0, off), __shfl_xor(S0, off));
+      lse_merge(M1, S1, __shfl_xor(M1, off), __shfl_xor(S1, off));
+    }
+    if (col == 0) {
+      stw[wave][p] = make_float2(M0, S0);
+      stw[wave][32 + p] = make_float2(M1, S1);
+    }
+  }
+  {
+    // ill-conditioned components, direct form, lane = point
+    const float thl = n0 + lane < n ? theta[n0 + lane] : INFINITY;
+    float mi = kEmpty, si = 0.0f;
+    for (int ki = wave; ki < n_ill; ki += 4) {
+      const int comp = ill_idx[ki];
+      const float l = ill_logit<D64>(xs + lane * P, dmu + (size_t)comp * D64,
+                                     dh + (size_t)comp * D64, dc[comp]);
+      if (l >= thl && l > -INFINITY) {
+        const int pos = atomicAdd(&ccnt[lane], 1);
+        if (pos < kACap) cand[lane][pos] = -(comp + 1);
+      } else {
+        lse_add_e(mi, si, l);
+      }
+    }
+    sti[wave][lane] = make_float2(mi, si);
+  }
+  __syncthreads();
+  {
+    // exact fp64 log-densities of the candidates, spread over the waves
+    const int p = lane;
+    const int cnt = ccnt[p];
+    if (cnt <= kACap && n0 + p < n) {
+      for (int j = wave; j < cnt; j += 4) {
+        const int code = cand[p][j];
+        const int comp = code >= 0 ? well_idx[code] : -code - 1;
+        cl[p][j] = ell64(xs + p * P, mu + (size_t)comp * d, var + (size_t)comp * d, cdir[comp], d);
+      }
+    }
+  }
+  __syncthreads();
+  if (tid < 64 && n0 + tid < n) {
+    const int p = tid;
+    const int64_t nn = n0 + p;
+    const int cnt = ccnt[p];
+    if (cnt > kACap) {
+      ovf[nn] = 1;
+      return;
+    }
+    ovf[nn] = 0;
+    // screened sum of the non-candidates (log2 units) -> natural log, fp64
+    float mm = kEmpty;
+    for (int w2 = 0; w2 < 4; ++w2) mm = fmaxf(mm, fmaxf(stw[w2][p].x, sti[w2][p].x));
+    double snc = 0.0;
+    for (int w2 = 0; w2 < 4; ++w2) {
+      snc += (double)stw[w2][p].y * exp2((double)stw[w2][p].x - (double)mm);
+      snc += (double)sti[w2][p].y * exp2((double)sti[w2][p].x - (double)mm);
+    }
+    const double lnc = snc > 0.0 ? (double)mm * kLn2 + log(snc) : -INFINITY;
+    // rank the candidates: exact log-density descending, ties to the lower index
+    double tl[GMM_MAX_M];
+    int ti[GMM_MAX_M];
+#pragma unroll
+    for (int j = 0; j < GMM_MAX_M; ++j) { tl[j] = -INFINITY; ti[j] = -1; }
+    double lmx = lnc;
+    for (int j = 0; j < cnt; ++j) {
+      const int code = cand[p][j];
+      const int comp = code >= 0 ? well_idx[code] : -code - 1;
+      const double l = cl[p][j];
+      lmx = fmax(lmx, l);
+#pragma unroll
+      for (int q = GMM_MAX_M - 1; q >= 0; --q) {
+        const bool above = l > tl[q] || (l == tl[q] && ti[q] >= 0 && comp < ti[q]) || ti[q] < 0;
+        const bool above_prev =
+            q > 0 && (l > tl[q - 1] || (l == tl[q - 1] && ti[q - 1] >= 0 && comp < ti[q - 1]) ||
+                      ti[q - 1] < 0);
+        if (above_prev) { tl[q] = tl[q - 1]; ti[q] = ti[q - 1]; }
+        else if (above) { tl[q] = l; ti[q] = comp; }
+      }
+    }
+    double z = lnc > -INFINITY ? exp(lnc - lmx) : 0.0;
+    for (int j = 0; j < cnt; ++j) z += exp(cl[p][j] - lmx);
+    const double lz = lmx + log(z);
+#pragma unroll
+    for (int j = 0; j < GMM_MAX_M; ++j) {
+      if (j >= m) break;
+      int oi = -1;
+      float orr = 0.0f;
+      if (ti[j] >= 0) {
+        const double r = exp(tl[j] - lz);
+        if (j == 0 || r > (double)tau) { oi = ti[j]; orr = (float)r; }
+      }
+      idx[nn * m + j] = oi;
+      resp[nn * m + j] = orr;
+    }
+  }
+}
+
+// Points whose candidate list overflowed: every component's log-density in
+// fp64, thread t taking components t, t + 256, ...; per-thread top-m lists and
+// log-sum-exp states merged by one thread in thread order.
+__global__ __launch_bounds__(256) void k_assign_fallback(
+    const float* __restrict__ x, int64_t n, int d, int k, const float* __restrict__ mu,
+    const float* __restrict__ var, const double* __restrict__ cdir, int m, float tau,
+    const int* __restrict__ ovf, int* __restrict__ idx, float* __restrict__ resp) {
+  __shared__ float xr[GMM_MAX_D];
+  __shared__ int plist[1024];
+  __shared__ int pcnt;
+  __shared__ double lm[256], ls[256];
+  __shared__ double ltl[256][GMM_MAX_M];
+  __shared__ int lti[256][GMM_MAX_M];
+  const int tid = threadIdx.x;
+  const int64_t b0 = (int64_t)blockIdx.x * 1024;
+  if (tid == 0) pcnt = 0;
+  __syncthreads();
+  // the order of the list does not matter: every point's result is its own
+  for (int i = tid; i < 1024; i += 256)
+    if (b0 + i < n && ovf[b0 + i]) plist[atomicAdd(&pcnt, 1)] = i;
+  __syncthreads();
+  const int np = pcnt;
+  for (int ip = 0; ip < np; ++ip) {
+    const int64_t nn = b0 + plist[ip];
+    for (int j = tid; j < d; j += 256) xr[j] = x[nn * d + j];
+    __syncthreads();
+    double tl[GMM_MAX_M];
+    int ti[GMM_MAX_M];
+#pragma unroll
+    for (int j = 0; j < GMM_MAX_M; ++j) { tl[j] = -INFINITY; ti[j] = -1; }
+    double mx = -INFINITY, sm = 0.0;
+    for (int comp = tid; comp < k; comp += 256) {
+      const double l = ell64(xr, mu + (size_t)comp * d, var + (size_t)comp * d, cdir[comp], d);
+      if (!(l > -INFINITY)) continue;
+      if (l > mx) { sm = sm * exp(mx - l) + 1.0; mx = l; }
+      else sm += exp(l - mx);
+#pragma unroll
+      for (int q = GMM_MAX_M - 1; q >= 0; --q) {
+        // components arrive in increasing index order: ties keep the earlier
+        const bool above = ti[q] < 0 || l > tl[q];
+        const bool above_prev = q > 0 && (ti[q - 1] < 0 || l > tl[q - 1]);
+        if (above_prev) { tl[q] = tl[q - 1]; ti[q] = ti[q - 1]; }
+        else if (above) { tl[q] = l; ti[q] = comp; }
+      }
+    }
+    lm[tid] = mx;
+    ls[tid] = sm;
+#pragma unroll
+    for (int j = 0; j < GMM_MAX_M; ++j) { ltl[tid][j] = tl[j]; lti[tid][j] = ti[j]; }
+    __syncthreads();
+    if (tid == 0) {
+      double M = -INFINITY;
+      for (int t = 0; t < 256; ++t) M = fmax(M, lm[t]);
+      double z = 0.0;
+      for (int t = 0; t < 256; ++t)
+        if (lm[t] > -INFINITY) z += ls[t] * exp(lm[t] - M);
+      const double lz = M + log(z);
+      double bl[GMM_MAX_M];
+      int bi[GMM_MAX_M];
+      for (int j = 0; j < GMM_MAX_M; ++j) { bl[j] = -INFINITY; bi[j] = -1; }
+      for (int t = 0; t < 256; ++t)
+        for (int j2 = 0; j2 < GMM_MAX_M; ++j2) {
+          const int c = lti[t][j2];
+          if (c < 0) break;
+          const double l = ltl[t][j2];
+          for (int q = GMM_MAX_M - 1; q >= 0; --q) {
+            const bool above = bi[q] < 0 || l > bl[q] || (l == bl[q] && c < bi[q]);
+            const bool above_prev =
+                q > 0 && (bi[q - 1] < 0 || l > bl[q - 1] || (l == bl[q - 1] && c < bi[q - 1]));
+            if (above_prev) { bl[q] = bl[q - 1]; bi[q] = bi[q - 1]; }
+            else if (above) { bl[q] = l; bi[q] = c; }
+          }
+        }
+      for (int j = 0; j < m; ++j) {
+        int oi = -1;
+        float orr = 0.0f;
+        if (bi[j] >= 0) {
+          const double r = exp(bl[j] - lz);
+          if (j == 0 || r > (double)tau) { oi = bi[j]; orr = (float)r; }
+        }
+        idx[nn * m + j] = oi;
+        resp[nn * m + j] = orr;
+      }
+    }
+    __syncthreads();
+  }
+}
+
 // ---------------------------------------------------------------- fixed-order reductions
 __global__ __launch_bounds__(256) void k_reduce_stats(
     const double* __restrict__ part_w, const double* __restrict__ part_s,
@@ -1288,6 +1663,49 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
   return launch_status();
 }
 
+template <int D64>
+int assign_impl(const Layout& L, const float* x, const float* w, const float* mu,
+                const float* var, int m, float tau, int* idx, float* resp, void* ws,
+                hipStream_t st) {
+  const int64_t n = L.n;
+  const int d = L.d, k = L.k, kpad = L.kpad;
+  int* counts = at<int>(ws, L.off_counts);
+  int* cls = at<int>(ws, L.off_cls);
+  double* cwell = at<double>(ws, L.off_cwell);
+  double* cdir = at<double>(ws, L.off_cdir);
+  float* cthr = at<float>(ws, L.off_cthr);
+  float* thr = at<float>(ws, L.off_thr);
+  int* well_idx = at<int>(ws, L.off_well_idx);
+  int* ill_idx = at<int>(ws, L.off_ill_idx);
+  float* cw = at<float>(ws, L.off_cw);
+  float4* wp = at<float4>(ws, L.off_wp);
+  float* dmu = at<float>(ws, L.off_dmu);
+  float* dh = at<float>(ws, L.off_dh);
+  float* dc = at<float>(ws, L.off_dc);
+  float* theta = at<float>(ws, L.off_logz2);      // n floats, free during assignment
+  int* ovf = at<int>(ws, L.off_cslot);            // n ints, likewise
+  const int vec4 = ((d & 3) == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0) ? 1 : 0;
+  hipLaunchKernelGGL(k_prep_class, dim3(k), dim3(64), 0, st, w, mu, var, d, cls, cwell, cdir,
+                     cthr);
+  hipLaunchKernelGGL(k_prep_scan, dim3(1), dim3(256), 0, st, cls, k, well_idx, ill_idx, counts);
+  {
+    const int64_t tot = (int64_t)kpad * (D64 / 4) * 2;
+    hipLaunchKernelGGL(k_prep_pack_well<D64>, dim3((unsigned)cdiv(tot, 256)), dim3(256), 0, st,
+                       mu, var, d, kpad, cwell, cthr, counts, well_idx, wp, cw, thr);
+    const int64_t toti = (int64_t)k * D64;
+    hipLaunchKernelGGL(k_prep_pack_direct<D64>, dim3((unsigned)cdiv(toti, 256)), dim3(256), 0,
+                       st, mu, var, d, k, cdir, dmu, dh, dc);
+  }
+  hipLaunchKernelGGL(k_assign_theta<D64>, dim3((unsigned)L.n_wg_logz), dim3(256), 0, st, x, n, d,
+                     vec4, wp, cw, counts, m + 2, theta);
+  hipLaunchKernelGGL(k_assign_collect<D64>, dim3((unsigned)L.n_wg_logz), dim3(256), 0, st, x, n,
+                     d, vec4, wp, cw, well_idx, ill_idx, dmu, dh, dc, counts, theta, mu, var,
+                     cdir, m, tau, idx, resp, ovf);
+  hipLaunchKernelGGL(k_assign_fallback, dim3((unsigned)cdiv(n, 1024)), dim3(256), 0, st, x, n, d,
+                     k, mu, var, cdir, m, tau, ovf, idx, resp);
+  return launch_status();
+}
+
 int estep_dispatch(const Layout& L, const float* x, const float* w, const float* mu,
                    const float* var, double* nk, double* s, double* q, double* loglik,
                    int ll_accumulate, void* ws, hipStream_t st) {
@@ -1393,9 +1811,22 @@ int gmm_fit(const float* x, int64_t n, int32_t d, int32_t k, int32_t n_iters, fl
 int gmm_assign_topk(const float* x, int64_t n, int32_t d, int32_t k, const float* weights,
                     const float* means, const float* vars, int32_t m, float tau, int32_t* idx,
                     float* resp, void* ws, size_t ws_bytes, hipStream_t stream) {
-  (void)x; (void)n; (void)d; (void)k; (void)weights; (void)means; (void)vars; (void)m;
-  (void)tau; (void)idx; (void)resp; (void)ws; (void)ws_bytes; (void)stream;
-  return GMM_ERR_UNSUPPORTED;
+  int rc = check_shape(n, d, k);
+  if (rc != GMM_OK) return rc;
+  if (m > GMM_MAX_M) return GMM_ERR_UNSUPPORTED;
+  if (!x || !weights || !means || !vars || !idx || !resp) return GMM_ERR_INVALID_ARG;
+  if (m < 1 || m > k || !(tau >= 0.0f && tau < 1.0f)) return GMM_ERR_INVALID_ARG;
+  Layout L;
+  if (!make_layout(n, d, k, m, &L)) return GMM_ERR_UNSUPPORTED;
+  rc = check_ws(L, ws, ws_bytes);
+  if (rc != GMM_OK) return rc;
+  switch (L.D64) {
+    case 64: return assign_impl<64>(L, x, weights, means, vars, m, tau, idx, resp, ws, stream);
+    case 128: return assign_impl<128>(L, x, weights, means, vars, m, tau, idx, resp, ws, stream);
+    case 192: return assign_impl<192>(L, x, weights, means, vars, m, tau, idx, resp, ws, stream);
+    case 256: return assign_impl<256>(L, x, weights, means, vars, m, tau, idx, resp, ws, stream);
+    default: return GMM_ERR_UNSUPPORTED;
+  }
 }
 
 }  // extern "C"

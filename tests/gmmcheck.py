@@ -100,3 +100,66 @@ def check_params(w, mu, var, ref, n_total, label=""):
     assert err_v.max() <= TOL_VAR, (f"{label} vars: {err_v.max():.3e} at {i} "
                                     f"(gpu {var[i]}, ref {ref['vars'][i]}, Nk {nk_ref[i[0]]})")
     return f"mu {err_mu.max():.2e} var {err_v.max():.2e}"
+
+
+# ---- top-m assignment (Sec. 4.2 / 4.3)
+MARGIN = 1e-6   # an index must match where the checker's top-m margin exceeds this
+TOL_RESP = 1e-4
+
+
+def gpu_assign(x, w, mu, var, m, tau, xd=None, ws=None):
+    import torch
+    import paper_2606_10896_amd as gmm
+    if xd is None:
+        (xd,) = to_dev(x)
+    n, d = xd.shape
+    k = w.shape[0]
+    wd, mud, vd = to_dev(w, mu, var)
+    idx = torch.full((n, m), -7, dtype=torch.int32, device="cuda")
+    resp = torch.full((n, m), -7.0, dtype=torch.float32, device="cuda")
+    if ws is None:
+        ws = gmm.workspace(n, d, k, m)
+    gmm.gmm_assign_topk(xd, wd, mud, vd, m, tau, idx, resp, ws)
+    torch.cuda.synchronize()
+    return idx.cpu().numpy(), resp.cpu().numpy()
+
+
+def check_assign(gidx, gresp, ref, m, tau, label="", min_checked=0.9):
+    """ref = oracle.assign_topk(..., mr=m+1).  Rank j of point i is checked where its margin
+    min(r_(j-1) - r_(j), r_(j) - r_(j+1)) in the checker's fp64 responsibilities exceeds MARGIN
+    (r_(0) = +inf) and, for j > 0, |r_(j) - tau| > MARGIN: there the index must be identical and
+    the responsibility within TOL_RESP (an empty slot is -1 / 0 on both sides).  At least
+    min_checked of the rank-1 entries must be decisive (later ranks often are not: two
+    responsibilities below 1e-6 differ by less than the margin).  Returns the fraction of all
+    (point, rank) pairs checked."""
+    idx, resp, ridx, rresp = ref
+    n = idx.shape[0]
+    assert gidx.shape == (n, m) and gresp.shape == (n, m)
+    rp = np.concatenate([np.full((n, 1), np.inf), rresp], axis=1)   # r_(0) = +inf
+    checked = 0
+    checked0 = 0
+    bad = []
+    for j in range(m):
+        r = rp[:, j + 1]
+        margin = np.minimum(rp[:, j] - r, r - rp[:, j + 2])
+        ok = margin > MARGIN
+        if j > 0:
+            ok &= np.abs(r - tau) > MARGIN
+        sel = np.nonzero(ok)[0]
+        checked += sel.size
+        if j == 0:
+            checked0 = sel.size
+        wrong = sel[gidx[sel, j] != idx[sel, j]]
+        if wrong.size:
+            i = wrong[0]
+            bad.append(f"rank {j}: {wrong.size} index mismatches, e.g. point {i}: gpu "
+                       f"{gidx[i]} ref {idx[i]} r {rresp[i]}")
+        same = sel[gidx[sel, j] == idx[sel, j]]
+        err = np.abs(gresp[same, j].astype(np.float64) - resp[same, j].astype(np.float64))
+        if err.size and err.max() > TOL_RESP:
+            i = same[err.argmax()]
+            bad.append(f"rank {j}: resp err {err.max():.3e} at point {i}")
+    assert not bad, f"{label}: " + "; ".join(bad)
+    assert checked0 >= min_checked * n, \
+        f"{label}: only {checked0 / n:.3f} of the rank-1 entries are decisive"
+    return checked / (n * m)

@@ -1,0 +1,104 @@
+"""GPU parity of gmm_assign_topk (Sec. 4.2 single assignment, Sec. 4.3 multiple
+assignment) against the fp64 checker: indices identical wherever the checker's
+top-m margin exceeds 1e-6, responsibilities within 1e-4."""
+import sys
+
+import numpy as np
+import pytest
+
+import gmm_synth as g
+import oracle
+from gmmcheck import check_assign, gpu_assign
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _run(x, th, m, tau, label, min_checked=0.9):
+    ref = oracle.assign_topk(x, *th, m, tau, mr=m + 1)
+    gidx, gresp = gpu_assign(x, *th, m, tau)
+    frac = check_assign(gidx, gresp, ref, m, tau, label, min_checked)
+    kept = (gidx >= 0).sum(axis=0)
+    _say(f"  {label}: checked {frac:.4f} of ranks, kept per rank {kept.tolist()}")
+    return gidx, gresp
+
+
+def test_tiny_trained():
+    """The paper's setting: m = 2, tau = 1/K, at parameters after a few EM iterations."""
+    x, th0 = g.make("tiny")
+    f = oracle.fit(x, *th0, 5, keep_thetas=True)
+    th = f["thetas"][-1]
+    _run(x, th, 2, 1.0 / 8, "tiny m2")
+
+
+@pytest.mark.parametrize("n,d,kt,k,m", [
+    (1000, 37, 6, 45, 2), (3001, 128, 40, 64, 3), (2049, 200, 10, 17, 1), (777, 256, 8, 8, 8),
+    (5, 3, 2, 2, 2), (1500, 150, 7, 40, 4), (20000, 8, 4, 300, 2)])
+def test_ragged_shapes(n, d, kt, k, m):
+    w = g.custom(f"a{n}_{d}_{k}", n, d, kt, k, data_seed=n + d, init_seed=k + 17)
+    x, (wt, mu, var) = g.make(w)
+    var = np.where(var > 0, var, np.float32(1.0)).astype(np.float32)
+    f = oracle.fit(x, wt, mu, var, 2, keep_thetas=True)
+    _run(x, f["thetas"][-1], m, 1.0 / k, f"n{n} d{d} k{k} m{m}", min_checked=0.9)
+
+
+def test_small_paper_shape():
+    """N = 5000 rows of the paper-shape small workload, K = 1024, at Theta_0 and Theta_2."""
+    x, th0 = g.make(g.custom("s5k", 5000, 128, 1024, 1024, data_seed=2, init_seed=1002))
+    _run(x, th0, 2, 1.0 / 1024, "small Theta_0", min_checked=0.9)
+    f = oracle.fit(x, *th0, 2, keep_thetas=True)
+    _run(x, f["thetas"][-1], 2, 1.0 / 1024, "small Theta_2", min_checked=0.9)
+
+
+def test_tau_zero_and_m_one():
+    x, th0 = g.make("tiny")
+    f = oracle.fit(x, *th0, 3, keep_thetas=True)
+    gidx, _ = _run(x, f["thetas"][-1], 3, 0.0, "tau 0")
+    gidx1, gresp1 = _run(x, f["thetas"][-1], 1, 0.5, "m 1")
+    assert np.all(gidx1[:, 0] >= 0) and np.all(gresp1[:, 0] > 0)
+
+
+def test_collapsed_and_dead_components():
+    w = g.custom("acol", 6000, 64, 12, 40, data_seed=5, init_seed=55)
+    x, (wt, mu, var) = g.make(w)
+    rng = np.random.default_rng(0)
+    var = var.copy()
+    mu = mu.copy()
+    for c in rng.choice(40, 10, replace=False):
+        var[c] = rng.uniform(1e-5, 1e-3, var.shape[1]).astype(np.float32)
+        mu[c] = x[rng.integers(0, x.shape[0])] + np.float32(1e-3)
+    wt = wt.copy()
+    wt[[3, 9]] = 0.0
+    wt = (wt / wt.sum()).astype(np.float32)
+    gidx, _ = _run(x, (wt, mu, var), 2, 1.0 / 40, "collapsed+dead", min_checked=0.9)
+    assert not np.isin(gidx, [3, 9]).any()
+
+
+def test_many_equal_candidates_take_the_exact_path():
+    """Forty copies of one component (plus a few others): every point has more candidates than
+    the collection pass keeps, so the exact all-component path must produce the ranking, ties
+    going to the lower index."""
+    w = g.custom("adup", 2000, 16, 4, 48, data_seed=9, init_seed=99)
+    x, (wt, mu, var) = g.make(w)
+    mu = mu.copy()
+    var = var.copy()
+    mu[:40] = mu[0]
+    var[:40] = var[0]
+    wt = np.full(48, 1.0 / 48, dtype=np.float32)
+    _run(x, (wt, mu, var), 4, 1e-4, "duplicates", min_checked=0.0)
+    gidx, gresp = gpu_assign(x, wt, mu, var, 4, 1e-4)
+    ref = oracle.assign_topk(x, wt, mu, var, 4, 1e-4)
+    # exact ties among the copies: the order is fixed by the index rule, so everything matches
+    np.testing.assert_array_equal(gidx, ref[0])
+    np.testing.assert_allclose(gresp, ref[1], atol=1e-6)
+
+
+def test_deterministic():
+    x, th0 = g.make("tiny")
+    a = gpu_assign(x, *th0, 2, 0.125)
+    b = gpu_assign(x, *th0, 2, 0.125)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])

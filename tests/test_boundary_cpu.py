@@ -83,3 +83,23 @@ def test_host_validation_returns_before_any_launch():
     assert lib.gmm_mstep(p, p, p, 0.0, 8, 4, 1e-6, p, p, p, None) == gmm.GMM_ERR_INVALID_ARG
     assert lib.gmm_mstep(p, p, p, 10.0, 8, 4, -1.0, p, p, p, None) == gmm.GMM_ERR_INVALID_ARG
     assert lib.gmm_mstep(None, p, p, 10.0, 8, 4, 1e-6, p, p, p, None) == gmm.GMM_ERR_INVALID_ARG
+
+
+def test_assign_host_validation():
+    lib = gmm.load_library()
+    p, ws = _fake(), _fake(0x200000)
+    big = gmm.workspace_bytes(1000, 8, 4, 2)
+    call = lambda m, tau, **kw: lib.gmm_assign_topk(
+        kw.get("x", p), kw.get("n", 1000), kw.get("d", 8), kw.get("k", 4), p, p, p, m,
+        ctypes.c_float(tau), kw.get("idx", p), p, kw.get("ws", ws), kw.get("wsb", big), None)
+    assert call(9, 0.1) == gmm.GMM_ERR_UNSUPPORTED            # m > GMM_MAX_M
+    assert call(0, 0.1) == gmm.GMM_ERR_INVALID_ARG            # m < 1
+    assert call(5, 0.1) == gmm.GMM_ERR_INVALID_ARG            # m > k
+    assert call(2, -0.1) == gmm.GMM_ERR_INVALID_ARG           # tau < 0
+    assert call(2, 1.0) == gmm.GMM_ERR_INVALID_ARG            # tau >= 1
+    assert call(2, float("nan")) == gmm.GMM_ERR_INVALID_ARG
+    assert call(2, 0.1, idx=None) == gmm.GMM_ERR_INVALID_ARG
+    assert call(2, 0.1, d=300) == gmm.GMM_ERR_UNSUPPORTED
+    assert call(2, 0.1, n=0) == gmm.GMM_ERR_INVALID_ARG
+    assert call(2, 0.1, ws=None) == gmm.GMM_ERR_WORKSPACE
+    assert call(2, 0.1, wsb=big - 1) == gmm.GMM_ERR_WORKSPACE
