@@ -100,6 +100,41 @@ def cpu_baseline(w, mix, theta, sample_rows):
                       f"of the same data at Theta_0, {dt:.2f} s wall, scaled by N/{sample_rows}"}
 
 
+COPY_BYTES = 2 << 30
+
+
+def calibrate_copy():
+    """One device-to-device copy of COPY_BYTES: reads and writes exactly that many bytes, the
+    scale for FETCH_SIZE / WRITE_SIZE."""
+    import torch
+    a = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": COPY_BYTES}), flush=True)
+
+
+def source_digest():
+    import hashlib
+    src = os.path.join(ROOT, "paper_2606_10896_amd", "csrc", "flashgmm.hip")
+    with open(src, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic(workload):
+    """HBM bytes per gmm_estep_accumulate call from the committed counter runs
+    (profiles/estep_traffic_<workload>.json), or None when the kernels have changed since."""
+    path = os.path.join(ROOT, "profiles", f"estep_traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("source_sha256") != source_digest():
+        return None
+    return t.get("bytes_per_call")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -108,7 +143,13 @@ def main():
     ap.add_argument("--workload", default="large")
     ap.add_argument("--cpu-sample", type=int, default=100_000,
                     help="rows of the CPU-baseline slice (0 = skip)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only copy a 2 GiB device buffer once (the reference for the HBM byte "
+                         "counters) and exit")
     args = ap.parse_args()
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: --gpus {args.gpus} is not supported "
               "(the hot path is single-GPU; sharding is described, not built)", file=sys.stderr)
@@ -181,7 +222,7 @@ def main():
         "roofline": {"bound": "mfma", "kernel": "gmm_estep_accumulate (fused E-step + statistics)",
                      "achieved": round(achieved, 2), "peak": FP32_MFMA_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / FP32_MFMA_PEAK_TFLOPS, 4),
-                     "traffic": None, "estep_ms": round(estep_ms, 3),
+                     "traffic": measured_traffic(w.name), "estep_ms": round(estep_ms, 3),
                      "whole_iteration_frac": round(flops / (ms_step * 1e-3) / 1e12
                                                    / FP32_MFMA_PEAK_TFLOPS, 4)},
         "cpu_baseline": None,

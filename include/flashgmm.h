@@ -39,7 +39,7 @@ extern "C" {
 #endif
 
 #define GMM_MAX_D 256
-#define GMM_MAX_K 65536
+#define GMM_MAX_K 65535
 #define GMM_MAX_M 8
 
 typedef enum {

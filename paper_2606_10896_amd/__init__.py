@@ -21,7 +21,7 @@ GMM_ERR_UNSUPPORTED = -2
 GMM_ERR_WORKSPACE = -3
 GMM_ERR_DEVICE = -4
 GMM_MAX_D = 256
-GMM_MAX_K = 65536
+GMM_MAX_K = 65535
 GMM_MAX_M = 8
 
 #: every symbol the C ABI exports

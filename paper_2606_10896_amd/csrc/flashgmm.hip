@@ -53,7 +53,10 @@ constexpr double kLog2Pi = 1.8378770664093454835606594728112;  // log(2 pi)
 // the fp32 expanded form is good to ~1e-2 in log2 units, plenty for screening
 constexpr double kIllSum = 2.0e5;
 constexpr int kT = 4;                   // exact responsibilities stored per point
-constexpr int kFlush = 64;              // k_stats_well: fp32 -> fp64 every 64 iterations
+constexpr int kFlush = 128;             // k_stats_well: fp32 -> fp64 every 128 iterations
+// Refined lists store component slots as 16-bit values; kNoSlot marks an
+// empty entry (slots are < k <= GMM_MAX_K = 65535).
+constexpr unsigned short kNoSlot = 0xFFFF;
 // Refinement rule of k_logz.  A screened term r (relative to the screening
 // normaliser) is recomputed exactly when r > 2^-window, with window = 40 for
 // components whose fp32 expanded-form error bound (about 4 u log2(e) (e + d),
@@ -429,8 +432,8 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_logz(
     const float* __restrict__ cw, const float* __restrict__ thr,
     const int* __restrict__ well_idx, const int* __restrict__ ill_idx,
     const float* __restrict__ dmu, const float* __restrict__ dh, const float* __restrict__ dc,
-    const int* __restrict__ counts, float* __restrict__ logz2, int* __restrict__ cslot,
-    float* __restrict__ cr, double* __restrict__ ll_part) {
+    const int* __restrict__ counts, float* __restrict__ logz2,
+    unsigned short* __restrict__ cslot, float* __restrict__ cr, double* __restrict__ ll_part) {
   constexpr int P = D64 + 4;
   __shared__ __align__(16) float xs[64 * P];
   __shared__ float2 stw[4][64];      // per wave: merged well state (M_w, S_w) per point
@@ -607,7 +610,7 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_logz(
       contrib = (double)lz;
 #pragma unroll
       for (int j = 0; j < kT; ++j) {
-        cslot[nn * kT + j] = tsl[j];
+        cslot[nn * kT + j] = tsl[j] >= 0 ? (unsigned short)tsl[j] : kNoSlot;
         cr[nn * kT + j] = tsl[j] >= 0 ? exp2_fast(tl[j] - lz) : 0.0f;
       }
     }
@@ -646,7 +649,7 @@ template <int D64>
 __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
     const float* __restrict__ x, int64_t n, int d, int vec4, const float* __restrict__ wq,
     const float* __restrict__ cw, const int* __restrict__ counts,
-    const float* __restrict__ logz2, const int* __restrict__ cslot, int nch,
+    const float* __restrict__ logz2, const unsigned short* __restrict__ cslot, int nch,
     int64_t chunk_pts, double* __restrict__ part) {
   constexpr int P = D64 + 4;
   constexpr int NS = D64 / 4;                   // MFMA steps per chain
@@ -707,11 +710,11 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
       prb = 0ull;
       if (nn < p1) {
         plz = logz2[nn];
-        const int4 sl = *reinterpret_cast<const int4*>(cslot + nn * kT);
+        const ushort4 sl = *reinterpret_cast<const ushort4*>(cslot + nn * kT);
         const int v4[4] = {sl.x, sl.y, sl.z, sl.w};
 #pragma unroll
         for (int j = 0; j < kT; ++j)
-          if (v4[j] >= 0 && v4[j] / kWB == kb) prb |= 1ull << (v4[j] % kWB);
+          if (v4[j] != kNoSlot && v4[j] / kWB == kb) prb |= 1ull << (v4[j] % kWB);
       }
     }
   };
@@ -848,8 +851,8 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
 template <int D64>
 __global__ __launch_bounds__(256) void k_stats_sparse(
     const float* __restrict__ x, int64_t n, int d, const int* __restrict__ counts,
-    const int* __restrict__ cslot, const float* __restrict__ cr, int nch, int64_t chunk_pts,
-    double* __restrict__ part) {
+    const unsigned short* __restrict__ cslot, const float* __restrict__ cr, int nch,
+    int64_t chunk_pts, double* __restrict__ part) {
   constexpr int STRIDE = 1 + 2 * D64, NCI = (STRIDE + 63) / 64, NB = 32, G = 2;
   constexpr int GL = NB * D64 / 256;            // gathered values per thread and batch
   __shared__ float xb[2][NB * D64];
@@ -865,22 +868,32 @@ __global__ __launch_bounds__(256) void k_stats_sparse(
   for (int j = 0; j < 8; ++j)
 #pragma unroll
     for (int i = 0; i < NCI; ++i) acc[j][i] = 0.0;
-  int4 sl[G];
-  float4 rr[G];
-  auto load_lists = [&](int64_t base) {
+  // three-stage prefetch over groups of G*256 points: while group g is staged,
+  // the responsibilities of group g+1 (only for points with a pair in this
+  // block, known from its slots) and the slots of group g+2 are in flight
+  auto in_block = [&](int v) { return v >= 0 && (v >> 5) == kb; };
+  int4 sl[G], sl1[G], sl2[G];
+  float4 rr[G], rr1[G];
+  auto load_slots = [&](int64_t base, int4* dst) {
 #pragma unroll
     for (int u = 0; u < G; ++u) {
       const int64_t nn = base + u * 256 + tid;
+      dst[u] = make_int4(-1, -1, -1, -1);
       if (nn < p1) {
-        sl[u] = *reinterpret_cast<const int4*>(cslot + nn * kT);
-        rr[u] = *reinterpret_cast<const float4*>(cr + nn * kT);
-      } else {
-        sl[u] = make_int4(-1, -1, -1, -1);
-        rr[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+        const ushort4 s4 = *reinterpret_cast<const ushort4*>(cslot + nn * kT);
+        dst[u] = make_int4(s4.x == kNoSlot ? -1 : s4.x, s4.y == kNoSlot ? -1 : s4.y,
+                           s4.z == kNoSlot ? -1 : s4.z, s4.w == kNoSlot ? -1 : s4.w);
       }
     }
   };
-  auto in_block = [&](int v) { return v >= 0 && (v >> 5) == kb; };
+  auto load_resp = [&](int64_t base, const int4* src, float4* dst) {
+#pragma unroll
+    for (int u = 0; u < G; ++u) {
+      dst[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (in_block(src[u].x) || in_block(src[u].y) || in_block(src[u].z) || in_block(src[u].w))
+        dst[u] = *reinterpret_cast<const float4*>(cr + (base + u * 256 + tid) * kT);
+    }
+  };
   float gv[GL];
   // rows of the staged pairs b0 .. b0+nb-1 into registers (column c of pair e
   // is value i = e * D64 + c, thread tid takes i = tid + 256 j)
@@ -893,7 +906,9 @@ __global__ __launch_bounds__(256) void k_stats_sparse(
       gv[j] = v;
     }
   };
-  if (p0 < p1) load_lists(p0);
+  load_slots(p0, sl);
+  load_resp(p0, sl, rr);
+  load_slots(p0 + G * 256, sl1);
   int buf = 0;
   for (int64_t base = p0; base < p1; base += G * 256) {
     int mine[G];
@@ -934,7 +949,15 @@ __global__ __launch_bounds__(256) void k_stats_sparse(
           stage[q++] = make_int2(((u * 256 + tid) << 5) | (vs[j] & 31), __float_as_int(rs[j]));
       }
     }
-    if (base + G * 256 < p1) load_lists(base + G * 256);
+    // advance the prefetch pipeline (loads past the chunk end return empty lists)
+    load_resp(base + G * 256, sl1, rr1);
+    load_slots(base + 2 * G * 256, sl2);
+#pragma unroll
+    for (int u = 0; u < G; ++u) {
+      sl[u] = sl1[u];
+      sl1[u] = sl2[u];
+      rr[u] = rr1[u];
+    }
     if (total == 0) continue;
     __syncthreads();                            // stage complete
     gather(base, 0, total < NB ? total : NB);
@@ -1580,7 +1603,8 @@ bool make_layout(int64_t n, int d, int k, int m, Layout* L) {
   L->off_dh = take((size_t)k * L->D64 * sizeof(float));
   L->off_dc = take((size_t)k * sizeof(float));
   L->off_logz2 = take((size_t)n * sizeof(float));
-  L->off_cslot = take((size_t)n * kT * sizeof(int));
+  // refined slots (16-bit); gmm_assign_topk reuses the region for n int flags
+  L->off_cslot = take((size_t)n * kT * sizeof(unsigned short));
   L->off_cr = take((size_t)n * kT * sizeof(float));
   L->off_llpart = take((size_t)L->n_wg_logz * sizeof(double));
   L->off_part_w = take((size_t)nwb * L->nch * kWB * (1 + 2 * (size_t)L->D64) * sizeof(double));
@@ -1621,7 +1645,7 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
   float* dmu = at<float>(ws, L.off_dmu);
   float* dh = at<float>(ws, L.off_dh);
   float* dc = at<float>(ws, L.off_dc);
-  int* cslot = at<int>(ws, L.off_cslot);
+  unsigned short* cslot = at<unsigned short>(ws, L.off_cslot);
   float* cr = at<float>(ws, L.off_cr);
   float* logz2 = at<float>(ws, L.off_logz2);
   double* llpart = at<double>(ws, L.off_llpart);
