@@ -61,9 +61,10 @@ constexpr unsigned short kNoSlot = 0xFFFF;
 // normaliser) is recomputed exactly when r > 2^-window, with window = 40 for
 // components whose fp32 expanded-form error bound (about 4 u log2(e) (e + d),
 // e = sum mu^2 / var) exceeds 2^-12 log2 units, and window = 10 for the others,
-// whose screened terms are already good to that bound.  Tight components need
-// the wide window: far points with small r still carry a measurable share of
-// their variance.
+// whose screened terms are already good to that bound; and, within 2^-40,
+// whenever its lane state is among the point's four largest.  The exact
+// top-kT list then holds a point's largest pairs even when they are tiny:
+// those pairs carry the variance of a component that sits on a few points.
 constexpr double kWideWindow = 40.0;
 constexpr double kNarrowWindow = 10.0;
 constexpr double kLooseBound = -12.0;
@@ -298,29 +299,55 @@ __global__ __launch_bounds__(256) void k_prep_pack_well(
   }
 }
 
-// Packed 16x16x4 operand of k_stats_well: wq[(g * D64/2 + s) * 64 + lane] is,
+// Packed 16x16x4 operand of k_stats_well: wq[(g * WQS + s) * 64 + lane] is,
 // for 16-component group g and lane l, component slot 16g + l%16 at step s:
 // W of dimension 16(s/4) + 4(l/16) + s%4 for s < D64/4, P of that dimension
-// (s - D64/4 in place of s) above.  Same fp64 -> fp32 values as wp.
+// (s - D64/4 in place of s) for s < D64/2 (same fp64 -> fp32 values as wp),
+// then for each 32-dimension group b the bias step s = D64/2 + b: 1 in lane
+// group l/16 = 0, the group's share of the log-density constant,
+// log2(e) (log pi / NGB - 1/2 sum over its dimensions of (mu^2/var + log 2 pi var)),
+// in lane group 1, and 0 in the others (-inf for a dead or padded slot).
+constexpr int wq_steps(int D64) { return D64 / 2 + D64 / 32; }
+
 template <int D64>
 __global__ __launch_bounds__(256) void k_prep_pack_w16(
-    const float* __restrict__ mu, const float* __restrict__ var, int d, int kpad,
-    const int* __restrict__ counts, const int* __restrict__ well_idx, float* __restrict__ wq) {
-  constexpr int NS = D64 / 4;
+    const float* __restrict__ w, const float* __restrict__ mu, const float* __restrict__ var,
+    int d, int kpad, const int* __restrict__ counts, const int* __restrict__ well_idx,
+    float* __restrict__ wq) {
+  constexpr int NS = D64 / 4, NGB = D64 / 32, WQS = wq_steps(D64);
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= (int64_t)kpad * 2 * D64) return;     // (kpad/16) groups * 2NS steps * 64 lanes
+  if (t >= (int64_t)(kpad / 16) * WQS * 64) return;
   const int lane = (int)(t & 63);
-  const int s = (int)((t >> 6) % (2 * NS));
-  const int g = (int)((t >> 6) / (2 * NS));
+  const int s = (int)((t >> 6) % WQS);
+  const int g = (int)((t >> 6) / WQS);
   const int slot = g * 16 + (lane & 15);
   const int comp = slot < counts[0] ? well_idx[slot] : -1;
-  const bool xpart = s < NS;
-  const int ss = xpart ? s : s - NS;
-  const int j = 16 * (ss / 4) + 4 * (lane >> 4) + ss % 4;
   float v = 0.0f;
-  if (comp >= 0 && j < d) {
-    const double m = mu[(int64_t)comp * d + j], s2 = var[(int64_t)comp * d + j];
-    v = xpart ? (float)(kLog2e * m / s2) : (float)(-0.5 * kLog2e / s2);
+  if (s < 2 * NS) {
+    const bool xpart = s < NS;
+    const int ss = xpart ? s : s - NS;
+    const int j = 16 * (ss / 4) + 4 * (lane >> 4) + ss % 4;
+    if (comp >= 0 && j < d) {
+      const double m = mu[(int64_t)comp * d + j], s2 = var[(int64_t)comp * d + j];
+      v = xpart ? (float)(kLog2e * m / s2) : (float)(-0.5 * kLog2e / s2);
+    }
+  } else {
+    const int b = s - 2 * NS, lg = lane >> 4;
+    if (lg == 0) {
+      v = 1.0f;
+    } else if (lg == 1) {
+      const double wk = comp >= 0 ? (double)w[comp] : 0.0;
+      if (!(wk > 0.0)) {
+        v = -INFINITY;
+      } else {
+        double e = 0.0;
+        for (int j = 32 * b; j < 32 * b + 32 && j < d; ++j) {
+          const double m = mu[(int64_t)comp * d + j], s2 = var[(int64_t)comp * d + j];
+          e += m * m / s2 + kLog2Pi + log(s2);
+        }
+        v = (float)(kLog2e * (log(wk) / NGB - 0.5 * e));
+      }
+    }
   }
   wq[t] = v;
 }
@@ -440,6 +467,8 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_logz(
   __shared__ float2 sti[4][64];      // per wave: ill state per point
   __shared__ float cms[4][64];       // per wave: candidate mass relative to M_w
   __shared__ float lzm[64];          // screening log2 Z
+  __shared__ float2 top2[4][64];     // per wave: the two largest lane-state maxima per point
+  __shared__ float s4m[64];          // lower bound of the 4th largest lane-state maximum
   __shared__ unsigned cmask[64][4];  // candidate lane columns per (point, wave)
   __shared__ unsigned short cidx[64][128];  // arg-max well slot per (point, lane state)
   __shared__ float2 rmc[4][64];      // per (wave, point): exact candidate LSE state
@@ -494,13 +523,23 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_logz(
     cidx[p][wave * 32 + col] = (unsigned short)a0[v];
     cidx[32 + p][wave * 32 + col] = (unsigned short)a1[v];
     float M0 = m0[v], S0 = s0[v], M1 = m1[v], S1 = s1[v];
+    // the two largest lane-state maxima of the wave (A >= B)
+    float A0 = m0[v], B0 = kEmpty, A1 = m1[v], B1 = kEmpty;
     for (int off = 16; off > 0; off >>= 1) {
       lse_merge(M0, S0, __shfl_xor(M0, off), __shfl_xor(S0, off));
       lse_merge(M1, S1, __shfl_xor(M1, off), __shfl_xor(S1, off));
+      const float pa0 = __shfl_xor(A0, off), pb0 = __shfl_xor(B0, off);
+      const float pa1 = __shfl_xor(A1, off), pb1 = __shfl_xor(B1, off);
+      B0 = fmaxf(fminf(A0, pa0), fmaxf(B0, pb0));
+      A0 = fmaxf(A0, pa0);
+      B1 = fmaxf(fminf(A1, pa1), fmaxf(B1, pb1));
+      A1 = fmaxf(A1, pa1);
     }
     if (col == 0) {
       stw[wave][p] = make_float2(M0, S0);
       stw[wave][32 + p] = make_float2(M1, S1);
+      top2[wave][p] = make_float2(A0, B0);
+      top2[wave][32 + p] = make_float2(A1, B1);
     }
   }
   // ill-conditioned components, direct form, lane = point
@@ -520,6 +559,22 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_logz(
       lse_merge(mm, ss, sti[w2][tid].x, sti[w2][tid].y);
     }
     lzm[tid] = mm + __log2f(ss);
+    // a lower bound of the 4th largest lane-state maximum: the 4th largest of
+    // the waves' two largest (eight distinct lane states)
+    float t4[4] = {kEmpty, kEmpty, kEmpty, kEmpty};
+    for (int w2 = 0; w2 < 4; ++w2) {
+      const float vv[2] = {top2[w2][tid].x, top2[w2][tid].y};
+      for (int u = 0; u < 2; ++u) {
+        const float v = vv[u];
+#pragma unroll
+        for (int j = 3; j > 0; --j) {
+          if (v > t4[j - 1]) t4[j] = t4[j - 1];
+          else if (v > t4[j]) t4[j] = v;
+        }
+        if (v > t4[0]) t4[0] = v;
+      }
+    }
+    s4m[tid] = t4[3];
   }
   __syncthreads();
   // candidates: lane states whose maximum is within the window of the screening log2 Z
@@ -531,7 +586,11 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_logz(
       const int pp = blk * 32 + p;
       const float mv = blk ? m1[v] : m0[v];
       const int av = blk ? a1[v] : a0[v];
-      const bool cand = av >= 0 && mv - lzm[pp] > thr[av];
+      // refined: within the component's window, or among the point's four
+      // largest lane states (those fill the exact top-kT list)
+      const float rel = mv - lzm[pp];
+      const bool cand =
+          av >= 0 && (rel > thr[av] || (mv >= s4m[pp] && rel > -(float)kWideWindow));
       float term = cand ? exp2_fast(mv - stw[wave][pp].x) : 0.0f;
       for (int off = 16; off > 0; off >>= 1) term += __shfl_xor(term, off);
       const unsigned long long bal = __ballot(cand);
@@ -625,8 +684,8 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_logz(
 // log-density operand (W and P of its components, 2 * D64 values per lane in
 // the MFMA B-operand order of the packed array wq) stays in registers for the
 // whole chunk; for every 16-point tile it forms the log-densities of its
-// components (one chain: bias, x steps, x^2 steps), takes r = 2^(l - log2 Z)
-// with the refined pairs set to 0 (k_stats_sparse sums those exactly), and
+// components, takes r = 2^(l - log2 Z) with the refined pairs set to 0
+// (k_stats_sparse sums those exactly), and
 // contracts r^T [x | x^2] into fp32 accumulators (its 16 components x 2 D64
 // columns) that are folded into the workgroup's fp64 partial every kFlush
 // iterations; N_k is summed on the vector ALU.  The log-density accumulator
@@ -635,6 +694,13 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_logz(
 // 32 points per iteration, double-buffered in LDS and loaded one iteration
 // ahead, one barrier per iteration.
 //
+// The log-density chain yields l - log2 Z directly: for every group of 32
+// dimensions its x steps, its x^2 steps, then one step that adds the group's
+// share of the constant and -log2 Z / NGB (operands from the packed bias
+// steps and the point's log2 Z).  The running sum then stays near the result
+// instead of passing through values of the size of sum mu^2/var, which keeps
+// the fp32 rounding of far-from-centre pairs about ten times smaller (their
+// share of a variance can be large when a component sits on one point).
 // Orders.  Log-density step s (< D64/4) of lane l uses dimension
 // 16(s/4) + 4(l/16) + s%4, so a lane reads 4 dimensions with one float4.
 // Statistic column block c = 4g + e (x part; the x^2 part likewise) row i is
@@ -655,6 +721,8 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
   constexpr int NS = D64 / 4;                   // MFMA steps per chain
   constexpr int NG = D64 / 64;                  // float4 column groups per part
   constexpr int NB = D64 / 16;                  // 16-column blocks per part
+  constexpr int NGB = D64 / 32;                 // 32-dimension groups (bias steps)
+  constexpr int WQS = wq_steps(D64);
   constexpr int PTS = 32;                       // points per iteration (two tiles)
   constexpr int Q4 = D64 / 4;
   constexpr int LD = PTS * Q4 / 256;            // float4 per thread per X tile
@@ -677,10 +745,9 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
   }
   const int niter = (int)((p1 - p0 + PTS - 1) / PTS);
   const int grp = kb * 4 + wave;                // 16-component group
-  const float cb = cw[grp * 16 + i16];
-  float wb[2 * NS];
+  float wb[WQS];
 #pragma unroll
-  for (int s2 = 0; s2 < 2 * NS; ++s2) wb[s2] = wq[((size_t)grp * 2 * NS + s2) * 64 + lane];
+  for (int s2 = 0; s2 < WQS; ++s2) wb[s2] = wq[((size_t)grp * WQS + s2) * 64 + lane];
 
   // ---- X tile: global -> registers -> LDS
   float4 px[LD];
@@ -780,38 +847,43 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       // log-densities of points t*16 .. t*16+15 against this wave's components
-      f4v la = {cb, cb, cb, cb};
+      f4v la = {0.f, 0.f, 0.f, 0.f};
       const float* xr = &xs[cur][(t * 16 + i16) * P + 4 * k4];
-      // wide D: keep each group's operand load one group ahead and no further
-      // (hoisting all of them exhausts the registers)
+      // A operand of the bias steps: -log2 Z / NGB of row point i16 in lane
+      // group 0, 1 in lane group 1, 0 elsewhere
+      const float ab = k4 == 0 ? -lzb[cur][t * 16 + i16] * (1.0f / NGB) : (k4 == 1 ? 1.0f : 0.0f);
+      // wide D: keep each group's operand loads in their group (hoisting all
+      // of them exhausts the registers)
       constexpr bool kPin = D64 > 128;
-      float4 un = *reinterpret_cast<const float4*>(xr);
 #pragma unroll
-      for (int j = 0; j < NS / 4; ++j) {
-        const float4 u = un;
-        if (j + 1 < NS / 4) un = *reinterpret_cast<const float4*>(xr + 16 * (j + 1));
-        la = mfma16(u.x, wb[4 * j], la);
-        la = mfma16(u.y, wb[4 * j + 1], la);
-        la = mfma16(u.z, wb[4 * j + 2], la);
-        la = mfma16(u.w, wb[4 * j + 3], la);
-        if constexpr (kPin) __builtin_amdgcn_sched_barrier(0);
-      }
-      un = *reinterpret_cast<const float4*>(xr);
-#pragma unroll
-      for (int j = 0; j < NS / 4; ++j) {
-        const float4 u = un;
-        if (j + 1 < NS / 4) un = *reinterpret_cast<const float4*>(xr + 16 * (j + 1));
-        la = mfma16(u.x * u.x, wb[NS + 4 * j], la);
-        la = mfma16(u.y * u.y, wb[NS + 4 * j + 1], la);
-        la = mfma16(u.z * u.z, wb[NS + 4 * j + 2], la);
-        la = mfma16(u.w * u.w, wb[NS + 4 * j + 3], la);
+      for (int b = 0; b < NGB; ++b) {
+        const float4 u0 = *reinterpret_cast<const float4*>(xr + 32 * b);
+        const float4 u1 = *reinterpret_cast<const float4*>(xr + 32 * b + 16);
+        const int j0 = 8 * b;                   // steps of dims 32b .. 32b+31
+        la = mfma16(u0.x, wb[j0], la);
+        la = mfma16(u0.y, wb[j0 + 1], la);
+        la = mfma16(u0.z, wb[j0 + 2], la);
+        la = mfma16(u0.w, wb[j0 + 3], la);
+        la = mfma16(u1.x, wb[j0 + 4], la);
+        la = mfma16(u1.y, wb[j0 + 5], la);
+        la = mfma16(u1.z, wb[j0 + 6], la);
+        la = mfma16(u1.w, wb[j0 + 7], la);
+        la = mfma16(u0.x * u0.x, wb[NS + j0], la);
+        la = mfma16(u0.y * u0.y, wb[NS + j0 + 1], la);
+        la = mfma16(u0.z * u0.z, wb[NS + j0 + 2], la);
+        la = mfma16(u0.w * u0.w, wb[NS + j0 + 3], la);
+        la = mfma16(u1.x * u1.x, wb[NS + j0 + 4], la);
+        la = mfma16(u1.y * u1.y, wb[NS + j0 + 5], la);
+        la = mfma16(u1.z * u1.z, wb[NS + j0 + 6], la);
+        la = mfma16(u1.w * u1.w, wb[NS + j0 + 7], la);
+        la = mfma16(ab, wb[2 * NS + b], la);
         if constexpr (kPin) __builtin_amdgcn_sched_barrier(0);
       }
       float r[4];
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         const int pt = t * 16 + 4 * k4 + v;
-        const float e = exp2_fast(la[v] - lzb[cur][pt]);
+        const float e = exp2_fast(la[v]);
         r[v] = ((rbb[cur][pt] >> myc) & 1ull) ? 0.0f : e;
         nkacc += r[v];
       }
@@ -1598,7 +1670,7 @@ bool make_layout(int64_t n, int d, int k, int m, Layout* L) {
   L->off_cthr = take((size_t)k * sizeof(float));
   L->off_thr = take((size_t)L->kpad * sizeof(float));
   L->off_wp = take((size_t)L->kpad * 2 * L->D64 * sizeof(float));
-  L->off_wq = take((size_t)L->kpad * 2 * L->D64 * sizeof(float));
+  L->off_wq = take((size_t)(L->kpad / 16) * (L->D64 / 2 + L->D64 / 32) * 64 * sizeof(float));
   L->off_dmu = take((size_t)k * L->D64 * sizeof(float));
   L->off_dh = take((size_t)k * L->D64 * sizeof(float));
   L->off_dc = take((size_t)k * sizeof(float));
@@ -1661,8 +1733,9 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
     const int64_t tot = (int64_t)kpad * (D64 / 4) * 2;
     hipLaunchKernelGGL(k_prep_pack_well<D64>, dim3((unsigned)cdiv(tot, 256)), dim3(256), 0, st,
                        mu, var, d, kpad, cwell, cthr, counts, well_idx, wp, cw, thr);
-    hipLaunchKernelGGL(k_prep_pack_w16<D64>, dim3((unsigned)cdiv((int64_t)kpad * 2 * D64, 256)),
-                       dim3(256), 0, st, mu, var, d, kpad, counts, well_idx, wq);
+    hipLaunchKernelGGL(k_prep_pack_w16<D64>,
+                       dim3((unsigned)cdiv((int64_t)(kpad / 16) * wq_steps(D64) * 64, 256)),
+                       dim3(256), 0, st, w, mu, var, d, kpad, counts, well_idx, wq);
     const int64_t toti = (int64_t)k * D64;
     hipLaunchKernelGGL(k_prep_pack_direct<D64>, dim3((unsigned)cdiv(toti, 256)), dim3(256), 0,
                        st, mu, var, d, k, cdir, dmu, dh, dc);
