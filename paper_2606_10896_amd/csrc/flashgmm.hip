@@ -192,6 +192,34 @@ __device__ __forceinline__ float ill_logit(const float* xrow, const float* __res
   return c - acc;
 }
 
+// Same sum with a per-lane bound: the terms are >= 0, so once the partial sum
+// of a lane exceeds `bound` its log-density is below c - bound, where the
+// callers treat it as exactly nothing; such a lane returns -inf.  Every 16
+// dimensions the wave stops when all of its lanes are past their bound
+// (collapsed components are far from almost every point), so the result of a
+// lane never depends on the other lanes.
+template <int D64>
+__device__ __forceinline__ float ill_logit_bounded(const float* xrow, const float* __restrict__ mu,
+                                                   const float* __restrict__ hh, float c,
+                                                   float bound) {
+  float acc = 0.0f;
+  for (int j0 = 0; j0 < D64; j0 += 16) {
+#pragma unroll
+    for (int j = j0; j < j0 + 16; j += 4) {
+      const float4 xv = *reinterpret_cast<const float4*>(xrow + j);
+      const float4 m = *reinterpret_cast<const float4*>(mu + j);
+      const float4 g = *reinterpret_cast<const float4*>(hh + j);
+      float t;
+      t = xv.x - m.x; acc = __fmaf_rn(__fmul_rn(t, t), g.x, acc);
+      t = xv.y - m.y; acc = __fmaf_rn(__fmul_rn(t, t), g.y, acc);
+      t = xv.z - m.z; acc = __fmaf_rn(__fmul_rn(t, t), g.z, acc);
+      t = xv.w - m.w; acc = __fmaf_rn(__fmul_rn(t, t), g.w, acc);
+    }
+    if (__ballot(!(acc > bound)) == 0ull) break;
+  }
+  return acc > bound ? -INFINITY : c - acc;
+}
+
 // ---------------------------------------------------------------- prep
 // Workspace counters: [0] well components, [1] ill-conditioned components,
 // [2] well 32-blocks, [3] ill 32-blocks.
@@ -542,15 +570,23 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_logz(
       top2[wave][32 + p] = make_float2(A1, B1);
     }
   }
-  // ill-conditioned components, direct form, lane = point
-  float mi = -INFINITY, si = 0.0f;
-  for (int ki = wave; ki < n_ill; ki += 4) {
-    const int comp = ill_idx[ki];
-    const float l = ill_logit<D64>(xs + lane * P, dmu + (size_t)comp * D64,
-                                   dh + (size_t)comp * D64, dc[comp]);
-    lse_add(mi, si, l);
+  // ill-conditioned components, direct form, lane = point; a term 2^-60 below
+  // the point's largest well lane state is nothing in the sum and is not
+  // finished (a routed component that is the point's largest is finished)
+  __syncthreads();
+  {
+    float mw = kEmpty;
+    for (int w2 = 0; w2 < 4; ++w2) mw = fmaxf(mw, stw[w2][lane].x);
+    float mi = -INFINITY, si = 0.0f;
+    for (int ki = wave; ki < n_ill; ki += 4) {
+      const int comp = ill_idx[ki];
+      const float c = dc[comp];
+      const float l = ill_logit_bounded<D64>(xs + lane * P, dmu + (size_t)comp * D64,
+                                             dh + (size_t)comp * D64, c, c - (mw - 60.0f));
+      lse_add(mi, si, l);
+    }
+    sti[wave][lane] = make_float2(mi, si);
   }
-  sti[wave][lane] = make_float2(mi, si);
   __syncthreads();
   if (tid < 64) {
     float mm = -INFINITY, ss = 0.0f;
@@ -1137,8 +1173,10 @@ __global__ __launch_bounds__(256) void k_stats_ill(
       float r = 0.0f;
       if (ki < n_ill) {
         const int comp = ill_idx[ki];
-        const float l = ill_logit<D64>(xs + lane * P, dmu + (size_t)comp * D64,
-                                       dh + (size_t)comp * D64, dc[comp]);
+        const float c = dc[comp];
+        // r < 2^-150 is 0 in fp32: such pairs are not finished
+        const float l = ill_logit_bounded<D64>(xs + lane * P, dmu + (size_t)comp * D64,
+                                               dh + (size_t)comp * D64, c, c - (lzs[lane] - 150.0f));
         r = exp2_fast(l - lzs[lane]);
       }
       rs[(wave * 8 + c) * 64 + lane] = r;
