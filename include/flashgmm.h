@@ -38,7 +38,7 @@
 extern "C" {
 #endif
 
-#define GMM_MAX_D 256
+#define GMM_MAX_D 1024
 #define GMM_MAX_K 65535
 #define GMM_MAX_M 8
 

@@ -20,7 +20,7 @@ GMM_ERR_INVALID_ARG = -1
 GMM_ERR_UNSUPPORTED = -2
 GMM_ERR_WORKSPACE = -3
 GMM_ERR_DEVICE = -4
-GMM_MAX_D = 256
+GMM_MAX_D = 1024
 GMM_MAX_K = 65535
 GMM_MAX_M = 8
 

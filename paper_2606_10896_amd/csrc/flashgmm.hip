@@ -44,7 +44,7 @@
 
 namespace {
 
-constexpr int kBK = 32;                 // components per MFMA block (log-normalisers, sparse)
+constexpr int kBK = 32;                 // components per MFMA block of the screening pass
 constexpr int kWB = 64;                 // components per workgroup of k_stats_well
 constexpr double kLog2e = 1.4426950408889634073599246810019;
 constexpr double kLn2 = 0.69314718055994530941723212145818;
@@ -66,6 +66,9 @@ constexpr unsigned short kNoSlot = 0xFFFF;
 // top-kT list then holds a point's largest pairs even when they are tiny:
 // those pairs carry the variance of a component that sits on a few points.
 constexpr double kWideWindow = 40.0;
+// a lane state whose components other than its arg-max carry more than this
+// share of the point's screened mass is refined in full
+constexpr float kFullMass = 0x1p-20f;
 constexpr double kNarrowWindow = 10.0;
 constexpr double kLooseBound = -12.0;
 
@@ -172,22 +175,26 @@ __device__ __forceinline__ void load_tile(const float* __restrict__ x, int64_t n
 // screening error that both passes tolerate.
 
 // ---------------------------------------------------------------- direct-form logits (VALU)
-// l2 = c - sum_d (x_d - mu_d)^2 * hh_d, hh = log2(e) / (2 var), summed in
-// dimension order; padded dimensions have x = mu = hh = 0.
+// l2 = c - sum_d (x_d - mu_d)^2 hh_d in log2 units, hh = log2(e) / (2 var) and c
+// in fp64, summed in fp64 in dimension order; padded dimensions have
+// x = mu = hh = 0.  fp64 because with small variances or many dimensions the
+// constant and the sum reach 1e3 log2 units and more, where fp32 rounding alone
+// (of the sum, of c and of hh) would exceed the responsibility tolerances.
 template <int D64>
-__device__ __forceinline__ float ill_logit(const float* xrow, const float* __restrict__ mu,
-                                           const float* __restrict__ hh, float c) {
-  float acc = 0.0f;
+__device__ __forceinline__ double ill_logit(const float* xrow, const float* __restrict__ mu,
+                                            const double* __restrict__ hh, double c) {
+  double acc = 0.0;
 #pragma unroll 4
   for (int j = 0; j < D64; j += 4) {
     const float4 xv = *reinterpret_cast<const float4*>(xrow + j);
     const float4 m = *reinterpret_cast<const float4*>(mu + j);
-    const float4 g = *reinterpret_cast<const float4*>(hh + j);
-    float t;
-    t = xv.x - m.x; acc = __fmaf_rn(__fmul_rn(t, t), g.x, acc);
-    t = xv.y - m.y; acc = __fmaf_rn(__fmul_rn(t, t), g.y, acc);
-    t = xv.z - m.z; acc = __fmaf_rn(__fmul_rn(t, t), g.z, acc);
-    t = xv.w - m.w; acc = __fmaf_rn(__fmul_rn(t, t), g.w, acc);
+    const double2 g0 = *reinterpret_cast<const double2*>(hh + j);
+    const double2 g1 = *reinterpret_cast<const double2*>(hh + j + 2);
+    double t;
+    t = (double)xv.x - (double)m.x; acc = fma(t * t, g0.x, acc);
+    t = (double)xv.y - (double)m.y; acc = fma(t * t, g0.y, acc);
+    t = (double)xv.z - (double)m.z; acc = fma(t * t, g1.x, acc);
+    t = (double)xv.w - (double)m.w; acc = fma(t * t, g1.y, acc);
   }
   return c - acc;
 }
@@ -199,21 +206,23 @@ __device__ __forceinline__ float ill_logit(const float* xrow, const float* __res
 // (collapsed components are far from almost every point), so the result of a
 // lane never depends on the other lanes.
 template <int D64>
-__device__ __forceinline__ float ill_logit_bounded(const float* xrow, const float* __restrict__ mu,
-                                                   const float* __restrict__ hh, float c,
-                                                   float bound) {
-  float acc = 0.0f;
+__device__ __forceinline__ double ill_logit_bounded(const float* xrow,
+                                                    const float* __restrict__ mu,
+                                                    const double* __restrict__ hh, double c,
+                                                    double bound) {
+  double acc = 0.0;
   for (int j0 = 0; j0 < D64; j0 += 16) {
 #pragma unroll
     for (int j = j0; j < j0 + 16; j += 4) {
       const float4 xv = *reinterpret_cast<const float4*>(xrow + j);
       const float4 m = *reinterpret_cast<const float4*>(mu + j);
-      const float4 g = *reinterpret_cast<const float4*>(hh + j);
-      float t;
-      t = xv.x - m.x; acc = __fmaf_rn(__fmul_rn(t, t), g.x, acc);
-      t = xv.y - m.y; acc = __fmaf_rn(__fmul_rn(t, t), g.y, acc);
-      t = xv.z - m.z; acc = __fmaf_rn(__fmul_rn(t, t), g.z, acc);
-      t = xv.w - m.w; acc = __fmaf_rn(__fmul_rn(t, t), g.w, acc);
+      const double2 g0 = *reinterpret_cast<const double2*>(hh + j);
+      const double2 g1 = *reinterpret_cast<const double2*>(hh + j + 2);
+      double t;
+      t = (double)xv.x - (double)m.x; acc = fma(t * t, g0.x, acc);
+      t = (double)xv.y - (double)m.y; acc = fma(t * t, g0.y, acc);
+      t = (double)xv.z - (double)m.z; acc = fma(t * t, g1.x, acc);
+      t = (double)xv.w - (double)m.w; acc = fma(t * t, g1.y, acc);
     }
     if (__ballot(!(acc > bound)) == 0ull) break;
   }
@@ -332,9 +341,9 @@ __global__ __launch_bounds__(256) void k_prep_pack_well(
 // W of dimension 16(s/4) + 4(l/16) + s%4 for s < D64/4, P of that dimension
 // (s - D64/4 in place of s) for s < D64/2 (same fp64 -> fp32 values as wp),
 // then for each 32-dimension group b the bias step s = D64/2 + b: 1 in lane
-// group l/16 = 0, the group's share of the log-density constant,
+// groups l/16 = 0 and 2, the group's share of the log-density constant,
 // log2(e) (log pi / NGB - 1/2 sum over its dimensions of (mu^2/var + log 2 pi var)),
-// in lane group 1, and 0 in the others (-inf for a dead or padded slot).
+// in lane group 1 (-inf for a dead or padded slot), and 0 in group 3.
 constexpr int wq_steps(int D64) { return D64 / 2 + D64 / 32; }
 
 template <int D64>
@@ -375,52 +384,60 @@ __global__ __launch_bounds__(256) void k_prep_pack_w16(
         }
         v = (float)(kLog2e * (log(wk) / NGB - 0.5 * e));
       }
+    } else if (lg == 2) {
+      v = 1.0f;
     }
   }
   wq[t] = v;
 }
 
 // Direct-form parameters of every component (indexed by component):
-// dmu = mu, dh = log2(e) / (2 var), dc = log2(e) (log pi - 1/2 sum_d log(2 pi var)),
-// zero-padded to D64 dimensions.
+// dmu = mu (fp32), dh = log2(e) / (2 var) (fp64), zero-padded to D64
+// dimensions; the constant is cdir (fp64, from k_prep_class).
 template <int D64>
 __global__ __launch_bounds__(256) void k_prep_pack_direct(
     const float* __restrict__ mu, const float* __restrict__ var, int d, int k,
-    const double* __restrict__ cdir, float* __restrict__ dmu, float* __restrict__ dh,
-    float* __restrict__ dc) {
+    float* __restrict__ dmu, double* __restrict__ dh) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= (int64_t)k * D64) return;
   const int comp = (int)(t / D64), j = (int)(t % D64);
-  float m = 0.0f, g = 0.0f;
+  float m = 0.0f;
+  double g = 0.0;
   if (j < d) {
     m = mu[(int64_t)comp * d + j];
-    g = (float)(0.5 * kLog2e / (double)var[(int64_t)comp * d + j]);
+    g = 0.5 * kLog2e / (double)var[(int64_t)comp * d + j];
   }
   dmu[t] = m;
   dh[t] = g;
-  if (j == 0) dc[comp] = (float)cdir[comp];
 }
 
 // ---------------------------------------------------------------- Step 1: log-normalisers
+// Points per screening workgroup: two 32-point MFMA tiles while a 64-point X
+// tile fits in LDS next to the per-point state (D64 <= 256), one tile above.
+__host__ __device__ constexpr int logz_tiles(int D64) { return D64 <= 256 ? 2 : 1; }
+
 // One software-pipelined step of a screening pass for one wave: when MF, the
-// log-densities of 64 points (two 32-point tiles) against component block wpb
-// are formed on MFMA into n0, n1, one chain per tile: bias first, then for
+// log-densities of the NT 32-point tiles against component block wpb are
+// formed on MFMA into n0 (and n1), one chain per tile: bias first, then for
 // every group of 8 dimensions the four x steps and the four x^2 steps.  When
-// EPI, epi(v, c0[v], c1[v]) takes in the previous block's log-densities,
-// spread over the contraction so that the vector ALU work overlaps the matrix
-// work.
-template <int D64, bool MF, bool EPI, class Epi>
+// EPI, epi(v, c0[v], c1[v]) takes in the previous block's log-densities
+// (c1 = c0 when NT == 1), spread over the contraction so that the vector ALU
+// work overlaps the matrix work.
+template <int D64, bool MF, bool EPI, int NT, class Epi>
 __device__ __forceinline__ void logz_step(const float* xs, const float4* __restrict__ wpb,
                                           float cb, f16v& n0, f16v& n1, const f16v& c0,
                                           const f16v& c1, Epi&& epi) {
   constexpr int P = D64 + 4, QH = D64 / 8;
   const int lane = threadIdx.x & 63, h = lane >> 5, col = lane & 31;
   const float* xr0 = xs + col * P + 4 * h;
-  const float* xr1 = xs + (32 + col) * P + 4 * h;
+  const float* xr1 = xs + ((NT == 2 ? 32 : 0) + col) * P + 4 * h;
   float4 bw[3], bp[3];
   if (MF) {
 #pragma unroll
-    for (int v = 0; v < 16; ++v) { n0[v] = cb; n1[v] = cb; }
+    for (int v = 0; v < 16; ++v) {
+      n0[v] = cb;
+      if constexpr (NT == 2) n1[v] = cb;
+    }
     bw[0] = wpb[lane];
     bp[0] = wpb[QH * 64 + lane];
     bw[1] = wpb[64 + lane];
@@ -434,36 +451,51 @@ __device__ __forceinline__ void logz_step(const float* xs, const float4* __restr
         bp[(q + 2) % 3] = wpb[(QH + q + 2) * 64 + lane];
       }
       const float4 a = *reinterpret_cast<const float4*>(xr0 + 8 * q);
-      const float4 c = *reinterpret_cast<const float4*>(xr1 + 8 * q);
       const float4 w = bw[q % 3], pp = bp[q % 3];
-      n0 = mfma32(a.x, w.x, n0);
-      n1 = mfma32(c.x, w.x, n1);
-      n0 = mfma32(a.y, w.y, n0);
-      n1 = mfma32(c.y, w.y, n1);
-      n0 = mfma32(a.z, w.z, n0);
-      n1 = mfma32(c.z, w.z, n1);
-      n0 = mfma32(a.w, w.w, n0);
-      n1 = mfma32(c.w, w.w, n1);
-      n0 = mfma32(a.x * a.x, pp.x, n0);
-      n1 = mfma32(c.x * c.x, pp.x, n1);
-      n0 = mfma32(a.y * a.y, pp.y, n0);
-      n1 = mfma32(c.y * c.y, pp.y, n1);
-      n0 = mfma32(a.z * a.z, pp.z, n0);
-      n1 = mfma32(c.z * c.z, pp.z, n1);
-      n0 = mfma32(a.w * a.w, pp.w, n0);
-      n1 = mfma32(c.w * c.w, pp.w, n1);
+      if constexpr (NT == 2) {
+        const float4 c = *reinterpret_cast<const float4*>(xr1 + 8 * q);
+        n0 = mfma32(a.x, w.x, n0);
+        n1 = mfma32(c.x, w.x, n1);
+        n0 = mfma32(a.y, w.y, n0);
+        n1 = mfma32(c.y, w.y, n1);
+        n0 = mfma32(a.z, w.z, n0);
+        n1 = mfma32(c.z, w.z, n1);
+        n0 = mfma32(a.w, w.w, n0);
+        n1 = mfma32(c.w, w.w, n1);
+        n0 = mfma32(a.x * a.x, pp.x, n0);
+        n1 = mfma32(c.x * c.x, pp.x, n1);
+        n0 = mfma32(a.y * a.y, pp.y, n0);
+        n1 = mfma32(c.y * c.y, pp.y, n1);
+        n0 = mfma32(a.z * a.z, pp.z, n0);
+        n1 = mfma32(c.z * c.z, pp.z, n1);
+        n0 = mfma32(a.w * a.w, pp.w, n0);
+        n1 = mfma32(c.w * c.w, pp.w, n1);
+      } else {
+        n0 = mfma32(a.x, w.x, n0);
+        n0 = mfma32(a.y, w.y, n0);
+        n0 = mfma32(a.z, w.z, n0);
+        n0 = mfma32(a.w, w.w, n0);
+        n0 = mfma32(a.x * a.x, pp.x, n0);
+        n0 = mfma32(a.y * a.y, pp.y, n0);
+        n0 = mfma32(a.z * a.z, pp.z, n0);
+        n0 = mfma32(a.w * a.w, pp.w, n0);
+      }
     }
     if (EPI) {
 #pragma unroll
-      for (int v = q * 16 / QH; v < (q + 1) * 16 / QH; ++v) epi(v, c0[v], c1[v]);
+      for (int v = q * 16 / QH; v < (q + 1) * 16 / QH; ++v) {
+        if constexpr (NT == 2) epi(v, c0[v], c1[v]);
+        else epi(v, c0[v], c0[v]);
+      }
     }
     // keep each step's loads in their step (unbounded hoisting exhausts registers)
     __builtin_amdgcn_sched_barrier(0);
   }
 }
 
-// One workgroup = 64 points, 4 waves; wave w takes well component blocks w,
-// w+4, ... and ill-conditioned components w, w+4, ...
+// One workgroup = PTS = 32 NT points (64 for D64 <= 256, else 32), 4 waves;
+// wave w takes well component blocks w, w+4, ... and ill-conditioned
+// components w, w+4, ...
 //
 //   1. screen: expanded-form log-densities on MFMA with a per-lane online LSE
 //      that also remembers the arg-max; a "lane state" (wave, lane column,
@@ -486,27 +518,29 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_logz(
     const float* __restrict__ x, int64_t n, int d, int vec4, const float4* __restrict__ wp,
     const float* __restrict__ cw, const float* __restrict__ thr,
     const int* __restrict__ well_idx, const int* __restrict__ ill_idx,
-    const float* __restrict__ dmu, const float* __restrict__ dh, const float* __restrict__ dc,
-    const int* __restrict__ counts, float* __restrict__ logz2,
+    const float* __restrict__ dmu, const double* __restrict__ dh, const double* __restrict__ cdir,
+    const int* __restrict__ counts, double* __restrict__ logz2,
     unsigned short* __restrict__ cslot, float* __restrict__ cr, double* __restrict__ ll_part) {
-  constexpr int P = D64 + 4;
-  __shared__ __align__(16) float xs[64 * P];
-  __shared__ float2 stw[4][64];      // per wave: merged well state (M_w, S_w) per point
-  __shared__ float2 sti[4][64];      // per wave: ill state per point
-  __shared__ float cms[4][64];       // per wave: candidate mass relative to M_w
-  __shared__ float lzm[64];          // screening log2 Z
-  __shared__ float2 top2[4][64];     // per wave: the two largest lane-state maxima per point
-  __shared__ float s4m[64];          // lower bound of the 4th largest lane-state maximum
-  __shared__ unsigned cmask[64][4];  // candidate lane columns per (point, wave)
-  __shared__ unsigned short cidx[64][128];  // arg-max well slot per (point, lane state)
-  __shared__ float2 rmc[4][64];      // per (wave, point): exact candidate LSE state
-  __shared__ int rts[4][kT][64];     // per (wave, point): largest exact candidates
-  __shared__ float rtl[4][kT][64];
+  constexpr int P = D64 + 4, NT = logz_tiles(D64), PTS = 32 * NT;
+  __shared__ __align__(16) float xs[PTS * P];
+  __shared__ float2 stw[4][PTS];     // per wave: merged well state (M_w, S_w) per point
+  __shared__ float2 sti[4][PTS];     // per wave: ill state per point (maximum rounded to fp32)
+  __shared__ double stim[4][PTS];    // per wave: the ill state's maximum in fp64
+  __shared__ float cms[4][PTS];      // per wave: candidate mass relative to M_w
+  __shared__ float lzm[PTS];         // screening log2 Z
+  __shared__ float2 top2[4][PTS];    // per wave: the two largest lane-state maxima per point
+  __shared__ float s4m[PTS];         // lower bound of the 4th largest lane-state maximum
+  __shared__ unsigned cmask[PTS][4]; // candidate lane columns per (point, wave)
+  __shared__ unsigned fmask[PTS][4]; // of those, the lane states refined in full
+  __shared__ unsigned short cidx[PTS][128];  // arg-max well slot per (point, lane state)
+  __shared__ float2 rmc[4][PTS];     // per (wave, point): exact candidate LSE state
+  __shared__ int rts[4][kT][PTS];    // per (wave, point): largest exact candidates
+  __shared__ float rtl[4][kT][PTS];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, h = lane >> 5, col = lane & 31;
-  const int64_t n0 = (int64_t)blockIdx.x * 64;
-  load_tile<D64>(x, n, d, n0, 64, xs, vec4 != 0);
+  const int64_t n0 = (int64_t)blockIdx.x * PTS;
+  load_tile<D64>(x, n, d, n0, PTS, xs, vec4 != 0);
   __syncthreads();
-  const int n_wkb = counts[2], n_ill = counts[1];
+  const int n_wkb = counts[2], n_ill = counts[1], n_well = counts[0];
 
   float m0[16], s0[16], m1[16], s1[16];
   int a0[16], a1[16];
@@ -525,23 +559,23 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_logz(
     int slot = 0;
     auto epi = [&](int v, float l0, float l1) {
       lse_add_arg(m0[v], s0[v], a0[v], l0, slot);
-      lse_add_arg(m1[v], s1[v], a1[v], l1, slot);
+      if constexpr (NT == 2) lse_add_arg(m1[v], s1[v], a1[v], l1, slot);
     };
     if (nb > 0) {
-      logz_step<D64, true, false>(xs, wp + (size_t)wave * BS, cw[wave * kBK + col], c0, c1, x0,
-                                  x1, epi);
+      logz_step<D64, true, false, NT>(xs, wp + (size_t)wave * BS, cw[wave * kBK + col], c0, c1,
+                                      x0, x1, epi);
       float cbn = nb > 1 ? cw[(wave + 4) * kBK + col] : 0.0f;
       for (int i = 0; i + 1 < nb; ++i) {
         const int kb = wave + 4 * i;
         const float cb = cbn;
         if (i + 2 < nb) cbn = cw[(kb + 8) * kBK + col];
         slot = kb * kBK + col;
-        logz_step<D64, true, true>(xs, wp + (size_t)(kb + 4) * BS, cb, x0, x1, c0, c1, epi);
+        logz_step<D64, true, true, NT>(xs, wp + (size_t)(kb + 4) * BS, cb, x0, x1, c0, c1, epi);
         c0 = x0;
         c1 = x1;
       }
       slot = (wave + 4 * (nb - 1)) * kBK + col;
-      logz_step<D64, false, true>(xs, wp, 0.0f, x0, x1, c0, c1, epi);
+      logz_step<D64, false, true, NT>(xs, wp, 0.0f, x0, x1, c0, c1, epi);
     }
   }
   // arg-max of every lane state, and the per-wave merged state of every point
@@ -549,46 +583,60 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_logz(
   for (int v = 0; v < 16; ++v) {
     const int p = 8 * (v >> 2) + 4 * h + (v & 3);
     cidx[p][wave * 32 + col] = (unsigned short)a0[v];
-    cidx[32 + p][wave * 32 + col] = (unsigned short)a1[v];
+    if constexpr (NT == 2) cidx[32 + p][wave * 32 + col] = (unsigned short)a1[v];
     float M0 = m0[v], S0 = s0[v], M1 = m1[v], S1 = s1[v];
     // the two largest lane-state maxima of the wave (A >= B)
     float A0 = m0[v], B0 = kEmpty, A1 = m1[v], B1 = kEmpty;
     for (int off = 16; off > 0; off >>= 1) {
       lse_merge(M0, S0, __shfl_xor(M0, off), __shfl_xor(S0, off));
-      lse_merge(M1, S1, __shfl_xor(M1, off), __shfl_xor(S1, off));
       const float pa0 = __shfl_xor(A0, off), pb0 = __shfl_xor(B0, off);
-      const float pa1 = __shfl_xor(A1, off), pb1 = __shfl_xor(B1, off);
       B0 = fmaxf(fminf(A0, pa0), fmaxf(B0, pb0));
       A0 = fmaxf(A0, pa0);
-      B1 = fmaxf(fminf(A1, pa1), fmaxf(B1, pb1));
-      A1 = fmaxf(A1, pa1);
+      if constexpr (NT == 2) {
+        lse_merge(M1, S1, __shfl_xor(M1, off), __shfl_xor(S1, off));
+        const float pa1 = __shfl_xor(A1, off), pb1 = __shfl_xor(B1, off);
+        B1 = fmaxf(fminf(A1, pa1), fmaxf(B1, pb1));
+        A1 = fmaxf(A1, pa1);
+      }
     }
     if (col == 0) {
       stw[wave][p] = make_float2(M0, S0);
-      stw[wave][32 + p] = make_float2(M1, S1);
       top2[wave][p] = make_float2(A0, B0);
-      top2[wave][32 + p] = make_float2(A1, B1);
+      if constexpr (NT == 2) {
+        stw[wave][32 + p] = make_float2(M1, S1);
+        top2[wave][32 + p] = make_float2(A1, B1);
+      }
     }
   }
   // ill-conditioned components, direct form, lane = point; a term 2^-60 below
   // the point's largest well lane state is nothing in the sum and is not
   // finished (a routed component that is the point's largest is finished)
   __syncthreads();
-  {
+  if (lane < PTS) {
     float mw = kEmpty;
     for (int w2 = 0; w2 < 4; ++w2) mw = fmaxf(mw, stw[w2][lane].x);
-    float mi = -INFINITY, si = 0.0f;
+    // maximum kept in fp64: routed components can have log-densities of 1e4
+    // log2 units, where an fp32 value is off by up to 5e-4
+    double mi = -INFINITY;
+    float si = 0.0f;
     for (int ki = wave; ki < n_ill; ki += 4) {
       const int comp = ill_idx[ki];
-      const float c = dc[comp];
-      const float l = ill_logit_bounded<D64>(xs + lane * P, dmu + (size_t)comp * D64,
-                                             dh + (size_t)comp * D64, c, c - (mw - 60.0f));
-      lse_add(mi, si, l);
+      const double c = cdir[comp];
+      const double l = ill_logit_bounded<D64>(xs + lane * P, dmu + (size_t)comp * D64,
+                                              dh + (size_t)comp * D64, c,
+                                              c - ((double)mw - 60.0));
+      if (l > mi) {
+        si = __fmaf_rn(si, exp2_fast((float)(mi - l)), 1.0f);
+        mi = l;
+      } else if (l > -INFINITY) {
+        si += exp2_fast((float)(l - mi));
+      }
     }
-    sti[wave][lane] = make_float2(mi, si);
+    sti[wave][lane] = make_float2((float)mi, si);
+    stim[wave][lane] = mi;
   }
   __syncthreads();
-  if (tid < 64) {
+  if (tid < PTS) {
     float mm = -INFINITY, ss = 0.0f;
     for (int w2 = 0; w2 < 4; ++w2) {
       lse_merge(mm, ss, stw[w2][tid].x, stw[w2][tid].y);
@@ -618,43 +666,65 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_logz(
   for (int v = 0; v < 16; ++v) {
     const int p = 8 * (v >> 2) + 4 * h + (v & 3);
 #pragma unroll
-    for (int blk = 0; blk < 2; ++blk) {
+    for (int blk = 0; blk < NT; ++blk) {
       const int pp = blk * 32 + p;
       const float mv = blk ? m1[v] : m0[v];
+      const float sv = blk ? s1[v] : s0[v];
       const int av = blk ? a1[v] : a0[v];
       // refined: within the component's window, or among the point's four
-      // largest lane states (those fill the exact top-kT list)
+      // largest lane states (those fill the exact top-kT list); refined in full
+      // (every component of the lane state) when its other components carry a
+      // screened mass above kFullMass of the point's total
       const float rel = mv - lzm[pp];
-      const bool cand =
-          av >= 0 && (rel > thr[av] || (mv >= s4m[pp] && rel > -(float)kWideWindow));
-      float term = cand ? exp2_fast(mv - stw[wave][pp].x) : 0.0f;
+      const bool full = av >= 0 && (sv - 1.0f) * exp2_fast(rel) > kFullMass;
+      const bool cand = av >= 0 && (full || rel > thr[av] ||
+                                    (mv >= s4m[pp] && rel > -(float)kWideWindow));
+      float term = cand ? (full ? sv : 1.0f) * exp2_fast(mv - stw[wave][pp].x) : 0.0f;
       for (int off = 16; off > 0; off >>= 1) term += __shfl_xor(term, off);
       const unsigned long long bal = __ballot(cand);
+      const unsigned long long balf = __ballot(full);
       if (col == 0) {
         cms[wave][pp] = term;
         cmask[pp][wave] = (unsigned)(bal >> (32 * h));
+        fmask[pp][wave] = (unsigned)(balf >> (32 * h));
       }
     }
   }
   __syncthreads();
-  {
-    // exact log-densities of wave w's candidates of point p, in lane column order
+  if (lane < PTS) {
+    // exact log-densities of wave w's candidates of point p, in lane column
+    // order, relative to the point's screening log2 Z (small numbers, so fp32
+    // keeps them to its full relative precision)
     const int p = lane, w2 = wave;
+    const double ref = lzm[p] > -INFINITY ? (double)lzm[p] : 0.0;
     float mc = -INFINITY, sc = 0.0f;
     int tsl[kT];
     float tl[kT];
 #pragma unroll
     for (int j = 0; j < kT; ++j) { tsl[j] = -1; tl[j] = -INFINITY; }
     unsigned msk = cmask[p][w2];
+    const unsigned fm = fmask[p][w2];
+    const float* xr = xs + p * P;
+    auto refine = [&](int slot) {
+      const int comp = well_idx[slot];
+      const float l = (float)(ill_logit<D64>(xr, dmu + (size_t)comp * D64,
+                                             dh + (size_t)comp * D64, cdir[comp]) - ref);
+      lse_add(mc, sc, l);
+      topk_insert(tl, tsl, l, slot);
+    };
     while (msk) {
       const int b = __ffs(msk) - 1;
       msk &= msk - 1;
-      const int slot = cidx[p][w2 * 32 + b];
-      const int comp = well_idx[slot];
-      const float l = ill_logit<D64>(xs + p * P, dmu + (size_t)comp * D64,
-                                     dh + (size_t)comp * D64, dc[comp]);
-      lse_add(mc, sc, l);
-      topk_insert(tl, tsl, l, slot);
+      if ((fm >> b) & 1u) {
+        // every component of lane state (w2, b): slots 32 kb + b, kb = w2, w2 + 4, ...
+        for (int kb = w2; kb < n_wkb; kb += 4) {
+          const int slot = kb * kBK + b;
+          if (slot >= n_well) break;
+          refine(slot);
+        }
+      } else {
+        refine(cidx[p][w2 * 32 + b]);
+      }
     }
     rmc[w2][p] = make_float2(mc, sc);
 #pragma unroll
@@ -666,47 +736,51 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_logz(
   __syncthreads();
   if (tid < 64) {
     const int p = tid;
-    // screened mass of everything that is not a candidate (ill states are exact)
-    float mm = -INFINITY;
-    for (int w2 = 0; w2 < 4; ++w2) mm = fmaxf(mm, fmaxf(stw[w2][p].x, sti[w2][p].x));
-    float snc = 0.0f;
-    if (mm > -INFINITY) {
-      for (int w2 = 0; w2 < 4; ++w2) {
-        const float2 a = stw[w2][p], b = sti[w2][p];
-        if (a.x > -INFINITY) snc += fmaxf(a.y - cms[w2][p], 0.0f) * exp2_fast(a.x - mm);
-        if (b.x > -INFINITY) snc += b.y * exp2_fast(b.x - mm);
-      }
-    }
-    // merge the per-wave exact candidates in wave order
-    float mc = -INFINITY, sc = 0.0f;
-    int tsl[kT];
-    float tl[kT];
-#pragma unroll
-    for (int j = 0; j < kT; ++j) { tsl[j] = -1; tl[j] = -INFINITY; }
-    for (int w2 = 0; w2 < 4; ++w2) {
-      const float2 st2 = rmc[w2][p];
-      lse_merge(mc, sc, st2.x, st2.y);
-      for (int j2 = 0; j2 < kT; ++j2) {
-        const int sl2 = rts[w2][j2][p];
-        const float l = rtl[w2][j2][p];
-        if (sl2 >= 0) topk_insert(tl, tsl, l, sl2);
-      }
-    }
-    float mt = fmaxf(mm, mc), stot = 0.0f;
-    if (mt > -INFINITY) {
-      if (mm > -INFINITY) stot += snc * exp2_fast(mm - mt);
-      if (mc > -INFINITY) stot += sc * exp2_fast(mc - mt);
-    }
-    const float lz = mt + __log2f(stot);
-    const int64_t nn = n0 + p;
     double contrib = 0.0;
-    if (nn < n) {
-      logz2[nn] = lz;
-      contrib = (double)lz;
+    if (p < PTS) {
+      const float ref = lzm[p] > -INFINITY ? lzm[p] : 0.0f;
+      // screened mass of everything that is not a candidate (ill states are exact)
+      float mm = -INFINITY;
+      for (int w2 = 0; w2 < 4; ++w2) mm = fmaxf(mm, fmaxf(stw[w2][p].x, sti[w2][p].x));
+      float snc = 0.0f;
+      if (mm > -INFINITY) {
+        for (int w2 = 0; w2 < 4; ++w2) {
+          const float2 a = stw[w2][p], b = sti[w2][p];
+          if (a.x > -INFINITY) snc += fmaxf(a.y - cms[w2][p], 0.0f) * exp2_fast(a.x - mm);
+          if (b.x > -INFINITY) snc += b.y * exp2_fast((float)(stim[w2][p] - (double)mm));
+        }
+      }
+      // merge the per-wave exact candidates (relative to ref) in wave order
+      float mc = -INFINITY, sc = 0.0f;
+      int tsl[kT];
+      float tl[kT];
 #pragma unroll
-      for (int j = 0; j < kT; ++j) {
-        cslot[nn * kT + j] = tsl[j] >= 0 ? (unsigned short)tsl[j] : kNoSlot;
-        cr[nn * kT + j] = tsl[j] >= 0 ? exp2_fast(tl[j] - lz) : 0.0f;
+      for (int j = 0; j < kT; ++j) { tsl[j] = -1; tl[j] = -INFINITY; }
+      for (int w2 = 0; w2 < 4; ++w2) {
+        const float2 st2 = rmc[w2][p];
+        lse_merge(mc, sc, st2.x, st2.y);
+        for (int j2 = 0; j2 < kT; ++j2) {
+          const int sl2 = rts[w2][j2][p];
+          const float l = rtl[w2][j2][p];
+          if (sl2 >= 0) topk_insert(tl, tsl, l, sl2);
+        }
+      }
+      const float mmr = mm - ref;
+      float mt = fmaxf(mmr, mc), stot = 0.0f;
+      if (mt > -INFINITY) {
+        if (mmr > -INFINITY) stot += snc * exp2_fast(mmr - mt);
+        if (mc > -INFINITY) stot += sc * exp2_fast(mc - mt);
+      }
+      const float lzr = mt + __log2f(stot);   // log2 Z - ref
+      const int64_t nn = n0 + p;
+      if (nn < n) {
+        contrib = (double)ref + (double)lzr;
+        logz2[nn] = contrib;
+#pragma unroll
+        for (int j = 0; j < kT; ++j) {
+          cslot[nn * kT + j] = tsl[j] >= 0 ? (unsigned short)tsl[j] : kNoSlot;
+          cr[nn * kT + j] = tsl[j] >= 0 ? exp2_fast(tl[j] - lzr) : 0.0f;
+        }
       }
     }
     for (int off = 32; off > 0; off >>= 1) contrib += __shfl_xor(contrib, off);
@@ -751,7 +825,7 @@ template <int D64>
 __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
     const float* __restrict__ x, int64_t n, int d, int vec4, const float* __restrict__ wq,
     const float* __restrict__ cw, const int* __restrict__ counts,
-    const float* __restrict__ logz2, const unsigned short* __restrict__ cslot, int nch,
+    const double* __restrict__ logz2, const unsigned short* __restrict__ cslot, int nch,
     int64_t chunk_pts, double* __restrict__ part) {
   constexpr int P = D64 + 4;
   constexpr int NS = D64 / 4;                   // MFMA steps per chain
@@ -766,7 +840,7 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
   static_assert(kT == 4, "refined lists are loaded as int4");
   static_assert(LD >= 1 && PTS * Q4 % 256 == 0, "tile split");
   __shared__ __align__(16) float xs[2][PTS * P];
-  __shared__ float lzb[2][PTS];
+  __shared__ float2 lzb[2][PTS];                // -log2 Z / NGB as a (hi, lo) pair
   __shared__ unsigned long long rbb[2][PTS];
   const int kb = blockIdx.x / nch, chunk = blockIdx.x % nch;
   if (2 * kb >= counts[2]) return;              // counts[2]: well blocks of 32
@@ -787,7 +861,7 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
 
   // ---- X tile: global -> registers -> LDS
   float4 px[LD];
-  float plz = INFINITY;
+  float2 plz = make_float2(-INFINITY, 0.0f);
   unsigned long long prb = 0ull;
   auto load_regs = [&](int i) {
     const int64_t it = p0 + (int64_t)i * PTS;
@@ -809,10 +883,12 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
     }
     if (tid < PTS) {
       const int64_t nn = it + tid;
-      plz = INFINITY;
+      plz = make_float2(-INFINITY, 0.0f);
       prb = 0ull;
       if (nn < p1) {
-        plz = logz2[nn];
+        const double b64 = -logz2[nn] / NGB;
+        const float bh = (float)b64;
+        plz = make_float2(bh, (float)(b64 - (double)bh));
         const ushort4 sl = *reinterpret_cast<const ushort4*>(cslot + nn * kT);
         const int v4[4] = {sl.x, sl.y, sl.z, sl.w};
 #pragma unroll
@@ -885,9 +961,10 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
       // log-densities of points t*16 .. t*16+15 against this wave's components
       f4v la = {0.f, 0.f, 0.f, 0.f};
       const float* xr = &xs[cur][(t * 16 + i16) * P + 4 * k4];
-      // A operand of the bias steps: -log2 Z / NGB of row point i16 in lane
-      // group 0, 1 in lane group 1, 0 elsewhere
-      const float ab = k4 == 0 ? -lzb[cur][t * 16 + i16] * (1.0f / NGB) : (k4 == 1 ? 1.0f : 0.0f);
+      // A operand of the bias steps: -log2 Z / NGB of row point i16 as a
+      // (hi, lo) pair in lane groups 0 and 2, 1 in lane group 1, 0 in group 3
+      const float2 bz = lzb[cur][t * 16 + i16];
+      const float ab = k4 == 0 ? bz.x : (k4 == 1 ? 1.0f : (k4 == 2 ? bz.y : 0.0f));
       // wide D: keep each group's operand loads in their group (hoisting all
       // of them exhausts the registers)
       constexpr bool kPin = D64 > 128;
@@ -947,171 +1024,443 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
   }
 }
 
-// Refined pairs of a well block, in fp64.  Grid: (block, sparse chunk).  The
-// chunk's refined lists are scanned G*256 points at a time (the next group's
-// lists are loaded while the current one is processed); the pairs that fall in
-// this block are compacted in (point, rank) order.  Their rows are gathered in
-// batches of NB through registers into a double-buffered LDS tile, the next
-// batch's loads in flight while the current one is consumed.  Wave w owns
-// components 8w .. 8w+7 of the block and picks its pairs out of a batch with a
-// ballot; lane l owns columns l, l + 64, ... of [1 | x | x^2] and adds r,
-// r * x, r * x^2 (exact products of fp32 values) in pair order, in registers.
-template <int D64>
-__global__ __launch_bounds__(256) void k_stats_sparse(
-    const float* __restrict__ x, int64_t n, int d, const int* __restrict__ counts,
-    const unsigned short* __restrict__ cslot, const float* __restrict__ cr, int nch,
-    int64_t chunk_pts, double* __restrict__ part) {
-  constexpr int STRIDE = 1 + 2 * D64, NCI = (STRIDE + 63) / 64, NB = 32, G = 2;
-  constexpr int GL = NB * D64 / 256;            // gathered values per thread and batch
-  __shared__ float xb[2][NB * D64];
-  __shared__ int2 stage[G * 256 * kT];
-  __shared__ int wcnt[4];
-  const int kb = blockIdx.x / nch, chunk = blockIdx.x % nch;
-  if (kb >= counts[2]) return;
+// ---------------------------------------------------------------- Step 2: statistics, wide D
+// Well set for DW >= 256 (DW a multiple of 128).  A workgroup owns one
+// 16-component group and a chunk of points; its NW = DW / 128 waves split the
+// dimensions, wave w owning [128 w, 128 w + 128): the W and P steps of those
+// dimensions (from the packed operand wq) stay in registers, and its 16-point
+// X tiles pass through its own LDS region.  Per tile every wave forms the
+// x . W + x^2 . P part of the log-densities over its dimensions in 16-dimension
+// subgroups, each summed from zero on fp32 MFMA (x and x^2 steps of the same
+// four dimensions in turn, so the running sum stays small) and folded into
+// fp64; the waves' fp64 partials are exchanged through LDS and summed in wave
+// order, identically in every wave, and the constant and -log2 Z are added in
+// fp64.  With hundreds of dimensions the terms reach 1e3 log2 units in total,
+// and a single fp32 chain would leave errors of 1e-4 on log2 r, too much for a
+// pair that carries the variance of a component sitting on one point.  Then
+// r = 2^(sum) (refined pairs set to 0) and each wave contracts r^T [x | x^2]
+// over its own dimensions into fp32 accumulators, folded into the
+// workgroup's fp64 partial every kFlushWide tiles.  N_k is summed by wave 0.
+constexpr int kFlushWide = 256;
+
+template <int DW>
+__global__ __launch_bounds__(64 * (DW / 128)) void k_stats_wide(
+    const float* __restrict__ x, int64_t n, int d, int vec4, const float* __restrict__ wq,
+    const double* __restrict__ cwell, const int* __restrict__ well_idx,
+    const int* __restrict__ counts, const double* __restrict__ logz2,
+    const unsigned short* __restrict__ cslot, int nch, int64_t chunk_pts,
+    double* __restrict__ part) {
+  constexpr int NW = DW / 128, DQ = 128, P = DQ + 4;
+  constexpr int NS = DW / 4, WQS = wq_steps(DW);
+  constexpr int SW = DQ / 4, NBQ = DQ / 16, NG = DQ / 64;
+  constexpr int STRIDE = 1 + 2 * DW;
+  constexpr int LD = 16 * DQ / 4 / 64;          // float4 per lane per X tile
+  static_assert(kT == 4, "refined lists are loaded as ushort4");
+  __shared__ __align__(16) float xs[NW][16 * P];
+  __shared__ double lpart[2][NW][4][64];
+  const int g = blockIdx.x / nch, chunk = blockIdx.x % nch;
+  const int n_well = counts[0];
+  if (16 * g >= n_well) return;                // no well component in this group
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int i16 = lane & 15, k4 = lane >> 4;
   const int64_t p0 = (int64_t)chunk * chunk_pts;
   const int64_t p1 = p0 + chunk_pts < n ? p0 + chunk_pts : n;
-  double acc[8][NCI];
+  double* pw = part + (size_t)blockIdx.x * 16 * STRIDE;
+  if (p0 >= p1) {
+    for (int i = tid; i < 16 * STRIDE; i += 64 * NW) pw[i] = 0.0;
+    return;
+  }
+  const int niter = (int)((p1 - p0 + 15) / 16);
+  const int dq0 = DQ * wave;                    // this wave's first dimension
+  // this lane's component (B-operand column i16): its expanded-form constant
+  const int myslot = 16 * g + i16;
+  const double cst = myslot < n_well ? cwell[well_idx[myslot]] : -INFINITY;
+  float wb[2 * SW];
 #pragma unroll
-  for (int j = 0; j < 8; ++j)
+  for (int s2 = 0; s2 < SW; ++s2) {
+    wb[s2] = wq[((size_t)g * WQS + SW * wave + s2) * 64 + lane];
+    wb[SW + s2] = wq[((size_t)g * WQS + NS + SW * wave + s2) * 64 + lane];
+  }
+
+  // this wave's 16 x 128 block of the next tile, in registers; lanes 0..15
+  // also hold the tile's log2 Z and refined-slot mask (bits of this group)
+  float4 px[LD];
+  double plz = INFINITY;
+  unsigned prb = 0u;
+  auto load_regs = [&](int i) {
+    const int64_t it = p0 + (int64_t)i * 16;
 #pragma unroll
-    for (int i = 0; i < NCI; ++i) acc[j][i] = 0.0;
-  // three-stage prefetch over groups of G*256 points: while group g is staged,
-  // the responsibilities of group g+1 (only for points with a pair in this
-  // block, known from its slots) and the slots of group g+2 are in flight
-  auto in_block = [&](int v) { return v >= 0 && (v >> 5) == kb; };
-  int4 sl[G], sl1[G], sl2[G];
-  float4 rr[G], rr1[G];
-  auto load_slots = [&](int64_t base, int4* dst) {
-#pragma unroll
-    for (int u = 0; u < G; ++u) {
-      const int64_t nn = base + u * 256 + tid;
-      dst[u] = make_int4(-1, -1, -1, -1);
+    for (int j = 0; j < LD; ++j) {
+      const int idx = lane + 64 * j, r = idx / (DQ / 4), c = dq0 + (idx % (DQ / 4)) * 4;
+      const int64_t nn = it + r;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (vec4) {
+        if (nn < p1 && c < d) v = *reinterpret_cast<const float4*>(x + nn * d + c);
+      } else if (nn < p1) {
+        const float* xr = x + nn * d;
+        v.x = c < d ? xr[c] : 0.f;
+        v.y = c + 1 < d ? xr[c + 1] : 0.f;
+        v.z = c + 2 < d ? xr[c + 2] : 0.f;
+        v.w = c + 3 < d ? xr[c + 3] : 0.f;
+      }
+      px[j] = v;
+    }
+    if (lane < 16) {
+      const int64_t nn = it + lane;
+      plz = INFINITY;
+      prb = 0u;
       if (nn < p1) {
-        const ushort4 s4 = *reinterpret_cast<const ushort4*>(cslot + nn * kT);
-        dst[u] = make_int4(s4.x == kNoSlot ? -1 : s4.x, s4.y == kNoSlot ? -1 : s4.y,
-                           s4.z == kNoSlot ? -1 : s4.z, s4.w == kNoSlot ? -1 : s4.w);
+        plz = logz2[nn];
+        const ushort4 sl = *reinterpret_cast<const ushort4*>(cslot + nn * kT);
+        const int v4[4] = {sl.x, sl.y, sl.z, sl.w};
+#pragma unroll
+        for (int j = 0; j < kT; ++j)
+          if (v4[j] != kNoSlot && (v4[j] >> 4) == g) prb |= 1u << (v4[j] & 15);
       }
     }
   };
-  auto load_resp = [&](int64_t base, const int4* src, float4* dst) {
+  auto store_regs = [&]() {
 #pragma unroll
-    for (int u = 0; u < G; ++u) {
-      dst[u] = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (in_block(src[u].x) || in_block(src[u].y) || in_block(src[u].z) || in_block(src[u].w))
-        dst[u] = *reinterpret_cast<const float4*>(cr + (base + u * 256 + tid) * kT);
+    for (int j = 0; j < LD; ++j) {
+      const int idx = lane + 64 * j, r = idx / (DQ / 4), c = (idx % (DQ / 4)) * 4;
+      *reinterpret_cast<float4*>(&xs[wave][r * P + c]) = px[j];
+    }
+  };
+
+  f4v acc[2 * NBQ];
+#pragma unroll
+  for (int c = 0; c < 2 * NBQ; ++c) acc[c] = f4v{0.f, 0.f, 0.f, 0.f};
+  float nkacc = 0.0f;
+  bool first = true;
+  // fp32 accumulators -> fp64 partial.  Register v of block c at lane l is
+  // column 4(l/16) + v of the block: local dimension 64 (c/4 % NG) + 4 (4 k4 + v) + c % 4.
+  auto flush = [&]() {
+    double* row = pw + (size_t)i16 * STRIDE;
+    if (wave == 0) {
+      float nk2 = nkacc + __shfl_xor(nkacc, 16);
+      nk2 += __shfl_xor(nk2, 32);
+      if (k4 == 0) row[0] = first ? (double)nk2 : row[0] + (double)nk2;
+    }
+#pragma unroll
+    for (int c = 0; c < 2 * NBQ; ++c) {
+      const int part2 = c / NBQ, gg = (c % NBQ) / 4, e = c % 4;
+      double* dst = row + 1 + part2 * DW + dq0 + 64 * gg + 16 * k4 + e;
+      double o[4];
+#pragma unroll
+      for (int v = 0; v < 4; ++v) o[v] = first ? 0.0 : dst[4 * v];
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        dst[4 * v] = o[v] + (double)acc[c][v];
+        acc[c][v] = 0.0f;
+      }
+    }
+    nkacc = 0.0f;
+    first = false;
+  };
+
+  load_regs(0);
+  for (int i = 0; i < niter; ++i) {
+    const int buf = i & 1;
+    store_regs();
+    unsigned rbv[4];
+    double lzv[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      rbv[v] = __shfl(prb, 4 * k4 + v);
+      lzv[v] = __shfl(plz, 4 * k4 + v);
+    }
+    __builtin_amdgcn_wave_barrier();
+    if (i + 1 < niter) load_regs(i + 1);
+    // x . W + x^2 . P of the tile's 16 points against the group's 16
+    // components over this wave's dimensions, 16 dimensions per fp32 sum
+    double t64[4] = {0.0, 0.0, 0.0, 0.0};
+    const float* xr = &xs[wave][i16 * P + 4 * k4];
+#pragma unroll
+    for (int q = 0; q < DQ / 16; ++q) {
+      const float4 u = *reinterpret_cast<const float4*>(xr + 16 * q);
+      f4v la = {0.f, 0.f, 0.f, 0.f};
+      la = mfma16(u.x, wb[4 * q], la);
+      la = mfma16(u.x * u.x, wb[SW + 4 * q], la);
+      la = mfma16(u.y, wb[4 * q + 1], la);
+      la = mfma16(u.y * u.y, wb[SW + 4 * q + 1], la);
+      la = mfma16(u.z, wb[4 * q + 2], la);
+      la = mfma16(u.z * u.z, wb[SW + 4 * q + 2], la);
+      la = mfma16(u.w, wb[4 * q + 3], la);
+      la = mfma16(u.w * u.w, wb[SW + 4 * q + 3], la);
+#pragma unroll
+      for (int v = 0; v < 4; ++v) t64[v] += (double)la[v];
+    }
+#pragma unroll
+    for (int v = 0; v < 4; ++v) lpart[buf][wave][v][lane] = t64[v];
+    __syncthreads();
+    float r[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      double tot = lpart[buf][0][v][lane];
+#pragma unroll
+      for (int w2 = 1; w2 < NW; ++w2) tot += lpart[buf][w2][v][lane];
+      tot += cst - lzv[v];
+      const float e = exp2_fast((float)tot);
+      r[v] = ((rbv[v] >> i16) & 1u) ? 0.0f : e;
+      nkacc += r[v];
+    }
+    // statistics over this wave's dimensions: step v contracts points 4k + v
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const float* yr = &xs[wave][(4 * k4 + v) * P + 4 * i16];
+#pragma unroll
+      for (int gg = 0; gg < NG; ++gg) {
+        const float4 y = *reinterpret_cast<const float4*>(yr + 64 * gg);
+        acc[4 * gg + 0] = mfma16(y.x, r[v], acc[4 * gg + 0]);
+        acc[4 * gg + 1] = mfma16(y.y, r[v], acc[4 * gg + 1]);
+        acc[4 * gg + 2] = mfma16(y.z, r[v], acc[4 * gg + 2]);
+        acc[4 * gg + 3] = mfma16(y.w, r[v], acc[4 * gg + 3]);
+        acc[NBQ + 4 * gg + 0] = mfma16(y.x * y.x, r[v], acc[NBQ + 4 * gg + 0]);
+        acc[NBQ + 4 * gg + 1] = mfma16(y.y * y.y, r[v], acc[NBQ + 4 * gg + 1]);
+        acc[NBQ + 4 * gg + 2] = mfma16(y.z * y.z, r[v], acc[NBQ + 4 * gg + 2]);
+        acc[NBQ + 4 * gg + 3] = mfma16(y.w * y.w, r[v], acc[NBQ + 4 * gg + 3]);
+      }
+    }
+    if ((i % kFlushWide) == kFlushWide - 1 || i + 1 == niter) flush();
+    __builtin_amdgcn_wave_barrier();            // this tile's LDS reads before the next store
+  }
+}
+
+// ---------------------------------------------------------------- Step 2: refined pairs
+// The stored refined pairs (at most kT per point, the pairs that carry a
+// component's mass) are summed exactly in fp64, grouped by bucket: a bucket is
+// sparse_cb(D64) consecutive well slots.  Three light passes put the pairs of
+// every bucket into one contiguous list, in a fixed order:
+//   k_sparse_count    per unit (a contiguous range of points): pairs per bucket
+//   k_sparse_scan     exclusive prefix over (bucket, unit), bucket-major
+//   k_sparse_scatter  per unit: every pair to its bucket's segment, the unit's
+//                     points taken 64 at a time, slot rank j outer, lanes inner
+// and k_stats_sparse sums each bucket's list, split into parts, in list order.
+// Integer counts make the lists, and so the sums, independent of scheduling.
+struct SPair {
+  int64_t pt;   // point index
+  float r;      // exact responsibility
+  int c;        // component slot within the bucket
+};
+
+__host__ __device__ constexpr int sparse_cb(int D64) {
+  return D64 <= 128 ? 32 : (D64 <= 256 ? 16 : (D64 <= 512 ? 8 : 4));
+}
+__host__ __device__ constexpr int sparse_lcb(int D64) {
+  return D64 <= 128 ? 5 : (D64 <= 256 ? 4 : (D64 <= 512 ? 3 : 2));
+}
+constexpr int kSparseTab = 1 << 18;     // (bucket, unit) table entries at most
+
+__global__ __launch_bounds__(64) void k_sparse_count(const unsigned short* __restrict__ cslot,
+                                                     int64_t n, int64_t upts, int nb, int lcb,
+                                                     int nunit, int* __restrict__ gcnt) {
+  extern __shared__ int lc[];
+  const int u = blockIdx.x, lane = threadIdx.x;
+  for (int b = lane; b < nb; b += 64) lc[b] = 0;
+  __syncthreads();
+  const int64_t p0 = (int64_t)u * upts;
+  const int64_t p1 = p0 + upts < n ? p0 + upts : n;
+  for (int64_t p = p0 + lane; p < p1; p += 64) {
+    const ushort4 s4 = *reinterpret_cast<const ushort4*>(cslot + p * kT);
+    if (s4.x != kNoSlot) atomicAdd(&lc[s4.x >> lcb], 1);
+    if (s4.y != kNoSlot) atomicAdd(&lc[s4.y >> lcb], 1);
+    if (s4.z != kNoSlot) atomicAdd(&lc[s4.z >> lcb], 1);
+    if (s4.w != kNoSlot) atomicAdd(&lc[s4.w >> lcb], 1);
+  }
+  __syncthreads();
+  for (int b = lane; b < nb; b += 64) gcnt[(size_t)b * nunit + u] = lc[b];
+}
+
+// Exclusive prefix of cnt[0 .. tot) into off[0 .. tot] (64-bit), off[tot] =
+// total.  One workgroup of 1024 threads, 4096 entries per round.
+__global__ __launch_bounds__(1024) void k_sparse_scan(const int* __restrict__ cnt, int tot,
+                                                      int64_t* __restrict__ off) {
+  __shared__ int64_t wsum[16];
+  __shared__ int64_t carry_s;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (tid == 0) carry_s = 0;
+  __syncthreads();
+  for (int base = 0; base < tot; base += 4096) {
+    int64_t v[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int i = base + 4 * tid + j;
+      v[j] = i < tot ? (int64_t)(unsigned)cnt[i] : 0;
+    }
+    const int64_t own = v[0] + v[1] + v[2] + v[3];
+    int64_t inc = own;
+    for (int o = 1; o < 64; o <<= 1) {
+      const int64_t t = __shfl_up(inc, o);
+      if (lane >= o) inc += t;
+    }
+    if (lane == 63) wsum[wave] = inc;
+    __syncthreads();
+    int64_t before = carry_s, all = 0;
+    for (int w = 0; w < 16; ++w) {
+      if (w < wave) before += wsum[w];
+      all += wsum[w];
+    }
+    int64_t run = before + inc - own;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int i = base + 4 * tid + j;
+      if (i < tot) off[i] = run;
+      run += v[j];
+    }
+    __syncthreads();                            // wsum and carry_s read by all
+    if (tid == 0) carry_s += all;
+    __syncthreads();
+  }
+  if (tid == 0) off[tot] = carry_s;
+}
+
+__global__ __launch_bounds__(64) void k_sparse_scatter(
+    const unsigned short* __restrict__ cslot, const float* __restrict__ cr, int64_t n,
+    int64_t upts, int nb, int lcb, int nunit, const int64_t* __restrict__ goff,
+    SPair* __restrict__ list) {
+  extern __shared__ int pos[];               // pairs of this unit placed so far, per bucket
+  const int u = blockIdx.x, lane = threadIdx.x;
+  for (int b = lane; b < nb; b += 64) pos[b] = 0;
+  __syncthreads();
+  const int64_t p0 = (int64_t)u * upts;
+  const int64_t p1 = p0 + upts < n ? p0 + upts : n;
+  const unsigned long long below = (1ull << lane) - 1ull;
+  for (int64_t pb = p0; pb < p1; pb += 64) {
+    const int64_t p = pb + lane;
+    int sl[kT] = {-1, -1, -1, -1};
+    float4 r4 = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (p < p1) {
+      const ushort4 s4 = *reinterpret_cast<const ushort4*>(cslot + p * kT);
+      sl[0] = s4.x == kNoSlot ? -1 : s4.x;
+      sl[1] = s4.y == kNoSlot ? -1 : s4.y;
+      sl[2] = s4.z == kNoSlot ? -1 : s4.z;
+      sl[3] = s4.w == kNoSlot ? -1 : s4.w;
+      if (sl[0] >= 0 || sl[1] >= 0 || sl[2] >= 0 || sl[3] >= 0)
+        r4 = *reinterpret_cast<const float4*>(cr + p * kT);
+    }
+    const float rr[kT] = {r4.x, r4.y, r4.z, r4.w};
+#pragma unroll
+    for (int j = 0; j < kT; ++j) {
+      const bool valid = sl[j] >= 0;
+      const int bk = valid ? (sl[j] >> lcb) : -1;
+      unsigned long long act = __ballot(valid);
+      while (act) {
+        const int leader = __ffsll(act) - 1;
+        const int bl = __shfl(bk, leader);
+        const unsigned long long same = __ballot(bk == bl);
+        const int done = pos[bl];
+        if (bk == bl) {
+          SPair e;
+          e.pt = p;
+          e.r = rr[j];
+          e.c = sl[j] & ((1 << lcb) - 1);
+          list[goff[(size_t)bl * nunit + u] + done + __popcll(same & below)] = e;
+        }
+        __builtin_amdgcn_wave_barrier();
+        if (lane == leader) pos[bl] = done + __popcll(same);
+        __builtin_amdgcn_wave_barrier();
+        act &= ~same;
+      }
+    }
+  }
+}
+
+// Sums of one part of one bucket's list.  Batches of NB pairs: the records of
+// batch t+1 are in LDS and its rows are gathered into registers while batch t
+// is consumed from LDS.  Wave w owns the CW = C/4 slots CW w .. CW w + CW - 1
+// of the bucket and takes its pairs of a batch in order; lane l owns columns
+// l, l + 64, ... of [1 | x | x^2] and adds r, r x, r x^2 in fp64 (r x is exact).
+template <int D64>
+__global__ __launch_bounds__(256) void k_stats_sparse(
+    const float* __restrict__ x, int64_t n, int d, const SPair* __restrict__ list,
+    const int64_t* __restrict__ goff, int nunit, int nparts, double* __restrict__ part) {
+  constexpr int C = sparse_cb(D64), CW = C / 4;
+  constexpr int STRIDE = 1 + 2 * D64, NCI = (STRIDE + 63) / 64;
+  constexpr int NB = D64 <= 64 ? 64 : 4096 / D64;
+  constexpr int GL = (NB * D64 + 255) / 256;     // gathered values per thread and batch
+  __shared__ float xb[2][NB * D64];
+  __shared__ int2 rb[3][NB];                     // (slot in bucket, r bits) per pair
+  __shared__ int64_t pb[3][NB];                  // point per pair
+  const int bucket = blockIdx.x / nparts, prt = blockIdx.x % nparts;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int64_t lo = goff[(size_t)bucket * nunit], hi = goff[(size_t)(bucket + 1) * nunit];
+  const int64_t cnt = hi - lo;
+  const int64_t a0 = lo + cnt * prt / nparts, a1 = lo + cnt * (prt + 1) / nparts;
+  const int nbatch = (int)((a1 - a0 + NB - 1) / NB);
+  double acc[CW][NCI];
+#pragma unroll
+  for (int j = 0; j < CW; ++j)
+#pragma unroll
+    for (int i = 0; i < NCI; ++i) acc[j][i] = 0.0;
+  auto load_rec = [&](int t, int buf) {
+    if (tid < NB) {
+      const int64_t e = a0 + (int64_t)t * NB + tid;
+      if (e < a1) {
+        const SPair q = list[e];
+        rb[buf][tid] = make_int2(q.c, __float_as_int(q.r));
+        pb[buf][tid] = q.pt;
+      }
     }
   };
   float gv[GL];
-  // rows of the staged pairs b0 .. b0+nb-1 into registers (column c of pair e
-  // is value i = e * D64 + c, thread tid takes i = tid + 256 j)
-  auto gather = [&](int64_t base, int b0, int nb) {
+  auto gather = [&](int t, int buf) {
+    const int nbt = (int)(a1 - a0 - (int64_t)t * NB < NB ? a1 - a0 - (int64_t)t * NB : NB);
 #pragma unroll
     for (int j = 0; j < GL; ++j) {
       const int i = tid + 256 * j, e = i / D64, c = i % D64;
       float v = 0.0f;
-      if (e < nb && c < d) v = x[(base + (stage[b0 + e].x >> 5)) * d + c];
+      if (i < NB * D64 && e < nbt && c < d) v = x[pb[buf][e] * d + c];
       gv[j] = v;
     }
   };
-  load_slots(p0, sl);
-  load_resp(p0, sl, rr);
-  load_slots(p0 + G * 256, sl1);
-  int buf = 0;
-  for (int64_t base = p0; base < p1; base += G * 256) {
-    int mine[G];
+  if (nbatch > 0) {
+    load_rec(0, 0);
+    if (nbatch > 1) load_rec(1, 1);
+    __syncthreads();
+    gather(0, 0);
+  }
+  for (int t = 0; t < nbatch; ++t) {
+    const int xbuf = t & 1, rcur = t % 3;
 #pragma unroll
-    for (int u = 0; u < G; ++u) {
-      mine[u] = (int)in_block(sl[u].x) + (int)in_block(sl[u].y) + (int)in_block(sl[u].z) +
-                (int)in_block(sl[u].w);
-    }
-    // entries are staged in (group, thread, rank) order, i.e. in point order
-    int total = 0, pos[G];
+    for (int j = 0; j < GL; ++j)
+      if (tid + 256 * j < NB * D64) xb[xbuf][tid + 256 * j] = gv[j];
+    __syncthreads();            // rows of batch t, records of batches t, t+1 in LDS
+    // the record buffer of batch t+2 was last read while consuming batch t-1
+    if (t + 2 < nbatch) load_rec(t + 2, (t + 2) % 3);
+    if (t + 1 < nbatch) gather(t + 1, (t + 1) % 3);
+    const int nbt = (int)(a1 - a0 - (int64_t)t * NB < NB ? a1 - a0 - (int64_t)t * NB : NB);
+    int2 en = make_int2(0, 0);
+    if (lane < nbt) en = rb[rcur][lane];
+    const int cl = en.x - CW * wave;
+    unsigned long long own = __ballot(lane < nbt && cl >= 0 && cl < CW);
+    while (own) {
+      const int e = __ffsll(own) - 1;
+      own &= own - 1;
+      const int jc = __builtin_amdgcn_readlane(en.x, e) - CW * wave;
+      const double r = (double)__int_as_float(__builtin_amdgcn_readlane(en.y, e));
+      const float* xr = xb[xbuf] + e * D64;
+      double y[NCI];
 #pragma unroll
-    for (int u = 0; u < G; ++u) {
-      int inc = mine[u];
-      for (int off = 1; off < 64; off <<= 1) {
-        const int v = __shfl_up(inc, off);
-        if (lane >= off) inc += v;
+      for (int i = 0; i < NCI; ++i) {
+        const int c = lane + 64 * i;
+        double v = 0.0;
+        if (c == 0) v = 1.0;
+        else if (c <= D64) v = (double)xr[c - 1];
+        else if (c < STRIDE) { const double xv = (double)xr[c - 1 - D64]; v = xv * xv; }
+        y[i] = v;
       }
-      __syncthreads();                          // wcnt free / previous stage consumed
-      if (lane == 63) wcnt[wave] = inc;
-      __syncthreads();
-      int before = 0, all = 0;
-      for (int w2 = 0; w2 < 4; ++w2) {
-        const int c2 = wcnt[w2];
-        if (w2 < wave) before += c2;
-        all += c2;
-      }
-      pos[u] = total + before + inc - mine[u];
-      total += all;
-    }
 #pragma unroll
-    for (int u = 0; u < G; ++u) {
-      const int vs[4] = {sl[u].x, sl[u].y, sl[u].z, sl[u].w};
-      const float rs[4] = {rr[u].x, rr[u].y, rr[u].z, rr[u].w};
-      int q = pos[u];
+      for (int j = 0; j < CW; ++j) {
+        if (jc == j) {
 #pragma unroll
-      for (int j = 0; j < kT; ++j) {
-        if (in_block(vs[j]))
-          stage[q++] = make_int2(((u * 256 + tid) << 5) | (vs[j] & 31), __float_as_int(rs[j]));
-      }
-    }
-    // advance the prefetch pipeline (loads past the chunk end return empty lists)
-    load_resp(base + G * 256, sl1, rr1);
-    load_slots(base + 2 * G * 256, sl2);
-#pragma unroll
-    for (int u = 0; u < G; ++u) {
-      sl[u] = sl1[u];
-      sl1[u] = sl2[u];
-      rr[u] = rr1[u];
-    }
-    if (total == 0) continue;
-    __syncthreads();                            // stage complete
-    gather(base, 0, total < NB ? total : NB);
-    for (int b0 = 0; b0 < total; b0 += NB) {
-      const int nb = total - b0 < NB ? total - b0 : NB;
-#pragma unroll
-      for (int j = 0; j < GL; ++j) xb[buf][tid + 256 * j] = gv[j];
-      __syncthreads();                          // batch b0 in xb[buf]
-      if (b0 + NB < total) gather(base, b0 + NB, total - b0 - NB < NB ? total - b0 - NB : NB);
-      // this wave's pairs of the batch
-      int2 en = make_int2(0, 0);
-      if (lane < nb) en = stage[b0 + lane];
-      const int cl = (en.x & 31) - 8 * wave;
-      unsigned long long own = __ballot(lane < nb && cl >= 0 && cl < 8);
-      while (own) {
-        const int e = __ffsll(own) - 1;
-        own &= own - 1;
-        const int ex = __builtin_amdgcn_readlane(en.x, e);
-        const int ey = __builtin_amdgcn_readlane(en.y, e);
-        const int jc = (ex & 31) - 8 * wave;
-        const double r = (double)__int_as_float(ey);
-        const float* xr = xb[buf] + e * D64;
-        double y[NCI];
-#pragma unroll
-        for (int i = 0; i < NCI; ++i) {
-          const int c = lane + 64 * i;
-          double v = 0.0;
-          if (c == 0) v = 1.0;
-          else if (c <= D64) v = (double)xr[c - 1];
-          else if (c < STRIDE) { const double xv = (double)xr[c - 1 - D64]; v = xv * xv; }
-          y[i] = v;
-        }
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          if (jc == j) {
-#pragma unroll
-            for (int i = 0; i < NCI; ++i) acc[j][i] = fma(r, y[i], acc[j][i]);
-          }
+          for (int i = 0; i < NCI; ++i) acc[j][i] = fma(r, y[i], acc[j][i]);
         }
       }
-      buf ^= 1;
     }
   }
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    double* out = part + ((size_t)blockIdx.x * kBK + 8 * wave + j) * STRIDE;
+  for (int j = 0; j < CW; ++j) {
+    double* out = part + ((size_t)blockIdx.x * C + CW * wave + j) * STRIDE;
 #pragma unroll
     for (int i = 0; i < NCI; ++i) {
       const int c = lane + 64 * i;
@@ -1121,14 +1470,17 @@ __global__ __launch_bounds__(256) void k_stats_sparse(
 }
 
 // ---------------------------------------------------------------- Step 2: statistics, ill set
-// Ill-conditioned components (few).  Grid of fixed size; each of the n_ikb
-// blocks of 32 such components gets grid/n_ikb point chunks.  Per 64-point
-// iteration wave w forms r for components 8w..8w+7 of the block with the
-// direct form (lane = point), then accumulates the statistics of those
-// components in fp64 (lane = column).
-__host__ __device__ inline int ill_chunks(int grid, int n_ikb, int64_t n) {
+// Ill-conditioned components (few).  Grid of fixed size; each of the
+// cdiv(n_ill, ICB) blocks of ICB = 4 CW such components gets grid/blocks point
+// chunks.  Per PT-point iteration wave w forms r for components CW w ..
+// CW w + CW - 1 of the block with the direct form (lane = point), then
+// accumulates the statistics of those components in fp64 (lane = column).
+__host__ __device__ constexpr int ill_pt(int D64) { return D64 <= 256 ? 64 : (D64 <= 512 ? 32 : 16); }
+__host__ __device__ constexpr int ill_cw(int D64) { return D64 <= 256 ? 8 : (D64 <= 512 ? 4 : 2); }
+
+__host__ __device__ inline int ill_chunks(int grid, int n_ikb, int64_t n, int pt) {
   int c = grid / (n_ikb > 0 ? n_ikb : 1);
-  const int64_t cap = (n + 63) / 64;
+  const int64_t cap = (n + pt - 1) / pt;
   if (c > cap) c = (int)cap;
   return c < 1 ? 1 : c;
 }
@@ -1136,62 +1488,64 @@ __host__ __device__ inline int ill_chunks(int grid, int n_ikb, int64_t n) {
 template <int D64>
 __global__ __launch_bounds__(256) void k_stats_ill(
     const float* __restrict__ x, int64_t n, int d, int vec4, const int* __restrict__ ill_idx,
-    const float* __restrict__ dmu, const float* __restrict__ dh, const float* __restrict__ dc,
-    const int* __restrict__ counts, const float* __restrict__ logz2,
-    double* __restrict__ part) {
+    const float* __restrict__ dmu, const double* __restrict__ dh,
+    const double* __restrict__ cdir, const int* __restrict__ counts,
+    const double* __restrict__ logz2, double* __restrict__ part) {
   constexpr int P = D64 + 4, NJ = D64 / 64, STRIDE = 1 + 2 * D64;
-  __shared__ __align__(16) float xs[64 * P];
-  __shared__ float rs[32 * 64];
-  __shared__ float lzs[64];
-  const int n_ikb = counts[3];
+  constexpr int PT = ill_pt(D64), CW = ill_cw(D64), ICB = 4 * CW;
+  __shared__ __align__(16) float xs[PT * P];
+  __shared__ float rs[ICB * PT];
+  __shared__ double lzs[PT];
+  const int n_ill = counts[1];
+  const int n_ikb = (n_ill + ICB - 1) / ICB;
   if (n_ikb == 0) return;
-  const int nchk = ill_chunks(gridDim.x, n_ikb, n);
+  const int nchk = ill_chunks(gridDim.x, n_ikb, n, PT);
   const int kb = blockIdx.x / nchk, chunk = blockIdx.x % nchk;
   if (kb >= n_ikb) return;
   const int64_t chunk_pts = (n + nchk - 1) / nchk;
-  const int n_ill = counts[1];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int64_t p0 = (int64_t)chunk * chunk_pts;
   const int64_t p1 = p0 + chunk_pts < n ? p0 + chunk_pts : n;
-  double S[8][NJ], Q[8][NJ], NK[8];
+  double S[CW][NJ], Q[CW][NJ], NK[CW];
 #pragma unroll
-  for (int c = 0; c < 8; ++c) {
+  for (int c = 0; c < CW; ++c) {
     NK[c] = 0.0;
 #pragma unroll
     for (int j = 0; j < NJ; ++j) S[c][j] = Q[c][j] = 0.0;
   }
-  for (int64_t it = p0; it < p1; it += 64) {
+  for (int64_t it = p0; it < p1; it += PT) {
     __syncthreads();
-    load_tile<D64>(x, p1, d, it, 64, xs, vec4 != 0);
-    if (tid < 64) lzs[tid] = (it + tid < p1) ? logz2[it + tid] : INFINITY;
+    load_tile<D64>(x, p1, d, it, PT, xs, vec4 != 0);
+    if (tid < PT) lzs[tid] = (it + tid < p1) ? logz2[it + tid] : INFINITY;
     __syncthreads();
     // nz[c]: the points of this tile with r > 0 for component c (wave-uniform)
-    unsigned long long nz[8];
+    unsigned long long nz[CW];
 #pragma unroll
-    for (int c = 0; c < 8; ++c) {
-      const int ki = kb * kBK + wave * 8 + c;
+    for (int c = 0; c < CW; ++c) {
+      const int ki = kb * ICB + wave * CW + c;
       float r = 0.0f;
-      if (ki < n_ill) {
+      if (ki < n_ill && lane < PT) {
         const int comp = ill_idx[ki];
-        const float c = dc[comp];
+        const double c0 = cdir[comp];
         // r < 2^-150 is 0 in fp32: such pairs are not finished
-        const float l = ill_logit_bounded<D64>(xs + lane * P, dmu + (size_t)comp * D64,
-                                               dh + (size_t)comp * D64, c, c - (lzs[lane] - 150.0f));
-        r = exp2_fast(l - lzs[lane]);
+        const double l = ill_logit_bounded<D64>(xs + lane * P, dmu + (size_t)comp * D64,
+                                                dh + (size_t)comp * D64, c0,
+                                                c0 - (lzs[lane] - 150.0));
+        r = exp2_fast((float)(l - lzs[lane]));
       }
-      rs[(wave * 8 + c) * 64 + lane] = r;
+      if (lane < PT) rs[(wave * CW + c) * PT + lane] = r;
       nz[c] = __ballot(r > 0.0f);
     }
     __syncthreads();
     // pairs with r == 0 add exactly nothing and are skipped; per component the
     // points are still taken in increasing order
 #pragma unroll
-    for (int c = 0; c < 8; ++c) {
+    for (int c = 0; c < CW; ++c) {
       unsigned long long msk = nz[c];
       while (msk) {
         const int p = __ffsll(msk) - 1;
         msk &= msk - 1;
-        const double r = (double)rs[(wave * 8 + c) * 64 + p];
+        const double r = (double)rs[(wave * CW + c) * PT + p];
         NK[c] += r;
 #pragma unroll
         for (int j = 0; j < NJ; ++j) {
@@ -1204,8 +1558,8 @@ __global__ __launch_bounds__(256) void k_stats_ill(
     }
   }
 #pragma unroll
-  for (int c = 0; c < 8; ++c) {
-    double* base = part + ((size_t)blockIdx.x * kBK + wave * 8 + c) * STRIDE;
+  for (int c = 0; c < CW; ++c) {
+    double* base = part + ((size_t)blockIdx.x * ICB + wave * CW + c) * STRIDE;
     if (lane == 0) base[0] = NK[c];
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
@@ -1254,12 +1608,12 @@ __global__ __launch_bounds__(256) void k_assign_theta(
     const float* __restrict__ x, int64_t n, int d, int vec4, const float4* __restrict__ wp,
     const float* __restrict__ cw, const int* __restrict__ counts, int tsel,
     float* __restrict__ theta) {
-  constexpr int P = D64 + 4;
-  __shared__ __align__(16) float xs[64 * P];
-  __shared__ float lmax[64][129];
+  constexpr int P = D64 + 4, NT = logz_tiles(D64), PTS = 32 * NT;
+  __shared__ __align__(16) float xs[PTS * P];
+  __shared__ float lmax[PTS][129];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, h = lane >> 5, col = lane & 31;
-  const int64_t n0 = (int64_t)blockIdx.x * 64;
-  load_tile<D64>(x, n, d, n0, 64, xs, vec4 != 0);
+  const int64_t n0 = (int64_t)blockIdx.x * PTS;
+  load_tile<D64>(x, n, d, n0, PTS, xs, vec4 != 0);
   __syncthreads();
   const int n_wkb = counts[2];
   float m0[16], m1[16];
@@ -1271,29 +1625,29 @@ __global__ __launch_bounds__(256) void k_assign_theta(
     f16v c0, c1, x0, x1;
     auto epi = [&](int v, float l0, float l1) {
       m0[v] = fmaxf(m0[v], l0);
-      m1[v] = fmaxf(m1[v], l1);
+      if constexpr (NT == 2) m1[v] = fmaxf(m1[v], l1);
     };
     if (nb > 0) {
-      logz_step<D64, true, false>(xs, wp + (size_t)wave * BS, cw[wave * kBK + col], c0, c1, x0,
-                                  x1, epi);
+      logz_step<D64, true, false, NT>(xs, wp + (size_t)wave * BS, cw[wave * kBK + col], c0, c1,
+                                      x0, x1, epi);
       for (int i = 0; i + 1 < nb; ++i) {
         const int kb = wave + 4 * i;
-        logz_step<D64, true, true>(xs, wp + (size_t)(kb + 4) * BS, cw[(kb + 4) * kBK + col], x0,
-                                   x1, c0, c1, epi);
+        logz_step<D64, true, true, NT>(xs, wp + (size_t)(kb + 4) * BS, cw[(kb + 4) * kBK + col],
+                                       x0, x1, c0, c1, epi);
         c0 = x0;
         c1 = x1;
       }
-      logz_step<D64, false, true>(xs, wp, 0.0f, x0, x1, c0, c1, epi);
+      logz_step<D64, false, true, NT>(xs, wp, 0.0f, x0, x1, c0, c1, epi);
     }
   }
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
     const int p = 8 * (v >> 2) + 4 * h + (v & 3);
     lmax[p][wave * 32 + col] = m0[v];
-    lmax[32 + p][wave * 32 + col] = m1[v];
+    if constexpr (NT == 2) lmax[32 + p][wave * 32 + col] = m1[v];
   }
   __syncthreads();
-  if (tid < 64 && n0 + tid < n) {
+  if (tid < PTS && n0 + tid < n) {
     float tl[kTMax];
 #pragma unroll
     for (int j = 0; j < kTMax; ++j) tl[j] = -INFINITY;
@@ -1320,21 +1674,21 @@ __global__ __launch_bounds__(256) void k_assign_collect(
     const float* __restrict__ x, int64_t n, int d, int vec4, const float4* __restrict__ wp,
     const float* __restrict__ cw, const int* __restrict__ well_idx,
     const int* __restrict__ ill_idx, const float* __restrict__ dmu,
-    const float* __restrict__ dh, const float* __restrict__ dc, const int* __restrict__ counts,
+    const double* __restrict__ dh, const int* __restrict__ counts,
     const float* __restrict__ theta, const float* __restrict__ mu,
     const float* __restrict__ var, const double* __restrict__ cdir, int m, float tau,
     int* __restrict__ idx, float* __restrict__ resp, int* __restrict__ ovf) {
-  constexpr int P = D64 + 4;
-  __shared__ __align__(16) float xs[64 * P];
-  __shared__ int ccnt[64];
-  __shared__ int cand[64][kACap];          // well slot s >= 0, or -(ill component + 1)
-  __shared__ double cl[64][kACap];
-  __shared__ float2 stw[4][64];
-  __shared__ float2 sti[4][64];
+  constexpr int P = D64 + 4, NT = logz_tiles(D64), PTS = 32 * NT;
+  __shared__ __align__(16) float xs[PTS * P];
+  __shared__ int ccnt[PTS];
+  __shared__ int cand[PTS][kACap];         // well slot s >= 0, or -(ill component + 1)
+  __shared__ double cl[PTS][kACap];
+  __shared__ float2 stw[4][PTS];
+  __shared__ float2 sti[4][PTS];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, h = lane >> 5, col = lane & 31;
-  const int64_t n0 = (int64_t)blockIdx.x * 64;
-  load_tile<D64>(x, n, d, n0, 64, xs, vec4 != 0);
-  if (tid < 64) ccnt[tid] = 0;
+  const int64_t n0 = (int64_t)blockIdx.x * PTS;
+  load_tile<D64>(x, n, d, n0, PTS, xs, vec4 != 0);
+  if (tid < PTS) ccnt[tid] = 0;
   __syncthreads();
   const int n_wkb = counts[2], n_ill = counts[1];
   float th0[16], th1[16], m0[16], s0[16], m1[16], s1[16];
@@ -1342,7 +1696,7 @@ __global__ __launch_bounds__(256) void k_assign_collect(
   for (int v = 0; v < 16; ++v) {
     const int p = 8 * (v >> 2) + 4 * h + (v & 3);
     th0[v] = n0 + p < n ? theta[n0 + p] : INFINITY;
-    th1[v] = n0 + 32 + p < n ? theta[n0 + 32 + p] : INFINITY;
+    th1[v] = (NT == 2 && n0 + 32 + p < n) ? theta[n0 + 32 + p] : INFINITY;
     m0[v] = m1[v] = kEmpty;
     s0[v] = s1[v] = 0.0f;
   }
@@ -1359,26 +1713,28 @@ __global__ __launch_bounds__(256) void k_assign_collect(
       } else {
         lse_add_e(m0[v], s0[v], l0);
       }
-      if (l1 >= th1[v] && l1 > -INFINITY) {
-        const int pos = atomicAdd(&ccnt[32 + p], 1);
-        if (pos < kACap) cand[32 + p][pos] = slot;
-      } else {
-        lse_add_e(m1[v], s1[v], l1);
+      if constexpr (NT == 2) {
+        if (l1 >= th1[v] && l1 > -INFINITY) {
+          const int pos = atomicAdd(&ccnt[32 + p], 1);
+          if (pos < kACap) cand[32 + p][pos] = slot;
+        } else {
+          lse_add_e(m1[v], s1[v], l1);
+        }
       }
     };
     if (nb > 0) {
-      logz_step<D64, true, false>(xs, wp + (size_t)wave * BS, cw[wave * kBK + col], c0, c1, x0,
-                                  x1, epi);
+      logz_step<D64, true, false, NT>(xs, wp + (size_t)wave * BS, cw[wave * kBK + col], c0, c1,
+                                      x0, x1, epi);
       for (int i = 0; i + 1 < nb; ++i) {
         const int kb = wave + 4 * i;
         slot = kb * kBK + col;
-        logz_step<D64, true, true>(xs, wp + (size_t)(kb + 4) * BS, cw[(kb + 4) * kBK + col], x0,
-                                   x1, c0, c1, epi);
+        logz_step<D64, true, true, NT>(xs, wp + (size_t)(kb + 4) * BS, cw[(kb + 4) * kBK + col],
+                                       x0, x1, c0, c1, epi);
         c0 = x0;
         c1 = x1;
       }
       slot = (wave + 4 * (nb - 1)) * kBK + col;
-      logz_step<D64, false, true>(xs, wp, 0.0f, x0, x1, c0, c1, epi);
+      logz_step<D64, false, true, NT>(xs, wp, 0.0f, x0, x1, c0, c1, epi);
     }
   }
 #pragma unroll
@@ -1387,21 +1743,21 @@ __global__ __launch_bounds__(256) void k_assign_collect(
     float M0 = m0[v], S0 = s0[v], M1 = m1[v], S1 = s1[v];
     for (int off = 16; off > 0; off >>= 1) {
       lse_merge(M0, S0, __shfl_xor(M0, off), __shfl_xor(S0, off));
-      lse_merge(M1, S1, __shfl_xor(M1, off), __shfl_xor(S1, off));
+      if constexpr (NT == 2) lse_merge(M1, S1, __shfl_xor(M1, off), __shfl_xor(S1, off));
     }
     if (col == 0) {
       stw[wave][p] = make_float2(M0, S0);
-      stw[wave][32 + p] = make_float2(M1, S1);
+      if constexpr (NT == 2) stw[wave][32 + p] = make_float2(M1, S1);
     }
   }
-  {
+  if (lane < PTS) {
     // ill-conditioned components, direct form, lane = point
     const float thl = n0 + lane < n ? theta[n0 + lane] : INFINITY;
     float mi = kEmpty, si = 0.0f;
     for (int ki = wave; ki < n_ill; ki += 4) {
       const int comp = ill_idx[ki];
-      const float l = ill_logit<D64>(xs + lane * P, dmu + (size_t)comp * D64,
-                                     dh + (size_t)comp * D64, dc[comp]);
+      const float l = (float)ill_logit<D64>(xs + lane * P, dmu + (size_t)comp * D64,
+                                            dh + (size_t)comp * D64, cdir[comp]);
       if (l >= thl && l > -INFINITY) {
         const int pos = atomicAdd(&ccnt[lane], 1);
         if (pos < kACap) cand[lane][pos] = -(comp + 1);
@@ -1412,7 +1768,7 @@ __global__ __launch_bounds__(256) void k_assign_collect(
     sti[wave][lane] = make_float2(mi, si);
   }
   __syncthreads();
-  {
+  if (lane < PTS) {
     // exact fp64 log-densities of the candidates, spread over the waves
     const int p = lane;
     const int cnt = ccnt[p];
@@ -1425,7 +1781,7 @@ __global__ __launch_bounds__(256) void k_assign_collect(
     }
   }
   __syncthreads();
-  if (tid < 64 && n0 + tid < n) {
+  if (tid < PTS && n0 + tid < n) {
     const int p = tid;
     const int64_t nn = n0 + p;
     const int cnt = ccnt[p];
@@ -1571,12 +1927,18 @@ __global__ __launch_bounds__(256) void k_assign_fallback(
 }
 
 // ---------------------------------------------------------------- fixed-order reductions
+// Partial layouts (rows of 1 + 2 D64 fp64: N, then S over D64, then Q):
+//   well    ((slot / wbk) * nch + chunk) * wbk + slot % wbk
+//   sparse  ((slot / sbk) * nparts + part) * sbk + slot % sbk
+//   ill     ((islot / ibk) * nchk + chunk) * ibk + islot % ibk
+// summed here in chunk (part) order.
 __global__ __launch_bounds__(256) void k_reduce_stats(
     const double* __restrict__ part_w, const double* __restrict__ part_s,
     const double* __restrict__ part_i,
     const int* __restrict__ counts, const int* __restrict__ well_idx,
-    const int* __restrict__ ill_idx, int nch, int nch_s, int grid_i, int64_t n, int k, int d,
-    int D64, double* __restrict__ nk, double* __restrict__ s, double* __restrict__ q) {
+    const int* __restrict__ ill_idx, int nch, int wbk, int nparts, int sbk, int grid_i, int ibk,
+    int ipt, int64_t n, int k, int d, int D64, double* __restrict__ nk, double* __restrict__ s,
+    double* __restrict__ q) {
   const int64_t width = 1 + 2 * (int64_t)d;
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= 2 * (int64_t)k * width) return;
@@ -1585,22 +1947,23 @@ __global__ __launch_bounds__(256) void k_reduce_stats(
   const int slot = (int)(rem / width), c = (int)(rem % width);
   const int64_t stride = 1 + 2 * (int64_t)D64;
   const int64_t off = c == 0 ? 0 : (c <= d ? 1 + (c - 1) : 1 + D64 + (c - 1 - d));
-  const int dim = c == 0 ? 0 : (c <= d ? c - 1 : c - 1 - d);
   double acc = 0.0;
   int comp;
   if (which == 0) {
     if (slot >= counts[0]) return;
     comp = well_idx[slot];
-    const double* p = part_w + ((size_t)(slot / kWB) * nch * kWB + (slot % kWB)) * stride + off;
-    for (int ch = 0; ch < nch; ++ch) acc += p[(size_t)ch * kWB * stride];
-    const double* ps = part_s + ((size_t)(slot / kBK) * nch_s * kBK + (slot % kBK)) * stride + off;
-    for (int ch = 0; ch < nch_s; ++ch) acc += ps[(size_t)ch * kBK * stride];
+    const double* p = part_w + ((size_t)(slot / wbk) * nch * wbk + (slot % wbk)) * stride + off;
+    for (int ch = 0; ch < nch; ++ch) acc += p[(size_t)ch * wbk * stride];
+    const double* ps =
+        part_s + ((size_t)(slot / sbk) * nparts * sbk + (slot % sbk)) * stride + off;
+    for (int ch = 0; ch < nparts; ++ch) acc += ps[(size_t)ch * sbk * stride];
   } else {
     if (slot >= counts[1]) return;
     comp = ill_idx[slot];
-    const int nchk = ill_chunks(grid_i, counts[3], n);
-    const double* p = part_i + ((size_t)(slot / kBK) * nchk * kBK + (slot % kBK)) * stride + off;
-    for (int ch = 0; ch < nchk; ++ch) acc += p[(size_t)ch * kBK * stride];
+    const int n_ikb = (counts[1] + ibk - 1) / ibk;
+    const int nchk = ill_chunks(grid_i, n_ikb, n, ipt);
+    const double* p = part_i + ((size_t)(slot / ibk) * nchk * ibk + (slot % ibk)) * stride + off;
+    for (int ch = 0; ch < nchk; ++ch) acc += p[(size_t)ch * ibk * stride];
   }
   if (c == 0) nk[comp] += acc;
   else if (c <= d) s[(int64_t)comp * d + (c - 1)] += acc;
@@ -1660,42 +2023,72 @@ inline size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 struct Layout {
   int64_t n;
   int d, k, kpad, D64, m;
-  int nch, grid_i, nch_s;   // nch: chunks of k_stats_well (64-component blocks)
-  int64_t chunk_s;
-  int64_t chunk, n_wg_logz;
+  bool wide;                // D64 > 256: 32-point screening tiles
+  int wbk, nch;             // well statistics: components per workgroup (64 for
+                            // k_stats_well, 16 for k_stats_wide at D64 >= 256), chunks
+  int64_t chunk;
+  int ibk, ipt, grid_i;     // ill set: components per block, points per tile, grid
+  int sbk, lsbk, nb;        // refined pairs: bucket size (log2), buckets
+  int nunit, nparts;        // refined pairs: units, parts per bucket
+  int64_t upts;
+  int pts_logz;
+  int64_t n_wg_logz;
   size_t off_counts, off_cls, off_cwell, off_cdir, off_cthr, off_thr, off_well_idx, off_ill_idx,
-      off_cw, off_wp, off_wq,
-      off_dmu, off_dh, off_dc, off_logz2, off_cslot, off_cr, off_llpart, off_part_w, off_part_s, off_part_i,
-      off_fit_nk, off_fit_s, off_fit_q, total;
+      off_cw, off_wp, off_wq, off_dmu, off_dh, off_logz2, off_cslot, off_cr, off_llpart,
+      off_part_w, off_part_s, off_part_i, off_scnt, off_soff, off_slist, off_fit_nk, off_fit_s,
+      off_fit_q, total;
 };
+
+// Padded dimension count of the kernels: a multiple of 64 up to 256, of 128 above.
+inline int padded_d(int d) { return d <= 256 ? (int)cdiv(d, 64) * 64 : (int)cdiv(d, 128) * 128; }
 
 bool make_layout(int64_t n, int d, int k, int m, Layout* L) {
   if (n < 1 || d < 1 || k < 1 || d > GMM_MAX_D || k > GMM_MAX_K || m < 0 || m > GMM_MAX_M)
     return false;
   L->n = n; L->d = d; L->k = k; L->m = m;
   L->kpad = (int)cdiv(k, kWB) * kWB;
-  L->D64 = (int)cdiv(d, 64) * 64;
-  const int nkb = L->kpad / kBK;
-  const int nwb = L->kpad / kWB;
-  // chunking depends only on (n, k), never on the device: about 512
-  // workgroups (two per CU) for k_stats_well
-  int maxc = 512 / nwb;
-  if (maxc < 8) maxc = 8;
-  int64_t c = cdiv(n, 1024);
-  if (c > maxc) c = maxc;
-  if (c >= 8) c = c / 8 * 8;
-  L->nch = (int)(c < 1 ? 1 : c);
-  L->chunk = cdiv(n, L->nch);
-  {
-    int maxs = 2048 / nkb;
-    if (maxs < 8) maxs = 8;
-    int64_t cs = cdiv(n, 4096);
-    if (cs > maxs) cs = maxs;
-    L->nch_s = (int)(cs < 1 ? 1 : cs);
-    L->chunk_s = cdiv(n, L->nch_s);
+  L->D64 = padded_d(d);
+  L->wide = L->D64 > 256;
+  const int stride = 1 + 2 * L->D64;
+  // chunking depends only on (n, d, k), never on the device
+  L->wbk = L->D64 >= 256 ? 16 : kWB;
+  const int nwb = L->kpad / L->wbk;
+  if (L->D64 < 256) {
+    // about 512 workgroups (two per CU) for k_stats_well
+    int maxc = 512 / nwb;
+    if (maxc < 8) maxc = 8;
+    int64_t c = cdiv(n, 1024);
+    if (c > maxc) c = maxc;
+    if (c >= 8) c = c / 8 * 8;
+    L->nch = (int)(c < 1 ? 1 : c);
+  } else {
+    int maxc = 2048 / nwb;
+    if (maxc < 1) maxc = 1;
+    int64_t c = cdiv(n, 1024);
+    if (c > maxc) c = maxc;
+    L->nch = (int)(c < 1 ? 1 : c);
   }
-  L->grid_i = nkb > 512 ? nkb : 512;
-  L->n_wg_logz = cdiv(n, 64);
+  L->chunk = cdiv(n, L->nch);
+  L->sbk = L->wide ? (L->D64 <= 512 ? 8 : 4) : (L->D64 <= 128 ? 32 : 16);
+  L->lsbk = L->sbk == 32 ? 5 : (L->sbk == 16 ? 4 : (L->sbk == 8 ? 3 : 2));
+  L->nb = L->kpad / L->sbk;
+  {
+    int64_t u = cdiv(n, 256);
+    const int64_t cap = kSparseTab / L->nb;
+    if (u > cap) u = cap;
+    L->nunit = (int)(u < 1 ? 1 : u);
+    L->upts = cdiv(n, L->nunit);
+    int pp = 2048 / L->nb;
+    L->nparts = pp < 1 ? 1 : pp;
+  }
+  L->ipt = L->D64 <= 256 ? 64 : (L->D64 <= 512 ? 32 : 16);
+  L->ibk = 4 * (L->D64 <= 256 ? 8 : (L->D64 <= 512 ? 4 : 2));
+  {
+    const int nib = (int)cdiv(k, L->ibk);
+    L->grid_i = nib > 512 ? nib : 512;
+  }
+  L->pts_logz = L->D64 <= 256 ? 64 : 32;
+  L->n_wg_logz = cdiv(n, L->pts_logz);
   size_t o = 0;
   auto take = [&](size_t bytes) { const size_t r = o; o = align256(o + bytes); return r; };
   L->off_counts = take(16 * sizeof(int));
@@ -1710,16 +2103,18 @@ bool make_layout(int64_t n, int d, int k, int m, Layout* L) {
   L->off_wp = take((size_t)L->kpad * 2 * L->D64 * sizeof(float));
   L->off_wq = take((size_t)(L->kpad / 16) * (L->D64 / 2 + L->D64 / 32) * 64 * sizeof(float));
   L->off_dmu = take((size_t)k * L->D64 * sizeof(float));
-  L->off_dh = take((size_t)k * L->D64 * sizeof(float));
-  L->off_dc = take((size_t)k * sizeof(float));
-  L->off_logz2 = take((size_t)n * sizeof(float));
+  L->off_dh = take((size_t)k * L->D64 * sizeof(double));
+  L->off_logz2 = take((size_t)n * sizeof(double));
   // refined slots (16-bit); gmm_assign_topk reuses the region for n int flags
   L->off_cslot = take((size_t)n * kT * sizeof(unsigned short));
   L->off_cr = take((size_t)n * kT * sizeof(float));
   L->off_llpart = take((size_t)L->n_wg_logz * sizeof(double));
-  L->off_part_w = take((size_t)nwb * L->nch * kWB * (1 + 2 * (size_t)L->D64) * sizeof(double));
-  L->off_part_s = take((size_t)nkb * L->nch_s * kBK * (1 + 2 * (size_t)L->D64) * sizeof(double));
-  L->off_part_i = take((size_t)L->grid_i * kBK * (1 + 2 * (size_t)L->D64) * sizeof(double));
+  L->off_part_w = take((size_t)nwb * L->nch * L->wbk * stride * sizeof(double));
+  L->off_part_s = take((size_t)L->nb * L->nparts * L->sbk * stride * sizeof(double));
+  L->off_part_i = take((size_t)L->grid_i * L->ibk * stride * sizeof(double));
+  L->off_scnt = take((size_t)L->nb * L->nunit * sizeof(int));
+  L->off_soff = take(((size_t)L->nb * L->nunit + 1) * sizeof(int64_t));
+  L->off_slist = take((size_t)n * kT * sizeof(SPair));
   L->off_fit_nk = take((size_t)k * sizeof(double) + sizeof(double));  // + loglik slot
   L->off_fit_s = take((size_t)k * d * sizeof(double));
   L->off_fit_q = take((size_t)k * d * sizeof(double));
@@ -1753,11 +2148,10 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
   float4* wp = at<float4>(ws, L.off_wp);
   float* wq = at<float>(ws, L.off_wq);
   float* dmu = at<float>(ws, L.off_dmu);
-  float* dh = at<float>(ws, L.off_dh);
-  float* dc = at<float>(ws, L.off_dc);
+  double* dh = at<double>(ws, L.off_dh);
   unsigned short* cslot = at<unsigned short>(ws, L.off_cslot);
   float* cr = at<float>(ws, L.off_cr);
-  float* logz2 = at<float>(ws, L.off_logz2);
+  double* logz2 = at<double>(ws, L.off_logz2);
   double* llpart = at<double>(ws, L.off_llpart);
   double* part_w = at<double>(ws, L.off_part_w);
   double* part_s = at<double>(ws, L.off_part_s);
@@ -1776,22 +2170,39 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
                        dim3(256), 0, st, w, mu, var, d, kpad, counts, well_idx, wq);
     const int64_t toti = (int64_t)k * D64;
     hipLaunchKernelGGL(k_prep_pack_direct<D64>, dim3((unsigned)cdiv(toti, 256)), dim3(256), 0,
-                       st, mu, var, d, k, cdir, dmu, dh, dc);
+                       st, mu, var, d, k, dmu, dh);
   }
   hipLaunchKernelGGL(k_logz<D64>, dim3((unsigned)L.n_wg_logz), dim3(256), 0, st, x, n, d, vec4,
-                     wp, cw, thr, well_idx, ill_idx, dmu, dh, dc, counts, logz2, cslot, cr,
+                     wp, cw, thr, well_idx, ill_idx, dmu, dh, cdir, counts, logz2, cslot, cr,
                      llpart);
-  hipLaunchKernelGGL(k_stats_well<D64>, dim3((unsigned)((kpad / kWB) * L.nch)), dim3(256),
-                     0, st, x, n, d, vec4, wq, cw, counts, logz2, cslot, L.nch, L.chunk, part_w);
-  hipLaunchKernelGGL(k_stats_sparse<D64>, dim3((unsigned)((kpad / kBK) * L.nch_s)), dim3(256), 0,
-                     st, x, n, d, counts, cslot, cr, L.nch_s, L.chunk_s, part_s);
+  if constexpr (D64 < 256) {
+    hipLaunchKernelGGL(k_stats_well<D64>, dim3((unsigned)((kpad / kWB) * L.nch)), dim3(256), 0,
+                       st, x, n, d, vec4, wq, cw, counts, logz2, cslot, L.nch, L.chunk, part_w);
+  } else {
+    hipLaunchKernelGGL(k_stats_wide<D64>, dim3((unsigned)((kpad / 16) * L.nch)),
+                       dim3(64 * (D64 / 128)), 0, st, x, n, d, vec4, wq, cwell, well_idx, counts,
+                       logz2, cslot, L.nch, L.chunk, part_w);
+  }
+  {
+    int* scnt = at<int>(ws, L.off_scnt);
+    int64_t* soff = at<int64_t>(ws, L.off_soff);
+    SPair* slist = at<SPair>(ws, L.off_slist);
+    const size_t lds = (size_t)L.nb * sizeof(int);
+    hipLaunchKernelGGL(k_sparse_count, dim3((unsigned)L.nunit), dim3(64), lds, st, cslot, n,
+                       L.upts, L.nb, L.lsbk, L.nunit, scnt);
+    hipLaunchKernelGGL(k_sparse_scan, dim3(1), dim3(1024), 0, st, scnt, L.nb * L.nunit, soff);
+    hipLaunchKernelGGL(k_sparse_scatter, dim3((unsigned)L.nunit), dim3(64), lds, st, cslot, cr,
+                       n, L.upts, L.nb, L.lsbk, L.nunit, soff, slist);
+    hipLaunchKernelGGL(k_stats_sparse<D64>, dim3((unsigned)(L.nb * L.nparts)), dim3(256), 0, st,
+                       x, n, d, slist, soff, L.nunit, L.nparts, part_s);
+  }
   hipLaunchKernelGGL(k_stats_ill<D64>, dim3((unsigned)L.grid_i), dim3(256), 0, st, x, n, d, vec4,
-                     ill_idx, dmu, dh, dc, counts, logz2, part_i);
+                     ill_idx, dmu, dh, cdir, counts, logz2, part_i);
   {
     const int64_t tot = 2 * (int64_t)k * (1 + 2 * (int64_t)d);
     hipLaunchKernelGGL(k_reduce_stats, dim3((unsigned)cdiv(tot, 256)), dim3(256), 0, st, part_w,
-                       part_s, part_i, counts, well_idx, ill_idx, L.nch, L.nch_s, L.grid_i, n, k, d,
-                       D64, nk, s, q);
+                       part_s, part_i, counts, well_idx, ill_idx, L.nch, L.wbk, L.nparts, L.sbk,
+                       L.grid_i, L.ibk, L.ipt, n, k, d, D64, nk, s, q);
   }
   hipLaunchKernelGGL(k_reduce_ll, dim3(1), dim3(1024), 0, st, llpart, L.n_wg_logz, loglik,
                      ll_accumulate);
@@ -1815,8 +2226,7 @@ int assign_impl(const Layout& L, const float* x, const float* w, const float* mu
   float* cw = at<float>(ws, L.off_cw);
   float4* wp = at<float4>(ws, L.off_wp);
   float* dmu = at<float>(ws, L.off_dmu);
-  float* dh = at<float>(ws, L.off_dh);
-  float* dc = at<float>(ws, L.off_dc);
+  double* dh = at<double>(ws, L.off_dh);
   float* theta = at<float>(ws, L.off_logz2);      // n floats, free during assignment
   int* ovf = at<int>(ws, L.off_cslot);            // n ints, likewise
   const int vec4 = ((d & 3) == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0) ? 1 : 0;
@@ -1829,26 +2239,29 @@ int assign_impl(const Layout& L, const float* x, const float* w, const float* mu
                        mu, var, d, kpad, cwell, cthr, counts, well_idx, wp, cw, thr);
     const int64_t toti = (int64_t)k * D64;
     hipLaunchKernelGGL(k_prep_pack_direct<D64>, dim3((unsigned)cdiv(toti, 256)), dim3(256), 0,
-                       st, mu, var, d, k, cdir, dmu, dh, dc);
+                       st, mu, var, d, k, dmu, dh);
   }
   hipLaunchKernelGGL(k_assign_theta<D64>, dim3((unsigned)L.n_wg_logz), dim3(256), 0, st, x, n, d,
                      vec4, wp, cw, counts, m + 2, theta);
   hipLaunchKernelGGL(k_assign_collect<D64>, dim3((unsigned)L.n_wg_logz), dim3(256), 0, st, x, n,
-                     d, vec4, wp, cw, well_idx, ill_idx, dmu, dh, dc, counts, theta, mu, var,
+                     d, vec4, wp, cw, well_idx, ill_idx, dmu, dh, counts, theta, mu, var,
                      cdir, m, tau, idx, resp, ovf);
   hipLaunchKernelGGL(k_assign_fallback, dim3((unsigned)cdiv(n, 1024)), dim3(256), 0, st, x, n, d,
                      k, mu, var, cdir, m, tau, ovf, idx, resp);
   return launch_status();
 }
 
+#define GMM_FOR_EACH_D64(X) \
+  X(64) X(128) X(192) X(256) X(384) X(512) X(640) X(768) X(896) X(1024)
+
 int estep_dispatch(const Layout& L, const float* x, const float* w, const float* mu,
                    const float* var, double* nk, double* s, double* q, double* loglik,
                    int ll_accumulate, void* ws, hipStream_t st) {
   switch (L.D64) {
-    case 64: return estep_impl<64>(L, x, w, mu, var, nk, s, q, loglik, ll_accumulate, ws, st);
-    case 128: return estep_impl<128>(L, x, w, mu, var, nk, s, q, loglik, ll_accumulate, ws, st);
-    case 192: return estep_impl<192>(L, x, w, mu, var, nk, s, q, loglik, ll_accumulate, ws, st);
-    case 256: return estep_impl<256>(L, x, w, mu, var, nk, s, q, loglik, ll_accumulate, ws, st);
+#define GMM_CASE(D) \
+  case D: return estep_impl<D>(L, x, w, mu, var, nk, s, q, loglik, ll_accumulate, ws, st);
+    GMM_FOR_EACH_D64(GMM_CASE)
+#undef GMM_CASE
     default: return GMM_ERR_UNSUPPORTED;
   }
 }
@@ -1956,10 +2369,10 @@ int gmm_assign_topk(const float* x, int64_t n, int32_t d, int32_t k, const float
   rc = check_ws(L, ws, ws_bytes);
   if (rc != GMM_OK) return rc;
   switch (L.D64) {
-    case 64: return assign_impl<64>(L, x, weights, means, vars, m, tau, idx, resp, ws, stream);
-    case 128: return assign_impl<128>(L, x, weights, means, vars, m, tau, idx, resp, ws, stream);
-    case 192: return assign_impl<192>(L, x, weights, means, vars, m, tau, idx, resp, ws, stream);
-    case 256: return assign_impl<256>(L, x, weights, means, vars, m, tau, idx, resp, ws, stream);
+#define GMM_CASE(D) \
+  case D: return assign_impl<D>(L, x, weights, means, vars, m, tau, idx, resp, ws, stream);
+    GMM_FOR_EACH_D64(GMM_CASE)
+#undef GMM_CASE
     default: return GMM_ERR_UNSUPPORTED;
   }
 }

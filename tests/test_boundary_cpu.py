@@ -36,26 +36,29 @@ def test_status_strings():
 
 @pytest.mark.parametrize("n,d,k", [(1, 1, 1), (10_000, 16, 8), (100_000, 128, 1024),
                                    (100_000_000, 128, 1024), (1_000_003, 37, 45),
-                                   (5_000, 256, 65535)])
+                                   (5_000, 256, 65535), (5_000_000, 768, 4096), (1_000, 1024, 64),
+                                   (3_000, 300, 17)])
 def test_workspace_is_o_n_plus_o_kd(n, d, k):
     nb = gmm.workspace_bytes(n, d, k)
     assert nb > 0 and nb % 256 == 0
-    # per point: one fp32 log-normaliser, 4 refined (16-bit slot, fp32 responsibility) pairs and
-    # 1/8 of an fp64 log-likelihood partial; plus O(k d) parameters and partial statistics:
-    # never an n x k array
-    assert nb >= 28 * n
-    d64 = (d + 63) // 64 * 64
+    # per point: one fp64 log-normaliser, 4 refined (16-bit slot, fp32 responsibility) pairs,
+    # room for 4 bucketed pair records (16 B each) and at most 1/4 of an fp64 log-likelihood
+    # partial; plus O(k d) parameters and partial statistics: never an n x k array
+    assert nb >= 96 * n
+    dp = (d + 63) // 64 * 64 if d <= 256 else (d + 127) // 128 * 128
     kpad = (k + 63) // 64 * 64
-    well_part = 8 * (1 + 2 * d64) * max(8 * kpad, 512 * 64)
-    ill_part = 8 * (1 + 2 * d64) * 32 * max(512, kpad // 32)
-    sparse_part = 8 * (1 + 2 * d64) * max(8 * kpad, 2048 * 32)
-    okd = well_part + sparse_part + ill_part + 40 * kpad * d64 + 8 * 2 * k * d
-    assert nb <= 28 * n + n // 8 + okd + 64 * k + (1 << 16)
-    if n >= 10 ** 7:
+    row = 8 * (1 + 2 * dp)
+    well_part = row * max(8 * kpad, 512 * 64)
+    sparse_part = row * max(kpad, 2048 * 32)
+    ill_part = row * max(kpad + 32, 512 * 32)
+    okd = well_part + sparse_part + ill_part + 40 * kpad * dp + 8 * 2 * k * d
+    assert nb <= 96 * n + n // 4 + okd + 64 * k + (4 << 20)
+    if n >= 10 ** 6 and k >= 1024:
+        # a small fraction of what an n x k fp32 responsibility array would take
         assert nb < n * k * 4 / 25
 
 
-@pytest.mark.parametrize("n,d,k,m", [(0, 8, 4, 0), (10, 0, 4, 0), (10, 8, 0, 0), (10, 257, 4, 0),
+@pytest.mark.parametrize("n,d,k,m", [(0, 8, 4, 0), (10, 0, 4, 0), (10, 8, 0, 0), (10, 1025, 4, 0),
                                      (10, 8, 65536, 0), (10, 8, 4, 9), (10, 8, 4, -1)])
 def test_workspace_rejects_bad_shapes(n, d, k, m):
     assert gmm.workspace_bytes(n, d, k, m) == 0
@@ -72,7 +75,7 @@ def test_host_validation_returns_before_any_launch():
     # non-positive sizes and null pointers
     assert lib.gmm_estep_accumulate(p, 0, 8, 4, p, p, p, p, p, p, p, ws, big, None) == gmm.GMM_ERR_INVALID_ARG
     assert lib.gmm_estep_accumulate(p, 1000, 8, 4, None, p, p, p, p, p, p, ws, big, None) == gmm.GMM_ERR_INVALID_ARG
-    assert lib.gmm_estep_accumulate(p, 1000, 300, 4, p, p, p, p, p, p, p, ws, big, None) == gmm.GMM_ERR_UNSUPPORTED
+    assert lib.gmm_estep_accumulate(p, 1000, 1025, 4, p, p, p, p, p, p, p, ws, big, None) == gmm.GMM_ERR_UNSUPPORTED
     # workspace: missing, misaligned, too small
     assert lib.gmm_estep_accumulate(p, 1000, 8, 4, p, p, p, p, p, p, p, None, big, None) == gmm.GMM_ERR_WORKSPACE
     assert lib.gmm_estep_accumulate(p, 1000, 8, 4, p, p, p, p, p, p, p, _fake(0x200010), big, None) == gmm.GMM_ERR_WORKSPACE
@@ -99,7 +102,7 @@ def test_assign_host_validation():
     assert call(2, 1.0) == gmm.GMM_ERR_INVALID_ARG            # tau >= 1
     assert call(2, float("nan")) == gmm.GMM_ERR_INVALID_ARG
     assert call(2, 0.1, idx=None) == gmm.GMM_ERR_INVALID_ARG
-    assert call(2, 0.1, d=300) == gmm.GMM_ERR_UNSUPPORTED
+    assert call(2, 0.1, d=1025) == gmm.GMM_ERR_UNSUPPORTED
     assert call(2, 0.1, n=0) == gmm.GMM_ERR_INVALID_ARG
     assert call(2, 0.1, ws=None) == gmm.GMM_ERR_WORKSPACE
     assert call(2, 0.1, wsb=big - 1) == gmm.GMM_ERR_WORKSPACE

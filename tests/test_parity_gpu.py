@@ -43,7 +43,10 @@ def test_tiny_teacher_forced_all_iterations():
 @pytest.mark.parametrize("n,d,kt,k", [
     (1, 16, 3, 1), (5, 3, 2, 2), (63, 16, 3, 5), (1000, 37, 6, 45), (5000, 100, 20, 33),
     (3001, 128, 40, 64), (2049, 200, 10, 17), (777, 256, 8, 8), (4000, 64, 5, 1),
-    (20000, 8, 4, 300), (1500, 150, 7, 40)])
+    (20000, 8, 4, 300), (1500, 150, 7, 40),
+    # wide D: 32-point screening tiles, dimensions split over the statistics waves
+    (2000, 300, 8, 24), (1500, 513, 6, 20), (1200, 768, 10, 70), (800, 1024, 5, 16),
+    (2500, 640, 12, 33), (900, 1000, 4, 9)])
 def test_ragged_shapes(n, d, kt, k):
     """Shapes off every tile boundary: points, dimensions and components."""
     w = g.custom(f"r{n}_{d}_{k}", n, d, kt, max(k, 1), data_seed=n + d, init_seed=k + 17)
