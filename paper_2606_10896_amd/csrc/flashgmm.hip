@@ -66,9 +66,11 @@ constexpr unsigned short kNoSlot = 0xFFFF;
 // top-kT list then holds a point's largest pairs even when they are tiny:
 // those pairs carry the variance of a component that sits on a few points.
 constexpr double kWideWindow = 40.0;
-// a lane state whose components other than its arg-max carry more than this
-// share of the point's screened mass is refined in full
-constexpr float kFullMass = 0x1p-20f;
+// a lane state whose components other than its arg-max carry a screened mass
+// whose error bound exceeds this share of the point's total is refined in full
+constexpr float kFullErr = 0x1p-20f;
+// refinement list entries held in LDS at a time by k_logz
+constexpr int kRefCap = 1024;
 constexpr double kNarrowWindow = 10.0;
 constexpr double kLooseBound = -12.0;
 
@@ -239,7 +241,7 @@ __global__ __launch_bounds__(64) void k_prep_class(const float* __restrict__ w,
                                                    int* __restrict__ cls,
                                                    double* __restrict__ cwell,
                                                    double* __restrict__ cdir,
-                                                   float* __restrict__ cthr) {
+                                                   float2* __restrict__ cthr) {
   const int comp = blockIdx.x, lane = threadIdx.x;
   double e = 0.0, lg = 0.0;
   for (int j = lane; j < d; j += 64) {
@@ -264,7 +266,13 @@ __global__ __launch_bounds__(64) void k_prep_class(const float* __restrict__ w,
     // screening error bound: about u * sum of |terms|, the terms of size
     // log2(e) * (mu^2 + x^2) / var for x near mu; taken as 4 u log2(e) (e + d)
     const double ldelta = -22.0 + log2(kLog2e * (e + d));
-    cthr[comp] = (float)(ldelta > kLooseBound ? -kWideWindow : -kNarrowWindow);
+    // relative error bound of a screened responsibility: 4 u per step of the
+    // running sum, over sqrt(2 d) steps of a random walk, the running sum of the
+    // size of the constant plus the terms, in log2 units, times ln 2
+    const double mag = fabs(kLog2e * (lw - 0.5 * (e + lg))) + kLog2e * (e + d);
+    const double feb = kLn2 * 0x1p-22 * sqrt(2.0 * d) * mag;
+    cthr[comp] = make_float2((float)(ldelta > kLooseBound ? -kWideWindow : -kNarrowWindow),
+                             wk > 0.0 ? (float)feb : 0.0f);
   }
 }
 
@@ -305,9 +313,9 @@ __global__ __launch_bounds__(256) void k_prep_scan(const int* __restrict__ cls, 
 template <int D64>
 __global__ __launch_bounds__(256) void k_prep_pack_well(
     const float* __restrict__ mu, const float* __restrict__ var, int d, int kpad,
-    const double* __restrict__ cwell, const float* __restrict__ cthr,
+    const double* __restrict__ cwell, const float2* __restrict__ cthr,
     const int* __restrict__ counts, const int* __restrict__ well_idx, float4* __restrict__ wp,
-    float* __restrict__ cw, float* __restrict__ thr) {
+    float* __restrict__ cw, float2* __restrict__ thr) {
   constexpr int QQ = D64 / 4, QH = D64 / 8;
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= (int64_t)kpad * QQ * 2) return;   // kpad/32 blocks * QQ * 64 lanes
@@ -332,7 +340,7 @@ __global__ __launch_bounds__(256) void k_prep_pack_well(
   wp[t] = make_float4(vals[0], vals[1], vals[2], vals[3]);
   if (q == 0 && h == 0) {
     cw[slot] = comp >= 0 ? (float)cwell[comp] : -INFINITY;
-    thr[slot] = comp >= 0 ? cthr[comp] : 0.0f;
+    thr[slot] = comp >= 0 ? cthr[comp] : make_float2(0.0f, 0.0f);
   }
 }
 
@@ -516,7 +524,7 @@ __device__ __forceinline__ void logz_step(const float* xs, const float4* __restr
 template <int D64>
 __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_logz(
     const float* __restrict__ x, int64_t n, int d, int vec4, const float4* __restrict__ wp,
-    const float* __restrict__ cw, const float* __restrict__ thr,
+    const float* __restrict__ cw, const float2* __restrict__ thr,
     const int* __restrict__ well_idx, const int* __restrict__ ill_idx,
     const float* __restrict__ dmu, const double* __restrict__ dh, const double* __restrict__ cdir,
     const int* __restrict__ counts, double* __restrict__ logz2,
@@ -534,6 +542,10 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_logz(
   __shared__ unsigned fmask[PTS][4]; // of those, the lane states refined in full
   __shared__ unsigned short cidx[PTS][128];  // arg-max well slot per (point, lane state)
   __shared__ float2 rmc[4][PTS];     // per (wave, point): exact candidate LSE state
+  __shared__ int rcnt[256];          // refinement list: entries per (point, wave), then offsets
+  __shared__ int rwsum[5];
+  __shared__ int rlist[kRefCap];     // (point << 16) | slot
+  __shared__ float rres[kRefCap];    // exact log-density relative to the screening log2 Z
   __shared__ int rts[4][kT][PTS];    // per (wave, point): largest exact candidates
   __shared__ float rtl[4][kT][PTS];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, h = lane >> 5, col = lane & 31;
@@ -673,11 +685,13 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_logz(
       const int av = blk ? a1[v] : a0[v];
       // refined: within the component's window, or among the point's four
       // largest lane states (those fill the exact top-kT list); refined in full
-      // (every component of the lane state) when its other components carry a
-      // screened mass above kFullMass of the point's total
+      // (every component of the lane state) when the screening error of its
+      // other components' mass (bound: that mass times the arg-max component's
+      // relative error bound) could exceed kFullErr of the point's total
       const float rel = mv - lzm[pp];
-      const bool full = av >= 0 && (sv - 1.0f) * exp2_fast(rel) > kFullMass;
-      const bool cand = av >= 0 && (full || rel > thr[av] ||
+      const float2 tf = av >= 0 ? thr[av] : make_float2(0.0f, 0.0f);
+      const bool full = av >= 0 && (sv - 1.0f) * exp2_fast(rel) * tf.y > kFullErr;
+      const bool cand = av >= 0 && (full || rel > tf.x ||
                                     (mv >= s4m[pp] && rel > -(float)kWideWindow));
       float term = cand ? (full ? sv : 1.0f) * exp2_fast(mv - stw[wave][pp].x) : 0.0f;
       for (int off = 16; off > 0; off >>= 1) term += __shfl_xor(term, off);
@@ -691,46 +705,105 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_logz(
     }
   }
   __syncthreads();
-  if (lane < PTS) {
-    // exact log-densities of wave w's candidates of point p, in lane column
-    // order, relative to the point's screening log2 Z (small numbers, so fp32
-    // keeps them to its full relative precision)
+  // Refinement, spread over the workgroup: the candidates of (point p, wave
+  // w2) are listed in (point, wave, lane column, block) order, every thread
+  // computes exact log-densities of list entries (relative to the point's
+  // screening log2 Z, fp64 sums), and the owner thread of (w2, p) then takes
+  // its entries in list order, so the result does not depend on the split.
+  {
     const int p = lane, w2 = wave;
-    const double ref = lzm[p] > -INFINITY ? (double)lzm[p] : 0.0;
+    const bool owner = lane < PTS;
+    unsigned cm = 0u, fm = 0u;
+    int my_c = 0;
+    // components of lane state (w2, b): slots 32 kb + b, kb = w2, w2 + 4, ... < n_wkb
+    const int nkb_w = n_wkb > w2 ? (n_wkb - w2 + 3) / 4 : 0;
+    const int kb_last = w2 + 4 * (nkb_w - 1);
+    if (owner) {
+      cm = cmask[p][w2];
+      fm = fmask[p][w2];
+      my_c = __popc(cm & ~fm);
+      unsigned f = fm;
+      while (f) {
+        const int b = __ffs(f) - 1;
+        f &= f - 1;
+        my_c += nkb_w - (kb_last * kBK + b >= n_well ? 1 : 0);
+      }
+    }
+    rcnt[p * 4 + w2] = owner ? my_c : 0;
+    __syncthreads();
+    // exclusive scan of rcnt in (point, wave) order, entry t by thread t
+    {
+      const int v = rcnt[tid];
+      int inc = v;
+      for (int o = 1; o < 64; o <<= 1) {
+        const int t2 = __shfl_up(inc, o);
+        if (lane >= o) inc += t2;
+      }
+      if (lane == 63) rwsum[wave] = inc;
+      __syncthreads();
+      int before = 0, all = 0;
+      for (int q = 0; q < 4; ++q) {
+        if (q < wave) before += rwsum[q];
+        all += rwsum[q];
+      }
+      __syncthreads();                          // every thread has read rcnt[tid]
+      rcnt[tid] = before + inc - v;
+      if (tid == 0) rwsum[4] = all;
+    }
+    __syncthreads();
+    const int total = rwsum[4];
+    const int my_base = owner ? rcnt[p * 4 + w2] : 0;
     float mc = -INFINITY, sc = 0.0f;
     int tsl[kT];
     float tl[kT];
 #pragma unroll
     for (int j = 0; j < kT; ++j) { tsl[j] = -1; tl[j] = -INFINITY; }
-    unsigned msk = cmask[p][w2];
-    const unsigned fm = fmask[p][w2];
-    const float* xr = xs + p * P;
-    auto refine = [&](int slot) {
-      const int comp = well_idx[slot];
-      const float l = (float)(ill_logit<D64>(xr, dmu + (size_t)comp * D64,
-                                             dh + (size_t)comp * D64, cdir[comp]) - ref);
-      lse_add(mc, sc, l);
-      topk_insert(tl, tsl, l, slot);
-    };
-    while (msk) {
-      const int b = __ffs(msk) - 1;
-      msk &= msk - 1;
-      if ((fm >> b) & 1u) {
-        // every component of lane state (w2, b): slots 32 kb + b, kb = w2, w2 + 4, ...
-        for (int kb = w2; kb < n_wkb; kb += 4) {
-          const int slot = kb * kBK + b;
-          if (slot >= n_well) break;
-          refine(slot);
+    for (int lo = 0; lo < total; lo += kRefCap) {
+      const int hi = total < lo + kRefCap ? total : lo + kRefCap;
+      if (owner && my_base < hi && my_base + my_c > lo) {
+        int j = my_base;
+        unsigned msk = cm;
+        while (msk && j < hi) {
+          const int b = __ffs(msk) - 1;
+          msk &= msk - 1;
+          if ((fm >> b) & 1u) {
+            for (int kb = w2; kb < n_wkb && j < hi; kb += 4) {
+              const int slot = kb * kBK + b;
+              if (slot >= n_well) break;
+              if (j >= lo) rlist[j - lo] = (p << 16) | slot;
+              ++j;
+            }
+          } else {
+            if (j >= lo) rlist[j - lo] = (p << 16) | cidx[p][w2 * 32 + b];
+            ++j;
+          }
         }
-      } else {
-        refine(cidx[p][w2 * 32 + b]);
       }
+      __syncthreads();
+      for (int j = lo + tid; j < hi; j += 256) {
+        const int e = rlist[j - lo], pp = e >> 16, comp = well_idx[e & 0xFFFF];
+        const double ref = lzm[pp] > -INFINITY ? (double)lzm[pp] : 0.0;
+        rres[j - lo] = (float)(ill_logit<D64>(xs + pp * P, dmu + (size_t)comp * D64,
+                                              dh + (size_t)comp * D64, cdir[comp]) - ref);
+      }
+      __syncthreads();
+      if (owner) {
+        const int j1 = my_base + my_c < hi ? my_base + my_c : hi;
+        for (int j = my_base > lo ? my_base : lo; j < j1; ++j) {
+          const float l = rres[j - lo];
+          lse_add(mc, sc, l);
+          topk_insert(tl, tsl, l, rlist[j - lo] & 0xFFFF);
+        }
+      }
+      __syncthreads();                          // the next pass reuses rlist / rres
     }
-    rmc[w2][p] = make_float2(mc, sc);
+    if (owner) {
+      rmc[w2][p] = make_float2(mc, sc);
 #pragma unroll
-    for (int j = 0; j < kT; ++j) {
-      rts[w2][j][p] = tsl[j];
-      rtl[w2][j][p] = tl[j];
+      for (int j = 0; j < kT; ++j) {
+        rts[w2][j][p] = tsl[j];
+        rtl[w2][j][p] = tl[j];
+      }
     }
   }
   __syncthreads();
@@ -2098,8 +2171,8 @@ bool make_layout(int64_t n, int d, int k, int m, Layout* L) {
   L->off_well_idx = take((size_t)k * sizeof(int));
   L->off_ill_idx = take((size_t)k * sizeof(int));
   L->off_cw = take((size_t)L->kpad * sizeof(float));
-  L->off_cthr = take((size_t)k * sizeof(float));
-  L->off_thr = take((size_t)L->kpad * sizeof(float));
+  L->off_cthr = take((size_t)k * sizeof(float2));
+  L->off_thr = take((size_t)L->kpad * sizeof(float2));
   L->off_wp = take((size_t)L->kpad * 2 * L->D64 * sizeof(float));
   L->off_wq = take((size_t)(L->kpad / 16) * (L->D64 / 2 + L->D64 / 32) * 64 * sizeof(float));
   L->off_dmu = take((size_t)k * L->D64 * sizeof(float));
@@ -2143,8 +2216,8 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
   int* well_idx = at<int>(ws, L.off_well_idx);
   int* ill_idx = at<int>(ws, L.off_ill_idx);
   float* cw = at<float>(ws, L.off_cw);
-  float* cthr = at<float>(ws, L.off_cthr);
-  float* thr = at<float>(ws, L.off_thr);
+  float2* cthr = at<float2>(ws, L.off_cthr);
+  float2* thr = at<float2>(ws, L.off_thr);
   float4* wp = at<float4>(ws, L.off_wp);
   float* wq = at<float>(ws, L.off_wq);
   float* dmu = at<float>(ws, L.off_dmu);
@@ -2219,8 +2292,8 @@ int assign_impl(const Layout& L, const float* x, const float* w, const float* mu
   int* cls = at<int>(ws, L.off_cls);
   double* cwell = at<double>(ws, L.off_cwell);
   double* cdir = at<double>(ws, L.off_cdir);
-  float* cthr = at<float>(ws, L.off_cthr);
-  float* thr = at<float>(ws, L.off_thr);
+  float2* cthr = at<float2>(ws, L.off_cthr);
+  float2* thr = at<float2>(ws, L.off_thr);
   int* well_idx = at<int>(ws, L.off_well_idx);
   int* ill_idx = at<int>(ws, L.off_ill_idx);
   float* cw = at<float>(ws, L.off_cw);
