@@ -122,6 +122,42 @@ def source_digest():
         return hashlib.sha256(f.read()).hexdigest()
 
 
+ESTEP_KERNELS = ("k_prep_", "k_logz", "k_stats_", "k_sparse_", "k_reduce_")
+
+
+def counter_per_call(csv_path, kernels=ESTEP_KERNELS):
+    """Sum of a rocprofv3 --pmc counter (KiB) over the dispatches whose kernel name contains one
+    of `kernels`, divided by the number of gmm_estep_accumulate calls in the run (k_logz
+    dispatches)."""
+    import csv
+    tot, calls = 0.0, 0
+    with open(csv_path) as f:
+        for row in csv.DictReader(f):
+            name = row["Kernel_Name"]
+            if any(k in name for k in kernels):
+                tot += float(row["Counter_Value"])
+                calls += "k_logz" in name
+    return tot / max(calls, 1)
+
+
+def write_traffic(workload, fetch_csv, write_csv, copy_fetch_csv, copy_write_csv):
+    """profiles/estep_traffic_<workload>.json from two counter runs of the bench (FETCH_SIZE,
+    WRITE_SIZE) and the same counters over a COPY_BYTES device copy, which fix the scale of
+    each counter."""
+    f_copy = counter_per_call(copy_fetch_csv, ("copyBuffer",)) * 1024.0
+    w_copy = counter_per_call(copy_write_csv, ("copyBuffer",)) * 1024.0
+    f_scale, w_scale = COPY_BYTES / f_copy, COPY_BYTES / w_copy
+    fetch = counter_per_call(fetch_csv) * 1024.0 * f_scale
+    write = counter_per_call(write_csv) * 1024.0 * w_scale
+    out = {"workload": workload, "bytes_per_call": fetch + write, "fetch_bytes": fetch,
+           "write_bytes": write, "fetch_scale": f_scale, "write_scale": w_scale,
+           "source_sha256": source_digest()}
+    path = os.path.join(ROOT, "profiles", f"estep_traffic_{workload}.json")
+    with open(path, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps(out))
+
+
 def measured_traffic(workload):
     """HBM bytes per gmm_estep_accumulate call from the committed counter runs
     (profiles/estep_traffic_<workload>.json), or None when the kernels have changed since."""
@@ -146,7 +182,14 @@ def main():
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only copy a 2 GiB device buffer once (the reference for the HBM byte "
                          "counters) and exit")
+    ap.add_argument("--write-traffic", nargs=4, metavar="CSV",
+                    help="write profiles/estep_traffic_<workload>.json from rocprofv3 counter "
+                         "CSVs: bench FETCH_SIZE, bench WRITE_SIZE, copy FETCH_SIZE, copy "
+                         "WRITE_SIZE (no GPU needed)")
     args = ap.parse_args()
+    if args.write_traffic:
+        write_traffic(args.workload, *args.write_traffic)
+        return
     if args.calibrate_copy:
         calibrate_copy()
         return
