@@ -45,6 +45,10 @@ def load_library():
     if not os.path.exists(LIB_PATH):
         raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_2606_10896_amd.build "
                            "(no CPU fallback exists)")
+    # torch first: the library must bind to the HIP runtime that allocates the tensors it
+    # is given (loading it first would pull in a second runtime, whose device pointers
+    # differ from torch's)
+    import torch  # noqa: F401
     lib = ctypes.CDLL(LIB_PATH)
     vp, i64, i32, f32, f64 = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_float,
                               ctypes.c_double)

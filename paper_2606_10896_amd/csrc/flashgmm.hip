@@ -82,6 +82,16 @@ __device__ __forceinline__ f16v mfma32(float a, float b, f16v c) {
 
 __device__ __forceinline__ float exp2_fast(float v) { return __builtin_amdgcn_exp2f(v); }
 
+// bf16 MFMA (32x32x16): lane l holds A[l % 32][8 (l / 32) + e] and B[8 (l / 32) + e][l % 32],
+// e = 0..7; the accumulator has the layout of the fp32 32x32 MFMAs.  An fp32 value v is
+// carried as hi + lo, hi = bf16(v), lo = bf16(v - hi) (16 of its 24 bits), and a product
+// as hi.hi + hi.lo + lo.hi; the dropped lo.lo and the representation error leave a
+// relative error of about 2^-16 per product.
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ f16v mfma32b(bf16x8 a, bf16x8 b, f16v c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
 // ---------------------------------------------------------------- online LSE (base 2)
 // State (m, s) represents log2 sum_j 2^(l_j) = m + log2 s, with m = -inf, s = 0
 // for the empty set.
@@ -344,6 +354,41 @@ __global__ __launch_bounds__(256) void k_prep_pack_well(
   }
 }
 
+// bf16 screening operand: for 32-component block kb and 16-k step s (k over
+// [x | x^2], k < D64 the x part), wpb[((kb * NS16 + s) * 64 + l) * 2 + {0, 1}] holds the
+// hi and lo parts of B[k = 16 s + 8 (l / 32) + e][slot 32 kb + l % 32], e = 0..7, where
+// B is log2(e) mu/var (x part) or -log2(e) / (2 var) (x^2 part), split from fp64.
+template <int D64>
+__global__ __launch_bounds__(256) void k_prep_pack_b16(
+    const float* __restrict__ mu, const float* __restrict__ var, int d, int kpad,
+    const int* __restrict__ counts, const int* __restrict__ well_idx, bf16x8* __restrict__ wpb) {
+  constexpr int NS16 = D64 / 8;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (int64_t)(kpad / kBK) * NS16 * 64) return;
+  const int lane = (int)(t & 63);
+  const int s = (int)((t >> 6) % NS16);
+  const int kb = (int)((t >> 6) / NS16);
+  const int slot = kb * kBK + (lane & 31), h = lane >> 5;
+  const int comp = slot < counts[0] ? well_idx[slot] : -1;
+  bf16x8 hi, lo;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int k = 16 * s + 8 * h + e;
+    const bool xpart = k < D64;
+    const int j = xpart ? k : k - D64;
+    double v = 0.0;
+    if (comp >= 0 && j < d) {
+      const double m = mu[(int64_t)comp * d + j], s2 = var[(int64_t)comp * d + j];
+      v = xpart ? kLog2e * m / s2 : -0.5 * kLog2e / s2;
+    }
+    const __bf16 vh = (__bf16)(float)v;
+    hi[e] = vh;
+    lo[e] = (__bf16)(float)(v - (double)(float)vh);
+  }
+  wpb[2 * t] = hi;
+  wpb[2 * t + 1] = lo;
+}
+
 // Packed 16x16x4 operand of k_stats_well: wq[(g * WQS + s) * 64 + lane] is,
 // for 16-component group g and lane l, component slot 16g + l%16 at step s:
 // W of dimension 16(s/4) + 4(l/16) + s%4 for s < D64/4, P of that dimension
@@ -423,6 +468,12 @@ __global__ __launch_bounds__(256) void k_prep_pack_direct(
 // Points per screening workgroup: two 32-point MFMA tiles while a 64-point X
 // tile fits in LDS next to the per-point state (D64 <= 256), one tile above.
 __host__ __device__ constexpr int logz_tiles(int D64) { return D64 <= 256 ? 2 : 1; }
+// The screening contraction runs on split bf16 MFMA while the split X tile fits in
+// LDS next to the fp32 one (D64 <= 128).  Its error, about 2^-16.5 per product over
+// D64/8 accumulation steps, is of the order of the fp32 chain's (2^-24 per step of a
+// running sum of some hundred log2 units over D64 steps), so the refinement rules
+// are the same for both.
+__host__ __device__ constexpr bool screen_b16(int D64) { return D64 <= 128; }
 
 // One software-pipelined step of a screening pass for one wave: when MF, the
 // log-densities of the NT 32-point tiles against component block wpb are
@@ -501,6 +552,64 @@ __device__ __forceinline__ void logz_step(const float* xs, const float4* __restr
   }
 }
 
+// The same step on bf16 MFMA (32x32x16, hi/lo split): the X tile is held in
+// LDS as split 8-value chunks xa[p * (D64/2 + 1) + 2 c + {hi, lo}], chunk c
+// covering k = 8c .. 8c+7 of [x | x^2]; step s consumes chunks 2s (lane half 0)
+// and 2s + 1 (lane half 1); wpb is the block's packed split operand.
+template <int D64, bool MF, bool EPI, int NT, class Epi>
+__device__ __forceinline__ void logz_step16(const bf16x8* xa, const bf16x8* __restrict__ wpb,
+                                            float cb, f16v& n0, f16v& n1, const f16v& c0,
+                                            const f16v& c1, Epi&& epi) {
+  constexpr int NS = D64 / 8, RPV = D64 / 2 + 1;
+  const int lane = threadIdx.x & 63, h = lane >> 5, col = lane & 31;
+  const bf16x8* xr0 = xa + col * RPV + 2 * h;
+  const bf16x8* xr1 = xa + ((NT == 2 ? 32 : 0) + col) * RPV + 2 * h;
+  bf16x8 bh[3], bl[3];
+  if (MF) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      n0[v] = cb;
+      if constexpr (NT == 2) n1[v] = cb;
+    }
+    bh[0] = wpb[2 * lane];
+    bl[0] = wpb[2 * lane + 1];
+    bh[1] = wpb[2 * (64 + lane)];
+    bl[1] = wpb[2 * (64 + lane) + 1];
+  }
+#pragma unroll
+  for (int q = 0; q < NS; ++q) {
+    if (MF) {
+      if (q + 2 < NS) {
+        bh[(q + 2) % 3] = wpb[2 * ((q + 2) * 64 + lane)];
+        bl[(q + 2) % 3] = wpb[2 * ((q + 2) * 64 + lane) + 1];
+      }
+      const bf16x8 wh = bh[q % 3], wl = bl[q % 3];
+      const bf16x8 ah = xr0[4 * q], al = xr0[4 * q + 1];
+      if constexpr (NT == 2) {
+        const bf16x8 ch = xr1[4 * q], cl = xr1[4 * q + 1];
+        n0 = mfma32b(ah, wh, n0);
+        n1 = mfma32b(ch, wh, n1);
+        n0 = mfma32b(ah, wl, n0);
+        n1 = mfma32b(ch, wl, n1);
+        n0 = mfma32b(al, wh, n0);
+        n1 = mfma32b(cl, wh, n1);
+      } else {
+        n0 = mfma32b(ah, wh, n0);
+        n0 = mfma32b(ah, wl, n0);
+        n0 = mfma32b(al, wh, n0);
+      }
+    }
+    if (EPI) {
+#pragma unroll
+      for (int v = q * 16 / NS; v < (q + 1) * 16 / NS; ++v) {
+        if constexpr (NT == 2) epi(v, c0[v], c1[v]);
+        else epi(v, c0[v], c0[v]);
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
 // One workgroup = PTS = 32 NT points (64 for D64 <= 256, else 32), 4 waves;
 // wave w takes well component blocks w, w+4, ... and ill-conditioned
 // components w, w+4, ...
@@ -522,15 +631,19 @@ __device__ __forceinline__ void logz_step(const float* xs, const float4* __restr
 // A significant component is missed only if a larger one of the same point
 // shares its lane state; its responsibility then keeps the screening error.
 template <int D64>
-__global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_logz(
+__global__ __launch_bounds__(256, 1) void k_logz(
     const float* __restrict__ x, int64_t n, int d, int vec4, const float4* __restrict__ wp,
+    const bf16x8* __restrict__ wpb,
     const float* __restrict__ cw, const float2* __restrict__ thr,
     const int* __restrict__ well_idx, const int* __restrict__ ill_idx,
     const float* __restrict__ dmu, const double* __restrict__ dh, const double* __restrict__ cdir,
     const int* __restrict__ counts, double* __restrict__ logz2,
     unsigned short* __restrict__ cslot, float* __restrict__ cr, double* __restrict__ ll_part) {
   constexpr int P = D64 + 4, NT = logz_tiles(D64), PTS = 32 * NT;
+  constexpr bool B16 = screen_b16(D64);
+  constexpr int RPV = D64 / 2 + 1;
   __shared__ __align__(16) float xs[PTS * P];
+  __shared__ bf16x8 xa[B16 ? PTS * RPV : 1];   // split [x | x^2] tile of the bf16 screening
   __shared__ float2 stw[4][PTS];     // per wave: merged well state (M_w, S_w) per point
   __shared__ float2 sti[4][PTS];     // per wave: ill state per point (maximum rounded to fp32)
   __shared__ double stim[4][PTS];    // per wave: the ill state's maximum in fp64
@@ -552,6 +665,26 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_logz(
   const int64_t n0 = (int64_t)blockIdx.x * PTS;
   load_tile<D64>(x, n, d, n0, PTS, xs, vec4 != 0);
   __syncthreads();
+  if constexpr (B16) {
+    // split tile: chunk c < D64/8 holds x of dims 8c.., the others x^2 of dims 8(c - D64/8)..
+    constexpr int NCH = D64 / 4;
+    for (int t = tid; t < PTS * NCH; t += 256) {
+      const int p = t / NCH, c = t % NCH;
+      const bool sq = c >= NCH / 2;
+      const float* xr = xs + p * P + 8 * (sq ? c - NCH / 2 : c);
+      bf16x8 hi, lo;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float v = sq ? xr[e] * xr[e] : xr[e];
+        const __bf16 vh = (__bf16)v;
+        hi[e] = vh;
+        lo[e] = (__bf16)(v - (float)vh);
+      }
+      xa[p * RPV + 2 * c] = hi;
+      xa[p * RPV + 2 * c + 1] = lo;
+    }
+    __syncthreads();
+  }
   const int n_wkb = counts[2], n_ill = counts[1], n_well = counts[0];
 
   float m0[16], s0[16], m1[16], s1[16];
@@ -573,21 +706,33 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_logz(
       lse_add_arg(m0[v], s0[v], a0[v], l0, slot);
       if constexpr (NT == 2) lse_add_arg(m1[v], s1[v], a1[v], l1, slot);
     };
+    constexpr size_t BS16 = (size_t)(D64 / 8) * 64 * 2;
     if (nb > 0) {
-      logz_step<D64, true, false, NT>(xs, wp + (size_t)wave * BS, cw[wave * kBK + col], c0, c1,
-                                      x0, x1, epi);
+      if constexpr (B16)
+        logz_step16<D64, true, false, NT>(xa, wpb + (size_t)wave * BS16, cw[wave * kBK + col], c0,
+                                          c1, x0, x1, epi);
+      else
+        logz_step<D64, true, false, NT>(xs, wp + (size_t)wave * BS, cw[wave * kBK + col], c0, c1,
+                                        x0, x1, epi);
       float cbn = nb > 1 ? cw[(wave + 4) * kBK + col] : 0.0f;
       for (int i = 0; i + 1 < nb; ++i) {
         const int kb = wave + 4 * i;
         const float cb = cbn;
         if (i + 2 < nb) cbn = cw[(kb + 8) * kBK + col];
         slot = kb * kBK + col;
-        logz_step<D64, true, true, NT>(xs, wp + (size_t)(kb + 4) * BS, cb, x0, x1, c0, c1, epi);
+        if constexpr (B16)
+          logz_step16<D64, true, true, NT>(xa, wpb + (size_t)(kb + 4) * BS16, cb, x0, x1, c0, c1,
+                                           epi);
+        else
+          logz_step<D64, true, true, NT>(xs, wp + (size_t)(kb + 4) * BS, cb, x0, x1, c0, c1, epi);
         c0 = x0;
         c1 = x1;
       }
       slot = (wave + 4 * (nb - 1)) * kBK + col;
-      logz_step<D64, false, true, NT>(xs, wp, 0.0f, x0, x1, c0, c1, epi);
+      if constexpr (B16)
+        logz_step16<D64, false, true, NT>(xa, wpb, 0.0f, x0, x1, c0, c1, epi);
+      else
+        logz_step<D64, false, true, NT>(xs, wp, 0.0f, x0, x1, c0, c1, epi);
     }
   }
   // arg-max of every lane state, and the per-wave merged state of every point
@@ -2107,7 +2252,7 @@ struct Layout {
   int pts_logz;
   int64_t n_wg_logz;
   size_t off_counts, off_cls, off_cwell, off_cdir, off_cthr, off_thr, off_well_idx, off_ill_idx,
-      off_cw, off_wp, off_wq, off_dmu, off_dh, off_logz2, off_cslot, off_cr, off_llpart,
+      off_cw, off_wp, off_wq, off_wpb, off_dmu, off_dh, off_logz2, off_cslot, off_cr, off_llpart,
       off_part_w, off_part_s, off_part_i, off_scnt, off_soff, off_slist, off_fit_nk, off_fit_s,
       off_fit_q, total;
 };
@@ -2175,6 +2320,7 @@ bool make_layout(int64_t n, int d, int k, int m, Layout* L) {
   L->off_thr = take((size_t)L->kpad * sizeof(float2));
   L->off_wp = take((size_t)L->kpad * 2 * L->D64 * sizeof(float));
   L->off_wq = take((size_t)(L->kpad / 16) * (L->D64 / 2 + L->D64 / 32) * 64 * sizeof(float));
+  L->off_wpb = take(screen_b16(L->D64) ? (size_t)L->kpad * L->D64 * 8 : 16);
   L->off_dmu = take((size_t)k * L->D64 * sizeof(float));
   L->off_dh = take((size_t)k * L->D64 * sizeof(double));
   L->off_logz2 = take((size_t)n * sizeof(double));
@@ -2230,6 +2376,7 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
   double* part_s = at<double>(ws, L.off_part_s);
   double* part_i = at<double>(ws, L.off_part_i);
   const int vec4 = ((d & 3) == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0) ? 1 : 0;
+  bf16x8* wpb = at<bf16x8>(ws, L.off_wpb);
 
   hipLaunchKernelGGL(k_prep_class, dim3(k), dim3(64), 0, st, w, mu, var, d, cls, cwell, cdir,
                      cthr);
@@ -2238,6 +2385,11 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
     const int64_t tot = (int64_t)kpad * (D64 / 4) * 2;
     hipLaunchKernelGGL(k_prep_pack_well<D64>, dim3((unsigned)cdiv(tot, 256)), dim3(256), 0, st,
                        mu, var, d, kpad, cwell, cthr, counts, well_idx, wp, cw, thr);
+    if constexpr (screen_b16(D64)) {
+      const int64_t tb = (int64_t)(kpad / kBK) * (D64 / 8) * 64;
+      hipLaunchKernelGGL(k_prep_pack_b16<D64>, dim3((unsigned)cdiv(tb, 256)), dim3(256), 0, st,
+                         mu, var, d, kpad, counts, well_idx, wpb);
+    }
     hipLaunchKernelGGL(k_prep_pack_w16<D64>,
                        dim3((unsigned)cdiv((int64_t)(kpad / 16) * wq_steps(D64) * 64, 256)),
                        dim3(256), 0, st, w, mu, var, d, kpad, counts, well_idx, wq);
@@ -2246,7 +2398,7 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
                        st, mu, var, d, k, dmu, dh);
   }
   hipLaunchKernelGGL(k_logz<D64>, dim3((unsigned)L.n_wg_logz), dim3(256), 0, st, x, n, d, vec4,
-                     wp, cw, thr, well_idx, ill_idx, dmu, dh, cdir, counts, logz2, cslot, cr,
+                     wp, wpb, cw, thr, well_idx, ill_idx, dmu, dh, cdir, counts, logz2, cslot, cr,
                      llpart);
   if constexpr (D64 < 256) {
     hipLaunchKernelGGL(k_stats_well<D64>, dim3((unsigned)((kpad / kWB) * L.nch)), dim3(256), 0,
