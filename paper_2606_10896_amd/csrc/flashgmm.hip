@@ -241,6 +241,64 @@ __device__ __forceinline__ double ill_logit_bounded(const float* xrow,
   return acc > bound ? -INFINITY : c - acc;
 }
 
+// The same two sums over a row of x in global memory (d values, no padding):
+// the terms are taken in the same order, and the padded dimensions of the
+// tile forms add exact zeros, so the results are bit-identical to theirs.
+__device__ __forceinline__ double ill_logit_gr(const float* __restrict__ xrow, int d, int vec4,
+                                               const float* __restrict__ mu,
+                                               const double* __restrict__ hh, double c) {
+  double acc = 0.0;
+  int j = 0;
+  if (vec4) {
+    for (; j + 4 <= d; j += 4) {
+      const float4 xv = *reinterpret_cast<const float4*>(xrow + j);
+      const float4 m = *reinterpret_cast<const float4*>(mu + j);
+      const double2 g0 = *reinterpret_cast<const double2*>(hh + j);
+      const double2 g1 = *reinterpret_cast<const double2*>(hh + j + 2);
+      double t;
+      t = (double)xv.x - (double)m.x; acc = fma(t * t, g0.x, acc);
+      t = (double)xv.y - (double)m.y; acc = fma(t * t, g0.y, acc);
+      t = (double)xv.z - (double)m.z; acc = fma(t * t, g1.x, acc);
+      t = (double)xv.w - (double)m.w; acc = fma(t * t, g1.y, acc);
+    }
+  }
+  for (; j < d; ++j) {
+    const double t = (double)xrow[j] - (double)mu[j];
+    acc = fma(t * t, hh[j], acc);
+  }
+  return c - acc;
+}
+
+__device__ __forceinline__ double ill_logit_bounded_gr(const float* __restrict__ xrow, int d,
+                                                       int vec4, const float* __restrict__ mu,
+                                                       const double* __restrict__ hh, double c,
+                                                       double bound) {
+  double acc = 0.0;
+  for (int j0 = 0; j0 < d; j0 += 16) {
+    const int j1 = j0 + 16 < d ? j0 + 16 : d;
+    int j = j0;
+    if (vec4) {
+      for (; j + 4 <= j1; j += 4) {
+        const float4 xv = *reinterpret_cast<const float4*>(xrow + j);
+        const float4 m = *reinterpret_cast<const float4*>(mu + j);
+        const double2 g0 = *reinterpret_cast<const double2*>(hh + j);
+        const double2 g1 = *reinterpret_cast<const double2*>(hh + j + 2);
+        double t;
+        t = (double)xv.x - (double)m.x; acc = fma(t * t, g0.x, acc);
+        t = (double)xv.y - (double)m.y; acc = fma(t * t, g0.y, acc);
+        t = (double)xv.z - (double)m.z; acc = fma(t * t, g1.x, acc);
+        t = (double)xv.w - (double)m.w; acc = fma(t * t, g1.y, acc);
+      }
+    }
+    for (; j < j1; ++j) {
+      const double t = (double)xrow[j] - (double)mu[j];
+      acc = fma(t * t, hh[j], acc);
+    }
+    if (__ballot(!(acc > bound)) == 0ull) break;
+  }
+  return acc > bound ? -INFINITY : c - acc;
+}
+
 // ---------------------------------------------------------------- prep
 // Workspace counters: [0] well components, [1] ill-conditioned components,
 // [2] well 32-blocks, [3] ill 32-blocks.
@@ -630,8 +688,30 @@ __device__ __forceinline__ void logz_step16(const bf16x8* xa, const bf16x8* __re
 //      pass.
 // A significant component is missed only if a larger one of the same point
 // shares its lane state; its responsibility then keeps the screening error.
+// LDS state of k_logz after the screening pass, per workgroup of PTS points.
+template <int PTS>
+struct LogzPost {
+  float2 stw[4][PTS];         // per wave: merged well state (M_w, S_w) per point
+  float2 sti[4][PTS];         // per wave: ill state per point (maximum rounded to fp32)
+  double stim[4][PTS];        // per wave: the ill state's maximum in fp64
+  float cms[4][PTS];          // per wave: candidate mass relative to M_w
+  float lzm[PTS];             // screening log2 Z
+  float2 top2[4][PTS];        // per wave: the two largest lane-state maxima per point
+  float s4m[PTS];             // lower bound of the 4th largest lane-state maximum
+  unsigned cmask[PTS][4];     // candidate lane columns per (point, wave)
+  unsigned fmask[PTS][4];     // of those, the lane states refined in full
+  unsigned short cidx[PTS][128];  // arg-max well slot per (point, lane state)
+  float2 rmc[4][PTS];         // per (wave, point): exact candidate LSE state
+  int rcnt[256];              // refinement list: entries per (point, wave), then offsets
+  int rwsum[8];
+  int rlist[kRefCap];         // (point << 16) | slot
+  float rres[kRefCap];        // exact log-density relative to the screening log2 Z
+  int rts[4][kT][PTS];        // per (wave, point): largest exact candidates
+  float rtl[4][kT][PTS];
+};
+
 template <int D64>
-__global__ __launch_bounds__(256, 1) void k_logz(
+__global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
     const float* __restrict__ x, int64_t n, int d, int vec4, const float4* __restrict__ wp,
     const bf16x8* __restrict__ wpb,
     const float* __restrict__ cw, const float2* __restrict__ thr,
@@ -642,49 +722,84 @@ __global__ __launch_bounds__(256, 1) void k_logz(
   constexpr int P = D64 + 4, NT = logz_tiles(D64), PTS = 32 * NT;
   constexpr bool B16 = screen_b16(D64);
   constexpr int RPV = D64 / 2 + 1;
-  __shared__ __align__(16) float xs[PTS * P];
-  __shared__ bf16x8 xa[B16 ? PTS * RPV : 1];   // split [x | x^2] tile of the bf16 screening
-  __shared__ float2 stw[4][PTS];     // per wave: merged well state (M_w, S_w) per point
-  __shared__ float2 sti[4][PTS];     // per wave: ill state per point (maximum rounded to fp32)
-  __shared__ double stim[4][PTS];    // per wave: the ill state's maximum in fp64
-  __shared__ float cms[4][PTS];      // per wave: candidate mass relative to M_w
-  __shared__ float lzm[PTS];         // screening log2 Z
-  __shared__ float2 top2[4][PTS];    // per wave: the two largest lane-state maxima per point
-  __shared__ float s4m[PTS];         // lower bound of the 4th largest lane-state maximum
-  __shared__ unsigned cmask[PTS][4]; // candidate lane columns per (point, wave)
-  __shared__ unsigned fmask[PTS][4]; // of those, the lane states refined in full
-  __shared__ unsigned short cidx[PTS][128];  // arg-max well slot per (point, lane state)
-  __shared__ float2 rmc[4][PTS];     // per (wave, point): exact candidate LSE state
-  __shared__ int rcnt[256];          // refinement list: entries per (point, wave), then offsets
-  __shared__ int rwsum[5];
-  __shared__ int rlist[kRefCap];     // (point << 16) | slot
-  __shared__ float rres[kRefCap];    // exact log-density relative to the screening log2 Z
-  __shared__ int rts[4][kT][PTS];    // per (wave, point): largest exact candidates
-  __shared__ float rtl[4][kT][PTS];
+  // bf16 screening: the split [x | x^2] tile, whose space the post-screening
+  // state takes over (direct-form sums then read x from global memory), so
+  // that two workgroups fit a compute unit.  fp32 screening: the fp32 tile,
+  // which the direct-form sums also read, and the state after it.
+  constexpr size_t XS_BYTES = B16 ? 0 : (size_t)PTS * P * sizeof(float);
+  constexpr size_t XA_BYTES = B16 ? (size_t)PTS * RPV * sizeof(bf16x8) : 0;
+  constexpr size_t PS_BYTES = sizeof(LogzPost<PTS>);
+  constexpr size_t SM_BYTES =
+      B16 ? (XA_BYTES > PS_BYTES ? XA_BYTES : PS_BYTES) : XS_BYTES + PS_BYTES;
+  __shared__ __align__(16) unsigned char smem[SM_BYTES];
+  float* const xs = reinterpret_cast<float*>(smem);
+  bf16x8* const xa = reinterpret_cast<bf16x8*>(smem);
+  LogzPost<PTS>& post = *reinterpret_cast<LogzPost<PTS>*>(smem + XS_BYTES);
+  auto& stw = post.stw;
+  auto& sti = post.sti;
+  auto& stim = post.stim;
+  auto& cms = post.cms;
+  auto& lzm = post.lzm;
+  auto& top2 = post.top2;
+  auto& s4m = post.s4m;
+  auto& cmask = post.cmask;
+  auto& fmask = post.fmask;
+  auto& cidx = post.cidx;
+  auto& rmc = post.rmc;
+  auto& rcnt = post.rcnt;
+  auto& rwsum = post.rwsum;
+  auto& rlist = post.rlist;
+  auto& rres = post.rres;
+  auto& rts = post.rts;
+  auto& rtl = post.rtl;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, h = lane >> 5, col = lane & 31;
   const int64_t n0 = (int64_t)blockIdx.x * PTS;
-  load_tile<D64>(x, n, d, n0, PTS, xs, vec4 != 0);
-  __syncthreads();
   if constexpr (B16) {
-    // split tile: chunk c < D64/8 holds x of dims 8c.., the others x^2 of dims 8(c - D64/8)..
-    constexpr int NCH = D64 / 4;
-    for (int t = tid; t < PTS * NCH; t += 256) {
-      const int p = t / NCH, c = t % NCH;
-      const bool sq = c >= NCH / 2;
-      const float* xr = xs + p * P + 8 * (sq ? c - NCH / 2 : c);
-      bf16x8 hi, lo;
+    // split tile: chunk c < D64/8 holds x of dims 8c .. 8c+7, chunk c + D64/8
+    // x^2 of the same dims; rows >= n and dims >= d are zero
+    constexpr int NC8 = D64 / 8;
+    for (int t = tid; t < PTS * NC8; t += 256) {
+      const int p = t / NC8, c = t % NC8;
+      const int64_t row = n0 + p;
+      float v[8];
+      if (vec4 && row < n) {
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+          const int j = 8 * c + 4 * hf;
+          float4 q = make_float4(0.f, 0.f, 0.f, 0.f);
+          if (j < d) q = *reinterpret_cast<const float4*>(x + row * d + j);
+          v[4 * hf] = q.x;
+          v[4 * hf + 1] = q.y;
+          v[4 * hf + 2] = q.z;
+          v[4 * hf + 3] = q.w;
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int j = 8 * c + e;
+          v[e] = (row < n && j < d) ? x[row * d + j] : 0.0f;
+        }
+      }
+      bf16x8 hi, lo, hq, lq;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float v = sq ? xr[e] * xr[e] : xr[e];
-        const __bf16 vh = (__bf16)v;
+        const __bf16 vh = (__bf16)v[e];
         hi[e] = vh;
-        lo[e] = (__bf16)(v - (float)vh);
+        lo[e] = (__bf16)(v[e] - (float)vh);
+        const float q = v[e] * v[e];
+        const __bf16 qh = (__bf16)q;
+        hq[e] = qh;
+        lq[e] = (__bf16)(q - (float)qh);
       }
       xa[p * RPV + 2 * c] = hi;
       xa[p * RPV + 2 * c + 1] = lo;
+      xa[p * RPV + 2 * (c + NC8)] = hq;
+      xa[p * RPV + 2 * (c + NC8) + 1] = lq;
     }
-    __syncthreads();
+  } else {
+    load_tile<D64>(x, n, d, n0, PTS, xs, vec4 != 0);
   }
+  __syncthreads();
   const int n_wkb = counts[2], n_ill = counts[1], n_well = counts[0];
 
   float m0[16], s0[16], m1[16], s1[16];
@@ -735,6 +850,8 @@ __global__ __launch_bounds__(256, 1) void k_logz(
         logz_step<D64, false, true, NT>(xs, wp, 0.0f, x0, x1, c0, c1, epi);
     }
   }
+  // the state below takes over the split tile's space
+  if constexpr (B16) __syncthreads();
   // arg-max of every lane state, and the per-wave merged state of every point
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
@@ -776,12 +893,17 @@ __global__ __launch_bounds__(256, 1) void k_logz(
     // log2 units, where an fp32 value is off by up to 5e-4
     double mi = -INFINITY;
     float si = 0.0f;
-    for (int ki = wave; ki < n_ill; ki += 4) {
+    // rows >= n (zero rows of the fp32 tile) are skipped with the split tile
+    const int64_t row = n0 + lane;
+    for (int ki = wave; ki < n_ill && (!B16 || row < n); ki += 4) {
       const int comp = ill_idx[ki];
       const double c = cdir[comp];
-      const double l = ill_logit_bounded<D64>(xs + lane * P, dmu + (size_t)comp * D64,
-                                              dh + (size_t)comp * D64, c,
-                                              c - ((double)mw - 60.0));
+      const double bnd = c - ((double)mw - 60.0);
+      const double l =
+          B16 ? ill_logit_bounded_gr(x + row * d, d, vec4, dmu + (size_t)comp * D64,
+                                     dh + (size_t)comp * D64, c, bnd)
+              : ill_logit_bounded<D64>(xs + lane * P, dmu + (size_t)comp * D64,
+                                       dh + (size_t)comp * D64, c, bnd);
       if (l > mi) {
         si = __fmaf_rn(si, exp2_fast((float)(mi - l)), 1.0f);
         mi = l;
@@ -857,7 +979,7 @@ __global__ __launch_bounds__(256, 1) void k_logz(
   // its entries in list order, so the result does not depend on the split.
   {
     const int p = lane, w2 = wave;
-    const bool owner = lane < PTS;
+    const bool owner = lane < PTS && n0 + lane < n;
     unsigned cm = 0u, fm = 0u;
     int my_c = 0;
     // components of lane state (w2, b): slots 32 kb + b, kb = w2, w2 + 4, ... < n_wkb
@@ -928,8 +1050,12 @@ __global__ __launch_bounds__(256, 1) void k_logz(
       for (int j = lo + tid; j < hi; j += 256) {
         const int e = rlist[j - lo], pp = e >> 16, comp = well_idx[e & 0xFFFF];
         const double ref = lzm[pp] > -INFINITY ? (double)lzm[pp] : 0.0;
-        rres[j - lo] = (float)(ill_logit<D64>(xs + pp * P, dmu + (size_t)comp * D64,
-                                              dh + (size_t)comp * D64, cdir[comp]) - ref);
+        const double l =
+            B16 ? ill_logit_gr(x + (n0 + pp) * d, d, vec4, dmu + (size_t)comp * D64,
+                               dh + (size_t)comp * D64, cdir[comp])
+                : ill_logit<D64>(xs + pp * P, dmu + (size_t)comp * D64, dh + (size_t)comp * D64,
+                                 cdir[comp]);
+        rres[j - lo] = (float)(l - ref);
       }
       __syncthreads();
       if (owner) {
