@@ -56,9 +56,11 @@ const char* gmm_status_string(int status);
 /*
  * Bytes of workspace needed by gmm_estep_accumulate / gmm_fit (m = 0) or by
  * gmm_assign_topk (m >= 1) for n points in d dimensions and k components.
- * Returns 0 when the shape is unsupported.  The size grows as O(n) (one fp32
- * log-normaliser per point) plus O(k d) for the parameters and the
- * per-workgroup partial statistics; it never holds an n x k array.
+ * Returns 0 when the shape is unsupported.  The size grows as O(n) (about
+ * 100 bytes per point: the fp64 log-normaliser, the stored exact pairs and
+ * their bucketed records, and a mask of the component blocks the dense
+ * statistics take) plus O(k d) for the parameters and the per-workgroup
+ * partial statistics; it never holds an n x k array.
  */
 size_t gmm_workspace_bytes(int64_t n, int32_t d, int32_t k, int32_t m);
 

@@ -54,6 +54,7 @@ constexpr double kLog2Pi = 1.8378770664093454835606594728112;  // log(2 pi)
 constexpr double kIllSum = 2.0e5;
 constexpr int kT = 4;                   // exact responsibilities stored per point
 constexpr int kFlush = 128;             // k_stats_well: fp32 -> fp64 every 128 iterations
+constexpr int kStatsWin = 4096;         // k_stats_well: points scanned per queue window
 // Refined lists store component slots as 16-bit values; kNoSlot marks an
 // empty entry (slots are < k <= GMM_MAX_K = 65535).
 constexpr unsigned short kNoSlot = 0xFFFF;
@@ -73,6 +74,16 @@ constexpr float kFullErr = 0x1p-20f;
 constexpr int kRefCap = 1024;
 constexpr double kNarrowWindow = 10.0;
 constexpr double kLooseBound = -12.0;
+// Dense statistics are formed only for the (point, 64-component block) pairs
+// that can hold a responsibility above 2^-kDenseWindow that is not among the
+// point's stored exact pairs: a lane state within kDenseWindow of the
+// screening log2 Z marks its arg-max component's block (unless that component
+// is stored), and all of its blocks when the screened mass of its other
+// components exceeds kDenseMass of the point's total.  Every pair left out
+// has r < 2^-kDenseWindow up to the screening error (a few log2 units at
+// most), so a component's N_k moves by less than N 2^-58.
+constexpr float kDenseWindow = 64.0f;
+constexpr float kDenseMass = 0x1p-64f;
 
 typedef float f16v __attribute__((ext_vector_type(16)));
 
@@ -700,6 +711,8 @@ struct LogzPost {
   float s4m[PTS];             // lower bound of the 4th largest lane-state maximum
   unsigned cmask[PTS][4];     // candidate lane columns per (point, wave)
   unsigned fmask[PTS][4];     // of those, the lane states refined in full
+  unsigned smask[PTS][4];     // lane states within kDenseWindow of the screening log2 Z
+  unsigned omask[PTS][4];     // of those, the ones whose other components carry mass
   unsigned short cidx[PTS][128];  // arg-max well slot per (point, lane state)
   float2 rmc[4][PTS];         // per (wave, point): exact candidate LSE state
   int rcnt[256];              // refinement list: entries per (point, wave), then offsets
@@ -718,7 +731,8 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
     const int* __restrict__ well_idx, const int* __restrict__ ill_idx,
     const float* __restrict__ dmu, const double* __restrict__ dh, const double* __restrict__ cdir,
     const int* __restrict__ counts, double* __restrict__ logz2,
-    unsigned short* __restrict__ cslot, float* __restrict__ cr, double* __restrict__ ll_part) {
+    unsigned short* __restrict__ cslot, float* __restrict__ cr, double* __restrict__ ll_part,
+    unsigned long long* __restrict__ bmask) {
   constexpr int P = D64 + 4, NT = logz_tiles(D64), PTS = 32 * NT;
   constexpr bool B16 = screen_b16(D64);
   constexpr int RPV = D64 / 2 + 1;
@@ -744,6 +758,8 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
   auto& s4m = post.s4m;
   auto& cmask = post.cmask;
   auto& fmask = post.fmask;
+  auto& smask = post.smask;
+  auto& omask = post.omask;
   auto& cidx = post.cidx;
   auto& rmc = post.rmc;
   auto& rcnt = post.rcnt;
@@ -969,6 +985,16 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
         cmask[pp][wave] = (unsigned)(bal >> (32 * h));
         fmask[pp][wave] = (unsigned)(balf >> (32 * h));
       }
+      if (bmask != nullptr) {
+        const bool sig = av >= 0 && rel > -kDenseWindow;
+        const bool oth = sig && (sv - 1.0f) * exp2_fast(rel) > kDenseMass;
+        const unsigned long long bals = __ballot(sig);
+        const unsigned long long balo = __ballot(oth);
+        if (col == 0) {
+          smask[pp][wave] = (unsigned)(bals >> (32 * h));
+          omask[pp][wave] = (unsigned)(balo >> (32 * h));
+        }
+      }
     }
   }
   __syncthreads();
@@ -1125,6 +1151,25 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
           cslot[nn * kT + j] = tsl[j] >= 0 ? (unsigned short)tsl[j] : kNoSlot;
           cr[nn * kT + j] = tsl[j] >= 0 ? exp2_fast(tl[j] - lzr) : 0.0f;
         }
+        if (bmask != nullptr) {
+          // 64-component blocks the dense statistics pass takes for this point
+          unsigned long long bm = 0ull;
+          for (int w2 = 0; w2 < 4; ++w2) {
+            if (omask[p][w2] != 0u)
+              for (int kb = w2; kb < n_wkb; kb += 4) bm |= 1ull << (kb >> 1);
+            unsigned sm = smask[p][w2];
+            while (sm) {
+              const int b = __ffs(sm) - 1;
+              sm &= sm - 1;
+              const int slot = cidx[p][w2 * 32 + b];
+              bool stored = false;
+#pragma unroll
+              for (int j = 0; j < kT; ++j) stored = stored || tsl[j] == slot;
+              if (!stored) bm |= 1ull << (slot >> 6);
+            }
+          }
+          bmask[nn] = bm;
+        }
       }
     }
     for (int off = 32; off > 0; off >>= 1) contrib += __shfl_xor(contrib, off);
@@ -1169,8 +1214,9 @@ template <int D64>
 __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
     const float* __restrict__ x, int64_t n, int d, int vec4, const float* __restrict__ wq,
     const float* __restrict__ cw, const int* __restrict__ counts,
-    const double* __restrict__ logz2, const unsigned short* __restrict__ cslot, int nch,
-    int64_t chunk_pts, double* __restrict__ part) {
+    const double* __restrict__ logz2, const unsigned short* __restrict__ cslot,
+    const unsigned long long* __restrict__ bmask, int nch, int64_t chunk_pts,
+    double* __restrict__ part) {
   constexpr int P = D64 + 4;
   constexpr int NS = D64 / 4;                   // MFMA steps per chain
   constexpr int NG = D64 / 64;                  // float4 column groups per part
@@ -1186,6 +1232,9 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
   __shared__ __align__(16) float xs[2][PTS * P];
   __shared__ float2 lzb[2][PTS];                // -log2 Z / NGB as a (hi, lo) pair
   __shared__ unsigned long long rbb[2][PTS];
+  __shared__ unsigned qpt[kStatsWin + PTS];     // queued points (offsets from the chunk start)
+  static_assert(kStatsWin == 16 * 256, "a window is 16 points per thread");
+  __shared__ int qsum[4];
   const int kb = blockIdx.x / nch, chunk = blockIdx.x % nch;
   if (2 * kb >= counts[2]) return;              // counts[2]: well blocks of 32
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -1197,7 +1246,6 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
     for (int i = tid; i < kWB * STRIDE; i += 256) pw[i] = 0.0;
     return;
   }
-  const int niter = (int)((p1 - p0 + PTS - 1) / PTS);
   const int grp = kb * 4 + wave;                // 16-component group
   float wb[WQS];
 #pragma unroll
@@ -1207,12 +1255,14 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
   float4 px[LD];
   float2 plz = make_float2(-INFINITY, 0.0f);
   unsigned long long prb = 0ull;
+  // tile i holds queue entries PTS i .. PTS i + PTS - 1 (rows past qn are zero)
+  int qn = 0;                                   // queued points (uniform)
   auto load_regs = [&](int i) {
-    const int64_t it = p0 + (int64_t)i * PTS;
 #pragma unroll
     for (int j = 0; j < LD; ++j) {
       const int idx = tid + 256 * j, r = idx / Q4, c = (idx % Q4) * 4;
-      const int64_t nn = it + r;
+      const int e = PTS * i + r;
+      const int64_t nn = e < qn ? p0 + qpt[e] : p1;
       float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
       if (vec4) {
         if (nn < p1 && c < d) v = *reinterpret_cast<const float4*>(x + nn * d + c);
@@ -1226,7 +1276,8 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
       px[j] = v;
     }
     if (tid < PTS) {
-      const int64_t nn = it + tid;
+      const int e = PTS * i + tid;
+      const int64_t nn = e < qn ? p0 + qpt[e] : p1;
       plz = make_float2(-INFINITY, 0.0f);
       prb = 0ull;
       if (nn < p1) {
@@ -1294,12 +1345,53 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
     first = false;
   };
 
+  // The chunk is taken in windows of kStatsWin points: the points of a window
+  // that need this block (every point when bmask is null) are appended to the
+  // queue in point order, the full tiles of the queue are processed (at the
+  // chunk's end also the partial one) and the rest moves to the queue's front.
+  const unsigned long long kbit = 1ull << (kb & 63);
+  int tiles = 0;                                // tiles processed (flush schedule)
+  for (int64_t wb0 = p0; wb0 < p1; wb0 += kStatsWin) {
+    const int64_t we = wb0 + kStatsWin < p1 ? wb0 + kStatsWin : p1;
+    {
+      // thread t takes points wb0 + 16 t .. wb0 + 16 t + 15
+      const int64_t a = wb0 + 16 * tid;
+      unsigned sel = 0u;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int64_t pt = a + e;
+        if (pt < we && (bmask == nullptr || (bmask[pt] & kbit) != 0ull)) sel |= 1u << e;
+      }
+      const int c = __popc(sel);
+      int inc = c;
+      for (int o = 1; o < 64; o <<= 1) {
+        const int t2 = __shfl_up(inc, o);
+        if (lane >= o) inc += t2;
+      }
+      if (lane == 63) qsum[wave] = inc;
+      __syncthreads();
+      int pos = qn + inc - c, all = 0;
+#pragma unroll
+      for (int w2 = 0; w2 < 4; ++w2) {
+        if (w2 < wave) pos += qsum[w2];
+        all += qsum[w2];
+      }
+      while (sel) {
+        const int e = __ffs(sel) - 1;
+        sel &= sel - 1;
+        qpt[pos++] = (unsigned)(a + e - p0);
+      }
+      qn += all;
+      __syncthreads();                          // queue complete, qsum free
+    }
+    const int nt = we >= p1 ? (qn + PTS - 1) / PTS : qn / PTS;
+    if (nt > 0) {
   load_regs(0);
   store_regs(0);
-  for (int i = 0; i < niter; ++i) {
+  for (int i = 0; i < nt; ++i) {
     const int cur = i & 1;
     __syncthreads();                            // tile i in xs[cur]; xs[cur ^ 1] free
-    if (i + 1 < niter) load_regs(i + 1);
+    if (i + 1 < nt) load_regs(i + 1);
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       // log-densities of points t*16 .. t*16+15 against this wave's components
@@ -1363,9 +1455,22 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
         }
       }
     }
-    if (i + 1 < niter) store_regs(cur ^ 1);
-    if ((i % kFlush) == kFlush - 1 || i + 1 == niter) flush();
+    if (i + 1 < nt) store_regs(cur ^ 1);
+    if ((tiles % kFlush) == kFlush - 1) flush();
+    ++tiles;
   }
+    }
+    // the entries not taken move to the front of the queue
+    const int used = PTS * nt < qn ? PTS * nt : qn;
+    const int left = qn - used;
+    __syncthreads();                            // every read of the queue and the tiles done
+    const unsigned keep = tid < left ? qpt[used + tid] : 0u;
+    __syncthreads();
+    if (tid < left) qpt[tid] = keep;
+    qn = left;
+  }
+  // the last partial sums (zeros when no point of the chunk needs this block)
+  if (first || (tiles % kFlush) != 0) flush();
 }
 
 // ---------------------------------------------------------------- Step 2: statistics, wide D
@@ -2377,10 +2482,11 @@ struct Layout {
   int64_t upts;
   int pts_logz;
   int64_t n_wg_logz;
+  bool bmask_on;            // per-point dense-block masks (k_stats_well, at most 64 blocks)
   size_t off_counts, off_cls, off_cwell, off_cdir, off_cthr, off_thr, off_well_idx, off_ill_idx,
       off_cw, off_wp, off_wq, off_wpb, off_dmu, off_dh, off_logz2, off_cslot, off_cr, off_llpart,
-      off_part_w, off_part_s, off_part_i, off_scnt, off_soff, off_slist, off_fit_nk, off_fit_s,
-      off_fit_q, total;
+      off_part_w, off_part_s, off_part_i, off_scnt, off_soff, off_slist, off_bmask, off_fit_nk,
+      off_fit_s, off_fit_q, total;
 };
 
 // Padded dimension count of the kernels: a multiple of 64 up to 256, of 128 above.
@@ -2433,6 +2539,7 @@ bool make_layout(int64_t n, int d, int k, int m, Layout* L) {
   }
   L->pts_logz = L->D64 <= 256 ? 64 : 32;
   L->n_wg_logz = cdiv(n, L->pts_logz);
+  L->bmask_on = L->D64 < 256 && L->kpad / kWB <= 64;
   size_t o = 0;
   auto take = [&](size_t bytes) { const size_t r = o; o = align256(o + bytes); return r; };
   L->off_counts = take(16 * sizeof(int));
@@ -2460,6 +2567,7 @@ bool make_layout(int64_t n, int d, int k, int m, Layout* L) {
   L->off_scnt = take((size_t)L->nb * L->nunit * sizeof(int));
   L->off_soff = take(((size_t)L->nb * L->nunit + 1) * sizeof(int64_t));
   L->off_slist = take((size_t)n * kT * sizeof(SPair));
+  L->off_bmask = take(L->bmask_on ? (size_t)n * sizeof(unsigned long long) : 16);
   L->off_fit_nk = take((size_t)k * sizeof(double) + sizeof(double));  // + loglik slot
   L->off_fit_s = take((size_t)k * d * sizeof(double));
   L->off_fit_q = take((size_t)k * d * sizeof(double));
@@ -2503,6 +2611,7 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
   double* part_i = at<double>(ws, L.off_part_i);
   const int vec4 = ((d & 3) == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0) ? 1 : 0;
   bf16x8* wpb = at<bf16x8>(ws, L.off_wpb);
+  unsigned long long* bmask = L.bmask_on ? at<unsigned long long>(ws, L.off_bmask) : nullptr;
 
   hipLaunchKernelGGL(k_prep_class, dim3(k), dim3(64), 0, st, w, mu, var, d, cls, cwell, cdir,
                      cthr);
@@ -2525,10 +2634,11 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
   }
   hipLaunchKernelGGL(k_logz<D64>, dim3((unsigned)L.n_wg_logz), dim3(256), 0, st, x, n, d, vec4,
                      wp, wpb, cw, thr, well_idx, ill_idx, dmu, dh, cdir, counts, logz2, cslot, cr,
-                     llpart);
+                     llpart, bmask);
   if constexpr (D64 < 256) {
     hipLaunchKernelGGL(k_stats_well<D64>, dim3((unsigned)((kpad / kWB) * L.nch)), dim3(256), 0,
-                       st, x, n, d, vec4, wq, cw, counts, logz2, cslot, L.nch, L.chunk, part_w);
+                       st, x, n, d, vec4, wq, cw, counts, logz2, cslot, bmask, L.nch, L.chunk,
+                       part_w);
   } else {
     hipLaunchKernelGGL(k_stats_wide<D64>, dim3((unsigned)((kpad / 16) * L.nch)),
                        dim3(64 * (D64 / 128)), 0, st, x, n, d, vec4, wq, cwell, well_idx, counts,
