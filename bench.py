@@ -7,12 +7,18 @@ M-step) over the whole synthetic data set, already resident in HBM.  The
 default workload is the paper-shape large one: N = 1e8 points, D = 128,
 K = 1024 components (51.2 GB of fp32 data), random-point initialisation.
 
-Prints one JSON line on stdout.  `roofline` covers the fused E-step +
-statistic accumulation (gmm_estep_accumulate), timed with HIP events on the
-stream it runs on; its algorithmic work is 8*N*K*D flop per call (the two
-log-density contractions and the two statistic contractions, 2*N*K*D each).
-`cpu_baseline` times the fp64 CPU checker on a bounded slice of the same data
-and scales it linearly in N (the E-step is exactly linear in N).
+Prints one JSON line on stdout.  `roofline` covers the dominant kernel,
+k_logz (log-densities of every point against every component, their
+log-sum-exp, the exact refinement and log Z), timed over the timed steps with
+the library's phase timer (HIP events recorded on the stream the kernels run
+on).  Its algorithmic work is the log-density contraction over all N x K
+pairs, 4*N*K*D flop per launch ([x | x^2] against [W | P], depth 2D), priced
+against the peak of the MFMA type it runs on (bf16 for D <= 128, where the
+fp32 operands are split in hi/lo bf16 parts and three products are summed,
+fp32 above).  The E-step as a whole is also reported against the 8*N*K*D
+flop of the dense algorithm.  `cpu_baseline` times the fp64 CPU checker on a
+bounded slice of the same data and scales it linearly in N (the E-step is
+exactly linear in N).
 """
 from __future__ import annotations
 
@@ -28,7 +34,10 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 FP32_MFMA_PEAK_TFLOPS = 157.3   # MI355X dense fp32 matrix peak
+BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak
 HBM_PEAK_GBS = 8000.0
+METRIC = ("ms per EM iteration + % MFMA roofline (8\u00b7N\u00b7K\u00b7D flop/iter), "
+          "N=1M..100M, K=1024, D=128")
 
 
 def log(*a):
@@ -103,6 +112,11 @@ def cpu_baseline(w, mix, theta, sample_rows):
 COPY_BYTES = 2 << 30
 
 
+def padded_d(d):
+    """The library's padded dimension count (a multiple of 64 up to 256, of 128 above)."""
+    return -(-d // 64) * 64 if d <= 256 else -(-d // 128) * 128
+
+
 def calibrate_copy():
     """One device-to-device copy of COPY_BYTES: reads and writes exactly that many bytes, the
     scale for FETCH_SIZE / WRITE_SIZE."""
@@ -128,7 +142,7 @@ ESTEP_KERNELS = ("k_prep_", "k_logz", "k_stats_", "k_sparse_", "k_reduce_")
 def counter_per_call(csv_path, kernels=ESTEP_KERNELS):
     """Sum of a rocprofv3 --pmc counter (KiB) over the dispatches whose kernel name contains one
     of `kernels`, divided by the number of gmm_estep_accumulate calls in the run (k_logz
-    dispatches)."""
+    dispatches): per E-step, or per k_logz launch when kernels = ("k_logz",)."""
     import csv
     tot, calls = 0.0, 0
     with open(csv_path) as f:
@@ -149,8 +163,11 @@ def write_traffic(workload, fetch_csv, write_csv, copy_fetch_csv, copy_write_csv
     f_scale, w_scale = COPY_BYTES / f_copy, COPY_BYTES / w_copy
     fetch = counter_per_call(fetch_csv) * 1024.0 * f_scale
     write = counter_per_call(write_csv) * 1024.0 * w_scale
+    lf = counter_per_call(fetch_csv, ("k_logz",)) * 1024.0 * f_scale
+    lw = counter_per_call(write_csv, ("k_logz",)) * 1024.0 * w_scale
     out = {"workload": workload, "bytes_per_call": fetch + write, "fetch_bytes": fetch,
-           "write_bytes": write, "fetch_scale": f_scale, "write_scale": w_scale,
+           "write_bytes": write, "logz_bytes_per_launch": lf + lw, "logz_fetch_bytes": lf,
+           "logz_write_bytes": lw, "fetch_scale": f_scale, "write_scale": w_scale,
            "source_sha256": source_digest()}
     path = os.path.join(ROOT, "profiles", f"estep_traffic_{workload}.json")
     with open(path, "w") as f:
@@ -158,9 +175,10 @@ def write_traffic(workload, fetch_csv, write_csv, copy_fetch_csv, copy_write_csv
     print(json.dumps(out))
 
 
-def measured_traffic(workload):
-    """HBM bytes per gmm_estep_accumulate call from the committed counter runs
-    (profiles/estep_traffic_<workload>.json), or None when the kernels have changed since."""
+def measured_traffic(workload, key="logz_bytes_per_launch"):
+    """HBM bytes per k_logz launch (or, with key="bytes_per_call", per E-step) from the
+    committed counter runs (profiles/estep_traffic_<workload>.json), or None when the kernels
+    have changed since."""
     path = os.path.join(ROOT, "profiles", f"estep_traffic_{workload}.json")
     if not os.path.exists(path):
         return None
@@ -168,7 +186,7 @@ def measured_traffic(workload):
         t = json.load(f)
     if t.get("source_sha256") != source_digest():
         return None
-    return t.get("bytes_per_call")
+    return t.get(key)
 
 
 def main():
@@ -234,20 +252,31 @@ def main():
         log(f"  warmup step {i} done")
     events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
               for _ in range(args.steps)]
+    gmm.gmm_timing_enable(True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
         step(args.warmup + i, events[i])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    phase_tot, ncalls = gmm.gmm_timing_read()
+    gmm.gmm_timing_enable(False)
+    phases = {p: round(v / max(ncalls, 1), 3) for p, v in phase_tot.items()}
     ms_step = (t1 - t0) * 1e3 / args.steps
     estep_ms = float(np.mean([a.elapsed_time(b) for a, b in events]))
     hist = ll.cpu().numpy()
     log(f"  loglik: {hist[0]:.6e} -> {hist[-1]:.6e}")
+    log(f"  phases (ms per E-step): {phases}")
     flops = 8.0 * w.n * k * d
-    achieved = flops / (estep_ms * 1e-3) / 1e12
+    dense_rate = flops / (estep_ms * 1e-3) / 1e12
+    # dominant kernel: k_logz, 4 N K D flop of log-densities per launch
+    logz_ms = phases["logz"]
+    logz_b16 = padded_d(d) <= 128
+    logz_peak = BF16_MFMA_PEAK_TFLOPS if logz_b16 else FP32_MFMA_PEAK_TFLOPS
+    logz_alg = 4.0 * w.n * k * d / (logz_ms * 1e-3) / 1e12
+    dominant = max(phases, key=phases.get)
     result = {
-        "metric": "ms per EM iteration + % fp32 MFMA roofline (8*N*K*D flop/iter)",
+        "metric": METRIC,
         "value": round(ms_step, 3),
         "unit": "ms/iter",
         "n_gpus": 1,
@@ -257,17 +286,27 @@ def main():
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32 (MFMA log-densities), f64 statistics",
+        "dtype": ("bf16 hi/lo split MFMA (screening log-densities), f32 MFMA (dense statistics), "
+                  "f64 (exact pairs, sums)") if logz_b16 else
+                 "f32 MFMA (log-densities, dense statistics), f64 (exact pairs, sums)",
         "data": "synthetic",
         "config": {"workload": f"{w.name}: diag-GMM EM, N={w.n}, D={d}, K={k}, fp32 points from "
                                f"{w.k_true} seeded diagonal Gaussians, random-point init",
                    "n": w.n, "d": d, "k": k, "parallelism": "single GPU"},
-        "roofline": {"bound": "mfma", "kernel": "gmm_estep_accumulate (fused E-step + statistics)",
-                     "achieved": round(achieved, 2), "peak": FP32_MFMA_PEAK_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(achieved / FP32_MFMA_PEAK_TFLOPS, 4),
-                     "traffic": measured_traffic(w.name), "estep_ms": round(estep_ms, 3),
-                     "whole_iteration_frac": round(flops / (ms_step * 1e-3) / 1e12
-                                                   / FP32_MFMA_PEAK_TFLOPS, 4)},
+        "roofline": {"bound": "mfma",
+                     "kernel": "k_logz (4*N*K*D flop of log-densities per launch, "
+                               + ("bf16 MFMA peak; 3 bf16 products per fp32 product"
+                                  if logz_b16 else "fp32 MFMA peak") + ")",
+                     "achieved": round(logz_alg, 2), "peak": logz_peak, "unit": "TFLOP/s",
+                     "frac": round(logz_alg / logz_peak, 4),
+                     "traffic": measured_traffic(w.name),
+                     "kernel_ms": logz_ms,
+                     "executed_tflops": round(logz_alg * (3 if logz_b16 else 1), 2),
+                     "dominant_phase": dominant, "phases_ms": phases,
+                     "estep_ms": round(estep_ms, 3),
+                     "estep_8nkd_tflops": round(dense_rate, 2),
+                     "estep_8nkd_frac_fp32_peak": round(dense_rate / FP32_MFMA_PEAK_TFLOPS, 4),
+                     "estep_8nkd_frac_bf16_peak": round(dense_rate / BF16_MFMA_PEAK_TFLOPS, 4)},
         "cpu_baseline": None,
     }
     if args.cpu_sample > 0:

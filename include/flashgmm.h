@@ -127,6 +127,29 @@ int gmm_assign_topk(const float* x, int64_t n, int32_t d, int32_t k, const float
                     const float* means, const float* vars, int32_t m, float tau, int32_t* idx,
                     float* resp, void* ws, size_t ws_bytes, hipStream_t stream);
 
+/*
+ * Phase timing of the E-step, a measurement aid (no part of the method).
+ * While enabled, every E-step (gmm_estep_accumulate, each iteration of
+ * gmm_fit) records HIP events on its stream between its phases, waits for the
+ * last of them and adds each phase's GPU duration to a process-wide total:
+ *   0  parameter preparation (k_prep_*)
+ *   1  screening, refinement and log Z of every point (k_logz)
+ *   2  dense statistics of the well-conditioned components (k_stats_well /
+ *      k_stats_wide)
+ *   3  statistics of the stored exact pairs (k_sparse_*, k_stats_sparse)
+ *   4  routed components and the fixed-order reductions (k_stats_ill,
+ *      k_reduce_stats, k_reduce_ll)
+ * gmm_timing_enable(on) switches it on (creating the events on the current
+ * device at first use) or off, and zeroes the totals.  gmm_timing_read copies
+ * the first n_phases totals (ms; phases past GMM_TIMING_PHASES read 0) and the
+ * number of timed E-steps.  The waiting makes timed calls synchronous.  Not
+ * for concurrent callers.  Returns GMM_OK, GMM_ERR_INVALID_ARG (null pointer,
+ * n_phases < 0) or GMM_ERR_DEVICE (event creation failed).
+ */
+#define GMM_TIMING_PHASES 5
+int gmm_timing_enable(int on);
+int gmm_timing_read(double* ms, int32_t n_phases, int64_t* calls);
+
 #ifdef __cplusplus
 }
 #endif

@@ -26,7 +26,7 @@ GMM_MAX_M = 8
 
 #: every symbol the C ABI exports
 EXPORTS = ("gmm_status_string", "gmm_workspace_bytes", "gmm_estep_accumulate", "gmm_mstep",
-           "gmm_fit", "gmm_assign_topk")
+           "gmm_fit", "gmm_assign_topk", "gmm_timing_enable", "gmm_timing_read")
 
 _lib = None
 
@@ -66,6 +66,10 @@ def load_library():
     lib.gmm_assign_topk.argtypes = [vp, i64, i32, i32, vp, vp, vp, i32, f32, vp, vp, vp,
                                     ctypes.c_size_t, vp]
     lib.gmm_assign_topk.restype = ctypes.c_int
+    lib.gmm_timing_enable.argtypes = [ctypes.c_int]
+    lib.gmm_timing_enable.restype = ctypes.c_int
+    lib.gmm_timing_read.argtypes = [vp, i32, vp]
+    lib.gmm_timing_read.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -168,3 +172,21 @@ def gmm_assign_topk(x, weights, means, variances, m, tau, idx, resp, ws, stream=
         _ptr(_dev(resp, torch.float32, "resp")), _ptr(ws), ws.numel() if ws is not None else 0,
         _stream(stream))
     _check("gmm_assign_topk", rc)
+
+
+TIMING_PHASES = ("prep", "logz", "dense_stats", "exact_pairs", "ill_and_reduce")
+
+
+def gmm_timing_enable(on: bool = True):
+    """Switches the E-step phase timing on or off and zeroes its totals."""
+    _check("gmm_timing_enable", load_library().gmm_timing_enable(1 if on else 0))
+
+
+def gmm_timing_read():
+    """(dict phase -> total GPU ms, number of timed E-steps) since gmm_timing_enable."""
+    ms = (ctypes.c_double * len(TIMING_PHASES))()
+    calls = ctypes.c_int64(0)
+    _check("gmm_timing_read", load_library().gmm_timing_read(
+        ctypes.cast(ms, ctypes.c_void_p), len(TIMING_PHASES),
+        ctypes.cast(ctypes.byref(calls), ctypes.c_void_p)))
+    return dict(zip(TIMING_PHASES, list(ms))), calls.value

@@ -2583,6 +2583,35 @@ int launch_status() {
   return e == hipSuccess ? GMM_OK : GMM_ERR_DEVICE;
 }
 
+// ---------------------------------------------------------------- phase timing
+// Measurement aid: while enabled, every E-step records HIP events on its
+// stream between its phases, waits for the last one and adds the phase
+// durations up.  Process-wide state for one device; not for concurrent calls.
+struct PhaseTimer {
+  bool on = false;
+  bool made = false;
+  hipEvent_t ev[GMM_TIMING_PHASES + 1];
+  double ms[GMM_TIMING_PHASES] = {};
+  int64_t calls = 0;
+};
+PhaseTimer g_timer;
+
+inline bool phase_mark(int i, hipStream_t st) {
+  return !g_timer.on || hipEventRecord(g_timer.ev[i], st) == hipSuccess;
+}
+
+inline bool phase_collect() {
+  if (!g_timer.on) return true;
+  if (hipEventSynchronize(g_timer.ev[GMM_TIMING_PHASES]) != hipSuccess) return false;
+  for (int i = 0; i < GMM_TIMING_PHASES; ++i) {
+    float t = 0.0f;
+    if (hipEventElapsedTime(&t, g_timer.ev[i], g_timer.ev[i + 1]) != hipSuccess) return false;
+    g_timer.ms[i] += t;
+  }
+  ++g_timer.calls;
+  return true;
+}
+
 template <int D64>
 int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
                const float* var, double* nk, double* s, double* q, double* loglik,
@@ -2613,6 +2642,7 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
   bf16x8* wpb = at<bf16x8>(ws, L.off_wpb);
   unsigned long long* bmask = L.bmask_on ? at<unsigned long long>(ws, L.off_bmask) : nullptr;
 
+  bool tm = phase_mark(0, st);
   hipLaunchKernelGGL(k_prep_class, dim3(k), dim3(64), 0, st, w, mu, var, d, cls, cwell, cdir,
                      cthr);
   hipLaunchKernelGGL(k_prep_scan, dim3(1), dim3(256), 0, st, cls, k, well_idx, ill_idx, counts);
@@ -2632,9 +2662,11 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
     hipLaunchKernelGGL(k_prep_pack_direct<D64>, dim3((unsigned)cdiv(toti, 256)), dim3(256), 0,
                        st, mu, var, d, k, dmu, dh);
   }
+  tm = phase_mark(1, st) && tm;
   hipLaunchKernelGGL(k_logz<D64>, dim3((unsigned)L.n_wg_logz), dim3(256), 0, st, x, n, d, vec4,
                      wp, wpb, cw, thr, well_idx, ill_idx, dmu, dh, cdir, counts, logz2, cslot, cr,
                      llpart, bmask);
+  tm = phase_mark(2, st) && tm;
   if constexpr (D64 < 256) {
     hipLaunchKernelGGL(k_stats_well<D64>, dim3((unsigned)((kpad / kWB) * L.nch)), dim3(256), 0,
                        st, x, n, d, vec4, wq, cw, counts, logz2, cslot, bmask, L.nch, L.chunk,
@@ -2644,6 +2676,7 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
                        dim3(64 * (D64 / 128)), 0, st, x, n, d, vec4, wq, cwell, well_idx, counts,
                        logz2, cslot, L.nch, L.chunk, part_w);
   }
+  tm = phase_mark(3, st) && tm;
   {
     int* scnt = at<int>(ws, L.off_scnt);
     int64_t* soff = at<int64_t>(ws, L.off_soff);
@@ -2657,6 +2690,7 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
     hipLaunchKernelGGL(k_stats_sparse<D64>, dim3((unsigned)(L.nb * L.nparts)), dim3(256), 0, st,
                        x, n, d, slist, soff, L.nunit, L.nparts, part_s);
   }
+  tm = phase_mark(4, st) && tm;
   hipLaunchKernelGGL(k_stats_ill<D64>, dim3((unsigned)L.grid_i), dim3(256), 0, st, x, n, d, vec4,
                      ill_idx, dmu, dh, cdir, counts, logz2, part_i);
   {
@@ -2667,7 +2701,10 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
   }
   hipLaunchKernelGGL(k_reduce_ll, dim3(1), dim3(1024), 0, st, llpart, L.n_wg_logz, loglik,
                      ll_accumulate);
-  return launch_status();
+  const int rc = launch_status();
+  if (rc != GMM_OK) return rc;
+  tm = phase_mark(GMM_TIMING_PHASES, st) && tm;
+  return tm && phase_collect() ? GMM_OK : GMM_ERR_DEVICE;
 }
 
 template <int D64>
@@ -2742,6 +2779,25 @@ int check_shape(int64_t n, int32_t d, int32_t k) {
 }  // namespace
 
 extern "C" {
+
+int gmm_timing_enable(int on) {
+  if (on && !g_timer.made) {
+    for (int i = 0; i <= GMM_TIMING_PHASES; ++i)
+      if (hipEventCreate(&g_timer.ev[i]) != hipSuccess) return GMM_ERR_DEVICE;
+    g_timer.made = true;
+  }
+  g_timer.on = on != 0;
+  for (int i = 0; i < GMM_TIMING_PHASES; ++i) g_timer.ms[i] = 0.0;
+  g_timer.calls = 0;
+  return GMM_OK;
+}
+
+int gmm_timing_read(double* ms, int32_t n_phases, int64_t* calls) {
+  if (!ms || !calls || n_phases < 0) return GMM_ERR_INVALID_ARG;
+  for (int i = 0; i < n_phases; ++i) ms[i] = i < GMM_TIMING_PHASES ? g_timer.ms[i] : 0.0;
+  *calls = g_timer.calls;
+  return GMM_OK;
+}
 
 const char* gmm_status_string(int status) {
   switch (status) {

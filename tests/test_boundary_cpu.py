@@ -108,3 +108,21 @@ def test_assign_host_validation():
     assert call(2, 0.1, n=0) == gmm.GMM_ERR_INVALID_ARG
     assert call(2, 0.1, ws=None) == gmm.GMM_ERR_WORKSPACE
     assert call(2, 0.1, wsb=big - 1) == gmm.GMM_ERR_WORKSPACE
+
+
+def test_timing_switch_and_read_on_the_host():
+    # switching off creates no events and needs no device; the totals read back as zeros
+    lib = gmm.load_library()
+    assert lib.gmm_timing_enable(0) == 0
+    totals, calls = gmm.gmm_timing_read()
+    assert calls == 0 and set(totals) == set(gmm.TIMING_PHASES)
+    assert all(v == 0.0 for v in totals.values())
+    assert lib.gmm_timing_read(None, 5, None) == -1
+    ms = (ctypes.c_double * 7)(*([1.0] * 7))
+    calls_c = ctypes.c_int64(5)
+    assert lib.gmm_timing_read(ctypes.cast(ms, ctypes.c_void_p), 7,
+                               ctypes.cast(ctypes.byref(calls_c), ctypes.c_void_p)) == 0
+    assert list(ms) == [0.0] * 7 and calls_c.value == 0
+    assert lib.gmm_timing_read(ctypes.cast(ms, ctypes.c_void_p), -1,
+                               ctypes.cast(ctypes.byref(calls_c), ctypes.c_void_p)) == -1
+
