@@ -40,6 +40,8 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <type_traits>
+
 #include "flashgmm.h"
 
 namespace {
@@ -679,6 +681,45 @@ __device__ __forceinline__ void logz_step16(const bf16x8* xa, const bf16x8* __re
   }
 }
 
+// Transposing reduction over the 32 lanes of a lane half.  Every lane holds NV
+// (16 or 32) values, value i of lane col belonging to the same point in every
+// lane of the half; comb(j, half, off, up) merges value j (up: value j + half)
+// of this lane with the other of the pair j, j + half of lane col ^ off (the
+// partner sends the value this lane does not keep) into value j.  Each level
+// halves the values, the last ones pair lanes with a plain butterfly, so after
+// the five levels value 0 of lane col holds the reduction of value index col
+// (NV = 32) or col / 2 (NV = 16): 31 merges per lane instead of 5 NV.
+// j and half reach comb as std::integral_constant, so that the register
+// arrays it indexes stay in registers.
+template <int J, int HALF, class Comb>
+__device__ __forceinline__ void xpose_pairs(Comb& comb, int off, bool up) {
+  if constexpr (J < HALF) {
+    comb(std::integral_constant<int, J>{}, std::integral_constant<int, HALF>{}, off, up);
+    xpose_pairs<J + 1, HALF>(comb, off, up);
+  }
+}
+
+template <int NV, int LVL = 0, class Comb>
+__device__ __forceinline__ void xpose_levels(int col, Comb&& comb) {
+  if constexpr (LVL < 5) {
+    constexpr int off = 16 >> LVL, cnt = NV >> LVL;
+    if constexpr (cnt > 1)
+      xpose_pairs<0, cnt / 2>(comb, off, (col & off) != 0);
+    else
+      comb(std::integral_constant<int, 0>{}, std::integral_constant<int, 0>{}, off, false);
+    xpose_levels<NV, LVL + 1>(col, comb);
+  }
+}
+
+// The point whose reduction xpose_levels leaves in lane (h, col): value index
+// i = col (NT = 2) or col / 2 (NT = 1) is block i / 16, register i % 16.
+template <int NT>
+__device__ __forceinline__ int xpose_point(int col, int h) {
+  const int i = NT == 2 ? col : (col >> 1);
+  const int v = i & 15;
+  return 32 * (i >> 4) + 8 * (v >> 2) + 4 * h + (v & 3);
+}
+
 // One workgroup = PTS = 32 NT points (64 for D64 <= 256, else 32), 4 waves;
 // wave w takes well component blocks w, w+4, ... and ill-conditioned
 // components w, w+4, ...
@@ -868,34 +909,50 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
   }
   // the state below takes over the split tile's space
   if constexpr (B16) __syncthreads();
-  // arg-max of every lane state, and the per-wave merged state of every point
+  // arg-max of every lane state, and the per-wave merged state of every point:
+  // the LSE states and the two largest lane-state maxima (A >= B) of the 32
+  // lanes of a lane half are merged by a transposing reduction (xpose_levels)
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
     const int p = 8 * (v >> 2) + 4 * h + (v & 3);
     cidx[p][wave * 32 + col] = (unsigned short)a0[v];
     if constexpr (NT == 2) cidx[32 + p][wave * 32 + col] = (unsigned short)a1[v];
-    float M0 = m0[v], S0 = s0[v], M1 = m1[v], S1 = s1[v];
-    // the two largest lane-state maxima of the wave (A >= B)
-    float A0 = m0[v], B0 = kEmpty, A1 = m1[v], B1 = kEmpty;
-    for (int off = 16; off > 0; off >>= 1) {
-      lse_merge(M0, S0, __shfl_xor(M0, off), __shfl_xor(S0, off));
-      const float pa0 = __shfl_xor(A0, off), pb0 = __shfl_xor(B0, off);
-      B0 = fmaxf(fminf(A0, pa0), fmaxf(B0, pb0));
-      A0 = fmaxf(A0, pa0);
+  }
+  {
+    constexpr int NV = 16 * NT;
+    float XM[NV], XS[NV], XA[NV], XB[NV];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      XM[v] = m0[v];
+      XS[v] = s0[v];
+      XA[v] = m0[v];
+      XB[v] = kEmpty;
       if constexpr (NT == 2) {
-        lse_merge(M1, S1, __shfl_xor(M1, off), __shfl_xor(S1, off));
-        const float pa1 = __shfl_xor(A1, off), pb1 = __shfl_xor(B1, off);
-        B1 = fmaxf(fminf(A1, pa1), fmaxf(B1, pb1));
-        A1 = fmaxf(A1, pa1);
+        XM[16 + v] = m1[v];
+        XS[16 + v] = s1[v];
+        XA[16 + v] = m1[v];
+        XB[16 + v] = kEmpty;
       }
     }
-    if (col == 0) {
-      stw[wave][p] = make_float2(M0, S0);
-      top2[wave][p] = make_float2(A0, B0);
-      if constexpr (NT == 2) {
-        stw[wave][32 + p] = make_float2(M1, S1);
-        top2[wave][32 + p] = make_float2(A1, B1);
-      }
+    xpose_levels<NV>(col, [&](auto jc, auto hc, int off, bool up) {
+      constexpr int j = decltype(jc)::value, half = decltype(hc)::value;
+      const float km = up ? XM[j + half] : XM[j], sm = up ? XM[j] : XM[j + half];
+      const float ks = up ? XS[j + half] : XS[j], ss = up ? XS[j] : XS[j + half];
+      const float ka = up ? XA[j + half] : XA[j], sa = up ? XA[j] : XA[j + half];
+      const float kb = up ? XB[j + half] : XB[j], sb = up ? XB[j] : XB[j + half];
+      const float rm = __shfl_xor(sm, off), rs = __shfl_xor(ss, off);
+      const float ra = __shfl_xor(sa, off), rb = __shfl_xor(sb, off);
+      float M = km, S = ks;
+      lse_merge(M, S, rm, rs);
+      XM[j] = M;
+      XS[j] = S;
+      XB[j] = fmaxf(fminf(ka, ra), fmaxf(kb, rb));
+      XA[j] = fmaxf(ka, ra);
+    });
+    const int p = xpose_point<NT>(col, h);
+    if (NT == 2 || (col & 1) == 0) {
+      stw[wave][p] = make_float2(XM[0], XS[0]);
+      top2[wave][p] = make_float2(XA[0], XB[0]);
     }
   }
   // ill-conditioned components, direct form, lane = point; a term 2^-60 below
@@ -957,6 +1014,7 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
   }
   __syncthreads();
   // candidates: lane states whose maximum is within the window of the screening log2 Z
+  float XT[16 * NT];                 // candidate mass per lane state, summed below
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
     const int p = 8 * (v >> 2) + 4 * h + (v & 3);
@@ -976,12 +1034,10 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
       const bool full = av >= 0 && (sv - 1.0f) * exp2_fast(rel) * tf.y > kFullErr;
       const bool cand = av >= 0 && (full || rel > tf.x ||
                                     (mv >= s4m[pp] && rel > -(float)kWideWindow));
-      float term = cand ? (full ? sv : 1.0f) * exp2_fast(mv - stw[wave][pp].x) : 0.0f;
-      for (int off = 16; off > 0; off >>= 1) term += __shfl_xor(term, off);
+      XT[16 * blk + v] = cand ? (full ? sv : 1.0f) * exp2_fast(mv - stw[wave][pp].x) : 0.0f;
       const unsigned long long bal = __ballot(cand);
       const unsigned long long balf = __ballot(full);
       if (col == 0) {
-        cms[wave][pp] = term;
         cmask[pp][wave] = (unsigned)(bal >> (32 * h));
         fmask[pp][wave] = (unsigned)(balf >> (32 * h));
       }
@@ -997,6 +1053,12 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
       }
     }
   }
+  xpose_levels<16 * NT>(col, [&](auto jc, auto hc, int off, bool up) {
+    constexpr int j = decltype(jc)::value, half = decltype(hc)::value;
+    const float kt = up ? XT[j + half] : XT[j], st = up ? XT[j] : XT[j + half];
+    XT[j] = kt + __shfl_xor(st, off);
+  });
+  if (NT == 2 || (col & 1) == 0) cms[wave][xpose_point<NT>(col, h)] = XT[0];
   __syncthreads();
   // Refinement, spread over the workgroup: the candidates of (point p, wave
   // w2) are listed in (point, wave, lane column, block) order, every thread
