@@ -74,6 +74,8 @@ constexpr double kWideWindow = 40.0;
 constexpr float kFullErr = 0x1p-20f;
 // refinement list entries held in LDS at a time by k_logz
 constexpr int kRefCap = 1024;
+// lanes that share one direct-form sum of the k_logz refinement (bf16 path)
+constexpr int kRefLanes = 4;
 constexpr double kNarrowWindow = 10.0;
 constexpr double kLooseBound = -12.0;
 // Dense statistics are formed only for the (point, 64-component block) pairs
@@ -1135,15 +1137,51 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
         }
       }
       __syncthreads();
-      for (int j = lo + tid; j < hi; j += 256) {
-        const int e = rlist[j - lo], pp = e >> 16, comp = well_idx[e & 0xFFFF];
-        const double ref = lzm[pp] > -INFINITY ? (double)lzm[pp] : 0.0;
-        const double l =
-            B16 ? ill_logit_gr(x + (n0 + pp) * d, d, vec4, dmu + (size_t)comp * D64,
-                               dh + (size_t)comp * D64, cdir[comp])
-                : ill_logit<D64>(xs + pp * P, dmu + (size_t)comp * D64, dh + (size_t)comp * D64,
-                                 cdir[comp]);
-        rres[j - lo] = (float)(l - ref);
+      if (B16 && vec4) {
+        // kRefLanes lanes per entry: lane g of a group sums, in fp64, the float4
+        // chunks g, g + kRefLanes, ... of the row (coalesced over the group),
+        // and the group adds its partial sums in a fixed butterfly order
+        constexpr int G = kRefLanes, NCK = D64 / 4 / G;
+        const int g = tid & (G - 1);
+        for (int j = lo + tid / G; j < hi; j += 256 / G) {
+          const int e = rlist[j - lo], pp = e >> 16, comp = well_idx[e & 0xFFFF];
+          const float* xr = x + (n0 + pp) * d;
+          const float* mu = dmu + (size_t)comp * D64;
+          const double* hh = dh + (size_t)comp * D64;
+          double acc = 0.0;
+#pragma unroll
+          for (int t = 0; t < NCK; ++t) {
+            const int c4 = 4 * (g + G * t);
+            if (c4 < d) {
+              const float4 xv = *reinterpret_cast<const float4*>(xr + c4);
+              const float4 m = *reinterpret_cast<const float4*>(mu + c4);
+              const double2 g0 = *reinterpret_cast<const double2*>(hh + c4);
+              const double2 g1 = *reinterpret_cast<const double2*>(hh + c4 + 2);
+              double u;
+              u = (double)xv.x - (double)m.x; acc = fma(u * u, g0.x, acc);
+              u = (double)xv.y - (double)m.y; acc = fma(u * u, g0.y, acc);
+              u = (double)xv.z - (double)m.z; acc = fma(u * u, g1.x, acc);
+              u = (double)xv.w - (double)m.w; acc = fma(u * u, g1.y, acc);
+            }
+          }
+#pragma unroll
+          for (int o = 1; o < G; o <<= 1) acc += __shfl_xor(acc, o);
+          if (g == 0) {
+            const double ref = lzm[pp] > -INFINITY ? (double)lzm[pp] : 0.0;
+            rres[j - lo] = (float)((cdir[comp] - acc) - ref);
+          }
+        }
+      } else {
+        for (int j = lo + tid; j < hi; j += 256) {
+          const int e = rlist[j - lo], pp = e >> 16, comp = well_idx[e & 0xFFFF];
+          const double ref = lzm[pp] > -INFINITY ? (double)lzm[pp] : 0.0;
+          const double l =
+              B16 ? ill_logit_gr(x + (n0 + pp) * d, d, vec4, dmu + (size_t)comp * D64,
+                                 dh + (size_t)comp * D64, cdir[comp])
+                  : ill_logit<D64>(xs + pp * P, dmu + (size_t)comp * D64,
+                                   dh + (size_t)comp * D64, cdir[comp]);
+          rres[j - lo] = (float)(l - ref);
+        }
       }
       __syncthreads();
       if (owner) {
