@@ -1917,14 +1917,15 @@ __global__ __launch_bounds__(64) void k_sparse_scatter(
 // Sums of one part of one bucket's list.  Batches of NB pairs: the records of
 // batch t+1 are in LDS and its rows are gathered into registers while batch t
 // is consumed from LDS.  Wave w owns the CW = C/4 slots CW w .. CW w + CW - 1
-// of the bucket and takes its pairs of a batch in order; lane l owns columns
-// l, l + 64, ... of [1 | x | x^2] and adds r, r x, r x^2 in fp64 (r x is exact).
+// of the bucket and takes its pairs of a batch in order, two at a time; lane l
+// owns dimensions l, l + 64, ... and adds r x and r x^2 of them in fp64 (r x
+// is exact), and r itself (N_k, every lane the same sum; lane 0 writes it).
 template <int D64>
 __global__ __launch_bounds__(256) void k_stats_sparse(
     const float* __restrict__ x, int64_t n, int d, const SPair* __restrict__ list,
     const int64_t* __restrict__ goff, int nunit, int nparts, double* __restrict__ part) {
   constexpr int C = sparse_cb(D64), CW = C / 4;
-  constexpr int STRIDE = 1 + 2 * D64, NCI = (STRIDE + 63) / 64;
+  constexpr int STRIDE = 1 + 2 * D64;
   constexpr int NB = D64 <= 64 ? 64 : 4096 / D64;
   constexpr int GL = (NB * D64 + 255) / 256;     // gathered values per thread and batch
   __shared__ float xb[2][NB * D64];
@@ -1936,11 +1937,14 @@ __global__ __launch_bounds__(256) void k_stats_sparse(
   const int64_t cnt = hi - lo;
   const int64_t a0 = lo + cnt * prt / nparts, a1 = lo + cnt * (prt + 1) / nparts;
   const int nbatch = (int)((a1 - a0 + NB - 1) / NB);
-  double acc[CW][NCI];
+  constexpr int NX = D64 / 64;                   // dimensions per lane
+  double accs[CW][NX], accq[CW][NX], accn[CW];
 #pragma unroll
-  for (int j = 0; j < CW; ++j)
+  for (int j = 0; j < CW; ++j) {
+    accn[j] = 0.0;
 #pragma unroll
-    for (int i = 0; i < NCI; ++i) acc[j][i] = 0.0;
+    for (int u = 0; u < NX; ++u) accs[j][u] = accq[j][u] = 0.0;
+  }
   auto load_rec = [&](int t, int buf) {
     if (tid < NB) {
       const int64_t e = a0 + (int64_t)t * NB + tid;
@@ -1974,46 +1978,70 @@ __global__ __launch_bounds__(256) void k_stats_sparse(
     for (int j = 0; j < GL; ++j)
       if (tid + 256 * j < NB * D64) xb[xbuf][tid + 256 * j] = gv[j];
     __syncthreads();            // rows of batch t, records of batches t, t+1 in LDS
-    // the record buffer of batch t+2 was last read while consuming batch t-1
-    if (t + 2 < nbatch) load_rec(t + 2, (t + 2) % 3);
+    // records of batch t+2: loaded now, stored after the consumption (their
+    // buffer was last read while consuming batch t-1)
+    SPair qn;
+    bool has_rec = false;
+    if (t + 2 < nbatch && tid < NB) {
+      const int64_t e = a0 + (int64_t)(t + 2) * NB + tid;
+      if (e < a1) {
+        qn = list[e];
+        has_rec = true;
+      }
+    }
     if (t + 1 < nbatch) gather(t + 1, (t + 1) % 3);
     const int nbt = (int)(a1 - a0 - (int64_t)t * NB < NB ? a1 - a0 - (int64_t)t * NB : NB);
     int2 en = make_int2(0, 0);
     if (lane < nbt) en = rb[rcur][lane];
     const int cl = en.x - CW * wave;
-    unsigned long long own = __ballot(lane < nbt && cl >= 0 && cl < CW);
-    while (own) {
-      const int e = __ffsll(own) - 1;
-      own &= own - 1;
-      const int jc = __builtin_amdgcn_readlane(en.x, e) - CW * wave;
-      const double r = (double)__int_as_float(__builtin_amdgcn_readlane(en.y, e));
-      const float* xr = xb[xbuf] + e * D64;
-      double y[NCI];
+    // slot by slot (each slot's pairs in list order), two pairs at a time
 #pragma unroll
-      for (int i = 0; i < NCI; ++i) {
-        const int c = lane + 64 * i;
-        double v = 0.0;
-        if (c == 0) v = 1.0;
-        else if (c <= D64) v = (double)xr[c - 1];
-        else if (c < STRIDE) { const double xv = (double)xr[c - 1 - D64]; v = xv * xv; }
-        y[i] = v;
-      }
+    for (int j = 0; j < CW; ++j) {
+      unsigned long long own = __ballot(lane < nbt && cl == j);
+      while (own) {
+        const int e0 = __ffsll(own) - 1;
+        own &= own - 1;
+        const int e1 = own ? __ffsll(own) - 1 : -1;
+        if (e1 >= 0) own &= own - 1;
+        const float* xr0 = xb[xbuf] + e0 * D64 + lane;
+        const float* xr1 = xb[xbuf] + (e1 >= 0 ? e1 : e0) * D64 + lane;
+        double x0[NX], x1[NX];
 #pragma unroll
-      for (int j = 0; j < CW; ++j) {
-        if (jc == j) {
+        for (int u = 0; u < NX; ++u) {
+          x0[u] = (double)xr0[64 * u];
+          x1[u] = (double)xr1[64 * u];
+        }
+        const double r0 = (double)__int_as_float(__builtin_amdgcn_readlane(en.y, e0));
+        accn[j] += r0;
 #pragma unroll
-          for (int i = 0; i < NCI; ++i) acc[j][i] = fma(r, y[i], acc[j][i]);
+        for (int u = 0; u < NX; ++u) {
+          accs[j][u] = fma(r0, x0[u], accs[j][u]);
+          accq[j][u] = fma(r0, x0[u] * x0[u], accq[j][u]);
+        }
+        if (e1 >= 0) {
+          const double r1 = (double)__int_as_float(__builtin_amdgcn_readlane(en.y, e1));
+          accn[j] += r1;
+#pragma unroll
+          for (int u = 0; u < NX; ++u) {
+            accs[j][u] = fma(r1, x1[u], accs[j][u]);
+            accq[j][u] = fma(r1, x1[u] * x1[u], accq[j][u]);
+          }
         }
       }
+    }
+    if (has_rec) {
+      rb[(t + 2) % 3][tid] = make_int2(qn.c, __float_as_int(qn.r));
+      pb[(t + 2) % 3][tid] = qn.pt;
     }
   }
 #pragma unroll
   for (int j = 0; j < CW; ++j) {
     double* out = part + ((size_t)blockIdx.x * C + CW * wave + j) * STRIDE;
+    if (lane == 0) out[0] = accn[j];
 #pragma unroll
-    for (int i = 0; i < NCI; ++i) {
-      const int c = lane + 64 * i;
-      if (c < STRIDE) out[c] = acc[j][i];
+    for (int u = 0; u < NX; ++u) {
+      out[1 + lane + 64 * u] = accs[j][u];
+      out[1 + D64 + lane + 64 * u] = accq[j][u];
     }
   }
 }
