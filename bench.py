@@ -139,36 +139,40 @@ def source_digest():
 ESTEP_KERNELS = ("k_prep_", "k_logz", "k_stats_", "k_sparse_", "k_reduce_")
 
 
-def counter_per_call(csv_path, kernels=ESTEP_KERNELS):
+def counter_per_call(csv_path, kernels=ESTEP_KERNELS, skip=0):
     """Sum of a rocprofv3 --pmc counter (KiB) over the dispatches whose kernel name contains one
-    of `kernels`, divided by the number of gmm_estep_accumulate calls in the run (k_logz
-    dispatches): per E-step, or per k_logz launch when kernels = ("k_logz",)."""
+    of `kernels`, per gmm_estep_accumulate call (a call starts with its k_prep_class dispatch),
+    leaving out the first `skip` calls (the warm-up iterations): per E-step, or per k_logz
+    launch when kernels = ("k_logz",)."""
     import csv
-    tot, calls = 0.0, 0
     with open(csv_path) as f:
-        for row in csv.DictReader(f):
-            name = row["Kernel_Name"]
-            if any(k in name for k in kernels):
-                tot += float(row["Counter_Value"])
-                calls += "k_logz" in name
-    return tot / max(calls, 1)
+        rows = sorted(csv.DictReader(f), key=lambda r: int(r["Dispatch_Id"]))
+    tot, call, calls = 0.0, 0, set()
+    for row in rows:
+        name = row["Kernel_Name"]
+        if ("copyBuffer" if "copyBuffer" in kernels else "k_prep_class") in name:
+            call += 1
+        if call > skip and any(k in name for k in kernels):
+            tot += float(row["Counter_Value"])
+            calls.add(call)
+    return tot / max(len(calls), 1)
 
 
-def write_traffic(workload, fetch_csv, write_csv, copy_fetch_csv, copy_write_csv):
+def write_traffic(workload, fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, skip=1):
     """profiles/estep_traffic_<workload>.json from two counter runs of the bench (FETCH_SIZE,
-    WRITE_SIZE) and the same counters over a COPY_BYTES device copy, which fix the scale of
-    each counter."""
+    WRITE_SIZE; the first `skip` E-steps, the warm-up, left out) and the same counters over a
+    COPY_BYTES device copy, which fix the scale of each counter."""
     f_copy = counter_per_call(copy_fetch_csv, ("copyBuffer",)) * 1024.0
     w_copy = counter_per_call(copy_write_csv, ("copyBuffer",)) * 1024.0
     f_scale, w_scale = COPY_BYTES / f_copy, COPY_BYTES / w_copy
-    fetch = counter_per_call(fetch_csv) * 1024.0 * f_scale
-    write = counter_per_call(write_csv) * 1024.0 * w_scale
-    lf = counter_per_call(fetch_csv, ("k_logz",)) * 1024.0 * f_scale
-    lw = counter_per_call(write_csv, ("k_logz",)) * 1024.0 * w_scale
+    fetch = counter_per_call(fetch_csv, skip=skip) * 1024.0 * f_scale
+    write = counter_per_call(write_csv, skip=skip) * 1024.0 * w_scale
+    lf = counter_per_call(fetch_csv, ("k_logz",), skip) * 1024.0 * f_scale
+    lw = counter_per_call(write_csv, ("k_logz",), skip) * 1024.0 * w_scale
     out = {"workload": workload, "bytes_per_call": fetch + write, "fetch_bytes": fetch,
            "write_bytes": write, "logz_bytes_per_launch": lf + lw, "logz_fetch_bytes": lf,
            "logz_write_bytes": lw, "fetch_scale": f_scale, "write_scale": w_scale,
-           "source_sha256": source_digest()}
+           "warmup_calls_skipped": skip, "source_sha256": source_digest()}
     path = os.path.join(ROOT, "profiles", f"estep_traffic_{workload}.json")
     with open(path, "w") as f:
         json.dump(out, f, indent=1)
