@@ -2632,8 +2632,10 @@ bool make_layout(int64_t n, int d, int k, int m, Layout* L) {
   L->wbk = L->D64 >= 256 ? 16 : kWB;
   const int nwb = L->kpad / L->wbk;
   if (L->D64 < 256) {
-    // about 512 workgroups (two per CU) for k_stats_well
-    int maxc = 512 / nwb;
+    // about 2048 workgroups (four rounds at two per CU) for k_stats_well: the
+    // blocks' shares of the points differ, and several rounds let the
+    // workgroups of the busy blocks spread over the chip
+    int maxc = 2048 / nwb;
     if (maxc < 8) maxc = 8;
     int64_t c = cdiv(n, 1024);
     if (c > maxc) c = maxc;
