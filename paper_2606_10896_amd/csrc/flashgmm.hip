@@ -1597,8 +1597,8 @@ __global__ __launch_bounds__(64 * (DW / 128)) void k_stats_wide(
     const float* __restrict__ x, int64_t n, int d, int vec4, const float* __restrict__ wq,
     const double* __restrict__ cwell, const int* __restrict__ well_idx,
     const int* __restrict__ counts, const double* __restrict__ logz2,
-    const unsigned short* __restrict__ cslot, int nch, int64_t chunk_pts,
-    double* __restrict__ part) {
+    const unsigned short* __restrict__ cslot, const unsigned long long* __restrict__ bmask,
+    int nch, int64_t chunk_pts, double* __restrict__ part) {
   constexpr int NW = DW / 128, DQ = 128, P = DQ + 4;
   constexpr int NS = DW / 4, WQS = wq_steps(DW);
   constexpr int SW = DQ / 4, NBQ = DQ / 16, NG = DQ / 64;
@@ -1606,7 +1606,10 @@ __global__ __launch_bounds__(64 * (DW / 128)) void k_stats_wide(
   constexpr int LD = 16 * DQ / 4 / 64;          // float4 per lane per X tile
   static_assert(kT == 4, "refined lists are loaded as ushort4");
   __shared__ __align__(16) float xs[NW][16 * P];
-  __shared__ double lpart[2][NW][4][64];
+  __shared__ double lpart[NW][4][64];
+  constexpr int WPT = 8, WIN = WPT * 64 * NW;   // points per thread and per queue window
+  __shared__ unsigned qpt[WIN + 16];            // queued points (offsets from the chunk start)
+  __shared__ int qsum[NW];
   const int g = blockIdx.x / nch, chunk = blockIdx.x % nch;
   const int n_well = counts[0];
   if (16 * g >= n_well) return;                // no well component in this group
@@ -1619,7 +1622,6 @@ __global__ __launch_bounds__(64 * (DW / 128)) void k_stats_wide(
     for (int i = tid; i < 16 * STRIDE; i += 64 * NW) pw[i] = 0.0;
     return;
   }
-  const int niter = (int)((p1 - p0 + 15) / 16);
   const int dq0 = DQ * wave;                    // this wave's first dimension
   // this lane's component (B-operand column i16): its expanded-form constant
   const int myslot = 16 * g + i16;
@@ -1636,12 +1638,14 @@ __global__ __launch_bounds__(64 * (DW / 128)) void k_stats_wide(
   float4 px[LD];
   double plz = INFINITY;
   unsigned prb = 0u;
+  // tile i holds queue entries 16 i .. 16 i + 15 (rows past qn are zero)
+  int qn = 0;                                   // queued points (uniform)
   auto load_regs = [&](int i) {
-    const int64_t it = p0 + (int64_t)i * 16;
 #pragma unroll
     for (int j = 0; j < LD; ++j) {
       const int idx = lane + 64 * j, r = idx / (DQ / 4), c = dq0 + (idx % (DQ / 4)) * 4;
-      const int64_t nn = it + r;
+      const int e = 16 * i + r;
+      const int64_t nn = e < qn ? p0 + qpt[e] : p1;
       float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
       if (vec4) {
         if (nn < p1 && c < d) v = *reinterpret_cast<const float4*>(x + nn * d + c);
@@ -1655,7 +1659,8 @@ __global__ __launch_bounds__(64 * (DW / 128)) void k_stats_wide(
       px[j] = v;
     }
     if (lane < 16) {
-      const int64_t nn = it + lane;
+      const int e = 16 * i + lane;
+      const int64_t nn = e < qn ? p0 + qpt[e] : p1;
       plz = INFINITY;
       prb = 0u;
       if (nn < p1) {
@@ -1707,9 +1712,48 @@ __global__ __launch_bounds__(64 * (DW / 128)) void k_stats_wide(
     first = false;
   };
 
+  // Windows of WIN points: the points that need this group's 64-component
+  // block (every point when bmask is null) are queued in point order, the
+  // full 16-point tiles of the queue are processed (at the chunk's end also
+  // the partial one) and the rest moves to the queue's front.
+  const unsigned long long kbit = 1ull << ((g >> 2) & 63);
+  int tiles = 0;                                // tiles processed (flush schedule)
+  for (int64_t wb0 = p0; wb0 < p1; wb0 += WIN) {
+    const int64_t we = wb0 + WIN < p1 ? wb0 + WIN : p1;
+    {
+      const int64_t a = wb0 + WPT * tid;
+      unsigned sel = 0u;
+#pragma unroll
+      for (int e = 0; e < WPT; ++e) {
+        const int64_t pt = a + e;
+        if (pt < we && (bmask == nullptr || (bmask[pt] & kbit) != 0ull)) sel |= 1u << e;
+      }
+      const int c = __popc(sel);
+      int inc = c;
+      for (int o = 1; o < 64; o <<= 1) {
+        const int t2 = __shfl_up(inc, o);
+        if (lane >= o) inc += t2;
+      }
+      if (lane == 63) qsum[wave] = inc;
+      __syncthreads();
+      int pos = qn + inc - c, all = 0;
+#pragma unroll
+      for (int w2 = 0; w2 < NW; ++w2) {
+        if (w2 < wave) pos += qsum[w2];
+        all += qsum[w2];
+      }
+      while (sel) {
+        const int e = __ffs(sel) - 1;
+        sel &= sel - 1;
+        qpt[pos++] = (unsigned)(a + e - p0);
+      }
+      qn += all;
+      __syncthreads();                          // queue complete, qsum free
+    }
+    const int nt = we >= p1 ? (qn + 15) / 16 : qn / 16;
+    if (nt > 0) {
   load_regs(0);
-  for (int i = 0; i < niter; ++i) {
-    const int buf = i & 1;
+  for (int i = 0; i < nt; ++i) {
     store_regs();
     unsigned rbv[4];
     double lzv[4];
@@ -1719,7 +1763,7 @@ __global__ __launch_bounds__(64 * (DW / 128)) void k_stats_wide(
       lzv[v] = __shfl(plz, 4 * k4 + v);
     }
     __builtin_amdgcn_wave_barrier();
-    if (i + 1 < niter) load_regs(i + 1);
+    if (i + 1 < nt) load_regs(i + 1);
     // x . W + x^2 . P of the tile's 16 points against the group's 16
     // components over this wave's dimensions, 16 dimensions per fp32 sum
     double t64[4] = {0.0, 0.0, 0.0, 0.0};
@@ -1740,14 +1784,14 @@ __global__ __launch_bounds__(64 * (DW / 128)) void k_stats_wide(
       for (int v = 0; v < 4; ++v) t64[v] += (double)la[v];
     }
 #pragma unroll
-    for (int v = 0; v < 4; ++v) lpart[buf][wave][v][lane] = t64[v];
+    for (int v = 0; v < 4; ++v) lpart[wave][v][lane] = t64[v];
     __syncthreads();
     float r[4];
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-      double tot = lpart[buf][0][v][lane];
+      double tot = lpart[0][v][lane];
 #pragma unroll
-      for (int w2 = 1; w2 < NW; ++w2) tot += lpart[buf][w2][v][lane];
+      for (int w2 = 1; w2 < NW; ++w2) tot += lpart[w2][v][lane];
       tot += cst - lzv[v];
       const float e = exp2_fast((float)tot);
       r[v] = ((rbv[v] >> i16) & 1u) ? 0.0f : e;
@@ -1770,9 +1814,22 @@ __global__ __launch_bounds__(64 * (DW / 128)) void k_stats_wide(
         acc[NBQ + 4 * gg + 3] = mfma16(y.w * y.w, r[v], acc[NBQ + 4 * gg + 3]);
       }
     }
-    if ((i % kFlushWide) == kFlushWide - 1 || i + 1 == niter) flush();
-    __builtin_amdgcn_wave_barrier();            // this tile's LDS reads before the next store
+    if ((tiles % kFlushWide) == kFlushWide - 1) flush();
+    ++tiles;
+    __syncthreads();                            // this tile's LDS reads before the next writes
   }
+    }
+    // the entries not taken move to the front of the queue
+    const int used = 16 * nt < qn ? 16 * nt : qn;
+    const int left = qn - used;
+    __syncthreads();
+    const unsigned keep = tid < left ? qpt[used + tid] : 0u;
+    __syncthreads();
+    if (tid < left) qpt[tid] = keep;
+    qn = left;
+  }
+  // the last partial sums (zeros when no point of the chunk needs this group)
+  if (first || (tiles % kFlushWide) != 0) flush();
 }
 
 // ---------------------------------------------------------------- Step 2: refined pairs
@@ -2610,7 +2667,7 @@ struct Layout {
   int64_t upts;
   int pts_logz;
   int64_t n_wg_logz;
-  bool bmask_on;            // per-point dense-block masks (k_stats_well, at most 64 blocks)
+  bool bmask_on;            // per-point dense-block masks (at most 64 blocks of 64 components)
   size_t off_counts, off_cls, off_cwell, off_cdir, off_cthr, off_thr, off_well_idx, off_ill_idx,
       off_cw, off_wp, off_wq, off_wpb, off_dmu, off_dh, off_logz2, off_cslot, off_cr, off_llpart,
       off_part_w, off_part_s, off_part_i, off_scnt, off_soff, off_slist, off_bmask, off_fit_nk,
@@ -2669,7 +2726,7 @@ bool make_layout(int64_t n, int d, int k, int m, Layout* L) {
   }
   L->pts_logz = L->D64 <= 256 ? 64 : 32;
   L->n_wg_logz = cdiv(n, L->pts_logz);
-  L->bmask_on = L->D64 < 256 && L->kpad / kWB <= 64;
+  L->bmask_on = L->kpad / kWB <= 64;
   size_t o = 0;
   auto take = [&](size_t bytes) { const size_t r = o; o = align256(o + bytes); return r; };
   L->off_counts = take(16 * sizeof(int));
@@ -2804,7 +2861,7 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
   } else {
     hipLaunchKernelGGL(k_stats_wide<D64>, dim3((unsigned)((kpad / 16) * L.nch)),
                        dim3(64 * (D64 / 128)), 0, st, x, n, d, vec4, wq, cwell, well_idx, counts,
-                       logz2, cslot, L.nch, L.chunk, part_w);
+                       logz2, cslot, bmask, L.nch, L.chunk, part_w);
   }
   tm = phase_mark(3, st) && tm;
   {
