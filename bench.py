@@ -95,6 +95,20 @@ def load_data(w, dev, chunk_rows=1 << 22):
     return x, mix, colsum, colsq
 
 
+def gpu_clocks():
+    """Current GPU clocks as rocm-smi reports them (None when it cannot be read)."""
+    import subprocess
+    try:
+        out = subprocess.run(["rocm-smi", "--showclocks", "--json"], capture_output=True,
+                             text=True, timeout=20)
+        info = json.loads(out.stdout)
+        card = next(iter(info.values()))
+        return {k: v for k, v in card.items() if "clock" in k.lower() and "sclk" in k.lower()
+                or "mclk" in k.lower()} or None
+    except Exception:
+        return None
+
+
 def cpu_baseline(w, mix, theta, sample_rows):
     """The fp64 checker on the first `sample_rows` rows, one full EM iteration, scaled to N."""
     import oracle
@@ -306,6 +320,8 @@ def main():
                      "traffic": measured_traffic(w.name),
                      "kernel_ms": logz_ms,
                      "executed_tflops": round(logz_alg * (3 if logz_b16 else 1), 2),
+                     # k_logz reads X once: its X stream against the HBM peak
+                     "x_stream_gbs": round(4.0 * w.n * d / (logz_ms * 1e-3) / 1e9, 1),
                      "dominant_phase": dominant, "phases_ms": phases,
                      "estep_ms": round(estep_ms, 3),
                      "estep_8nkd_tflops": round(dense_rate, 2),
@@ -313,6 +329,7 @@ def main():
                      "estep_8nkd_frac_bf16_peak": round(dense_rate / BF16_MFMA_PEAK_TFLOPS, 4)},
         "cpu_baseline": None,
     }
+    result["gpu_clocks"] = gpu_clocks()
     if args.cpu_sample > 0:
         log("  cpu baseline ...")
         result["cpu_baseline"] = cpu_baseline(w, mix, th0, min(args.cpu_sample, w.n))
