@@ -52,6 +52,11 @@ def _load():
         lib.oracle_assign_topk.argtypes = [vp, i64, i32, i32, vp, vp, vp, i32, f64, vp, vp, i32,
                                            vp, vp, i32]
         lib.oracle_assign_topk.restype = ctypes.c_int
+        lib.oracle_iso_estep.argtypes = [vp, i64, i32, i32, vp, vp, vp, vp, vp, vp, vp, i32]
+        lib.oracle_iso_estep.restype = None
+        lib.oracle_iso_iterate.argtypes = [vp, i64, i32, i32, vp, vp, vp, f64, vp, vp, vp, vp,
+                                           vp, vp, vp, i32]
+        lib.oracle_iso_iterate.restype = None
         _lib = lib
     return _lib
 
@@ -160,3 +165,58 @@ def assign_topk(x, weights, means, variances, m, tau, mr=0, nthreads=None):
     if mr:
         return idx, resp, ridx, rresp
     return idx, resp
+
+
+# ---------------------------------------------------------------- isotropic model (Sec. 2)
+def _theta_iso(weights, means, variances):
+    w, mu, var = _f32(weights), _f32(means), _f32(variances)
+    k, d = mu.shape
+    assert w.shape == (k,) and var.shape == (k,)
+    return w, mu, var, k, d
+
+
+def iso_estep(x, weights, means, variances, nthreads=None):
+    """Isotropic E-step statistics (one scalar variance per component), fp64:
+    dict(nk[K], s[K,D], q[K] = sum r ||x||^2, loglik)."""
+    x = _f32(x)
+    w, mu, var, k, d = _theta_iso(weights, means, variances)
+    n = x.shape[0]
+    assert x.shape == (n, d)
+    nk, s, q, ll = np.zeros(k), np.zeros((k, d)), np.zeros(k), np.zeros(1)
+    _load().oracle_iso_estep(_p(x), n, d, k, _p(w), _p(mu), _p(var), _p(nk), _p(s), _p(q),
+                             _p(ll), nthreads or default_threads())
+    return dict(nk=nk, s=s, q=q, loglik=float(ll[0]))
+
+
+def iso_iterate(x, weights, means, variances, var_floor=DEFAULT_VAR_FLOOR, nthreads=None):
+    """One isotropic EM iteration.  Returns dict(weights, means, vars[K] (fp64, Theta_{t+1}),
+    loglik (= LL(Theta_t)), nk, s, q[K])."""
+    x = _f32(x)
+    w, mu, var, k, d = _theta_iso(weights, means, variances)
+    n = x.shape[0]
+    assert x.shape == (n, d)
+    w1, mu1, var1 = np.zeros(k), np.zeros((k, d)), np.zeros(k)
+    nk, s, q, ll = np.zeros(k), np.zeros((k, d)), np.zeros(k), np.zeros(1)
+    _load().oracle_iso_iterate(_p(x), n, d, k, _p(w), _p(mu), _p(var), float(var_floor), _p(w1),
+                               _p(mu1), _p(var1), _p(nk), _p(s), _p(q), _p(ll),
+                               nthreads or default_threads())
+    return dict(weights=w1, means=mu1, vars=var1, loglik=float(ll[0]), nk=nk, s=s, q=q)
+
+
+def iso_fit(x, weights, means, variances, n_iters, var_floor=DEFAULT_VAR_FLOOR, nthreads=None,
+            keep_thetas=False):
+    """n_iters isotropic EM iterations from Theta_0 (fp32 parameters between iterations)."""
+    th = (_f32(weights), _f32(means), _f32(variances))
+    hist = np.zeros(n_iters)
+    thetas = []
+    for t in range(n_iters):
+        if keep_thetas:
+            thetas.append(th)
+        r = iso_iterate(x, *th, var_floor=var_floor, nthreads=nthreads)
+        hist[t] = r["loglik"]
+        th = (_f32(r["weights"]), _f32(r["means"]), _f32(r["vars"]))
+    out = dict(weights=th[0], means=th[1], vars=th[2], loglik_hist=hist)
+    if keep_thetas:
+        out["thetas"] = thetas
+    return out
+

@@ -335,3 +335,173 @@ int oracle_assign_topk(const float* x, int64_t n, int32_t d, int32_t k, const fl
   params_free(&p);
   return 0;
 }
+
+/* ------------------------------------------------------------------ */
+/*
+ * The paper's own model (Sec. 2): isotropic components N(mu_k, var_k I) with
+ * one scalar variance per component.  Written on its own from the model,
+ * not through the diagonal code above:
+ *
+ *   log-density  l_ik = log pi_k - D/2 log(2 pi var_k) - ||x_i - mu_k||^2 / (2 var_k)
+ *   statistics   N_k = sum_i r_ik,  S_kd = sum_i r_ik x_id,
+ *                Q_k = sum_i r_ik ||x_i||^2   (raw, scalar per component)
+ *   M-step       pi_k = N_k / N,  mu_k = S_k / N_k                     (Eqs. Nk, muk)
+ *                var_k = max(var_floor, sum_i r_ik ||x_i - mu_k||^2 / (D N_k))  (Eq. sig,
+ *                the new mean, a second sweep); dead rule as above.
+ */
+typedef struct {
+  int32_t d, k;
+  const float* mu;   /* k*d, fp32 as given */
+  double* ivar;      /* k: 1 / var_k */
+  double* cst;       /* k: log pi_k - D/2 log(2 pi var_k), -inf if pi_k == 0 */
+} iso_params;
+
+static void iso_init(iso_params* p, int32_t d, int32_t k, const float* w, const float* mu,
+                     const float* var) {
+  p->d = d; p->k = k; p->mu = mu;
+  p->ivar = (double*)malloc(sizeof(double) * (size_t)k);
+  p->cst = (double*)malloc(sizeof(double) * (size_t)k);
+  for (int32_t c = 0; c < k; ++c) {
+    const double v = (double)var[c];
+    p->ivar[c] = 1.0 / v;
+    p->cst[c] = (w[c] > 0.0f) ? log((double)w[c]) - 0.5 * (double)d * (LOG_2PI + log(v))
+                              : -INFINITY;
+  }
+}
+
+static void iso_free(iso_params* p) { free(p->ivar); free(p->cst); }
+
+static void iso_logdens(const iso_params* p, const float* x, double* l) {
+  for (int32_t c = 0; c < p->k; ++c) {
+    if (p->cst[c] == -INFINITY) { l[c] = -INFINITY; continue; }
+    const float* mu = p->mu + (int64_t)c * p->d;
+    double dist = 0.0;
+    for (int32_t j = 0; j < p->d; ++j) {
+      const double t = (double)x[j] - (double)mu[j];
+      dist += t * t;
+    }
+    l[c] = p->cst[c] - 0.5 * dist * p->ivar[c];
+  }
+}
+
+typedef struct {
+  const iso_params* p;
+  const float* x;
+  int64_t i0, i1;
+  int mode;              /* 0: N, S, Q, LL; 1: V about mu2 */
+  const double* mu2;
+  double *nk, *s, *q, *v, ll;
+} iso_job;
+
+static void* iso_worker(void* arg) {
+  iso_job* jb = (iso_job*)arg;
+  const iso_params* p = jb->p;
+  const int32_t d = p->d, k = p->k;
+  double* l = (double*)malloc(sizeof(double) * (size_t)k);
+  jb->ll = 0.0;
+  for (int64_t i = jb->i0; i < jb->i1; ++i) {
+    const float* x = jb->x + i * (int64_t)d;
+    iso_logdens(p, x, l);
+    const double lz = lse(l, k);
+    if (jb->mode == 0) jb->ll += lz;
+    double xx = 0.0;
+    for (int32_t j = 0; j < d; ++j) xx += (double)x[j] * (double)x[j];
+    for (int32_t c = 0; c < k; ++c) {
+      const double r = exp(l[c] - lz);
+      if (r == 0.0) continue;
+      if (jb->mode == 0) {
+        jb->nk[c] += r;
+        jb->q[c] += r * xx;
+        for (int32_t j = 0; j < d; ++j) jb->s[(int64_t)c * d + j] += r * (double)x[j];
+      } else {
+        double dist = 0.0;
+        for (int32_t j = 0; j < d; ++j) {
+          const double t = (double)x[j] - jb->mu2[(int64_t)c * d + j];
+          dist += t * t;
+        }
+        jb->v[c] += r * dist;
+      }
+    }
+  }
+  free(l);
+  return NULL;
+}
+
+static void iso_sweep(const iso_params* p, const float* x, int64_t n, int mode, const double* mu2,
+                      double* nk, double* s, double* q, double* v, double* ll, int32_t nthreads) {
+  const int32_t d = p->d, k = p->k;
+  const size_t kd = (size_t)k * d, per = (size_t)3 * k + kd;
+  iso_job jobs[ORACLE_SLOTS];
+  double* buf = (double*)calloc((size_t)ORACLE_SLOTS * per, sizeof(double));
+  for (int t = 0; t < ORACLE_SLOTS; ++t) {
+    iso_job* jb = &jobs[t];
+    memset(jb, 0, sizeof(*jb));
+    jb->p = p; jb->x = x; jb->mode = mode; jb->mu2 = mu2;
+    jb->i0 = n * t / ORACLE_SLOTS;
+    jb->i1 = n * (t + 1) / ORACLE_SLOTS;
+    double* b = buf + (size_t)t * per;
+    jb->nk = b; jb->q = b + k; jb->v = b + 2 * k; jb->s = b + 3 * k;
+  }
+  if (nthreads < 1) nthreads = 1;
+  if (nthreads > ORACLE_SLOTS) nthreads = ORACLE_SLOTS;
+  for (int t0 = 0; t0 < ORACLE_SLOTS; t0 += nthreads) {
+    pthread_t th[ORACLE_SLOTS];
+    int t1 = t0 + nthreads < ORACLE_SLOTS ? t0 + nthreads : ORACLE_SLOTS;
+    for (int t = t0; t < t1; ++t) pthread_create(&th[t], NULL, iso_worker, &jobs[t]);
+    for (int t = t0; t < t1; ++t) pthread_join(th[t], NULL);
+  }
+  for (int t = 0; t < ORACLE_SLOTS; ++t) {
+    const iso_job* jb = &jobs[t];
+    if (mode == 0) {
+      for (int32_t c = 0; c < k; ++c) { nk[c] += jb->nk[c]; q[c] += jb->q[c]; }
+      for (size_t e = 0; e < kd; ++e) s[e] += jb->s[e];
+      *ll += jb->ll;
+    } else {
+      for (int32_t c = 0; c < k; ++c) v[c] += jb->v[c];
+    }
+  }
+  free(buf);
+}
+
+/* Isotropic E-step statistics: ADDS N_k, S (k*d), Q (k) and LL. */
+void oracle_iso_estep(const float* x, int64_t n, int32_t d, int32_t k, const float* w,
+                      const float* mu, const float* var, double* nk, double* s, double* q,
+                      double* ll, int32_t nthreads) {
+  iso_params p;
+  iso_init(&p, d, k, w, mu, var);
+  iso_sweep(&p, x, n, 0, NULL, nk, s, q, NULL, ll, nthreads);
+  iso_free(&p);
+}
+
+/* One isotropic EM iteration; Theta_{t+1} as fp64, statistics overwritten. */
+void oracle_iso_iterate(const float* x, int64_t n, int32_t d, int32_t k, const float* w,
+                        const float* mu, const float* var, double var_floor, double* w_out,
+                        double* mu_out, double* var_out, double* nk, double* s, double* q,
+                        double* ll, int32_t nthreads) {
+  iso_params p;
+  iso_init(&p, d, k, w, mu, var);
+  const size_t kd = (size_t)k * d;
+  memset(nk, 0, sizeof(double) * (size_t)k);
+  memset(q, 0, sizeof(double) * (size_t)k);
+  memset(s, 0, sizeof(double) * kd);
+  *ll = 0.0;
+  iso_sweep(&p, x, n, 0, NULL, nk, s, q, NULL, ll, nthreads);
+  for (int32_t c = 0; c < k; ++c)
+    for (int32_t j = 0; j < d; ++j) {
+      const size_t e = (size_t)c * d + j;
+      mu_out[e] = nk[c] > 0.0 ? s[e] / nk[c] : (double)mu[e];
+    }
+  double* v = (double*)calloc((size_t)k, sizeof(double));
+  iso_sweep(&p, x, n, 1, mu_out, NULL, NULL, NULL, v, NULL, nthreads);
+  for (int32_t c = 0; c < k; ++c) {
+    w_out[c] = nk[c] / (double)n;
+    if (nk[c] > 0.0) {
+      const double vv = v[c] / ((double)d * nk[c]);
+      var_out[c] = vv > var_floor ? vv : var_floor;
+    } else {
+      var_out[c] = (double)var[c];
+    }
+  }
+  free(v);
+  iso_free(&p);
+}
