@@ -128,6 +128,32 @@ int gmm_assign_topk(const float* x, int64_t n, int32_t d, int32_t k, const float
                     float* resp, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * The paper's own model (Sec. 2, Eqs. Nk, muk, sig): isotropic components
+ * N(mu_k, var_k I) with ONE variance per component, vars[k] (fp32, device).
+ * The same conventions as the diagonal calls above, with
+ *   l_ik = log pi_k - D/2 log(2 pi var_k) - ||x_i - mu_k||^2 / (2 var_k)
+ * gmm_estep_accumulate_iso ADDS nk[k], s[k*d] as above and the scalar
+ *   q[k] += sum_i r_ik ||x_i||^2
+ * (it runs the diagonal E-step with var_kd = var_k; its workspace is the one
+ * gmm_workspace_bytes(n, d, k, 0) gives).  gmm_mstep_iso writes
+ *   pi_k = nk[k] / n_total,  mu_kj = s[k*d+j] / nk[k],
+ *   var_k = max(var_floor, (q[k] / nk[k] - ||mu_k||^2) / d)
+ * (= sum_i r_ik ||x_i - mu_k||^2 / (d nk[k]) for the new mean), with the same
+ * dead-component rule.  gmm_fit_iso runs n_iters isotropic iterations, as
+ * gmm_fit does.  Same status codes as the diagonal calls.
+ */
+int gmm_estep_accumulate_iso(const float* x, int64_t n, int32_t d, int32_t k,
+                             const float* weights, const float* means, const float* vars,
+                             double* nk, double* s, double* q, double* loglik, void* ws,
+                             size_t ws_bytes, hipStream_t stream);
+int gmm_mstep_iso(const double* nk, const double* s, const double* q, double n_total, int32_t d,
+                  int32_t k, float var_floor, float* weights, float* means, float* vars,
+                  hipStream_t stream);
+int gmm_fit_iso(const float* x, int64_t n, int32_t d, int32_t k, int32_t n_iters, float var_floor,
+                float* weights, float* means, float* vars, double* loglik_hist, void* ws,
+                size_t ws_bytes, hipStream_t stream);
+
+/*
  * Phase timing of the E-step, a measurement aid (no part of the method).
  * While enabled, every E-step (gmm_estep_accumulate, each iteration of
  * gmm_fit) records HIP events on its stream between its phases, waits for the

@@ -26,7 +26,8 @@ GMM_MAX_M = 8
 
 #: every symbol the C ABI exports
 EXPORTS = ("gmm_status_string", "gmm_workspace_bytes", "gmm_estep_accumulate", "gmm_mstep",
-           "gmm_fit", "gmm_assign_topk", "gmm_timing_enable", "gmm_timing_read")
+           "gmm_fit", "gmm_assign_topk", "gmm_estep_accumulate_iso", "gmm_mstep_iso",
+           "gmm_fit_iso", "gmm_timing_enable", "gmm_timing_read")
 
 _lib = None
 
@@ -66,6 +67,12 @@ def load_library():
     lib.gmm_assign_topk.argtypes = [vp, i64, i32, i32, vp, vp, vp, i32, f32, vp, vp, vp,
                                     ctypes.c_size_t, vp]
     lib.gmm_assign_topk.restype = ctypes.c_int
+    lib.gmm_estep_accumulate_iso.argtypes = lib.gmm_estep_accumulate.argtypes
+    lib.gmm_estep_accumulate_iso.restype = ctypes.c_int
+    lib.gmm_mstep_iso.argtypes = lib.gmm_mstep.argtypes
+    lib.gmm_mstep_iso.restype = ctypes.c_int
+    lib.gmm_fit_iso.argtypes = lib.gmm_fit.argtypes
+    lib.gmm_fit_iso.restype = ctypes.c_int
     lib.gmm_timing_enable.argtypes = [ctypes.c_int]
     lib.gmm_timing_enable.restype = ctypes.c_int
     lib.gmm_timing_read.argtypes = [vp, i32, vp]
@@ -100,10 +107,14 @@ def _check(fn, rc):
         raise GMMError(fn, rc)
 
 
-def _dev(t, dtype, name):
+def _dev(t, dtype, name, numel=None):
+    """t as given, after checking that it is a contiguous CUDA tensor of `dtype` holding at
+    least `numel` elements (the library reads and writes exactly the sizes (n, d, k) imply)."""
     import torch
     if not (isinstance(t, torch.Tensor) and t.is_cuda and t.dtype == dtype and t.is_contiguous()):
         raise TypeError(f"{name} must be a contiguous {dtype} CUDA tensor")
+    if numel is not None and t.numel() < numel:
+        raise ValueError(f"{name} holds {t.numel()} elements, {numel} needed")
     return t
 
 
@@ -124,10 +135,11 @@ def gmm_estep_accumulate(x, weights, means, variances, nk, s, q, loglik, ws, str
     n, d = x.shape
     k = weights.shape[0]
     rc = load_library().gmm_estep_accumulate(
-        _ptr(x), n, d, k, _ptr(_dev(weights, torch.float32, "weights")),
-        _ptr(_dev(means, torch.float32, "means")), _ptr(_dev(variances, torch.float32, "vars")),
-        _ptr(_dev(nk, torch.float64, "nk")), _ptr(_dev(s, torch.float64, "s")),
-        _ptr(_dev(q, torch.float64, "q")), _ptr(_dev(loglik, torch.float64, "loglik")),
+        _ptr(x), n, d, k, _ptr(_dev(weights, torch.float32, "weights", k)),
+        _ptr(_dev(means, torch.float32, "means", k * d)),
+        _ptr(_dev(variances, torch.float32, "vars", k * d)),
+        _ptr(_dev(nk, torch.float64, "nk", k)), _ptr(_dev(s, torch.float64, "s", k * d)),
+        _ptr(_dev(q, torch.float64, "q", k * d)), _ptr(_dev(loglik, torch.float64, "loglik", 1)),
         _ptr(ws), ws.numel() if ws is not None else 0, _stream(stream))
     _check("gmm_estep_accumulate", rc)
 
@@ -137,10 +149,11 @@ def gmm_mstep(nk, s, q, n_total, weights, means, variances, var_floor=1e-6, stre
     import torch
     k, d = means.shape
     rc = load_library().gmm_mstep(
-        _ptr(_dev(nk, torch.float64, "nk")), _ptr(_dev(s, torch.float64, "s")),
-        _ptr(_dev(q, torch.float64, "q")), float(n_total), d, k, float(var_floor),
-        _ptr(_dev(weights, torch.float32, "weights")), _ptr(_dev(means, torch.float32, "means")),
-        _ptr(_dev(variances, torch.float32, "vars")), _stream(stream))
+        _ptr(_dev(nk, torch.float64, "nk", k)), _ptr(_dev(s, torch.float64, "s", k * d)),
+        _ptr(_dev(q, torch.float64, "q", k * d)), float(n_total), d, k, float(var_floor),
+        _ptr(_dev(weights, torch.float32, "weights", k)),
+        _ptr(_dev(means, torch.float32, "means", k * d)),
+        _ptr(_dev(variances, torch.float32, "vars", k * d)), _stream(stream))
     _check("gmm_mstep", rc)
 
 
@@ -152,9 +165,10 @@ def gmm_fit(x, weights, means, variances, n_iters, loglik_hist, ws, var_floor=1e
     k = weights.shape[0]
     rc = load_library().gmm_fit(
         _ptr(x), n, d, k, int(n_iters), float(var_floor),
-        _ptr(_dev(weights, torch.float32, "weights")), _ptr(_dev(means, torch.float32, "means")),
-        _ptr(_dev(variances, torch.float32, "vars")),
-        _ptr(_dev(loglik_hist, torch.float64, "loglik_hist")), _ptr(ws),
+        _ptr(_dev(weights, torch.float32, "weights", k)),
+        _ptr(_dev(means, torch.float32, "means", k * d)),
+        _ptr(_dev(variances, torch.float32, "vars", k * d)),
+        _ptr(_dev(loglik_hist, torch.float64, "loglik_hist", n_iters)), _ptr(ws),
         ws.numel() if ws is not None else 0, _stream(stream))
     _check("gmm_fit", rc)
 
@@ -166,12 +180,60 @@ def gmm_assign_topk(x, weights, means, variances, m, tau, idx, resp, ws, stream=
     n, d = x.shape
     k = weights.shape[0]
     rc = load_library().gmm_assign_topk(
-        _ptr(x), n, d, k, _ptr(_dev(weights, torch.float32, "weights")),
-        _ptr(_dev(means, torch.float32, "means")), _ptr(_dev(variances, torch.float32, "vars")),
-        int(m), float(tau), _ptr(_dev(idx, torch.int32, "idx")),
-        _ptr(_dev(resp, torch.float32, "resp")), _ptr(ws), ws.numel() if ws is not None else 0,
-        _stream(stream))
+        _ptr(x), n, d, k, _ptr(_dev(weights, torch.float32, "weights", k)),
+        _ptr(_dev(means, torch.float32, "means", k * d)),
+        _ptr(_dev(variances, torch.float32, "vars", k * d)),
+        int(m), float(tau), _ptr(_dev(idx, torch.int32, "idx", n * m)),
+        _ptr(_dev(resp, torch.float32, "resp", n * m)), _ptr(ws),
+        ws.numel() if ws is not None else 0, _stream(stream))
     _check("gmm_assign_topk", rc)
+
+
+def gmm_estep_accumulate_iso(x, weights, means, variances, nk, s, q, loglik, ws, stream=None):
+    """Isotropic E-step (one variance per component, variances [k]): adds nk, s and the
+    scalar q[k] = sum r ||x||^2 (fp64 CUDA tensors) and loglik."""
+    import torch
+    _dev(x, torch.float32, "x")
+    n, d = x.shape
+    k = weights.shape[0]
+    rc = load_library().gmm_estep_accumulate_iso(
+        _ptr(x), n, d, k, _ptr(_dev(weights, torch.float32, "weights", k)),
+        _ptr(_dev(means, torch.float32, "means", k * d)),
+        _ptr(_dev(variances, torch.float32, "vars", k)),
+        _ptr(_dev(nk, torch.float64, "nk", k)), _ptr(_dev(s, torch.float64, "s", k * d)),
+        _ptr(_dev(q, torch.float64, "q", k)), _ptr(_dev(loglik, torch.float64, "loglik", 1)),
+        _ptr(ws), ws.numel() if ws is not None else 0, _stream(stream))
+    _check("gmm_estep_accumulate_iso", rc)
+
+
+def gmm_mstep_iso(nk, s, q, n_total, weights, means, variances, var_floor=1e-6, stream=None):
+    """Isotropic M-step from fp64 statistics (q[k] scalar); updates the fp32 parameters."""
+    import torch
+    k, d = means.shape
+    rc = load_library().gmm_mstep_iso(
+        _ptr(_dev(nk, torch.float64, "nk", k)), _ptr(_dev(s, torch.float64, "s", k * d)),
+        _ptr(_dev(q, torch.float64, "q", k)), float(n_total), d, k, float(var_floor),
+        _ptr(_dev(weights, torch.float32, "weights", k)),
+        _ptr(_dev(means, torch.float32, "means", k * d)),
+        _ptr(_dev(variances, torch.float32, "vars", k)), _stream(stream))
+    _check("gmm_mstep_iso", rc)
+
+
+def gmm_fit_iso(x, weights, means, variances, n_iters, loglik_hist, ws, var_floor=1e-6,
+                stream=None):
+    """n_iters isotropic EM iterations (variances [k]); loglik_hist[t] = LL(Theta_t)."""
+    import torch
+    _dev(x, torch.float32, "x")
+    n, d = x.shape
+    k = weights.shape[0]
+    rc = load_library().gmm_fit_iso(
+        _ptr(x), n, d, k, int(n_iters), float(var_floor),
+        _ptr(_dev(weights, torch.float32, "weights", k)),
+        _ptr(_dev(means, torch.float32, "means", k * d)),
+        _ptr(_dev(variances, torch.float32, "vars", k)),
+        _ptr(_dev(loglik_hist, torch.float64, "loglik_hist", n_iters)), _ptr(ws),
+        ws.numel() if ws is not None else 0, _stream(stream))
+    _check("gmm_fit_iso", rc)
 
 
 TIMING_PHASES = ("prep", "logz", "dense_stats", "exact_pairs", "ill_and_reduce")

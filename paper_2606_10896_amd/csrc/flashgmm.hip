@@ -2645,6 +2645,56 @@ __global__ __launch_bounds__(256) void k_mstep(const double* __restrict__ nk,
   if (j == 0) w[comp] = (float)(nn / n_total);
 }
 
+// ---------------------------------------------------------------- isotropic model
+// The paper's own model (Sec. 2): one variance per component, N(mu_k, var_k I).
+// Its E-step is the diagonal one with var_kd = var_k for every d, so the
+// isotropic calls expand the variances and run the diagonal kernels; the
+// isotropic second moment is Q_k = sum_d Q_kd = sum_i r_ik ||x_i||^2.
+__global__ __launch_bounds__(256) void k_iso_expand(const float* __restrict__ var_iso, int d,
+                                                    int k, float* __restrict__ var) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (int64_t)k * d) return;
+  var[t] = var_iso[t / d];
+}
+
+// q[c] += sum_d qd[c d + j], dimensions in order, fp64.
+__global__ __launch_bounds__(256) void k_iso_qsum(const double* __restrict__ qd, int d, int k,
+                                                  double* __restrict__ q) {
+  const int c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= k) return;
+  double acc = 0.0;
+  for (int j = 0; j < d; ++j) acc += qd[(int64_t)c * d + j];
+  q[c] += acc;
+}
+
+// Isotropic M-step (Eqs. Nk, muk, sig): pi = N / n, mu = S / N and
+// var = max(floor, (Q / N - ||mu||^2) / D), which is sum_i r ||x_i - mu||^2 / (D N)
+// for the new mean; N == 0 exactly keeps mu and var and sets pi = 0.
+__global__ __launch_bounds__(256) void k_mstep_iso(const double* __restrict__ nk,
+                                                   const double* __restrict__ s,
+                                                   const double* __restrict__ q, double n_total,
+                                                   int d, int k, double var_floor,
+                                                   float* __restrict__ w, float* __restrict__ mu,
+                                                   float* __restrict__ var) {
+  const int c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= k) return;
+  const double nn = nk[c];
+  if (nn == 0.0) {
+    w[c] = 0.0f;
+    return;
+  }
+  double mm = 0.0;
+  for (int j = 0; j < d; ++j) {
+    const double m = s[(int64_t)c * d + j] / nn;
+    mm += m * m;
+    mu[(int64_t)c * d + j] = (float)m;
+  }
+  double v = (q[c] / nn - mm) / (double)d;
+  if (!(v > var_floor)) v = var_floor;
+  var[c] = (float)v;
+  w[c] = (float)(nn / n_total);
+}
+
 __global__ __launch_bounds__(256) void k_zero(double* __restrict__ p, int64_t cnt) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t < cnt) p[t] = 0.0;
@@ -2671,7 +2721,7 @@ struct Layout {
   size_t off_counts, off_cls, off_cwell, off_cdir, off_cthr, off_thr, off_well_idx, off_ill_idx,
       off_cw, off_wp, off_wq, off_wpb, off_dmu, off_dh, off_logz2, off_cslot, off_cr, off_llpart,
       off_part_w, off_part_s, off_part_i, off_scnt, off_soff, off_slist, off_bmask, off_fit_nk,
-      off_fit_s, off_fit_q, total;
+      off_fit_s, off_fit_q, off_iso_var, off_iso_q, total;
 };
 
 // Padded dimension count of the kernels: a multiple of 64 up to 256, of 128 above.
@@ -2758,6 +2808,9 @@ bool make_layout(int64_t n, int d, int k, int m, Layout* L) {
   L->off_fit_nk = take((size_t)k * sizeof(double) + sizeof(double));  // + loglik slot
   L->off_fit_s = take((size_t)k * d * sizeof(double));
   L->off_fit_q = take((size_t)k * d * sizeof(double));
+  // isotropic calls: the expanded variances and the isotropic Q of gmm_fit_iso
+  L->off_iso_var = take((size_t)k * d * sizeof(float));
+  L->off_iso_q = take((size_t)k * sizeof(double));
   L->total = o;
   return true;
 }
@@ -3054,6 +3107,81 @@ int gmm_fit(const float* x, int64_t n, int32_t d, int32_t k, int32_t n_iters, fl
     if (rc != GMM_OK) return rc;
     hipLaunchKernelGGL(k_mstep, dim3((unsigned)cdiv(kd, 256)), dim3(256), 0, stream, fnk, fs, fq,
                        (double)n, d, k, (double)var_floor, weights, means, vars);
+    rc = launch_status();
+    if (rc != GMM_OK) return rc;
+  }
+  return GMM_OK;
+}
+
+int gmm_estep_accumulate_iso(const float* x, int64_t n, int32_t d, int32_t k,
+                             const float* weights, const float* means, const float* vars,
+                             double* nk, double* s, double* q, double* loglik, void* ws,
+                             size_t ws_bytes, hipStream_t stream) {
+  int rc = check_shape(n, d, k);
+  if (rc != GMM_OK) return rc;
+  if (!x || !weights || !means || !vars || !nk || !s || !q || !loglik) return GMM_ERR_INVALID_ARG;
+  Layout L;
+  if (!make_layout(n, d, k, 0, &L)) return GMM_ERR_UNSUPPORTED;
+  rc = check_ws(L, ws, ws_bytes);
+  if (rc != GMM_OK) return rc;
+  float* vfull = at<float>(ws, L.off_iso_var);
+  double* qd = at<double>(ws, L.off_fit_q);
+  const int64_t kd = (int64_t)k * d;
+  hipLaunchKernelGGL(k_iso_expand, dim3((unsigned)cdiv(kd, 256)), dim3(256), 0, stream, vars, d,
+                     k, vfull);
+  hipLaunchKernelGGL(k_zero, dim3((unsigned)cdiv(kd, 256)), dim3(256), 0, stream, qd, kd);
+  rc = estep_dispatch(L, x, weights, means, vfull, nk, s, qd, loglik, 1, ws, stream);
+  if (rc != GMM_OK) return rc;
+  hipLaunchKernelGGL(k_iso_qsum, dim3((unsigned)cdiv(k, 256)), dim3(256), 0, stream, qd, d, k, q);
+  return launch_status();
+}
+
+int gmm_mstep_iso(const double* nk, const double* s, const double* q, double n_total, int32_t d,
+                  int32_t k, float var_floor, float* weights, float* means, float* vars,
+                  hipStream_t stream) {
+  if (d < 1 || k < 1) return GMM_ERR_INVALID_ARG;
+  if (d > GMM_MAX_D || k > GMM_MAX_K) return GMM_ERR_UNSUPPORTED;
+  if (!nk || !s || !q || !weights || !means || !vars) return GMM_ERR_INVALID_ARG;
+  if (!(n_total > 0.0) || !(var_floor >= 0.0f)) return GMM_ERR_INVALID_ARG;
+  hipLaunchKernelGGL(k_mstep_iso, dim3((unsigned)cdiv(k, 256)), dim3(256), 0, stream, nk, s, q,
+                     n_total, d, k, (double)var_floor, weights, means, vars);
+  return launch_status();
+}
+
+int gmm_fit_iso(const float* x, int64_t n, int32_t d, int32_t k, int32_t n_iters, float var_floor,
+                float* weights, float* means, float* vars, double* loglik_hist, void* ws,
+                size_t ws_bytes, hipStream_t stream) {
+  int rc = check_shape(n, d, k);
+  if (rc != GMM_OK) return rc;
+  if (n_iters < 0 || !x || !weights || !means || !vars || (n_iters > 0 && !loglik_hist))
+    return GMM_ERR_INVALID_ARG;
+  if (!(var_floor >= 0.0f)) return GMM_ERR_INVALID_ARG;
+  Layout L;
+  if (!make_layout(n, d, k, 0, &L)) return GMM_ERR_UNSUPPORTED;
+  rc = check_ws(L, ws, ws_bytes);
+  if (rc != GMM_OK) return rc;
+  double* fnk = at<double>(ws, L.off_fit_nk);
+  double* fs = at<double>(ws, L.off_fit_s);
+  double* fqd = at<double>(ws, L.off_fit_q);
+  double* fq = at<double>(ws, L.off_iso_q);
+  float* vfull = at<float>(ws, L.off_iso_var);
+  const int64_t kd = (int64_t)k * d;
+  for (int t = 0; t < n_iters; ++t) {
+    hipLaunchKernelGGL(k_zero, dim3((unsigned)cdiv(k, 256)), dim3(256), 0, stream, fnk,
+                       (int64_t)k);
+    hipLaunchKernelGGL(k_zero, dim3((unsigned)cdiv(k, 256)), dim3(256), 0, stream, fq,
+                       (int64_t)k);
+    hipLaunchKernelGGL(k_zero, dim3((unsigned)cdiv(kd, 256)), dim3(256), 0, stream, fs, kd);
+    hipLaunchKernelGGL(k_zero, dim3((unsigned)cdiv(kd, 256)), dim3(256), 0, stream, fqd, kd);
+    hipLaunchKernelGGL(k_iso_expand, dim3((unsigned)cdiv(kd, 256)), dim3(256), 0, stream, vars,
+                       d, k, vfull);
+    rc = estep_dispatch(L, x, weights, means, vfull, fnk, fs, fqd, loglik_hist + t, 0, ws,
+                        stream);
+    if (rc != GMM_OK) return rc;
+    hipLaunchKernelGGL(k_iso_qsum, dim3((unsigned)cdiv(k, 256)), dim3(256), 0, stream, fqd, d, k,
+                       fq);
+    hipLaunchKernelGGL(k_mstep_iso, dim3((unsigned)cdiv(k, 256)), dim3(256), 0, stream, fnk, fs,
+                       fq, (double)n, d, k, (double)var_floor, weights, means, vars);
     rc = launch_status();
     if (rc != GMM_OK) return rc;
   }

@@ -102,6 +102,57 @@ def check_params(w, mu, var, ref, n_total, label=""):
     return f"mu {err_mu.max():.2e} var {err_v.max():.2e}"
 
 
+# ---- isotropic model (one variance per component)
+def gpu_estep_iso(x, w, mu, var, xd=None, ws=None):
+    import torch
+    import paper_2606_10896_amd as gmm
+    if xd is None:
+        (xd,) = to_dev(x)
+    n, d = xd.shape
+    k = w.shape[0]
+    wd, mud, vd = to_dev(w, mu, var)
+    nk = torch.zeros(k, dtype=torch.float64, device="cuda")
+    s = torch.zeros(k, d, dtype=torch.float64, device="cuda")
+    q = torch.zeros(k, dtype=torch.float64, device="cuda")
+    ll = torch.zeros(1, dtype=torch.float64, device="cuda")
+    if ws is None:
+        ws = gmm.workspace(n, d, k)
+    gmm.gmm_estep_accumulate_iso(xd, wd, mud, vd, nk, s, q, ll, ws)
+    torch.cuda.synchronize()
+    return dict(nk=nk.cpu().numpy(), s=s.cpu().numpy(), q=q.cpu().numpy(), loglik=ll.item())
+
+
+def gpu_mstep_iso(st, n_total, w, mu, var, var_floor=1e-6):
+    import torch
+    import paper_2606_10896_amd as gmm
+    nk, s, q = to_dev(st["nk"], st["s"], st["q"])
+    wd, mud, vd = to_dev(w, mu, var)
+    gmm.gmm_mstep_iso(nk, s, q, n_total, wd, mud, vd, var_floor=var_floor)
+    torch.cuda.synchronize()
+    return wd.cpu().numpy(), mud.cpu().numpy(), vd.cpu().numpy()
+
+
+def gpu_fit_iso(x, w, mu, var, n_iters, var_floor=1e-6, xd=None):
+    import torch
+    import paper_2606_10896_amd as gmm
+    if xd is None:
+        (xd,) = to_dev(x)
+    n, d = xd.shape
+    k = w.shape[0]
+    wd, mud, vd = to_dev(w, mu, var)
+    hist = torch.zeros(max(n_iters, 1), dtype=torch.float64, device="cuda")
+    ws = gmm.workspace(n, d, k)
+    gmm.gmm_fit_iso(xd, wd, mud, vd, n_iters, hist, ws, var_floor=var_floor)
+    torch.cuda.synchronize()
+    return wd.cpu().numpy(), mud.cpu().numpy(), vd.cpu().numpy(), hist.cpu().numpy()[:n_iters]
+
+
+def check_params_iso(w, mu, var, ref, n_total, label=""):
+    """Isotropic M-step against the checker: as check_params, with one variance per
+    component (and sigma = sqrt(var_k) for every dimension of the mean)."""
+    return check_params(w, mu, var[:, None], dict(ref, vars=ref["vars"][:, None]), n_total, label)
+
+
 # ---- top-m assignment (Sec. 4.2 / 4.3)
 MARGIN = 1e-6   # an index must match where the checker's top-m margin exceeds this
 TOL_RESP = 1e-4

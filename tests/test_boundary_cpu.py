@@ -90,6 +90,22 @@ def test_host_validation_returns_before_any_launch():
     assert lib.gmm_mstep(None, p, p, 10.0, 8, 4, 1e-6, p, p, p, None) == gmm.GMM_ERR_INVALID_ARG
 
 
+def test_isotropic_host_validation():
+    lib = gmm.load_library()
+    p, ws = _fake(), _fake(0x200000)
+    big = gmm.workspace_bytes(1000, 8, 4)
+    assert lib.gmm_estep_accumulate_iso(p, 0, 8, 4, p, p, p, p, p, p, p, ws, big, None) == gmm.GMM_ERR_INVALID_ARG
+    assert lib.gmm_estep_accumulate_iso(p, 1000, 8, 4, p, p, None, p, p, p, p, ws, big, None) == gmm.GMM_ERR_INVALID_ARG
+    assert lib.gmm_estep_accumulate_iso(p, 1000, 1025, 4, p, p, p, p, p, p, p, ws, big, None) == gmm.GMM_ERR_UNSUPPORTED
+    assert lib.gmm_estep_accumulate_iso(p, 1000, 8, 4, p, p, p, p, p, p, p, ws, big - 1, None) == gmm.GMM_ERR_WORKSPACE
+    assert lib.gmm_fit_iso(p, 1000, 8, 4, -1, 1e-6, p, p, p, p, ws, big, None) == gmm.GMM_ERR_INVALID_ARG
+    assert lib.gmm_fit_iso(p, 1000, 8, 4, 3, 1e-6, p, p, p, None, ws, big, None) == gmm.GMM_ERR_INVALID_ARG
+    assert lib.gmm_fit_iso(p, 1000, 8, 4, 3, 1e-6, p, p, p, p, None, big, None) == gmm.GMM_ERR_WORKSPACE
+    assert lib.gmm_mstep_iso(p, p, p, 0.0, 8, 4, 1e-6, p, p, p, None) == gmm.GMM_ERR_INVALID_ARG
+    assert lib.gmm_mstep_iso(p, p, None, 10.0, 8, 4, 1e-6, p, p, p, None) == gmm.GMM_ERR_INVALID_ARG
+    assert lib.gmm_mstep_iso(p, p, p, 10.0, 1025, 4, 1e-6, p, p, p, None) == gmm.GMM_ERR_UNSUPPORTED
+
+
 def test_assign_host_validation():
     lib = gmm.load_library()
     p, ws = _fake(), _fake(0x200000)
