@@ -109,13 +109,13 @@ def gpu_clocks():
         return None
 
 
-def cpu_baseline(w, mix, theta, sample_rows):
+def cpu_baseline(w, mix, theta, sample_rows, iso=False):
     """The fp64 checker on the first `sample_rows` rows, one full EM iteration, scaled to N."""
     import oracle
     x = mix.rows(0, sample_rows, nthreads=max(1, min(16, os.cpu_count() or 1)))
     nthreads = oracle.default_threads()
     t0 = time.time()
-    oracle.iterate(x, *theta, nthreads=nthreads)
+    (oracle.iso_iterate if iso else oracle.iterate)(x, *theta, nthreads=nthreads)
     dt = time.time() - t0
     return {"value": dt * 1e3 * (w.n / sample_rows), "unit": "ms/iter", "cores": nthreads,
             "kind": "oracle",
@@ -213,6 +213,9 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="large")
+    ap.add_argument("--covariance", choices=("diag", "iso"), default="diag",
+                    help="diagonal components (default) or the paper's isotropic ones (one "
+                         "variance per component, the *_iso calls)")
     ap.add_argument("--cpu-sample", type=int, default=100_000,
                     help="rows of the CPU-baseline slice (0 = skip)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -246,6 +249,9 @@ def main():
     log(f"workload {w.name}: N={w.n} D={w.d} K={w.k}")
     x, mix, colsum, colsq = load_data(w, dev)
     th0 = gmm_synth.random_point_init(w, mix, colsum, colsq)
+    iso = args.covariance == "iso"
+    if iso:   # isotropic start: the mean over the dimensions of the init variances
+        th0 = (th0[0], th0[1], th0[2].astype(np.float64).mean(1).astype(np.float32))
     wt, mu, var = (torch.from_numpy(a).to(dev) for a in th0)
     k, d = w.k, w.d
     nk = torch.zeros(k, dtype=torch.float64, device=dev)
@@ -255,14 +261,19 @@ def main():
     ws = gmm.workspace(w.n, d, k, device=dev)
     stream = torch.cuda.current_stream()
 
+    if iso:
+        q = torch.zeros(k, dtype=torch.float64, device=dev)
+    estep = gmm.gmm_estep_accumulate_iso if iso else gmm.gmm_estep_accumulate
+    mstep = gmm.gmm_mstep_iso if iso else gmm.gmm_mstep
+
     def step(i, ev=None):
         nk.zero_(); s.zero_(); q.zero_()
         if ev is not None:
             ev[0].record(stream)
-        gmm.gmm_estep_accumulate(x, wt, mu, var, nk, s, q, ll[i:i + 1], ws, stream=stream)
+        estep(x, wt, mu, var, nk, s, q, ll[i:i + 1], ws, stream=stream)
         if ev is not None:
             ev[1].record(stream)
-        gmm.gmm_mstep(nk, s, q, float(w.n), wt, mu, var, var_floor=1e-6, stream=stream)
+        mstep(nk, s, q, float(w.n), wt, mu, var, var_floor=1e-6, stream=stream)
 
     for i in range(args.warmup):
         step(i)
@@ -308,8 +319,9 @@ def main():
                   "f64 (exact pairs, sums)") if logz_b16 else
                  "f32 MFMA (log-densities, dense statistics), f64 (exact pairs, sums)",
         "data": "synthetic",
-        "config": {"workload": f"{w.name}: diag-GMM EM, N={w.n}, D={d}, K={k}, fp32 points from "
-                               f"{w.k_true} seeded diagonal Gaussians, random-point init",
+        "config": {"workload": f"{w.name}: {'isotropic' if iso else 'diag'}-GMM EM, N={w.n}, "
+                               f"D={d}, K={k}, fp32 points from {w.k_true} seeded diagonal "
+                               "Gaussians, random-point init",
                    "n": w.n, "d": d, "k": k, "parallelism": "single GPU"},
         "roofline": {"bound": "mfma",
                      "kernel": "k_logz (4*N*K*D flop of log-densities per launch, "
@@ -332,7 +344,7 @@ def main():
     result["gpu_clocks"] = gpu_clocks()
     if args.cpu_sample > 0:
         log("  cpu baseline ...")
-        result["cpu_baseline"] = cpu_baseline(w, mix, th0, min(args.cpu_sample, w.n))
+        result["cpu_baseline"] = cpu_baseline(w, mix, th0, min(args.cpu_sample, w.n), iso)
     print(json.dumps(result), flush=True)
 
 
