@@ -213,6 +213,12 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="large")
+    ap.add_argument("--rows", type=int, default=0,
+                    help="take only the first ROWS rows of the workload (0 = all of them)")
+    ap.add_argument("--stream-chunk", type=int, default=0,
+                    help="rows per chunk of the out-of-core E-step (X in pinned host memory, "
+                         "uploaded while the previous chunk runs); 0 = X resident in HBM "
+                         "(the default and the reported value)")
     ap.add_argument("--covariance", choices=("diag", "iso"), default="diag",
                     help="diagonal components (default) or the paper's isotropic ones (one "
                          "variance per component, the *_iso calls)")
@@ -245,6 +251,9 @@ def main():
 
     gmm.load_library()
     w = gmm_synth.WORKLOADS[args.workload]
+    if args.rows > 0:   # the first `rows` rows of the workload's data (same generator)
+        import dataclasses
+        w = dataclasses.replace(w, name=f"{w.name}[:{args.rows}]", n=args.rows)
     dev = torch.device("cuda:0")
     log(f"workload {w.name}: N={w.n} D={w.d} K={w.k}")
     x, mix, colsum, colsq = load_data(w, dev)
@@ -265,6 +274,23 @@ def main():
         q = torch.zeros(k, dtype=torch.float64, device=dev)
     estep = gmm.gmm_estep_accumulate_iso if iso else gmm.gmm_estep_accumulate
     mstep = gmm.gmm_mstep_iso if iso else gmm.gmm_mstep
+    if args.stream_chunk > 0:
+        if iso:
+            sys.exit("--stream-chunk runs the diagonal model only")
+        # out-of-core: X in page-locked host memory, uploaded chunk by chunk
+        rows = min(args.stream_chunk, w.n)
+        xh = torch.empty((w.n, w.d), dtype=torch.float32, pin_memory=True)
+        xh.copy_(x)
+        del x
+        torch.cuda.empty_cache()
+        staging = torch.empty(2 * rows * w.d, dtype=torch.float32, device=dev)
+        ws = gmm.workspace(rows, d, k, device=dev)
+        copy_stream = torch.cuda.Stream()
+
+        def estep(_x, *a, stream=None):
+            gmm.gmm_estep_accumulate_streamed(xh, *a[:7], rows, staging, a[7], stream=stream,
+                                              copy_stream=copy_stream)
+        x = None
 
     def step(i, ev=None):
         nk.zero_(); s.zero_(); q.zero_()
@@ -341,6 +367,9 @@ def main():
                      "estep_8nkd_frac_bf16_peak": round(dense_rate / BF16_MFMA_PEAK_TFLOPS, 4)},
         "cpu_baseline": None,
     }
+    if args.stream_chunk > 0:
+        result["config"]["x_residency"] = (f"pinned host memory, uploaded in chunks of {rows} rows "
+                                           "(PCIe-inclusive rate)")
     result["gpu_clocks"] = gpu_clocks()
     if args.cpu_sample > 0:
         log("  cpu baseline ...")

@@ -128,6 +128,28 @@ int gmm_assign_topk(const float* x, int64_t n, int32_t d, int32_t k, const float
                     float* resp, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * Out-of-core E-step (data larger than the GPU's memory, Sec. 6 of the paper:
+ * X streamed through the device in chunks).  x_host [n*d] fp32 lives in
+ * page-locked host memory that the caller allocated (hipHostMalloc); the
+ * rows are uploaded chunk_rows at a time on copy_stream into the two halves
+ * of the caller's device staging buffer staging [2*min(chunk_rows, n)*d fp32],
+ * while the E-step of the previous chunk runs on `stream`.  The statistics
+ * are ADDED exactly as gmm_estep_accumulate adds them when called chunk by
+ * chunk, in row order, on device copies of the chunks (the result is the
+ * same, bit for bit).  ws is sized by gmm_workspace_bytes(min(chunk_rows, n),
+ * d, k, 0).  The first upload waits for the work already enqueued on `stream`
+ * (which may still read the staging buffer); `stream` holds the statistics
+ * when it completes.  copy_stream and stream may be the same stream (then
+ * nothing overlaps).  Returns GMM_ERR_INVALID_ARG for a null pointer or
+ * chunk_rows < 1, plus the codes of gmm_estep_accumulate.
+ */
+int gmm_estep_accumulate_streamed(const float* x_host, int64_t n, int32_t d, int32_t k,
+                                  const float* weights, const float* means, const float* vars,
+                                  double* nk, double* s, double* q, double* loglik,
+                                  int64_t chunk_rows, float* staging, void* ws, size_t ws_bytes,
+                                  hipStream_t stream, hipStream_t copy_stream);
+
+/*
  * The paper's own model (Sec. 2, Eqs. Nk, muk, sig): isotropic components
  * N(mu_k, var_k I) with ONE variance per component, vars[k] (fp32, device).
  * The same conventions as the diagonal calls above, with

@@ -26,8 +26,9 @@ GMM_MAX_M = 8
 
 #: every symbol the C ABI exports
 EXPORTS = ("gmm_status_string", "gmm_workspace_bytes", "gmm_estep_accumulate", "gmm_mstep",
-           "gmm_fit", "gmm_assign_topk", "gmm_estep_accumulate_iso", "gmm_mstep_iso",
-           "gmm_fit_iso", "gmm_timing_enable", "gmm_timing_read")
+           "gmm_fit", "gmm_assign_topk", "gmm_estep_accumulate_streamed",
+           "gmm_estep_accumulate_iso", "gmm_mstep_iso", "gmm_fit_iso", "gmm_timing_enable",
+           "gmm_timing_read")
 
 _lib = None
 
@@ -67,6 +68,9 @@ def load_library():
     lib.gmm_assign_topk.argtypes = [vp, i64, i32, i32, vp, vp, vp, i32, f32, vp, vp, vp,
                                     ctypes.c_size_t, vp]
     lib.gmm_assign_topk.restype = ctypes.c_int
+    lib.gmm_estep_accumulate_streamed.argtypes = [vp, i64, i32, i32, vp, vp, vp, vp, vp, vp,
+                                                  vp, i64, vp, vp, ctypes.c_size_t, vp, vp]
+    lib.gmm_estep_accumulate_streamed.restype = ctypes.c_int
     lib.gmm_estep_accumulate_iso.argtypes = lib.gmm_estep_accumulate.argtypes
     lib.gmm_estep_accumulate_iso.restype = ctypes.c_int
     lib.gmm_mstep_iso.argtypes = lib.gmm_mstep.argtypes
@@ -187,6 +191,31 @@ def gmm_assign_topk(x, weights, means, variances, m, tau, idx, resp, ws, stream=
         _ptr(_dev(resp, torch.float32, "resp", n * m)), _ptr(ws),
         ws.numel() if ws is not None else 0, _stream(stream))
     _check("gmm_assign_topk", rc)
+
+
+def gmm_estep_accumulate_streamed(x_host, weights, means, variances, nk, s, q, loglik,
+                                  chunk_rows, staging, ws, stream=None, copy_stream=None):
+    """E-step of data held in page-locked host memory (x_host: a pinned fp32 CPU tensor
+    [n, d]), uploaded chunk_rows rows at a time into `staging` (fp32 CUDA tensor of at least
+    2 * min(chunk_rows, n) * d elements) on copy_stream while the previous chunk's E-step
+    runs on `stream`; adds into nk, s, q, loglik as gmm_estep_accumulate does."""
+    import torch
+    if not (isinstance(x_host, torch.Tensor) and not x_host.is_cuda and x_host.is_pinned()
+            and x_host.dtype == torch.float32 and x_host.is_contiguous() and x_host.dim() == 2):
+        raise TypeError("x_host must be a contiguous pinned fp32 CPU tensor [n, d]")
+    n, d = x_host.shape
+    k = weights.shape[0]
+    rows = min(int(chunk_rows), n) if chunk_rows >= 1 else 0
+    rc = load_library().gmm_estep_accumulate_streamed(
+        ctypes.c_void_p(x_host.data_ptr()), n, d, k,
+        _ptr(_dev(weights, torch.float32, "weights", k)),
+        _ptr(_dev(means, torch.float32, "means", k * d)),
+        _ptr(_dev(variances, torch.float32, "vars", k * d)),
+        _ptr(_dev(nk, torch.float64, "nk", k)), _ptr(_dev(s, torch.float64, "s", k * d)),
+        _ptr(_dev(q, torch.float64, "q", k * d)), _ptr(_dev(loglik, torch.float64, "loglik", 1)),
+        int(chunk_rows), _ptr(_dev(staging, torch.float32, "staging", 2 * rows * d)), _ptr(ws),
+        ws.numel() if ws is not None else 0, _stream(stream), _stream(copy_stream))
+    _check("gmm_estep_accumulate_streamed", rc)
 
 
 def gmm_estep_accumulate_iso(x, weights, means, variances, nk, s, q, loglik, ws, stream=None):

@@ -3016,6 +3016,24 @@ int check_shape(int64_t n, int32_t d, int32_t k) {
   return GMM_OK;
 }
 
+// Events of the streamed E-step, created once: start (the compute stream's work
+// before the call), and per staging buffer b: up[b] (its chunk uploaded) and
+// done[b] (the E-step that read it finished).
+struct StreamEvents {
+  bool made = false;
+  hipEvent_t start, up[2], done[2];
+};
+StreamEvents g_sev;
+
+bool stream_events() {
+  if (g_sev.made) return true;
+  hipEvent_t* all[5] = {&g_sev.start, &g_sev.up[0], &g_sev.up[1], &g_sev.done[0], &g_sev.done[1]};
+  for (hipEvent_t* e : all)
+    if (hipEventCreateWithFlags(e, hipEventDisableTiming) != hipSuccess) return false;
+  g_sev.made = true;
+  return true;
+}
+
 }  // namespace
 
 extern "C" {
@@ -3184,6 +3202,49 @@ int gmm_fit_iso(const float* x, int64_t n, int32_t d, int32_t k, int32_t n_iters
                        fq, (double)n, d, k, (double)var_floor, weights, means, vars);
     rc = launch_status();
     if (rc != GMM_OK) return rc;
+  }
+  return GMM_OK;
+}
+
+int gmm_estep_accumulate_streamed(const float* x_host, int64_t n, int32_t d, int32_t k,
+                                  const float* weights, const float* means, const float* vars,
+                                  double* nk, double* s, double* q, double* loglik,
+                                  int64_t chunk_rows, float* staging, void* ws, size_t ws_bytes,
+                                  hipStream_t stream, hipStream_t copy_stream) {
+  int rc = check_shape(n, d, k);
+  if (rc != GMM_OK) return rc;
+  if (!x_host || !weights || !means || !vars || !nk || !s || !q || !loglik || !staging ||
+      chunk_rows < 1)
+    return GMM_ERR_INVALID_ARG;
+  const int64_t rows = chunk_rows < n ? chunk_rows : n;
+  Layout L;
+  if (!make_layout(rows, d, k, 0, &L)) return GMM_ERR_UNSUPPORTED;
+  rc = check_ws(L, ws, ws_bytes);
+  if (rc != GMM_OK) return rc;
+  if (!stream_events()) return GMM_ERR_DEVICE;
+  // the staging buffers may still be read by work enqueued on `stream` before
+  // this call: the first uploads wait for it
+  if (hipEventRecord(g_sev.start, stream) != hipSuccess ||
+      hipStreamWaitEvent(copy_stream, g_sev.start, 0) != hipSuccess)
+    return GMM_ERR_DEVICE;
+  const int64_t nchunks = (n + rows - 1) / rows;
+  for (int64_t c = 0; c < nchunks; ++c) {
+    const int b = (int)(c & 1);
+    const int64_t r0 = c * rows, nr = n - r0 < rows ? n - r0 : rows;
+    float* buf = staging + (size_t)b * rows * d;
+    // upload chunk c once the E-step of chunk c - 2 has read this buffer
+    if (c >= 2 && hipStreamWaitEvent(copy_stream, g_sev.done[b], 0) != hipSuccess)
+      return GMM_ERR_DEVICE;
+    if (hipMemcpyAsync(buf, x_host + r0 * d, (size_t)nr * d * sizeof(float),
+                       hipMemcpyHostToDevice, copy_stream) != hipSuccess ||
+        hipEventRecord(g_sev.up[b], copy_stream) != hipSuccess ||
+        hipStreamWaitEvent(stream, g_sev.up[b], 0) != hipSuccess)
+      return GMM_ERR_DEVICE;
+    Layout Lc;
+    if (!make_layout(nr, d, k, 0, &Lc)) return GMM_ERR_UNSUPPORTED;
+    rc = estep_dispatch(Lc, buf, weights, means, vars, nk, s, q, loglik, 1, ws, stream);
+    if (rc != GMM_OK) return rc;
+    if (hipEventRecord(g_sev.done[b], stream) != hipSuccess) return GMM_ERR_DEVICE;
   }
   return GMM_OK;
 }

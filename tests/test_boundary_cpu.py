@@ -106,6 +106,22 @@ def test_isotropic_host_validation():
     assert lib.gmm_mstep_iso(p, p, p, 10.0, 1025, 4, 1e-6, p, p, p, None) == gmm.GMM_ERR_UNSUPPORTED
 
 
+def test_streamed_host_validation():
+    lib = gmm.load_library()
+    p, ws = _fake(), _fake(0x200000)
+    small = gmm.workspace_bytes(500, 8, 4)
+    call = lambda xh, chunk, stg, w, nb: lib.gmm_estep_accumulate_streamed(
+        xh, 1000, 8, 4, p, p, p, p, p, p, p, chunk, stg, w, nb, None, None)
+    assert call(None, 500, p, ws, small) == gmm.GMM_ERR_INVALID_ARG
+    assert call(p, 0, p, ws, small) == gmm.GMM_ERR_INVALID_ARG
+    assert call(p, 500, None, ws, small) == gmm.GMM_ERR_INVALID_ARG
+    # the workspace is sized for one chunk of min(chunk_rows, n) rows
+    assert call(p, 500, p, ws, small - 1) == gmm.GMM_ERR_WORKSPACE
+    assert call(p, 5000, p, ws, small) == gmm.GMM_ERR_WORKSPACE
+    assert lib.gmm_estep_accumulate_streamed(p, 1000, 1025, 4, p, p, p, p, p, p, p, 500, p, ws,
+                                             small, None, None) == gmm.GMM_ERR_UNSUPPORTED
+
+
 def test_assign_host_validation():
     lib = gmm.load_library()
     p, ws = _fake(), _fake(0x200000)
