@@ -52,6 +52,8 @@ def _load():
         lib.oracle_assign_topk.argtypes = [vp, i64, i32, i32, vp, vp, vp, i32, f64, vp, vp, i32,
                                            vp, vp, i32]
         lib.oracle_assign_topk.restype = ctypes.c_int
+        lib.oracle_kmeanspp.argtypes = [vp, i64, i32, i32, vp, vp, vp]
+        lib.oracle_kmeanspp.restype = None
         lib.oracle_iso_estep.argtypes = [vp, i64, i32, i32, vp, vp, vp, vp, vp, vp, vp, i32]
         lib.oracle_iso_estep.restype = None
         lib.oracle_iso_iterate.argtypes = [vp, i64, i32, i32, vp, vp, vp, f64, vp, vp, vp, vp,
@@ -219,4 +221,18 @@ def iso_fit(x, weights, means, variances, n_iters, var_floor=DEFAULT_VAR_FLOOR, 
     if keep_thetas:
         out["thetas"] = thetas
     return out
+
+
+# ---------------------------------------------------------------- k-means++ seeding
+def kmeanspp(x, k, u):
+    """k-means++ seeding with the given uniforms u[k] in [0, 1) (see oracle.c for the orders
+    that fix every decision).  Returns (rows int64 [k], centres fp32 [k, d])."""
+    x = _f32(x)
+    n, d = x.shape
+    u = np.ascontiguousarray(u, dtype=np.float64)
+    assert u.shape == (k,) and np.all((u >= 0.0) & (u < 1.0))
+    idx = np.zeros(k, dtype=np.int64)
+    cen = np.zeros((k, d), dtype=np.float32)
+    _load().oracle_kmeanspp(_p(x), n, d, k, _p(u), _p(idx), _p(cen))
+    return idx, cen
 

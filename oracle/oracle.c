@@ -505,3 +505,102 @@ void oracle_iso_iterate(const float* x, int64_t n, int32_t d, int32_t k, const f
   free(v);
   iso_free(&p);
 }
+
+/* ------------------------------------------------------------------ */
+/*
+ * k-means++ seeding (Arthur and Vassilvitskii, SODA 2007; the paper's
+ * initialisation options): the first centre is row floor(u_0 N); centre t is
+ * drawn with probability proportional to D(x)^2, the squared distance of a
+ * row to its nearest chosen centre, by inversion of u_t against the running
+ * sum of D^2.  The uniforms u are inputs.
+ *
+ * Orders (part of the definition, so that a parallel implementation can
+ * reproduce every decision exactly): D^2 of a row is summed in fp64 over the
+ * dimensions in order with fused multiply-adds, fma(t, t, acc), t = x - c;
+ * the rows are taken in blocks of KPP_BLOCK = 4096 rows, each block in 256
+ * runs of 16 consecutive rows; a run's sum adds its rows in order, a block's
+ * sum adds its runs in order, the total adds the blocks in order.  Centre t
+ * is the first row whose running sum, accumulated in that same order (blocks,
+ * then runs, then rows), exceeds u_t times the total.  When the total is 0
+ * (every row sits on a chosen centre) centre t is row floor(u_t N).
+ */
+#define KPP_BLOCK 4096
+#define KPP_RUN 16
+
+static double kpp_dist(const float* x, const float* c, int32_t d) {
+  double acc = 0.0;
+  for (int32_t j = 0; j < d; ++j) {
+    const double t = (double)x[j] - (double)c[j];
+    acc = fma(t, t, acc);
+  }
+  return acc;
+}
+
+static int64_t kpp_first(double u, int64_t n) {
+  int64_t i = (int64_t)(u * (double)n);
+  return i < 0 ? 0 : (i >= n ? n - 1 : i);
+}
+
+/* idx[k]: the chosen rows; centers[k*d] (may be NULL): their coordinates. */
+void oracle_kmeanspp(const float* x, int64_t n, int32_t d, int32_t k, const double* u,
+                     int64_t* idx, float* centers) {
+  double* dist = (double*)malloc(sizeof(double) * (size_t)n);
+  const int64_t nblk = (n + KPP_BLOCK - 1) / KPP_BLOCK;
+  double* bsum = (double*)malloc(sizeof(double) * (size_t)nblk);
+  for (int64_t i = 0; i < n; ++i) dist[i] = INFINITY;
+  for (int32_t t = 0; t < k; ++t) {
+    int64_t pick;
+    if (t == 0) {
+      pick = kpp_first(u[0], n);
+    } else {
+      double total = 0.0;
+      for (int64_t b = 0; b < nblk; ++b) {
+        double s = 0.0;
+        for (int64_t r0 = b * KPP_BLOCK; r0 < (b + 1) * KPP_BLOCK && r0 < n; r0 += KPP_RUN) {
+          double rs = 0.0;
+          for (int64_t i = r0; i < r0 + KPP_RUN && i < n; ++i) rs += dist[i];
+          s += rs;
+        }
+        bsum[b] = s;
+        total += s;
+      }
+      if (!(total > 0.0)) {
+        pick = kpp_first(u[t], n);
+      } else {
+        /* the running sum reaches total (same additions in the same order) and
+           u_t < 1, so the block, the run and the row below always exist */
+        const double target = u[t] * total;
+        double run = 0.0;
+        int64_t b = 0;
+        while (!(run + bsum[b] > target)) run += bsum[b++];
+        double bs = 0.0;
+        pick = -1;
+        const int64_t bend = (b + 1) * KPP_BLOCK < n ? (b + 1) * KPP_BLOCK : n;
+        for (int64_t r0 = b * KPP_BLOCK; pick < 0 && r0 < bend; r0 += KPP_RUN) {
+          const int64_t r1 = r0 + KPP_RUN < n ? r0 + KPP_RUN : n;
+          double rs = 0.0;
+          for (int64_t i = r0; i < r1; ++i) rs += dist[i];
+          if (!(run + (bs + rs) > target)) {
+            bs += rs;
+            continue;
+          }
+          double ps = 0.0;
+          for (int64_t i = r0; i < r1; ++i) {
+            ps += dist[i];
+            if (run + (bs + ps) > target) { pick = i; break; }
+          }
+        }
+        if (pick < 0) pick = kpp_first(u[t], n);   /* not reached for finite data */
+      }
+    }
+    idx[t] = pick;
+    const float* c = x + pick * (int64_t)d;
+    if (centers) memcpy(centers + (int64_t)t * d, c, sizeof(float) * (size_t)d);
+    for (int64_t i = 0; i < n; ++i) {
+      const double dd = kpp_dist(x + i * (int64_t)d, c, d);
+      if (dd < dist[i]) dist[i] = dd;
+    }
+  }
+  free(dist);
+  free(bsum);
+}
