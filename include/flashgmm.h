@@ -150,6 +150,26 @@ int gmm_estep_accumulate_streamed(const float* x_host, int64_t n, int32_t d, int
                                   hipStream_t stream, hipStream_t copy_stream);
 
 /*
+ * k-means++ seeding (the paper's initialisation, Sec. 4.1 and App. B; Arthur
+ * and Vassilvitskii 2007): D^2 sampling of k rows of x with the caller's
+ * uniforms u[k] (fp64, device, 0 <= u < 1).  Centre 0 is row floor(u_0 n);
+ * centre t is the first row whose running sum of D^2 (squared distance to the
+ * nearest centre chosen so far) exceeds u_t times the total, the sums taken
+ * in a fixed order: D^2 of a row as fp64 fused multiply-adds over the
+ * dimensions in order; blocks of 4096 rows, each 256 runs of 16 consecutive
+ * rows; runs add their rows, blocks their runs, the total its blocks, and
+ * the search walks blocks, runs and rows in order.  Every choice is thus a
+ * pure function of (x, u).  When the total is 0 (every row on a centre),
+ * centre t is row floor(u_t n).  idx[k] (int64, device) receives the rows,
+ * centers[k*d] (fp32, device) their coordinates.  ws: device workspace of
+ * gmm_kmeanspp_workspace_bytes(n) bytes, 256-byte aligned.  k rounds of two
+ * kernels on `stream`; the same status codes as the calls above.
+ */
+size_t gmm_kmeanspp_workspace_bytes(int64_t n);
+int gmm_kmeanspp(const float* x, int64_t n, int32_t d, int32_t k, const double* u, int64_t* idx,
+                 float* centers, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
  * The paper's own model (Sec. 2, Eqs. Nk, muk, sig): isotropic components
  * N(mu_k, var_k I) with ONE variance per component, vars[k] (fp32, device).
  * The same conventions as the diagonal calls above, with

@@ -26,7 +26,8 @@ GMM_MAX_M = 8
 
 #: every symbol the C ABI exports
 EXPORTS = ("gmm_status_string", "gmm_workspace_bytes", "gmm_estep_accumulate", "gmm_mstep",
-           "gmm_fit", "gmm_assign_topk", "gmm_estep_accumulate_streamed",
+           "gmm_fit", "gmm_assign_topk", "gmm_kmeanspp_workspace_bytes", "gmm_kmeanspp",
+           "gmm_estep_accumulate_streamed",
            "gmm_estep_accumulate_iso", "gmm_mstep_iso", "gmm_fit_iso", "gmm_timing_enable",
            "gmm_timing_read")
 
@@ -68,6 +69,10 @@ def load_library():
     lib.gmm_assign_topk.argtypes = [vp, i64, i32, i32, vp, vp, vp, i32, f32, vp, vp, vp,
                                     ctypes.c_size_t, vp]
     lib.gmm_assign_topk.restype = ctypes.c_int
+    lib.gmm_kmeanspp_workspace_bytes.argtypes = [i64]
+    lib.gmm_kmeanspp_workspace_bytes.restype = ctypes.c_size_t
+    lib.gmm_kmeanspp.argtypes = [vp, i64, i32, i32, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.gmm_kmeanspp.restype = ctypes.c_int
     lib.gmm_estep_accumulate_streamed.argtypes = [vp, i64, i32, i32, vp, vp, vp, vp, vp, vp,
                                                   vp, i64, vp, vp, ctypes.c_size_t, vp, vp]
     lib.gmm_estep_accumulate_streamed.restype = ctypes.c_int
@@ -191,6 +196,24 @@ def gmm_assign_topk(x, weights, means, variances, m, tau, idx, resp, ws, stream=
         _ptr(_dev(resp, torch.float32, "resp", n * m)), _ptr(ws),
         ws.numel() if ws is not None else 0, _stream(stream))
     _check("gmm_assign_topk", rc)
+
+
+def gmm_kmeanspp(x, u, idx, centers, ws=None, stream=None):
+    """k-means++ seeding of k = u.numel() rows of x with the uniforms u (fp64 CUDA tensor,
+    0 <= u < 1): chosen rows into idx (int64 [k]), their coordinates into centers (fp32
+    [k, d]).  ws: a uint8 CUDA workspace (allocated here when None)."""
+    import torch
+    _dev(x, torch.float32, "x")
+    n, d = x.shape
+    k = u.numel()
+    nb = load_library().gmm_kmeanspp_workspace_bytes(n)
+    if ws is None:
+        ws = torch.empty(nb, dtype=torch.uint8, device=x.device)
+    rc = load_library().gmm_kmeanspp(
+        _ptr(x), n, d, k, _ptr(_dev(u, torch.float64, "u", k)),
+        _ptr(_dev(idx, torch.int64, "idx", k)), _ptr(_dev(centers, torch.float32, "centers", k * d)),
+        _ptr(ws), ws.numel(), _stream(stream))
+    _check("gmm_kmeanspp", rc)
 
 
 def gmm_estep_accumulate_streamed(x_host, weights, means, variances, nk, s, q, loglik,

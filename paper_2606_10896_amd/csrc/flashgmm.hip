@@ -2695,6 +2695,125 @@ __global__ __launch_bounds__(256) void k_mstep_iso(const double* __restrict__ nk
   w[c] = (float)(nn / n_total);
 }
 
+// ---------------------------------------------------------------- k-means++ seeding
+// D^2 sampling (Arthur and Vassilvitskii 2007) with the caller's uniforms:
+// centre 0 is row floor(u_0 n); centre t is the first row whose running sum
+// of D^2 (squared distance to the nearest chosen centre) exceeds u_t times
+// the total.  Every sum has a fixed order, so each choice is a pure function
+// of the data and u: D^2 of a row is fma(t, t, acc) over the dimensions in
+// order (fp64, t = x - c); a block of kKppBlock rows is 256 runs of 16
+// consecutive rows; a run adds its rows in order, a block its runs, the total
+// its blocks, and the search walks blocks, runs and rows in that order.
+constexpr int kKppBlock = 4096;
+constexpr int kKppRun = 16;
+
+__device__ __forceinline__ int64_t kpp_first(double u, int64_t n) {
+  int64_t i = (int64_t)(u * (double)n);
+  return i < 0 ? 0 : (i >= n ? n - 1 : i);
+}
+
+// One workgroup per block: folds centre idx[t-1] into D^2 (first: D^2 is
+// that centre's distance) and writes the block's sum.  Thread j owns run j.
+__global__ __launch_bounds__(256) void k_kpp_update(const float* __restrict__ x, int64_t n, int d,
+                                                    const int64_t* __restrict__ idx, int t,
+                                                    int first, double* __restrict__ dist,
+                                                    double* __restrict__ bsum) {
+  __shared__ double rsum[256];
+  const int64_t b = blockIdx.x;
+  const int j = threadIdx.x;
+  const float* c = x + idx[t - 1] * (int64_t)d;
+  const int64_t r0 = b * kKppBlock + (int64_t)kKppRun * j;
+  double rs = 0.0;
+  for (int64_t i = r0; i < r0 + kKppRun && i < n; ++i) {
+    const float* xr = x + i * (int64_t)d;
+    double acc = 0.0;
+    for (int e = 0; e < d; ++e) {
+      const double u = (double)xr[e] - (double)c[e];
+      acc = fma(u, u, acc);
+    }
+    double v = dist[i];
+    if (first || acc < v) v = acc;
+    dist[i] = v;
+    rs += v;
+  }
+  rsum[j] = rs;
+  __syncthreads();
+  if (j == 0) {
+    double s = 0.0;
+    for (int q = 0; q < 256; ++q) s += rsum[q];
+    bsum[b] = s;
+  }
+}
+
+// One workgroup: centre t (t = 0: floor(u_0 n)) into idx[t] and its row into centres.
+__global__ __launch_bounds__(256) void k_kpp_select(const float* __restrict__ x, int64_t n, int d,
+                                                    const double* __restrict__ uu, int t,
+                                                    const double* __restrict__ dist,
+                                                    const double* __restrict__ bsum,
+                                                    int64_t nblk, int64_t* __restrict__ idx,
+                                                    float* __restrict__ centres) {
+  __shared__ double rsum[256];
+  __shared__ double sh[2];      // run (sum of the blocks before), target
+  __shared__ int64_t sb[2];     // block, pick
+  const int j = threadIdx.x;
+  if (j == 0) {
+    int64_t pick = -1, blk = -1;
+    const double u = uu[t];
+    if (t > 0) {
+      double total = 0.0;
+      for (int64_t b = 0; b < nblk; ++b) total += bsum[b];
+      if (total > 0.0) {
+        const double target = u * total;
+        double run = 0.0;
+        int64_t b = 0;
+        while (b + 1 < nblk && !(run + bsum[b] > target)) run += bsum[b++];
+        blk = b;
+        sh[0] = run;
+        sh[1] = target;
+      }
+    }
+    if (blk < 0) pick = kpp_first(u, n);
+    sb[0] = blk;
+    sb[1] = pick;
+  }
+  __syncthreads();
+  const int64_t blk = sb[0];
+  if (blk >= 0) {
+    // run sums of the block, as k_kpp_update formed them
+    const int64_t r0 = blk * kKppBlock + (int64_t)kKppRun * j;
+    double rs = 0.0;
+    for (int64_t i = r0; i < r0 + kKppRun && i < n; ++i) rs += dist[i];
+    rsum[j] = rs;
+    __syncthreads();
+    if (j == 0) {
+      const double run = sh[0], target = sh[1];
+      double bs = 0.0;
+      int64_t pick = -1;
+      for (int q = 0; q < 256 && pick < 0; ++q) {
+        const int64_t q0 = blk * kKppBlock + (int64_t)kKppRun * q;
+        if (q0 >= n) break;
+        if (!(run + (bs + rsum[q]) > target)) {
+          bs += rsum[q];
+          continue;
+        }
+        double ps = 0.0;
+        for (int64_t i = q0; i < q0 + kKppRun && i < n; ++i) {
+          ps += dist[i];
+          if (run + (bs + ps) > target) {
+            pick = i;
+            break;
+          }
+        }
+      }
+      sb[1] = pick >= 0 ? pick : kpp_first(uu[t], n);   // not reached for finite data
+    }
+  }
+  __syncthreads();
+  const int64_t pick = sb[1];
+  if (j == 0) idx[t] = pick;
+  for (int e = j; e < d; e += 256) centres[(int64_t)t * d + e] = x[pick * (int64_t)d + e];
+}
+
 __global__ __launch_bounds__(256) void k_zero(double* __restrict__ p, int64_t cnt) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t < cnt) p[t] = 0.0;
@@ -3247,6 +3366,34 @@ int gmm_estep_accumulate_streamed(const float* x_host, int64_t n, int32_t d, int
     if (hipEventRecord(g_sev.done[b], stream) != hipSuccess) return GMM_ERR_DEVICE;
   }
   return GMM_OK;
+}
+
+size_t gmm_kmeanspp_workspace_bytes(int64_t n) {
+  if (n < 1) return 0;
+  const int64_t nblk = cdiv(n, kKppBlock);
+  return align256((size_t)n * sizeof(double)) + align256((size_t)nblk * sizeof(double));
+}
+
+int gmm_kmeanspp(const float* x, int64_t n, int32_t d, int32_t k, const double* u, int64_t* idx,
+                 float* centers, void* ws, size_t ws_bytes, hipStream_t stream) {
+  int rc = check_shape(n, d, k);
+  if (rc != GMM_OK) return rc;
+  if (!x || !u || !idx || !centers) return GMM_ERR_INVALID_ARG;
+  if (ws == nullptr || (reinterpret_cast<uintptr_t>(ws) & 255) != 0 ||
+      ws_bytes < gmm_kmeanspp_workspace_bytes(n))
+    return GMM_ERR_WORKSPACE;
+  const int64_t nblk = cdiv(n, kKppBlock);
+  double* dist = static_cast<double*>(ws);
+  double* bsum = at<double>(ws, align256((size_t)n * sizeof(double)));
+  hipLaunchKernelGGL(k_kpp_select, dim3(1), dim3(256), 0, stream, x, n, d, u, 0, dist, bsum,
+                     nblk, idx, centers);
+  for (int t = 1; t < k; ++t) {
+    hipLaunchKernelGGL(k_kpp_update, dim3((unsigned)nblk), dim3(256), 0, stream, x, n, d, idx, t,
+                       t == 1 ? 1 : 0, dist, bsum);
+    hipLaunchKernelGGL(k_kpp_select, dim3(1), dim3(256), 0, stream, x, n, d, u, t, dist, bsum,
+                       nblk, idx, centers);
+  }
+  return launch_status();
 }
 
 int gmm_assign_topk(const float* x, int64_t n, int32_t d, int32_t k, const float* weights,

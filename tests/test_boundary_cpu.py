@@ -122,6 +122,19 @@ def test_streamed_host_validation():
                                              small, None, None) == gmm.GMM_ERR_UNSUPPORTED
 
 
+def test_kmeanspp_host_validation():
+    lib = gmm.load_library()
+    p, ws = _fake(), _fake(0x200000)
+    nb = lib.gmm_kmeanspp_workspace_bytes(10000)
+    assert nb >= 8 * 10000 and nb % 256 == 0 and lib.gmm_kmeanspp_workspace_bytes(0) == 0
+    assert lib.gmm_kmeanspp(None, 10000, 8, 4, p, p, p, ws, nb, None) == gmm.GMM_ERR_INVALID_ARG
+    assert lib.gmm_kmeanspp(p, 10000, 8, 4, None, p, p, ws, nb, None) == gmm.GMM_ERR_INVALID_ARG
+    assert lib.gmm_kmeanspp(p, 0, 8, 4, p, p, p, ws, nb, None) == gmm.GMM_ERR_INVALID_ARG
+    assert lib.gmm_kmeanspp(p, 10000, 1025, 4, p, p, p, ws, nb, None) == gmm.GMM_ERR_UNSUPPORTED
+    assert lib.gmm_kmeanspp(p, 10000, 8, 4, p, p, p, ws, nb - 1, None) == gmm.GMM_ERR_WORKSPACE
+    assert lib.gmm_kmeanspp(p, 10000, 8, 4, p, p, p, _fake(0x200008), nb, None) == gmm.GMM_ERR_WORKSPACE
+
+
 def test_assign_host_validation():
     lib = gmm.load_library()
     p, ws = _fake(), _fake(0x200000)
