@@ -213,6 +213,9 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="large")
+    ap.add_argument("--kmeanspp", action="store_true",
+                    help="time only the k-means++ seeding of the workload's K centres (one JSON "
+                         "line, not the EM metric)")
     ap.add_argument("--rows", type=int, default=0,
                     help="take only the first ROWS rows of the workload (0 = all of them)")
     ap.add_argument("--stream-chunk", type=int, default=0,
@@ -257,6 +260,27 @@ def main():
     dev = torch.device("cuda:0")
     log(f"workload {w.name}: N={w.n} D={w.d} K={w.k}")
     x, mix, colsum, colsq = load_data(w, dev)
+    if args.kmeanspp:
+        u = torch.from_numpy(np.random.default_rng(w.init_seed).random(w.k)).to(dev)
+        idx = torch.empty(w.k, dtype=torch.int64, device=dev)
+        cen = torch.empty(w.k, w.d, dtype=torch.float32, device=dev)
+        kws = torch.empty(gmm.load_library().gmm_kmeanspp_workspace_bytes(w.n), dtype=torch.uint8,
+                          device=dev)
+        gmm.gmm_kmeanspp(x, u, idx, cen, kws)   # warm-up
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        gmm.gmm_kmeanspp(x, u, idx, cen, kws)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        print(json.dumps({"metric": "k-means++ seeding time", "value": round(ms, 3), "unit": "ms",
+                          "higher_is_better": False, "n_gpus": 1, "data": "synthetic",
+                          "config": {"workload": w.name, "n": w.n, "d": w.d, "k": w.k},
+                          "ms_per_centre": round(ms / w.k, 4),
+                          "x_gbs": round(4.0 * w.n * w.d * (w.k - 1) / (ms * 1e-3) / 1e9, 1)}),
+              flush=True)
+        return
     th0 = gmm_synth.random_point_init(w, mix, colsum, colsq)
     iso = args.covariance == "iso"
     if iso:   # isotropic start: the mean over the dimensions of the init variances

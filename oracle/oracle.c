@@ -515,8 +515,10 @@ void oracle_iso_iterate(const float* x, int64_t n, int32_t d, int32_t k, const f
  * sum of D^2.  The uniforms u are inputs.
  *
  * Orders (part of the definition, so that a parallel implementation can
- * reproduce every decision exactly): D^2 of a row is summed in fp64 over the
- * dimensions in order with fused multiply-adds, fma(t, t, acc), t = x - c;
+ * reproduce every decision exactly): D^2 of a row is 16 partial sums in fp64,
+ * partial l adding the dimensions l, l + 16, l + 32, ... in order with fused
+ * multiply-adds fma(t, t, acc), t = x - c, then combined by four pairwise
+ * levels p_l <- p_l + p_(l xor o) for o = 8, 4, 2, 1 (every p_l ends equal);
  * the rows are taken in blocks of KPP_BLOCK = 4096 rows, each block in 256
  * runs of 16 consecutive rows; a run's sum adds its rows in order, a block's
  * sum adds its runs in order, the total adds the blocks in order.  Centre t
@@ -528,12 +530,20 @@ void oracle_iso_iterate(const float* x, int64_t n, int32_t d, int32_t k, const f
 #define KPP_RUN 16
 
 static double kpp_dist(const float* x, const float* c, int32_t d) {
-  double acc = 0.0;
-  for (int32_t j = 0; j < d; ++j) {
-    const double t = (double)x[j] - (double)c[j];
-    acc = fma(t, t, acc);
+  double p[16], q[16];
+  for (int l = 0; l < 16; ++l) {
+    double acc = 0.0;
+    for (int32_t j = l; j < d; j += 16) {
+      const double t = (double)x[j] - (double)c[j];
+      acc = fma(t, t, acc);
+    }
+    p[l] = acc;
   }
-  return acc;
+  for (int o = 8; o >= 1; o >>= 1) {
+    for (int l = 0; l < 16; ++l) q[l] = p[l] + p[l ^ o];
+    for (int l = 0; l < 16; ++l) p[l] = q[l];
+  }
+  return p[0];
 }
 
 static int64_t kpp_first(double u, int64_t n) {

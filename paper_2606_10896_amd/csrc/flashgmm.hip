@@ -2700,10 +2700,12 @@ __global__ __launch_bounds__(256) void k_mstep_iso(const double* __restrict__ nk
 // centre 0 is row floor(u_0 n); centre t is the first row whose running sum
 // of D^2 (squared distance to the nearest chosen centre) exceeds u_t times
 // the total.  Every sum has a fixed order, so each choice is a pure function
-// of the data and u: D^2 of a row is fma(t, t, acc) over the dimensions in
-// order (fp64, t = x - c); a block of kKppBlock rows is 256 runs of 16
-// consecutive rows; a run adds its rows in order, a block its runs, the total
-// its blocks, and the search walks blocks, runs and rows in that order.
+// of the data and u: D^2 of a row is 16 fp64 partial sums (partial l takes
+// dimensions l, l + 16, ... in order, fma(t, t, acc), t = x - c) combined
+// pairwise by xor 8, 4, 2, 1 (16 lanes per row, coalesced loads); a block of
+// kKppBlock rows is 256 runs of 16 consecutive rows; a run adds its rows in
+// order, a block its runs, the total its blocks, and the search walks
+// blocks, runs and rows in that order.
 constexpr int kKppBlock = 4096;
 constexpr int kKppRun = 16;
 
@@ -2713,35 +2715,55 @@ __device__ __forceinline__ int64_t kpp_first(double u, int64_t n) {
 }
 
 // One workgroup per block: folds centre idx[t-1] into D^2 (first: D^2 is
-// that centre's distance) and writes the block's sum.  Thread j owns run j.
-__global__ __launch_bounds__(256) void k_kpp_update(const float* __restrict__ x, int64_t n, int d,
+// that centre's distance) and writes the block's sum.  Wave w of the 16 takes
+// runs w, w + 16, ...; a run's 16 rows go 4 at a time, lane group g (16
+// lanes) forming the D^2 of row 4 s + g, and lane 0 adds the rows in order.
+__global__ __launch_bounds__(1024) void k_kpp_update(const float* __restrict__ x, int64_t n, int d,
                                                     const int64_t* __restrict__ idx, int t,
                                                     int first, double* __restrict__ dist,
                                                     double* __restrict__ bsum) {
   __shared__ double rsum[256];
+  __shared__ float cs[GMM_MAX_D];
   const int64_t b = blockIdx.x;
-  const int j = threadIdx.x;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, g = lane >> 4, l16 = lane & 15;
   const float* c = x + idx[t - 1] * (int64_t)d;
-  const int64_t r0 = b * kKppBlock + (int64_t)kKppRun * j;
-  double rs = 0.0;
-  for (int64_t i = r0; i < r0 + kKppRun && i < n; ++i) {
-    const float* xr = x + i * (int64_t)d;
-    double acc = 0.0;
-    for (int e = 0; e < d; ++e) {
-      const double u = (double)xr[e] - (double)c[e];
-      acc = fma(u, u, acc);
-    }
-    double v = dist[i];
-    if (first || acc < v) v = acc;
-    dist[i] = v;
-    rs += v;
-  }
-  rsum[j] = rs;
+  for (int e = tid; e < d; e += 1024) cs[e] = c[e];
   __syncthreads();
-  if (j == 0) {
-    double s = 0.0;
-    for (int q = 0; q < 256; ++q) s += rsum[q];
-    bsum[b] = s;
+  for (int q = wave; q < 256; q += 16) {
+    const int64_t r0 = b * kKppBlock + (int64_t)kKppRun * q;
+    double rs = 0.0;
+    for (int sub = 0; sub < kKppRun / 4; ++sub) {
+      const int64_t i = r0 + 4 * sub + g;
+      double v = 0.0;
+      if (i < n) {
+        const float* xr = x + i * (int64_t)d;
+        double acc = 0.0;
+        for (int e = l16; e < d; e += 16) {
+          const double u = (double)xr[e] - (double)cs[e];
+          acc = fma(u, u, acc);
+        }
+        acc += __shfl_xor(acc, 8);
+        acc += __shfl_xor(acc, 4);
+        acc += __shfl_xor(acc, 2);
+        acc += __shfl_xor(acc, 1);
+        v = acc;
+        if (l16 == 0) {
+          const double old = dist[i];
+          if (!first && !(acc < old)) v = old;
+          dist[i] = v;
+        }
+      }
+      // the run's rows in order (rows past n add 0)
+#pragma unroll
+      for (int gg = 0; gg < 4; ++gg) rs += __shfl(v, 16 * gg);
+    }
+    if (lane == 0) rsum[q] = rs;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    double sb = 0.0;
+    for (int q = 0; q < 256; ++q) sb += rsum[q];
+    bsum[b] = sb;
   }
 }
 
@@ -3388,7 +3410,7 @@ int gmm_kmeanspp(const float* x, int64_t n, int32_t d, int32_t k, const double* 
   hipLaunchKernelGGL(k_kpp_select, dim3(1), dim3(256), 0, stream, x, n, d, u, 0, dist, bsum,
                      nblk, idx, centers);
   for (int t = 1; t < k; ++t) {
-    hipLaunchKernelGGL(k_kpp_update, dim3((unsigned)nblk), dim3(256), 0, stream, x, n, d, idx, t,
+    hipLaunchKernelGGL(k_kpp_update, dim3((unsigned)nblk), dim3(1024), 0, stream, x, n, d, idx, t,
                        t == 1 ? 1 : 0, dist, bsum);
     hipLaunchKernelGGL(k_kpp_select, dim3(1), dim3(256), 0, stream, x, n, d, u, t, dist, bsum,
                        nblk, idx, centers);
