@@ -52,6 +52,8 @@ def _load():
         lib.oracle_assign_topk.argtypes = [vp, i64, i32, i32, vp, vp, vp, i32, f64, vp, vp, i32,
                                            vp, vp, i32]
         lib.oracle_assign_topk.restype = ctypes.c_int
+        lib.oracle_kmeans.argtypes = [vp, i64, i32, i32, i32, f64, vp, vp, vp, vp, vp, vp, vp]
+        lib.oracle_kmeans.restype = None
         lib.oracle_kmeanspp.argtypes = [vp, i64, i32, i32, vp, vp, vp]
         lib.oracle_kmeanspp.restype = None
         lib.oracle_iso_estep.argtypes = [vp, i64, i32, i32, vp, vp, vp, vp, vp, vp, vp, i32]
@@ -235,4 +237,21 @@ def kmeanspp(x, k, u):
     cen = np.zeros((k, d), dtype=np.float32)
     _load().oracle_kmeanspp(_p(x), n, d, k, _p(u), _p(idx), _p(cen))
     return idx, cen
+
+
+def kmeans(x, centres, variances, n_iters, var_floor=DEFAULT_VAR_FLOOR):
+    """k-means warm start: n_iters Lloyd iterations from `centres` (centres rounded to fp32
+    after every move, as the GPU stores them), then the hard-assignment mixture (see oracle.c).
+    Returns dict(centres (fp64, after n_iters moves), weights, means, vars (fp64), assign)."""
+    x = _f32(x)
+    n, d = x.shape
+    c0 = _f32(centres)
+    k = c0.shape[0]
+    var = _f32(variances)
+    assert c0.shape == (k, d) and var.shape == (k, d)
+    cen, w1, mu1, var1 = np.zeros((k, d)), np.zeros(k), np.zeros((k, d)), np.zeros((k, d))
+    asg = np.zeros(n, dtype=np.int32)
+    _load().oracle_kmeans(_p(x), n, d, k, int(n_iters), float(var_floor), _p(c0), _p(var),
+                          _p(cen), _p(w1), _p(mu1), _p(var1), _p(asg))
+    return dict(centres=cen, weights=w1, means=mu1, vars=var1, assign=asg)
 

@@ -614,3 +614,84 @@ void oracle_kmeanspp(const float* x, int64_t n, int32_t d, int32_t k, const doub
   free(dist);
   free(bsum);
 }
+
+/* ------------------------------------------------------------------ */
+/*
+ * k-means warm start (the paper's initialisation, App. B: Lloyd iterations
+ * from given centres, then EM from the result).  An iteration assigns every
+ * row to its nearest centre (squared Euclidean distance summed in fp64 over
+ * the dimensions in order; ties to the lower index) and moves every centre
+ * to the mean of its rows (a centre without rows stays).  After n_iters
+ * iterations a last assignment gives the mixture the EM starts from, the
+ * M-step of Eqs. Nk / muk / sig with hard responsibilities:
+ *   pi_k = N_k / N, mu_k = mean of its rows, var_kd = max(var_floor,
+ *   sum over its rows (x_d - mu_kd)^2 / N_k) (about the new mean), and for a
+ *   centre without rows: pi_k = 0, mu_k its centre, var_k as given.
+ * centres [k*d] (in: initial, out: after n_iters iterations), var [k*d] (in:
+ * for centres without rows), outputs w_out, mu_out, var_out (fp64) and the
+ * final assignment (int32).
+ */
+static int32_t km_nearest(const float* x, const double* c, int32_t d, int32_t k) {
+  int32_t best = 0;
+  double bd = INFINITY;
+  for (int32_t q = 0; q < k; ++q) {
+    double s = 0.0;
+    for (int32_t j = 0; j < d; ++j) {
+      const double t = (double)x[j] - c[(int64_t)q * d + j];
+      s += t * t;
+    }
+    if (s < bd) { bd = s; best = q; }
+  }
+  return best;
+}
+
+void oracle_kmeans(const float* x, int64_t n, int32_t d, int32_t k, int32_t n_iters,
+                   double var_floor, const float* centres_in, const float* var_in, double* centres,
+                   double* w_out, double* mu_out, double* var_out, int32_t* assign) {
+  const size_t kd = (size_t)k * d;
+  double* sum = (double*)malloc(sizeof(double) * kd);
+  double* cnt = (double*)malloc(sizeof(double) * (size_t)k);
+  for (size_t e = 0; e < kd; ++e) centres[e] = (double)centres_in[e];
+  for (int32_t it = 0; it <= n_iters; ++it) {
+    for (int64_t i = 0; i < n; ++i) assign[i] = km_nearest(x + i * (int64_t)d, centres, d, k);
+    memset(sum, 0, sizeof(double) * kd);
+    memset(cnt, 0, sizeof(double) * (size_t)k);
+    for (int64_t i = 0; i < n; ++i) {
+      const int32_t q = assign[i];
+      cnt[q] += 1.0;
+      for (int32_t j = 0; j < d; ++j) sum[(int64_t)q * d + j] += (double)x[i * (int64_t)d + j];
+    }
+    if (it == n_iters) break;    /* the last assignment feeds the mixture below */
+    for (int32_t q = 0; q < k; ++q)
+      if (cnt[q] > 0.0)
+        for (int32_t j = 0; j < d; ++j)
+          centres[(int64_t)q * d + j] = (double)(float)(sum[(int64_t)q * d + j] / cnt[q]);
+  }
+  for (int32_t q = 0; q < k; ++q) {
+    w_out[q] = cnt[q] / (double)n;
+    for (int32_t j = 0; j < d; ++j) {
+      const size_t e = (size_t)q * d + j;
+      mu_out[e] = cnt[q] > 0.0 ? sum[e] / cnt[q] : centres[e];
+      var_out[e] = 0.0;
+    }
+  }
+  for (int64_t i = 0; i < n; ++i) {
+    const int32_t q = assign[i];
+    for (int32_t j = 0; j < d; ++j) {
+      const double t = (double)x[i * (int64_t)d + j] - mu_out[(int64_t)q * d + j];
+      var_out[(int64_t)q * d + j] += t * t;
+    }
+  }
+  for (int32_t q = 0; q < k; ++q)
+    for (int32_t j = 0; j < d; ++j) {
+      const size_t e = (size_t)q * d + j;
+      if (cnt[q] > 0.0) {
+        const double v = var_out[e] / cnt[q];
+        var_out[e] = v > var_floor ? v : var_floor;
+      } else {
+        var_out[e] = (double)var_in[e];
+      }
+    }
+  free(sum);
+  free(cnt);
+}
