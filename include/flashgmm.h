@@ -166,6 +166,25 @@ int gmm_estep_accumulate_streamed(const float* x_host, int64_t n, int32_t d, int
  * kernels on `stream`; the same status codes as the calls above.
  */
 size_t gmm_kmeanspp_workspace_bytes(int64_t n);
+
+/*
+ * k-means warm start (the paper's initialisation, App. B: k-means iterations,
+ * then EM from the result).  means [k*d] holds the initial centres; n_iters
+ * Lloyd iterations each assign every row to its nearest centre (squared
+ * Euclidean distance, evaluated exactly in the ranking as gmm_assign_topk
+ * does with equal weights and unit variances; ties to the lower index) and
+ * move every centre to the mean of its rows (fp64 sums, stored fp32; a centre
+ * without rows stays).  A last assignment then gives the mixture EM starts
+ * from, by the M-step of gmm_mstep with hard responsibilities:
+ *   weights[k] = rows / n, means = the rows' means, vars[k*d] = max(var_floor,
+ *   the rows' per-dimension variance); a centre without rows keeps its centre,
+ *   its vars as given on entry and weight 0.
+ * assign[n] (int32, device) receives the last assignment.  ws: the workspace
+ * of gmm_workspace_bytes(n, d, k, 1).  Same status codes as gmm_fit.
+ */
+int gmm_kmeans(const float* x, int64_t n, int32_t d, int32_t k, int32_t n_iters, float var_floor,
+               float* weights, float* means, float* vars, int32_t* assign, void* ws,
+               size_t ws_bytes, hipStream_t stream);
 int gmm_kmeanspp(const float* x, int64_t n, int32_t d, int32_t k, const double* u, int64_t* idx,
                  float* centers, void* ws, size_t ws_bytes, hipStream_t stream);
 

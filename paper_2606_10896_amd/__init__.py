@@ -27,6 +27,7 @@ GMM_MAX_M = 8
 #: every symbol the C ABI exports
 EXPORTS = ("gmm_status_string", "gmm_workspace_bytes", "gmm_estep_accumulate", "gmm_mstep",
            "gmm_fit", "gmm_assign_topk", "gmm_kmeanspp_workspace_bytes", "gmm_kmeanspp",
+           "gmm_kmeans",
            "gmm_estep_accumulate_streamed",
            "gmm_estep_accumulate_iso", "gmm_mstep_iso", "gmm_fit_iso", "gmm_timing_enable",
            "gmm_timing_read")
@@ -69,6 +70,9 @@ def load_library():
     lib.gmm_assign_topk.argtypes = [vp, i64, i32, i32, vp, vp, vp, i32, f32, vp, vp, vp,
                                     ctypes.c_size_t, vp]
     lib.gmm_assign_topk.restype = ctypes.c_int
+    lib.gmm_kmeans.argtypes = [vp, i64, i32, i32, i32, f32, vp, vp, vp, vp, vp, ctypes.c_size_t,
+                               vp]
+    lib.gmm_kmeans.restype = ctypes.c_int
     lib.gmm_kmeanspp_workspace_bytes.argtypes = [i64]
     lib.gmm_kmeanspp_workspace_bytes.restype = ctypes.c_size_t
     lib.gmm_kmeanspp.argtypes = [vp, i64, i32, i32, vp, vp, vp, vp, ctypes.c_size_t, vp]
@@ -196,6 +200,24 @@ def gmm_assign_topk(x, weights, means, variances, m, tau, idx, resp, ws, stream=
         _ptr(_dev(resp, torch.float32, "resp", n * m)), _ptr(ws),
         ws.numel() if ws is not None else 0, _stream(stream))
     _check("gmm_assign_topk", rc)
+
+
+def gmm_kmeans(x, weights, means, variances, n_iters, assign, ws, var_floor=1e-6, stream=None):
+    """k-means warm start: n_iters Lloyd iterations on the centres in `means`, then the
+    hard-assignment mixture into weights / means / variances (fp32 CUDA tensors, updated in
+    place) and the last assignment into assign (int32 [n]).  ws: gmm.workspace(n, d, k, 1)."""
+    import torch
+    _dev(x, torch.float32, "x")
+    n, d = x.shape
+    k = weights.shape[0]
+    rc = load_library().gmm_kmeans(
+        _ptr(x), n, d, k, int(n_iters), float(var_floor),
+        _ptr(_dev(weights, torch.float32, "weights", k)),
+        _ptr(_dev(means, torch.float32, "means", k * d)),
+        _ptr(_dev(variances, torch.float32, "vars", k * d)),
+        _ptr(_dev(assign, torch.int32, "assign", n)), _ptr(ws),
+        ws.numel() if ws is not None else 0, _stream(stream))
+    _check("gmm_kmeans", rc)
 
 
 def gmm_kmeanspp(x, u, idx, centers, ws=None, stream=None):

@@ -2836,6 +2836,60 @@ __global__ __launch_bounds__(256) void k_kpp_select(const float* __restrict__ x,
   for (int e = j; e < d; e += 256) centres[(int64_t)t * d + e] = x[pick * (int64_t)d + e];
 }
 
+// ---------------------------------------------------------------- k-means warm start
+// Lloyd iterations with the pieces of the EM path: the nearest centre is the
+// top-1 of the exact assignment with equal weights and unit variances (its
+// ranking is the fp64 direct form, ties to the lower index), a row and its
+// centre form one stored pair with r = 1, and the exact-pair pipeline sums
+// them per centre in a fixed order (N_k, sum x, sum x^2, fp64).
+__global__ __launch_bounds__(256) void k_km_fill(float* __restrict__ w, int k, float wv,
+                                                 float* __restrict__ ones, int64_t kd) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t < k) w[t] = wv;
+  if (t < kd) ones[t] = 1.0f;
+}
+
+__global__ __launch_bounds__(256) void k_km_pairs(const int* __restrict__ assign, int64_t n,
+                                                  unsigned short* __restrict__ cslot,
+                                                  float* __restrict__ cr) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int a = assign[i];
+  *reinterpret_cast<ushort4*>(cslot + i * kT) =
+      make_ushort4(a >= 0 ? (unsigned short)a : kNoSlot, kNoSlot, kNoSlot, kNoSlot);
+  *reinterpret_cast<float4*>(cr + i * kT) = make_float4(a >= 0 ? 1.0f : 0.0f, 0.f, 0.f, 0.f);
+}
+
+// nk, s, q of every centre (slot = centre) from the exact-pair partials, parts in order.
+__global__ __launch_bounds__(256) void k_km_reduce(const double* __restrict__ part_s,
+                                                   int nparts, int sbk, int k, int d, int D64,
+                                                   double* __restrict__ nk,
+                                                   double* __restrict__ s,
+                                                   double* __restrict__ q) {
+  const int64_t width = 1 + 2 * (int64_t)d;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (int64_t)k * width) return;
+  const int slot = (int)(t / width), c = (int)(t % width);
+  const int64_t stride = 1 + 2 * (int64_t)D64;
+  const int64_t off = c == 0 ? 0 : (c <= d ? 1 + (c - 1) : 1 + D64 + (c - 1 - d));
+  const double* ps = part_s + ((size_t)(slot / sbk) * nparts * sbk + (slot % sbk)) * stride + off;
+  double acc = 0.0;
+  for (int ch = 0; ch < nparts; ++ch) acc += ps[(size_t)ch * sbk * stride];
+  if (c == 0) nk[slot] = acc;
+  else if (c <= d) s[(int64_t)slot * d + (c - 1)] = acc;
+  else q[(int64_t)slot * d + (c - 1 - d)] = acc;
+}
+
+// centre = mean of its rows (fp64, stored fp32); a centre without rows stays.
+__global__ __launch_bounds__(256) void k_km_move(const double* __restrict__ nk,
+                                                 const double* __restrict__ s, int d, int k,
+                                                 float* __restrict__ centres) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (int64_t)k * d) return;
+  const double nn = nk[t / d];
+  if (nn > 0.0) centres[t] = (float)(s[t] / nn);
+}
+
 __global__ __launch_bounds__(256) void k_zero(double* __restrict__ p, int64_t cnt) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t < cnt) p[t] = 0.0;
@@ -3133,6 +3187,53 @@ int assign_impl(const Layout& L, const float* x, const float* w, const float* mu
 #define GMM_FOR_EACH_D64(X) \
   X(64) X(128) X(192) X(256) X(384) X(512) X(640) X(768) X(896) X(1024)
 
+// n_iters Lloyd iterations on `means` (the centres), a last assignment, and
+// the hard-assignment mixture by the M-step (k_mstep with r in {0, 1}).
+template <int D64>
+int kmeans_impl(const Layout& L, const float* x, int n_iters, float var_floor, float* weights,
+                float* means, float* vars, int* assign, void* ws, hipStream_t st) {
+  const int64_t n = L.n;
+  const int d = L.d, k = L.k;
+  const int64_t kd = (int64_t)k * d;
+  float* weq = at<float>(ws, L.off_iso_q);       // k floats: equal weights
+  float* ones = at<float>(ws, L.off_iso_var);    // k*d unit variances
+  unsigned short* cslot = at<unsigned short>(ws, L.off_cslot);
+  float* cr = at<float>(ws, L.off_cr);
+  double* fnk = at<double>(ws, L.off_fit_nk);
+  double* fs = at<double>(ws, L.off_fit_s);
+  double* fq = at<double>(ws, L.off_fit_q);
+  double* part_s = at<double>(ws, L.off_part_s);
+  int* scnt = at<int>(ws, L.off_scnt);
+  int64_t* soff = at<int64_t>(ws, L.off_soff);
+  SPair* slist = at<SPair>(ws, L.off_slist);
+  hipLaunchKernelGGL(k_km_fill, dim3((unsigned)cdiv(kd > k ? kd : k, 256)), dim3(256), 0, st, weq,
+                     k, 1.0f / (float)k, ones, kd);
+  for (int it = 0; it <= n_iters; ++it) {
+    // nearest centre; the top-1 responsibility goes to the cr region, which the
+    // pairs overwrite below
+    int rc = assign_impl<D64>(L, x, weq, means, ones, 1, 0.0f, assign, cr, ws, st);
+    if (rc != GMM_OK) return rc;
+    hipLaunchKernelGGL(k_km_pairs, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, st, assign, n,
+                       cslot, cr);
+    const size_t lds = (size_t)L.nb * sizeof(int);
+    hipLaunchKernelGGL(k_sparse_count, dim3((unsigned)L.nunit), dim3(64), lds, st, cslot, n,
+                       L.upts, L.nb, L.lsbk, L.nunit, scnt);
+    hipLaunchKernelGGL(k_sparse_scan, dim3(1), dim3(1024), 0, st, scnt, L.nb * L.nunit, soff);
+    hipLaunchKernelGGL(k_sparse_scatter, dim3((unsigned)L.nunit), dim3(64), lds, st, cslot, cr,
+                       n, L.upts, L.nb, L.lsbk, L.nunit, soff, slist);
+    hipLaunchKernelGGL(k_stats_sparse<D64>, dim3((unsigned)(L.nb * L.nparts)), dim3(256), 0, st,
+                       x, n, d, slist, soff, L.nunit, L.nparts, part_s);
+    hipLaunchKernelGGL(k_km_reduce, dim3((unsigned)cdiv((int64_t)k * (1 + 2 * (int64_t)d), 256)),
+                       dim3(256), 0, st, part_s, L.nparts, L.sbk, k, d, D64, fnk, fs, fq);
+    if (it < n_iters)
+      hipLaunchKernelGGL(k_km_move, dim3((unsigned)cdiv(kd, 256)), dim3(256), 0, st, fnk, fs, d,
+                         k, means);
+  }
+  hipLaunchKernelGGL(k_mstep, dim3((unsigned)cdiv(kd, 256)), dim3(256), 0, st, fnk, fs, fq,
+                     (double)n, d, k, (double)var_floor, weights, means, vars);
+  return launch_status();
+}
+
 int estep_dispatch(const Layout& L, const float* x, const float* w, const float* mu,
                    const float* var, double* nk, double* s, double* q, double* loglik,
                    int ll_accumulate, void* ws, hipStream_t st) {
@@ -3388,6 +3489,26 @@ int gmm_estep_accumulate_streamed(const float* x_host, int64_t n, int32_t d, int
     if (hipEventRecord(g_sev.done[b], stream) != hipSuccess) return GMM_ERR_DEVICE;
   }
   return GMM_OK;
+}
+
+int gmm_kmeans(const float* x, int64_t n, int32_t d, int32_t k, int32_t n_iters, float var_floor,
+               float* weights, float* means, float* vars, int32_t* assign, void* ws,
+               size_t ws_bytes, hipStream_t stream) {
+  int rc = check_shape(n, d, k);
+  if (rc != GMM_OK) return rc;
+  if (n_iters < 0 || !x || !weights || !means || !vars || !assign || !(var_floor >= 0.0f))
+    return GMM_ERR_INVALID_ARG;
+  Layout L;
+  if (!make_layout(n, d, k, 1, &L)) return GMM_ERR_UNSUPPORTED;
+  rc = check_ws(L, ws, ws_bytes);
+  if (rc != GMM_OK) return rc;
+  switch (L.D64) {
+#define GMM_CASE(D) \
+  case D: return kmeans_impl<D>(L, x, n_iters, var_floor, weights, means, vars, assign, ws, stream);
+    GMM_FOR_EACH_D64(GMM_CASE)
+#undef GMM_CASE
+    default: return GMM_ERR_UNSUPPORTED;
+  }
 }
 
 size_t gmm_kmeanspp_workspace_bytes(int64_t n) {

@@ -135,6 +135,17 @@ def test_kmeanspp_host_validation():
     assert lib.gmm_kmeanspp(p, 10000, 8, 4, p, p, p, _fake(0x200008), nb, None) == gmm.GMM_ERR_WORKSPACE
 
 
+def test_kmeans_host_validation():
+    lib = gmm.load_library()
+    p, ws = _fake(), _fake(0x200000)
+    nb = gmm.workspace_bytes(1000, 8, 4, 1)
+    assert lib.gmm_kmeans(p, 1000, 8, 4, -1, 1e-6, p, p, p, p, ws, nb, None) == gmm.GMM_ERR_INVALID_ARG
+    assert lib.gmm_kmeans(p, 1000, 8, 4, 3, -1.0, p, p, p, p, ws, nb, None) == gmm.GMM_ERR_INVALID_ARG
+    assert lib.gmm_kmeans(p, 1000, 8, 4, 3, 1e-6, p, p, p, None, ws, nb, None) == gmm.GMM_ERR_INVALID_ARG
+    assert lib.gmm_kmeans(p, 1000, 1025, 4, 3, 1e-6, p, p, p, p, ws, nb, None) == gmm.GMM_ERR_UNSUPPORTED
+    assert lib.gmm_kmeans(p, 1000, 8, 4, 3, 1e-6, p, p, p, p, ws, nb - 1, None) == gmm.GMM_ERR_WORKSPACE
+
+
 def test_assign_host_validation():
     lib = gmm.load_library()
     p, ws = _fake(), _fake(0x200000)
