@@ -213,6 +213,9 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="large")
+    ap.add_argument("--kmeans", type=int, default=0, metavar="ITERS",
+                    help="time only the k-means warm start (ITERS Lloyd iterations from the "
+                         "random-point centres, then the hard mixture; one JSON line)")
     ap.add_argument("--kmeanspp", action="store_true",
                     help="time only the k-means++ seeding of the workload's K centres (one JSON "
                          "line, not the EM metric)")
@@ -282,6 +285,24 @@ def main():
               flush=True)
         return
     th0 = gmm_synth.random_point_init(w, mix, colsum, colsq)
+    if args.kmeans > 0:
+        wt, mu, var = (torch.from_numpy(a).to(dev) for a in th0)
+        asg = torch.empty(w.n, dtype=torch.int32, device=dev)
+        kws = gmm.workspace(w.n, w.d, w.k, 1, device=dev)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        gmm.gmm_kmeans(x, wt, mu, var, args.kmeans, asg, kws)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        print(json.dumps({"metric": "k-means warm start time", "value": round(ms, 3),
+                          "unit": "ms", "higher_is_better": False, "n_gpus": 1,
+                          "data": "synthetic",
+                          "config": {"workload": w.name, "n": w.n, "d": w.d, "k": w.k,
+                                     "lloyd_iterations": args.kmeans},
+                          "ms_per_assignment": round(ms / (args.kmeans + 1), 3)}), flush=True)
+        return
     iso = args.covariance == "iso"
     if iso:   # isotropic start: the mean over the dimensions of the init variances
         th0 = (th0[0], th0[1], th0[2].astype(np.float64).mean(1).astype(np.float32))
