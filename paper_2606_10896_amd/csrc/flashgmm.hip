@@ -775,7 +775,7 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
     const float* __restrict__ dmu, const double* __restrict__ dh, const double* __restrict__ cdir,
     const int* __restrict__ counts, double* __restrict__ logz2,
     unsigned short* __restrict__ cslot, float* __restrict__ cr, double* __restrict__ ll_part,
-    unsigned long long* __restrict__ bmask) {
+    unsigned long long* __restrict__ bmask, unsigned char* __restrict__ iflag) {
   constexpr int P = D64 + 4, NT = logz_tiles(D64), PTS = 32 * NT;
   constexpr bool B16 = screen_b16(D64);
   constexpr int RPV = D64 / 2 + 1;
@@ -1250,6 +1250,14 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
         for (int j = 0; j < kT; ++j) {
           cslot[nn * kT + j] = tsl[j] >= 0 ? (unsigned short)tsl[j] : kNoSlot;
           cr[nn * kT + j] = tsl[j] >= 0 ? exp2_fast(tl[j] - lzr) : 0.0f;
+        }
+        // routed components: the ill sums above are -inf for every component more
+        // than 2^-60 below the point's largest well lane state, so a finite
+        // maximum marks the points k_stats_ill has to take
+        {
+          double mi_all = -INFINITY;
+          for (int w2 = 0; w2 < 4; ++w2) mi_all = fmax(mi_all, stim[w2][p]);
+          iflag[nn] = mi_all > -INFINITY ? 1 : 0;
         }
         if (bmask != nullptr) {
           // 64-component blocks the dense statistics pass takes for this point
@@ -2124,12 +2132,16 @@ __global__ __launch_bounds__(256) void k_stats_ill(
     const float* __restrict__ x, int64_t n, int d, int vec4, const int* __restrict__ ill_idx,
     const float* __restrict__ dmu, const double* __restrict__ dh,
     const double* __restrict__ cdir, const int* __restrict__ counts,
-    const double* __restrict__ logz2, double* __restrict__ part) {
+    const double* __restrict__ logz2, const unsigned char* __restrict__ iflag,
+    double* __restrict__ part) {
   constexpr int P = D64 + 4, NJ = D64 / 64, STRIDE = 1 + 2 * D64;
   constexpr int PT = ill_pt(D64), CW = ill_cw(D64), ICB = 4 * CW;
+  constexpr int WIN = 16 * 256;                 // points scanned per queue window
   __shared__ __align__(16) float xs[PT * P];
   __shared__ float rs[ICB * PT];
   __shared__ double lzs[PT];
+  __shared__ unsigned qpt[WIN + PT];            // queued points (offsets from the chunk start)
+  __shared__ int qsum[4];
   const int n_ill = counts[1];
   const int n_ikb = (n_ill + ICB - 1) / ICB;
   if (n_ikb == 0) return;
@@ -2147,10 +2159,71 @@ __global__ __launch_bounds__(256) void k_stats_ill(
 #pragma unroll
     for (int j = 0; j < NJ; ++j) S[c][j] = Q[c][j] = 0.0;
   }
-  for (int64_t it = p0; it < p1; it += PT) {
-    __syncthreads();
-    load_tile<D64>(x, p1, d, it, PT, xs, vec4 != 0);
-    if (tid < PT) lzs[tid] = (it + tid < p1) ? logz2[it + tid] : INFINITY;
+  // Only the points whose flag says a routed component holds more than 2^-60
+  // of them (every point when iflag is null) are taken: windows of WIN points
+  // are scanned, flagged points queued in order, and tiles of PT queued points
+  // gathered (the queue's rest moves to its front).
+  int qn = 0;
+  for (int64_t wb0 = p0; wb0 < p1; wb0 += WIN) {
+    const int64_t we = wb0 + WIN < p1 ? wb0 + WIN : p1;
+    {
+      const int64_t a = wb0 + 16 * tid;
+      unsigned sel = 0u;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int64_t pt = a + e;
+        if (pt < we && (iflag == nullptr || iflag[pt] != 0)) sel |= 1u << e;
+      }
+      const int cnt = __popc(sel);
+      int inc = cnt;
+      for (int o = 1; o < 64; o <<= 1) {
+        const int t2 = __shfl_up(inc, o);
+        if (lane >= o) inc += t2;
+      }
+      if (lane == 63) qsum[wave] = inc;
+      __syncthreads();
+      int pos = qn + inc - cnt, all = 0;
+#pragma unroll
+      for (int w2 = 0; w2 < 4; ++w2) {
+        if (w2 < wave) pos += qsum[w2];
+        all += qsum[w2];
+      }
+      while (sel) {
+        const int e = __ffs(sel) - 1;
+        sel &= sel - 1;
+        qpt[pos++] = (unsigned)(a + e - p0);
+      }
+      qn += all;
+      __syncthreads();                          // queue complete, qsum free
+    }
+    const int nt = we >= p1 ? (qn + PT - 1) / PT : qn / PT;
+  for (int ti = 0; ti < nt; ++ti) {
+    __syncthreads();                            // the previous tile's reads are done
+    {
+      // gathered tile: queue entries PT ti .. PT ti + PT - 1 (rows past qn are zero)
+      constexpr int Q4 = D64 / 4;
+      for (int idx = tid; idx < PT * Q4; idx += 256) {
+        const int r = idx / Q4, c = (idx % Q4) * 4;
+        const int e = PT * ti + r;
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (e < qn && c < d) {
+          const float* xr = x + (p0 + qpt[e]) * d;
+          if (vec4) {
+            v = *reinterpret_cast<const float4*>(xr + c);
+          } else {
+            v.x = xr[c];
+            v.y = c + 1 < d ? xr[c + 1] : 0.f;
+            v.z = c + 2 < d ? xr[c + 2] : 0.f;
+            v.w = c + 3 < d ? xr[c + 3] : 0.f;
+          }
+        }
+        *reinterpret_cast<float4*>(xs + r * P + c) = v;
+      }
+      if (tid < PT) {
+        const int e = PT * ti + tid;
+        lzs[tid] = e < qn ? logz2[p0 + qpt[e]] : INFINITY;
+      }
+    }
     __syncthreads();
     // nz[c]: the points of this tile with r > 0 for component c (wave-uniform)
     unsigned long long nz[CW];
@@ -2190,6 +2263,15 @@ __global__ __launch_bounds__(256) void k_stats_ill(
         }
       }
     }
+  }
+    // the entries not taken move to the front of the queue
+    const int used = PT * nt < qn ? PT * nt : qn;
+    const int left = qn - used;
+    __syncthreads();
+    const unsigned keep = tid < left ? qpt[used + tid] : 0u;
+    __syncthreads();
+    if (tid < left) qpt[tid] = keep;
+    qn = left;
   }
 #pragma unroll
   for (int c = 0; c < CW; ++c) {
@@ -2916,7 +2998,7 @@ struct Layout {
   size_t off_counts, off_cls, off_cwell, off_cdir, off_cthr, off_thr, off_well_idx, off_ill_idx,
       off_cw, off_wp, off_wq, off_wpb, off_dmu, off_dh, off_logz2, off_cslot, off_cr, off_llpart,
       off_part_w, off_part_s, off_part_i, off_scnt, off_soff, off_slist, off_bmask, off_fit_nk,
-      off_fit_s, off_fit_q, off_iso_var, off_iso_q, total;
+      off_fit_s, off_fit_q, off_iso_var, off_iso_q, off_iflag, total;
 };
 
 // Padded dimension count of the kernels: a multiple of 64 up to 256, of 128 above.
@@ -3000,6 +3082,7 @@ bool make_layout(int64_t n, int d, int k, int m, Layout* L) {
   L->off_soff = take(((size_t)L->nb * L->nunit + 1) * sizeof(int64_t));
   L->off_slist = take((size_t)n * kT * sizeof(SPair));
   L->off_bmask = take(L->bmask_on ? (size_t)n * sizeof(unsigned long long) : 16);
+  L->off_iflag = take((size_t)n);                // points with a routed component's mass
   L->off_fit_nk = take((size_t)k * sizeof(double) + sizeof(double));  // + loglik slot
   L->off_fit_s = take((size_t)k * d * sizeof(double));
   L->off_fit_q = take((size_t)k * d * sizeof(double));
@@ -3076,6 +3159,7 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
   const int vec4 = ((d & 3) == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0) ? 1 : 0;
   bf16x8* wpb = at<bf16x8>(ws, L.off_wpb);
   unsigned long long* bmask = L.bmask_on ? at<unsigned long long>(ws, L.off_bmask) : nullptr;
+  unsigned char* iflag = at<unsigned char>(ws, L.off_iflag);
 
   bool tm = phase_mark(0, st);
   hipLaunchKernelGGL(k_prep_class, dim3(k), dim3(64), 0, st, w, mu, var, d, cls, cwell, cdir,
@@ -3100,7 +3184,7 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
   tm = phase_mark(1, st) && tm;
   hipLaunchKernelGGL(k_logz<D64>, dim3((unsigned)L.n_wg_logz), dim3(256), 0, st, x, n, d, vec4,
                      wp, wpb, cw, thr, well_idx, ill_idx, dmu, dh, cdir, counts, logz2, cslot, cr,
-                     llpart, bmask);
+                     llpart, bmask, iflag);
   tm = phase_mark(2, st) && tm;
   if constexpr (D64 < 256) {
     hipLaunchKernelGGL(k_stats_well<D64>, dim3((unsigned)((kpad / kWB) * L.nch)), dim3(256), 0,
@@ -3127,7 +3211,7 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
   }
   tm = phase_mark(4, st) && tm;
   hipLaunchKernelGGL(k_stats_ill<D64>, dim3((unsigned)L.grid_i), dim3(256), 0, st, x, n, d, vec4,
-                     ill_idx, dmu, dh, cdir, counts, logz2, part_i);
+                     ill_idx, dmu, dh, cdir, counts, logz2, iflag, part_i);
   {
     const int64_t tot = 2 * (int64_t)k * (1 + 2 * (int64_t)d);
     hipLaunchKernelGGL(k_reduce_stats, dim3((unsigned)cdiv(tot, 256)), dim3(256), 0, st, part_w,

@@ -43,8 +43,9 @@ def test_workspace_is_o_n_plus_o_kd(n, d, k):
     assert nb > 0 and nb % 256 == 0
     # per point: one fp64 log-normaliser, 4 refined (16-bit slot, fp32 responsibility) pairs,
     # room for 4 bucketed pair records (16 B each), a 64-bit mask of the component blocks
-    # the dense statistics take (k <= 4096) and at most 1/4 of an fp64
-    # log-likelihood partial; plus O(k d) parameters and partial statistics: never n x k
+    # the dense statistics take (k <= 4096), a flag byte for the routed components and at most
+    # 1/4 of an fp64 log-likelihood partial; plus O(k d) parameters and partial statistics:
+    # never n x k
     assert nb >= 96 * n
     dp = (d + 63) // 64 * 64 if d <= 256 else (d + 127) // 128 * 128
     kpad = (k + 63) // 64 * 64
@@ -53,7 +54,7 @@ def test_workspace_is_o_n_plus_o_kd(n, d, k):
     sparse_part = row * max(kpad, 2048 * 32)
     ill_part = row * max(kpad + 32, 512 * 32)
     okd = well_part + sparse_part + ill_part + 40 * kpad * dp + 8 * 2 * k * d
-    per_pt = 104 if kpad <= 4096 else 96
+    per_pt = (104 if kpad <= 4096 else 96) + 1   # + a byte: the routed-component flag
     assert nb <= per_pt * n + n // 4 + okd + 64 * k + (4 << 20)
     if n >= 10 ** 6 and k >= 1024:
         # a small fraction of what an n x k fp32 responsibility array would take
