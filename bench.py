@@ -172,7 +172,7 @@ def counter_per_call(csv_path, kernels=ESTEP_KERNELS, skip=0):
     return tot / max(len(calls), 1)
 
 
-def write_traffic(workload, fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, skip=1):
+def write_traffic(workload, fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, skip=2):
     """profiles/estep_traffic_<workload>.json from two counter runs of the bench (FETCH_SIZE,
     WRITE_SIZE; the first `skip` E-steps, the warm-up, left out) and the same counters over a
     COPY_BYTES device copy, which fix the scale of each counter."""
