@@ -742,6 +742,28 @@ __device__ __forceinline__ int xpose_point(int col, int h) {
 //      pass.
 // A significant component is missed only if a larger one of the same point
 // shares its lane state; its responsibility then keeps the screening error.
+// Chunk c of point p of the split [x | x^2] tile of k_logz: v holds x of
+// dims 8c .. 8c+7; each value and its square are stored as bf16 hi + lo.
+template <int D64>
+__device__ __forceinline__ void split_store(bf16x8* xa, int p, int c, const float (&v)[8]) {
+  constexpr int NC8 = D64 / 8, RPV = D64 / 2 + 1;
+  bf16x8 hi, lo, hq, lq;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const __bf16 vh = (__bf16)v[e];
+    hi[e] = vh;
+    lo[e] = (__bf16)(v[e] - (float)vh);
+    const float q = v[e] * v[e];
+    const __bf16 qh = (__bf16)q;
+    hq[e] = qh;
+    lq[e] = (__bf16)(q - (float)qh);
+  }
+  xa[p * RPV + 2 * c] = hi;
+  xa[p * RPV + 2 * c + 1] = lo;
+  xa[p * RPV + 2 * (c + NC8)] = hq;
+  xa[p * RPV + 2 * (c + NC8) + 1] = lq;
+}
+
 // LDS state of k_logz after the screening pass, per workgroup of PTS points.
 template <int PTS>
 struct LogzPost {
@@ -816,44 +838,56 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
   if constexpr (B16) {
     // split tile: chunk c < D64/8 holds x of dims 8c .. 8c+7, chunk c + D64/8
     // x^2 of the same dims; rows >= n and dims >= d are zero
-    constexpr int NC8 = D64 / 8;
-    for (int t = tid; t < PTS * NC8; t += 256) {
-      const int p = t / NC8, c = t % NC8;
-      const int64_t row = n0 + p;
-      float v[8];
-      if (vec4 && row < n) {
+    constexpr int NC8 = D64 / 8, NIT = (PTS * NC8 + 255) / 256;
+    if (vec4) {
+      // every load of the thread issued before the first conversion (one
+      // memory round trip per workgroup); out-of-range chunks load row 0,
+      // dims 0..3 (always present: d is a multiple of 4 here) and are zeroed
+      // after the load
+      float4 ld[NIT][2];
+      bool ok[NIT][2];
+#pragma unroll
+      for (int it = 0; it < NIT; ++it) {
+        const int t = tid + 256 * it, p = t / NC8, c = t % NC8;
+        const int64_t row = n0 + p;
 #pragma unroll
         for (int hf = 0; hf < 2; ++hf) {
           const int j = 8 * c + 4 * hf;
-          float4 q = make_float4(0.f, 0.f, 0.f, 0.f);
-          if (j < d) q = *reinterpret_cast<const float4*>(x + row * d + j);
-          v[4 * hf] = q.x;
-          v[4 * hf + 1] = q.y;
-          v[4 * hf + 2] = q.z;
-          v[4 * hf + 3] = q.w;
+          ok[it][hf] = t < PTS * NC8 && row < n && j < d;
+          ld[it][hf] = *reinterpret_cast<const float4*>(x + (ok[it][hf] ? row * d + j : 0));
         }
-      } else {
+      }
+      // the loaded registers are made opaque, so that the zeroing below stays a
+      // register select and no load is moved under a branch
+#pragma unroll
+      for (int it = 0; it < NIT; ++it)
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+          asm volatile("" : "+v"(ld[it][hf].x), "+v"(ld[it][hf].y), "+v"(ld[it][hf].z),
+                       "+v"(ld[it][hf].w));
+          if (!ok[it][hf]) ld[it][hf] = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+      for (int it = 0; it < NIT; ++it) {
+        const int t = tid + 256 * it;
+        if (t < PTS * NC8) {
+          const float v[8] = {ld[it][0].x, ld[it][0].y, ld[it][0].z, ld[it][0].w,
+                              ld[it][1].x, ld[it][1].y, ld[it][1].z, ld[it][1].w};
+          split_store<D64>(xa, t / NC8, t % NC8, v);
+        }
+      }
+    } else {
+      for (int t = tid; t < PTS * NC8; t += 256) {
+        const int p = t / NC8, c = t % NC8;
+        const int64_t row = n0 + p;
+        float v[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           const int j = 8 * c + e;
           v[e] = (row < n && j < d) ? x[row * d + j] : 0.0f;
         }
+        split_store<D64>(xa, p, c, v);
       }
-      bf16x8 hi, lo, hq, lq;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const __bf16 vh = (__bf16)v[e];
-        hi[e] = vh;
-        lo[e] = (__bf16)(v[e] - (float)vh);
-        const float q = v[e] * v[e];
-        const __bf16 qh = (__bf16)q;
-        hq[e] = qh;
-        lq[e] = (__bf16)(q - (float)qh);
-      }
-      xa[p * RPV + 2 * c] = hi;
-      xa[p * RPV + 2 * c + 1] = lo;
-      xa[p * RPV + 2 * (c + NC8)] = hq;
-      xa[p * RPV + 2 * (c + NC8) + 1] = lq;
     }
   } else {
     load_tile<D64>(x, n, d, n0, PTS, xs, vec4 != 0);
@@ -1928,13 +1962,29 @@ __global__ __launch_bounds__(1024) void k_sparse_scan(const int* __restrict__ cn
   if (tid == 0) off[tot] = carry_s;
 }
 
+// Buckets up to which k_sparse_scatter keeps its unit's list positions in LDS
+// (8 bytes each); above, it reads each segment start with a scalar load.
+constexpr int kScatterCache = 4096;
+
+__host__ __device__ inline size_t scatter_lds(int nb) {
+  return (size_t)nb * (nb <= kScatterCache ? sizeof(int64_t) : sizeof(int));
+}
+
+// No memory load waits inside the per-bucket loop: on this GPU a wait for a
+// vector load also waits for every store before it, so a load there would
+// serialise the scattered stores.
 __global__ __launch_bounds__(64) void k_sparse_scatter(
     const unsigned short* __restrict__ cslot, const float* __restrict__ cr, int64_t n,
     int64_t upts, int nb, int lcb, int nunit, const int64_t* __restrict__ goff,
     SPair* __restrict__ list) {
-  extern __shared__ int pos[];               // pairs of this unit placed so far, per bucket
+  extern __shared__ int64_t cur[];           // cached: next list position per bucket
+  int* const pos = reinterpret_cast<int*>(cur);  // else: pairs placed so far per bucket
+  const bool cached = nb <= kScatterCache;
   const int u = blockIdx.x, lane = threadIdx.x;
-  for (int b = lane; b < nb; b += 64) pos[b] = 0;
+  for (int b = lane; b < nb; b += 64) {
+    if (cached) cur[b] = goff[(size_t)b * nunit + u];
+    else pos[b] = 0;
+  }
   __syncthreads();
   const int64_t p0 = (int64_t)u * upts;
   const int64_t p1 = p0 + upts < n ? p0 + upts : n;
@@ -1960,18 +2010,22 @@ __global__ __launch_bounds__(64) void k_sparse_scatter(
       unsigned long long act = __ballot(valid);
       while (act) {
         const int leader = __ffsll(act) - 1;
-        const int bl = __shfl(bk, leader);
+        const int bl = __builtin_amdgcn_readfirstlane(__shfl(bk, leader));
         const unsigned long long same = __ballot(bk == bl);
-        const int done = pos[bl];
+        const int64_t base =
+            cached ? cur[bl] : goff[(size_t)bl * nunit + u] + (int64_t)pos[bl];
         if (bk == bl) {
           SPair e;
           e.pt = p;
           e.r = rr[j];
           e.c = sl[j] & ((1 << lcb) - 1);
-          list[goff[(size_t)bl * nunit + u] + done + __popcll(same & below)] = e;
+          list[base + __popcll(same & below)] = e;
         }
         __builtin_amdgcn_wave_barrier();
-        if (lane == leader) pos[bl] = done + __popcll(same);
+        if (lane == leader) {
+          if (cached) cur[bl] = base + __popcll(same);
+          else pos[bl] += __popcll(same);
+        }
         __builtin_amdgcn_wave_barrier();
         act &= ~same;
       }
@@ -1979,12 +2033,14 @@ __global__ __launch_bounds__(64) void k_sparse_scatter(
   }
 }
 
-// Sums of one part of one bucket's list.  Batches of NB pairs: the records of
-// batch t+1 are in LDS and its rows are gathered into registers while batch t
-// is consumed from LDS.  Wave w owns the CW = C/4 slots CW w .. CW w + CW - 1
-// of the bucket and takes its pairs of a batch in order, two at a time; lane l
-// owns dimensions l, l + 64, ... and adds r x and r x^2 of them in fp64 (r x
-// is exact), and r itself (N_k, every lane the same sum; lane 0 writes it).
+// Sums of one part of one bucket's list.  Batches of NB pairs: while batch t
+// is consumed from LDS, the rows of batches t+1 and t+2 are in flight into
+// registers, and the records of batch t+4 (stored to LDS one batch later), so
+// that no memory round trip is waited for within a batch.  Wave w owns the
+// CW = C/4 slots CW w .. CW w + CW - 1 of the bucket and takes its pairs of a
+// batch in order, two at a time; lane l owns dimensions l, l + 64, ... and
+// adds r x and r x^2 of them in fp64 (r x is exact), and r itself (N_k, every
+// lane the same sum; lane 0 writes it).
 template <int D64>
 __global__ __launch_bounds__(256) void k_stats_sparse(
     const float* __restrict__ x, int64_t n, int d, const SPair* __restrict__ list,
@@ -1992,16 +2048,18 @@ __global__ __launch_bounds__(256) void k_stats_sparse(
   constexpr int C = sparse_cb(D64), CW = C / 4;
   constexpr int STRIDE = 1 + 2 * D64;
   constexpr int NB = D64 <= 64 ? 64 : 4096 / D64;
-  constexpr int GL = (NB * D64 + 255) / 256;     // gathered values per thread and batch
-  __shared__ float xb[2][NB * D64];
-  __shared__ int2 rb[3][NB];                     // (slot in bucket, r bits) per pair
-  __shared__ int64_t pb[3][NB];                  // point per pair
+  constexpr int CPR = D64 / 4;                   // float4 chunks per row
+  constexpr int GQ = (NB * CPR + 255) / 256;     // float4 gathered per thread and batch
+  __shared__ __align__(16) float xb[2][NB * D64];
+  __shared__ int2 rb[4][NB];                     // (slot in bucket, r bits) per pair
+  __shared__ int64_t pb[4][NB];                  // point per pair
   const int bucket = blockIdx.x / nparts, prt = blockIdx.x % nparts;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int64_t lo = goff[(size_t)bucket * nunit], hi = goff[(size_t)(bucket + 1) * nunit];
   const int64_t cnt = hi - lo;
   const int64_t a0 = lo + cnt * prt / nparts, a1 = lo + cnt * (prt + 1) / nparts;
   const int nbatch = (int)((a1 - a0 + NB - 1) / NB);
+  const bool vec4 = (d & 3) == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0;
   constexpr int NX = D64 / 64;                   // dimensions per lane
   double accs[CW][NX], accq[CW][NX], accn[CW];
 #pragma unroll
@@ -2010,54 +2068,77 @@ __global__ __launch_bounds__(256) void k_stats_sparse(
 #pragma unroll
     for (int u = 0; u < NX; ++u) accs[j][u] = accq[j][u] = 0.0;
   }
-  auto load_rec = [&](int t, int buf) {
+  auto batch_len = [&](int t) {
+    const int64_t left = a1 - a0 - (int64_t)t * NB;
+    return (int)(left < NB ? left : NB);
+  };
+  auto load_rec = [&](int t) {
     if (tid < NB) {
       const int64_t e = a0 + (int64_t)t * NB + tid;
       if (e < a1) {
         const SPair q = list[e];
-        rb[buf][tid] = make_int2(q.c, __float_as_int(q.r));
-        pb[buf][tid] = q.pt;
+        rb[t & 3][tid] = make_int2(q.c, __float_as_int(q.r));
+        pb[t & 3][tid] = q.pt;
       }
     }
   };
-  float gv[GL];
-  auto gather = [&](int t, int buf) {
-    const int nbt = (int)(a1 - a0 - (int64_t)t * NB < NB ? a1 - a0 - (int64_t)t * NB : NB);
+  // flat float4 index f = tid + 256 i of a batch: row f / CPR, chunk f % CPR;
+  // chunks past the batch load row 0, dims 0..3 (always present) and are
+  // zeroed afterwards
+  float4 gA[GQ], gB[GQ];
+  auto gather = [&](int t, float4 (&g)[GQ]) {
+    const int nbt = batch_len(t);
+    int64_t pt[GQ];
+    bool ok[GQ];
 #pragma unroll
-    for (int j = 0; j < GL; ++j) {
-      const int i = tid + 256 * j, e = i / D64, c = i % D64;
-      float v = 0.0f;
-      if (i < NB * D64 && e < nbt && c < d) v = x[pb[buf][e] * d + c];
-      gv[j] = v;
+    for (int i = 0; i < GQ; ++i) {
+      const int f = tid + 256 * i, e = f / CPR, c4 = 4 * (f % CPR);
+      ok[i] = f < NB * CPR && e < nbt && c4 < d;
+      pt[i] = ok[i] ? pb[t & 3][e] : 0;
     }
-  };
-  if (nbatch > 0) {
-    load_rec(0, 0);
-    if (nbatch > 1) load_rec(1, 1);
-    __syncthreads();
-    gather(0, 0);
-  }
-  for (int t = 0; t < nbatch; ++t) {
-    const int xbuf = t & 1, rcur = t % 3;
+    if (vec4) {
 #pragma unroll
-    for (int j = 0; j < GL; ++j)
-      if (tid + 256 * j < NB * D64) xb[xbuf][tid + 256 * j] = gv[j];
-    __syncthreads();            // rows of batch t, records of batches t, t+1 in LDS
-    // records of batch t+2: loaded now, stored after the consumption (their
-    // buffer was last read while consuming batch t-1)
-    SPair qn;
-    bool has_rec = false;
-    if (t + 2 < nbatch && tid < NB) {
-      const int64_t e = a0 + (int64_t)(t + 2) * NB + tid;
-      if (e < a1) {
-        qn = list[e];
-        has_rec = true;
+      for (int i = 0; i < GQ; ++i) {
+        const int c4 = 4 * ((tid + 256 * i) % CPR);
+        g[i] = *reinterpret_cast<const float4*>(x + (ok[i] ? pt[i] * d + c4 : 0));
+      }
+#pragma unroll
+      for (int i = 0; i < GQ; ++i) {
+        asm volatile("" : "+v"(g[i].x), "+v"(g[i].y), "+v"(g[i].z), "+v"(g[i].w));
+        if (!ok[i]) g[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < GQ; ++i) {
+        const int c4 = 4 * ((tid + 256 * i) % CPR);
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          v[e] = ok[i] && c4 + e < d ? x[pt[i] * d + c4 + e] : 0.0f;
+        g[i] = make_float4(v[0], v[1], v[2], v[3]);
       }
     }
-    if (t + 1 < nbatch) gather(t + 1, (t + 1) % 3);
-    const int nbt = (int)(a1 - a0 - (int64_t)t * NB < NB ? a1 - a0 - (int64_t)t * NB : NB);
+  };
+  auto consume = [&](int t, const float4 (&g)[GQ]) {
+    const int xbuf = t & 1;
+    float4* const xw = reinterpret_cast<float4*>(xb[xbuf]);
+#pragma unroll
+    for (int i = 0; i < GQ; ++i)
+      if (tid + 256 * i < NB * CPR) xw[tid + 256 * i] = g[i];
+    __syncthreads();            // rows of batch t, records of batches t .. t+3 in LDS
+    // records of batch t+4: loaded now, stored at the end of the next batch
+    SPair qn = SPair{-1, 0.0f, 0};
+    if (t + 4 < nbatch && tid < NB) {
+      const int64_t e = a0 + (int64_t)(t + 4) * NB + tid;
+      if (e < a1) qn = list[e];
+    }
+    return qn;
+  };
+  auto accumulate = [&](int t) {
+    const int xbuf = t & 1;
+    const int nbt = batch_len(t);
     int2 en = make_int2(0, 0);
-    if (lane < nbt) en = rb[rcur][lane];
+    if (lane < nbt) en = rb[t & 3][lane];
     const int cl = en.x - CW * wave;
     // slot by slot (each slot's pairs in list order), two pairs at a time
 #pragma unroll
@@ -2094,9 +2175,39 @@ __global__ __launch_bounds__(256) void k_stats_sparse(
         }
       }
     }
-    if (has_rec) {
-      rb[(t + 2) % 3][tid] = make_int2(qn.c, __float_as_int(qn.r));
-      pb[(t + 2) % 3][tid] = qn.pt;
+  };
+  // at the end of batch t: the records of batch t+3 (loaded during batch
+  // t-1) go to the buffer of batch t-1, whose rows and records every wave has
+  // finished with (the barrier of batch t)
+  auto store_rec = [&](int t, const SPair& q) {
+    if (q.pt >= 0) {
+      rb[(t + 3) & 3][tid] = make_int2(q.c, __float_as_int(q.r));
+      pb[(t + 3) & 3][tid] = q.pt;
+    }
+  };
+  SPair qA = SPair{-1, 0.0f, 0}, qB = SPair{-1, 0.0f, 0};
+  if (nbatch > 0) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+      if (t < nbatch) load_rec(t);
+    __syncthreads();
+    gather(0, gA);
+    if (nbatch > 1) gather(1, gB);
+  }
+  // two batches per trip, so that the register sets gA / gB and qA / qB are
+  // named statically
+  for (int t = 0; t < nbatch; t += 2) {
+    {
+      qA = consume(t, gA);
+      if (t + 2 < nbatch) gather(t + 2, gA);
+      accumulate(t);
+      store_rec(t, qB);
+    }
+    if (t + 1 < nbatch) {
+      qB = consume(t + 1, gB);
+      if (t + 3 < nbatch) gather(t + 3, gB);
+      accumulate(t + 1);
+      store_rec(t + 1, qA);
     }
   }
 #pragma unroll
@@ -3204,8 +3315,8 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
     hipLaunchKernelGGL(k_sparse_count, dim3((unsigned)L.nunit), dim3(64), lds, st, cslot, n,
                        L.upts, L.nb, L.lsbk, L.nunit, scnt);
     hipLaunchKernelGGL(k_sparse_scan, dim3(1), dim3(1024), 0, st, scnt, L.nb * L.nunit, soff);
-    hipLaunchKernelGGL(k_sparse_scatter, dim3((unsigned)L.nunit), dim3(64), lds, st, cslot, cr,
-                       n, L.upts, L.nb, L.lsbk, L.nunit, soff, slist);
+    hipLaunchKernelGGL(k_sparse_scatter, dim3((unsigned)L.nunit), dim3(64), scatter_lds(L.nb), st,
+                       cslot, cr, n, L.upts, L.nb, L.lsbk, L.nunit, soff, slist);
     hipLaunchKernelGGL(k_stats_sparse<D64>, dim3((unsigned)(L.nb * L.nparts)), dim3(256), 0, st,
                        x, n, d, slist, soff, L.nunit, L.nparts, part_s);
   }
@@ -3303,8 +3414,8 @@ int kmeans_impl(const Layout& L, const float* x, int n_iters, float var_floor, f
     hipLaunchKernelGGL(k_sparse_count, dim3((unsigned)L.nunit), dim3(64), lds, st, cslot, n,
                        L.upts, L.nb, L.lsbk, L.nunit, scnt);
     hipLaunchKernelGGL(k_sparse_scan, dim3(1), dim3(1024), 0, st, scnt, L.nb * L.nunit, soff);
-    hipLaunchKernelGGL(k_sparse_scatter, dim3((unsigned)L.nunit), dim3(64), lds, st, cslot, cr,
-                       n, L.upts, L.nb, L.lsbk, L.nunit, soff, slist);
+    hipLaunchKernelGGL(k_sparse_scatter, dim3((unsigned)L.nunit), dim3(64), scatter_lds(L.nb), st,
+                       cslot, cr, n, L.upts, L.nb, L.lsbk, L.nunit, soff, slist);
     hipLaunchKernelGGL(k_stats_sparse<D64>, dim3((unsigned)(L.nb * L.nparts)), dim3(256), 0, st,
                        x, n, d, slist, soff, L.nunit, L.nparts, part_s);
     hipLaunchKernelGGL(k_km_reduce, dim3((unsigned)cdiv((int64_t)k * (1 + 2 * (int64_t)d), 256)),
@@ -3342,23 +3453,26 @@ int check_shape(int64_t n, int32_t d, int32_t k) {
   return GMM_OK;
 }
 
-// Events of the streamed E-step, created once: start (the compute stream's work
-// before the call), and per staging buffer b: up[b] (its chunk uploaded) and
-// done[b] (the E-step that read it finished).
+// Events of one streamed E-step call: start (the compute stream's work before
+// the call), and per staging buffer b: up[b] (its chunk uploaded) and done[b]
+// (the E-step that read it finished).  Each call makes its own and releases
+// them once everything is enqueued (HIP frees an event only after its
+// pending records and waits), so concurrent calls never share one.
 struct StreamEvents {
-  bool made = false;
-  hipEvent_t start, up[2], done[2];
+  hipEvent_t ev[5] = {nullptr, nullptr, nullptr, nullptr, nullptr};
+  hipEvent_t& start() { return ev[0]; }
+  hipEvent_t& up(int b) { return ev[1 + b]; }
+  hipEvent_t& done(int b) { return ev[3 + b]; }
+  bool make() {
+    for (hipEvent_t& e : ev)
+      if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return false;
+    return true;
+  }
+  ~StreamEvents() {
+    for (hipEvent_t e : ev)
+      if (e) (void)hipEventDestroy(e);
+  }
 };
-StreamEvents g_sev;
-
-bool stream_events() {
-  if (g_sev.made) return true;
-  hipEvent_t* all[5] = {&g_sev.start, &g_sev.up[0], &g_sev.up[1], &g_sev.done[0], &g_sev.done[1]};
-  for (hipEvent_t* e : all)
-    if (hipEventCreateWithFlags(e, hipEventDisableTiming) != hipSuccess) return false;
-  g_sev.made = true;
-  return true;
-}
 
 }  // namespace
 
@@ -3547,11 +3661,12 @@ int gmm_estep_accumulate_streamed(const float* x_host, int64_t n, int32_t d, int
   if (!make_layout(rows, d, k, 0, &L)) return GMM_ERR_UNSUPPORTED;
   rc = check_ws(L, ws, ws_bytes);
   if (rc != GMM_OK) return rc;
-  if (!stream_events()) return GMM_ERR_DEVICE;
+  StreamEvents sev;
+  if (!sev.make()) return GMM_ERR_DEVICE;
   // the staging buffers may still be read by work enqueued on `stream` before
   // this call: the first uploads wait for it
-  if (hipEventRecord(g_sev.start, stream) != hipSuccess ||
-      hipStreamWaitEvent(copy_stream, g_sev.start, 0) != hipSuccess)
+  if (hipEventRecord(sev.start(), stream) != hipSuccess ||
+      hipStreamWaitEvent(copy_stream, sev.start(), 0) != hipSuccess)
     return GMM_ERR_DEVICE;
   const int64_t nchunks = (n + rows - 1) / rows;
   for (int64_t c = 0; c < nchunks; ++c) {
@@ -3559,18 +3674,18 @@ int gmm_estep_accumulate_streamed(const float* x_host, int64_t n, int32_t d, int
     const int64_t r0 = c * rows, nr = n - r0 < rows ? n - r0 : rows;
     float* buf = staging + (size_t)b * rows * d;
     // upload chunk c once the E-step of chunk c - 2 has read this buffer
-    if (c >= 2 && hipStreamWaitEvent(copy_stream, g_sev.done[b], 0) != hipSuccess)
+    if (c >= 2 && hipStreamWaitEvent(copy_stream, sev.done(b), 0) != hipSuccess)
       return GMM_ERR_DEVICE;
     if (hipMemcpyAsync(buf, x_host + r0 * d, (size_t)nr * d * sizeof(float),
                        hipMemcpyHostToDevice, copy_stream) != hipSuccess ||
-        hipEventRecord(g_sev.up[b], copy_stream) != hipSuccess ||
-        hipStreamWaitEvent(stream, g_sev.up[b], 0) != hipSuccess)
+        hipEventRecord(sev.up(b), copy_stream) != hipSuccess ||
+        hipStreamWaitEvent(stream, sev.up(b), 0) != hipSuccess)
       return GMM_ERR_DEVICE;
     Layout Lc;
     if (!make_layout(nr, d, k, 0, &Lc)) return GMM_ERR_UNSUPPORTED;
     rc = estep_dispatch(Lc, buf, weights, means, vars, nk, s, q, loglik, 1, ws, stream);
     if (rc != GMM_OK) return rc;
-    if (hipEventRecord(g_sev.done[b], stream) != hipSuccess) return GMM_ERR_DEVICE;
+    if (hipEventRecord(sev.done(b), stream) != hipSuccess) return GMM_ERR_DEVICE;
   }
   return GMM_OK;
 }
