@@ -284,12 +284,14 @@ __device__ __forceinline__ double ill_logit_gr(const float* __restrict__ xrow, i
   return c - acc;
 }
 
+// acc0 carries the sum of dimensions 0 .. j_start-1 (j_start a multiple of 4).
 __device__ __forceinline__ double ill_logit_bounded_gr(const float* __restrict__ xrow, int d,
                                                        int vec4, const float* __restrict__ mu,
                                                        const double* __restrict__ hh, double c,
-                                                       double bound) {
-  double acc = 0.0;
-  for (int j0 = 0; j0 < d; j0 += 16) {
+                                                       double bound, double acc0 = 0.0,
+                                                       int j_start = 0) {
+  double acc = acc0;
+  for (int j0 = j_start; j0 < d; j0 += 16) {
     const int j1 = j0 + 16 < d ? j0 + 16 : d;
     int j = j0;
     if (vec4) {
@@ -1004,20 +1006,102 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
     float si = 0.0f;
     // rows >= n (zero rows of the fp32 tile) are skipped with the split tile
     const int64_t row = n0 + lane;
-    for (int ki = wave; ki < n_ill && (!B16 || row < n); ki += 4) {
-      const int comp = ill_idx[ki];
-      const double c = cdir[comp];
-      const double bnd = c - ((double)mw - 60.0);
-      const double l =
-          B16 ? ill_logit_bounded_gr(x + row * d, d, vec4, dmu + (size_t)comp * D64,
-                                     dh + (size_t)comp * D64, c, bnd)
-              : ill_logit_bounded<D64>(xs + lane * P, dmu + (size_t)comp * D64,
-                                       dh + (size_t)comp * D64, c, bnd);
+    auto take = [&](double l) {
       if (l > mi) {
         si = __fmaf_rn(si, exp2_fast((float)(mi - l)), 1.0f);
         mi = l;
       } else if (l > -INFINITY) {
         si += exp2_fast((float)(l - mi));
+      }
+    };
+    if constexpr (B16) {
+      // The first 8 dimensions of the point's row are read once for all of the
+      // wave's ill components (lane = point, so these reads are not
+      // coalesced); the first chunk dismisses almost every component.  The
+      // operands of that chunk are fetched one component ahead.  Same sums,
+      // in the same order, as the plain bounded form; the partial sums only
+      // grow, so an earlier dismissal gives the same -inf.
+      constexpr int H = 8;
+      const bool live = row < n;
+      float xh[H];
+#pragma unroll
+      for (int q4 = 0; q4 < H / 4; ++q4) {
+        const int j = 4 * q4;
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (live && vec4) {
+          if (j < d) v = *reinterpret_cast<const float4*>(x + row * d + j);
+        } else if (live) {
+          v.x = j < d ? x[row * d + j] : 0.0f;
+          v.y = j + 1 < d ? x[row * d + j + 1] : 0.0f;
+          v.z = j + 2 < d ? x[row * d + j + 2] : 0.0f;
+          v.w = j + 3 < d ? x[row * d + j + 3] : 0.0f;
+        }
+        xh[j] = v.x;
+        xh[j + 1] = v.y;
+        xh[j + 2] = v.z;
+        xh[j + 3] = v.w;
+      }
+      float mA[H], mB[H];
+      double hA[H], hB[H];
+      double cA = 0.0, cB = 0.0;
+      int pA = 0, pB = 0;
+      auto fetch = [&](int ki, float (&m)[H], double (&hq)[H], double& c, int& cp) {
+        cp = ill_idx[ki];
+        c = cdir[cp];
+        const float4* mp = reinterpret_cast<const float4*>(dmu + (size_t)cp * D64);
+        const double2* hp = reinterpret_cast<const double2*>(dh + (size_t)cp * D64);
+#pragma unroll
+        for (int q4 = 0; q4 < H / 4; ++q4) {
+          const float4 mv = mp[q4];
+          m[4 * q4] = mv.x;
+          m[4 * q4 + 1] = mv.y;
+          m[4 * q4 + 2] = mv.z;
+          m[4 * q4 + 3] = mv.w;
+        }
+#pragma unroll
+        for (int q2 = 0; q2 < H / 2; ++q2) {
+          const double2 hv = hp[q2];
+          hq[2 * q2] = hv.x;
+          hq[2 * q2 + 1] = hv.y;
+        }
+      };
+      // component ki with the operands in (m, hq, c, cp); those of ki + 4 are
+      // fetched into the other set meanwhile (two sets, named statically, so
+      // that no wait falls between a fetch and its use)
+      auto step = [&](int ki, const float (&m)[H], const double (&hq)[H], double c, int cp) {
+        if (live) {
+          const double bnd = c - ((double)mw - 60.0);
+          double acc = 0.0;
+#pragma unroll
+          for (int j = 0; j < H; ++j) {
+            if (j < d) {
+              const double t = (double)xh[j] - (double)m[j];
+              acc = fma(t * t, hq[j], acc);
+            }
+          }
+          double l = -INFINITY;
+          if (__ballot(!(acc > bnd)) != 0ull)
+            l = ill_logit_bounded_gr(x + row * d, d, vec4, dmu + (size_t)cp * D64,
+                                     dh + (size_t)cp * D64, c, bnd, acc, H);
+          take(l);
+        }
+      };
+      if (wave < n_ill) fetch(wave, mA, hA, cA, pA);
+      for (int ki = wave; ki < n_ill; ki += 8) {
+        if (ki + 4 < n_ill) fetch(ki + 4, mB, hB, cB, pB);
+        step(ki, mA, hA, cA, pA);
+        if (ki + 4 < n_ill) {
+          if (ki + 8 < n_ill) fetch(ki + 8, mA, hA, cA, pA);
+          step(ki + 4, mB, hB, cB, pB);
+        }
+      }
+    } else {
+      for (int ki = wave; ki < n_ill; ki += 4) {
+        const int comp = ill_idx[ki];
+        const double c = cdir[comp];
+        const double bnd = c - ((double)mw - 60.0);
+        take(ill_logit_bounded<D64>(xs + lane * P, dmu + (size_t)comp * D64,
+                                    dh + (size_t)comp * D64, c, bnd));
       }
     }
     sti[wave][lane] = make_float2((float)mi, si);
