@@ -30,7 +30,7 @@ EXPORTS = ("gmm_status_string", "gmm_workspace_bytes", "gmm_estep_accumulate", "
            "gmm_kmeans",
            "gmm_estep_accumulate_streamed",
            "gmm_estep_accumulate_iso", "gmm_mstep_iso", "gmm_fit_iso", "gmm_timing_enable",
-           "gmm_timing_read")
+           "gmm_timing_read", "gmm_estep_accumulate_screened", "gmm_fit_screened")
 
 _lib = None
 
@@ -67,6 +67,10 @@ def load_library():
     lib.gmm_mstep.restype = ctypes.c_int
     lib.gmm_fit.argtypes = [vp, i64, i32, i32, i32, f32, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.gmm_fit.restype = ctypes.c_int
+    lib.gmm_estep_accumulate_screened.argtypes = lib.gmm_estep_accumulate.argtypes
+    lib.gmm_estep_accumulate_screened.restype = ctypes.c_int
+    lib.gmm_fit_screened.argtypes = lib.gmm_fit.argtypes
+    lib.gmm_fit_screened.restype = ctypes.c_int
     lib.gmm_assign_topk.argtypes = [vp, i64, i32, i32, vp, vp, vp, i32, f32, vp, vp, vp,
                                     ctypes.c_size_t, vp]
     lib.gmm_assign_topk.restype = ctypes.c_int
@@ -140,21 +144,30 @@ def workspace(n: int, d: int, k: int, m: int = 0, device="cuda"):
     return torch.empty(nb, dtype=torch.uint8, device=device)
 
 
-def gmm_estep_accumulate(x, weights, means, variances, nk, s, q, loglik, ws, stream=None):
+def gmm_estep_accumulate(x, weights, means, variances, nk, s, q, loglik, ws, stream=None,
+                         _fn="gmm_estep_accumulate"):
     """Adds the E-step statistics of x at (weights, means, variances) into fp64 nk, s, q and
     loglik (all CUDA tensors)."""
     import torch
     _dev(x, torch.float32, "x")
     n, d = x.shape
     k = weights.shape[0]
-    rc = load_library().gmm_estep_accumulate(
+    rc = getattr(load_library(), _fn)(
         _ptr(x), n, d, k, _ptr(_dev(weights, torch.float32, "weights", k)),
         _ptr(_dev(means, torch.float32, "means", k * d)),
         _ptr(_dev(variances, torch.float32, "vars", k * d)),
         _ptr(_dev(nk, torch.float64, "nk", k)), _ptr(_dev(s, torch.float64, "s", k * d)),
         _ptr(_dev(q, torch.float64, "q", k * d)), _ptr(_dev(loglik, torch.float64, "loglik", 1)),
         _ptr(ws), ws.numel() if ws is not None else 0, _stream(stream))
-    _check("gmm_estep_accumulate", rc)
+    _check(_fn, rc)
+
+
+def gmm_estep_accumulate_screened(x, weights, means, variances, nk, s, q, loglik, ws,
+                                  stream=None):
+    """gmm_estep_accumulate at the screening pass's precision (no fp64 refinement of the
+    pairs that carry a point's mass); looser tolerances, stated in the C header."""
+    gmm_estep_accumulate(x, weights, means, variances, nk, s, q, loglik, ws, stream,
+                         _fn="gmm_estep_accumulate_screened")
 
 
 def gmm_mstep(nk, s, q, n_total, weights, means, variances, var_floor=1e-6, stream=None):
@@ -170,20 +183,28 @@ def gmm_mstep(nk, s, q, n_total, weights, means, variances, var_floor=1e-6, stre
     _check("gmm_mstep", rc)
 
 
-def gmm_fit(x, weights, means, variances, n_iters, loglik_hist, ws, var_floor=1e-6, stream=None):
+def gmm_fit(x, weights, means, variances, n_iters, loglik_hist, ws, var_floor=1e-6, stream=None,
+            _fn="gmm_fit"):
     """n_iters EM iterations; parameters updated in place, loglik_hist[t] = LL(Theta_t)."""
     import torch
     _dev(x, torch.float32, "x")
     n, d = x.shape
     k = weights.shape[0]
-    rc = load_library().gmm_fit(
+    rc = getattr(load_library(), _fn)(
         _ptr(x), n, d, k, int(n_iters), float(var_floor),
         _ptr(_dev(weights, torch.float32, "weights", k)),
         _ptr(_dev(means, torch.float32, "means", k * d)),
         _ptr(_dev(variances, torch.float32, "vars", k * d)),
         _ptr(_dev(loglik_hist, torch.float64, "loglik_hist", n_iters)), _ptr(ws),
         ws.numel() if ws is not None else 0, _stream(stream))
-    _check("gmm_fit", rc)
+    _check(_fn, rc)
+
+
+def gmm_fit_screened(x, weights, means, variances, n_iters, loglik_hist, ws, var_floor=1e-6,
+                     stream=None):
+    """gmm_fit with the screened-precision E-step (gmm_estep_accumulate_screened)."""
+    gmm_fit(x, weights, means, variances, n_iters, loglik_hist, ws, var_floor, stream,
+            _fn="gmm_fit_screened")
 
 
 def gmm_assign_topk(x, weights, means, variances, m, tau, idx, resp, ws, stream=None):

@@ -790,7 +790,9 @@ struct LogzPost {
   float rtl[4][kT][PTS];
 };
 
-template <int D64>
+// REFINE = false (the screened E-step): the candidates keep their screened
+// log-densities instead of the direct-form ones; everything else is the same.
+template <int D64, bool REFINE>
 __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
     const float* __restrict__ x, int64_t n, int d, int vec4, const float4* __restrict__ wp,
     const bf16x8* __restrict__ wpb,
@@ -1135,6 +1137,7 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
   __syncthreads();
   // candidates: lane states whose maximum is within the window of the screening log2 Z
   float XT[16 * NT];                 // candidate mass per lane state, summed below
+  unsigned cbits = 0u;               // this lane's candidate lane states, bit 16 blk + v
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
     const int p = 8 * (v >> 2) + 4 * h + (v & 3);
@@ -1151,9 +1154,10 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
       // relative error bound) could exceed kFullErr of the point's total
       const float rel = mv - lzm[pp];
       const float2 tf = av >= 0 ? thr[av] : make_float2(0.0f, 0.0f);
-      const bool full = av >= 0 && (sv - 1.0f) * exp2_fast(rel) * tf.y > kFullErr;
+      const bool full = REFINE && av >= 0 && (sv - 1.0f) * exp2_fast(rel) * tf.y > kFullErr;
       const bool cand = av >= 0 && (full || rel > tf.x ||
                                     (mv >= s4m[pp] && rel > -(float)kWideWindow));
+      if (cand) cbits |= 1u << (16 * blk + v);
       XT[16 * blk + v] = cand ? (full ? sv : 1.0f) * exp2_fast(mv - stw[wave][pp].x) : 0.0f;
       const unsigned long long bal = __ballot(cand);
       const unsigned long long balf = __ballot(full);
@@ -1235,70 +1239,92 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
     for (int j = 0; j < kT; ++j) { tsl[j] = -1; tl[j] = -INFINITY; }
     for (int lo = 0; lo < total; lo += kRefCap) {
       const int hi = total < lo + kRefCap ? total : lo + kRefCap;
-      if (owner && my_base < hi && my_base + my_c > lo) {
-        int j = my_base;
-        unsigned msk = cm;
-        while (msk && j < hi) {
-          const int b = __ffs(msk) - 1;
-          msk &= msk - 1;
-          if ((fm >> b) & 1u) {
-            for (int kb = w2; kb < n_wkb && j < hi; kb += 4) {
-              const int slot = kb * kBK + b;
-              if (slot >= n_well) break;
-              if (j >= lo) rlist[j - lo] = (p << 16) | slot;
+      if constexpr (REFINE) {
+        if (owner && my_base < hi && my_base + my_c > lo) {
+          int j = my_base;
+          unsigned msk = cm;
+          while (msk && j < hi) {
+            const int b = __ffs(msk) - 1;
+            msk &= msk - 1;
+            if ((fm >> b) & 1u) {
+              for (int kb = w2; kb < n_wkb && j < hi; kb += 4) {
+                const int slot = kb * kBK + b;
+                if (slot >= n_well) break;
+                if (j >= lo) rlist[j - lo] = (p << 16) | slot;
+                ++j;
+              }
+            } else {
+              if (j >= lo) rlist[j - lo] = (p << 16) | cidx[p][w2 * 32 + b];
               ++j;
             }
-          } else {
-            if (j >= lo) rlist[j - lo] = (p << 16) | cidx[p][w2 * 32 + b];
-            ++j;
           }
         }
-      }
-      __syncthreads();
-      if (B16 && vec4) {
-        // kRefLanes lanes per entry: lane g of a group sums, in fp64, the float4
-        // chunks g, g + kRefLanes, ... of the row (coalesced over the group),
-        // and the group adds its partial sums in a fixed butterfly order
-        constexpr int G = kRefLanes, NCK = D64 / 4 / G;
-        const int g = tid & (G - 1);
-        for (int j = lo + tid / G; j < hi; j += 256 / G) {
-          const int e = rlist[j - lo], pp = e >> 16, comp = well_idx[e & 0xFFFF];
-          const float* xr = x + (n0 + pp) * d;
-          const float* mu = dmu + (size_t)comp * D64;
-          const double* hh = dh + (size_t)comp * D64;
-          double acc = 0.0;
-#pragma unroll
-          for (int t = 0; t < NCK; ++t) {
-            const int c4 = 4 * (g + G * t);
-            if (c4 < d) {
-              const float4 xv = *reinterpret_cast<const float4*>(xr + c4);
-              const float4 m = *reinterpret_cast<const float4*>(mu + c4);
-              const double2 g0 = *reinterpret_cast<const double2*>(hh + c4);
-              const double2 g1 = *reinterpret_cast<const double2*>(hh + c4 + 2);
-              double u;
-              u = (double)xv.x - (double)m.x; acc = fma(u * u, g0.x, acc);
-              u = (double)xv.y - (double)m.y; acc = fma(u * u, g0.y, acc);
-              u = (double)xv.z - (double)m.z; acc = fma(u * u, g1.x, acc);
-              u = (double)xv.w - (double)m.w; acc = fma(u * u, g1.y, acc);
+        __syncthreads();
+        if (B16 && vec4) {
+          // kRefLanes lanes per entry: lane g of a group sums, in fp64, the float4
+          // chunks g, g + kRefLanes, ... of the row (coalesced over the group),
+          // and the group adds its partial sums in a fixed butterfly order
+          constexpr int G = kRefLanes, NCK = D64 / 4 / G;
+          const int g = tid & (G - 1);
+          for (int j = lo + tid / G; j < hi; j += 256 / G) {
+            const int e = rlist[j - lo], pp = e >> 16, comp = well_idx[e & 0xFFFF];
+            const float* xr = x + (n0 + pp) * d;
+            const float* mu = dmu + (size_t)comp * D64;
+            const double* hh = dh + (size_t)comp * D64;
+            double acc = 0.0;
+  #pragma unroll
+            for (int t = 0; t < NCK; ++t) {
+              const int c4 = 4 * (g + G * t);
+              if (c4 < d) {
+                const float4 xv = *reinterpret_cast<const float4*>(xr + c4);
+                const float4 m = *reinterpret_cast<const float4*>(mu + c4);
+                const double2 g0 = *reinterpret_cast<const double2*>(hh + c4);
+                const double2 g1 = *reinterpret_cast<const double2*>(hh + c4 + 2);
+                double u;
+                u = (double)xv.x - (double)m.x; acc = fma(u * u, g0.x, acc);
+                u = (double)xv.y - (double)m.y; acc = fma(u * u, g0.y, acc);
+                u = (double)xv.z - (double)m.z; acc = fma(u * u, g1.x, acc);
+                u = (double)xv.w - (double)m.w; acc = fma(u * u, g1.y, acc);
+              }
+            }
+  #pragma unroll
+            for (int o = 1; o < G; o <<= 1) acc += __shfl_xor(acc, o);
+            if (g == 0) {
+              const double ref = lzm[pp] > -INFINITY ? (double)lzm[pp] : 0.0;
+              rres[j - lo] = (float)((cdir[comp] - acc) - ref);
             }
           }
-#pragma unroll
-          for (int o = 1; o < G; o <<= 1) acc += __shfl_xor(acc, o);
-          if (g == 0) {
+        } else {
+          for (int j = lo + tid; j < hi; j += 256) {
+            const int e = rlist[j - lo], pp = e >> 16, comp = well_idx[e & 0xFFFF];
             const double ref = lzm[pp] > -INFINITY ? (double)lzm[pp] : 0.0;
-            rres[j - lo] = (float)((cdir[comp] - acc) - ref);
+            const double l =
+                B16 ? ill_logit_gr(x + (n0 + pp) * d, d, vec4, dmu + (size_t)comp * D64,
+                                   dh + (size_t)comp * D64, cdir[comp])
+                    : ill_logit<D64>(xs + pp * P, dmu + (size_t)comp * D64,
+                                     dh + (size_t)comp * D64, cdir[comp]);
+            rres[j - lo] = (float)(l - ref);
           }
         }
       } else {
-        for (int j = lo + tid; j < hi; j += 256) {
-          const int e = rlist[j - lo], pp = e >> 16, comp = well_idx[e & 0xFFFF];
-          const double ref = lzm[pp] > -INFINITY ? (double)lzm[pp] : 0.0;
-          const double l =
-              B16 ? ill_logit_gr(x + (n0 + pp) * d, d, vec4, dmu + (size_t)comp * D64,
-                                 dh + (size_t)comp * D64, cdir[comp])
-                  : ill_logit<D64>(xs + pp * P, dmu + (size_t)comp * D64,
-                                   dh + (size_t)comp * D64, cdir[comp]);
-          rres[j - lo] = (float)(l - ref);
+        // screened E-step: every candidate lane state puts its own entry, with
+        // its screened log-density, where the owner would have listed it
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+#pragma unroll
+          for (int blk = 0; blk < NT; ++blk) {
+            const int pp = blk * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
+            if (((cbits >> (16 * blk + v)) & 1u) && n0 + pp < n) {
+              const int pos = rcnt[pp * 4 + wave] + __popc(cmask[pp][wave] & ((1u << col) - 1u));
+              if (pos >= lo && pos < hi) {
+                const float mv = blk ? m1[v] : m0[v];
+                const int av = blk ? a1[v] : a0[v];
+                const double ref = lzm[pp] > -INFINITY ? (double)lzm[pp] : 0.0;
+                rlist[pos - lo] = (pp << 16) | av;
+                rres[pos - lo] = (float)((double)mv - ref);
+              }
+            }
+          }
         }
       }
       __syncthreads();
@@ -3190,6 +3216,7 @@ struct Layout {
   int pts_logz;
   int64_t n_wg_logz;
   bool bmask_on;            // per-point dense-block masks (at most 64 blocks of 64 components)
+  bool refine = true;       // false: the screened E-step (no direct-form refinement)
   size_t off_counts, off_cls, off_cwell, off_cdir, off_cthr, off_thr, off_well_idx, off_ill_idx,
       off_cw, off_wp, off_wq, off_wpb, off_dmu, off_dh, off_logz2, off_cslot, off_cr, off_llpart,
       off_part_w, off_part_s, off_part_i, off_scnt, off_soff, off_slist, off_bmask, off_fit_nk,
@@ -3377,9 +3404,14 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
                        st, mu, var, d, k, dmu, dh);
   }
   tm = phase_mark(1, st) && tm;
-  hipLaunchKernelGGL(k_logz<D64>, dim3((unsigned)L.n_wg_logz), dim3(256), 0, st, x, n, d, vec4,
-                     wp, wpb, cw, thr, well_idx, ill_idx, dmu, dh, cdir, counts, logz2, cslot, cr,
-                     llpart, bmask, iflag);
+  if (L.refine)
+    hipLaunchKernelGGL((k_logz<D64, true>), dim3((unsigned)L.n_wg_logz), dim3(256), 0, st, x, n,
+                       d, vec4, wp, wpb, cw, thr, well_idx, ill_idx, dmu, dh, cdir, counts, logz2,
+                       cslot, cr, llpart, bmask, iflag);
+  else
+    hipLaunchKernelGGL((k_logz<D64, false>), dim3((unsigned)L.n_wg_logz), dim3(256), 0, st, x, n,
+                       d, vec4, wp, wpb, cw, thr, well_idx, ill_idx, dmu, dh, cdir, counts, logz2,
+                       cslot, cr, llpart, bmask, iflag);
   tm = phase_mark(2, st) && tm;
   if constexpr (D64 < 256) {
     hipLaunchKernelGGL(k_stats_well<D64>, dim3((unsigned)((kpad / kWB) * L.nch)), dim3(256), 0,
@@ -3598,17 +3630,34 @@ size_t gmm_workspace_bytes(int64_t n, int32_t d, int32_t k, int32_t m) {
   return L.total;
 }
 
-int gmm_estep_accumulate(const float* x, int64_t n, int32_t d, int32_t k, const float* weights,
-                         const float* means, const float* vars, double* nk, double* s, double* q,
-                         double* loglik, void* ws, size_t ws_bytes, hipStream_t stream) {
+static int estep_entry(const float* x, int64_t n, int32_t d, int32_t k, const float* weights,
+                       const float* means, const float* vars, double* nk, double* s, double* q,
+                       double* loglik, void* ws, size_t ws_bytes, hipStream_t stream,
+                       bool refine) {
   int rc = check_shape(n, d, k);
   if (rc != GMM_OK) return rc;
   if (!x || !weights || !means || !vars || !nk || !s || !q || !loglik) return GMM_ERR_INVALID_ARG;
   Layout L;
   if (!make_layout(n, d, k, 0, &L)) return GMM_ERR_UNSUPPORTED;
+  L.refine = refine;
   rc = check_ws(L, ws, ws_bytes);
   if (rc != GMM_OK) return rc;
   return estep_dispatch(L, x, weights, means, vars, nk, s, q, loglik, 1, ws, stream);
+}
+
+int gmm_estep_accumulate(const float* x, int64_t n, int32_t d, int32_t k, const float* weights,
+                         const float* means, const float* vars, double* nk, double* s, double* q,
+                         double* loglik, void* ws, size_t ws_bytes, hipStream_t stream) {
+  return estep_entry(x, n, d, k, weights, means, vars, nk, s, q, loglik, ws, ws_bytes, stream,
+                     true);
+}
+
+int gmm_estep_accumulate_screened(const float* x, int64_t n, int32_t d, int32_t k,
+                                  const float* weights, const float* means, const float* vars,
+                                  double* nk, double* s, double* q, double* loglik, void* ws,
+                                  size_t ws_bytes, hipStream_t stream) {
+  return estep_entry(x, n, d, k, weights, means, vars, nk, s, q, loglik, ws, ws_bytes, stream,
+                     false);
 }
 
 int gmm_mstep(const double* nk, const double* s, const double* q, double n_total, int32_t d,
@@ -3624,9 +3673,10 @@ int gmm_mstep(const double* nk, const double* s, const double* q, double n_total
   return launch_status();
 }
 
-int gmm_fit(const float* x, int64_t n, int32_t d, int32_t k, int32_t n_iters, float var_floor,
-            float* weights, float* means, float* vars, double* loglik_hist, void* ws,
-            size_t ws_bytes, hipStream_t stream) {
+static int fit_entry(const float* x, int64_t n, int32_t d, int32_t k, int32_t n_iters,
+                     float var_floor, float* weights, float* means, float* vars,
+                     double* loglik_hist, void* ws, size_t ws_bytes, hipStream_t stream,
+                     bool refine) {
   int rc = check_shape(n, d, k);
   if (rc != GMM_OK) return rc;
   if (n_iters < 0 || !x || !weights || !means || !vars || (n_iters > 0 && !loglik_hist))
@@ -3634,6 +3684,7 @@ int gmm_fit(const float* x, int64_t n, int32_t d, int32_t k, int32_t n_iters, fl
   if (!(var_floor >= 0.0f)) return GMM_ERR_INVALID_ARG;
   Layout L;
   if (!make_layout(n, d, k, 0, &L)) return GMM_ERR_UNSUPPORTED;
+  L.refine = refine;
   rc = check_ws(L, ws, ws_bytes);
   if (rc != GMM_OK) return rc;
   double* fnk = at<double>(ws, L.off_fit_nk);
@@ -3653,6 +3704,20 @@ int gmm_fit(const float* x, int64_t n, int32_t d, int32_t k, int32_t n_iters, fl
     if (rc != GMM_OK) return rc;
   }
   return GMM_OK;
+}
+
+int gmm_fit(const float* x, int64_t n, int32_t d, int32_t k, int32_t n_iters, float var_floor,
+            float* weights, float* means, float* vars, double* loglik_hist, void* ws,
+            size_t ws_bytes, hipStream_t stream) {
+  return fit_entry(x, n, d, k, n_iters, var_floor, weights, means, vars, loglik_hist, ws,
+                   ws_bytes, stream, true);
+}
+
+int gmm_fit_screened(const float* x, int64_t n, int32_t d, int32_t k, int32_t n_iters,
+                     float var_floor, float* weights, float* means, float* vars,
+                     double* loglik_hist, void* ws, size_t ws_bytes, hipStream_t stream) {
+  return fit_entry(x, n, d, k, n_iters, var_floor, weights, means, vars, loglik_hist, ws,
+                   ws_bytes, stream, false);
 }
 
 int gmm_estep_accumulate_iso(const float* x, int64_t n, int32_t d, int32_t k,

@@ -9,6 +9,17 @@ both):
   LL       |gpu - ref| <= 1e-5 * |LL|
 Components with N_k < 1 are excluded from the mean and variance checks: their
 statistics are dominated by responsibilities below fp32's range.
+
+The reduced-precision calls (gmm_estep_accumulate_screened, gmm_fit_screened)
+keep the screening pass's log-densities (split bf16 products) for every pair;
+their tolerances, stated in the C header, are SCREENED_TOL:
+  N_k 2e-3, mu_kd 2e-3 (same normalisations), LL 1e-5, and
+  var_kd |gpu - ref| <= 5e-3 * (mu_kd^2 + var_kd)                 where ref N_k >= 1
+A screened responsibility is within about e = 2^-20 (S + d) relative, S =
+sum_j mu_j^2 / var_j of the components involved (S + d is 600 .. 1800 on the
+tested inputs, e up to 1.7e-3).  The variance is Q/N - mu^2: a relative error
+e of the weighted sums gives an error of about 3 e (mu^2 + var) in it, far
+more than e var when a component narrows away from the origin.
 """
 from __future__ import annotations
 
@@ -18,6 +29,8 @@ TOL_N = 1e-4
 TOL_MU = 1e-4
 TOL_VAR = 1e-4
 TOL_LL = 1e-5
+EXACT_TOL = dict(n=TOL_N, mu=TOL_MU, var=TOL_VAR, ll=TOL_LL)
+SCREENED_TOL = dict(n=2e-3, mu=2e-3, var=5e-3, ll=1e-5, var_second_moment=True)
 
 
 def to_dev(*arrays, device="cuda"):
@@ -25,7 +38,7 @@ def to_dev(*arrays, device="cuda"):
     return [torch.from_numpy(np.ascontiguousarray(a)).to(device) for a in arrays]
 
 
-def gpu_estep(x, w, mu, var, xd=None, ws=None):
+def gpu_estep(x, w, mu, var, xd=None, ws=None, screened=False):
     """GPU statistics at fp32 parameters (numpy in, numpy fp64 out)."""
     import torch
     import paper_2606_10896_amd as gmm
@@ -40,7 +53,8 @@ def gpu_estep(x, w, mu, var, xd=None, ws=None):
     ll = torch.zeros(1, dtype=torch.float64, device="cuda")
     if ws is None:
         ws = gmm.workspace(n, d, k)
-    gmm.gmm_estep_accumulate(xd, wd, mud, vd, nk, s, q, ll, ws)
+    fn = gmm.gmm_estep_accumulate_screened if screened else gmm.gmm_estep_accumulate
+    fn(xd, wd, mud, vd, nk, s, q, ll, ws)
     torch.cuda.synchronize()
     return dict(nk=nk.cpu().numpy(), s=s.cpu().numpy(), q=q.cpu().numpy(), loglik=ll.item())
 
@@ -55,7 +69,7 @@ def gpu_mstep(st, n_total, w, mu, var, var_floor=1e-6):
     return wd.cpu().numpy(), mud.cpu().numpy(), vd.cpu().numpy()
 
 
-def gpu_fit(x, w, mu, var, n_iters, var_floor=1e-6, xd=None, ws=None):
+def gpu_fit(x, w, mu, var, n_iters, var_floor=1e-6, xd=None, ws=None, screened=False):
     import torch
     import paper_2606_10896_amd as gmm
     if xd is None:
@@ -66,38 +80,40 @@ def gpu_fit(x, w, mu, var, n_iters, var_floor=1e-6, xd=None, ws=None):
     hist = torch.zeros(max(n_iters, 1), dtype=torch.float64, device="cuda")
     if ws is None:
         ws = gmm.workspace(n, d, k)
-    gmm.gmm_fit(xd, wd, mud, vd, n_iters, hist, ws, var_floor=var_floor)
+    fn = gmm.gmm_fit_screened if screened else gmm.gmm_fit
+    fn(xd, wd, mud, vd, n_iters, hist, ws, var_floor=var_floor)
     torch.cuda.synchronize()
     return wd.cpu().numpy(), mud.cpu().numpy(), vd.cpu().numpy(), hist.cpu().numpy()[:n_iters]
 
 
-def check_stats(gpu, ref, label=""):
+def check_stats(gpu, ref, label="", tol=EXACT_TOL):
     """N_k and LL against the checker; returns a short report string."""
     nk_ref = ref["nk"]
     err_n = np.abs(gpu["nk"] - nk_ref) / np.maximum(nk_ref, 1.0)
-    assert err_n.max() <= TOL_N, f"{label} N_k: max rel err {err_n.max():.3e} at {err_n.argmax()}"
+    assert err_n.max() <= tol["n"], f"{label} N_k: max rel err {err_n.max():.3e} at {err_n.argmax()}"
     err_ll = abs(gpu["loglik"] - ref["loglik"]) / abs(ref["loglik"])
-    assert err_ll <= TOL_LL, f"{label} LL: rel err {err_ll:.3e} ({gpu['loglik']} vs {ref['loglik']})"
+    assert err_ll <= tol["ll"], f"{label} LL: rel err {err_ll:.3e} ({gpu['loglik']} vs {ref['loglik']})"
     return f"N {err_n.max():.2e} LL {err_ll:.2e}"
 
 
-def check_params(w, mu, var, ref, n_total, label=""):
+def check_params(w, mu, var, ref, n_total, label="", tol=EXACT_TOL):
     """M-step results against the checker's Theta_{t+1} (fp64).  Weights are N_k / N, so they
     carry the N_k tolerance (plus fp32 storage rounding)."""
     nk_ref = ref["nk"]
     live = nk_ref >= 1.0
     rw = ref["weights"]
     err_w = np.abs(w - rw) / np.maximum(rw, 1.0 / n_total)
-    assert err_w.max() <= TOL_N + 1e-7, f"{label} weights: {err_w.max():.3e}"
+    assert err_w.max() <= tol["n"] + 1e-7, f"{label} weights: {err_w.max():.3e}"
     sig = np.sqrt(ref["vars"])
     err_mu = np.abs(mu - ref["means"]) / np.maximum(np.abs(ref["means"]), sig)
     err_mu = np.where(live[:, None], err_mu, 0.0)
     i = np.unravel_index(err_mu.argmax(), err_mu.shape)
-    assert err_mu.max() <= TOL_MU, f"{label} means: {err_mu.max():.3e} at {i}"
-    err_v = np.abs(var - ref["vars"]) / ref["vars"]
+    assert err_mu.max() <= tol["mu"], f"{label} means: {err_mu.max():.3e} at {i}"
+    scale = ref["vars"] + ref["means"] ** 2 if tol.get("var_second_moment") else ref["vars"]
+    err_v = np.abs(var - ref["vars"]) / scale
     err_v = np.where(live[:, None], err_v, 0.0)
     i = np.unravel_index(err_v.argmax(), err_v.shape)
-    assert err_v.max() <= TOL_VAR, (f"{label} vars: {err_v.max():.3e} at {i} "
+    assert err_v.max() <= tol["var"], (f"{label} vars: {err_v.max():.3e} at {i} "
                                     f"(gpu {var[i]}, ref {ref['vars'][i]}, Nk {nk_ref[i[0]]})")
     return f"mu {err_mu.max():.2e} var {err_v.max():.2e}"
 

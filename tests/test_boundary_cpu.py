@@ -107,6 +107,23 @@ def test_isotropic_host_validation():
     assert lib.gmm_mstep_iso(p, p, p, 10.0, 1025, 4, 1e-6, p, p, p, None) == gmm.GMM_ERR_UNSUPPORTED
 
 
+def test_screened_host_validation():
+    """The reduced-precision calls validate their arguments as the exact ones do."""
+    lib = gmm.load_library()
+    p, ws = _fake(), _fake(0x200000)
+    big = gmm.workspace_bytes(1000, 8, 4)
+    e = lib.gmm_estep_accumulate_screened
+    assert e(p, 0, 8, 4, p, p, p, p, p, p, p, ws, big, None) == gmm.GMM_ERR_INVALID_ARG
+    assert e(p, 1000, 8, 4, None, p, p, p, p, p, p, ws, big, None) == gmm.GMM_ERR_INVALID_ARG
+    assert e(p, 1000, 1025, 4, p, p, p, p, p, p, p, ws, big, None) == gmm.GMM_ERR_UNSUPPORTED
+    assert e(p, 1000, 8, 4, p, p, p, p, p, p, p, ws, big - 1, None) == gmm.GMM_ERR_WORKSPACE
+    f = lib.gmm_fit_screened
+    assert f(p, 1000, 8, 4, -1, 1e-6, p, p, p, p, ws, big, None) == gmm.GMM_ERR_INVALID_ARG
+    assert f(p, 1000, 8, 4, 3, -1.0, p, p, p, p, ws, big, None) == gmm.GMM_ERR_INVALID_ARG
+    assert f(p, 1000, 8, 4, 3, 1e-6, p, p, p, None, ws, big, None) == gmm.GMM_ERR_INVALID_ARG
+    assert f(p, 1000, 8, 4, 3, 1e-6, p, p, p, p, None, big, None) == gmm.GMM_ERR_WORKSPACE
+
+
 def test_streamed_host_validation():
     lib = gmm.load_library()
     p, ws = _fake(), _fake(0x200000)
