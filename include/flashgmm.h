@@ -125,16 +125,16 @@ int gmm_fit(const float* x, int64_t n, int32_t d, int32_t k, int32_t n_iters, fl
  * codes) is as in gmm_estep_accumulate / gmm_fit.
  * Error: a screened log-density is within about 2^-22 log2(e) (S_k + d)
  * log2 units of the exact one, S_k = sum_j mu_kj^2 / var_kj, so a
- * responsibility is within about e = 2^-20 (S + d) relative (both the pair
- * and log Z_i carry the error; log2(e) ln(2) = 1), S the largest S_k among
- * the point's significant components: e is about 6e-4 at S + d = 640, the
- * paper-shape workloads.  The variances the M-step forms from these
+ * responsibility is within about e = 2 ln(2) 2^-22 log2(e) (S + d) =
+ * 2^-21 (S + d) relative (both the pair and log Z_i carry the error), S the
+ * largest S_k among the point's significant components: e is about 3e-4 at
+ * S + d = 640, the paper-shape workloads.  The variances the M-step forms from these
  * statistics are differences Q/N - mu^2, so a relative error e of the
  * weighted sums becomes about 3 e (mu^2 + var) in a variance.  The stated
  * tolerances of these calls (statistics and the M-step's parameters, against
  * exact fp64 arithmetic; for inputs with S + d up to about 1800) are
  *   N_k |err| <= 2e-3 max(N_k, 1),  mu_kj |err| <= 2e-3 max(|mu_kj|, sigma_kj),
- *   var_kj |err| <= 5e-3 (mu_kj^2 + var_kj) (N_k >= 1),  LL |err| <= 1e-5 |LL|.
+ *   var_kj |err| <= 5e-3 (mu_kj^2 + var_kj) (N_k >= 1),  LL |err| <= 2e-5 |LL|.
  */
 int gmm_estep_accumulate_screened(const float* x, int64_t n, int32_t d, int32_t k,
                                   const float* weights, const float* means, const float* vars,

@@ -13,11 +13,11 @@ statistics are dominated by responsibilities below fp32's range.
 The reduced-precision calls (gmm_estep_accumulate_screened, gmm_fit_screened)
 keep the screening pass's log-densities (split bf16 products) for every pair;
 their tolerances, stated in the C header, are SCREENED_TOL:
-  N_k 2e-3, mu_kd 2e-3 (same normalisations), LL 1e-5, and
+  N_k 2e-3, mu_kd 2e-3 (same normalisations), LL 2e-5, and
   var_kd |gpu - ref| <= 5e-3 * (mu_kd^2 + var_kd)                 where ref N_k >= 1
-A screened responsibility is within about e = 2^-20 (S + d) relative, S =
+A screened responsibility is within about e = 2^-21 (S + d) relative, S =
 sum_j mu_j^2 / var_j of the components involved (S + d is 600 .. 1800 on the
-tested inputs, e up to 1.7e-3).  The variance is Q/N - mu^2: a relative error
+tested inputs, e up to 9e-4).  The variance is Q/N - mu^2: a relative error
 e of the weighted sums gives an error of about 3 e (mu^2 + var) in it, far
 more than e var when a component narrows away from the origin.
 """
@@ -30,7 +30,7 @@ TOL_MU = 1e-4
 TOL_VAR = 1e-4
 TOL_LL = 1e-5
 EXACT_TOL = dict(n=TOL_N, mu=TOL_MU, var=TOL_VAR, ll=TOL_LL)
-SCREENED_TOL = dict(n=2e-3, mu=2e-3, var=5e-3, ll=1e-5, var_second_moment=True)
+SCREENED_TOL = dict(n=2e-3, mu=2e-3, var=5e-3, ll=2e-5, var_second_moment=True)
 
 
 def to_dev(*arrays, device="cuda"):
