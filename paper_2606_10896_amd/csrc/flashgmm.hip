@@ -766,6 +766,16 @@ __device__ __forceinline__ void split_store(bf16x8* xa, int p, int c, const floa
   xa[p * RPV + 2 * (c + NC8) + 1] = lq;
 }
 
+// First-chunk operands (dimensions 0..7) of a batch of ill-conditioned
+// components, staged in LDS by k_logz.
+constexpr int kIllStage = 128;
+struct IllStage {
+  float mu[kIllStage][8];
+  double h[kIllStage][8];
+  double c[kIllStage];
+  int comp[kIllStage];
+};
+
 // LDS state of k_logz after the screening pass, per workgroup of PTS points.
 template <int PTS>
 struct LogzPost {
@@ -812,8 +822,12 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
   constexpr size_t XS_BYTES = B16 ? 0 : (size_t)PTS * P * sizeof(float);
   constexpr size_t XA_BYTES = B16 ? (size_t)PTS * RPV * sizeof(bf16x8) : 0;
   constexpr size_t PS_BYTES = sizeof(LogzPost<PTS>);
+  // bf16 screening: the ill components' staged operands follow the state
+  constexpr size_t IST_OFF = (PS_BYTES + 15) / 16 * 16;
+  constexpr size_t IST_END = B16 ? IST_OFF + sizeof(IllStage) : PS_BYTES;
   constexpr size_t SM_BYTES =
-      B16 ? (XA_BYTES > PS_BYTES ? XA_BYTES : PS_BYTES) : XS_BYTES + PS_BYTES;
+      B16 ? (XA_BYTES > IST_END ? XA_BYTES : IST_END) : XS_BYTES + PS_BYTES;
+  static_assert(!B16 || SM_BYTES <= 80 * 1024, "two workgroups per compute unit");
   __shared__ __align__(16) unsigned char smem[SM_BYTES];
   float* const xs = reinterpret_cast<float*>(smem);
   bf16x8* const xa = reinterpret_cast<bf16x8*>(smem);
@@ -1020,10 +1034,14 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
       // The first 8 dimensions of the point's row are read once for all of the
       // wave's ill components (lane = point, so these reads are not
       // coalesced); the first chunk dismisses almost every component.  The
-      // operands of that chunk are fetched one component ahead.  Same sums,
-      // in the same order, as the plain bounded form; the partial sums only
-      // grow, so an earlier dismissal gives the same -inf.
+      // first-chunk operands of up to kIllStage components at a time are
+      // staged in LDS by the whole workgroup (one memory round trip per batch
+      // instead of one per component).  Same sums, in the same order, as the
+      // plain bounded form; the partial sums only grow, so an earlier
+      // dismissal gives the same -inf.
       constexpr int H = 8;
+      static_assert(PTS == 64, "every thread of the workgroup stages operands");
+      IllStage& ist = *reinterpret_cast<IllStage*>(smem + IST_OFF);
       const bool live = row < n;
       float xh[H];
 #pragma unroll
@@ -1043,59 +1061,48 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
         xh[j + 2] = v.z;
         xh[j + 3] = v.w;
       }
-      float mA[H], mB[H];
-      double hA[H], hB[H];
-      double cA = 0.0, cB = 0.0;
-      int pA = 0, pB = 0;
-      auto fetch = [&](int ki, float (&m)[H], double (&hq)[H], double& c, int& cp) {
-        cp = ill_idx[ki];
-        c = cdir[cp];
-        const float4* mp = reinterpret_cast<const float4*>(dmu + (size_t)cp * D64);
-        const double2* hp = reinterpret_cast<const double2*>(dh + (size_t)cp * D64);
-#pragma unroll
-        for (int q4 = 0; q4 < H / 4; ++q4) {
-          const float4 mv = mp[q4];
-          m[4 * q4] = mv.x;
-          m[4 * q4 + 1] = mv.y;
-          m[4 * q4 + 2] = mv.z;
-          m[4 * q4 + 3] = mv.w;
-        }
-#pragma unroll
-        for (int q2 = 0; q2 < H / 2; ++q2) {
-          const double2 hv = hp[q2];
-          hq[2 * q2] = hv.x;
-          hq[2 * q2 + 1] = hv.y;
-        }
-      };
-      // component ki with the operands in (m, hq, c, cp); those of ki + 4 are
-      // fetched into the other set meanwhile (two sets, named statically, so
-      // that no wait falls between a fetch and its use)
-      auto step = [&](int ki, const float (&m)[H], const double (&hq)[H], double c, int cp) {
-        if (live) {
-          const double bnd = c - ((double)mw - 60.0);
-          double acc = 0.0;
-#pragma unroll
-          for (int j = 0; j < H; ++j) {
-            if (j < d) {
-              const double t = (double)xh[j] - (double)m[j];
-              acc = fma(t * t, hq[j], acc);
-            }
+      for (int base = 0; base < n_ill; base += kIllStage) {
+        const int cnt = n_ill - base < kIllStage ? n_ill - base : kIllStage;
+        // thread t: half t % 2 (dimensions 4 (t % 2) .. + 3) of component t / 2
+        if (tid < 2 * cnt) {
+          const int i = tid >> 1, hf = tid & 1;
+          const int cp = ill_idx[base + i];
+          const float4 mv = *reinterpret_cast<const float4*>(dmu + (size_t)cp * D64 + 4 * hf);
+          const double2 h0 = *reinterpret_cast<const double2*>(dh + (size_t)cp * D64 + 4 * hf);
+          const double2 h1 = *reinterpret_cast<const double2*>(dh + (size_t)cp * D64 + 4 * hf + 2);
+          *reinterpret_cast<float4*>(&ist.mu[i][4 * hf]) = mv;
+          *reinterpret_cast<double2*>(&ist.h[i][4 * hf]) = h0;
+          *reinterpret_cast<double2*>(&ist.h[i][4 * hf + 2]) = h1;
+          if (hf == 0) {
+            ist.c[i] = cdir[cp];
+            ist.comp[i] = cp;
           }
-          double l = -INFINITY;
-          if (__ballot(!(acc > bnd)) != 0ull)
-            l = ill_logit_bounded_gr(x + row * d, d, vec4, dmu + (size_t)cp * D64,
-                                     dh + (size_t)cp * D64, c, bnd, acc, H);
-          take(l);
         }
-      };
-      if (wave < n_ill) fetch(wave, mA, hA, cA, pA);
-      for (int ki = wave; ki < n_ill; ki += 8) {
-        if (ki + 4 < n_ill) fetch(ki + 4, mB, hB, cB, pB);
-        step(ki, mA, hA, cA, pA);
-        if (ki + 4 < n_ill) {
-          if (ki + 8 < n_ill) fetch(ki + 8, mA, hA, cA, pA);
-          step(ki + 4, mB, hB, cB, pB);
+        __syncthreads();
+        // components base + kl, kl = wave, wave + 4, ...: the order of the
+        // unbatched loop, as kIllStage is a multiple of 4
+        if (live) {
+          for (int kl = wave; kl < cnt; kl += 4) {
+            const double c = ist.c[kl];
+            const double bnd = c - ((double)mw - 60.0);
+            double acc = 0.0;
+#pragma unroll
+            for (int j = 0; j < H; ++j) {
+              if (j < d) {
+                const double t = (double)xh[j] - (double)ist.mu[kl][j];
+                acc = fma(t * t, ist.h[kl][j], acc);
+              }
+            }
+            double l = -INFINITY;
+            if (__ballot(!(acc > bnd)) != 0ull) {
+              const int cp = ist.comp[kl];
+              l = ill_logit_bounded_gr(x + row * d, d, vec4, dmu + (size_t)cp * D64,
+                                       dh + (size_t)cp * D64, c, bnd, acc, H);
+            }
+            take(l);
+          }
         }
+        __syncthreads();                        // the next batch reuses the staging
       }
     } else {
       for (int ki = wave; ki < n_ill; ki += 4) {
