@@ -769,6 +769,8 @@ __device__ __forceinline__ void split_store(bf16x8* xa, int p, int c, const floa
 // First-chunk operands (dimensions 0..7) of a batch of ill-conditioned
 // components, staged in LDS by k_logz.
 constexpr int kIllStage = 128;
+// Well slots whose refinement thresholds k_logz copies to LDS (bf16 screening).
+constexpr int kThrStage = 1024;
 struct IllStage {
   float mu[kIllStage][8];
   double h[kIllStage][8];
@@ -825,8 +827,10 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
   // bf16 screening: the ill components' staged operands follow the state
   constexpr size_t IST_OFF = (PS_BYTES + 15) / 16 * 16;
   constexpr size_t IST_END = B16 ? IST_OFF + sizeof(IllStage) : PS_BYTES;
+  // bf16 screening: then the refinement thresholds of up to kThrStage slots
+  constexpr size_t THR_END = B16 ? IST_END + kThrStage * sizeof(float2) : PS_BYTES;
   constexpr size_t SM_BYTES =
-      B16 ? (XA_BYTES > IST_END ? XA_BYTES : IST_END) : XS_BYTES + PS_BYTES;
+      B16 ? (XA_BYTES > THR_END ? XA_BYTES : THR_END) : XS_BYTES + PS_BYTES;
   static_assert(!B16 || SM_BYTES <= 80 * 1024, "two workgroups per compute unit");
   __shared__ __align__(16) unsigned char smem[SM_BYTES];
   float* const xs = reinterpret_cast<float*>(smem);
@@ -1009,6 +1013,21 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
       top2[wave][p] = make_float2(XA[0], XB[0]);
     }
   }
+  // the refinement thresholds, read by every lane state below: loaded now,
+  // stored to LDS after the ill-conditioned components (bf16 screening, at
+  // most kThrStage slots; else read from global memory)
+  const int kpad_w = (n_well + kWB - 1) / kWB * kWB;
+  const bool thr_lds = B16 && kpad_w <= kThrStage;
+  float2* const thr_s = reinterpret_cast<float2*>(smem + IST_END);
+  constexpr int NTHR = kThrStage / 256;
+  float2 thr_r[NTHR];
+  if (thr_lds) {
+#pragma unroll
+    for (int i = 0; i < NTHR; ++i) {
+      const int e = tid + 256 * i;
+      thr_r[i] = e < kpad_w ? thr[e] : make_float2(0.0f, 0.0f);
+    }
+  }
   // ill-conditioned components, direct form, lane = point; a term 2^-60 below
   // the point's largest well lane state is nothing in the sum and is not
   // finished (a routed component that is the point's largest is finished)
@@ -1116,6 +1135,13 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
     sti[wave][lane] = make_float2((float)mi, si);
     stim[wave][lane] = mi;
   }
+  if (thr_lds) {
+#pragma unroll
+    for (int i = 0; i < NTHR; ++i) {
+      const int e = tid + 256 * i;
+      if (e < kpad_w) thr_s[e] = thr_r[i];
+    }
+  }
   __syncthreads();
   if (tid < PTS) {
     float mm = -INFINITY, ss = 0.0f;
@@ -1160,7 +1186,7 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
       // other components' mass (bound: that mass times the arg-max component's
       // relative error bound) could exceed kFullErr of the point's total
       const float rel = mv - lzm[pp];
-      const float2 tf = av >= 0 ? thr[av] : make_float2(0.0f, 0.0f);
+      const float2 tf = av >= 0 ? (thr_lds ? thr_s[av] : thr[av]) : make_float2(0.0f, 0.0f);
       const bool full = REFINE && av >= 0 && (sv - 1.0f) * exp2_fast(rel) * tf.y > kFullErr;
       const bool cand = av >= 0 && (full || rel > tf.x ||
                                     (mv >= s4m[pp] && rel > -(float)kWideWindow));
