@@ -827,8 +827,10 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
   // bf16 screening: the ill components' staged operands follow the state
   constexpr size_t IST_OFF = (PS_BYTES + 15) / 16 * 16;
   constexpr size_t IST_END = B16 ? IST_OFF + sizeof(IllStage) : PS_BYTES;
-  // bf16 screening: then the refinement thresholds of up to kThrStage slots
-  constexpr size_t THR_END = B16 ? IST_END + kThrStage * sizeof(float2) : PS_BYTES;
+  // bf16 screening: then the refinement thresholds and the components of up to
+  // kThrStage well slots
+  constexpr size_t THR_END =
+      B16 ? IST_END + kThrStage * (sizeof(float2) + sizeof(int)) : PS_BYTES;
   constexpr size_t SM_BYTES =
       B16 ? (XA_BYTES > THR_END ? XA_BYTES : THR_END) : XS_BYTES + PS_BYTES;
   static_assert(!B16 || SM_BYTES <= 80 * 1024, "two workgroups per compute unit");
@@ -1013,19 +1015,23 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
       top2[wave][p] = make_float2(XA[0], XB[0]);
     }
   }
-  // the refinement thresholds, read by every lane state below: loaded now,
+  // the refinement thresholds, read by every lane state below, and the
+  // components of the well slots, read by every refined pair: loaded now,
   // stored to LDS after the ill-conditioned components (bf16 screening, at
   // most kThrStage slots; else read from global memory)
   const int kpad_w = (n_well + kWB - 1) / kWB * kWB;
   const bool thr_lds = B16 && kpad_w <= kThrStage;
   float2* const thr_s = reinterpret_cast<float2*>(smem + IST_END);
+  int* const wid_s = reinterpret_cast<int*>(smem + IST_END + kThrStage * sizeof(float2));
   constexpr int NTHR = kThrStage / 256;
   float2 thr_r[NTHR];
+  int wid_r[NTHR];
   if (thr_lds) {
 #pragma unroll
     for (int i = 0; i < NTHR; ++i) {
       const int e = tid + 256 * i;
       thr_r[i] = e < kpad_w ? thr[e] : make_float2(0.0f, 0.0f);
+      wid_r[i] = e < n_well ? well_idx[e] : 0;
     }
   }
   // ill-conditioned components, direct form, lane = point; a term 2^-60 below
@@ -1139,7 +1145,10 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
 #pragma unroll
     for (int i = 0; i < NTHR; ++i) {
       const int e = tid + 256 * i;
-      if (e < kpad_w) thr_s[e] = thr_r[i];
+      if (e < kpad_w) {
+        thr_s[e] = thr_r[i];
+        wid_s[e] = wid_r[i];
+      }
     }
   }
   __syncthreads();
@@ -1300,36 +1309,45 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
           constexpr int G = kRefLanes, NCK = D64 / 4 / G;
           const int g = tid & (G - 1);
           for (int j = lo + tid / G; j < hi; j += 256 / G) {
-            const int e = rlist[j - lo], pp = e >> 16, comp = well_idx[e & 0xFFFF];
+            const int e = rlist[j - lo], pp = e >> 16;
+            const int comp = thr_lds ? wid_s[e & 0xFFFF] : well_idx[e & 0xFFFF];
             const float* xr = x + (n0 + pp) * d;
             const float* mu = dmu + (size_t)comp * D64;
             const double* hh = dh + (size_t)comp * D64;
-            double acc = 0.0;
+            const double cd = cdir[comp];
+            // every chunk loaded before the arithmetic (no branch between the
+            // loads): chunks past d read dimensions 0..3 of the row, and their
+            // direct-form weights are the zero padding, so they add exact zeros
+            float4 xv[NCK], mv[NCK];
+            double2 g0[NCK], g1[NCK];
   #pragma unroll
             for (int t = 0; t < NCK; ++t) {
               const int c4 = 4 * (g + G * t);
-              if (c4 < d) {
-                const float4 xv = *reinterpret_cast<const float4*>(xr + c4);
-                const float4 m = *reinterpret_cast<const float4*>(mu + c4);
-                const double2 g0 = *reinterpret_cast<const double2*>(hh + c4);
-                const double2 g1 = *reinterpret_cast<const double2*>(hh + c4 + 2);
-                double u;
-                u = (double)xv.x - (double)m.x; acc = fma(u * u, g0.x, acc);
-                u = (double)xv.y - (double)m.y; acc = fma(u * u, g0.y, acc);
-                u = (double)xv.z - (double)m.z; acc = fma(u * u, g1.x, acc);
-                u = (double)xv.w - (double)m.w; acc = fma(u * u, g1.y, acc);
-              }
+              xv[t] = *reinterpret_cast<const float4*>(xr + (c4 < d ? c4 : 0));
+              mv[t] = *reinterpret_cast<const float4*>(mu + c4);
+              g0[t] = *reinterpret_cast<const double2*>(hh + c4);
+              g1[t] = *reinterpret_cast<const double2*>(hh + c4 + 2);
+            }
+            double acc = 0.0;
+  #pragma unroll
+            for (int t = 0; t < NCK; ++t) {
+              double u;
+              u = (double)xv[t].x - (double)mv[t].x; acc = fma(u * u, g0[t].x, acc);
+              u = (double)xv[t].y - (double)mv[t].y; acc = fma(u * u, g0[t].y, acc);
+              u = (double)xv[t].z - (double)mv[t].z; acc = fma(u * u, g1[t].x, acc);
+              u = (double)xv[t].w - (double)mv[t].w; acc = fma(u * u, g1[t].y, acc);
             }
   #pragma unroll
             for (int o = 1; o < G; o <<= 1) acc += __shfl_xor(acc, o);
             if (g == 0) {
               const double ref = lzm[pp] > -INFINITY ? (double)lzm[pp] : 0.0;
-              rres[j - lo] = (float)((cdir[comp] - acc) - ref);
+              rres[j - lo] = (float)((cd - acc) - ref);
             }
           }
         } else {
           for (int j = lo + tid; j < hi; j += 256) {
-            const int e = rlist[j - lo], pp = e >> 16, comp = well_idx[e & 0xFFFF];
+            const int e = rlist[j - lo], pp = e >> 16;
+            const int comp = thr_lds ? wid_s[e & 0xFFFF] : well_idx[e & 0xFFFF];
             const double ref = lzm[pp] > -INFINITY ? (double)lzm[pp] : 0.0;
             const double l =
                 B16 ? ill_logit_gr(x + (n0 + pp) * d, d, vec4, dmu + (size_t)comp * D64,
