@@ -64,3 +64,39 @@ def test_streamed_equals_chunk_by_chunk_calls(n, d, kt, k, chunk):
     torch.cuda.synchronize()
     for u, v in zip(tha, thb):
         assert torch.equal(u, v)
+
+
+def test_concurrent_streamed_calls_on_two_streams():
+    """Two out-of-core E-steps in flight at once, on two compute streams with their own copy
+    streams, staging buffers and workspaces: each call orders its uploads with events of its
+    own, so both results equal those of the same calls made one after the other."""
+    import torch
+    import paper_2606_10896_amd as gmm
+    sets = []
+    for i, (n, d, k, chunk) in enumerate([(30001, 64, 16, 7000), (24000, 64, 16, 5000)]):
+        w = g.custom(f"conc{i}", n, d, 8, k, data_seed=40 + i, init_seed=50 + i)
+        x, th = g.make(w)
+        sets.append(dict(xh=torch.from_numpy(x).pin_memory(), th=[torch.from_numpy(a).cuda() for a in th],
+                         chunk=chunk, k=k, d=d,
+                         staging=torch.empty(2 * chunk * d, dtype=torch.float32, device="cuda"),
+                         ws=gmm.workspace(chunk, d, k), copy=torch.cuda.Stream(),
+                         stream=torch.cuda.Stream()))
+    # one after the other
+    seq = []
+    for s in sets:
+        out = _zeros(s["k"], s["d"])
+        gmm.gmm_estep_accumulate_streamed(s["xh"], *s["th"], *out, s["chunk"], s["staging"], s["ws"],
+                                          copy_stream=s["copy"])
+        torch.cuda.synchronize()
+        seq.append(out)
+    # both in flight: each enqueued on its own stream before either is waited for
+    par = [_zeros(s["k"], s["d"]) for s in sets]
+    torch.cuda.synchronize()
+    for s, out in zip(sets, par):
+        gmm.gmm_estep_accumulate_streamed(s["xh"], *s["th"], *out, s["chunk"], s["staging"], s["ws"],
+                                          stream=s["stream"], copy_stream=s["copy"])
+    torch.cuda.synchronize()
+    for i, (a, b) in enumerate(zip(seq, par)):
+        for u, v in zip(a, b):
+            assert torch.equal(u, v), f"set {i}: concurrent and sequential statistics differ"
+    _say("  two concurrent streamed E-steps equal the sequential ones")
