@@ -429,15 +429,27 @@ __global__ __launch_bounds__(256) void k_prep_pack_well(
   }
 }
 
+// Steps (16 k each) of the split-bf16 screening: [x | x^2], or for tied
+// variances [x | ||x||^2] (the x part, then one step for ||x||^2).
+template <int D64, bool ISO>
+__host__ __device__ constexpr int screen_steps() {
+  return ISO ? D64 / 16 + 1 : D64 / 8;
+}
+
 // bf16 screening operand: for 32-component block kb and 16-k step s (k over
 // [x | x^2], k < D64 the x part), wpb[((kb * NS16 + s) * 64 + l) * 2 + {0, 1}] holds the
 // hi and lo parts of B[k = 16 s + 8 (l / 32) + e][slot 32 kb + l % 32], e = 0..7, where
 // B is log2(e) mu/var (x part) or -log2(e) / (2 var) (x^2 part), split from fp64.
-template <int D64>
+// ISO (tied variances, var[comp * d] the component's one variance): the x
+// part as above, then one step whose lane half 0 holds -1/2 log2(e) / var in
+// its first three places (they meet the three bf16 pieces of ||x||^2 in the
+// split tile) and zeros elsewhere.
+
+template <int D64, bool ISO>
 __global__ __launch_bounds__(256) void k_prep_pack_b16(
     const float* __restrict__ mu, const float* __restrict__ var, int d, int kpad,
     const int* __restrict__ counts, const int* __restrict__ well_idx, bf16x8* __restrict__ wpb) {
-  constexpr int NS16 = D64 / 8;
+  constexpr int NS16 = screen_steps<D64, ISO>();
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= (int64_t)(kpad / kBK) * NS16 * 64) return;
   const int lane = (int)(t & 63);
@@ -452,6 +464,23 @@ __global__ __launch_bounds__(256) void k_prep_pack_b16(
     const bool xpart = k < D64;
     const int j = xpart ? k : k - D64;
     double v = 0.0;
+    if (ISO && !xpart) {
+      // the ||x||^2 step, lane half 0: p = -1/2 log2(e) / var in three bf16
+      // pieces, (hi, lo) in places 0..2 and (rest, 0) in places 3..5, each
+      // group meeting the three pieces of ||x||^2 (one variance for all the
+      // dimensions: this product's rounding does not average out over them)
+      hi[e] = lo[e] = (__bf16)0.0f;
+      if (comp >= 0 && j < 6) {
+        const double pv = -0.5 * kLog2e / (double)var[(int64_t)comp * d];
+        const __bf16 ph = (__bf16)(float)pv;
+        const double r1 = pv - (double)(float)ph;
+        const __bf16 pl = (__bf16)(float)r1;
+        const __bf16 pr = (__bf16)(float)(r1 - (double)(float)pl);
+        hi[e] = j < 3 ? ph : pr;
+        lo[e] = j < 3 ? pl : (__bf16)0.0f;
+      }
+      continue;
+    }
     if (comp >= 0 && j < d) {
       const double m = mu[(int64_t)comp * d + j], s2 = var[(int64_t)comp * d + j];
       v = xpart ? kLog2e * m / s2 : -0.5 * kLog2e / s2;
@@ -631,11 +660,10 @@ __device__ __forceinline__ void logz_step(const float* xs, const float4* __restr
 // LDS as split 8-value chunks xa[p * (D64/2 + 1) + 2 c + {hi, lo}], chunk c
 // covering k = 8c .. 8c+7 of [x | x^2]; step s consumes chunks 2s (lane half 0)
 // and 2s + 1 (lane half 1); wpb is the block's packed split operand.
-template <int D64, bool MF, bool EPI, int NT, class Epi>
+template <int NS, int RPV, bool MF, bool EPI, int NT, class Epi>
 __device__ __forceinline__ void logz_step16(const bf16x8* xa, const bf16x8* __restrict__ wpb,
                                             float cb, f16v& n0, f16v& n1, const f16v& c0,
                                             const f16v& c1, Epi&& epi) {
-  constexpr int NS = D64 / 8, RPV = D64 / 2 + 1;
   const int lane = threadIdx.x & 63, h = lane >> 5, col = lane & 31;
   const bf16x8* xr0 = xa + col * RPV + 2 * h;
   const bf16x8* xr1 = xa + ((NT == 2 ? 32 : 0) + col) * RPV + 2 * h;
@@ -744,26 +772,61 @@ __device__ __forceinline__ int xpose_point(int col, int h) {
 //      pass.
 // A significant component is missed only if a larger one of the same point
 // shares its lane state; its responsibility then keeps the screening error.
-// Chunk c of point p of the split [x | x^2] tile of k_logz: v holds x of
-// dims 8c .. 8c+7; each value and its square are stored as bf16 hi + lo.
-template <int D64>
-__device__ __forceinline__ void split_store(bf16x8* xa, int p, int c, const float (&v)[8]) {
-  constexpr int NC8 = D64 / 8, RPV = D64 / 2 + 1;
+// Chunk c of point p of the split tile of k_logz: v holds x of dims
+// 8c .. 8c+7, each value stored as bf16 hi + lo; its square likewise in chunk
+// c + D64/8 ([x | x^2] tile), or, ISO, the chunk's sum of squares is
+// returned instead (fp32, in dimension order) for the ||x||^2 chunk.
+template <int D64, bool ISO>
+__device__ __forceinline__ float split_store(bf16x8* xa, int p, int c, const float (&v)[8]) {
+  constexpr int NC8 = D64 / 8, RPV = 4 * screen_steps<D64, ISO>() + 1;
   bf16x8 hi, lo, hq, lq;
+  float ssq = 0.0f;
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     const __bf16 vh = (__bf16)v[e];
     hi[e] = vh;
     lo[e] = (__bf16)(v[e] - (float)vh);
     const float q = v[e] * v[e];
-    const __bf16 qh = (__bf16)q;
-    hq[e] = qh;
-    lq[e] = (__bf16)(q - (float)qh);
+    if (ISO) {
+      ssq += q;
+    } else {
+      const __bf16 qh = (__bf16)q;
+      hq[e] = qh;
+      lq[e] = (__bf16)(q - (float)qh);
+    }
   }
   xa[p * RPV + 2 * c] = hi;
   xa[p * RPV + 2 * c + 1] = lo;
-  xa[p * RPV + 2 * (c + NC8)] = hq;
-  xa[p * RPV + 2 * (c + NC8) + 1] = lq;
+  if (!ISO) {
+    xa[p * RPV + 2 * (c + NC8)] = hq;
+    xa[p * RPV + 2 * (c + NC8) + 1] = lq;
+  }
+  return ssq;
+}
+
+// ISO: the ||x||^2 chunk of point p from its chunks' sums of squares (summed
+// in chunk order), split into three bf16 pieces (together exact to about
+// 2^-24), in places 0..2 and again in 3..5 (they meet the pieces of the
+// operand -1/2 log2(e) / var), followed by the zero chunk of the last step's
+// lane half 1.
+template <int D64>
+__device__ __forceinline__ void split_store_norm(bf16x8* xa, int p, const float* csq) {
+  constexpr int NC8 = D64 / 8, RPV = 4 * screen_steps<D64, true>() + 1;
+  float nrm = 0.0f;
+  for (int c = 0; c < NC8; ++c) nrm += csq[c];
+  bf16x8 hi, z;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) hi[e] = z[e] = (__bf16)0.0f;
+  const __bf16 n0 = (__bf16)nrm;
+  const float r1 = nrm - (float)n0;
+  const __bf16 n1 = (__bf16)r1;
+  hi[0] = hi[3] = n0;
+  hi[1] = hi[4] = n1;
+  hi[2] = hi[5] = (__bf16)(r1 - (float)n1);
+  xa[p * RPV + 2 * NC8] = hi;
+  xa[p * RPV + 2 * NC8 + 1] = z;
+  xa[p * RPV + 2 * NC8 + 2] = z;
+  xa[p * RPV + 2 * NC8 + 3] = z;
 }
 
 // First-chunk operands (dimensions 0..7) of a batch of ill-conditioned
@@ -804,7 +867,7 @@ struct LogzPost {
 
 // REFINE = false (the screened E-step): the candidates keep their screened
 // log-densities instead of the direct-form ones; everything else is the same.
-template <int D64, bool REFINE>
+template <int D64, bool REFINE, bool ISO>
 __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
     const float* __restrict__ x, int64_t n, int d, int vec4, const float4* __restrict__ wp,
     const bf16x8* __restrict__ wpb,
@@ -816,7 +879,11 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
     unsigned long long* __restrict__ bmask, unsigned char* __restrict__ iflag) {
   constexpr int P = D64 + 4, NT = logz_tiles(D64), PTS = 32 * NT;
   constexpr bool B16 = screen_b16(D64);
-  constexpr int RPV = D64 / 2 + 1;
+  static_assert(!ISO || B16, "the isotropic screening tile is a split-bf16 one");
+  // split tile row: [x | x^2] chunks (hi, lo), or for ISO the x chunks, one
+  // ||x||^2 chunk and one zero chunk; one padding entry
+  constexpr int NSTEP = screen_steps<D64, ISO>();
+  constexpr int RPV = 4 * NSTEP + 1;
   // bf16 screening: the split [x | x^2] tile, whose space the post-screening
   // state takes over (direct-form sums then read x from global memory), so
   // that two workgroups fit a compute unit.  fp32 screening: the fp32 tile,
@@ -831,12 +898,15 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
   // kThrStage well slots
   constexpr size_t THR_END =
       B16 ? IST_END + kThrStage * (sizeof(float2) + sizeof(int)) : PS_BYTES;
+  constexpr size_t CSQ_END = XA_BYTES + (ISO ? (size_t)PTS * (D64 / 8) * sizeof(float) : 0);
   constexpr size_t SM_BYTES =
-      B16 ? (XA_BYTES > THR_END ? XA_BYTES : THR_END) : XS_BYTES + PS_BYTES;
+      B16 ? (CSQ_END > THR_END ? CSQ_END : THR_END) : XS_BYTES + PS_BYTES;
   static_assert(!B16 || SM_BYTES <= 80 * 1024, "two workgroups per compute unit");
   __shared__ __align__(16) unsigned char smem[SM_BYTES];
   float* const xs = reinterpret_cast<float*>(smem);
   bf16x8* const xa = reinterpret_cast<bf16x8*>(smem);
+  // ISO: per-chunk sums of squares, after the tile (only used while building it)
+  float* const csq = reinterpret_cast<float*>(smem + XA_BYTES);
   LogzPost<PTS>& post = *reinterpret_cast<LogzPost<PTS>*>(smem + XS_BYTES);
   auto& stw = post.stw;
   auto& sti = post.sti;
@@ -897,7 +967,8 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
         if (t < PTS * NC8) {
           const float v[8] = {ld[it][0].x, ld[it][0].y, ld[it][0].z, ld[it][0].w,
                               ld[it][1].x, ld[it][1].y, ld[it][1].z, ld[it][1].w};
-          split_store<D64>(xa, t / NC8, t % NC8, v);
+          const float ssq = split_store<D64, ISO>(xa, t / NC8, t % NC8, v);
+          if constexpr (ISO) csq[t] = ssq;
         }
       }
     } else {
@@ -910,8 +981,13 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
           const int j = 8 * c + e;
           v[e] = (row < n && j < d) ? x[row * d + j] : 0.0f;
         }
-        split_store<D64>(xa, p, c, v);
+        const float ssq = split_store<D64, ISO>(xa, p, c, v);
+        if constexpr (ISO) csq[t] = ssq;
       }
+    }
+    if constexpr (ISO) {
+      __syncthreads();
+      if (tid < PTS) split_store_norm<D64>(xa, tid, csq + tid * NC8);
     }
   } else {
     load_tile<D64>(x, n, d, n0, PTS, xs, vec4 != 0);
@@ -938,10 +1014,10 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
       lse_add_arg(m0[v], s0[v], a0[v], l0, slot);
       if constexpr (NT == 2) lse_add_arg(m1[v], s1[v], a1[v], l1, slot);
     };
-    constexpr size_t BS16 = (size_t)(D64 / 8) * 64 * 2;
+    constexpr size_t BS16 = (size_t)NSTEP * 64 * 2;
     if (nb > 0) {
       if constexpr (B16)
-        logz_step16<D64, true, false, NT>(xa, wpb + (size_t)wave * BS16, cw[wave * kBK + col], c0,
+        logz_step16<NSTEP, RPV, true, false, NT>(xa, wpb + (size_t)wave * BS16, cw[wave * kBK + col], c0,
                                           c1, x0, x1, epi);
       else
         logz_step<D64, true, false, NT>(xs, wp + (size_t)wave * BS, cw[wave * kBK + col], c0, c1,
@@ -953,7 +1029,7 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
         if (i + 2 < nb) cbn = cw[(kb + 8) * kBK + col];
         slot = kb * kBK + col;
         if constexpr (B16)
-          logz_step16<D64, true, true, NT>(xa, wpb + (size_t)(kb + 4) * BS16, cb, x0, x1, c0, c1,
+          logz_step16<NSTEP, RPV, true, true, NT>(xa, wpb + (size_t)(kb + 4) * BS16, cb, x0, x1, c0, c1,
                                            epi);
         else
           logz_step<D64, true, true, NT>(xs, wp + (size_t)(kb + 4) * BS, cb, x0, x1, c0, c1, epi);
@@ -962,7 +1038,7 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
       }
       slot = (wave + 4 * (nb - 1)) * kBK + col;
       if constexpr (B16)
-        logz_step16<D64, false, true, NT>(xa, wpb, 0.0f, x0, x1, c0, c1, epi);
+        logz_step16<NSTEP, RPV, false, true, NT>(xa, wpb, 0.0f, x0, x1, c0, c1, epi);
       else
         logz_step<D64, false, true, NT>(xs, wp, 0.0f, x0, x1, c0, c1, epi);
     }
@@ -3268,6 +3344,7 @@ struct Layout {
   int64_t n_wg_logz;
   bool bmask_on;            // per-point dense-block masks (at most 64 blocks of 64 components)
   bool refine = true;       // false: the screened E-step (no direct-form refinement)
+  bool iso = false;         // tied variances: [x | ||x||^2] screening (split-bf16 path)
   size_t off_counts, off_cls, off_cwell, off_cdir, off_cthr, off_thr, off_well_idx, off_ill_idx,
       off_cw, off_wp, off_wq, off_wpb, off_dmu, off_dh, off_logz2, off_cslot, off_cr, off_llpart,
       off_part_w, off_part_s, off_part_i, off_scnt, off_soff, off_slist, off_bmask, off_fit_nk,
@@ -3443,9 +3520,15 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
     hipLaunchKernelGGL(k_prep_pack_well<D64>, dim3((unsigned)cdiv(tot, 256)), dim3(256), 0, st,
                        mu, var, d, kpad, cwell, cthr, counts, well_idx, wp, cw, thr);
     if constexpr (screen_b16(D64)) {
-      const int64_t tb = (int64_t)(kpad / kBK) * (D64 / 8) * 64;
-      hipLaunchKernelGGL(k_prep_pack_b16<D64>, dim3((unsigned)cdiv(tb, 256)), dim3(256), 0, st,
-                         mu, var, d, kpad, counts, well_idx, wpb);
+      if (L.iso) {
+        const int64_t tb = (int64_t)(kpad / kBK) * screen_steps<D64, true>() * 64;
+        hipLaunchKernelGGL((k_prep_pack_b16<D64, true>), dim3((unsigned)cdiv(tb, 256)), dim3(256),
+                           0, st, mu, var, d, kpad, counts, well_idx, wpb);
+      } else {
+        const int64_t tb = (int64_t)(kpad / kBK) * screen_steps<D64, false>() * 64;
+        hipLaunchKernelGGL((k_prep_pack_b16<D64, false>), dim3((unsigned)cdiv(tb, 256)),
+                           dim3(256), 0, st, mu, var, d, kpad, counts, well_idx, wpb);
+      }
     }
     hipLaunchKernelGGL(k_prep_pack_w16<D64>,
                        dim3((unsigned)cdiv((int64_t)(kpad / 16) * wq_steps(D64) * 64, 256)),
@@ -3455,14 +3538,25 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
                        st, mu, var, d, k, dmu, dh);
   }
   tm = phase_mark(1, st) && tm;
-  if (L.refine)
-    hipLaunchKernelGGL((k_logz<D64, true>), dim3((unsigned)L.n_wg_logz), dim3(256), 0, st, x, n,
-                       d, vec4, wp, wpb, cw, thr, well_idx, ill_idx, dmu, dh, cdir, counts, logz2,
-                       cslot, cr, llpart, bmask, iflag);
-  else
-    hipLaunchKernelGGL((k_logz<D64, false>), dim3((unsigned)L.n_wg_logz), dim3(256), 0, st, x, n,
-                       d, vec4, wp, wpb, cw, thr, well_idx, ill_idx, dmu, dh, cdir, counts, logz2,
-                       cslot, cr, llpart, bmask, iflag);
+  bool launched = false;
+  if constexpr (screen_b16(D64)) {
+    if (L.iso && L.refine) {
+      hipLaunchKernelGGL((k_logz<D64, true, true>), dim3((unsigned)L.n_wg_logz), dim3(256), 0, st,
+                         x, n, d, vec4, wp, wpb, cw, thr, well_idx, ill_idx, dmu, dh, cdir, counts,
+                         logz2, cslot, cr, llpart, bmask, iflag);
+      launched = true;
+    }
+  }
+  if (!launched) {
+    if (L.refine)
+      hipLaunchKernelGGL((k_logz<D64, true, false>), dim3((unsigned)L.n_wg_logz), dim3(256), 0, st,
+                         x, n, d, vec4, wp, wpb, cw, thr, well_idx, ill_idx, dmu, dh, cdir, counts,
+                         logz2, cslot, cr, llpart, bmask, iflag);
+    else
+      hipLaunchKernelGGL((k_logz<D64, false, false>), dim3((unsigned)L.n_wg_logz), dim3(256), 0,
+                         st, x, n, d, vec4, wp, wpb, cw, thr, well_idx, ill_idx, dmu, dh, cdir,
+                         counts, logz2, cslot, cr, llpart, bmask, iflag);
+  }
   tm = phase_mark(2, st) && tm;
   if constexpr (D64 < 256) {
     hipLaunchKernelGGL(k_stats_well<D64>, dim3((unsigned)((kpad / kWB) * L.nch)), dim3(256), 0,
@@ -3780,6 +3874,7 @@ int gmm_estep_accumulate_iso(const float* x, int64_t n, int32_t d, int32_t k,
   if (!x || !weights || !means || !vars || !nk || !s || !q || !loglik) return GMM_ERR_INVALID_ARG;
   Layout L;
   if (!make_layout(n, d, k, 0, &L)) return GMM_ERR_UNSUPPORTED;
+  L.iso = true;
   rc = check_ws(L, ws, ws_bytes);
   if (rc != GMM_OK) return rc;
   float* vfull = at<float>(ws, L.off_iso_var);
@@ -3816,6 +3911,7 @@ int gmm_fit_iso(const float* x, int64_t n, int32_t d, int32_t k, int32_t n_iters
   if (!(var_floor >= 0.0f)) return GMM_ERR_INVALID_ARG;
   Layout L;
   if (!make_layout(n, d, k, 0, &L)) return GMM_ERR_UNSUPPORTED;
+  L.iso = true;
   rc = check_ws(L, ws, ws_bytes);
   if (rc != GMM_OK) return rc;
   double* fnk = at<double>(ws, L.off_fit_nk);
