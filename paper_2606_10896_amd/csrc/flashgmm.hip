@@ -502,13 +502,19 @@ __global__ __launch_bounds__(256) void k_prep_pack_b16(
 // log2(e) (log pi / NGB - 1/2 sum over its dimensions of (mu^2/var + log 2 pi var)),
 // in lane group 1 (-inf for a dead or padded slot), and 0 in group 3.
 constexpr int wq_steps(int D64) { return D64 / 2 + D64 / 32; }
+// Tied variances (ISO): the x steps, then per 32-dimension group one norm step
+// (-1/2 log2(e) / var in every lane group: it meets each lane's sum of squares
+// over its 8 dimensions of the group), then the bias steps.
+constexpr int wq_steps_iso(int D64) { return D64 / 4 + D64 / 16; }
 
-template <int D64>
+template <int D64, bool ISO>
 __global__ __launch_bounds__(256) void k_prep_pack_w16(
     const float* __restrict__ w, const float* __restrict__ mu, const float* __restrict__ var,
     int d, int kpad, const int* __restrict__ counts, const int* __restrict__ well_idx,
     float* __restrict__ wq) {
-  constexpr int NS = D64 / 4, NGB = D64 / 32, WQS = wq_steps(D64);
+  constexpr int NS = D64 / 4, NGB = D64 / 32, WQS = ISO ? wq_steps_iso(D64) : wq_steps(D64);
+  // first bias step
+  constexpr int SB = ISO ? NS + NGB : 2 * NS;
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= (int64_t)(kpad / 16) * WQS * 64) return;
   const int lane = (int)(t & 63);
@@ -517,7 +523,9 @@ __global__ __launch_bounds__(256) void k_prep_pack_w16(
   const int slot = g * 16 + (lane & 15);
   const int comp = slot < counts[0] ? well_idx[slot] : -1;
   float v = 0.0f;
-  if (s < 2 * NS) {
+  if (ISO && s >= NS && s < SB) {
+    if (comp >= 0) v = (float)(-0.5 * kLog2e / (double)var[(int64_t)comp * d]);
+  } else if (s < SB) {
     const bool xpart = s < NS;
     const int ss = xpart ? s : s - NS;
     const int j = 16 * (ss / 4) + 4 * (lane >> 4) + ss % 4;
@@ -526,7 +534,7 @@ __global__ __launch_bounds__(256) void k_prep_pack_w16(
       v = xpart ? (float)(kLog2e * m / s2) : (float)(-0.5 * kLog2e / s2);
     }
   } else {
-    const int b = s - 2 * NS, lg = lane >> 4;
+    const int b = s - SB, lg = lane >> 4;
     if (lg == 0) {
       v = 1.0f;
     } else if (lg == 1) {
@@ -1589,7 +1597,13 @@ __device__ __forceinline__ f4v mfma16(float a, float b, f4v c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
-template <int D64>
+// ISO (tied variances): per 32-dimension group the x steps, one norm step
+// (each lane's sum of squares over its 8 dimensions of the group against
+// -1/2 log2(e) / var, the MFMA summing the four lane groups) and the bias
+// step; the statistics contract r^T x on MFMA and add r ||x||^2 on the vector
+// ALU, written into dimension 0 of Q (the isotropic Q is the sum over the
+// dimensions).
+template <int D64, bool ISO>
 __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
     const float* __restrict__ x, int64_t n, int d, int vec4, const float* __restrict__ wq,
     const float* __restrict__ cw, const int* __restrict__ counts,
@@ -1601,7 +1615,9 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
   constexpr int NG = D64 / 64;                  // float4 column groups per part
   constexpr int NB = D64 / 16;                  // 16-column blocks per part
   constexpr int NGB = D64 / 32;                 // 32-dimension groups (bias steps)
-  constexpr int WQS = wq_steps(D64);
+  constexpr int WQS = ISO ? wq_steps_iso(D64) : wq_steps(D64);
+  constexpr int SB = ISO ? NS + NGB : 2 * NS;   // first bias step
+  constexpr int NACC = ISO ? NB : 2 * NB;       // accumulator blocks
   constexpr int PTS = 32;                       // points per iteration (two tiles)
   constexpr int Q4 = D64 / 4;
   constexpr int LD = PTS * Q4 / 256;            // float4 per thread per X tile
@@ -1683,10 +1699,11 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
     }
   };
 
-  f4v acc[2 * NB];
+  f4v acc[NACC];
 #pragma unroll
-  for (int c = 0; c < 2 * NB; ++c) acc[c] = f4v{0.f, 0.f, 0.f, 0.f};
+  for (int c = 0; c < NACC; ++c) acc[c] = f4v{0.f, 0.f, 0.f, 0.f};
   float nkacc = 0.0f;
+  float qacc = 0.0f;                            // ISO: sum of r ||x||^2
   bool first = true;
   const int myc = wave * 16 + i16;              // this lane's component in the block
 
@@ -1695,6 +1712,11 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
   auto flush = [&]() {
     float nk2 = nkacc + __shfl_xor(nkacc, 16);
     nk2 += __shfl_xor(nk2, 32);
+    float q2 = 0.0f;
+    if constexpr (ISO) {
+      q2 = qacc + __shfl_xor(qacc, 16);
+      q2 += __shfl_xor(q2, 32);
+    }
     double* row = pw + (size_t)myc * STRIDE;
     if (k4 == 0) row[0] = first ? (double)nk2 : row[0] + (double)nk2;
 #pragma unroll
@@ -1714,13 +1736,19 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
             const int dim = 64 * g + 4 * (4 * k4 + v) + e;
-            const int c = part2 * NB + 4 * g + e;
-            row[1 + part2 * D64 + dim] = o[4 * e + v] + (double)acc[c][v];
-            acc[c][v] = 0.0f;
+            if (ISO && part2 == 1) {
+              // dimension 0 (lane group 0) carries the whole isotropic Q
+              row[1 + D64 + dim] = o[4 * e + v] + (dim == 0 ? (double)q2 : 0.0);
+            } else {
+              const int c = part2 * NB + 4 * g + e;
+              row[1 + part2 * D64 + dim] = o[4 * e + v] + (double)acc[c][v];
+              acc[c][v] = 0.0f;
+            }
           }
       }
     }
     nkacc = 0.0f;
+    qacc = 0.0f;
     first = false;
   };
 
@@ -1783,6 +1811,7 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
       // wide D: keep each group's operand loads in their group (hoisting all
       // of them exhausts the registers)
       constexpr bool kPin = D64 > 128;
+      float nrm = 0.0f;                         // ISO: this lane's sum of squares
 #pragma unroll
       for (int b = 0; b < NGB; ++b) {
         const float4 u0 = *reinterpret_cast<const float4*>(xr + 32 * b);
@@ -1796,16 +1825,30 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
         la = mfma16(u1.y, wb[j0 + 5], la);
         la = mfma16(u1.z, wb[j0 + 6], la);
         la = mfma16(u1.w, wb[j0 + 7], la);
-        la = mfma16(u0.x * u0.x, wb[NS + j0], la);
-        la = mfma16(u0.y * u0.y, wb[NS + j0 + 1], la);
-        la = mfma16(u0.z * u0.z, wb[NS + j0 + 2], la);
-        la = mfma16(u0.w * u0.w, wb[NS + j0 + 3], la);
-        la = mfma16(u1.x * u1.x, wb[NS + j0 + 4], la);
-        la = mfma16(u1.y * u1.y, wb[NS + j0 + 5], la);
-        la = mfma16(u1.z * u1.z, wb[NS + j0 + 6], la);
-        la = mfma16(u1.w * u1.w, wb[NS + j0 + 7], la);
-        la = mfma16(ab, wb[2 * NS + b], la);
+        if constexpr (ISO) {
+          const float sq = ((u0.x * u0.x + u0.y * u0.y) + (u0.z * u0.z + u0.w * u0.w)) +
+                           ((u1.x * u1.x + u1.y * u1.y) + (u1.z * u1.z + u1.w * u1.w));
+          nrm += sq;
+          la = mfma16(sq, wb[NS + b], la);
+        } else {
+          la = mfma16(u0.x * u0.x, wb[NS + j0], la);
+          la = mfma16(u0.y * u0.y, wb[NS + j0 + 1], la);
+          la = mfma16(u0.z * u0.z, wb[NS + j0 + 2], la);
+          la = mfma16(u0.w * u0.w, wb[NS + j0 + 3], la);
+          la = mfma16(u1.x * u1.x, wb[NS + j0 + 4], la);
+          la = mfma16(u1.y * u1.y, wb[NS + j0 + 5], la);
+          la = mfma16(u1.z * u1.z, wb[NS + j0 + 6], la);
+          la = mfma16(u1.w * u1.w, wb[NS + j0 + 7], la);
+        }
+        la = mfma16(ab, wb[SB + b], la);
         if constexpr (kPin) __builtin_amdgcn_sched_barrier(0);
+      }
+      // ISO: ||x||^2 of row point i16 (the four lane groups' sums, in a fixed
+      // order; every lane of the point gets the same value)
+      float nfull = 0.0f;
+      if constexpr (ISO) {
+        nfull = nrm + __shfl_xor(nrm, 16);
+        nfull += __shfl_xor(nfull, 32);
       }
       float r[4];
 #pragma unroll
@@ -1814,6 +1857,7 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
         const float e = exp2_fast(la[v]);
         r[v] = ((rbb[cur][pt] >> myc) & 1ull) ? 0.0f : e;
         nkacc += r[v];
+        if constexpr (ISO) qacc += r[v] * __shfl(nfull, 4 * k4 + v);
       }
       // statistics: step v contracts points t*16 + 4k + v (k = 0..3)
 #pragma unroll
@@ -1826,10 +1870,12 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
           acc[4 * g + 1] = mfma16(y.y, r[v], acc[4 * g + 1]);
           acc[4 * g + 2] = mfma16(y.z, r[v], acc[4 * g + 2]);
           acc[4 * g + 3] = mfma16(y.w, r[v], acc[4 * g + 3]);
-          acc[NB + 4 * g + 0] = mfma16(y.x * y.x, r[v], acc[NB + 4 * g + 0]);
-          acc[NB + 4 * g + 1] = mfma16(y.y * y.y, r[v], acc[NB + 4 * g + 1]);
-          acc[NB + 4 * g + 2] = mfma16(y.z * y.z, r[v], acc[NB + 4 * g + 2]);
-          acc[NB + 4 * g + 3] = mfma16(y.w * y.w, r[v], acc[NB + 4 * g + 3]);
+          if constexpr (!ISO) {
+            acc[NB + 4 * g + 0] = mfma16(y.x * y.x, r[v], acc[NB + 4 * g + 0]);
+            acc[NB + 4 * g + 1] = mfma16(y.y * y.y, r[v], acc[NB + 4 * g + 1]);
+            acc[NB + 4 * g + 2] = mfma16(y.z * y.z, r[v], acc[NB + 4 * g + 2]);
+            acc[NB + 4 * g + 3] = mfma16(y.w * y.w, r[v], acc[NB + 4 * g + 3]);
+          }
           if constexpr (kPin) __builtin_amdgcn_sched_barrier(0);
         }
       }
@@ -3530,9 +3576,14 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
                            dim3(256), 0, st, mu, var, d, kpad, counts, well_idx, wpb);
       }
     }
-    hipLaunchKernelGGL(k_prep_pack_w16<D64>,
-                       dim3((unsigned)cdiv((int64_t)(kpad / 16) * wq_steps(D64) * 64, 256)),
-                       dim3(256), 0, st, w, mu, var, d, kpad, counts, well_idx, wq);
+    if (D64 < 256 && L.iso)
+      hipLaunchKernelGGL((k_prep_pack_w16<D64, true>),
+                         dim3((unsigned)cdiv((int64_t)(kpad / 16) * wq_steps_iso(D64) * 64, 256)),
+                         dim3(256), 0, st, w, mu, var, d, kpad, counts, well_idx, wq);
+    else
+      hipLaunchKernelGGL((k_prep_pack_w16<D64, false>),
+                         dim3((unsigned)cdiv((int64_t)(kpad / 16) * wq_steps(D64) * 64, 256)),
+                         dim3(256), 0, st, w, mu, var, d, kpad, counts, well_idx, wq);
     const int64_t toti = (int64_t)k * D64;
     hipLaunchKernelGGL(k_prep_pack_direct<D64>, dim3((unsigned)cdiv(toti, 256)), dim3(256), 0,
                        st, mu, var, d, k, dmu, dh);
@@ -3559,9 +3610,14 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
   }
   tm = phase_mark(2, st) && tm;
   if constexpr (D64 < 256) {
-    hipLaunchKernelGGL(k_stats_well<D64>, dim3((unsigned)((kpad / kWB) * L.nch)), dim3(256), 0,
-                       st, x, n, d, vec4, wq, cw, counts, logz2, cslot, bmask, L.nch, L.chunk,
-                       part_w);
+    if (L.iso)
+      hipLaunchKernelGGL((k_stats_well<D64, true>), dim3((unsigned)((kpad / kWB) * L.nch)),
+                         dim3(256), 0, st, x, n, d, vec4, wq, cw, counts, logz2, cslot, bmask,
+                         L.nch, L.chunk, part_w);
+    else
+      hipLaunchKernelGGL((k_stats_well<D64, false>), dim3((unsigned)((kpad / kWB) * L.nch)),
+                         dim3(256), 0, st, x, n, d, vec4, wq, cw, counts, logz2, cslot, bmask,
+                         L.nch, L.chunk, part_w);
   } else {
     hipLaunchKernelGGL(k_stats_wide<D64>, dim3((unsigned)((kpad / 16) * L.nch)),
                        dim3(64 * (D64 / 128)), 0, st, x, n, d, vec4, wq, cwell, well_idx, counts,

@@ -38,8 +38,8 @@ def _teacher_forced(x, thetas, label, xd=None):
         _say(f"  {label} t={t}: {r1} Q {err_q.max():.2e} {r2}")
 
 
-@pytest.mark.parametrize("n,d,kt,k", [(2000, 37, 5, 7), (3000, 128, 20, 64), (1500, 300, 6, 20),
-                                      (1000, 768, 8, 33)])
+@pytest.mark.parametrize("n,d,kt,k", [(2000, 37, 5, 7), (3000, 128, 20, 64), (1800, 150, 6, 40),
+                                      (1500, 300, 6, 20), (1000, 768, 8, 33)])
 def test_isotropic_ragged_shapes(n, d, kt, k):
     w = g.custom(f"iso{n}_{d}", n, d, kt, k, data_seed=77 + d, init_seed=99 + k)
     x, th0 = g.make(w)
