@@ -3042,6 +3042,22 @@ __global__ __launch_bounds__(256) void k_assign_fallback(
 //   sparse  ((slot / sbk) * nparts + part) * sbk + slot % sbk
 //   ill     ((islot / ibk) * nchk + chunk) * ibk + islot % ibk
 // summed here in chunk (part) order.
+// acc + p[0] + p[step] + ... + p[(cnt - 1) step], added in that order, with
+// 8 loads in flight at a time.
+__device__ __forceinline__ double sum_strided(const double* __restrict__ p, int cnt, size_t step,
+                                              double acc) {
+  int ch = 0;
+  for (; ch + 8 <= cnt; ch += 8) {
+    double v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = p[(size_t)(ch + j) * step];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc += v[j];
+  }
+  for (; ch < cnt; ++ch) acc += p[(size_t)ch * step];
+  return acc;
+}
+
 __global__ __launch_bounds__(256) void k_reduce_stats(
     const double* __restrict__ part_w, const double* __restrict__ part_s,
     const double* __restrict__ part_i,
@@ -3063,17 +3079,17 @@ __global__ __launch_bounds__(256) void k_reduce_stats(
     if (slot >= counts[0]) return;
     comp = well_idx[slot];
     const double* p = part_w + ((size_t)(slot / wbk) * nch * wbk + (slot % wbk)) * stride + off;
-    for (int ch = 0; ch < nch; ++ch) acc += p[(size_t)ch * wbk * stride];
+    acc = sum_strided(p, nch, (size_t)wbk * stride, acc);
     const double* ps =
         part_s + ((size_t)(slot / sbk) * nparts * sbk + (slot % sbk)) * stride + off;
-    for (int ch = 0; ch < nparts; ++ch) acc += ps[(size_t)ch * sbk * stride];
+    acc = sum_strided(ps, nparts, (size_t)sbk * stride, acc);
   } else {
     if (slot >= counts[1]) return;
     comp = ill_idx[slot];
     const int n_ikb = (counts[1] + ibk - 1) / ibk;
     const int nchk = ill_chunks(grid_i, n_ikb, n, ipt);
     const double* p = part_i + ((size_t)(slot / ibk) * nchk * ibk + (slot % ibk)) * stride + off;
-    for (int ch = 0; ch < nchk; ++ch) acc += p[(size_t)ch * ibk * stride];
+    acc = sum_strided(p, nchk, (size_t)ibk * stride, acc);
   }
   if (c == 0) nk[comp] += acc;
   else if (c <= d) s[(int64_t)comp * d + (c - 1)] += acc;
@@ -3086,7 +3102,16 @@ __global__ __launch_bounds__(1024) void k_reduce_ll(const double* __restrict__ l
   __shared__ double sh[1024];
   const int t = threadIdx.x;
   double a = 0.0;
-  for (int64_t i = t; i < cnt; i += 1024) a += ll_part[i];
+  // entries t, t + 1024, ... added in that order; 16 loads in flight at a time
+  int64_t i = t;
+  for (; i + 15 * 1024 < cnt; i += 16 * 1024) {
+    double v[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) v[j] = ll_part[i + 1024 * j];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) a += v[j];
+  }
+  for (; i < cnt; i += 1024) a += ll_part[i];
   sh[t] = a;
   __syncthreads();
   for (int w = 512; w > 0; w >>= 1) {
