@@ -3374,8 +3374,7 @@ __global__ __launch_bounds__(256) void k_km_reduce(const double* __restrict__ pa
   const int64_t stride = 1 + 2 * (int64_t)D64;
   const int64_t off = c == 0 ? 0 : (c <= d ? 1 + (c - 1) : 1 + D64 + (c - 1 - d));
   const double* ps = part_s + ((size_t)(slot / sbk) * nparts * sbk + (slot % sbk)) * stride + off;
-  double acc = 0.0;
-  for (int ch = 0; ch < nparts; ++ch) acc += ps[(size_t)ch * sbk * stride];
+  const double acc = sum_strided(ps, nparts, (size_t)sbk * stride, 0.0);
   if (c == 0) nk[slot] = acc;
   else if (c <= d) s[(int64_t)slot * d + (c - 1)] = acc;
   else q[(int64_t)slot * d + (c - 1 - d)] = acc;
