@@ -15,7 +15,10 @@
  *     weights/nk[k].  Parameters are fp32, statistics fp64.
  *   - Every call only enqueues work on `stream` and returns; results are
  *     valid once the caller synchronises the stream.  Calls that share a
- *     workspace must be ordered on one stream.
+ *     workspace must be ordered on one stream.  Calls with separate
+ *     workspaces (and, for the out-of-core call, separate staging buffers and
+ *     copy streams) may run concurrently on different streams: the library
+ *     keeps no state between calls apart from the optional phase timer.
  *   - Errors: argument checks run on the host before anything is enqueued and
  *     return a negative gmm_status (nothing is enqueued then).  A HIP error
  *     reported at launch returns GMM_ERR_DEVICE.  NaN or Inf in the inputs is
