@@ -54,7 +54,7 @@ def _load():
         lib.oracle_assign_topk.restype = ctypes.c_int
         lib.oracle_kmeans.argtypes = [vp, i64, i32, i32, i32, f64, vp, vp, vp, vp, vp, vp, vp]
         lib.oracle_kmeans.restype = None
-        lib.oracle_kmeanspp.argtypes = [vp, i64, i32, i32, vp, vp, vp]
+        lib.oracle_kmeanspp.argtypes = [vp, i64, i32, i32, vp, vp, vp, vp]
         lib.oracle_kmeanspp.restype = None
         lib.oracle_iso_estep.argtypes = [vp, i64, i32, i32, vp, vp, vp, vp, vp, vp, vp, i32]
         lib.oracle_iso_estep.restype = None
@@ -226,16 +226,22 @@ def iso_fit(x, weights, means, variances, n_iters, var_floor=DEFAULT_VAR_FLOOR, 
 
 
 # ---------------------------------------------------------------- k-means++ seeding
-def kmeanspp(x, k, u):
-    """k-means++ seeding with the given uniforms u[k] in [0, 1) (see oracle.c for the orders
-    that fix every decision).  Returns (rows int64 [k], centres fp32 [k, d])."""
+def kmeanspp(x, k, u, want_margin=False):
+    """k-means++ seeding with the given uniforms u[k] in [0, 1): D^2 sampling by inversion
+    against the running sum in row order (see oracle.c).  Returns (rows int64 [k], centres
+    fp32 [k, d]) and, with want_margin, also margin fp64 [k]: how far each draw's target lies
+    inside the picked row's interval of the running sum, relative to the total (+inf for the
+    first centre and a zero total)."""
     x = _f32(x)
     n, d = x.shape
     u = np.ascontiguousarray(u, dtype=np.float64)
     assert u.shape == (k,) and np.all((u >= 0.0) & (u < 1.0))
     idx = np.zeros(k, dtype=np.int64)
     cen = np.zeros((k, d), dtype=np.float32)
-    _load().oracle_kmeanspp(_p(x), n, d, k, _p(u), _p(idx), _p(cen))
+    mg = np.zeros(k)
+    _load().oracle_kmeanspp(_p(x), n, d, k, _p(u), _p(idx), _p(cen), _p(mg))
+    if want_margin:
+        return idx, cen, mg
     return idx, cen
 
 

@@ -508,42 +508,28 @@ void oracle_iso_iterate(const float* x, int64_t n, int32_t d, int32_t k, const f
 
 /* ------------------------------------------------------------------ */
 /*
- * k-means++ seeding (Arthur and Vassilvitskii, SODA 2007; the paper's
- * initialisation options): the first centre is row floor(u_0 N); centre t is
- * drawn with probability proportional to D(x)^2, the squared distance of a
- * row to its nearest chosen centre, by inversion of u_t against the running
- * sum of D^2.  The uniforms u are inputs.
+ * k-means++ seeding (Arthur and Vassilvitskii, SODA 2007; the initialisation
+ * the paper compares with its warm start, Sec. 4.5 and App. C): the first
+ * centre is row floor(u_0 N); centre t is drawn with probability
+ * proportional to D(x)^2, the squared distance of a row to its nearest chosen
+ * centre, by inversion of u_t against the running sum of D^2 over the rows in
+ * order: the first row whose running sum exceeds u_t times the total.  The
+ * uniforms u are inputs.  When the total is 0 (every row sits on a chosen
+ * centre) centre t is row floor(u_t N).
  *
- * Orders (part of the definition, so that a parallel implementation can
- * reproduce every decision exactly): D^2 of a row is 16 partial sums in fp64,
- * partial l adding the dimensions l, l + 16, l + 32, ... in order with fused
- * multiply-adds fma(t, t, acc), t = x - c, then combined by four pairwise
- * levels p_l <- p_l + p_(l xor o) for o = 8, 4, 2, 1 (every p_l ends equal);
- * the rows are taken in blocks of KPP_BLOCK = 4096 rows, each block in 256
- * runs of 16 consecutive rows; a run's sum adds its rows in order, a block's
- * sum adds its runs in order, the total adds the blocks in order.  Centre t
- * is the first row whose running sum, accumulated in that same order (blocks,
- * then runs, then rows), exceeds u_t times the total.  When the total is 0
- * (every row sits on a chosen centre) centre t is row floor(u_t N).
+ * margin[t] (optional) is how far the target u_t * total lies inside the
+ * picked row's interval [running sum before it, running sum after it],
+ * divided by the total; +inf for centre 0 and for a zero total.  A method
+ * whose running sums differ from these by rounding alone picks the same row
+ * whenever the difference stays below that margin.
  */
-#define KPP_BLOCK 4096
-#define KPP_RUN 16
-
 static double kpp_dist(const float* x, const float* c, int32_t d) {
-  double p[16], q[16];
-  for (int l = 0; l < 16; ++l) {
-    double acc = 0.0;
-    for (int32_t j = l; j < d; j += 16) {
-      const double t = (double)x[j] - (double)c[j];
-      acc = fma(t, t, acc);
-    }
-    p[l] = acc;
+  double acc = 0.0;
+  for (int32_t j = 0; j < d; ++j) {
+    const double t = (double)x[j] - (double)c[j];
+    acc += t * t;
   }
-  for (int o = 8; o >= 1; o >>= 1) {
-    for (int l = 0; l < 16; ++l) q[l] = p[l] + p[l ^ o];
-    for (int l = 0; l < 16; ++l) p[l] = q[l];
-  }
-  return p[0];
+  return acc;
 }
 
 static int64_t kpp_first(double u, int64_t n) {
@@ -551,59 +537,37 @@ static int64_t kpp_first(double u, int64_t n) {
   return i < 0 ? 0 : (i >= n ? n - 1 : i);
 }
 
-/* idx[k]: the chosen rows; centers[k*d] (may be NULL): their coordinates. */
+/* idx[k]: the chosen rows; centers[k*d] (may be NULL): their coordinates;
+   margin[k] (may be NULL): see above. */
 void oracle_kmeanspp(const float* x, int64_t n, int32_t d, int32_t k, const double* u,
-                     int64_t* idx, float* centers) {
+                     int64_t* idx, float* centers, double* margin) {
   double* dist = (double*)malloc(sizeof(double) * (size_t)n);
-  const int64_t nblk = (n + KPP_BLOCK - 1) / KPP_BLOCK;
-  double* bsum = (double*)malloc(sizeof(double) * (size_t)nblk);
   for (int64_t i = 0; i < n; ++i) dist[i] = INFINITY;
   for (int32_t t = 0; t < k; ++t) {
-    int64_t pick;
-    if (t == 0) {
-      pick = kpp_first(u[0], n);
-    } else {
+    int64_t pick = -1;
+    double mg = INFINITY;
+    if (t > 0) {
       double total = 0.0;
-      for (int64_t b = 0; b < nblk; ++b) {
-        double s = 0.0;
-        for (int64_t r0 = b * KPP_BLOCK; r0 < (b + 1) * KPP_BLOCK && r0 < n; r0 += KPP_RUN) {
-          double rs = 0.0;
-          for (int64_t i = r0; i < r0 + KPP_RUN && i < n; ++i) rs += dist[i];
-          s += rs;
-        }
-        bsum[b] = s;
-        total += s;
-      }
-      if (!(total > 0.0)) {
-        pick = kpp_first(u[t], n);
-      } else {
-        /* the running sum reaches total (same additions in the same order) and
-           u_t < 1, so the block, the run and the row below always exist */
+      for (int64_t i = 0; i < n; ++i) total += dist[i];
+      if (total > 0.0) {
+        /* the running sum below repeats the total's additions, so it reaches
+           the total and, u_t < 1, passes the target at some row */
         const double target = u[t] * total;
         double run = 0.0;
-        int64_t b = 0;
-        while (!(run + bsum[b] > target)) run += bsum[b++];
-        double bs = 0.0;
-        pick = -1;
-        const int64_t bend = (b + 1) * KPP_BLOCK < n ? (b + 1) * KPP_BLOCK : n;
-        for (int64_t r0 = b * KPP_BLOCK; pick < 0 && r0 < bend; r0 += KPP_RUN) {
-          const int64_t r1 = r0 + KPP_RUN < n ? r0 + KPP_RUN : n;
-          double rs = 0.0;
-          for (int64_t i = r0; i < r1; ++i) rs += dist[i];
-          if (!(run + (bs + rs) > target)) {
-            bs += rs;
-            continue;
-          }
-          double ps = 0.0;
-          for (int64_t i = r0; i < r1; ++i) {
-            ps += dist[i];
-            if (run + (bs + ps) > target) { pick = i; break; }
+        for (int64_t i = 0; i < n; ++i) {
+          const double before = run;
+          run += dist[i];
+          if (run > target) {
+            pick = i;
+            mg = fmin(target - before, run - target) / total;
+            break;
           }
         }
-        if (pick < 0) pick = kpp_first(u[t], n);   /* not reached for finite data */
       }
     }
+    if (pick < 0) pick = kpp_first(u[t], n);
     idx[t] = pick;
+    if (margin) margin[t] = mg;
     const float* c = x + pick * (int64_t)d;
     if (centers) memcpy(centers + (int64_t)t * d, c, sizeof(float) * (size_t)d);
     for (int64_t i = 0; i < n; ++i) {
@@ -612,12 +576,11 @@ void oracle_kmeanspp(const float* x, int64_t n, int32_t d, int32_t k, const doub
     }
   }
   free(dist);
-  free(bsum);
 }
 
 /* ------------------------------------------------------------------ */
 /*
- * k-means warm start (the paper's initialisation, App. B: Lloyd iterations
+ * k-means warm start (the paper's initialisation, Sec. 4.4 and App. C: Lloyd iterations
  * from given centres, then EM from the result).  An iteration assigns every
  * row to its nearest centre (squared Euclidean distance summed in fp64 over
  * the dimensions in order; ties to the lower index) and moves every centre

@@ -1,7 +1,8 @@
-"""Pins for the checker's k-means++ seeding: a numpy implementation of the same D^2 inversion
-(plain cumulative sums, a different summation order; equal choices except on rounding
-boundaries, which random uniforms do not hit), the exact D^2 probabilities on a tiny set
-(frequencies over a fine grid of uniforms), and the special cases."""
+"""Pins for the checker's k-means++ seeding (Arthur and Vassilvitskii 2007; the paper's
+alternative initialisation, Sec. 4.5 and App. C): a numpy implementation of the D^2 inversion
+(numpy's own distance sums and cumulative sum; equal choices except on rounding boundaries,
+which random uniforms do not hit), the margins it reports, the exact D^2 probabilities on a
+tiny set (frequencies over a fine grid of uniforms), and the special cases."""
 import numpy as np
 import pytest
 
@@ -59,3 +60,26 @@ def test_special_cases():
     xs = np.ones((50, 3), dtype=np.float32)
     idx, _ = oracle.kmeanspp(xs, 3, np.array([0.5, 0.02, 0.98]))
     np.testing.assert_array_equal(idx, [25, 1, 49])
+
+
+def test_margins_locate_the_target_in_the_picked_interval():
+    """margin[t] = min(target - cum[pick - 1], cum[pick] - target) / total, cum the running
+    sum of D^2 at draw t, checked against numpy's cumulative sums (to rounding)."""
+    rng = np.random.default_rng(11)
+    x = (rng.standard_normal((2000, 6)) * 2.0).astype(np.float32)
+    k = 12
+    u = rng.random(k)
+    idx, _, mg = oracle.kmeanspp(x, k, u, want_margin=True)
+    assert mg[0] == np.inf
+    x64 = x.astype(np.float64)
+    dist = ((x64 - x64[idx[0]]) ** 2).sum(1)
+    for t in range(1, k):
+        c = np.cumsum(dist)
+        target = u[t] * c[-1]
+        i = idx[t]
+        lo = c[i - 1] if i > 0 else 0.0
+        assert lo <= target < c[i]
+        want = min(target - lo, c[i] - target) / c[-1]
+        assert mg[t] == pytest.approx(want, rel=1e-9, abs=1e-12)
+        assert 0.0 < mg[t] <= 0.5 * dist[i] / c[-1] + 1e-15
+        dist = np.minimum(dist, ((x64 - x64[i]) ** 2).sum(1))
