@@ -18,7 +18,8 @@
  *     workspace must be ordered on one stream.  Calls with separate
  *     workspaces (and, for the out-of-core call, separate staging buffers and
  *     copy streams) may run concurrently on different streams: the library
- *     keeps no state between calls apart from the optional phase timer.
+ *     keeps no state between calls apart from the optional phase timer and
+ *     the statistics chunk limit.
  *   - Errors: argument checks run on the host before anything is enqueued and
  *     return a negative gmm_status (nothing is enqueued then).  A HIP error
  *     reported at launch returns GMM_ERR_DEVICE.  NaN or Inf in the inputs is
@@ -26,8 +27,11 @@
  *   - Limits: 1 <= d <= GMM_MAX_D, 1 <= k <= GMM_MAX_K, n >= 1 (n may exceed
  *     2^31), 1 <= m <= GMM_MAX_M.  Shapes beyond them return
  *     GMM_ERR_UNSUPPORTED.
- *   - Results are bitwise deterministic for a given (n, d, k) and inputs: no
- *     atomics; every reduction runs in a fixed order.
+ *   - Results are bitwise deterministic for a given (n, d, k), inputs and
+ *     statistics chunk limit (gmm_set_stats_chunk_limit): every sum runs in a
+ *     fixed order.  The assignment kernels append candidates to per-point
+ *     lists with LDS atomics; each list is sorted before its terms are
+ *     summed, so no result depends on the order of arrival.
  */
 #ifndef FLASHGMM_H
 #define FLASHGMM_H
@@ -105,7 +109,9 @@ int gmm_mstep(const double* nk, const double* s, const double* q, double n_total
               hipStream_t stream);
 
 /*
- * n_iters full EM iterations from Theta_0 = (weights, means, vars), updated
+ * n_iters full EM iterations (Algorithm 1 of the paper, repeated; Sec. 2
+ * stops on a log-likelihood change or an iteration cap, here the cap alone)
+ * from Theta_0 = (weights, means, vars), updated
  * in place to Theta_{n_iters}.  loglik_hist[t] (fp64, device, n_iters
  * entries) receives LL(Theta_t), the log-likelihood computed in iteration
  * t's E-step, before its M-step.  Each iteration is gmm_estep_accumulate
@@ -162,8 +168,9 @@ int gmm_assign_topk(const float* x, int64_t n, int32_t d, int32_t k, const float
                     float* resp, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
- * Out-of-core E-step (data larger than the GPU's memory, Sec. 6 of the paper:
- * X streamed through the device in chunks).  x_host [n*d] fp32 lives in
+ * Out-of-core E-step (data larger than the GPU's memory, the paper's
+ * Limitations section, paragraph Scale: X streamed through the device in
+ * chunks accumulating into the same O(KD) statistics).  x_host [n*d] fp32 lives in
  * page-locked host memory that the caller allocated (hipHostMalloc); the
  * rows are uploaded chunk_rows at a time on copy_stream into the two halves
  * of the caller's device staging buffer staging [2*min(chunk_rows, n)*d fp32],
@@ -184,8 +191,8 @@ int gmm_estep_accumulate_streamed(const float* x_host, int64_t n, int32_t d, int
                                   hipStream_t stream, hipStream_t copy_stream);
 
 /*
- * k-means++ seeding (the paper's initialisation, Sec. 4.1 and App. B; Arthur
- * and Vassilvitskii 2007): D^2 sampling of k rows of x with the caller's
+ * k-means++ seeding (the initialisation the paper compares against its warm
+ * start, Sec. 4.5 and App. C; Arthur and Vassilvitskii 2007): D^2 sampling of k rows of x with the caller's
  * uniforms u[k] (fp64, device, 0 <= u < 1).  Centre 0 is row floor(u_0 n);
  * centre t is the first row whose running sum of D^2 (squared distance to the
  * nearest centre chosen so far) exceeds u_t times the total, the sums taken
@@ -202,8 +209,8 @@ int gmm_estep_accumulate_streamed(const float* x_host, int64_t n, int32_t d, int
 size_t gmm_kmeanspp_workspace_bytes(int64_t n);
 
 /*
- * k-means warm start (the paper's initialisation, App. B: k-means iterations,
- * then EM from the result).  means [k*d] holds the initial centres; n_iters
+ * k-means warm start (the paper's initialisation, Sec. 4.4 and App. C: k-means
+ * iterations, then EM from the result).  means [k*d] holds the initial centres; n_iters
  * Lloyd iterations each assign every row to its nearest centre (squared
  * Euclidean distance, evaluated exactly in the ranking as gmm_assign_topk
  * does with equal weights and unit variances; ties to the lower index) and
@@ -249,6 +256,22 @@ int gmm_fit_iso(const float* x, int64_t n, int32_t d, int32_t k, int32_t n_iters
                 size_t ws_bytes, hipStream_t stream);
 
 /*
+ * Chunking of the dense statistics pass, a tuning control (no part of the
+ * method).  That pass splits the points into chunks, one workgroup per
+ * (64-component block, chunk); a workgroup queues the chunk's points that
+ * need its block, sums their statistics on fp32 MFMA and adds the fp32 sums
+ * into fp64 partials every 4096 queued points; the partials are summed in
+ * chunk order.  The library picks the chunk count from (n, d, k) (about 2048
+ * workgroups); max_chunks > 0 caps it, 0 restores the automatic count.
+ * Fewer, longer chunks change the results by rounding only (the split of the
+ * fp32 runs moves) and never need a larger workspace.  The setting is
+ * process-wide and read when a call is made; calls made under different
+ * settings agree to rounding, not bit for bit.  Returns GMM_OK, or
+ * GMM_ERR_INVALID_ARG for max_chunks < 0.
+ */
+int gmm_set_stats_chunk_limit(int32_t max_chunks);
+
+/*
  * Phase timing of the E-step, a measurement aid (no part of the method).
  * While enabled, every E-step (gmm_estep_accumulate, each iteration of
  * gmm_fit) records HIP events on its stream between its phases, waits for the
@@ -258,8 +281,9 @@ int gmm_fit_iso(const float* x, int64_t n, int32_t d, int32_t k, int32_t n_iters
  *   2  dense statistics of the well-conditioned components (k_stats_well /
  *      k_stats_wide)
  *   3  statistics of the stored exact pairs (k_sparse_*, k_stats_sparse)
- *   4  routed components and the fixed-order reductions (k_stats_ill,
- *      k_reduce_stats, k_reduce_ll)
+ *   4  routed components, the exact recomputation of the components that
+ *      hold little mass, and the fixed-order reductions (k_stats_ill,
+ *      k_small_mass, k_small_list, k_reduce_stats, k_reduce_ll)
  * gmm_timing_enable(on) switches it on (creating the events on the current
  * device at first use) or off, and zeroes the totals.  gmm_timing_read copies
  * the first n_phases totals (ms; phases past GMM_TIMING_PHASES read 0) and the

@@ -30,7 +30,8 @@ EXPORTS = ("gmm_status_string", "gmm_workspace_bytes", "gmm_estep_accumulate", "
            "gmm_kmeans",
            "gmm_estep_accumulate_streamed",
            "gmm_estep_accumulate_iso", "gmm_mstep_iso", "gmm_fit_iso", "gmm_timing_enable",
-           "gmm_timing_read", "gmm_estep_accumulate_screened", "gmm_fit_screened")
+           "gmm_timing_read", "gmm_estep_accumulate_screened", "gmm_fit_screened",
+           "gmm_set_stats_chunk_limit")
 
 _lib = None
 
@@ -94,6 +95,8 @@ def load_library():
     lib.gmm_timing_enable.restype = ctypes.c_int
     lib.gmm_timing_read.argtypes = [vp, i32, vp]
     lib.gmm_timing_read.restype = ctypes.c_int
+    lib.gmm_set_stats_chunk_limit.argtypes = [i32]
+    lib.gmm_set_stats_chunk_limit.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -347,3 +350,9 @@ def gmm_timing_read():
         ctypes.cast(ms, ctypes.c_void_p), len(TIMING_PHASES),
         ctypes.cast(ctypes.byref(calls), ctypes.c_void_p)))
     return dict(zip(TIMING_PHASES, list(ms))), calls.value
+
+
+def gmm_set_stats_chunk_limit(max_chunks: int = 0):
+    """Caps the point chunks of the dense statistics pass (0: the automatic count).
+    Process-wide; results change by rounding only."""
+    _check("gmm_set_stats_chunk_limit", load_library().gmm_set_stats_chunk_limit(int(max_chunks)))

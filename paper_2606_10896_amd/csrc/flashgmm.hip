@@ -14,10 +14,14 @@
 //               on MFMA, an online log-sum-exp over all components, one fp32
 //               log-normaliser per point and per-workgroup log-likelihood
 //               partials.
-//   stats       Step 2 of Algorithm 1: the same log-densities recomputed for a
-//               32-component slice, r = 2^(l - log2 Z) kept on chip, and the
-//               statistic contraction r^T [x | x^2] in fp64 on the vector ALU
-//               (exact products), into per-workgroup partials.
+//   stats       Step 2 of Algorithm 1: the same log-densities recomputed on
+//               fp32 MFMA for the (point, 64-component block) pairs that can
+//               hold a responsibility above 2^-64, r = 2^(l - log2 Z) kept in
+//               registers, and the statistic contraction r^T [x | x^2] on fp32
+//               MFMA whose accumulators are added into fp64 partials every 4096
+//               queued points; the few pairs that carry most of a point's
+//               mass are summed exactly in fp64 on the vector ALU (fp32
+//               products are exact in fp64).
 //   reduce      fixed-order fp64 sums of the partials (instead of the paper's
 //               atomics), added into the caller's accumulators.
 //   mstep       closed-form M-step (Eqs. Nk, muk, sig per dimension) in fp64.
@@ -32,7 +36,11 @@
 // as q/n - mu^2, which cancels by a factor mu^2/var that reaches 1e7 for a
 // component collapsing onto one point, beyond any fp32 accumulation.
 //
-// No atomics anywhere: results are bitwise reproducible run to run.
+// Results are bitwise reproducible run to run: every sum runs in a fixed
+// order.  The only atomics are LDS counters with which the assignment
+// kernels append candidates to per-point lists; a list is sorted before its
+// terms are summed, and the fallback's list of points only decides which
+// points a workgroup visits, each point's result being its own.
 
 #include <hip/hip_runtime.h>
 
@@ -2878,6 +2886,24 @@ __global__ __launch_bounds__(256) void k_assign_collect(
     sti[wave][lane] = make_float2(mi, si);
   }
   __syncthreads();
+  // The waves appended the candidates in the order they found them; each
+  // point's list is put in ascending code order, so that the fp64 normaliser
+  // below adds the same terms in the same order on every run.
+  if (tid < PTS) {
+    const int cnt = ccnt[tid];
+    if (cnt <= kACap) {
+      for (int i = 1; i < cnt; ++i) {
+        const int v = cand[tid][i];
+        int j = i - 1;
+        while (j >= 0 && cand[tid][j] > v) {
+          cand[tid][j + 1] = cand[tid][j];
+          --j;
+        }
+        cand[tid][j + 1] = v;
+      }
+    }
+  }
+  __syncthreads();
   if (lane < PTS) {
     // exact fp64 log-densities of the candidates, spread over the waves
     const int p = lane;
@@ -3058,13 +3084,90 @@ __device__ __forceinline__ double sum_strided(const double* __restrict__ p, int 
   return acc;
 }
 
+// ---------------------------------------------------------------- light components
+// A component that holds little mass in a call can have its variance carried
+// by a few pairs outside the point's stored exact ones: a component sitting on
+// one point gets its variance from the tails of other points' responsibilities.
+// The dense pass forms those pairs' log-densities in fp32 with an error of up
+// to about 2^-16 (S + d) log2 units (the expanded form's terms cancel), far
+// too coarse when one pair makes the whole variance.  Every well-conditioned
+// component with 0 < N_k < kSmallMass in the fast passes therefore has its
+// statistics recomputed over every point in the direct form (fp64 sums,
+// k_stats_ill), and those replace the fast passes' ones.  A component with
+// more mass spreads its variance over enough pairs that their independent
+// rounding errors stay well inside the variance tolerance.
+constexpr double kSmallMass = 64.0;
+
+// flag[slot] = 1 for the well slots whose fast-pass mass is in (0, kSmallMass)
+// (live components only: a dead one has log pi = -inf).
+__global__ __launch_bounds__(256) void k_small_mass(
+    const double* __restrict__ part_w, const double* __restrict__ part_s,
+    const int* __restrict__ counts, const int* __restrict__ well_idx,
+    const double* __restrict__ cdir, int nch, int wbk, int nparts, int sbk, int D64,
+    unsigned char* __restrict__ flag) {
+  const int slot = blockIdx.x * blockDim.x + threadIdx.x;
+  if (slot >= counts[0]) return;
+  const size_t stride = 1 + 2 * (size_t)D64;
+  const double* p = part_w + ((size_t)(slot / wbk) * nch * wbk + (slot % wbk)) * stride;
+  double m = sum_strided(p, nch, (size_t)wbk * stride, 0.0);
+  const double* ps = part_s + ((size_t)(slot / sbk) * nparts * sbk + (slot % sbk)) * stride;
+  m = sum_strided(ps, nparts, (size_t)sbk * stride, m);
+  const bool live = cdir[well_idx[slot]] > -INFINITY;
+  flag[slot] = (live && m > 0.0 && m < kSmallMass) ? 1 : 0;
+}
+
+// The flagged slots in slot order: pos[slot] = index in the list or -1,
+// idx[i] = the component, cnt[1] = the list's length (cnt[0] = 0), so that
+// (idx, cnt) take the place of (ill_idx, counts) for k_stats_ill.
+__global__ __launch_bounds__(1024) void k_small_list(const unsigned char* __restrict__ flag,
+                                                     const int* __restrict__ counts,
+                                                     const int* __restrict__ well_idx,
+                                                     int* __restrict__ pos, int* __restrict__ idx,
+                                                     int* __restrict__ cnt) {
+  __shared__ int wsum[16];
+  const int nw = counts[0];
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int per = (nw + 1023) / 1024;
+  const int a = t * per < nw ? t * per : nw;
+  const int b = a + per < nw ? a + per : nw;
+  int c = 0;
+  for (int sl = a; sl < b; ++sl) c += flag[sl];
+  int inc = c;
+  for (int o = 1; o < 64; o <<= 1) {
+    const int v = __shfl_up(inc, o);
+    if (lane >= o) inc += v;
+  }
+  if (lane == 63) wsum[wave] = inc;
+  __syncthreads();
+  int before = 0, total = 0;
+  for (int w = 0; w < 16; ++w) {
+    if (w < wave) before += wsum[w];
+    total += wsum[w];
+  }
+  int p = before + inc - c;
+  for (int sl = a; sl < b; ++sl) {
+    if (flag[sl]) {
+      pos[sl] = p;
+      idx[p] = well_idx[sl];
+      ++p;
+    } else {
+      pos[sl] = -1;
+    }
+  }
+  if (t == 0) {
+    cnt[0] = 0;
+    cnt[1] = total;
+  }
+}
+
 __global__ __launch_bounds__(256) void k_reduce_stats(
     const double* __restrict__ part_w, const double* __restrict__ part_s,
     const double* __restrict__ part_i,
     const int* __restrict__ counts, const int* __restrict__ well_idx,
     const int* __restrict__ ill_idx, int nch, int wbk, int nparts, int sbk, int grid_i, int ibk,
-    int ipt, int64_t n, int k, int d, int D64, double* __restrict__ nk, double* __restrict__ s,
-    double* __restrict__ q) {
+    int ipt, int64_t n, int k, int d, int D64, const int* __restrict__ small_pos,
+    const double* __restrict__ part_x, const int* __restrict__ small_cnt,
+    double* __restrict__ nk, double* __restrict__ s, double* __restrict__ q) {
   const int64_t width = 1 + 2 * (int64_t)d;
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= 2 * (int64_t)k * width) return;
@@ -3078,11 +3181,20 @@ __global__ __launch_bounds__(256) void k_reduce_stats(
   if (which == 0) {
     if (slot >= counts[0]) return;
     comp = well_idx[slot];
-    const double* p = part_w + ((size_t)(slot / wbk) * nch * wbk + (slot % wbk)) * stride + off;
-    acc = sum_strided(p, nch, (size_t)wbk * stride, acc);
-    const double* ps =
-        part_s + ((size_t)(slot / sbk) * nparts * sbk + (slot % sbk)) * stride + off;
-    acc = sum_strided(ps, nparts, (size_t)sbk * stride, acc);
+    const int xp = small_pos != nullptr ? small_pos[slot] : -1;
+    if (xp >= 0) {
+      // a light component: its exact recomputation replaces the fast passes
+      const int n_xkb = (small_cnt[1] + ibk - 1) / ibk;
+      const int nchk = ill_chunks(grid_i, n_xkb, n, ipt);
+      const double* p = part_x + ((size_t)(xp / ibk) * nchk * ibk + (xp % ibk)) * stride + off;
+      acc = sum_strided(p, nchk, (size_t)ibk * stride, acc);
+    } else {
+      const double* p = part_w + ((size_t)(slot / wbk) * nch * wbk + (slot % wbk)) * stride + off;
+      acc = sum_strided(p, nch, (size_t)wbk * stride, acc);
+      const double* ps =
+          part_s + ((size_t)(slot / sbk) * nparts * sbk + (slot % sbk)) * stride + off;
+      acc = sum_strided(ps, nparts, (size_t)sbk * stride, acc);
+    }
   } else {
     if (slot >= counts[1]) return;
     comp = ill_idx[slot];
@@ -3418,8 +3530,13 @@ struct Layout {
   size_t off_counts, off_cls, off_cwell, off_cdir, off_cthr, off_thr, off_well_idx, off_ill_idx,
       off_cw, off_wp, off_wq, off_wpb, off_dmu, off_dh, off_logz2, off_cslot, off_cr, off_llpart,
       off_part_w, off_part_s, off_part_i, off_scnt, off_soff, off_slist, off_bmask, off_fit_nk,
-      off_fit_s, off_fit_q, off_iso_var, off_iso_q, off_iflag, total;
+      off_fit_s, off_fit_q, off_iso_var, off_iso_q, off_iflag, off_sflag, off_spos, off_sidx,
+      off_scnt2, off_part_x, total;
 };
+
+// Process-wide cap on the number of point chunks of the dense statistics pass
+// (0: the automatic count).  Set by gmm_set_stats_chunk_limit.
+int g_stats_chunk_cap = 0;
 
 // Padded dimension count of the kernels: a multiple of 64 up to 256, of 128 above.
 inline int padded_d(int d) { return d <= 256 ? (int)cdiv(d, 64) * 64 : (int)cdiv(d, 128) * 128; }
@@ -3451,6 +3568,12 @@ bool make_layout(int64_t n, int d, int k, int m, Layout* L) {
     int64_t c = cdiv(n, 1024);
     if (c > maxc) c = maxc;
     L->nch = (int)(c < 1 ? 1 : c);
+  }
+  {
+    // the caller's cap on the chunk count (gmm_set_stats_chunk_limit); fewer,
+    // longer chunks never need more workspace
+    const int cap = g_stats_chunk_cap;
+    if (cap > 0 && L->nch > cap) L->nch = cap;
   }
   L->chunk = cdiv(n, L->nch);
   L->sbk = L->wide ? (L->D64 <= 512 ? 8 : 4) : (L->D64 <= 128 ? 32 : 16);
@@ -3503,6 +3626,13 @@ bool make_layout(int64_t n, int d, int k, int m, Layout* L) {
   L->off_slist = take((size_t)n * kT * sizeof(SPair));
   L->off_bmask = take(L->bmask_on ? (size_t)n * sizeof(unsigned long long) : 16);
   L->off_iflag = take((size_t)n);                // points with a routed component's mass
+  // light components recomputed exactly: flags, list positions, the list, its
+  // length and the partials of its k_stats_ill pass
+  L->off_sflag = take((size_t)k);
+  L->off_spos = take((size_t)k * sizeof(int));
+  L->off_sidx = take((size_t)k * sizeof(int));
+  L->off_scnt2 = take(16 * sizeof(int));
+  L->off_part_x = take((size_t)L->grid_i * L->ibk * stride * sizeof(double));
   L->off_fit_nk = take((size_t)k * sizeof(double) + sizeof(double));  // + loglik slot
   L->off_fit_s = take((size_t)k * d * sizeof(double));
   L->off_fit_q = take((size_t)k * d * sizeof(double));
@@ -3664,11 +3794,26 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
   tm = phase_mark(4, st) && tm;
   hipLaunchKernelGGL(k_stats_ill<D64>, dim3((unsigned)L.grid_i), dim3(256), 0, st, x, n, d, vec4,
                      ill_idx, dmu, dh, cdir, counts, logz2, iflag, part_i);
+  int* spos = nullptr;
+  double* part_x = at<double>(ws, L.off_part_x);
+  int* scnt2 = at<int>(ws, L.off_scnt2);
+  if (L.refine) {
+    // light components: the exact recomputation over every point
+    unsigned char* sflag = at<unsigned char>(ws, L.off_sflag);
+    spos = at<int>(ws, L.off_spos);
+    int* sidx = at<int>(ws, L.off_sidx);
+    hipLaunchKernelGGL(k_small_mass, dim3((unsigned)cdiv(k, 256)), dim3(256), 0, st, part_w,
+                       part_s, counts, well_idx, cdir, L.nch, L.wbk, L.nparts, L.sbk, D64, sflag);
+    hipLaunchKernelGGL(k_small_list, dim3(1), dim3(1024), 0, st, sflag, counts, well_idx, spos,
+                       sidx, scnt2);
+    hipLaunchKernelGGL(k_stats_ill<D64>, dim3((unsigned)L.grid_i), dim3(256), 0, st, x, n, d,
+                       vec4, sidx, dmu, dh, cdir, scnt2, logz2, nullptr, part_x);
+  }
   {
     const int64_t tot = 2 * (int64_t)k * (1 + 2 * (int64_t)d);
     hipLaunchKernelGGL(k_reduce_stats, dim3((unsigned)cdiv(tot, 256)), dim3(256), 0, st, part_w,
                        part_s, part_i, counts, well_idx, ill_idx, L.nch, L.wbk, L.nparts, L.sbk,
-                       L.grid_i, L.ibk, L.ipt, n, k, d, D64, nk, s, q);
+                       L.grid_i, L.ibk, L.ipt, n, k, d, D64, spos, part_x, scnt2, nk, s, q);
   }
   hipLaunchKernelGGL(k_reduce_ll, dim3(1), dim3(1024), 0, st, llpart, L.n_wg_logz, loglik,
                      ll_accumulate);
@@ -3835,6 +3980,12 @@ int gmm_timing_read(double* ms, int32_t n_phases, int64_t* calls) {
   if (!ms || !calls || n_phases < 0) return GMM_ERR_INVALID_ARG;
   for (int i = 0; i < n_phases; ++i) ms[i] = i < GMM_TIMING_PHASES ? g_timer.ms[i] : 0.0;
   *calls = g_timer.calls;
+  return GMM_OK;
+}
+
+int gmm_set_stats_chunk_limit(int32_t max_chunks) {
+  if (max_chunks < 0) return GMM_ERR_INVALID_ARG;
+  g_stats_chunk_cap = max_chunks;
   return GMM_OK;
 }
 

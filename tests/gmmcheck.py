@@ -230,3 +230,46 @@ def check_assign(gidx, gresp, ref, m, tau, label="", min_checked=0.9):
     assert checked0 >= min_checked * n, \
         f"{label}: only {checked0 / n:.3f} of the rank-1 entries are decisive"
     return checked / (n * m)
+
+
+# ---- depth of the dense statistics pass's fp32 runs
+FOLD_POINTS = 4096   # queued points per fp32 run before the sums move into fp64
+
+
+def queue_lower_bound(x, w, mu, var, chunk_rows, block=64, skip_top=8, window=50.0,
+                      batch=20000):
+    """A lower bound, per (64-component block, chunk of chunk_rows consecutive points), of the
+    points the dense statistics pass queues for the block: the points holding a pair with
+    r > 2^-window in the block that is not among the point's skip_top largest (the GPU stores
+    its four largest exact pairs and leaves them out of the dense pass; every other pair above
+    2^-64, up to the screening error of a few log2 units, marks its block).  Log-densities in
+    fp64 by the expanded form with numpy (errors far below the 14 log2 units of slack between
+    2^-50 and 2^-64).  Returns the largest count over (block, chunk)."""
+    x = np.asarray(x, dtype=np.float64)
+    n, d = x.shape
+    k = mu.shape[0]
+    iv = 1.0 / var.astype(np.float64)
+    m64 = mu.astype(np.float64)
+    with np.errstate(divide="ignore"):
+        c = np.log(w.astype(np.float64)) - 0.5 * (np.log(2 * np.pi * var.astype(np.float64)).sum(1)
+                                                  + (m64 * m64 * iv).sum(1))
+    nb = (k + block - 1) // block
+    nch = (n + chunk_rows - 1) // chunk_rows
+    cnt = np.zeros((nb, nch), dtype=np.int64)
+    for a in range(0, n, batch):
+        xb = x[a:a + batch]
+        l = c[None, :] + xb @ (m64 * iv).T - 0.5 * ((xb * xb) @ iv.T)
+        mx = l.max(1, keepdims=True)
+        lz = mx + np.log(np.exp(l - mx).sum(1, keepdims=True))
+        lr2 = (l - lz) / np.log(2.0)
+        top = np.argpartition(-lr2, skip_top, axis=1)[:, :skip_top]
+        sig = lr2 > -window
+        sig[np.arange(xb.shape[0])[:, None], top] = False
+        pad = nb * block - k
+        if pad:
+            sig = np.concatenate([sig, np.zeros((sig.shape[0], pad), bool)], axis=1)
+        marked = sig.reshape(sig.shape[0], nb, block).any(2)          # [rows, blocks]
+        ch = (np.arange(a, a + xb.shape[0]) // chunk_rows)
+        for j in np.unique(ch):
+            cnt[:, j] += marked[ch == j].sum(0)
+    return int(cnt.max())

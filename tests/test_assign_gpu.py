@@ -103,3 +103,24 @@ def test_deterministic():
     a = gpu_assign(x, *th0, 2, 0.125)
     b = gpu_assign(x, *th0, 2, 0.125)
     assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+
+
+def test_deterministic_many_waves():
+    """Bitwise identical results over repeated calls when every wave of the collection pass
+    appends candidates (K = 512: four 32-component blocks per wave) and routed components
+    (collapsed variances) append theirs too: the candidates are summed in a fixed order."""
+    w = g.custom("adet", 20000, 96, 64, 512, data_seed=21, init_seed=2021)
+    x, (wt, mu, var) = g.make(w)
+    rng = np.random.default_rng(4)
+    var = var.copy()
+    mu = mu.copy()
+    for c in rng.choice(512, 12, replace=False):
+        var[c] = rng.uniform(1e-5, 1e-3, var.shape[1]).astype(np.float32)
+        mu[c] = x[rng.integers(0, x.shape[0])] + np.float32(1e-3)
+    th = (wt, mu, var)
+    a = _run(x, th, 2, 1.0 / 512, "K=512 + routed", min_checked=0.9)
+    for rep in range(4):
+        b = gpu_assign(x, *th, 2, 1.0 / 512)
+        assert np.array_equal(a[0], b[0]), f"indices differ on repeat {rep}"
+        assert np.array_equal(a[1].view(np.uint32), b[1].view(np.uint32)), \
+            f"responsibilities differ on repeat {rep}"

@@ -53,7 +53,9 @@ def test_workspace_is_o_n_plus_o_kd(n, d, k):
     well_part = row * max(8 * kpad, 2048 * 64)
     sparse_part = row * max(kpad, 2048 * 32)
     ill_part = row * max(kpad + 32, 512 * 32)
-    okd = well_part + sparse_part + ill_part + 40 * kpad * dp + 8 * 2 * k * d
+    # the routed components' partials, and as many for the exact recomputation of the light
+    # components (plus their flags, list positions and list: 9 bytes per component)
+    okd = well_part + sparse_part + 2 * ill_part + 40 * kpad * dp + 8 * 2 * k * d + 9 * k
     per_pt = (104 if kpad <= 4096 else 96) + 1   # + a byte: the routed-component flag
     assert nb <= per_pt * n + n // 4 + okd + 64 * k + (4 << 20)
     if n >= 10 ** 6 and k >= 1024:
@@ -200,3 +202,18 @@ def test_timing_switch_and_read_on_the_host():
     assert lib.gmm_timing_read(ctypes.cast(ms, ctypes.c_void_p), -1,
                                ctypes.cast(ctypes.byref(calls_c), ctypes.c_void_p)) == -1
 
+
+
+def test_stats_chunk_limit_is_checked_and_never_grows_the_workspace():
+    lib = gmm.load_library()
+    assert lib.gmm_set_stats_chunk_limit(-1) == gmm.GMM_ERR_INVALID_ARG
+    auto = gmm.workspace_bytes(1_000_000, 128, 1024)
+    try:
+        for cap in (1, 16, 100000):
+            assert lib.gmm_set_stats_chunk_limit(cap) == gmm.GMM_OK
+            assert 0 < gmm.workspace_bytes(1_000_000, 128, 1024) <= auto
+        assert lib.gmm_set_stats_chunk_limit(1) == gmm.GMM_OK
+        assert gmm.workspace_bytes(1_000_000, 128, 1024) < auto
+    finally:
+        assert lib.gmm_set_stats_chunk_limit(0) == gmm.GMM_OK
+    assert gmm.workspace_bytes(1_000_000, 128, 1024) == auto
