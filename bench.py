@@ -109,8 +109,22 @@ def gpu_clocks():
         return None
 
 
+def cpu_model():
+    """The host CPU's model name from /proc/cpuinfo (None when it cannot be read)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(w, mix, theta, sample_rows, iso=False):
-    """The fp64 checker on the first `sample_rows` rows, one full EM iteration, scaled to N."""
+    """The fp64 checker on the first `sample_rows` rows, one full EM iteration, scaled to N.
+    It runs on ORACLE_THREADS host threads: the CPU share one GPU is given on the machines this
+    is measured on (16), whatever the host's core count."""
     import oracle
     x = mix.rows(0, sample_rows, nthreads=max(1, min(16, os.cpu_count() or 1)))
     nthreads = oracle.default_threads()
@@ -118,9 +132,10 @@ def cpu_baseline(w, mix, theta, sample_rows, iso=False):
     (oracle.iso_iterate if iso else oracle.iterate)(x, *theta, nthreads=nthreads)
     dt = time.time() - t0
     return {"value": dt * 1e3 * (w.n / sample_rows), "unit": "ms/iter", "cores": nthreads,
-            "kind": "oracle",
+            "kind": "oracle", "host_cpus": os.cpu_count(), "cpu_model": cpu_model(),
             "sample": f"one EM iteration (E-step, M-step, second sweep) over rows 0..{sample_rows} "
-                      f"of the same data at Theta_0, {dt:.2f} s wall, scaled by N/{sample_rows}"}
+                      f"of the same data at Theta_0 on {nthreads} threads (the host's CPU share "
+                      f"per GPU), {dt:.2f} s wall, scaled by N/{sample_rows}"}
 
 
 COPY_BYTES = 2 << 30
@@ -207,6 +222,56 @@ def measured_traffic(workload, key="logz_bytes_per_launch"):
     return t.get(key)
 
 
+def bench_assign(args, w, x, th0, dev):
+    """gmm_assign_topk with m = 2, tau = 1/K over all N points (the paper's multi-assignment,
+    Sec. 4.3) at the parameters after the fit; timed with HIP events on the stream it runs on."""
+    import numpy as np
+    import torch
+    import paper_2606_10896_amd as gmm
+    k, d = w.k, w.d
+    stream = torch.cuda.current_stream()
+    wt, mu, var = (torch.from_numpy(a).to(dev) for a in th0)
+    n_fit = w.iters if args.assign_fit < 0 else args.assign_fit
+    if n_fit > 0:
+        ws = gmm.workspace(w.n, d, k, device=dev)
+        hist = torch.zeros(n_fit, dtype=torch.float64, device=dev)
+        gmm.gmm_fit(x, wt, mu, var, n_fit, hist, ws, stream=stream)
+        torch.cuda.synchronize()
+        log(f"  fit: {n_fit} iterations, LL {hist[-1].item():.6e}")
+        del ws
+        torch.cuda.empty_cache()
+    m, tau = 2, 1.0 / k
+    wsa = gmm.workspace(w.n, d, k, m, device=dev)
+    idx = torch.empty((w.n, m), dtype=torch.int32, device=dev)
+    resp = torch.empty((w.n, m), dtype=torch.float32, device=dev)
+    for _ in range(max(args.warmup, 1)):
+        gmm.gmm_assign_topk(x, wt, mu, var, m, tau, idx, resp, wsa, stream=stream)
+    torch.cuda.synchronize()
+    steps = max(args.steps, 1)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        gmm.gmm_assign_topk(x, wt, mu, var, m, tau, idx, resp, wsa, stream=stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    kept2 = int((idx[:, 1] >= 0).sum().item())
+    flop = 4.0 * w.n * k * d                  # log-densities of every (point, component) pair
+    rate = flop / (ms * 1e-3) / 1e12
+    print(json.dumps({
+        "metric": "gmm_assign_topk time (m=2, tau=1/K)", "value": round(ms, 3), "unit": "ms",
+        "higher_is_better": False, "n_gpus": 1, "steps": steps, "data": "synthetic",
+        "config": {"workload": f"{w.name}: top-2 multi-assignment after {n_fit} EM iterations, "
+                               f"N={w.n}, D={d}, K={k}", "n": w.n, "d": d, "k": k, "m": m,
+                   "tau": tau},
+        "second_rank_kept": kept2,
+        "roofline": {"bound": "mfma", "kernel": "k_assign_theta + k_assign_collect (4*N*K*D flop "
+                     "of log-densities, fp32 MFMA peak; both passes screen every pair)",
+                     "achieved": round(rate, 2), "peak": FP32_MFMA_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(rate / FP32_MFMA_PEAK_TFLOPS, 4)}}),
+          flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -219,6 +284,12 @@ def main():
     ap.add_argument("--kmeanspp", action="store_true",
                     help="time only the k-means++ seeding of the workload's K centres (one JSON "
                          "line, not the EM metric)")
+    ap.add_argument("--assign", action="store_true",
+                    help="time gmm_assign_topk (m = 2, tau = 1/K, Sec. 4.3) over all N points "
+                         "after --assign-fit EM iterations from the initialisation (one JSON "
+                         "line, not the EM metric)")
+    ap.add_argument("--assign-fit", type=int, default=-1, metavar="ITERS",
+                    help="EM iterations before the timed assignment (-1: the workload's own)")
     ap.add_argument("--rows", type=int, default=0,
                     help="take only the first ROWS rows of the workload (0 = all of them)")
     ap.add_argument("--stream-chunk", type=int, default=0,
@@ -232,7 +303,11 @@ def main():
                     help="exact E-step (default, the reported value) or the reduced-precision "
                          "one (gmm_estep_accumulate_screened: screened log-densities for every "
                          "pair, looser tolerances)")
-    ap.add_argument("--cpu-sample", type=int, default=100_000,
+    ap.add_argument("--from-init", type=int, default=-1, metavar="ITERS",
+                    help="after the timed steps, also time ITERS iterations of one gmm_fit call "
+                         "from the initialisation (-1: the workload's own iteration count, "
+                         "0: skip)")
+    ap.add_argument("--cpu-sample", type=int, default=1_000_000,
                     help="rows of the CPU-baseline slice (0 = skip)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only copy a 2 GiB device buffer once (the reference for the HBM byte "
@@ -307,6 +382,9 @@ def main():
                                      "lloyd_iterations": args.kmeans},
                           "ms_per_assignment": round(ms / (args.kmeans + 1), 3)}), flush=True)
         return
+    if args.assign:
+        bench_assign(args, w, x, th0, dev)
+        return
     iso = args.covariance == "iso"
     if iso:   # isotropic start: the mean over the dimensions of the init variances
         th0 = (th0[0], th0[1], th0[2].astype(np.float64).mean(1).astype(np.float32))
@@ -377,11 +455,14 @@ def main():
     log(f"  phases (ms per E-step): {phases}")
     flops = 8.0 * w.n * k * d
     dense_rate = flops / (estep_ms * 1e-3) / 1e12
-    # dominant kernel: k_logz, 4 N K D flop of log-densities per launch
+    # dominant kernel: k_logz, its log-density contraction per launch: [x | x^2] against
+    # [W | P] (depth 2D) for the diagonal model, 4 N K D flop; [x | ||x||^2] against
+    # [mu / var | -1/(2 var)] (depth D + 1) for the isotropic one, 2 N K (D + 1) flop
     logz_ms = phases["logz"]
     logz_b16 = padded_d(d) <= 128
     logz_peak = BF16_MFMA_PEAK_TFLOPS if logz_b16 else FP32_MFMA_PEAK_TFLOPS
-    logz_alg = 4.0 * w.n * k * d / (logz_ms * 1e-3) / 1e12
+    logz_flop = 2.0 * w.n * k * (d + 1) if iso else 4.0 * w.n * k * d
+    logz_alg = logz_flop / (logz_ms * 1e-3) / 1e12
     dominant = max(phases, key=phases.get)
     result = {
         "metric": METRIC,
@@ -405,7 +486,8 @@ def main():
                    "precision": ("screened: split-bf16 log-densities for every pair, no fp64 "
                                  "refinement" if screened else "exact")},
         "roofline": {"bound": "mfma",
-                     "kernel": "k_logz (4*N*K*D flop of log-densities per launch, "
+                     "kernel": "k_logz (" + ("2*N*K*(D+1)" if iso else "4*N*K*D")
+                               + " flop of log-densities per launch, "
                                + ("bf16 MFMA peak; 3 bf16 products per fp32 product"
                                   if logz_b16 else "fp32 MFMA peak") + ")",
                      "achieved": round(logz_alg, 2), "peak": logz_peak, "unit": "TFLOP/s",
@@ -425,6 +507,24 @@ def main():
     if args.stream_chunk > 0:
         result["config"]["x_residency"] = (f"pinned host memory, uploaded in chunks of {rows} rows "
                                            "(PCIe-inclusive rate)")
+    n_init = w.iters if args.from_init < 0 else args.from_init
+    if n_init > 0 and args.stream_chunk == 0:
+        # the whole trajectory from Theta_0 (the first iterations cost more than later ones)
+        wt0, mu0, var0 = (torch.from_numpy(a).to(dev) for a in th0)
+        hist = torch.zeros(n_init, dtype=torch.float64, device=dev)
+        fit = (gmm.gmm_fit_iso if iso else gmm.gmm_fit_screened if screened else gmm.gmm_fit)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        fit(x, wt0, mu0, var0, n_init, hist, ws, var_floor=1e-6, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        tot = e0.elapsed_time(e1)
+        result["from_init"] = {"iterations": n_init, "ms_total": round(tot, 2),
+                               "ms_per_iter": round(tot / n_init, 3),
+                               "note": "one gmm_fit call over iterations 0.." + str(n_init - 1)
+                                       + " from the random-point initialisation"}
+        log(f"  from init: {n_init} iterations in {tot:.1f} ms")
     result["gpu_clocks"] = gpu_clocks()
     if args.cpu_sample > 0:
         log("  cpu baseline ...")
