@@ -2535,7 +2535,8 @@ __global__ __launch_bounds__(256) void k_stats_ill(
     const float* __restrict__ dmu, const double* __restrict__ dh,
     const double* __restrict__ cdir, const int* __restrict__ counts,
     const double* __restrict__ logz2, const unsigned char* __restrict__ iflag,
-    double* __restrict__ part) {
+    const unsigned long long* __restrict__ bmask, const unsigned short* __restrict__ cslot,
+    const unsigned char* __restrict__ sflag, double* __restrict__ part) {
   constexpr int P = D64 + 4, NJ = D64 / 64, STRIDE = 1 + 2 * D64;
   constexpr int PT = ill_pt(D64), CW = ill_cw(D64), ICB = 4 * CW;
   constexpr int WIN = 16 * 256;                 // points scanned per queue window
@@ -2564,7 +2565,14 @@ __global__ __launch_bounds__(256) void k_stats_ill(
   // Only the points whose flag says a routed component holds more than 2^-60
   // of them (every point when iflag is null) are taken: windows of WIN points
   // are scanned, flagged points queued in order, and tiles of PT queued points
-  // gathered (the queue's rest moves to its front).
+  // gathered (the queue's rest moves to its front).  For the light components
+  // (sflag given: their well slots flagged, counts[2..3] the 64-bit mask of
+  // their 64-slot blocks) a point is taken when its dense-block mask has one
+  // of those blocks or one of its stored exact pairs is a light component: at
+  // every other point each of them has r < 2^-64 (every point when the
+  // masks are off, bmask null).
+  const unsigned long long lmask =
+      sflag != nullptr ? *reinterpret_cast<const unsigned long long*>(counts + 2) : 0ull;
   int qn = 0;
   for (int64_t wb0 = p0; wb0 < p1; wb0 += WIN) {
     const int64_t we = wb0 + WIN < p1 ? wb0 + WIN : p1;
@@ -2574,7 +2582,17 @@ __global__ __launch_bounds__(256) void k_stats_ill(
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int64_t pt = a + e;
-        if (pt < we && (iflag == nullptr || iflag[pt] != 0)) sel |= 1u << e;
+        bool take = pt < we;
+        if (take && iflag != nullptr) take = iflag[pt] != 0;
+        if (take && sflag != nullptr && bmask != nullptr) {
+          bool hit = (bmask[pt] & lmask) != 0ull;
+          const ushort4 sl = *reinterpret_cast<const ushort4*>(cslot + pt * kT);
+          const int v4[4] = {sl.x, sl.y, sl.z, sl.w};
+#pragma unroll
+          for (int j = 0; j < kT; ++j) hit = hit || (v4[j] != kNoSlot && sflag[v4[j]] != 0);
+          take = hit;
+        }
+        if (take) sel |= 1u << e;
       }
       const int cnt = __popc(sel);
       int inc = cnt;
@@ -3154,9 +3172,20 @@ __global__ __launch_bounds__(1024) void k_small_list(const unsigned char* __rest
       pos[sl] = -1;
     }
   }
+  // 64-bit mask of the 64-slot blocks holding light slots (counts[2..3])
+  unsigned long long bm = 0ull;
+  for (int sl = a; sl < b; ++sl)
+    if (flag[sl]) bm |= 1ull << ((sl >> 6) & 63);
+  for (int o = 32; o > 0; o >>= 1) bm |= __shfl_xor(bm, o);
+  __shared__ unsigned long long wbm[16];
+  if (lane == 0) wbm[wave] = bm;
+  __syncthreads();
   if (t == 0) {
+    unsigned long long all = 0ull;
+    for (int w = 0; w < 16; ++w) all |= wbm[w];
     cnt[0] = 0;
     cnt[1] = total;
+    *reinterpret_cast<unsigned long long*>(cnt + 2) = all;
   }
 }
 
@@ -3541,7 +3570,11 @@ int g_stats_chunk_cap = 0;
 // Padded dimension count of the kernels: a multiple of 64 up to 256, of 128 above.
 inline int padded_d(int d) { return d <= 256 ? (int)cdiv(d, 64) * 64 : (int)cdiv(d, 128) * 128; }
 
-bool make_layout(int64_t n, int d, int k, int m, Layout* L) {
+void layout_offsets(Layout* L);
+
+// budget > 0: shrink the split counts until the workspace fits in `budget`
+// bytes (false if it cannot).
+bool make_layout(int64_t n, int d, int k, int m, Layout* L, size_t budget = 0) {
   if (n < 1 || d < 1 || k < 1 || d > GMM_MAX_D || k > GMM_MAX_K || m < 0 || m > GMM_MAX_M)
     return false;
   L->n = n; L->d = d; L->k = k; L->m = m;
@@ -3585,18 +3618,55 @@ bool make_layout(int64_t n, int d, int k, int m, Layout* L) {
     if (u > cap) u = cap;
     L->nunit = (int)(u < 1 ? 1 : u);
     L->upts = cdiv(n, L->nunit);
-    int pp = 2048 / L->nb;
-    L->nparts = pp < 1 ? 1 : pp;
+    // about 2048 workgroups for the exact pairs, but no more parts than a few
+    // hundred stored pairs each would fill
+    int64_t pp = 2048 / L->nb;
+    const int64_t by_pairs = cdiv(n * kT, (int64_t)L->nb * 256);
+    if (pp > by_pairs) pp = by_pairs;
+    L->nparts = (int)(pp < 1 ? 1 : pp);
   }
   L->ipt = L->D64 <= 256 ? 64 : (L->D64 <= 512 ? 32 : 16);
   L->ibk = 4 * (L->D64 <= 256 ? 8 : (L->D64 <= 512 ? 4 : 2));
   {
-    const int nib = (int)cdiv(k, L->ibk);
-    L->grid_i = nib > 512 ? nib : 512;
+    // at least one workgroup per block of routed components; about 512 in all,
+    // but no more chunks than tiles of points
+    const int64_t nib = cdiv(k, L->ibk);
+    int64_t g = nib * cdiv(n, L->ipt);
+    if (g > 512) g = 512;
+    L->grid_i = (int)(g > nib ? g : nib);
   }
   L->pts_logz = L->D64 <= 256 ? 64 : 32;
   L->n_wg_logz = cdiv(n, L->pts_logz);
   L->bmask_on = L->kpad / kWB <= 64;
+  layout_offsets(L);
+  if (budget > 0) {
+    // fewer chunks of the dense statistics, fewer parts of the exact pairs and
+    // fewer chunks of the routed components (each a change of summation
+    // splits only) until the workspace fits the budget
+    const int nib = (int)cdiv(k, L->ibk);
+    while (L->total > budget) {
+      if (L->nch > 1) {
+        L->nch = (L->nch + 1) / 2;
+        L->chunk = cdiv(n, L->nch);
+      } else if (L->nparts > 1) {
+        L->nparts = (L->nparts + 1) / 2;
+      } else if (L->grid_i > nib) {
+        L->grid_i = (L->grid_i + 1) / 2 > nib ? (L->grid_i + 1) / 2 : nib;
+      } else {
+        return false;
+      }
+      layout_offsets(L);
+    }
+  }
+  return true;
+}
+
+// Byte offsets of the workspace regions for the layout's sizes.
+void layout_offsets(Layout* L) {
+  const int64_t n = L->n;
+  const int d = L->d, k = L->k;
+  const int stride = 1 + 2 * L->D64;
+  const int nwb = L->kpad / L->wbk;
   size_t o = 0;
   auto take = [&](size_t bytes) { const size_t r = o; o = align256(o + bytes); return r; };
   L->off_counts = take(16 * sizeof(int));
@@ -3640,7 +3710,6 @@ bool make_layout(int64_t n, int d, int k, int m, Layout* L) {
   L->off_iso_var = take((size_t)k * d * sizeof(float));
   L->off_iso_q = take((size_t)k * sizeof(double));
   L->total = o;
-  return true;
 }
 
 template <typename T>
@@ -3793,7 +3862,8 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
   }
   tm = phase_mark(4, st) && tm;
   hipLaunchKernelGGL(k_stats_ill<D64>, dim3((unsigned)L.grid_i), dim3(256), 0, st, x, n, d, vec4,
-                     ill_idx, dmu, dh, cdir, counts, logz2, iflag, part_i);
+                     ill_idx, dmu, dh, cdir, counts, logz2, iflag, nullptr, nullptr, nullptr,
+                     part_i);
   int* spos = nullptr;
   double* part_x = at<double>(ws, L.off_part_x);
   int* scnt2 = at<int>(ws, L.off_scnt2);
@@ -3807,7 +3877,8 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
     hipLaunchKernelGGL(k_small_list, dim3(1), dim3(1024), 0, st, sflag, counts, well_idx, spos,
                        sidx, scnt2);
     hipLaunchKernelGGL(k_stats_ill<D64>, dim3((unsigned)L.grid_i), dim3(256), 0, st, x, n, d,
-                       vec4, sidx, dmu, dh, cdir, scnt2, logz2, nullptr, part_x);
+                       vec4, sidx, dmu, dh, cdir, scnt2, logz2, nullptr, bmask, cslot, sflag,
+                       part_x);
   }
   {
     const int64_t tot = 2 * (int64_t)k * (1 + 2 * (int64_t)d);
