@@ -256,6 +256,27 @@ int gmm_fit_iso(const float* x, int64_t n, int32_t d, int32_t k, int32_t n_iters
                 size_t ws_bytes, hipStream_t stream);
 
 /*
+ * gmm_estep_accumulate without a workspace argument, for callers that cannot
+ * allocate device memory (code under stream capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments (minus ws / ws_bytes),
+ * semantics and status codes as gmm_estep_accumulate; the library's own
+ * 64 MiB device array (one per GPU, held until the process ends) serves as
+ * the workspace, and the call allocates and frees nothing.  The split counts
+ * of the statistics passes shrink until the workspace fits those 64 MiB, so
+ * the results can differ from gmm_estep_accumulate's by rounding; shapes
+ * whose per-point buffers (about 110 bytes a point) and O(k d) arrays cannot
+ * fit return GMM_ERR_WORKSPACE before anything is enqueued: at d = 128,
+ * k = 1024 calls of up to 480,240 points fit (larger data sets are
+ * accumulated over row chunks); at d = 768, k = 4096 the O(k d) arrays alone
+ * exceed the array.  Calls that overlap on one GPU share the array and race:
+ * order them on one stream.
+ */
+int gmm_estep_accumulate_static(const float* x, int64_t n, int32_t d, int32_t k,
+                                const float* weights, const float* means, const float* vars,
+                                double* nk, double* s, double* q, double* loglik,
+                                hipStream_t stream);
+
+/*
  * Chunking of the dense statistics pass, a tuning control (no part of the
  * method).  That pass splits the points into chunks, one workgroup per
  * (64-component block, chunk); a workgroup queues the chunk's points that

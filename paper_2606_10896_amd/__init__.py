@@ -31,7 +31,7 @@ EXPORTS = ("gmm_status_string", "gmm_workspace_bytes", "gmm_estep_accumulate", "
            "gmm_estep_accumulate_streamed",
            "gmm_estep_accumulate_iso", "gmm_mstep_iso", "gmm_fit_iso", "gmm_timing_enable",
            "gmm_timing_read", "gmm_estep_accumulate_screened", "gmm_fit_screened",
-           "gmm_set_stats_chunk_limit")
+           "gmm_set_stats_chunk_limit", "gmm_estep_accumulate_static")
 
 _lib = None
 
@@ -95,6 +95,9 @@ def load_library():
     lib.gmm_timing_enable.restype = ctypes.c_int
     lib.gmm_timing_read.argtypes = [vp, i32, vp]
     lib.gmm_timing_read.restype = ctypes.c_int
+    lib.gmm_estep_accumulate_static.argtypes = [vp, i64, i32, i32, vp, vp, vp, vp, vp, vp, vp,
+                                                vp]
+    lib.gmm_estep_accumulate_static.restype = ctypes.c_int
     lib.gmm_set_stats_chunk_limit.argtypes = [i32]
     lib.gmm_set_stats_chunk_limit.restype = ctypes.c_int
     _lib = lib
@@ -356,3 +359,21 @@ def gmm_set_stats_chunk_limit(max_chunks: int = 0):
     """Caps the point chunks of the dense statistics pass (0: the automatic count).
     Process-wide; results change by rounding only."""
     _check("gmm_set_stats_chunk_limit", load_library().gmm_set_stats_chunk_limit(int(max_chunks)))
+
+
+def gmm_estep_accumulate_static(x, weights, means, variances, nk, s, q, loglik, stream=None):
+    """gmm_estep_accumulate with the library's own static device workspace (no workspace
+    argument, nothing allocated); raises GMMError(GMM_ERR_WORKSPACE) for shapes it cannot
+    hold."""
+    import torch
+    _dev(x, torch.float32, "x")
+    n, d = x.shape
+    k = weights.shape[0]
+    rc = load_library().gmm_estep_accumulate_static(
+        _ptr(x), n, d, k, _ptr(_dev(weights, torch.float32, "weights", k)),
+        _ptr(_dev(means, torch.float32, "means", k * d)),
+        _ptr(_dev(variances, torch.float32, "vars", k * d)),
+        _ptr(_dev(nk, torch.float64, "nk", k)), _ptr(_dev(s, torch.float64, "s", k * d)),
+        _ptr(_dev(q, torch.float64, "q", k * d)), _ptr(_dev(loglik, torch.float64, "loglik", 1)),
+        _stream(stream))
+    _check("gmm_estep_accumulate_static", rc)

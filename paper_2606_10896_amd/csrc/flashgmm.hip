@@ -48,6 +48,7 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <mutex>
 #include <type_traits>
 
 #include "flashgmm.h"
@@ -4031,9 +4032,61 @@ struct StreamEvents {
   }
 };
 
+// ---------------------------------------------------------------- allocation-free E-step
+// The workspace of gmm_estep_accumulate_static: an array of the library's
+// code object, one per GPU, which that GPU holds until the process ends.  Host
+// code never uses the array's name as an address: its device address on each
+// GPU comes from hipGetSymbolAddress, taken once per device with the device
+// current.  Every call on a GPU uses the same array, so calls that overlap on
+// one GPU race; nothing in it needs to start at zero (every region is written
+// before it is read within a call).
+constexpr size_t kStaticScratchBytes = (size_t)64 << 20;
+constexpr int kStaticMaxDevices = 64;
+__device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+struct StaticScratch {
+  std::mutex mu;
+  void* ptr[kStaticMaxDevices] = {};
+};
+StaticScratch g_static;
+
+// The device address of `scratch` on the current device (looked up on the
+// device's first call, then reused).
+int static_scratch(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kStaticMaxDevices)
+    return GMM_ERR_DEVICE;
+  std::lock_guard<std::mutex> lock(g_static.mu);
+  if (g_static.ptr[dev] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr)
+      return GMM_ERR_DEVICE;
+    g_static.ptr[dev] = p;
+  }
+  *out = g_static.ptr[dev];
+  return GMM_OK;
+}
+
 }  // namespace
 
 extern "C" {
+
+int gmm_estep_accumulate_static(const float* x, int64_t n, int32_t d, int32_t k,
+                                const float* weights, const float* means, const float* vars,
+                                double* nk, double* s, double* q, double* loglik,
+                                hipStream_t stream) {
+  int rc = check_shape(n, d, k);
+  if (rc != GMM_OK) return rc;
+  if (!x || !weights || !means || !vars || !nk || !s || !q || !loglik) return GMM_ERR_INVALID_ARG;
+  Layout L;
+  // the split counts shrink until the workspace fits the static array; a
+  // shape whose per-point buffers alone exceed it is refused
+  if (!make_layout(n, d, k, 0, &L, kStaticScratchBytes)) return GMM_ERR_WORKSPACE;
+  void* ws = nullptr;
+  rc = static_scratch(&ws);
+  if (rc != GMM_OK) return rc;
+  return estep_dispatch(L, x, weights, means, vars, nk, s, q, loglik, 1, ws, stream);
+}
 
 int gmm_timing_enable(int on) {
   if (on && !g_timer.made) {

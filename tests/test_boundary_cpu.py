@@ -217,3 +217,19 @@ def test_stats_chunk_limit_is_checked_and_never_grows_the_workspace():
     finally:
         assert lib.gmm_set_stats_chunk_limit(0) == gmm.GMM_OK
     assert gmm.workspace_bytes(1_000_000, 128, 1024) == auto
+
+
+def test_static_estep_refuses_shapes_beyond_its_array_before_any_launch():
+    """gmm_estep_accumulate_static: a shape whose workspace cannot fit the library's 64 MiB
+    array is refused on the host (GMM_ERR_WORKSPACE), whatever the pointers; null pointers are
+    invalid arguments."""
+    lib = gmm.load_library()
+    f = _fake()
+    assert lib.gmm_estep_accumulate_static(f, 480_241, 128, 1024, f, f, f, f, f, f, f,
+                                           None) == gmm.GMM_ERR_WORKSPACE
+    assert lib.gmm_estep_accumulate_static(f, 1000, 768, 4096, f, f, f, f, f, f, f,
+                                           None) == gmm.GMM_ERR_WORKSPACE
+    assert lib.gmm_estep_accumulate_static(None, 1000, 16, 8, f, f, f, f, f, f, f,
+                                           None) == gmm.GMM_ERR_INVALID_ARG
+    assert lib.gmm_estep_accumulate_static(f, 0, 16, 8, f, f, f, f, f, f, f,
+                                           None) == gmm.GMM_ERR_INVALID_ARG
