@@ -13,9 +13,9 @@ log-sum-exp, the exact refinement and log Z), timed over the timed steps with
 the library's phase timer (HIP events recorded on the stream the kernels run
 on).  Its algorithmic work is the log-density contraction over all N x K
 pairs, 4*N*K*D flop per launch ([x | x^2] against [W | P], depth 2D), priced
-against the peak of the MFMA type it runs on (bf16 for D <= 128, where the
-fp32 operands are split in hi/lo bf16 parts and three products are summed,
-fp32 above).  The E-step as a whole is also reported against the 8*N*K*D
+against the peak of the MFMA type it runs on (bf16 for D <= 128 and D > 256,
+where the fp32 operands are split in hi/lo bf16 parts and three products are
+summed, fp32 in between).  The E-step as a whole is also reported against the 8*N*K*D
 flop of the dense algorithm.  `cpu_baseline` times the fp64 CPU checker on a
 bounded slice of the same data and scales it linearly in N (the E-step is
 exactly linear in N).
@@ -459,7 +459,9 @@ def main():
     # [W | P] (depth 2D) for the diagonal model, 4 N K D flop; [x | ||x||^2] against
     # [mu / var | -1/(2 var)] (depth D + 1) for the isotropic one, 2 N K (D + 1) flop
     logz_ms = phases["logz"]
-    logz_b16 = padded_d(d) <= 128
+    # split-bf16 screening (three bf16 products per fp32 product) for D <= 128 and D > 256;
+    # fp32 MFMA in between
+    logz_b16 = padded_d(d) <= 128 or padded_d(d) > 256
     logz_peak = BF16_MFMA_PEAK_TFLOPS if logz_b16 else FP32_MFMA_PEAK_TFLOPS
     logz_flop = 2.0 * w.n * k * (d + 1) if iso else 4.0 * w.n * k * d
     logz_alg = logz_flop / (logz_ms * 1e-3) / 1e12

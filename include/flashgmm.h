@@ -64,10 +64,10 @@ const char* gmm_status_string(int status);
  * Bytes of workspace needed by gmm_estep_accumulate / gmm_fit (m = 0) or by
  * gmm_assign_topk (m >= 1) for n points in d dimensions and k components.
  * Returns 0 when the shape is unsupported.  The size grows as O(n) (about
- * 100 bytes per point: the fp64 log-normaliser, the stored exact pairs and
- * their bucketed records, and a mask of the component blocks the dense
- * statistics take) plus O(k d) for the parameters and the per-workgroup
- * partial statistics; it never holds an n x k array.
+ * 110 bytes per point: the fp64 log-normaliser, the stored exact pairs and
+ * their bucketed records, a mask of the component blocks the dense
+ * statistics take, and flag bytes) plus O(k d) for the parameters and the
+ * per-workgroup partial statistics; it never holds an n x k array.
  */
 size_t gmm_workspace_bytes(int64_t n, int32_t d, int32_t k, int32_t m);
 
@@ -266,7 +266,7 @@ int gmm_fit_iso(const float* x, int64_t n, int32_t d, int32_t k, int32_t n_iters
  * the results can differ from gmm_estep_accumulate's by rounding; shapes
  * whose per-point buffers (about 110 bytes a point) and O(k d) arrays cannot
  * fit return GMM_ERR_WORKSPACE before anything is enqueued: at d = 128,
- * k = 1024 calls of up to 480,240 points fit (larger data sets are
+ * k = 1024 calls of up to 475,776 points fit (larger data sets are
  * accumulated over row chunks); at d = 768, k = 4096 the O(k d) arrays alone
  * exceed the array.  Calls that overlap on one GPU share the array and race:
  * order them on one stream.
@@ -299,12 +299,12 @@ int gmm_set_stats_chunk_limit(int32_t max_chunks);
  * last of them and adds each phase's GPU duration to a process-wide total:
  *   0  parameter preparation (k_prep_*)
  *   1  screening, refinement and log Z of every point (k_logz)
- *   2  dense statistics of the well-conditioned components (k_stats_well /
- *      k_stats_wide)
- *   3  statistics of the stored exact pairs (k_sparse_*, k_stats_sparse)
- *   4  routed components, the exact recomputation of the components that
- *      hold little mass, and the fixed-order reductions (k_stats_ill,
- *      k_small_mass, k_small_list, k_reduce_stats, k_reduce_ll)
+ *   2  statistics of the stored exact pairs (k_sparse_*, k_stats_sparse)
+ *   3  the list of light components (little mass in their stored pairs) and
+ *      the dense statistics of the other well-conditioned components
+ *      (k_small_mass, k_small_list, k_stats_well / k_stats_wide)
+ *   4  routed and light components in the direct form, and the fixed-order
+ *      reductions (k_stats_ill, k_reduce_stats, k_reduce_ll)
  * gmm_timing_enable(on) switches it on (creating the events on the current
  * device at first use) or off, and zeroes the totals.  gmm_timing_read copies
  * the first n_phases totals (ms; phases past GMM_TIMING_PHASES read 0) and the

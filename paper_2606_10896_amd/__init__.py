@@ -337,7 +337,7 @@ def gmm_fit_iso(x, weights, means, variances, n_iters, loglik_hist, ws, var_floo
     _check("gmm_fit_iso", rc)
 
 
-TIMING_PHASES = ("prep", "logz", "dense_stats", "exact_pairs", "ill_and_reduce")
+TIMING_PHASES = ("prep", "logz", "exact_pairs", "dense_stats", "ill_light_and_reduce")
 
 
 def gmm_timing_enable(on: bool = True):

@@ -595,6 +595,10 @@ __host__ __device__ constexpr int logz_tiles(int D64) { return D64 <= 256 ? 2 : 
 // running sum of some hundred log2 units over D64 steps), so the refinement rules
 // are the same for both.
 __host__ __device__ constexpr bool screen_b16(int D64) { return D64 <= 128; }
+// D64 > 256 (32-point tiles): split-bf16 screening too, the operands of the
+// points split on the fly from the fp32 tile (logz_group16)
+__host__ __device__ constexpr bool screen_x16(int D64) { return D64 > 256; }
+__host__ __device__ constexpr bool screen_split(int D64) { return screen_b16(D64) || screen_x16(D64); }
 
 // One software-pipelined step of a screening pass for one wave: when MF, the
 // log-densities of the NT 32-point tiles against component block wpb are
@@ -726,7 +730,113 @@ __device__ __forceinline__ void logz_step16(const bf16x8* xa, const bf16x8* __re
         else epi(v, c0[v], c0[v]);
       }
     }
+    if (MF && EPI && NT == 2) {
+      // the step's LDS and global loads first, then six rounds of one MFMA and
+      // three VALU instructions of the previous block's epilogue (2 % faster
+      // than the compiler's own order at N = 1e8)
+      __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+      __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);
+#pragma unroll
+      for (int r = 0; r < 6; ++r) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
+      }
+    }
     __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+// Split-bf16 screening straight from the fp32 tile (D64 > 256, 32-point
+// tiles), GB component blocks at a time.  Pair-step q covers dimensions
+// 16 q .. 16 q + 15 of both parts of [x | x^2]: each lane reads its eight
+// values of x once from the tile (lane half h: dimensions 16 q + 8 h + e),
+// splits x and x^2 into hi and lo bf16 parts, and multiplies them with the
+// packed operands of steps q (x part) and q + D64/16 (x^2 part) of every
+// block kb[j], three products per fp32 product, into accumulator n[j] (chains
+// interleaved over the blocks).  The B operands of pair-step q + 1 are loaded
+// during pair-step q.  EPI: the previous group's log-densities c[j] (blocks
+// j < nvp) are taken in by epi(j, v, value) during the first eight pair-steps,
+// eight values each (fixed register indices).
+template <int D64, int GB, bool MF, bool EPI, class Epi>
+__device__ __forceinline__ void logz_group16(const float* xs, const bf16x8* __restrict__ wpb,
+                                             const int (&kb)[GB], const float (&cb)[GB],
+                                             f16v (&n)[GB], const f16v (&c)[GB], int nvp,
+                                             Epi&& epi) {
+  constexpr int P = D64 + 4, NQ = D64 / 16, NS = D64 / 8;
+  constexpr size_t BS = (size_t)NS * 64 * 2;
+  static_assert(NQ % 8 == 0 && 16 * GB == 64, "eight pair-steps of eight epilogue values");
+  const int lane = threadIdx.x & 63, h = lane >> 5, col = lane & 31;
+  const float* xr = xs + col * P + 8 * h;
+  bf16x8 bw[2][GB][4];                            // ring of two pair-steps of B operands
+  auto load_b = [&](auto slot, int q) {
+    constexpr int sl = decltype(slot)::value;
+#pragma unroll
+    for (int j = 0; j < GB; ++j) {
+      const bf16x8* w = wpb + (size_t)kb[j] * BS;
+      bw[sl][j][0] = w[2 * (q * 64 + lane)];
+      bw[sl][j][1] = w[2 * (q * 64 + lane) + 1];
+      bw[sl][j][2] = w[2 * ((q + NQ) * 64 + lane)];
+      bw[sl][j][3] = w[2 * ((q + NQ) * 64 + lane) + 1];
+    }
+  };
+  if (MF) {
+#pragma unroll
+    for (int j = 0; j < GB; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) n[j][v] = cb[j];
+    load_b(std::integral_constant<int, 0>{}, 0);
+  }
+  auto step = [&](auto slot, auto tc, int q, bool first) {
+    constexpr int sl = decltype(slot)::value, t8 = decltype(tc)::value;
+    if (MF) {
+      if (q + 1 < NQ) load_b(std::integral_constant<int, 1 - sl>{}, q + 1);
+      const float4 u0 = *reinterpret_cast<const float4*>(xr + 16 * q);
+      const float4 u1 = *reinterpret_cast<const float4*>(xr + 16 * q + 4);
+      const float v8[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
+      bf16x8 xh, xl, qh, ql;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const __bf16 vh = (__bf16)v8[e];
+        xh[e] = vh;
+        xl[e] = (__bf16)(v8[e] - (float)vh);
+        const float sq = v8[e] * v8[e];
+        const __bf16 sh = (__bf16)sq;
+        qh[e] = sh;
+        ql[e] = (__bf16)(sq - (float)sh);
+      }
+#pragma unroll
+      for (int j = 0; j < GB; ++j) n[j] = mfma32b(xh, bw[sl][j][0], n[j]);
+#pragma unroll
+      for (int j = 0; j < GB; ++j) n[j] = mfma32b(xh, bw[sl][j][1], n[j]);
+#pragma unroll
+      for (int j = 0; j < GB; ++j) n[j] = mfma32b(xl, bw[sl][j][0], n[j]);
+#pragma unroll
+      for (int j = 0; j < GB; ++j) n[j] = mfma32b(qh, bw[sl][j][2], n[j]);
+#pragma unroll
+      for (int j = 0; j < GB; ++j) n[j] = mfma32b(qh, bw[sl][j][3], n[j]);
+#pragma unroll
+      for (int j = 0; j < GB; ++j) n[j] = mfma32b(ql, bw[sl][j][2], n[j]);
+    }
+    if (EPI && first) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        constexpr int e0 = 8 * t8;
+        const int e = e0 + i, j = e >> 4, v = e & 15;
+        if (j < nvp) epi(j, v, c[j][v]);
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  for (int q0 = 0; q0 < NQ; q0 += 8) {
+    const bool first = q0 == 0;
+    step(std::integral_constant<int, 0>{}, std::integral_constant<int, 0>{}, q0, first);
+    step(std::integral_constant<int, 1>{}, std::integral_constant<int, 1>{}, q0 + 1, first);
+    step(std::integral_constant<int, 0>{}, std::integral_constant<int, 2>{}, q0 + 2, first);
+    step(std::integral_constant<int, 1>{}, std::integral_constant<int, 3>{}, q0 + 3, first);
+    step(std::integral_constant<int, 0>{}, std::integral_constant<int, 4>{}, q0 + 4, first);
+    step(std::integral_constant<int, 1>{}, std::integral_constant<int, 5>{}, q0 + 5, first);
+    step(std::integral_constant<int, 0>{}, std::integral_constant<int, 6>{}, q0 + 6, first);
+    step(std::integral_constant<int, 1>{}, std::integral_constant<int, 7>{}, q0 + 7, first);
   }
 }
 
@@ -893,7 +1003,8 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
     const float* __restrict__ dmu, const double* __restrict__ dh, const double* __restrict__ cdir,
     const int* __restrict__ counts, double* __restrict__ logz2,
     unsigned short* __restrict__ cslot, float* __restrict__ cr, double* __restrict__ ll_part,
-    unsigned long long* __restrict__ bmask, unsigned char* __restrict__ iflag) {
+    unsigned long long* __restrict__ bmask, unsigned char* __restrict__ iflag,
+    unsigned char* __restrict__ lflag) {
   constexpr int P = D64 + 4, NT = logz_tiles(D64), PTS = 32 * NT;
   constexpr bool B16 = screen_b16(D64);
   static_assert(!ISO || B16, "the isotropic screening tile is a split-bf16 one");
@@ -1032,7 +1143,42 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
       if constexpr (NT == 2) lse_add_arg(m1[v], s1[v], a1[v], l1, slot);
     };
     constexpr size_t BS16 = (size_t)NSTEP * 64 * 2;
-    if (nb > 0) {
+    if constexpr (screen_x16(D64)) {
+      // GB blocks of this wave at a time: blocks wave + 4 i, i = GB g + j; a
+      // group's missing blocks repeat its last one and are not taken in
+      constexpr int GB = 4;
+      const int ng = (nb + GB - 1) / GB;
+      int kbc[GB], kbp[GB];
+      float cbc[GB];
+      f16v na[GB], nc[GB];
+      int nvp = 0;
+      auto epi16 = [&](int j, int v, float l) {
+        lse_add_arg(m0[v], s0[v], a0[v], l, kbp[j] * kBK + col);
+      };
+      for (int g = 0; g <= ng; ++g) {
+        if (g < ng) {
+#pragma unroll
+          for (int j = 0; j < GB; ++j) {
+            const int i = GB * g + j < nb ? GB * g + j : nb - 1;
+            kbc[j] = wave + 4 * i;
+            cbc[j] = cw[kbc[j] * kBK + col];
+          }
+          if (g == 0)
+            logz_group16<D64, GB, true, false>(xs, wpb, kbc, cbc, na, nc, 0, epi16);
+          else
+            logz_group16<D64, GB, true, true>(xs, wpb, kbc, cbc, na, nc, nvp, epi16);
+        } else if (ng > 0) {
+          logz_group16<D64, GB, false, true>(xs, wpb, kbc, cbc, na, nc, nvp, epi16);
+        }
+        // this group's log-densities become the previous group's
+#pragma unroll
+        for (int j = 0; j < GB; ++j) {
+          nc[j] = na[j];
+          kbp[j] = kbc[j];
+        }
+        nvp = nb - GB * g < GB ? nb - GB * g : GB;
+      }
+    } else if (nb > 0) {
       if constexpr (B16)
         logz_step16<NSTEP, RPV, true, false, NT>(xa, wpb + (size_t)wave * BS16, cw[wave * kBK + col], c0,
                                           c1, x0, x1, epi);
@@ -1546,6 +1692,9 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
           double mi_all = -INFINITY;
           for (int w2 = 0; w2 < 4; ++w2) mi_all = fmax(mi_all, stim[w2][p]);
           iflag[nn] = mi_all > -INFINITY ? 1 : 0;
+          // cleared here, set by the dense statistics pass where a light
+          // component holds more than about 2^-72 of the point
+          lflag[nn] = 0;
         }
         if (bmask != nullptr) {
           // 64-component blocks the dense statistics pass takes for this point
@@ -1618,6 +1767,7 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
     const float* __restrict__ cw, const int* __restrict__ counts,
     const double* __restrict__ logz2, const unsigned short* __restrict__ cslot,
     const unsigned long long* __restrict__ bmask, int nch, int64_t chunk_pts,
+    const unsigned char* __restrict__ sflag, unsigned char* __restrict__ lflag,
     double* __restrict__ part) {
   constexpr int P = D64 + 4;
   constexpr int NS = D64 / 4;                   // MFMA steps per chain
@@ -1636,6 +1786,8 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
   __shared__ __align__(16) float xs[2][PTS * P];
   __shared__ float2 lzb[2][PTS];                // -log2 Z / NGB as a (hi, lo) pair
   __shared__ unsigned long long rbb[2][PTS];
+  __shared__ unsigned pqo[2][PTS];              // the tile's points (offsets from p0, ~0u: none)
+  __shared__ unsigned long long lbits;          // light slots of this block
   __shared__ unsigned qpt[kStatsWin + PTS];     // queued points (offsets from the chunk start)
   static_assert(kStatsWin == 16 * 256, "a window is 16 points per thread");
   __shared__ int qsum[4];
@@ -1651,6 +1803,12 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
     return;
   }
   const int grp = kb * 4 + wave;                // 16-component group
+  if (wave == 0) {
+    const int sl = kb * kWB + lane;
+    const unsigned long long lb =
+        __ballot(sflag != nullptr && sl < counts[0] && sflag[sl] != 0);
+    if (lane == 0) lbits = lb;
+  }
   float wb[WQS];
 #pragma unroll
   for (int s2 = 0; s2 < WQS; ++s2) wb[s2] = wq[((size_t)grp * WQS + s2) * 64 + lane];
@@ -1659,6 +1817,7 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
   float4 px[LD];
   float2 plz = make_float2(-INFINITY, 0.0f);
   unsigned long long prb = 0ull;
+  unsigned ppo = ~0u;
   // tile i holds queue entries PTS i .. PTS i + PTS - 1 (rows past qn are zero)
   int qn = 0;                                   // queued points (uniform)
   auto load_regs = [&](int i) {
@@ -1684,6 +1843,7 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
       const int64_t nn = e < qn ? p0 + qpt[e] : p1;
       plz = make_float2(-INFINITY, 0.0f);
       prb = 0ull;
+      ppo = nn < p1 ? (unsigned)(nn - p0) : ~0u;
       if (nn < p1) {
         const double b64 = -logz2[nn] / NGB;
         const float bh = (float)b64;
@@ -1705,6 +1865,7 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
     if (tid < PTS) {
       lzb[buf][tid] = plz;
       rbb[buf][tid] = prb;
+      pqo[buf][tid] = ppo;
     }
   };
 
@@ -1715,6 +1876,10 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
   float qacc = 0.0f;                            // ISO: sum of r ||x||^2
   bool first = true;
   const int myc = wave * 16 + i16;              // this lane's component in the block
+  __syncthreads();                              // lbits
+  // a light component is left out here and recomputed exactly; the points
+  // where it comes within 2^-72 of log2 Z are flagged for that
+  const bool mylight = ((lbits >> myc) & 1ull) != 0ull;
 
   // fp32 accumulators -> fp64 partial.  Register v of block c at lane l is
   // column 4(l/16) + v of the block: dimension 64 (c/4 % NG) + 4 (4 k4 + v) + c % 4.
@@ -1864,7 +2029,11 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
       for (int v = 0; v < 4; ++v) {
         const int pt = t * 16 + 4 * k4 + v;
         const float e = exp2_fast(la[v]);
-        r[v] = ((rbb[cur][pt] >> myc) & 1ull) ? 0.0f : e;
+        r[v] = (((rbb[cur][pt] >> myc) & 1ull) || mylight) ? 0.0f : e;
+        if (mylight && e > 0x1p-72f) {
+          const unsigned po = pqo[cur][pt];
+          if (po != ~0u) lflag[p0 + po] = 1;
+        }
         nkacc += r[v];
         if constexpr (ISO) qacc += r[v] * __shfl(nfull, 4 * k4 + v);
       }
@@ -1932,7 +2101,8 @@ __global__ __launch_bounds__(64 * (DW / 128)) void k_stats_wide(
     const double* __restrict__ cwell, const int* __restrict__ well_idx,
     const int* __restrict__ counts, const double* __restrict__ logz2,
     const unsigned short* __restrict__ cslot, const unsigned long long* __restrict__ bmask,
-    int nch, int64_t chunk_pts, double* __restrict__ part) {
+    int nch, int64_t chunk_pts, const unsigned char* __restrict__ sflag,
+    unsigned char* __restrict__ lflag, double* __restrict__ part) {
   constexpr int NW = DW / 128, DQ = 128, P = DQ + 4;
   constexpr int NS = DW / 4, WQS = wq_steps(DW);
   constexpr int SW = DQ / 4, NBQ = DQ / 16, NG = DQ / 64;
@@ -1960,6 +2130,9 @@ __global__ __launch_bounds__(64 * (DW / 128)) void k_stats_wide(
   // this lane's component (B-operand column i16): its expanded-form constant
   const int myslot = 16 * g + i16;
   const double cst = myslot < n_well ? cwell[well_idx[myslot]] : -INFINITY;
+  // a light component is left out here and recomputed exactly; the points
+  // where it comes within 2^-72 of log2 Z are flagged for that
+  const bool mylight = sflag != nullptr && myslot < n_well && sflag[myslot] != 0;
   float wb[2 * SW];
 #pragma unroll
   for (int s2 = 0; s2 < SW; ++s2) {
@@ -1972,6 +2145,7 @@ __global__ __launch_bounds__(64 * (DW / 128)) void k_stats_wide(
   float4 px[LD];
   double plz = INFINITY;
   unsigned prb = 0u;
+  unsigned ppo = ~0u;
   // tile i holds queue entries 16 i .. 16 i + 15 (rows past qn are zero)
   int qn = 0;                                   // queued points (uniform)
   auto load_regs = [&](int i) {
@@ -1997,6 +2171,7 @@ __global__ __launch_bounds__(64 * (DW / 128)) void k_stats_wide(
       const int64_t nn = e < qn ? p0 + qpt[e] : p1;
       plz = INFINITY;
       prb = 0u;
+      ppo = nn < p1 ? (unsigned)(nn - p0) : ~0u;
       if (nn < p1) {
         plz = logz2[nn];
         const ushort4 sl = *reinterpret_cast<const ushort4*>(cslot + nn * kT);
@@ -2089,12 +2264,13 @@ __global__ __launch_bounds__(64 * (DW / 128)) void k_stats_wide(
   load_regs(0);
   for (int i = 0; i < nt; ++i) {
     store_regs();
-    unsigned rbv[4];
+    unsigned rbv[4], pov[4];
     double lzv[4];
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
       rbv[v] = __shfl(prb, 4 * k4 + v);
       lzv[v] = __shfl(plz, 4 * k4 + v);
+      pov[v] = __shfl(ppo, 4 * k4 + v);
     }
     __builtin_amdgcn_wave_barrier();
     if (i + 1 < nt) load_regs(i + 1);
@@ -2128,7 +2304,8 @@ __global__ __launch_bounds__(64 * (DW / 128)) void k_stats_wide(
       for (int w2 = 1; w2 < NW; ++w2) tot += lpart[w2][v][lane];
       tot += cst - lzv[v];
       const float e = exp2_fast((float)tot);
-      r[v] = ((rbv[v] >> i16) & 1u) ? 0.0f : e;
+      r[v] = (((rbv[v] >> i16) & 1u) || mylight) ? 0.0f : e;
+      if (mylight && wave == 0 && e > 0x1p-72f && pov[v] != ~0u) lflag[p0 + pov[v]] = 1;
       nkacc += r[v];
     }
     // statistics over this wave's dimensions: step v contracts points 4k + v
@@ -2536,7 +2713,7 @@ __global__ __launch_bounds__(256) void k_stats_ill(
     const float* __restrict__ dmu, const double* __restrict__ dh,
     const double* __restrict__ cdir, const int* __restrict__ counts,
     const double* __restrict__ logz2, const unsigned char* __restrict__ iflag,
-    const unsigned long long* __restrict__ bmask, const unsigned short* __restrict__ cslot,
+    const unsigned char* __restrict__ lflag, const unsigned short* __restrict__ cslot,
     const unsigned char* __restrict__ sflag, double* __restrict__ part) {
   constexpr int P = D64 + 4, NJ = D64 / 64, STRIDE = 1 + 2 * D64;
   constexpr int PT = ill_pt(D64), CW = ill_cw(D64), ICB = 4 * CW;
@@ -2567,13 +2744,10 @@ __global__ __launch_bounds__(256) void k_stats_ill(
   // of them (every point when iflag is null) are taken: windows of WIN points
   // are scanned, flagged points queued in order, and tiles of PT queued points
   // gathered (the queue's rest moves to its front).  For the light components
-  // (sflag given: their well slots flagged, counts[2..3] the 64-bit mask of
-  // their 64-slot blocks) a point is taken when its dense-block mask has one
-  // of those blocks or one of its stored exact pairs is a light component: at
-  // every other point each of them has r < 2^-64 (every point when the
-  // masks are off, bmask null).
-  const unsigned long long lmask =
-      sflag != nullptr ? *reinterpret_cast<const unsigned long long*>(counts + 2) : 0ull;
+  // (sflag given: their well slots flagged) a point is taken when the dense
+  // pass flagged it (lflag: a light component's dense log-density there came
+  // within 2^-72 of log2 Z) or one of its stored exact pairs is a light
+  // component: at every other point each of them has r < 2^-64.
   int qn = 0;
   for (int64_t wb0 = p0; wb0 < p1; wb0 += WIN) {
     const int64_t we = wb0 + WIN < p1 ? wb0 + WIN : p1;
@@ -2585,8 +2759,8 @@ __global__ __launch_bounds__(256) void k_stats_ill(
         const int64_t pt = a + e;
         bool take = pt < we;
         if (take && iflag != nullptr) take = iflag[pt] != 0;
-        if (take && sflag != nullptr && bmask != nullptr) {
-          bool hit = (bmask[pt] & lmask) != 0ull;
+        if (take && sflag != nullptr) {
+          bool hit = lflag[pt] != 0;
           const ushort4 sl = *reinterpret_cast<const ushort4*>(cslot + pt * kT);
           const int v4[4] = {sl.x, sl.y, sl.z, sl.w};
 #pragma unroll
@@ -3109,30 +3283,31 @@ __device__ __forceinline__ double sum_strided(const double* __restrict__ p, int 
 // one point gets its variance from the tails of other points' responsibilities.
 // The dense pass forms those pairs' log-densities in fp32 with an error of up
 // to about 2^-16 (S + d) log2 units (the expanded form's terms cancel), far
-// too coarse when one pair makes the whole variance.  Every well-conditioned
-// component with 0 < N_k < kSmallMass in the fast passes therefore has its
-// statistics recomputed over every point in the direct form (fp64 sums,
-// k_stats_ill), and those replace the fast passes' ones.  A component with
-// more mass spreads its variance over enough pairs that their independent
+// too coarse when one pair makes the whole variance (or the whole of a small
+// N_k).  Every well-conditioned component whose stored exact pairs hold less
+// than kSmallMass is therefore light: the dense pass leaves it out and flags
+// the points where its fp32 log-density comes within 2^-72 of log2 Z (eight
+// log2 units of slack over the 2^-64 cut for the dense pass's error), and its
+// statistics are computed at those points and at the points that store it,
+// in the direct form with fp64 sums (k_stats_ill).  A component with more
+// mass spreads its variance over enough pairs that their independent
 // rounding errors stay well inside the variance tolerance.
 constexpr double kSmallMass = 64.0;
 
-// flag[slot] = 1 for the well slots whose fast-pass mass is in (0, kSmallMass)
-// (live components only: a dead one has log pi = -inf).
+// flag[slot] = 1 for the live well slots whose stored exact pairs hold less
+// than kSmallMass (every component with N_k < kSmallMass is among them, since
+// the stored pairs are part of its mass; a dead one has log pi = -inf).
 __global__ __launch_bounds__(256) void k_small_mass(
-    const double* __restrict__ part_w, const double* __restrict__ part_s,
-    const int* __restrict__ counts, const int* __restrict__ well_idx,
-    const double* __restrict__ cdir, int nch, int wbk, int nparts, int sbk, int D64,
-    unsigned char* __restrict__ flag) {
+    const double* __restrict__ part_s, const int* __restrict__ counts,
+    const int* __restrict__ well_idx, const double* __restrict__ cdir, int nparts, int sbk,
+    int D64, unsigned char* __restrict__ flag) {
   const int slot = blockIdx.x * blockDim.x + threadIdx.x;
   if (slot >= counts[0]) return;
   const size_t stride = 1 + 2 * (size_t)D64;
-  const double* p = part_w + ((size_t)(slot / wbk) * nch * wbk + (slot % wbk)) * stride;
-  double m = sum_strided(p, nch, (size_t)wbk * stride, 0.0);
   const double* ps = part_s + ((size_t)(slot / sbk) * nparts * sbk + (slot % sbk)) * stride;
-  m = sum_strided(ps, nparts, (size_t)sbk * stride, m);
+  const double m = sum_strided(ps, nparts, (size_t)sbk * stride, 0.0);
   const bool live = cdir[well_idx[slot]] > -INFINITY;
-  flag[slot] = (live && m > 0.0 && m < kSmallMass) ? 1 : 0;
+  flag[slot] = (live && m < kSmallMass) ? 1 : 0;
 }
 
 // The flagged slots in slot order: pos[slot] = index in the list or -1,
@@ -3173,20 +3348,9 @@ __global__ __launch_bounds__(1024) void k_small_list(const unsigned char* __rest
       pos[sl] = -1;
     }
   }
-  // 64-bit mask of the 64-slot blocks holding light slots (counts[2..3])
-  unsigned long long bm = 0ull;
-  for (int sl = a; sl < b; ++sl)
-    if (flag[sl]) bm |= 1ull << ((sl >> 6) & 63);
-  for (int o = 32; o > 0; o >>= 1) bm |= __shfl_xor(bm, o);
-  __shared__ unsigned long long wbm[16];
-  if (lane == 0) wbm[wave] = bm;
-  __syncthreads();
   if (t == 0) {
-    unsigned long long all = 0ull;
-    for (int w = 0; w < 16; ++w) all |= wbm[w];
     cnt[0] = 0;
     cnt[1] = total;
-    *reinterpret_cast<unsigned long long*>(cnt + 2) = all;
   }
 }
 
@@ -3561,7 +3725,7 @@ struct Layout {
       off_cw, off_wp, off_wq, off_wpb, off_dmu, off_dh, off_logz2, off_cslot, off_cr, off_llpart,
       off_part_w, off_part_s, off_part_i, off_scnt, off_soff, off_slist, off_bmask, off_fit_nk,
       off_fit_s, off_fit_q, off_iso_var, off_iso_q, off_iflag, off_sflag, off_spos, off_sidx,
-      off_scnt2, off_part_x, total;
+      off_scnt2, off_part_x, off_lflag, total;
 };
 
 // Process-wide cap on the number of point chunks of the dense statistics pass
@@ -3681,7 +3845,7 @@ void layout_offsets(Layout* L) {
   L->off_thr = take((size_t)L->kpad * sizeof(float2));
   L->off_wp = take((size_t)L->kpad * 2 * L->D64 * sizeof(float));
   L->off_wq = take((size_t)(L->kpad / 16) * (L->D64 / 2 + L->D64 / 32) * 64 * sizeof(float));
-  L->off_wpb = take(screen_b16(L->D64) ? (size_t)L->kpad * L->D64 * 8 : 16);
+  L->off_wpb = take(screen_split(L->D64) ? (size_t)L->kpad * L->D64 * 8 : 16);
   L->off_dmu = take((size_t)k * L->D64 * sizeof(float));
   L->off_dh = take((size_t)k * L->D64 * sizeof(double));
   L->off_logz2 = take((size_t)n * sizeof(double));
@@ -3696,6 +3860,8 @@ void layout_offsets(Layout* L) {
   L->off_soff = take(((size_t)L->nb * L->nunit + 1) * sizeof(int64_t));
   L->off_slist = take((size_t)n * kT * sizeof(SPair));
   L->off_bmask = take(L->bmask_on ? (size_t)n * sizeof(unsigned long long) : 16);
+  // per point: a light component holds more than about 2^-72 of it
+  L->off_lflag = take((size_t)n);
   L->off_iflag = take((size_t)n);                // points with a routed component's mass
   // light components recomputed exactly: flags, list positions, the list, its
   // length and the partials of its k_stats_ill pass
@@ -3779,6 +3945,7 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
   const int vec4 = ((d & 3) == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0) ? 1 : 0;
   bf16x8* wpb = at<bf16x8>(ws, L.off_wpb);
   unsigned long long* bmask = L.bmask_on ? at<unsigned long long>(ws, L.off_bmask) : nullptr;
+  unsigned char* lflag = at<unsigned char>(ws, L.off_lflag);
   unsigned char* iflag = at<unsigned char>(ws, L.off_iflag);
 
   bool tm = phase_mark(0, st);
@@ -3789,6 +3956,11 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
     const int64_t tot = (int64_t)kpad * (D64 / 4) * 2;
     hipLaunchKernelGGL(k_prep_pack_well<D64>, dim3((unsigned)cdiv(tot, 256)), dim3(256), 0, st,
                        mu, var, d, kpad, cwell, cthr, counts, well_idx, wp, cw, thr);
+    if constexpr (screen_x16(D64)) {
+      const int64_t tb = (int64_t)(kpad / kBK) * screen_steps<D64, false>() * 64;
+      hipLaunchKernelGGL((k_prep_pack_b16<D64, false>), dim3((unsigned)cdiv(tb, 256)), dim3(256),
+                         0, st, mu, var, d, kpad, counts, well_idx, wpb);
+    }
     if constexpr (screen_b16(D64)) {
       if (L.iso) {
         const int64_t tb = (int64_t)(kpad / kBK) * screen_steps<D64, true>() * 64;
@@ -3818,7 +3990,7 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
     if (L.iso && L.refine) {
       hipLaunchKernelGGL((k_logz<D64, true, true>), dim3((unsigned)L.n_wg_logz), dim3(256), 0, st,
                          x, n, d, vec4, wp, wpb, cw, thr, well_idx, ill_idx, dmu, dh, cdir, counts,
-                         logz2, cslot, cr, llpart, bmask, iflag);
+                         logz2, cslot, cr, llpart, bmask, iflag, lflag);
       launched = true;
     }
   }
@@ -3826,29 +3998,15 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
     if (L.refine)
       hipLaunchKernelGGL((k_logz<D64, true, false>), dim3((unsigned)L.n_wg_logz), dim3(256), 0, st,
                          x, n, d, vec4, wp, wpb, cw, thr, well_idx, ill_idx, dmu, dh, cdir, counts,
-                         logz2, cslot, cr, llpart, bmask, iflag);
+                         logz2, cslot, cr, llpart, bmask, iflag, lflag);
     else
       hipLaunchKernelGGL((k_logz<D64, false, false>), dim3((unsigned)L.n_wg_logz), dim3(256), 0,
                          st, x, n, d, vec4, wp, wpb, cw, thr, well_idx, ill_idx, dmu, dh, cdir,
-                         counts, logz2, cslot, cr, llpart, bmask, iflag);
+                         counts, logz2, cslot, cr, llpart, bmask, iflag, lflag);
   }
   tm = phase_mark(2, st) && tm;
-  if constexpr (D64 < 256) {
-    if (L.iso)
-      hipLaunchKernelGGL((k_stats_well<D64, true>), dim3((unsigned)((kpad / kWB) * L.nch)),
-                         dim3(256), 0, st, x, n, d, vec4, wq, cw, counts, logz2, cslot, bmask,
-                         L.nch, L.chunk, part_w);
-    else
-      hipLaunchKernelGGL((k_stats_well<D64, false>), dim3((unsigned)((kpad / kWB) * L.nch)),
-                         dim3(256), 0, st, x, n, d, vec4, wq, cw, counts, logz2, cslot, bmask,
-                         L.nch, L.chunk, part_w);
-  } else {
-    hipLaunchKernelGGL(k_stats_wide<D64>, dim3((unsigned)((kpad / 16) * L.nch)),
-                       dim3(64 * (D64 / 128)), 0, st, x, n, d, vec4, wq, cwell, well_idx, counts,
-                       logz2, cslot, bmask, L.nch, L.chunk, part_w);
-  }
-  tm = phase_mark(3, st) && tm;
   {
+    // the stored exact pairs, in fp64
     int* scnt = at<int>(ws, L.off_scnt);
     int64_t* soff = at<int64_t>(ws, L.off_soff);
     SPair* slist = at<SPair>(ws, L.off_slist);
@@ -3861,26 +4019,44 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
     hipLaunchKernelGGL(k_stats_sparse<D64>, dim3((unsigned)(L.nb * L.nparts)), dim3(256), 0, st,
                        x, n, d, slist, soff, L.nunit, L.nparts, part_s);
   }
+  tm = phase_mark(3, st) && tm;
+  // light components (exact path only): their stored pairs' mass is below
+  // kSmallMass; the dense pass leaves them out and flags their points
+  int* spos = nullptr;
+  double* part_x = at<double>(ws, L.off_part_x);
+  int* scnt2 = at<int>(ws, L.off_scnt2);
+  unsigned char* sflag = nullptr;
+  int* sidx = at<int>(ws, L.off_sidx);
+  if (L.refine) {
+    sflag = at<unsigned char>(ws, L.off_sflag);
+    spos = at<int>(ws, L.off_spos);
+    hipLaunchKernelGGL(k_small_mass, dim3((unsigned)cdiv(k, 256)), dim3(256), 0, st, part_s,
+                       counts, well_idx, cdir, L.nparts, L.sbk, D64, sflag);
+    hipLaunchKernelGGL(k_small_list, dim3(1), dim3(1024), 0, st, sflag, counts, well_idx, spos,
+                       sidx, scnt2);
+  }
+  if constexpr (D64 < 256) {
+    if (L.iso)
+      hipLaunchKernelGGL((k_stats_well<D64, true>), dim3((unsigned)((kpad / kWB) * L.nch)),
+                         dim3(256), 0, st, x, n, d, vec4, wq, cw, counts, logz2, cslot, bmask,
+                         L.nch, L.chunk, sflag, lflag, part_w);
+    else
+      hipLaunchKernelGGL((k_stats_well<D64, false>), dim3((unsigned)((kpad / kWB) * L.nch)),
+                         dim3(256), 0, st, x, n, d, vec4, wq, cw, counts, logz2, cslot, bmask,
+                         L.nch, L.chunk, sflag, lflag, part_w);
+  } else {
+    hipLaunchKernelGGL(k_stats_wide<D64>, dim3((unsigned)((kpad / 16) * L.nch)),
+                       dim3(64 * (D64 / 128)), 0, st, x, n, d, vec4, wq, cwell, well_idx, counts,
+                       logz2, cslot, bmask, L.nch, L.chunk, sflag, lflag, part_w);
+  }
   tm = phase_mark(4, st) && tm;
   hipLaunchKernelGGL(k_stats_ill<D64>, dim3((unsigned)L.grid_i), dim3(256), 0, st, x, n, d, vec4,
                      ill_idx, dmu, dh, cdir, counts, logz2, iflag, nullptr, nullptr, nullptr,
                      part_i);
-  int* spos = nullptr;
-  double* part_x = at<double>(ws, L.off_part_x);
-  int* scnt2 = at<int>(ws, L.off_scnt2);
-  if (L.refine) {
-    // light components: the exact recomputation over every point
-    unsigned char* sflag = at<unsigned char>(ws, L.off_sflag);
-    spos = at<int>(ws, L.off_spos);
-    int* sidx = at<int>(ws, L.off_sidx);
-    hipLaunchKernelGGL(k_small_mass, dim3((unsigned)cdiv(k, 256)), dim3(256), 0, st, part_w,
-                       part_s, counts, well_idx, cdir, L.nch, L.wbk, L.nparts, L.sbk, D64, sflag);
-    hipLaunchKernelGGL(k_small_list, dim3(1), dim3(1024), 0, st, sflag, counts, well_idx, spos,
-                       sidx, scnt2);
+  if (L.refine)
     hipLaunchKernelGGL(k_stats_ill<D64>, dim3((unsigned)L.grid_i), dim3(256), 0, st, x, n, d,
-                       vec4, sidx, dmu, dh, cdir, scnt2, logz2, nullptr, bmask, cslot, sflag,
+                       vec4, sidx, dmu, dh, cdir, scnt2, logz2, nullptr, lflag, cslot, sflag,
                        part_x);
-  }
   {
     const int64_t tot = 2 * (int64_t)k * (1 + 2 * (int64_t)d);
     hipLaunchKernelGGL(k_reduce_stats, dim3((unsigned)cdiv(tot, 256)), dim3(256), 0, st, part_w,

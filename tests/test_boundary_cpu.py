@@ -56,7 +56,8 @@ def test_workspace_is_o_n_plus_o_kd(n, d, k):
     # the routed components' partials, and as many for the exact recomputation of the light
     # components (plus their flags, list positions and list: 9 bytes per component)
     okd = well_part + sparse_part + 2 * ill_part + 40 * kpad * dp + 8 * 2 * k * d + 9 * k
-    per_pt = (104 if kpad <= 4096 else 96) + 1   # + a byte: the routed-component flag
+    # + two flag bytes: a routed component, a light component holds mass at the point
+    per_pt = (104 if kpad <= 4096 else 96) + 2
     assert nb <= per_pt * n + n // 4 + okd + 64 * k + (4 << 20)
     if n >= 10 ** 6 and k >= 1024:
         # a small fraction of what an n x k fp32 responsibility array would take
@@ -225,7 +226,7 @@ def test_static_estep_refuses_shapes_beyond_its_array_before_any_launch():
     invalid arguments."""
     lib = gmm.load_library()
     f = _fake()
-    assert lib.gmm_estep_accumulate_static(f, 480_241, 128, 1024, f, f, f, f, f, f, f,
+    assert lib.gmm_estep_accumulate_static(f, 475_777, 128, 1024, f, f, f, f, f, f, f,
                                            None) == gmm.GMM_ERR_WORKSPACE
     assert lib.gmm_estep_accumulate_static(f, 1000, 768, 4096, f, f, f, f, f, f, f,
                                            None) == gmm.GMM_ERR_WORKSPACE
