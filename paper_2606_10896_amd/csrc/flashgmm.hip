@@ -1440,20 +1440,28 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
                                     (mv >= s4m[pp] && rel > -(float)kWideWindow));
       if (cand) cbits |= 1u << (16 * blk + v);
       XT[16 * blk + v] = cand ? (full ? sv : 1.0f) * exp2_fast(mv - stw[wave][pp].x) : 0.0f;
-      const unsigned long long bal = __ballot(cand);
-      const unsigned long long balf = __ballot(full);
-      if (col == 0) {
-        cmask[pp][wave] = (unsigned)(bal >> (32 * h));
-        fmask[pp][wave] = (unsigned)(balf >> (32 * h));
-      }
-      if (bmask != nullptr) {
-        const bool sig = av >= 0 && rel > -kDenseWindow;
-        const bool oth = sig && (sv - 1.0f) * exp2_fast(rel) > kDenseMass;
-        const unsigned long long bals = __ballot(sig);
-        const unsigned long long balo = __ballot(oth);
+      const bool sig = bmask != nullptr && av >= 0 && rel > -kDenseWindow;
+      const bool oth = sig && (sv - 1.0f) * exp2_fast(rel) > kDenseMass;
+      if constexpr (B16) {
+        // one flag byte per lane state (IllStage's space is free now); the
+        // (point, wave) masks are assembled from them below
+        unsigned char* fl = smem + IST_OFF;
+        fl[pp * 128 + wave * 32 + col] =
+            (unsigned char)((cand ? 1 : 0) | (full ? 2 : 0) | (sig ? 4 : 0) | (oth ? 8 : 0));
+      } else {
+        const unsigned long long bal = __ballot(cand);
+        const unsigned long long balf = __ballot(full);
         if (col == 0) {
-          smask[pp][wave] = (unsigned)(bals >> (32 * h));
-          omask[pp][wave] = (unsigned)(balo >> (32 * h));
+          cmask[pp][wave] = (unsigned)(bal >> (32 * h));
+          fmask[pp][wave] = (unsigned)(balf >> (32 * h));
+        }
+        if (bmask != nullptr) {
+          const unsigned long long bals = __ballot(sig);
+          const unsigned long long balo = __ballot(oth);
+          if (col == 0) {
+            smask[pp][wave] = (unsigned)(bals >> (32 * h));
+            omask[pp][wave] = (unsigned)(balo >> (32 * h));
+          }
         }
       }
     }
@@ -1465,6 +1473,29 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
   });
   if (NT == 2 || (col & 1) == 0) cms[wave][xpose_point<NT>(col, h)] = XT[0];
   __syncthreads();
+  if constexpr (B16) {
+    // thread (point tid / 4, wave tid % 4): its four 32-bit lane-column masks
+    // from the 32 flag bytes (bit b of byte c goes to bit c of mask b: four
+    // bytes at a time, (w & 0x01010101) * 0x01020408 gathers their bit 0 in
+    // bits 24..27 without carries)
+    static_assert(4 * PTS == 256, "one thread per (point, wave)");
+    const unsigned char* fl = smem + IST_OFF;
+    const int p = tid >> 2, w2 = tid & 3;
+    const uint4 f0 = *reinterpret_cast<const uint4*>(fl + p * 128 + w2 * 32);
+    const uint4 f1 = *reinterpret_cast<const uint4*>(fl + p * 128 + w2 * 32 + 16);
+    const unsigned wd[8] = {f0.x, f0.y, f0.z, f0.w, f1.x, f1.y, f1.z, f1.w};
+    unsigned mk[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+      for (int b = 0; b < 4; ++b)
+        mk[b] |= ((((wd[i] >> b) & 0x01010101u) * 0x01020408u) >> 24) << (4 * i);
+    cmask[p][w2] = mk[0];
+    fmask[p][w2] = mk[1];
+    smask[p][w2] = mk[2];
+    omask[p][w2] = mk[3];
+    __syncthreads();
+  }
   // Refinement, spread over the workgroup: the candidates of (point p, wave
   // w2) are listed in (point, wave, lane column, block) order, every thread
   // computes exact log-densities of list entries (relative to the point's
