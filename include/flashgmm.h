@@ -54,7 +54,8 @@ typedef enum {
   GMM_ERR_INVALID_ARG = -1, /* null pointer, non-positive size, bad m/tau */
   GMM_ERR_UNSUPPORTED = -2, /* d, k or m beyond the library's limits */
   GMM_ERR_WORKSPACE = -3,   /* workspace missing, misaligned or too small */
-  GMM_ERR_DEVICE = -4       /* a HIP call or kernel launch failed */
+  GMM_ERR_DEVICE = -4,      /* a HIP call or kernel launch failed */
+  GMM_ERR_FILL = -5         /* the caller's fill function reported a failure */
 } gmm_status;
 
 /* Human-readable name of a status code (static string). */
@@ -189,6 +190,55 @@ int gmm_estep_accumulate_streamed(const float* x_host, int64_t n, int32_t d, int
                                   double* nk, double* s, double* q, double* loglik,
                                   int64_t chunk_rows, float* staging, void* ws, size_t ws_bytes,
                                   hipStream_t stream, hipStream_t copy_stream);
+
+/*
+ * Source of the rows of an out-of-core E-step: writes rows row0 .. row0 +
+ * rows - 1 of X (fp32, d values a row, row-major) to dst [rows*d], a slot of
+ * the caller's page-locked ring, and returns 0, or non-zero to stop the call.
+ * It runs on the calling thread, in row order, each row exactly once.
+ */
+typedef int (*gmm_fill_fn)(void* user, int64_t row0, int64_t rows, int32_t d, float* dst);
+
+/*
+ * A gmm_fill_fn for X held whole in ordinary (pageable) host memory: user is
+ * the address of X [n*d] fp32, and the rows are copied with up to 8 host
+ * threads.  Returns 0, or 1 for a null pointer or rows < 0.
+ */
+int gmm_fill_pageable(void* user, int64_t row0, int64_t rows, int32_t d, float* dst);
+
+/*
+ * Out-of-core E-step over a ring of page-locked staging chunks (the paper's
+ * Limitations section, paragraph Scale: X streamed through the device in
+ * chunks accumulating into the same O(KD) statistics), for X that is not held
+ * whole in page-locked memory: in pageable memory (fill = gmm_fill_pageable),
+ * in a file, or produced as it is consumed.  For each chunk of chunk_rows rows,
+ * in row order, the calling thread has `fill` write the rows into the next of
+ * the ring_slots slots of ring [ring_slots*min(chunk_rows, n)*d fp32,
+ * page-locked host memory that the caller allocated], the slot is uploaded
+ * on copy_stream into one half of staging [2*min(chunk_rows, n)*d fp32,
+ * device], and the chunk's E-step is enqueued on `stream`.  A slot is filled
+ * again only once its previous upload has completed (the calling thread
+ * waits for it), so filling chunk c overlaps the upload of chunk c - 1 and
+ * the E-step of chunk c - 2.  Before the first fill the calling thread waits
+ * for the work already enqueued on copy_stream (which may still read the
+ * ring); the first upload waits for the work already enqueued on `stream`
+ * (which may still read the staging buffer).  The statistics are ADDED
+ * exactly as gmm_estep_accumulate adds them when called chunk by chunk, in
+ * row order, on device copies of the chunks (the same result, bit for bit).
+ * ws is sized by gmm_workspace_bytes(min(chunk_rows, n), d, k, 0).  The call
+ * returns once every chunk has been filled and enqueued; the ring and the
+ * staging buffer are read until `stream` completes.  Returns
+ * GMM_ERR_INVALID_ARG for a null pointer, chunk_rows < 1 or ring_slots < 2,
+ * GMM_ERR_FILL when `fill` returns non-zero (the chunks enqueued before it
+ * have already been added: the accumulators then hold a partial sum), plus
+ * the codes of gmm_estep_accumulate.
+ */
+int gmm_estep_accumulate_ring(gmm_fill_fn fill, void* user, int64_t n, int32_t d, int32_t k,
+                              const float* weights, const float* means, const float* vars,
+                              double* nk, double* s, double* q, double* loglik,
+                              int64_t chunk_rows, float* ring, int32_t ring_slots,
+                              float* staging, void* ws, size_t ws_bytes, hipStream_t stream,
+                              hipStream_t copy_stream);
 
 /*
  * k-means++ seeding (the initialisation the paper compares against its warm

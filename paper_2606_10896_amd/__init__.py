@@ -20,6 +20,7 @@ GMM_ERR_INVALID_ARG = -1
 GMM_ERR_UNSUPPORTED = -2
 GMM_ERR_WORKSPACE = -3
 GMM_ERR_DEVICE = -4
+GMM_ERR_FILL = -5
 GMM_MAX_D = 1024
 GMM_MAX_K = 65535
 GMM_MAX_M = 8
@@ -31,7 +32,8 @@ EXPORTS = ("gmm_status_string", "gmm_workspace_bytes", "gmm_estep_accumulate", "
            "gmm_estep_accumulate_streamed",
            "gmm_estep_accumulate_iso", "gmm_mstep_iso", "gmm_fit_iso", "gmm_timing_enable",
            "gmm_timing_read", "gmm_estep_accumulate_screened", "gmm_fit_screened",
-           "gmm_set_stats_chunk_limit", "gmm_estep_accumulate_static")
+           "gmm_set_stats_chunk_limit", "gmm_estep_accumulate_static",
+           "gmm_estep_accumulate_ring", "gmm_fill_pageable")
 
 _lib = None
 
@@ -85,6 +87,11 @@ def load_library():
     lib.gmm_estep_accumulate_streamed.argtypes = [vp, i64, i32, i32, vp, vp, vp, vp, vp, vp,
                                                   vp, i64, vp, vp, ctypes.c_size_t, vp, vp]
     lib.gmm_estep_accumulate_streamed.restype = ctypes.c_int
+    lib.gmm_fill_pageable.argtypes = [vp, i64, i64, i32, vp]
+    lib.gmm_fill_pageable.restype = ctypes.c_int
+    lib.gmm_estep_accumulate_ring.argtypes = [vp, vp, i64, i32, i32, vp, vp, vp, vp, vp, vp, vp,
+                                              i64, vp, i32, vp, vp, ctypes.c_size_t, vp, vp]
+    lib.gmm_estep_accumulate_ring.restype = ctypes.c_int
     lib.gmm_estep_accumulate_iso.argtypes = lib.gmm_estep_accumulate.argtypes
     lib.gmm_estep_accumulate_iso.restype = ctypes.c_int
     lib.gmm_mstep_iso.argtypes = lib.gmm_mstep.argtypes
@@ -288,6 +295,68 @@ def gmm_estep_accumulate_streamed(x_host, weights, means, variances, nk, s, q, l
         int(chunk_rows), _ptr(_dev(staging, torch.float32, "staging", 2 * rows * d)), _ptr(ws),
         ws.numel() if ws is not None else 0, _stream(stream), _stream(copy_stream))
     _check("gmm_estep_accumulate_streamed", rc)
+
+
+# the C type of a ring's row source: fill(user, row0, rows, d, dst) -> 0 on success
+FILL_FN = ctypes.CFUNCTYPE(ctypes.c_int, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
+                           ctypes.c_int32, ctypes.c_void_p)
+
+
+def gmm_estep_accumulate_ring(source, n, weights, means, variances, nk, s, q, loglik,
+                              chunk_rows, ring, staging, ws, stream=None, copy_stream=None):
+    """Out-of-core E-step whose rows come through a ring of page-locked staging chunks.
+
+    source: a C-contiguous fp32 numpy array [n, d] in ordinary host memory (copied into
+    the ring by the library's gmm_fill_pageable), or a callable fill(row0, rows, out) that
+    writes rows row0 .. row0 + rows - 1 into the numpy view out [rows, d] of a ring slot.
+    ring: a pinned fp32 CPU tensor [slots, min(chunk_rows, n), d] with slots >= 2; staging:
+    an fp32 CUDA tensor of at least 2 * min(chunk_rows, n) * d elements.  Adds into nk, s,
+    q, loglik as gmm_estep_accumulate does.  An exception raised by the callable ends the
+    call (GMM_ERR_FILL) and is re-raised here."""
+    import numpy as np
+    import torch
+    k = weights.shape[0]
+    if not (isinstance(ring, torch.Tensor) and not ring.is_cuda and ring.is_pinned()
+            and ring.dtype == torch.float32 and ring.is_contiguous() and ring.dim() == 3):
+        raise TypeError("ring must be a contiguous pinned fp32 CPU tensor [slots, rows, d]")
+    slots, rows, d = ring.shape
+    if rows != min(int(chunk_rows), int(n)):
+        raise ValueError(f"ring holds {rows} rows a slot, chunks are {min(int(chunk_rows), n)}")
+    lib = load_library()
+    failure = []
+    if isinstance(source, np.ndarray):
+        if not (source.dtype == np.float32 and source.flags.c_contiguous
+                and source.shape == (n, d)):
+            raise TypeError(f"source must be a C-contiguous float32 array [{n}, {d}]")
+        fn = ctypes.cast(lib.gmm_fill_pageable, ctypes.c_void_p)
+        user = ctypes.c_void_p(source.ctypes.data)
+    elif callable(source):
+        def trampoline(_user, row0, cnt, dd, dst):
+            try:
+                buf = (ctypes.c_float * (cnt * dd)).from_address(dst)
+                source(int(row0), int(cnt), np.ctypeslib.as_array(buf).reshape(cnt, dd))
+                return 0
+            except BaseException as e:        # noqa: BLE001 - re-raised after the call
+                failure.append(e)
+                return 1
+        cb = FILL_FN(trampoline)
+        fn = ctypes.cast(cb, ctypes.c_void_p)
+        user = ctypes.c_void_p(0)
+    else:
+        raise TypeError("source must be a numpy array or a callable")
+    rc = lib.gmm_estep_accumulate_ring(
+        fn, user, int(n), d, k,
+        _ptr(_dev(weights, torch.float32, "weights", k)),
+        _ptr(_dev(means, torch.float32, "means", k * d)),
+        _ptr(_dev(variances, torch.float32, "vars", k * d)),
+        _ptr(_dev(nk, torch.float64, "nk", k)), _ptr(_dev(s, torch.float64, "s", k * d)),
+        _ptr(_dev(q, torch.float64, "q", k * d)), _ptr(_dev(loglik, torch.float64, "loglik", 1)),
+        int(chunk_rows), ctypes.c_void_p(ring.data_ptr()), slots,
+        _ptr(_dev(staging, torch.float32, "staging", 2 * rows * d)), _ptr(ws),
+        ws.numel() if ws is not None else 0, _stream(stream), _stream(copy_stream))
+    if failure:
+        raise failure[0]
+    _check("gmm_estep_accumulate_ring", rc)
 
 
 def gmm_estep_accumulate_iso(x, weights, means, variances, nk, s, q, loglik, ws, stream=None):

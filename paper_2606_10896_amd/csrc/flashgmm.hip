@@ -49,6 +49,8 @@
 #include <string.h>
 
 #include <mutex>
+#include <thread>
+#include <vector>
 #include <type_traits>
 
 #include "flashgmm.h"
@@ -4327,6 +4329,7 @@ const char* gmm_status_string(int status) {
     case GMM_ERR_UNSUPPORTED: return "GMM_ERR_UNSUPPORTED";
     case GMM_ERR_WORKSPACE: return "GMM_ERR_WORKSPACE";
     case GMM_ERR_DEVICE: return "GMM_ERR_DEVICE";
+    case GMM_ERR_FILL: return "GMM_ERR_FILL";
     default: return "GMM_UNKNOWN_STATUS";
   }
 }
@@ -4536,6 +4539,104 @@ int gmm_estep_accumulate_streamed(const float* x_host, int64_t n, int32_t d, int
       return GMM_ERR_DEVICE;
     if (hipMemcpyAsync(buf, x_host + r0 * d, (size_t)nr * d * sizeof(float),
                        hipMemcpyHostToDevice, copy_stream) != hipSuccess ||
+        hipEventRecord(sev.up(b), copy_stream) != hipSuccess ||
+        hipStreamWaitEvent(stream, sev.up(b), 0) != hipSuccess)
+      return GMM_ERR_DEVICE;
+    Layout Lc;
+    if (!make_layout(nr, d, k, 0, &Lc)) return GMM_ERR_UNSUPPORTED;
+    rc = estep_dispatch(Lc, buf, weights, means, vars, nk, s, q, loglik, 1, ws, stream);
+    if (rc != GMM_OK) return rc;
+    if (hipEventRecord(sev.done(b), stream) != hipSuccess) return GMM_ERR_DEVICE;
+  }
+  return GMM_OK;
+}
+
+// ---------------------------------------------------------------- out-of-core ring
+int gmm_fill_pageable(void* user, int64_t row0, int64_t rows, int32_t d, float* dst) {
+  if (!user || !dst || rows < 0 || row0 < 0 || d < 1) return 1;
+  const char* src = reinterpret_cast<const char*>(user) + (size_t)row0 * d * sizeof(float);
+  char* out = reinterpret_cast<char*>(dst);
+  const size_t bytes = (size_t)rows * d * sizeof(float);
+  // one memcpy per thread over disjoint byte ranges; a single thread below 64 MiB
+  constexpr size_t kPiece = (size_t)64 << 20;
+  const size_t nt = bytes / kPiece < 8 ? (bytes / kPiece > 1 ? bytes / kPiece : 1) : 8;
+  if (nt == 1) {
+    memcpy(out, src, bytes);
+    return 0;
+  }
+  const size_t per = (bytes + nt - 1) / nt;
+  auto piece = [=](size_t t) {
+    const size_t b0 = t * per, b1 = b0 + per < bytes ? b0 + per : bytes;
+    if (b0 < b1) memcpy(out + b0, src + b0, b1 - b0);
+  };
+  std::vector<std::thread> th;
+  size_t t = 1;
+  for (; t < nt; ++t) {
+    try {
+      th.emplace_back(piece, t);
+    } catch (...) {
+      break;                    // no more threads: the calling thread copies the rest
+    }
+  }
+  for (; t < nt; ++t) piece(t);
+  piece(0);
+  for (std::thread& w : th) w.join();
+  return 0;
+}
+
+int gmm_estep_accumulate_ring(gmm_fill_fn fill, void* user, int64_t n, int32_t d, int32_t k,
+                              const float* weights, const float* means, const float* vars,
+                              double* nk, double* s, double* q, double* loglik,
+                              int64_t chunk_rows, float* ring, int32_t ring_slots,
+                              float* staging, void* ws, size_t ws_bytes, hipStream_t stream,
+                              hipStream_t copy_stream) {
+  int rc = check_shape(n, d, k);
+  if (rc != GMM_OK) return rc;
+  if (!fill || !weights || !means || !vars || !nk || !s || !q || !loglik || !ring || !staging ||
+      chunk_rows < 1 || ring_slots < 2)
+    return GMM_ERR_INVALID_ARG;
+  const int64_t rows = chunk_rows < n ? chunk_rows : n;
+  Layout L;
+  if (!make_layout(rows, d, k, 0, &L)) return GMM_ERR_UNSUPPORTED;
+  rc = check_ws(L, ws, ws_bytes);
+  if (rc != GMM_OK) return rc;
+  StreamEvents sev;
+  if (!sev.make()) return GMM_ERR_DEVICE;
+  // one event per ring slot: recorded after the slot's upload, waited for on
+  // the host before the slot is filled again
+  struct SlotEvents {
+    std::vector<hipEvent_t> ev;
+    ~SlotEvents() {
+      for (hipEvent_t e : ev)
+        if (e) (void)hipEventDestroy(e);
+    }
+  } slot;
+  slot.ev.assign((size_t)ring_slots, nullptr);
+  for (hipEvent_t& e : slot.ev)
+    if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return GMM_ERR_DEVICE;
+  // earlier uploads on copy_stream may still read the ring (the host waits for
+  // them), and earlier work on `stream` the staging buffer (the uploads wait)
+  if (hipEventRecord(slot.ev[0], copy_stream) != hipSuccess ||
+      hipEventSynchronize(slot.ev[0]) != hipSuccess ||
+      hipEventRecord(sev.start(), stream) != hipSuccess ||
+      hipStreamWaitEvent(copy_stream, sev.start(), 0) != hipSuccess)
+    return GMM_ERR_DEVICE;
+  const int64_t nchunks = (n + rows - 1) / rows;
+  const size_t slot_elems = (size_t)rows * d;
+  for (int64_t c = 0; c < nchunks; ++c) {
+    const int b = (int)(c & 1);
+    const int sl = (int)(c % ring_slots);
+    const int64_t r0 = c * rows, nr = n - r0 < rows ? n - r0 : rows;
+    float* src = ring + (size_t)sl * slot_elems;
+    float* buf = staging + (size_t)b * slot_elems;
+    if (c >= ring_slots && hipEventSynchronize(slot.ev[sl]) != hipSuccess) return GMM_ERR_DEVICE;
+    if (fill(user, r0, nr, d, src) != 0) return GMM_ERR_FILL;
+    // upload chunk c once the E-step of chunk c - 2 has read this half of staging
+    if (c >= 2 && hipStreamWaitEvent(copy_stream, sev.done(b), 0) != hipSuccess)
+      return GMM_ERR_DEVICE;
+    if (hipMemcpyAsync(buf, src, (size_t)nr * d * sizeof(float), hipMemcpyHostToDevice,
+                       copy_stream) != hipSuccess ||
+        hipEventRecord(slot.ev[sl], copy_stream) != hipSuccess ||
         hipEventRecord(sev.up(b), copy_stream) != hipSuccess ||
         hipStreamWaitEvent(stream, sev.up(b), 0) != hipSuccess)
       return GMM_ERR_DEVICE;

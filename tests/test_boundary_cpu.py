@@ -31,6 +31,7 @@ def test_status_strings():
     assert gmm.status_string(-2) == "GMM_ERR_UNSUPPORTED"
     assert gmm.status_string(-3) == "GMM_ERR_WORKSPACE"
     assert gmm.status_string(-4) == "GMM_ERR_DEVICE"
+    assert gmm.status_string(-5) == "GMM_ERR_FILL"
     assert gmm.status_string(12345) == "GMM_UNKNOWN_STATUS"
 
 
@@ -141,6 +142,44 @@ def test_streamed_host_validation():
     assert call(p, 5000, p, ws, small) == gmm.GMM_ERR_WORKSPACE
     assert lib.gmm_estep_accumulate_streamed(p, 1000, 1025, 4, p, p, p, p, p, p, p, 500, p, ws,
                                              small, None, None) == gmm.GMM_ERR_UNSUPPORTED
+
+
+def test_ring_host_validation():
+    lib = gmm.load_library()
+    p, ws = _fake(), _fake(0x200000)
+    fill = ctypes.cast(lib.gmm_fill_pageable, ctypes.c_void_p)
+    small = gmm.workspace_bytes(500, 8, 4)
+    call = lambda fn, chunk, ring, slots, stg, w, nb: lib.gmm_estep_accumulate_ring(
+        fn, p, 1000, 8, 4, p, p, p, p, p, p, p, chunk, ring, slots, stg, w, nb, None, None)
+    assert call(None, 500, p, 2, p, ws, small) == gmm.GMM_ERR_INVALID_ARG
+    assert call(fill, 0, p, 2, p, ws, small) == gmm.GMM_ERR_INVALID_ARG
+    assert call(fill, 500, None, 2, p, ws, small) == gmm.GMM_ERR_INVALID_ARG
+    assert call(fill, 500, p, 1, p, ws, small) == gmm.GMM_ERR_INVALID_ARG
+    assert call(fill, 500, p, 2, None, ws, small) == gmm.GMM_ERR_INVALID_ARG
+    # the workspace is sized for one chunk of min(chunk_rows, n) rows
+    assert call(fill, 500, p, 2, p, ws, small - 1) == gmm.GMM_ERR_WORKSPACE
+    assert call(fill, 5000, p, 3, p, ws, small) == gmm.GMM_ERR_WORKSPACE
+    assert lib.gmm_estep_accumulate_ring(fill, p, 1000, 1025, 4, p, p, p, p, p, p, p, 500, p, 2,
+                                         p, ws, small, None, None) == gmm.GMM_ERR_UNSUPPORTED
+
+
+@pytest.mark.parametrize("n,d,row0,rows", [(1000, 7, 0, 1000), (1000, 7, 993, 7), (1000, 7, 10, 0),
+                                           (170_000, 128, 3, 169_990)])
+def test_fill_pageable_copies_the_rows(n, d, row0, rows):
+    """The pageable-memory row source is plain host code: rows row0 .. row0 + rows - 1, whole,
+    also when the copy is split over threads (above 64 MiB: the last case, 87 MB)."""
+    import numpy as np
+    lib = gmm.load_library()
+    x = np.random.default_rng(n + row0).standard_normal((n, d)).astype(np.float32)
+    out = np.full((max(rows, 1) + 1, d), np.float32(-7.0))
+    rc = lib.gmm_fill_pageable(ctypes.c_void_p(x.ctypes.data), row0, rows, d,
+                               ctypes.c_void_p(out.ctypes.data))
+    assert rc == 0
+    np.testing.assert_array_equal(out[:rows], x[row0:row0 + rows])
+    assert np.all(out[rows:] == np.float32(-7.0))
+    assert lib.gmm_fill_pageable(None, 0, 1, d, ctypes.c_void_p(out.ctypes.data)) == 1
+    assert lib.gmm_fill_pageable(ctypes.c_void_p(x.ctypes.data), 0, -1, d,
+                                 ctypes.c_void_p(out.ctypes.data)) == 1
 
 
 def test_kmeanspp_host_validation():

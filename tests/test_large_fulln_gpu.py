@@ -28,34 +28,52 @@ def _say(*a):
     sys.stdout.flush()
 
 
-@pytest.mark.timeout(1100)
-def test_large_workload_whole_equals_sum_of_views():
+@pytest.fixture(scope="module")
+def large():
     import torch
     import bench
-    import paper_2606_10896_amd as gmm
     t0 = time.time()
     w = g.WORKLOADS["large"]
     dev = torch.device("cuda:0")
     x, mix, colsum, colsq = bench.load_data(w, dev)
     th0 = g.random_point_init(w, mix, colsum, colsq)
     _say(f"  large workload resident ({time.time() - t0:.1f}s)")
+    yield w, x, th0
+    del x
+    torch.cuda.empty_cache()
+
+
+def _stats(x, th, rows, ws):
+    """Statistics of x at th from gmm_estep_accumulate calls over views of `rows` rows."""
+    import torch
+    import paper_2606_10896_amd as gmm
+    n, d = x.shape
+    k = th[0].shape[0]
+    dev = x.device
+    wt, mu, var = (torch.from_numpy(np.ascontiguousarray(a)).to(dev) for a in th)
+    nk = torch.zeros(k, dtype=torch.float64, device=dev)
+    s = torch.zeros(k, d, dtype=torch.float64, device=dev)
+    q = torch.zeros(k, d, dtype=torch.float64, device=dev)
+    ll = torch.zeros(1, dtype=torch.float64, device=dev)
+    for r0 in range(0, n, rows):
+        gmm.gmm_estep_accumulate(x[r0:r0 + rows], wt, mu, var, nk, s, q, ll, ws)
+    torch.cuda.synchronize()
+    return nk.cpu().numpy(), s.cpu().numpy(), q.cpu().numpy(), ll.item()
+
+
+@pytest.mark.timeout(1100)
+def test_large_workload_whole_equals_sum_of_views(large):
+    import torch
+    import paper_2606_10896_amd as gmm
+    t0 = time.time()
+    w, x, th0 = large
+    dev = x.device
     n, d, k = w.n, w.d, w.k
     ws_all = gmm.workspace(n, d, k, device=dev)
     ws_view = gmm.workspace(VIEW, d, k, device=dev)
 
     def stats(th, views):
-        wt, mu, var = (torch.from_numpy(np.ascontiguousarray(a)).to(dev) for a in th)
-        nk = torch.zeros(k, dtype=torch.float64, device=dev)
-        s = torch.zeros(k, d, dtype=torch.float64, device=dev)
-        q = torch.zeros(k, d, dtype=torch.float64, device=dev)
-        ll = torch.zeros(1, dtype=torch.float64, device=dev)
-        if views:
-            for r0 in range(0, n, VIEW):
-                gmm.gmm_estep_accumulate(x[r0:r0 + VIEW], wt, mu, var, nk, s, q, ll, ws_view)
-        else:
-            gmm.gmm_estep_accumulate(x, wt, mu, var, nk, s, q, ll, ws_all)
-        torch.cuda.synchronize()
-        return nk.cpu().numpy(), s.cpu().numpy(), q.cpu().numpy(), ll.item()
+        return _stats(x, th, VIEW, ws_view) if views else _stats(x, th, n, ws_all)
 
     # Theta_2: two EM iterations of the library from Theta_0
     wt, mu, var = (torch.from_numpy(a).to(dev) for a in th0)
@@ -76,3 +94,43 @@ def test_large_workload_whole_equals_sum_of_views():
              f"Q {e_q.max():.2e}  LL {e_ll:.2e}  ({time.time() - t0:.1f}s)")
         assert e_n.max() <= TOL and e_s.max() <= TOL and e_q.max() <= TOL
         assert e_ll <= 1e-9
+
+
+@pytest.mark.timeout(1100)
+def test_large_workload_from_pageable_memory_through_the_ring(large):
+    """X of the 1e8-row workload in ordinary host memory (51.2 GB, more than could be pinned
+    whole), streamed through a ring of three page-locked 4,194,304-row slots by
+    gmm_estep_accumulate_ring: bit for bit the statistics of gmm_estep_accumulate over the
+    resident 4,194,304-row views."""
+    import torch
+    import paper_2606_10896_amd as gmm
+    w, x, th0 = large
+    dev = x.device
+    n, d, k = w.n, w.d, w.k
+    t0 = time.time()
+    xh = np.empty((n, d), dtype=np.float32)
+    for r0 in range(0, n, VIEW):
+        xh[r0:r0 + VIEW] = x[r0:r0 + VIEW].cpu().numpy()
+    _say(f"  pageable host copy of X ({time.time() - t0:.1f}s)")
+    ws = gmm.workspace(VIEW, d, k, device=dev)
+    ref = _stats(x, th0, VIEW, ws)
+    ring = torch.empty((3, VIEW, d), dtype=torch.float32, pin_memory=True)
+    staging = torch.empty(2 * VIEW * d, dtype=torch.float32, device=dev)
+    copy = torch.cuda.Stream()
+    wt, mu, var = (torch.from_numpy(np.ascontiguousarray(a)).to(dev) for a in th0)
+    for rep in range(2):
+        nk = torch.zeros(k, dtype=torch.float64, device=dev)
+        s = torch.zeros(k, d, dtype=torch.float64, device=dev)
+        q = torch.zeros(k, d, dtype=torch.float64, device=dev)
+        ll = torch.zeros(1, dtype=torch.float64, device=dev)
+        torch.cuda.synchronize()
+        t1 = time.time()
+        gmm.gmm_estep_accumulate_ring(xh, n, wt, mu, var, nk, s, q, ll, VIEW, ring, staging, ws,
+                                      copy_stream=copy)
+        torch.cuda.synchronize()
+        dt = time.time() - t1
+        _say(f"  ring E-step from pageable memory: {dt * 1e3:.0f} ms, "
+             f"{4.0 * n * d / dt / 1e9:.1f} GB/s of X")
+        got = (nk.cpu().numpy(), s.cpu().numpy(), q.cpu().numpy(), ll.item())
+        for a, b, name in zip(got, ref, ("N_k", "S", "Q", "LL")):
+            assert np.array_equal(a, b), f"pass {rep}: {name} differs from the resident views"
