@@ -2917,26 +2917,42 @@ __global__ __launch_bounds__(256) void k_stats_ill(
 // Top-m multi-assignment at the given parameters, exact in the component order:
 //   1. k_assign_theta: the screened log-densities of every point (the MFMA
 //      pass of k_logz) give the T-th largest of its 128 lane-state maxima,
-//      S_T (T = m + 2).  At least T components have a screened log-density
-//      >= S_T, so the T-th largest exact one is >= S_T - slack, and every
-//      component among the T largest has a screened log-density >= theta =
-//      S_T - 2 slack, slack = kScreenSlack >= the screening error (log2 units).
-//   2. k_assign_collect: a second screening pass keeps every component with a
-//      screened log-density >= theta as a candidate (at most kACap per point)
-//      and sums all others in a log-sum-exp; the candidates' log-densities are
+//      S_T (T = m + 2), and from it the thresholds below which no component
+//      among the point's T largest can have its screened log-density.
+//   2. k_assign_collect: a second screening pass keeps every component at or
+//      above its threshold as a candidate (at most kACap per point) and sums
+//      all others in a log-sum-exp; the candidates' log-densities are
 //      recomputed in fp64 (direct form), ranked (ties to the lower index), and
 //      normalised with log Z = log(sum over candidates of exp(exact) + the
 //      screened sum of the others).  Rank 1 is always assigned, rank j > 1
 //      only if its responsibility is > tau.
 //   3. k_assign_fallback: points with more than kACap candidates are done
 //      exactly over all components in fp64.
+// Thresholds, fp32 screening (D64 > 128): S_T - 2 kScreenSlack for every
+// component, kScreenSlack >= the screening error of the well-conditioned ones.
+// Split-bf16 screening (D64 <= 128), from an error bound of each component: a
+// screened log-density (log2 units) is the bias plus the products of [x | x^2]
+// with [W | P]; three split products per fp32 product leave out at most
+// 3 2^-16 of the product and the fp32 accumulation adds about 52 2^-24 of the
+// running sums, so its error is at most eps = 2^-13 (with room) times the sum
+// of the magnitudes of the bias and the products.  With |x mu| <= (x^2 +
+// mu^2) / 2 and x^2 <= 2 (x - mu)^2 + 2 mu^2, that sum is at most
+// 4 (cdir_k - l_k) + A_k, l_k the exact log-density, cdir_k its value at the
+// mean and A_k = 5 (cdir_k - cwell_k) + |cwell_k|.  The arg-max components of
+// the T largest lane states have exact log-densities of at least
+// theta0 = S_T - max_i eps (4 (cdir_i - S_T) + A_i) / (1 - 4 eps), and so has
+// the T-th largest component; a component j with l_j >= theta0 has a screened
+// value >= theta0 - eps (4 (cdir_j - theta0) + A_j) = theta0 (1 + 4 eps) - b_j,
+// b_j = eps (4 cdir_j + A_j), its candidate threshold.  Routed components,
+// whose fp64 log-densities are rounded to fp32, take theta0 less that rounding.
 constexpr int kACap = 32;
 constexpr float kScreenSlack = 1.0f;
+constexpr float kSplitEps = 0x1p-13f;
 constexpr int kTMax = GMM_MAX_M + 2;
 
 // fp64 direct-form log-density (natural log) of component comp at point xr
-// (fp32 row in LDS), from the caller's fp32 parameters and the fp64 constant
-// cdir (log2 units).
+// (fp32 row, LDS or global memory), from the caller's fp32 parameters and the
+// fp64 constant cdir (log2 units).
 __device__ __forceinline__ double ell64(const float* xr, const float* __restrict__ mu,
                                         const float* __restrict__ var, double cdir_k, int d) {
   double acc = 0.0;
@@ -2947,91 +2963,274 @@ __device__ __forceinline__ double ell64(const float* xr, const float* __restrict
   return cdir_k * kLn2 - 0.5 * acc;
 }
 
+// Per well slot, the terms of its error bound: (cdir_j, A_j) in log2 units;
+// (-inf, 0) for the padding slots.
+__global__ __launch_bounds__(256) void k_assign_slots(const double* __restrict__ cwell,
+                                                      const double* __restrict__ cdir,
+                                                      const int* __restrict__ counts,
+                                                      const int* __restrict__ well_idx, int kpad,
+                                                      float2* __restrict__ ca) {
+  const int slot = blockIdx.x * blockDim.x + threadIdx.x;
+  if (slot >= kpad) return;
+  float2 r = make_float2(-INFINITY, 0.0f);
+  if (slot < counts[0]) {
+    const int comp = well_idx[slot];
+    const double c = cdir[comp], cw = cwell[comp];
+    // rounded up to fp32: the bound only grows
+    r = make_float2(__double2float_ru(c), __double2float_ru(5.0 * (c - cw) + fabs(cw)));
+  }
+  ca[slot] = r;
+}
+
+// Split X tile of the bf16 screening (the [x | x^2] layout of k_logz) from
+// rows n0 .. n0 + 63; rows >= n and dimensions >= d are zero.  The whole
+// chunks of every thread are loaded first (one memory round trip), the
+// partial ones value by value.
 template <int D64>
-__global__ __launch_bounds__(256) void k_assign_theta(
-    const float* __restrict__ x, int64_t n, int d, int vec4, const float4* __restrict__ wp,
-    const float* __restrict__ cw, const int* __restrict__ counts, int tsel,
-    float* __restrict__ theta) {
-  constexpr int P = D64 + 4, NT = logz_tiles(D64), PTS = 32 * NT;
-  __shared__ __align__(16) float xs[PTS * P];
-  __shared__ float lmax[PTS][129];
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, h = lane >> 5, col = lane & 31;
-  const int64_t n0 = (int64_t)blockIdx.x * PTS;
-  load_tile<D64>(x, n, d, n0, PTS, xs, vec4 != 0);
-  __syncthreads();
-  const int n_wkb = counts[2];
-  float m0[16], m1[16];
+__device__ __forceinline__ void split_tile(const float* __restrict__ x, int64_t n, int d,
+                                           int vec4, int64_t n0, bf16x8* xa) {
+  constexpr int NC8 = D64 / 8, PTS = 64, NIT = (PTS * NC8 + 255) / 256;
+  const int tid = threadIdx.x;
+  float4 ld[NIT][2];
+  bool whole[NIT];
 #pragma unroll
-  for (int v = 0; v < 16; ++v) m0[v] = m1[v] = kEmpty;
-  {
-    const int nb = n_wkb > wave ? (n_wkb - wave + 3) / 4 : 0;
-    constexpr size_t BS = (size_t)(D64 / 4) * 64;
-    f16v c0, c1, x0, x1;
-    auto epi = [&](int v, float l0, float l1) {
-      m0[v] = fmaxf(m0[v], l0);
-      if constexpr (NT == 2) m1[v] = fmaxf(m1[v], l1);
-    };
-    if (nb > 0) {
-      logz_step<D64, true, false, NT>(xs, wp + (size_t)wave * BS, cw[wave * kBK + col], c0, c1,
-                                      x0, x1, epi);
-      for (int i = 0; i + 1 < nb; ++i) {
-        const int kb = wave + 4 * i;
-        logz_step<D64, true, true, NT>(xs, wp + (size_t)(kb + 4) * BS, cw[(kb + 4) * kBK + col],
-                                       x0, x1, c0, c1, epi);
-        c0 = x0;
-        c1 = x1;
-      }
-      logz_step<D64, false, true, NT>(xs, wp, 0.0f, x0, x1, c0, c1, epi);
+  for (int it = 0; it < NIT; ++it) {
+    const int t = tid + 256 * it, p = t / NC8, c = t % NC8;
+    const int64_t row = n0 + p;
+    whole[it] = vec4 && t < PTS * NC8 && row < n && 8 * c + 8 <= d;
+    if (whole[it]) {
+      ld[it][0] = *reinterpret_cast<const float4*>(x + row * d + 8 * c);
+      ld[it][1] = *reinterpret_cast<const float4*>(x + row * d + 8 * c + 4);
     }
   }
+#pragma unroll
+  for (int it = 0; it < NIT; ++it) {
+    const int t = tid + 256 * it, p = t / NC8, c = t % NC8;
+    if (t >= PTS * NC8) continue;
+    const int64_t row = n0 + p;
+    float v[8];
+    if (whole[it]) {
+      v[0] = ld[it][0].x; v[1] = ld[it][0].y; v[2] = ld[it][0].z; v[3] = ld[it][0].w;
+      v[4] = ld[it][1].x; v[5] = ld[it][1].y; v[6] = ld[it][1].z; v[7] = ld[it][1].w;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int j = 8 * c + e;
+        v[e] = (row < n && j < d) ? x[row * d + j] : 0.0f;
+      }
+    }
+    split_store<D64, false>(xa, p, c, v);
+  }
+}
+
+// Screening pass shared by the two assignment kernels: wave w takes the well
+// blocks w, w + 4, ...; epi(v, l0, l1, slot, b) receives the log-densities of
+// lane element v of the two point tiles for component slot `slot`, and b =
+// pre(slot), which is called one block ahead (its loads then have a block's
+// MFMA work to arrive).
+template <int D64, class Pre, class Epi>
+__device__ __forceinline__ void assign_screen(const float* xs, const bf16x8* xa,
+                                              const float4* __restrict__ wp,
+                                              const bf16x8* __restrict__ wpb,
+                                              const float* __restrict__ cw, int n_wkb,
+                                              Pre&& pre, Epi&& epi) {
+  constexpr int NT = logz_tiles(D64);
+  constexpr bool SPL = screen_b16(D64);
+  constexpr int NSTEP = screen_steps<D64, false>(), RPV = 4 * NSTEP + 1;
+  constexpr size_t BS = (size_t)(D64 / 4) * 64, BS16 = (size_t)NSTEP * 64 * 2;
+  const int tid = threadIdx.x, wave = tid >> 6, col = tid & 31;
+  const int nb = n_wkb > wave ? (n_wkb - wave + 3) / 4 : 0;
+  if (nb == 0) return;
+  f16v c0, c1, x0, x1;
+  int slot = 0;
+  float bv = 0.0f, bn = pre(wave * kBK + col);
+  auto e2 = [&](int v, float l0, float l1) { epi(v, l0, l1, slot, bv); };
+  if constexpr (SPL)
+    logz_step16<NSTEP, RPV, true, false, NT>(xa, wpb + (size_t)wave * BS16,
+                                             cw[wave * kBK + col], c0, c1, x0, x1, e2);
+  else
+    logz_step<D64, true, false, NT>(xs, wp + (size_t)wave * BS, cw[wave * kBK + col], c0, c1,
+                                    x0, x1, e2);
+  for (int i = 0; i + 1 < nb; ++i) {
+    const int kb = wave + 4 * i;
+    slot = kb * kBK + col;
+    bv = bn;
+    bn = pre((kb + 4) * kBK + col);
+    if constexpr (SPL)
+      logz_step16<NSTEP, RPV, true, true, NT>(xa, wpb + (size_t)(kb + 4) * BS16,
+                                              cw[(kb + 4) * kBK + col], x0, x1, c0, c1, e2);
+    else
+      logz_step<D64, true, true, NT>(xs, wp + (size_t)(kb + 4) * BS, cw[(kb + 4) * kBK + col],
+                                     x0, x1, c0, c1, e2);
+    c0 = x0;
+    c1 = x1;
+  }
+  slot = (wave + 4 * (nb - 1)) * kBK + col;
+  bv = bn;
+  if constexpr (SPL)
+    logz_step16<NSTEP, RPV, false, true, NT>(xa, wpb, 0.0f, x0, x1, c0, c1, e2);
+  else
+    logz_step<D64, false, true, NT>(xs, wp, 0.0f, x0, x1, c0, c1, e2);
+}
+
+// Thresholds of each point: theta[p] = (well-component base, routed-component
+// threshold); a well slot j is a candidate when its screened log-density is
+// >= theta[p].x - b_j (b_j = 0 for the fp32 screening).
+template <int D64>
+__global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_assign_theta(
+    const float* __restrict__ x, int64_t n, int d, int vec4, const float4* __restrict__ wp,
+    const bf16x8* __restrict__ wpb, const float* __restrict__ cw,
+    const float2* __restrict__ ca, const int* __restrict__ counts, int tsel,
+    float2* __restrict__ theta) {
+  constexpr int P = D64 + 4, NT = logz_tiles(D64), PTS = 32 * NT;
+  constexpr bool SPL = screen_b16(D64);
+  constexpr int RPV = 4 * screen_steps<D64, false>() + 1;
+  // SPL: the split tile, whose space the lane-state maxima and their arg-max
+  // slots take over after the screening; else the fp32 tile and the maxima
+  constexpr size_t XB = SPL ? (size_t)PTS * RPV * sizeof(bf16x8) : (size_t)PTS * P * sizeof(float);
+  constexpr size_t LB = (size_t)PTS * 129 * (SPL ? sizeof(float2) : sizeof(float));
+  constexpr size_t SB = SPL ? (XB > LB ? XB : LB) : XB + LB;
+  __shared__ __align__(16) unsigned char smem[SB];
+  float* const xs = reinterpret_cast<float*>(smem);
+  bf16x8* const xa = reinterpret_cast<bf16x8*>(smem);
+  float* const lmx = reinterpret_cast<float*>(smem + (SPL ? 0 : XB));      // [PTS][129]
+  float2* const lma = reinterpret_cast<float2*>(smem);                     // [PTS][129]
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, h = lane >> 5, col = lane & 31;
+  const int64_t n0 = (int64_t)blockIdx.x * PTS;
+  if constexpr (SPL) split_tile<D64>(x, n, d, vec4, n0, xa);
+  else load_tile<D64>(x, n, d, n0, PTS, xs, vec4 != 0);
+  __syncthreads();
+  float m0[16], m1[16];
+  int a0[16], a1[16];
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    m0[v] = m1[v] = kEmpty;
+    a0[v] = a1[v] = -1;
+  }
+  assign_screen<D64>(xs, xa, wp, wpb, cw, counts[2], [](int) { return 0.0f; },
+                     [&](int v, float l0, float l1, int slot, float) {
+    if constexpr (SPL) {
+      a0[v] = l0 > m0[v] ? slot : a0[v];
+      if constexpr (NT == 2) a1[v] = l1 > m1[v] ? slot : a1[v];
+    }
+    m0[v] = fmaxf(m0[v], l0);
+    if constexpr (NT == 2) m1[v] = fmaxf(m1[v], l1);
+  });
+  if constexpr (SPL) __syncthreads();        // the maxima take over the split tile
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
     const int p = 8 * (v >> 2) + 4 * h + (v & 3);
-    lmax[p][wave * 32 + col] = m0[v];
-    if constexpr (NT == 2) lmax[32 + p][wave * 32 + col] = m1[v];
+    if constexpr (SPL) {
+      lma[p * 129 + wave * 32 + col] = make_float2(m0[v], __int_as_float(a0[v]));
+      if constexpr (NT == 2) lma[(32 + p) * 129 + wave * 32 + col] = make_float2(m1[v], __int_as_float(a1[v]));
+    } else {
+      lmx[p * 129 + wave * 32 + col] = m0[v];
+      if constexpr (NT == 2) lmx[(32 + p) * 129 + wave * 32 + col] = m1[v];
+    }
   }
   __syncthreads();
-  if (tid < PTS && n0 + tid < n) {
+  {
+    // G threads per point, each over 128 / G lane states, then their lists
+    // merged across the group (disjoint lane states: no entry twice)
+    constexpr int G = 256 / PTS, LPT = 128 / G;
+    const int p = tid / G, r = tid % G;
     float tl[kTMax];
+    int ta[kTMax];
 #pragma unroll
-    for (int j = 0; j < kTMax; ++j) tl[j] = -INFINITY;
-    for (int c = 0; c < 128; ++c) {
-      const float v = lmax[tid][c];
-      if (!(v > 0.5f * kEmpty)) continue;      // empty lane state
+    for (int j = 0; j < kTMax; ++j) {
+      tl[j] = -INFINITY;
+      ta[j] = -1;
+    }
+    auto insert = [&](float v, int a) {
 #pragma unroll
       for (int j = kTMax - 1; j > 0; --j) {
-        if (v > tl[j - 1]) tl[j] = tl[j - 1];
-        else if (v > tl[j]) tl[j] = v;
+        if (v > tl[j - 1]) { tl[j] = tl[j - 1]; ta[j] = ta[j - 1]; }
+        else if (v > tl[j]) { tl[j] = v; ta[j] = a; }
       }
-      if (v > tl[0]) tl[0] = v;
+      if (v > tl[0]) { tl[0] = v; ta[0] = a; }
+    };
+    for (int c = LPT * r; c < LPT * r + LPT; ++c) {
+      float v;
+      int a = -1;
+      if constexpr (SPL) {
+        const float2 e = lma[p * 129 + c];
+        v = e.x;
+        a = __float_as_int(e.y);
+      } else {
+        v = lmx[p * 129 + c];
+      }
+      // empty lane states (kEmpty) and those below the list are skipped
+      if (v > 0.5f * kEmpty && v > tl[kTMax - 1]) insert(v, a);
     }
+#pragma unroll
+    for (int off = 1; off < G; off <<= 1) {
+      float ol[kTMax];
+      int oa[kTMax];
+#pragma unroll
+      for (int j = 0; j < kTMax; ++j) {
+        ol[j] = __shfl_xor(tl[j], off);
+        oa[j] = __shfl_xor(ta[j], off);
+      }
+#pragma unroll
+      for (int j = 0; j < kTMax; ++j)
+        if (ol[j] > tl[kTMax - 1]) insert(ol[j], oa[j]);
+    }
+    if (r != 0 || n0 + p >= n) return;
     float st = -INFINITY;
 #pragma unroll
     for (int j = 0; j < kTMax; ++j)
       if (j == tsel - 1) st = tl[j];
-    theta[n0 + tid] = st - 2.0f * kScreenSlack;
+    float2 out;
+    if constexpr (SPL) {
+      float dm = 0.0f;
+#pragma unroll
+      for (int j = 0; j < kTMax; ++j) {
+        if (j < tsel && ta[j] >= 0) {
+          const float2 e = ca[ta[j]];
+          dm = fmaxf(dm, kSplitEps * (4.0f * fmaxf(e.x - st, 0.0f) + e.y));
+        }
+      }
+      const float th0 = st - dm / (1.0f - 4.0f * kSplitEps);
+      // fp32 rounding of these few operations: 2^-20 of the magnitude
+      const float mg = 0x1p-20f * (fabsf(th0) + 1.0f);
+      out = make_float2(th0 * (1.0f + 4.0f * kSplitEps) - mg, th0 - 0x1p-22f * (fabsf(th0) + 1.0f) - mg);
+    } else {
+      out = make_float2(st - 2.0f * kScreenSlack, st - 2.0f * kScreenSlack);
+    }
+    theta[n0 + p] = out;
   }
 }
 
 template <int D64>
-__global__ __launch_bounds__(256) void k_assign_collect(
+__global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_assign_collect(
     const float* __restrict__ x, int64_t n, int d, int vec4, const float4* __restrict__ wp,
-    const float* __restrict__ cw, const int* __restrict__ well_idx,
+    const bf16x8* __restrict__ wpb, const float* __restrict__ cw,
+    const float2* __restrict__ ca, const int* __restrict__ well_idx,
     const int* __restrict__ ill_idx, const float* __restrict__ dmu,
     const double* __restrict__ dh, const int* __restrict__ counts,
-    const float* __restrict__ theta, const float* __restrict__ mu,
+    const float2* __restrict__ theta, const float* __restrict__ mu,
     const float* __restrict__ var, const double* __restrict__ cdir, int m, float tau,
     int* __restrict__ idx, float* __restrict__ resp, int* __restrict__ ovf) {
   constexpr int P = D64 + 4, NT = logz_tiles(D64), PTS = 32 * NT;
-  __shared__ __align__(16) float xs[PTS * P];
+  constexpr bool SPL = screen_b16(D64);
+  constexpr int RPV = 4 * screen_steps<D64, false>() + 1;
+  // the X tile (SPL: split, its space then taken over by the exact log-densities)
+  constexpr size_t XB = SPL ? (size_t)PTS * RPV * sizeof(bf16x8) : (size_t)PTS * P * sizeof(float);
+  constexpr size_t CB = (size_t)PTS * kACap * sizeof(double);
+  static_assert(!SPL || CB <= XB, "the exact log-densities fit the split tile's space");
+  constexpr size_t SB = SPL ? XB : XB + CB;
+  __shared__ __align__(16) unsigned char smem[SB];
   __shared__ int ccnt[PTS];
   __shared__ int cand[PTS][kACap];         // well slot s >= 0, or -(ill component + 1)
-  __shared__ double cl[PTS][kACap];
   __shared__ float2 stw[4][PTS];
   __shared__ float2 sti[4][PTS];
+  float* const xs = reinterpret_cast<float*>(smem);
+  bf16x8* const xa = reinterpret_cast<bf16x8*>(smem);
+  double* const cl = reinterpret_cast<double*>(smem + (SPL ? 0 : XB));    // [PTS][kACap]
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, h = lane >> 5, col = lane & 31;
   const int64_t n0 = (int64_t)blockIdx.x * PTS;
-  load_tile<D64>(x, n, d, n0, PTS, xs, vec4 != 0);
+  if constexpr (SPL) split_tile<D64>(x, n, d, vec4, n0, xa);
+  else load_tile<D64>(x, n, d, n0, PTS, xs, vec4 != 0);
   if (tid < PTS) ccnt[tid] = 0;
   __syncthreads();
   const int n_wkb = counts[2], n_ill = counts[1];
@@ -3039,47 +3238,39 @@ __global__ __launch_bounds__(256) void k_assign_collect(
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
     const int p = 8 * (v >> 2) + 4 * h + (v & 3);
-    th0[v] = n0 + p < n ? theta[n0 + p] : INFINITY;
-    th1[v] = (NT == 2 && n0 + 32 + p < n) ? theta[n0 + 32 + p] : INFINITY;
+    th0[v] = n0 + p < n ? theta[n0 + p].x : INFINITY;
+    th1[v] = (NT == 2 && n0 + 32 + p < n) ? theta[n0 + 32 + p].x : INFINITY;
     m0[v] = m1[v] = kEmpty;
     s0[v] = s1[v] = 0.0f;
   }
   {
-    const int nb = n_wkb > wave ? (n_wkb - wave + 3) / 4 : 0;
-    constexpr size_t BS = (size_t)(D64 / 4) * 64;
-    f16v c0, c1, x0, x1;
-    int slot = 0;
-    auto epi = [&](int v, float l0, float l1) {
+    // the slot's share b_j of its candidate threshold (0 for the fp32 screening)
+    auto pre = [&](int slot) {
+      if constexpr (SPL) {
+        const float2 e = ca[slot];
+        return kSplitEps * (4.0f * e.x + e.y);
+      } else {
+        return 0.0f;
+      }
+    };
+    assign_screen<D64>(xs, xa, wp, wpb, cw, n_wkb, pre,
+                       [&](int v, float l0, float l1, int slot, float bj) {
       const int p = 8 * (v >> 2) + 4 * h + (v & 3);
-      if (l0 >= th0[v] && l0 > -INFINITY) {
+      if (l0 >= th0[v] - bj && l0 > -INFINITY) {
         const int pos = atomicAdd(&ccnt[p], 1);
         if (pos < kACap) cand[p][pos] = slot;
       } else {
         lse_add_e(m0[v], s0[v], l0);
       }
       if constexpr (NT == 2) {
-        if (l1 >= th1[v] && l1 > -INFINITY) {
+        if (l1 >= th1[v] - bj && l1 > -INFINITY) {
           const int pos = atomicAdd(&ccnt[32 + p], 1);
           if (pos < kACap) cand[32 + p][pos] = slot;
         } else {
           lse_add_e(m1[v], s1[v], l1);
         }
       }
-    };
-    if (nb > 0) {
-      logz_step<D64, true, false, NT>(xs, wp + (size_t)wave * BS, cw[wave * kBK + col], c0, c1,
-                                      x0, x1, epi);
-      for (int i = 0; i + 1 < nb; ++i) {
-        const int kb = wave + 4 * i;
-        slot = kb * kBK + col;
-        logz_step<D64, true, true, NT>(xs, wp + (size_t)(kb + 4) * BS, cw[(kb + 4) * kBK + col],
-                                       x0, x1, c0, c1, epi);
-        c0 = x0;
-        c1 = x1;
-      }
-      slot = (wave + 4 * (nb - 1)) * kBK + col;
-      logz_step<D64, false, true, NT>(xs, wp, 0.0f, x0, x1, c0, c1, epi);
-    }
+    });
   }
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
@@ -3096,12 +3287,19 @@ __global__ __launch_bounds__(256) void k_assign_collect(
   }
   if (lane < PTS) {
     // ill-conditioned components, direct form, lane = point
-    const float thl = n0 + lane < n ? theta[n0 + lane] : INFINITY;
+    const int64_t row = n0 + lane;
+    const float thl = row < n ? theta[row].y : INFINITY;
     float mi = kEmpty, si = 0.0f;
     for (int ki = wave; ki < n_ill; ki += 4) {
       const int comp = ill_idx[ki];
-      const float l = (float)ill_logit<D64>(xs + lane * P, dmu + (size_t)comp * D64,
-                                            dh + (size_t)comp * D64, cdir[comp]);
+      float l;
+      if constexpr (SPL)
+        l = row < n ? (float)ill_logit_gr(x + row * d, d, vec4, dmu + (size_t)comp * D64,
+                                          dh + (size_t)comp * D64, cdir[comp])
+                    : -INFINITY;
+      else
+        l = (float)ill_logit<D64>(xs + lane * P, dmu + (size_t)comp * D64,
+                                  dh + (size_t)comp * D64, cdir[comp]);
       if (l >= thl && l > -INFINITY) {
         const int pos = atomicAdd(&ccnt[lane], 1);
         if (pos < kACap) cand[lane][pos] = -(comp + 1);
@@ -3135,10 +3333,15 @@ __global__ __launch_bounds__(256) void k_assign_collect(
     const int p = lane;
     const int cnt = ccnt[p];
     if (cnt <= kACap && n0 + p < n) {
+      // the direct form of the routed components (fp64, log2 units) in natural
+      // log: LDS rows are 16-byte aligned, global ones when vec4
+      const float* xr = SPL ? x + (n0 + p) * d : xs + p * P;
+      const int v4 = SPL ? vec4 : 1;
       for (int j = wave; j < cnt; j += 4) {
         const int code = cand[p][j];
         const int comp = code >= 0 ? well_idx[code] : -code - 1;
-        cl[p][j] = ell64(xs + p * P, mu + (size_t)comp * d, var + (size_t)comp * d, cdir[comp], d);
+        cl[p * kACap + j] = kLn2 * ill_logit_gr(xr, d, v4, dmu + (size_t)comp * D64,
+                                                dh + (size_t)comp * D64, cdir[comp]);
       }
     }
   }
@@ -3170,7 +3373,7 @@ __global__ __launch_bounds__(256) void k_assign_collect(
     for (int j = 0; j < cnt; ++j) {
       const int code = cand[p][j];
       const int comp = code >= 0 ? well_idx[code] : -code - 1;
-      const double l = cl[p][j];
+      const double l = cl[p * kACap + j];
       lmx = fmax(lmx, l);
 #pragma unroll
       for (int q = GMM_MAX_M - 1; q >= 0; --q) {
@@ -3183,7 +3386,7 @@ __global__ __launch_bounds__(256) void k_assign_collect(
       }
     }
     double z = lnc > -INFINITY ? exp(lnc - lmx) : 0.0;
-    for (int j = 0; j < cnt; ++j) z += exp(cl[p][j] - lmx);
+    for (int j = 0; j < cnt; ++j) z += exp(cl[p * kACap + j] - lmx);
     const double lz = lmx + log(z);
 #pragma unroll
     for (int j = 0; j < GMM_MAX_M; ++j) {
@@ -4122,8 +4325,10 @@ int assign_impl(const Layout& L, const float* x, const float* w, const float* mu
   float4* wp = at<float4>(ws, L.off_wp);
   float* dmu = at<float>(ws, L.off_dmu);
   double* dh = at<double>(ws, L.off_dh);
-  float* theta = at<float>(ws, L.off_logz2);      // n floats, free during assignment
+  float2* theta = at<float2>(ws, L.off_logz2);    // n float pairs, free during assignment
   int* ovf = at<int>(ws, L.off_cslot);            // n ints, likewise
+  float2* ca = thr;                               // kpad pairs, likewise
+  bf16x8* wpb = at<bf16x8>(ws, L.off_wpb);
   const int vec4 = ((d & 3) == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0) ? 1 : 0;
   hipLaunchKernelGGL(k_prep_class, dim3(k), dim3(64), 0, st, w, mu, var, d, cls, cwell, cdir,
                      cthr);
@@ -4135,11 +4340,18 @@ int assign_impl(const Layout& L, const float* x, const float* w, const float* mu
     const int64_t toti = (int64_t)k * D64;
     hipLaunchKernelGGL(k_prep_pack_direct<D64>, dim3((unsigned)cdiv(toti, 256)), dim3(256), 0,
                        st, mu, var, d, k, dmu, dh);
+    if constexpr (screen_b16(D64)) {
+      const int64_t tb = (int64_t)(kpad / kBK) * screen_steps<D64, false>() * 64;
+      hipLaunchKernelGGL((k_prep_pack_b16<D64, false>), dim3((unsigned)cdiv(tb, 256)), dim3(256),
+                         0, st, mu, var, d, kpad, counts, well_idx, wpb);
+      hipLaunchKernelGGL(k_assign_slots, dim3((unsigned)cdiv(kpad, 256)), dim3(256), 0, st,
+                         cwell, cdir, counts, well_idx, kpad, ca);
+    }
   }
   hipLaunchKernelGGL(k_assign_theta<D64>, dim3((unsigned)L.n_wg_logz), dim3(256), 0, st, x, n, d,
-                     vec4, wp, cw, counts, m + 2, theta);
+                     vec4, wp, wpb, cw, ca, counts, m + 2, theta);
   hipLaunchKernelGGL(k_assign_collect<D64>, dim3((unsigned)L.n_wg_logz), dim3(256), 0, st, x, n,
-                     d, vec4, wp, cw, well_idx, ill_idx, dmu, dh, counts, theta, mu, var,
+                     d, vec4, wp, wpb, cw, ca, well_idx, ill_idx, dmu, dh, counts, theta, mu, var,
                      cdir, m, tau, idx, resp, ovf);
   hipLaunchKernelGGL(k_assign_fallback, dim3((unsigned)cdiv(n, 1024)), dim3(256), 0, st, x, n, d,
                      k, mu, var, cdir, m, tau, ovf, idx, resp);
