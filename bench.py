@@ -259,8 +259,8 @@ def bench_assign(args, w, x, th0, dev):
     flop = 4.0 * w.n * k * d                  # log-densities of every (point, component) pair
     rate = flop / (ms * 1e-3) / 1e12
     # both passes screen on split-bf16 MFMA (three bf16 products per fp32 product) up to 128
-    # padded dimensions, on fp32 MFMA above
-    split = padded_d(d) <= 128
+    # and above 256 padded dimensions, on fp32 MFMA in between
+    split = padded_d(d) <= 128 or padded_d(d) > 256
     peak = BF16_MFMA_PEAK_TFLOPS if split else FP32_MFMA_PEAK_TFLOPS
     how = "split-bf16 MFMA, bf16 peak" if split else "fp32 MFMA peak"
     print(json.dumps({

@@ -2928,14 +2928,15 @@ __global__ __launch_bounds__(256) void k_stats_ill(
 //      only if its responsibility is > tau.
 //   3. k_assign_fallback: points with more than kACap candidates are done
 //      exactly over all components in fp64.
-// Thresholds, fp32 screening (D64 > 128): S_T - 2 kScreenSlack for every
-// component, kScreenSlack >= the screening error of the well-conditioned ones.
-// Split-bf16 screening (D64 <= 128), from an error bound of each component: a
-// screened log-density (log2 units) is the bias plus the products of [x | x^2]
-// with [W | P]; three split products per fp32 product leave out at most
-// 3 2^-16 of the product and the fp32 accumulation adds about 52 2^-24 of the
-// running sums, so its error is at most eps = 2^-13 (with room) times the sum
-// of the magnitudes of the bias and the products.  With |x mu| <= (x^2 +
+// Thresholds, fp32 screening (128 < D64 <= 256): S_T - 2 kScreenSlack for
+// every component, kScreenSlack >= the screening error of the well-conditioned
+// ones.  Split-bf16 screening (the other widths), from an error bound of each
+// component: a screened log-density (log2 units) is the bias plus the products
+// of [x | x^2] with [W | P]; three split products per fp32 product leave out at
+// most 3 2^-16 of the product and the fp32 accumulation adds (3 D64 / 8 + 8)
+// roundings of 2^-24 of the running sums, so its error is at most eps =
+// split_eps(D64) (twice that) times the sum of the magnitudes of the bias and
+// the products.  With |x mu| <= (x^2 +
 // mu^2) / 2 and x^2 <= 2 (x - mu)^2 + 2 mu^2, that sum is at most
 // 4 (cdir_k - l_k) + A_k, l_k the exact log-density, cdir_k its value at the
 // mean and A_k = 5 (cdir_k - cwell_k) + |cwell_k|.  The arg-max components of
@@ -2947,8 +2948,14 @@ __global__ __launch_bounds__(256) void k_stats_ill(
 // whose fp64 log-densities are rounded to fp32, take theta0 less that rounding.
 constexpr int kACap = 32;
 constexpr float kScreenSlack = 1.0f;
-constexpr float kSplitEps = 0x1p-13f;
 constexpr int kTMax = GMM_MAX_M + 2;
+// eps of the split-bf16 screening error bound: twice the three left-out
+// split terms (3 2^-16 of a product) plus the roundings of the accumulation
+// chain (3 D64 / 8 MFMAs of up to five roundings each, and the bias and x^2
+// in fp32), each 2^-24 of a running sum
+__host__ __device__ constexpr float split_eps(int D64) {
+  return 2.0f * (3.0f * 0x1p-16f + (3.0f * D64 / 8.0f + 8.0f) * 0x1p-24f);
+}
 
 // fp64 direct-form log-density (natural log) of component comp at point xr
 // (fp32 row, LDS or global memory), from the caller's fp32 parameters and the
@@ -3041,6 +3048,43 @@ __device__ __forceinline__ void assign_screen(const float* xs, const bf16x8* xa,
   const int tid = threadIdx.x, wave = tid >> 6, col = tid & 31;
   const int nb = n_wkb > wave ? (n_wkb - wave + 3) / 4 : 0;
   if (nb == 0) return;
+  if constexpr (screen_x16(D64)) {
+    // GB blocks at a time from the fp32 tile, as in k_logz: blocks wave + 4 i,
+    // i = GB g + j; a group's missing blocks repeat its last one and are not
+    // taken in
+    constexpr int GB = 4;
+    const int ng = (nb + GB - 1) / GB;
+    int kbc[GB], kbp[GB];
+    float cbc[GB], bc[GB], bp[GB];
+    f16v na[GB], nc[GB];
+    int nvp = 0;
+    auto epi16 = [&](int j, int v, float l) { epi(v, l, l, kbp[j] * kBK + col, bp[j]); };
+    for (int g = 0; g <= ng; ++g) {
+      if (g < ng) {
+#pragma unroll
+        for (int j = 0; j < GB; ++j) {
+          const int i = GB * g + j < nb ? GB * g + j : nb - 1;
+          kbc[j] = wave + 4 * i;
+          cbc[j] = cw[kbc[j] * kBK + col];
+          bc[j] = pre(kbc[j] * kBK + col);
+        }
+        if (g == 0)
+          logz_group16<D64, GB, true, false>(xs, wpb, kbc, cbc, na, nc, 0, epi16);
+        else
+          logz_group16<D64, GB, true, true>(xs, wpb, kbc, cbc, na, nc, nvp, epi16);
+      } else if (ng > 0) {
+        logz_group16<D64, GB, false, true>(xs, wpb, kbc, cbc, na, nc, nvp, epi16);
+      }
+#pragma unroll
+      for (int j = 0; j < GB; ++j) {
+        nc[j] = na[j];
+        kbp[j] = kbc[j];
+        bp[j] = bc[j];
+      }
+      nvp = nb - GB * g < GB ? nb - GB * g : GB;
+    }
+    return;
+  }
   f16v c0, c1, x0, x1;
   int slot = 0;
   float bv = 0.0f, bn = pre(wave * kBK + col);
@@ -3083,17 +3127,21 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_assign_theta(
     const float2* __restrict__ ca, const int* __restrict__ counts, int tsel,
     float2* __restrict__ theta) {
   constexpr int P = D64 + 4, NT = logz_tiles(D64), PTS = 32 * NT;
-  constexpr bool SPL = screen_b16(D64);
+  // SPL: split tile in LDS; SPB: split-bf16 screening (from the split tile or,
+  // D64 > 256, from the fp32 tile), whose thresholds need the arg-max slots
+  constexpr bool SPL = screen_b16(D64), SPB = screen_split(D64);
   constexpr int RPV = 4 * screen_steps<D64, false>() + 1;
-  // SPL: the split tile, whose space the lane-state maxima and their arg-max
-  // slots take over after the screening; else the fp32 tile and the maxima
+  constexpr float kEps = split_eps(D64);
+  // SPB: the X tile (split or fp32), whose space the lane-state maxima and their
+  // arg-max slots take over after the screening; else the fp32 tile and the
+  // maxima
   constexpr size_t XB = SPL ? (size_t)PTS * RPV * sizeof(bf16x8) : (size_t)PTS * P * sizeof(float);
-  constexpr size_t LB = (size_t)PTS * 129 * (SPL ? sizeof(float2) : sizeof(float));
-  constexpr size_t SB = SPL ? (XB > LB ? XB : LB) : XB + LB;
+  constexpr size_t LB = (size_t)PTS * 129 * (SPB ? sizeof(float2) : sizeof(float));
+  constexpr size_t SB = SPB ? (XB > LB ? XB : LB) : XB + LB;
   __shared__ __align__(16) unsigned char smem[SB];
   float* const xs = reinterpret_cast<float*>(smem);
   bf16x8* const xa = reinterpret_cast<bf16x8*>(smem);
-  float* const lmx = reinterpret_cast<float*>(smem + (SPL ? 0 : XB));      // [PTS][129]
+  float* const lmx = reinterpret_cast<float*>(smem + XB);                  // [PTS][129]
   float2* const lma = reinterpret_cast<float2*>(smem);                     // [PTS][129]
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, h = lane >> 5, col = lane & 31;
   const int64_t n0 = (int64_t)blockIdx.x * PTS;
@@ -3109,18 +3157,18 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_assign_theta(
   }
   assign_screen<D64>(xs, xa, wp, wpb, cw, counts[2], [](int) { return 0.0f; },
                      [&](int v, float l0, float l1, int slot, float) {
-    if constexpr (SPL) {
+    if constexpr (SPB) {
       a0[v] = l0 > m0[v] ? slot : a0[v];
       if constexpr (NT == 2) a1[v] = l1 > m1[v] ? slot : a1[v];
     }
     m0[v] = fmaxf(m0[v], l0);
     if constexpr (NT == 2) m1[v] = fmaxf(m1[v], l1);
   });
-  if constexpr (SPL) __syncthreads();        // the maxima take over the split tile
+  if constexpr (SPB) __syncthreads();        // the maxima take over the tile
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
     const int p = 8 * (v >> 2) + 4 * h + (v & 3);
-    if constexpr (SPL) {
+    if constexpr (SPB) {
       lma[p * 129 + wave * 32 + col] = make_float2(m0[v], __int_as_float(a0[v]));
       if constexpr (NT == 2) lma[(32 + p) * 129 + wave * 32 + col] = make_float2(m1[v], __int_as_float(a1[v]));
     } else {
@@ -3152,7 +3200,7 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_assign_theta(
     for (int c = LPT * r; c < LPT * r + LPT; ++c) {
       float v;
       int a = -1;
-      if constexpr (SPL) {
+      if constexpr (SPB) {
         const float2 e = lma[p * 129 + c];
         v = e.x;
         a = __float_as_int(e.y);
@@ -3181,19 +3229,19 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_assign_theta(
     for (int j = 0; j < kTMax; ++j)
       if (j == tsel - 1) st = tl[j];
     float2 out;
-    if constexpr (SPL) {
+    if constexpr (SPB) {
       float dm = 0.0f;
 #pragma unroll
       for (int j = 0; j < kTMax; ++j) {
         if (j < tsel && ta[j] >= 0) {
           const float2 e = ca[ta[j]];
-          dm = fmaxf(dm, kSplitEps * (4.0f * fmaxf(e.x - st, 0.0f) + e.y));
+          dm = fmaxf(dm, kEps * (4.0f * fmaxf(e.x - st, 0.0f) + e.y));
         }
       }
-      const float th0 = st - dm / (1.0f - 4.0f * kSplitEps);
+      const float th0 = st - dm / (1.0f - 4.0f * kEps);
       // fp32 rounding of these few operations: 2^-20 of the magnitude
       const float mg = 0x1p-20f * (fabsf(th0) + 1.0f);
-      out = make_float2(th0 * (1.0f + 4.0f * kSplitEps) - mg, th0 - 0x1p-22f * (fabsf(th0) + 1.0f) - mg);
+      out = make_float2(th0 * (1.0f + 4.0f * kEps) - mg, th0 - 0x1p-22f * (fabsf(th0) + 1.0f) - mg);
     } else {
       out = make_float2(st - 2.0f * kScreenSlack, st - 2.0f * kScreenSlack);
     }
@@ -3246,9 +3294,9 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_assign_collect
   {
     // the slot's share b_j of its candidate threshold (0 for the fp32 screening)
     auto pre = [&](int slot) {
-      if constexpr (SPL) {
+      if constexpr (screen_split(D64)) {
         const float2 e = ca[slot];
-        return kSplitEps * (4.0f * e.x + e.y);
+        return split_eps(D64) * (4.0f * e.x + e.y);
       } else {
         return 0.0f;
       }
@@ -4340,7 +4388,7 @@ int assign_impl(const Layout& L, const float* x, const float* w, const float* mu
     const int64_t toti = (int64_t)k * D64;
     hipLaunchKernelGGL(k_prep_pack_direct<D64>, dim3((unsigned)cdiv(toti, 256)), dim3(256), 0,
                        st, mu, var, d, k, dmu, dh);
-    if constexpr (screen_b16(D64)) {
+    if constexpr (screen_split(D64)) {
       const int64_t tb = (int64_t)(kpad / kBK) * screen_steps<D64, false>() * 64;
       hipLaunchKernelGGL((k_prep_pack_b16<D64, false>), dim3((unsigned)cdiv(tb, 256)), dim3(256),
                          0, st, mu, var, d, kpad, counts, well_idx, wpb);
