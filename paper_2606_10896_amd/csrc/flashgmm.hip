@@ -3334,20 +3334,25 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_assign_collect
     }
   }
   if (lane < PTS) {
-    // ill-conditioned components, direct form, lane = point
+    // ill-conditioned components, direct form, lane = point.  A component more
+    // than 64 log2 units below the point's threshold (so below 2^-62 of its
+    // mass) is left out of the normaliser: its sum stops early (most of them
+    // after 16 dimensions), as in k_logz.
     const int64_t row = n0 + lane;
     const float thl = row < n ? theta[row].y : INFINITY;
+    const float* xr = SPL ? x + (row < n ? row : 0) * d : xs + lane * P;
     float mi = kEmpty, si = 0.0f;
     for (int ki = wave; ki < n_ill; ki += 4) {
       const int comp = ill_idx[ki];
+      const double c = cdir[comp];
+      const double bnd = c - ((double)thl - 64.0);
       float l;
       if constexpr (SPL)
-        l = row < n ? (float)ill_logit_gr(x + row * d, d, vec4, dmu + (size_t)comp * D64,
-                                          dh + (size_t)comp * D64, cdir[comp])
-                    : -INFINITY;
+        l = (float)ill_logit_bounded_gr(xr, d, vec4, dmu + (size_t)comp * D64,
+                                        dh + (size_t)comp * D64, c, bnd);
       else
-        l = (float)ill_logit<D64>(xs + lane * P, dmu + (size_t)comp * D64,
-                                  dh + (size_t)comp * D64, cdir[comp]);
+        l = (float)ill_logit_bounded<D64>(xr, dmu + (size_t)comp * D64,
+                                          dh + (size_t)comp * D64, c, bnd);
       if (l >= thl && l > -INFINITY) {
         const int pos = atomicAdd(&ccnt[lane], 1);
         if (pos < kACap) cand[lane][pos] = -(comp + 1);
