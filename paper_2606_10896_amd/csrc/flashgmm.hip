@@ -759,17 +759,24 @@ __device__ __forceinline__ void logz_step16(const bf16x8* xa, const bf16x8* __re
 // during pair-step q.  EPI: the previous group's log-densities c[j] (blocks
 // j < nvp) are taken in by epi(j, v, value) during the first eight pair-steps,
 // eight values each (fixed register indices).
-template <int D64, int GB, bool MF, bool EPI, class Epi>
+// ISO (tied variances): the x part only, then one step for ||x||^2: each lane
+// sums the squares of its values (eight a pair-step, then over the
+// pair-steps), the two lane halves' sums are added, and lane half 0 meets
+// -1/2 log2(e) / var in three bf16 pieces with the three bf16 pieces of the
+// norm (the operand layout of k_prep_pack_b16<D64, true>).
+template <int D64, int GB, bool MF, bool EPI, bool ISO, class Epi>
 __device__ __forceinline__ void logz_group16(const float* xs, const bf16x8* __restrict__ wpb,
                                              const int (&kb)[GB], const float (&cb)[GB],
                                              f16v (&n)[GB], const f16v (&c)[GB], int nvp,
                                              Epi&& epi) {
-  constexpr int P = D64 + 4, NQ = D64 / 16, NS = D64 / 8;
-  constexpr size_t BS = (size_t)NS * 64 * 2;
+  constexpr int P = D64 + 4, NQ = D64 / 16;
+  constexpr size_t BS = (size_t)screen_steps<D64, ISO>() * 64 * 2;
+  constexpr int NB = ISO ? 2 : 4;                 // B operands a block and pair-step
   static_assert(NQ % 8 == 0 && 16 * GB == 64, "eight pair-steps of eight epilogue values");
   const int lane = threadIdx.x & 63, h = lane >> 5, col = lane & 31;
   const float* xr = xs + col * P + 8 * h;
-  bf16x8 bw[2][GB][4];                            // ring of two pair-steps of B operands
+  bf16x8 bw[2][GB][NB];                           // ring of two pair-steps of B operands
+  float ssq = 0.0f;                               // ISO: this lane's sum of squares
   auto load_b = [&](auto slot, int q) {
     constexpr int sl = decltype(slot)::value;
 #pragma unroll
@@ -777,8 +784,10 @@ __device__ __forceinline__ void logz_group16(const float* xs, const bf16x8* __re
       const bf16x8* w = wpb + (size_t)kb[j] * BS;
       bw[sl][j][0] = w[2 * (q * 64 + lane)];
       bw[sl][j][1] = w[2 * (q * 64 + lane) + 1];
-      bw[sl][j][2] = w[2 * ((q + NQ) * 64 + lane)];
-      bw[sl][j][3] = w[2 * ((q + NQ) * 64 + lane) + 1];
+      if constexpr (!ISO) {
+        bw[sl][j][2] = w[2 * ((q + NQ) * 64 + lane)];
+        bw[sl][j][3] = w[2 * ((q + NQ) * 64 + lane) + 1];
+      }
     }
   };
   if (MF) {
@@ -796,28 +805,36 @@ __device__ __forceinline__ void logz_group16(const float* xs, const bf16x8* __re
       const float4 u1 = *reinterpret_cast<const float4*>(xr + 16 * q + 4);
       const float v8[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
       bf16x8 xh, xl, qh, ql;
+      float sq8 = 0.0f;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const __bf16 vh = (__bf16)v8[e];
         xh[e] = vh;
         xl[e] = (__bf16)(v8[e] - (float)vh);
         const float sq = v8[e] * v8[e];
-        const __bf16 sh = (__bf16)sq;
-        qh[e] = sh;
-        ql[e] = (__bf16)(sq - (float)sh);
+        if constexpr (ISO) {
+          sq8 += sq;
+        } else {
+          const __bf16 sh = (__bf16)sq;
+          qh[e] = sh;
+          ql[e] = (__bf16)(sq - (float)sh);
+        }
       }
+      if constexpr (ISO) ssq += sq8;
 #pragma unroll
       for (int j = 0; j < GB; ++j) n[j] = mfma32b(xh, bw[sl][j][0], n[j]);
 #pragma unroll
       for (int j = 0; j < GB; ++j) n[j] = mfma32b(xh, bw[sl][j][1], n[j]);
 #pragma unroll
       for (int j = 0; j < GB; ++j) n[j] = mfma32b(xl, bw[sl][j][0], n[j]);
+      if constexpr (!ISO) {
 #pragma unroll
-      for (int j = 0; j < GB; ++j) n[j] = mfma32b(qh, bw[sl][j][2], n[j]);
+        for (int j = 0; j < GB; ++j) n[j] = mfma32b(qh, bw[sl][j][2], n[j]);
 #pragma unroll
-      for (int j = 0; j < GB; ++j) n[j] = mfma32b(qh, bw[sl][j][3], n[j]);
+        for (int j = 0; j < GB; ++j) n[j] = mfma32b(qh, bw[sl][j][3], n[j]);
 #pragma unroll
-      for (int j = 0; j < GB; ++j) n[j] = mfma32b(ql, bw[sl][j][2], n[j]);
+        for (int j = 0; j < GB; ++j) n[j] = mfma32b(ql, bw[sl][j][2], n[j]);
+      }
     }
     if (EPI && first) {
 #pragma unroll
@@ -839,6 +856,31 @@ __device__ __forceinline__ void logz_group16(const float* xs, const bf16x8* __re
     step(std::integral_constant<int, 1>{}, std::integral_constant<int, 5>{}, q0 + 5, first);
     step(std::integral_constant<int, 0>{}, std::integral_constant<int, 6>{}, q0 + 6, first);
     step(std::integral_constant<int, 1>{}, std::integral_constant<int, 7>{}, q0 + 7, first);
+  }
+  if constexpr (ISO) {
+    if (MF) {
+      // the norm step: ||x||^2 of point col in three bf16 pieces, in places
+      // 0..2 and 3..5 of lane half 0, against the step's (hi, lo) operands
+      const float nrm = ssq + __shfl_xor(ssq, 32);
+      const __bf16 p0 = (__bf16)nrm;
+      const float r1 = nrm - (float)p0;
+      const __bf16 p1 = (__bf16)r1;
+      const __bf16 p2 = (__bf16)(r1 - (float)p1);
+      bf16x8 a;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) a[e] = (__bf16)0.0f;
+      if (h == 0) {
+        a[0] = a[3] = p0;
+        a[1] = a[4] = p1;
+        a[2] = a[5] = p2;
+      }
+#pragma unroll
+      for (int j = 0; j < GB; ++j) {
+        const bf16x8* w = wpb + (size_t)kb[j] * BS;
+        n[j] = mfma32b(a, w[2 * (NQ * 64 + lane)], n[j]);
+        n[j] = mfma32b(a, w[2 * (NQ * 64 + lane) + 1], n[j]);
+      }
+    }
   }
 }
 
@@ -1009,7 +1051,7 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
     unsigned char* __restrict__ lflag) {
   constexpr int P = D64 + 4, NT = logz_tiles(D64), PTS = 32 * NT;
   constexpr bool B16 = screen_b16(D64);
-  static_assert(!ISO || B16, "the isotropic screening tile is a split-bf16 one");
+  static_assert(!ISO || screen_split(D64), "the isotropic screening is a split-bf16 one");
   // split tile row: [x | x^2] chunks (hi, lo), or for ISO the x chunks, one
   // ||x||^2 chunk and one zero chunk; one padding entry
   constexpr int NSTEP = screen_steps<D64, ISO>();
@@ -1166,11 +1208,11 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
             cbc[j] = cw[kbc[j] * kBK + col];
           }
           if (g == 0)
-            logz_group16<D64, GB, true, false>(xs, wpb, kbc, cbc, na, nc, 0, epi16);
+            logz_group16<D64, GB, true, false, ISO>(xs, wpb, kbc, cbc, na, nc, 0, epi16);
           else
-            logz_group16<D64, GB, true, true>(xs, wpb, kbc, cbc, na, nc, nvp, epi16);
+            logz_group16<D64, GB, true, true, ISO>(xs, wpb, kbc, cbc, na, nc, nvp, epi16);
         } else if (ng > 0) {
-          logz_group16<D64, GB, false, true>(xs, wpb, kbc, cbc, na, nc, nvp, epi16);
+          logz_group16<D64, GB, false, true, ISO>(xs, wpb, kbc, cbc, na, nc, nvp, epi16);
         }
         // this group's log-densities become the previous group's
 #pragma unroll
@@ -3069,11 +3111,11 @@ __device__ __forceinline__ void assign_screen(const float* xs, const bf16x8* xa,
           bc[j] = pre(kbc[j] * kBK + col);
         }
         if (g == 0)
-          logz_group16<D64, GB, true, false>(xs, wpb, kbc, cbc, na, nc, 0, epi16);
+          logz_group16<D64, GB, true, false, false>(xs, wpb, kbc, cbc, na, nc, 0, epi16);
         else
-          logz_group16<D64, GB, true, true>(xs, wpb, kbc, cbc, na, nc, nvp, epi16);
+          logz_group16<D64, GB, true, true, false>(xs, wpb, kbc, cbc, na, nc, nvp, epi16);
       } else if (ng > 0) {
-        logz_group16<D64, GB, false, true>(xs, wpb, kbc, cbc, na, nc, nvp, epi16);
+        logz_group16<D64, GB, false, true, false>(xs, wpb, kbc, cbc, na, nc, nvp, epi16);
       }
 #pragma unroll
       for (int j = 0; j < GB; ++j) {
@@ -4246,9 +4288,15 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
     hipLaunchKernelGGL(k_prep_pack_well<D64>, dim3((unsigned)cdiv(tot, 256)), dim3(256), 0, st,
                        mu, var, d, kpad, cwell, cthr, counts, well_idx, wp, cw, thr);
     if constexpr (screen_x16(D64)) {
-      const int64_t tb = (int64_t)(kpad / kBK) * screen_steps<D64, false>() * 64;
-      hipLaunchKernelGGL((k_prep_pack_b16<D64, false>), dim3((unsigned)cdiv(tb, 256)), dim3(256),
-                         0, st, mu, var, d, kpad, counts, well_idx, wpb);
+      if (L.iso && L.refine) {
+        const int64_t tb = (int64_t)(kpad / kBK) * screen_steps<D64, true>() * 64;
+        hipLaunchKernelGGL((k_prep_pack_b16<D64, true>), dim3((unsigned)cdiv(tb, 256)), dim3(256),
+                           0, st, mu, var, d, kpad, counts, well_idx, wpb);
+      } else {
+        const int64_t tb = (int64_t)(kpad / kBK) * screen_steps<D64, false>() * 64;
+        hipLaunchKernelGGL((k_prep_pack_b16<D64, false>), dim3((unsigned)cdiv(tb, 256)),
+                           dim3(256), 0, st, mu, var, d, kpad, counts, well_idx, wpb);
+      }
     }
     if constexpr (screen_b16(D64)) {
       if (L.iso) {
@@ -4275,7 +4323,7 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
   }
   tm = phase_mark(1, st) && tm;
   bool launched = false;
-  if constexpr (screen_b16(D64)) {
+  if constexpr (screen_split(D64)) {
     if (L.iso && L.refine) {
       hipLaunchKernelGGL((k_logz<D64, true, true>), dim3((unsigned)L.n_wg_logz), dim3(256), 0, st,
                          x, n, d, vec4, wp, wpb, cw, thr, well_idx, ill_idx, dmu, dh, cdir, counts,
