@@ -2168,9 +2168,14 @@ __global__ __launch_bounds__(256, D64 <= 128 ? 2 : 1) void k_stats_well(
 // r = 2^(sum) (refined pairs set to 0) and each wave contracts r^T [x | x^2]
 // over its own dimensions into fp32 accumulators, folded into the
 // workgroup's fp64 partial every kFlushWide tiles.  N_k is summed by wave 0.
+// ISO (tied variances, every P of a component equal): per lane and pair of its
+// four dimensions one step with the pair's sum of squares in place of the two
+// x^2 steps, and for the statistics r^T x on MFMA while r ||x||^2 (each wave
+// over its dimensions) is summed on the vector ALU into the first Q entry of
+// the wave's dimensions; the isotropic Q is the sum of Q over the dimensions.
 constexpr int kFlushWide = 256;
 
-template <int DW>
+template <int DW, bool ISO>
 __global__ __launch_bounds__(64 * (DW / 128)) void k_stats_wide(
     const float* __restrict__ x, int64_t n, int d, int vec4, const float* __restrict__ wq,
     const double* __restrict__ cwell, const int* __restrict__ well_idx,
@@ -2265,10 +2270,12 @@ __global__ __launch_bounds__(64 * (DW / 128)) void k_stats_wide(
     }
   };
 
-  f4v acc[2 * NBQ];
+  constexpr int NACC = ISO ? NBQ : 2 * NBQ;
+  f4v acc[NACC];
 #pragma unroll
-  for (int c = 0; c < 2 * NBQ; ++c) acc[c] = f4v{0.f, 0.f, 0.f, 0.f};
+  for (int c = 0; c < NACC; ++c) acc[c] = f4v{0.f, 0.f, 0.f, 0.f};
   float nkacc = 0.0f;
+  float qacc = 0.0f;                            // ISO: sum of r ||x||^2 over this wave's dims
   bool first = true;
   // fp32 accumulators -> fp64 partial.  Register v of block c at lane l is
   // column 4(l/16) + v of the block: local dimension 64 (c/4 % NG) + 4 (4 k4 + v) + c % 4.
@@ -2286,13 +2293,25 @@ __global__ __launch_bounds__(64 * (DW / 128)) void k_stats_wide(
       double o[4];
 #pragma unroll
       for (int v = 0; v < 4; ++v) o[v] = first ? 0.0 : dst[4 * v];
+      if constexpr (ISO) {
+        if (c >= NBQ) {
+          // the wave's r ||x||^2 in its first dimension's entry, zeros elsewhere
+          float q2 = qacc + __shfl_xor(qacc, 16);
+          q2 += __shfl_xor(q2, 32);
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+            dst[4 * v] = o[v] + (c == NBQ && k4 == 0 && v == 0 ? (double)q2 : 0.0);
+          continue;
+        }
+      }
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        dst[4 * v] = o[v] + (double)acc[c][v];
-        acc[c][v] = 0.0f;
+        dst[4 * v] = o[v] + (double)acc[c % NACC][v];
+        acc[c % NACC][v] = 0.0f;
       }
     }
     nkacc = 0.0f;
+    qacc = 0.0f;
     first = false;
   };
 
@@ -2353,20 +2372,39 @@ __global__ __launch_bounds__(64 * (DW / 128)) void k_stats_wide(
     // components over this wave's dimensions, 16 dimensions per fp32 sum
     double t64[4] = {0.0, 0.0, 0.0, 0.0};
     const float* xr = &xs[wave][i16 * P + 4 * k4];
+    float ssl = 0.0f;                           // ISO: point i16's squares over this lane's dims
 #pragma unroll
     for (int q = 0; q < DQ / 16; ++q) {
       const float4 u = *reinterpret_cast<const float4*>(xr + 16 * q);
       f4v la = {0.f, 0.f, 0.f, 0.f};
-      la = mfma16(u.x, wb[4 * q], la);
-      la = mfma16(u.x * u.x, wb[SW + 4 * q], la);
-      la = mfma16(u.y, wb[4 * q + 1], la);
-      la = mfma16(u.y * u.y, wb[SW + 4 * q + 1], la);
-      la = mfma16(u.z, wb[4 * q + 2], la);
-      la = mfma16(u.z * u.z, wb[SW + 4 * q + 2], la);
-      la = mfma16(u.w, wb[4 * q + 3], la);
-      la = mfma16(u.w * u.w, wb[SW + 4 * q + 3], la);
+      if constexpr (ISO) {
+        // P of the lane's first dimension: equal for its four (zero x past d)
+        const float sxy = u.x * u.x + u.y * u.y, szw = u.z * u.z + u.w * u.w;
+        ssl += sxy + szw;
+        la = mfma16(u.x, wb[4 * q], la);
+        la = mfma16(u.y, wb[4 * q + 1], la);
+        la = mfma16(sxy, wb[SW + 4 * q], la);
+        la = mfma16(u.z, wb[4 * q + 2], la);
+        la = mfma16(u.w, wb[4 * q + 3], la);
+        la = mfma16(szw, wb[SW + 4 * q], la);
+      } else {
+        la = mfma16(u.x, wb[4 * q], la);
+        la = mfma16(u.x * u.x, wb[SW + 4 * q], la);
+        la = mfma16(u.y, wb[4 * q + 1], la);
+        la = mfma16(u.y * u.y, wb[SW + 4 * q + 1], la);
+        la = mfma16(u.z, wb[4 * q + 2], la);
+        la = mfma16(u.z * u.z, wb[SW + 4 * q + 2], la);
+        la = mfma16(u.w, wb[4 * q + 3], la);
+        la = mfma16(u.w * u.w, wb[SW + 4 * q + 3], la);
+      }
 #pragma unroll
       for (int v = 0; v < 4; ++v) t64[v] += (double)la[v];
+    }
+    // ISO: point i16's ||x||^2 over this wave's dimensions (the four lane groups)
+    float ssw = 0.0f;
+    if constexpr (ISO) {
+      ssw = ssl + __shfl_xor(ssl, 16);
+      ssw += __shfl_xor(ssw, 32);
     }
 #pragma unroll
     for (int v = 0; v < 4; ++v) lpart[wave][v][lane] = t64[v];
@@ -2387,6 +2425,7 @@ __global__ __launch_bounds__(64 * (DW / 128)) void k_stats_wide(
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
       const float* yr = &xs[wave][(4 * k4 + v) * P + 4 * i16];
+      if constexpr (ISO) qacc += r[v] * __shfl(ssw, 4 * k4 + v);
 #pragma unroll
       for (int gg = 0; gg < NG; ++gg) {
         const float4 y = *reinterpret_cast<const float4*>(yr + 64 * gg);
@@ -2394,10 +2433,12 @@ __global__ __launch_bounds__(64 * (DW / 128)) void k_stats_wide(
         acc[4 * gg + 1] = mfma16(y.y, r[v], acc[4 * gg + 1]);
         acc[4 * gg + 2] = mfma16(y.z, r[v], acc[4 * gg + 2]);
         acc[4 * gg + 3] = mfma16(y.w, r[v], acc[4 * gg + 3]);
-        acc[NBQ + 4 * gg + 0] = mfma16(y.x * y.x, r[v], acc[NBQ + 4 * gg + 0]);
-        acc[NBQ + 4 * gg + 1] = mfma16(y.y * y.y, r[v], acc[NBQ + 4 * gg + 1]);
-        acc[NBQ + 4 * gg + 2] = mfma16(y.z * y.z, r[v], acc[NBQ + 4 * gg + 2]);
-        acc[NBQ + 4 * gg + 3] = mfma16(y.w * y.w, r[v], acc[NBQ + 4 * gg + 3]);
+        if constexpr (!ISO) {
+          acc[NBQ + 4 * gg + 0] = mfma16(y.x * y.x, r[v], acc[NBQ + 4 * gg + 0]);
+          acc[NBQ + 4 * gg + 1] = mfma16(y.y * y.y, r[v], acc[NBQ + 4 * gg + 1]);
+          acc[NBQ + 4 * gg + 2] = mfma16(y.z * y.z, r[v], acc[NBQ + 4 * gg + 2]);
+          acc[NBQ + 4 * gg + 3] = mfma16(y.w * y.w, r[v], acc[NBQ + 4 * gg + 3]);
+        }
       }
     }
     if ((tiles % kFlushWide) == kFlushWide - 1) flush();
@@ -4382,9 +4423,14 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
                          dim3(256), 0, st, x, n, d, vec4, wq, cw, counts, logz2, cslot, bmask,
                          L.nch, L.chunk, sflag, lflag, part_w);
   } else {
-    hipLaunchKernelGGL(k_stats_wide<D64>, dim3((unsigned)((kpad / 16) * L.nch)),
-                       dim3(64 * (D64 / 128)), 0, st, x, n, d, vec4, wq, cwell, well_idx, counts,
-                       logz2, cslot, bmask, L.nch, L.chunk, sflag, lflag, part_w);
+    if (L.iso)
+      hipLaunchKernelGGL((k_stats_wide<D64, true>), dim3((unsigned)((kpad / 16) * L.nch)),
+                         dim3(64 * (D64 / 128)), 0, st, x, n, d, vec4, wq, cwell, well_idx,
+                         counts, logz2, cslot, bmask, L.nch, L.chunk, sflag, lflag, part_w);
+    else
+      hipLaunchKernelGGL((k_stats_wide<D64, false>), dim3((unsigned)((kpad / 16) * L.nch)),
+                         dim3(64 * (D64 / 128)), 0, st, x, n, d, vec4, wq, cwell, well_idx,
+                         counts, logz2, cslot, bmask, L.nch, L.chunk, sflag, lflag, part_w);
   }
   tm = phase_mark(4, st) && tm;
   hipLaunchKernelGGL(k_stats_ill<D64>, dim3((unsigned)L.grid_i), dim3(256), 0, st, x, n, d, vec4,
