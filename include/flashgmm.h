@@ -162,7 +162,12 @@ int gmm_fit_screened(const float* x, int64_t n, int32_t d, int32_t k, int32_t n_
  * strictly greater than tau (the paper uses m = 2, tau = 1/K).
  *   idx  [n*m] int32: component indices, -1 for an empty slot
  *   resp [n*m] fp32 : their responsibilities, 0 for an empty slot
- * 1 <= m <= GMM_MAX_M and m <= k; 0 <= tau < 1.
+ * 1 <= m <= GMM_MAX_M and m <= k; 0 <= tau < 1.  The ranking is exact: a
+ * screening pass bounds its own error per component, every component that
+ * can be among a point's m + 2 largest is recomputed in fp64 and ranked (all
+ * k in fp64 when more than 32 qualify).  A responsibility divides the exact
+ * term by a normaliser whose part from the other components keeps the
+ * screening's error (within 1e-4 of exact in the tests).
  */
 int gmm_assign_topk(const float* x, int64_t n, int32_t d, int32_t k, const float* weights,
                     const float* means, const float* vars, int32_t m, float tau, int32_t* idx,
