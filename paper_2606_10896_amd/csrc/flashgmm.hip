@@ -2632,7 +2632,11 @@ __global__ __launch_bounds__(256) void k_stats_sparse(
     const int64_t* __restrict__ goff, int nunit, int nparts, double* __restrict__ part) {
   constexpr int C = sparse_cb(D64), CW = C / 4;
   constexpr int STRIDE = 1 + 2 * D64;
-  constexpr int NB = D64 <= 64 ? 64 : 4096 / D64;
+  // pairs per batch: as many as a wave has lanes up to 128 dimensions (one
+  // record per lane), 16 from 512 dimensions (two batches of rows then take
+  // 64 to 128 KB of LDS: one workgroup per compute unit, more rows in flight)
+  constexpr int NB = D64 <= 128 ? 64 : (D64 <= 256 ? 4096 / D64 : 16);
+  static_assert(NB <= 64, "a batch's records are held one per lane");
   constexpr int CPR = D64 / 4;                   // float4 chunks per row
   constexpr int GQ = (NB * CPR + 255) / 256;     // float4 gathered per thread and batch
   __shared__ __align__(16) float xb[2][NB * D64];
