@@ -3356,6 +3356,7 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_assign_collect
   constexpr size_t SB = SPL ? XB : XB + CB;
   __shared__ __align__(16) unsigned char smem[SB];
   __shared__ int ccnt[PTS];
+  __shared__ int eoff[PTS + 1];            // first entry of each point's candidates
   __shared__ int cand[PTS][kACap];         // well slot s >= 0, or -(ill component + 1)
   __shared__ float2 stw[4][PTS];
   __shared__ float2 sti[4][PTS];
@@ -3467,22 +3468,61 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_assign_collect
       }
     }
   }
+  if (tid == 0) {
+    // the (point, candidate) entries in point order: each point's first entry
+    // (points past n and overflowing lists have none)
+    int acc = 0;
+    for (int p = 0; p < PTS; ++p) {
+      eoff[p] = acc;
+      const int c = ccnt[p];
+      acc += (c <= kACap && n0 + p < n) ? c : 0;
+    }
+    eoff[PTS] = acc;
+  }
   __syncthreads();
-  if (lane < PTS) {
-    // exact fp64 log-densities of the candidates, spread over the waves
-    const int p = lane;
-    const int cnt = ccnt[p];
-    if (cnt <= kACap && n0 + p < n) {
-      // the direct form of the routed components (fp64, log2 units) in natural
-      // log: LDS rows are 16-byte aligned, global ones when vec4
+  {
+    // exact fp64 log-densities of the candidates: kRefLanes lanes per entry,
+    // lane g summing the direct form over the float4 chunks g, g + kRefLanes,
+    // ... of the row (coalesced over the group; global rows when SPL), the
+    // group's partial sums added in a fixed butterfly order; log2 units, then
+    // natural log
+    constexpr int G = kRefLanes;
+    const int g = tid & (G - 1);
+    const int total = eoff[PTS];
+    for (int e = tid / G; e < total; e += 256 / G) {
+      // the entry's point: the last one whose first entry is <= e
+      int p = 0;
+      for (int s = PTS / 2; s > 0; s >>= 1)
+        if (p + s < PTS && eoff[p + s] <= e) p += s;
+      const int j = e - eoff[p];
+      const int code = cand[p][j];
+      const int comp = code >= 0 ? well_idx[code] : -code - 1;
       const float* xr = SPL ? x + (n0 + p) * d : xs + p * P;
-      const int v4 = SPL ? vec4 : 1;
-      for (int j = wave; j < cnt; j += 4) {
-        const int code = cand[p][j];
-        const int comp = code >= 0 ? well_idx[code] : -code - 1;
-        cl[p * kACap + j] = kLn2 * ill_logit_gr(xr, d, v4, dmu + (size_t)comp * D64,
-                                                dh + (size_t)comp * D64, cdir[comp]);
+      const float* mu = dmu + (size_t)comp * D64;
+      const double* hh = dh + (size_t)comp * D64;
+      const bool v4 = !SPL || vec4;
+      double acc = 0.0;
+      for (int c4 = 4 * g; c4 < d; c4 += 4 * G) {
+        float xv[4];
+        if (v4 && c4 + 4 <= d) {
+          const float4 t4 = *reinterpret_cast<const float4*>(xr + c4);
+          xv[0] = t4.x; xv[1] = t4.y; xv[2] = t4.z; xv[3] = t4.w;
+        } else {
+#pragma unroll
+          for (int u = 0; u < 4; ++u) xv[u] = c4 + u < d ? xr[c4 + u] : 0.0f;
+        }
+        const float4 m4 = *reinterpret_cast<const float4*>(mu + c4);
+        const double2 h0 = *reinterpret_cast<const double2*>(hh + c4);
+        const double2 h1 = *reinterpret_cast<const double2*>(hh + c4 + 2);
+        double t;
+        t = (double)xv[0] - (double)m4.x; acc = fma(t * t, h0.x, acc);
+        t = (double)xv[1] - (double)m4.y; acc = fma(t * t, h0.y, acc);
+        t = (double)xv[2] - (double)m4.z; acc = fma(t * t, h1.x, acc);
+        t = (double)xv[3] - (double)m4.w; acc = fma(t * t, h1.y, acc);
       }
+#pragma unroll
+      for (int o = 1; o < G; o <<= 1) acc += __shfl_xor(acc, o);
+      if (g == 0) cl[p * kACap + j] = kLn2 * (cdir[comp] - acc);
     }
   }
   __syncthreads();
