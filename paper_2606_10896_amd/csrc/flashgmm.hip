@@ -7,11 +7,14 @@
 //   prep        per component: the expanded-form operands
 //                 W_kd = mu_kd / var_kd,  P_kd = -1/2 / var_kd,
 //                 c_k  = log pi_k - 1/2 sum_d (mu_kd^2 / var_kd + log(2 pi var_kd))
-//               (computed in fp64, stored fp32, all pre-scaled by log2(e) so
-//               the kernels work in base 2), packed in the register order the
-//               32x32x2 fp32 MFMA consumes them.
+//               (computed in fp64, all pre-scaled by log2(e) so the kernels
+//               work in base 2), packed in the register order of the MFMA B
+//               operands: bf16 hi and lo parts for the split-bf16 screening,
+//               fp32 for the fp32 screening and the statistics.
 //   logz        Step 1 of Algorithm 1: log-densities l = [x | x^2] . [W | P]^T + c
-//               on MFMA, an online log-sum-exp over all components, one fp32
+//               on MFMA (three bf16 products per fp32 product, or fp32), an
+//               online log-sum-exp over all components, the pairs that carry
+//               a point's mass recomputed in the direct form in fp64, one fp64
 //               log-normaliser per point and per-workgroup log-likelihood
 //               partials.
 //   stats       Step 2 of Algorithm 1: the same log-densities recomputed on
@@ -591,11 +594,11 @@ __global__ __launch_bounds__(256) void k_prep_pack_direct(
 // Points per screening workgroup: two 32-point MFMA tiles while a 64-point X
 // tile fits in LDS next to the per-point state (D64 <= 256), one tile above.
 __host__ __device__ constexpr int logz_tiles(int D64) { return D64 <= 256 ? 2 : 1; }
-// The screening contraction runs on split bf16 MFMA while the split X tile fits in
-// LDS next to the fp32 one (D64 <= 128).  Its error, about 2^-16.5 per product over
-// D64/8 accumulation steps, is of the order of the fp32 chain's (2^-24 per step of a
-// running sum of some hundred log2 units over D64 steps), so the refinement rules
-// are the same for both.
+// The screening contraction runs on split bf16 MFMA from a split X tile in LDS
+// while 64 points of it fit beside the post-screening state (D64 <= 128).  Its
+// error, typically about 2^-16.5 of a product over D64/8 accumulation steps, is of
+// the order of the fp32 chain's (2^-24 per step of a running sum of some hundred
+// log2 units over D64 steps), so the refinement rules are the same for both.
 __host__ __device__ constexpr bool screen_b16(int D64) { return D64 <= 128; }
 // D64 > 256 (32-point tiles): split-bf16 screening too, the operands of the
 // points split on the fly from the fp32 tile (logz_group16)
