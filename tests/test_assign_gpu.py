@@ -39,7 +39,7 @@ def test_tiny_trained():
     (1000, 37, 6, 45, 2), (3001, 128, 40, 64, 3), (2049, 200, 10, 17, 1), (777, 256, 8, 8, 8),
     (5, 3, 2, 2, 2), (1500, 150, 7, 40, 4), (20000, 8, 4, 300, 2),
     (1200, 768, 10, 70, 2), (800, 1024, 5, 16, 3), (1500, 513, 6, 20, 2),
-    (5000, 64, 40, 4500, 2), (4300, 400, 12, 4200, 2)])
+    (5000, 64, 40, 4500, 2), (4300, 400, 12, 4200, 2), (900, 850, 6, 12, 2)])
 def test_ragged_shapes(n, d, kt, k, m):
     w = g.custom(f"a{n}_{d}_{k}", n, d, kt, k, data_seed=n + d, init_seed=k + 17)
     x, (wt, mu, var) = g.make(w)

@@ -46,7 +46,7 @@ def test_tiny_teacher_forced_all_iterations():
     (20000, 8, 4, 300), (1500, 150, 7, 40),
     # wide D: 32-point screening tiles, dimensions split over the statistics waves
     (2000, 300, 8, 24), (1500, 513, 6, 20), (1200, 768, 10, 70), (800, 1024, 5, 16),
-    (2500, 640, 12, 33), (900, 1000, 4, 9)])
+    (2500, 640, 12, 33), (900, 1000, 4, 9), (1800, 450, 9, 28), (1000, 850, 6, 20)])
 def test_ragged_shapes(n, d, kt, k):
     """Shapes off every tile boundary: points, dimensions and components."""
     w = g.custom(f"r{n}_{d}_{k}", n, d, kt, max(k, 1), data_seed=n + d, init_seed=k + 17)
