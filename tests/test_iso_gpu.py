@@ -39,7 +39,8 @@ def _teacher_forced(x, thetas, label, xd=None):
 
 
 @pytest.mark.parametrize("n,d,kt,k", [(2000, 37, 5, 7), (3000, 128, 20, 64), (1800, 150, 6, 40),
-                                      (1200, 250, 6, 30), (1500, 300, 6, 20), (1000, 768, 8, 33)])
+                                      (1200, 250, 6, 30), (1500, 300, 6, 20), (1000, 768, 8, 33),
+                                      (1000, 450, 6, 15), (800, 1000, 5, 12)])
 def test_isotropic_ragged_shapes(n, d, kt, k):
     w = g.custom(f"iso{n}_{d}", n, d, kt, k, data_seed=77 + d, init_seed=99 + k)
     x, th0 = g.make(w)

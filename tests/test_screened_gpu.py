@@ -48,7 +48,8 @@ def test_tiny_teacher_forced_all_iterations():
     (63, 16, 3, 5), (1000, 37, 6, 45), (3001, 128, 40, 64), (2049, 200, 10, 17),
     (20000, 8, 4, 300), (2000, 300, 8, 24), (1200, 768, 10, 70)])
 def test_ragged_shapes(n, d, kt, k):
-    """Ragged points, dimensions and components, split-bf16 (d <= 128) and fp32 screening."""
+    """Ragged points, dimensions and components: split-bf16 screening from the split tile
+    (d <= 128) and split on the fly (d > 256), fp32 screening (d = 200)."""
     w = g.custom(f"r{n}_{d}_{k}", n, d, kt, k, data_seed=n + d, init_seed=k + 17)
     x, (wt, mu, var) = g.make(w)
     var = np.where(var > 0, var, np.float32(1.0)).astype(np.float32)
