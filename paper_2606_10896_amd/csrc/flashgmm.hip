@@ -3210,7 +3210,9 @@ __device__ __forceinline__ void assign_screen(const float* xs, const bf16x8* xa,
 // Thresholds of each point: theta[p] = (well-component base, routed-component
 // threshold); a well slot j is a candidate when its screened log-density is
 // >= theta[p].x - b_j (b_j = 0 for the fp32 screening).
-template <int D64>
+// TL: length of the per-point list of the largest lane states (>= tsel):
+// 4 for m <= 2, kTMax otherwise.
+template <int D64, int TL>
 __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_assign_theta(
     const float* __restrict__ x, int64_t n, int d, int vec4, const float4* __restrict__ wp,
     const bf16x8* __restrict__ wpb, const float* __restrict__ cw,
@@ -3272,16 +3274,16 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_assign_theta(
     // merged across the group (disjoint lane states: no entry twice)
     constexpr int G = 256 / PTS, LPT = 128 / G;
     const int p = tid / G, r = tid % G;
-    float tl[kTMax];
-    int ta[kTMax];
+    float tl[TL];
+    int ta[TL];
 #pragma unroll
-    for (int j = 0; j < kTMax; ++j) {
+    for (int j = 0; j < TL; ++j) {
       tl[j] = -INFINITY;
       ta[j] = -1;
     }
     auto insert = [&](float v, int a) {
 #pragma unroll
-      for (int j = kTMax - 1; j > 0; --j) {
+      for (int j = TL - 1; j > 0; --j) {
         if (v > tl[j - 1]) { tl[j] = tl[j - 1]; ta[j] = ta[j - 1]; }
         else if (v > tl[j]) { tl[j] = v; ta[j] = a; }
       }
@@ -3298,31 +3300,31 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_assign_theta(
         v = lmx[p * 129 + c];
       }
       // empty lane states (kEmpty) and those below the list are skipped
-      if (v > 0.5f * kEmpty && v > tl[kTMax - 1]) insert(v, a);
+      if (v > 0.5f * kEmpty && v > tl[TL - 1]) insert(v, a);
     }
 #pragma unroll
     for (int off = 1; off < G; off <<= 1) {
-      float ol[kTMax];
-      int oa[kTMax];
+      float ol[TL];
+      int oa[TL];
 #pragma unroll
-      for (int j = 0; j < kTMax; ++j) {
+      for (int j = 0; j < TL; ++j) {
         ol[j] = __shfl_xor(tl[j], off);
         oa[j] = __shfl_xor(ta[j], off);
       }
 #pragma unroll
-      for (int j = 0; j < kTMax; ++j)
-        if (ol[j] > tl[kTMax - 1]) insert(ol[j], oa[j]);
+      for (int j = 0; j < TL; ++j)
+        if (ol[j] > tl[TL - 1]) insert(ol[j], oa[j]);
     }
     if (r != 0 || n0 + p >= n) return;
     float st = -INFINITY;
 #pragma unroll
-    for (int j = 0; j < kTMax; ++j)
+    for (int j = 0; j < TL; ++j)
       if (j == tsel - 1) st = tl[j];
     float2 out;
     if constexpr (SPB) {
       float dm = 0.0f;
 #pragma unroll
-      for (int j = 0; j < kTMax; ++j) {
+      for (int j = 0; j < TL; ++j) {
         if (j < tsel && ta[j] >= 0) {
           const float2 e = ca[ta[j]];
           dm = fmaxf(dm, kEps * (4.0f * fmaxf(e.x - st, 0.0f) + e.y));
@@ -4542,8 +4544,12 @@ int assign_impl(const Layout& L, const float* x, const float* w, const float* mu
                          cwell, cdir, counts, well_idx, kpad, ca);
     }
   }
-  hipLaunchKernelGGL(k_assign_theta<D64>, dim3((unsigned)L.n_wg_logz), dim3(256), 0, st, x, n, d,
-                     vec4, wp, wpb, cw, ca, counts, m + 2, theta);
+  if (m + 2 <= 4)
+    hipLaunchKernelGGL((k_assign_theta<D64, 4>), dim3((unsigned)L.n_wg_logz), dim3(256), 0, st, x,
+                       n, d, vec4, wp, wpb, cw, ca, counts, m + 2, theta);
+  else
+    hipLaunchKernelGGL((k_assign_theta<D64, kTMax>), dim3((unsigned)L.n_wg_logz), dim3(256), 0, st,
+                       x, n, d, vec4, wp, wpb, cw, ca, counts, m + 2, theta);
   hipLaunchKernelGGL(k_assign_collect<D64>, dim3((unsigned)L.n_wg_logz), dim3(256), 0, st, x, n,
                      d, vec4, wp, wpb, cw, ca, well_idx, ill_idx, dmu, dh, counts, theta, mu, var,
                      cdir, m, tau, idx, resp, ovf);
