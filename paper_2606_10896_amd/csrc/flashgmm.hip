@@ -2482,10 +2482,17 @@ struct SPair {
 __host__ __device__ constexpr int sparse_cb(int D64) {
   return D64 <= 128 ? 32 : (D64 <= 256 ? 16 : (D64 <= 512 ? 8 : 4));
 }
+// k_stats_sparse waves per workgroup: eight (each owning C/8 slots) where the
+// bucket has eight slots or more, so that more waves share each SIMD and hide
+// one another's LDS and fp64 latencies; four for the widest rows
+__host__ __device__ constexpr int sparse_waves(int D64) { return sparse_cb(D64) >= 8 ? 8 : 4; }
 __host__ __device__ constexpr int sparse_lcb(int D64) {
   return D64 <= 128 ? 5 : (D64 <= 256 ? 4 : (D64 <= 512 ? 3 : 2));
 }
 constexpr int kSparseTab = 1 << 18;     // (bucket, unit) table entries at most
+// k_stats_sparse: batches of rows in flight into registers while one is summed
+constexpr int kSparseDepth = 3;
+static_assert(kSparseDepth <= 3, "records are stored four batches ahead");
 
 __global__ __launch_bounds__(64) void k_sparse_count(const unsigned short* __restrict__ cslot,
                                                      int64_t n, int64_t upts, int nb, int lcb,
@@ -2622,18 +2629,21 @@ __global__ __launch_bounds__(64) void k_sparse_scatter(
 }
 
 // Sums of one part of one bucket's list.  Batches of NB pairs: while batch t
-// is consumed from LDS, the rows of batches t+1 and t+2 are in flight into
-// registers, and the records of batch t+4 (stored to LDS one batch later), so
-// that no memory round trip is waited for within a batch.  Wave w owns the
-// CW = C/4 slots CW w .. CW w + CW - 1 of the bucket and takes its pairs of a
-// batch in order, two at a time; lane l owns dimensions l, l + 64, ... and
-// adds r x and r x^2 of them in fp64 (r x is exact), and r itself (N_k, every
-// lane the same sum; lane 0 writes it).
+// is consumed from LDS, the rows of batches t+1 .. t+kSparseDepth are in
+// flight into registers, and the records of batch t+4 (stored to LDS at the
+// end of batch t), so that no memory round trip is waited for within a
+// batch.  Wave w of the NWV waves owns the CW = C/NWV slots CW w .. CW w +
+// CW - 1 of the bucket and takes its pairs of a batch in order, two at a
+// time; lane l owns dimensions l, l + 64, ... and adds r x and r x^2 of them
+// in fp64 (r x is exact), and r itself (N_k, every lane the same sum; lane 0
+// writes it).
 template <int D64>
-__global__ __launch_bounds__(256) void k_stats_sparse(
+__global__ __launch_bounds__(64 * sparse_waves(D64)) void k_stats_sparse(
     const float* __restrict__ x, int64_t n, int d, const SPair* __restrict__ list,
     const int64_t* __restrict__ goff, int nunit, int nparts, double* __restrict__ part) {
-  constexpr int C = sparse_cb(D64), CW = C / 4;
+  constexpr int NWV = sparse_waves(D64), T = 64 * NWV;
+  constexpr int C = sparse_cb(D64), CW = C / NWV;
+  static_assert(CW >= 1 && CW * NWV == C, "slots split evenly over the waves");
   constexpr int STRIDE = 1 + 2 * D64;
   // pairs per batch: as many as a wave has lanes up to 128 dimensions (one
   // record per lane), 16 from 512 dimensions (two batches of rows then take
@@ -2641,10 +2651,10 @@ __global__ __launch_bounds__(256) void k_stats_sparse(
   constexpr int NB = D64 <= 128 ? 64 : (D64 <= 256 ? 4096 / D64 : 16);
   static_assert(NB <= 64, "a batch's records are held one per lane");
   constexpr int CPR = D64 / 4;                   // float4 chunks per row
-  constexpr int GQ = (NB * CPR + 255) / 256;     // float4 gathered per thread and batch
+  constexpr int GQ = (NB * CPR + T - 1) / T;     // float4 gathered per thread and batch
   __shared__ __align__(16) float xb[2][NB * D64];
-  __shared__ int2 rb[4][NB];                     // (slot in bucket, r bits) per pair
-  __shared__ int64_t pb[4][NB];                  // point per pair
+  __shared__ int2 rb[8][NB];                     // (slot in bucket, r bits) per pair
+  __shared__ int64_t pb[8][NB];                  // point per pair
   const int bucket = blockIdx.x / nparts, prt = blockIdx.x % nparts;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int64_t lo = goff[(size_t)bucket * nunit], hi = goff[(size_t)(bucket + 1) * nunit];
@@ -2669,29 +2679,29 @@ __global__ __launch_bounds__(256) void k_stats_sparse(
       const int64_t e = a0 + (int64_t)t * NB + tid;
       if (e < a1) {
         const SPair q = list[e];
-        rb[t & 3][tid] = make_int2(q.c, __float_as_int(q.r));
-        pb[t & 3][tid] = q.pt;
+        rb[t & 7][tid] = make_int2(q.c, __float_as_int(q.r));
+        pb[t & 7][tid] = q.pt;
       }
     }
   };
-  // flat float4 index f = tid + 256 i of a batch: row f / CPR, chunk f % CPR;
+  // flat float4 index f = tid + T i of a batch: row f / CPR, chunk f % CPR;
   // chunks past the batch load row 0, dims 0..3 (always present) and are
   // zeroed afterwards
-  float4 gA[GQ], gB[GQ];
+  float4 g[kSparseDepth][GQ];
   auto gather = [&](int t, float4 (&g)[GQ]) {
     const int nbt = batch_len(t);
     int64_t pt[GQ];
     bool ok[GQ];
 #pragma unroll
     for (int i = 0; i < GQ; ++i) {
-      const int f = tid + 256 * i, e = f / CPR, c4 = 4 * (f % CPR);
+      const int f = tid + T * i, e = f / CPR, c4 = 4 * (f % CPR);
       ok[i] = f < NB * CPR && e < nbt && c4 < d;
-      pt[i] = ok[i] ? pb[t & 3][e] : 0;
+      pt[i] = ok[i] ? pb[t & 7][e] : 0;
     }
     if (vec4) {
 #pragma unroll
       for (int i = 0; i < GQ; ++i) {
-        const int c4 = 4 * ((tid + 256 * i) % CPR);
+        const int c4 = 4 * ((tid + T * i) % CPR);
         g[i] = *reinterpret_cast<const float4*>(x + (ok[i] ? pt[i] * d + c4 : 0));
       }
 #pragma unroll
@@ -2702,7 +2712,7 @@ __global__ __launch_bounds__(256) void k_stats_sparse(
     } else {
 #pragma unroll
       for (int i = 0; i < GQ; ++i) {
-        const int c4 = 4 * ((tid + 256 * i) % CPR);
+        const int c4 = 4 * ((tid + T * i) % CPR);
         float v[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e)
@@ -2716,9 +2726,9 @@ __global__ __launch_bounds__(256) void k_stats_sparse(
     float4* const xw = reinterpret_cast<float4*>(xb[xbuf]);
 #pragma unroll
     for (int i = 0; i < GQ; ++i)
-      if (tid + 256 * i < NB * CPR) xw[tid + 256 * i] = g[i];
+      if (tid + T * i < NB * CPR) xw[tid + T * i] = g[i];
     __syncthreads();            // rows of batch t, records of batches t .. t+3 in LDS
-    // records of batch t+4: loaded now, stored at the end of the next batch
+    // records of batch t+4: loaded now, stored at the end of this batch
     SPair qn = SPair{-1, 0.0f, 0};
     if (t + 4 < nbatch && tid < NB) {
       const int64_t e = a0 + (int64_t)(t + 4) * NB + tid;
@@ -2730,7 +2740,7 @@ __global__ __launch_bounds__(256) void k_stats_sparse(
     const int xbuf = t & 1;
     const int nbt = batch_len(t);
     int2 en = make_int2(0, 0);
-    if (lane < nbt) en = rb[t & 3][lane];
+    if (lane < nbt) en = rb[t & 7][lane];
     const int cl = en.x - CW * wave;
     // slot by slot (each slot's pairs in list order), two pairs at a time
 #pragma unroll
@@ -2768,38 +2778,37 @@ __global__ __launch_bounds__(256) void k_stats_sparse(
       }
     }
   };
-  // at the end of batch t: the records of batch t+3 (loaded during batch
-  // t-1) go to the buffer of batch t-1, whose rows and records every wave has
-  // finished with (the barrier of batch t)
+  // at the end of batch t: the records of batch t+4 (loaded after the barrier
+  // of batch t) go to the buffer of batch t-4, whose rows and records every
+  // wave has finished with (the barrier of batch t); batch t+4's rows are
+  // gathered after the barrier of batch t+1
   auto store_rec = [&](int t, const SPair& q) {
     if (q.pt >= 0) {
-      rb[(t + 3) & 3][tid] = make_int2(q.c, __float_as_int(q.r));
-      pb[(t + 3) & 3][tid] = q.pt;
+      rb[(t + 4) & 7][tid] = make_int2(q.c, __float_as_int(q.r));
+      pb[(t + 4) & 7][tid] = q.pt;
     }
   };
-  SPair qA = SPair{-1, 0.0f, 0}, qB = SPair{-1, 0.0f, 0};
   if (nbatch > 0) {
 #pragma unroll
     for (int t = 0; t < 4; ++t)
       if (t < nbatch) load_rec(t);
     __syncthreads();
-    gather(0, gA);
-    if (nbatch > 1) gather(1, gB);
+#pragma unroll
+    for (int s = 0; s < kSparseDepth; ++s)
+      if (s < nbatch) gather(s, g[s]);
   }
-  // two batches per trip, so that the register sets gA / gB and qA / qB are
-  // named statically
-  for (int t = 0; t < nbatch; t += 2) {
-    {
-      qA = consume(t, gA);
-      if (t + 2 < nbatch) gather(t + 2, gA);
-      accumulate(t);
-      store_rec(t, qB);
-    }
-    if (t + 1 < nbatch) {
-      qB = consume(t + 1, gB);
-      if (t + 3 < nbatch) gather(t + 3, gB);
-      accumulate(t + 1);
-      store_rec(t + 1, qA);
+  // kSparseDepth batches per trip, so that the register sets g[s] are named
+  // statically
+  for (int t = 0; t < nbatch; t += kSparseDepth) {
+#pragma unroll
+    for (int s = 0; s < kSparseDepth; ++s) {
+      const int u = t + s;
+      if (u < nbatch) {
+        const SPair q = consume(u, g[s]);
+        if (u + kSparseDepth < nbatch) gather(u + kSparseDepth, g[s]);
+        accumulate(u);
+        store_rec(u, q);
+      }
     }
   }
 #pragma unroll
@@ -4443,7 +4452,8 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
     hipLaunchKernelGGL(k_sparse_scan, dim3(1), dim3(1024), 0, st, scnt, L.nb * L.nunit, soff);
     hipLaunchKernelGGL(k_sparse_scatter, dim3((unsigned)L.nunit), dim3(64), scatter_lds(L.nb), st,
                        cslot, cr, n, L.upts, L.nb, L.lsbk, L.nunit, soff, slist);
-    hipLaunchKernelGGL(k_stats_sparse<D64>, dim3((unsigned)(L.nb * L.nparts)), dim3(256), 0, st,
+    hipLaunchKernelGGL(k_stats_sparse<D64>, dim3((unsigned)(L.nb * L.nparts)),
+                       dim3(64 * sparse_waves(D64)), 0, st,
                        x, n, d, slist, soff, L.nunit, L.nparts, part_s);
   }
   tm = phase_mark(3, st) && tm;
@@ -4595,7 +4605,8 @@ int kmeans_impl(const Layout& L, const float* x, int n_iters, float var_floor, f
     hipLaunchKernelGGL(k_sparse_scan, dim3(1), dim3(1024), 0, st, scnt, L.nb * L.nunit, soff);
     hipLaunchKernelGGL(k_sparse_scatter, dim3((unsigned)L.nunit), dim3(64), scatter_lds(L.nb), st,
                        cslot, cr, n, L.upts, L.nb, L.lsbk, L.nunit, soff, slist);
-    hipLaunchKernelGGL(k_stats_sparse<D64>, dim3((unsigned)(L.nb * L.nparts)), dim3(256), 0, st,
+    hipLaunchKernelGGL(k_stats_sparse<D64>, dim3((unsigned)(L.nb * L.nparts)),
+                       dim3(64 * sparse_waves(D64)), 0, st,
                        x, n, d, slist, soff, L.nunit, L.nparts, part_s);
     hipLaunchKernelGGL(k_km_reduce, dim3((unsigned)cdiv((int64_t)k * (1 + 2 * (int64_t)d), 256)),
                        dim3(256), 0, st, part_s, L.nparts, L.sbk, k, d, D64, fnk, fs, fq);
