@@ -2482,10 +2482,11 @@ struct SPair {
 __host__ __device__ constexpr int sparse_cb(int D64) {
   return D64 <= 128 ? 32 : (D64 <= 256 ? 16 : (D64 <= 512 ? 8 : 4));
 }
-// k_stats_sparse waves per workgroup: eight (each owning C/8 slots) where the
-// bucket has eight slots or more, so that more waves share each SIMD and hide
-// one another's LDS and fp64 latencies; four for the widest rows
-__host__ __device__ constexpr int sparse_waves(int D64) { return sparse_cb(D64) >= 8 ? 8 : 4; }
+// k_stats_sparse waves per workgroup: eight, so that several waves share each
+// SIMD and hide one another's LDS and fp64 latencies.  Each wave owns C/8
+// slots of the bucket, or, for buckets of four slots (the widest rows), one
+// slot and half of the dimensions.
+constexpr int kSparseWaves = 8;
 __host__ __device__ constexpr int sparse_lcb(int D64) {
   return D64 <= 128 ? 5 : (D64 <= 256 ? 4 : (D64 <= 512 ? 3 : 2));
 }
@@ -2632,18 +2633,22 @@ __global__ __launch_bounds__(64) void k_sparse_scatter(
 // is consumed from LDS, the rows of batches t+1 .. t+kSparseDepth are in
 // flight into registers, and the records of batch t+4 (stored to LDS at the
 // end of batch t), so that no memory round trip is waited for within a
-// batch.  Wave w of the NWV waves owns the CW = C/NWV slots CW w .. CW w +
-// CW - 1 of the bucket and takes its pairs of a batch in order, two at a
-// time; lane l owns dimensions l, l + 64, ... and adds r x and r x^2 of them
-// in fp64 (r x is exact), and r itself (N_k, every lane the same sum; lane 0
-// writes it).
+// batch.  Each of the NWV waves owns CW slots of the bucket and one of DS
+// parts of the dimensions (DS = 2 for buckets of four slots, else 1) and
+// takes its slots' pairs of a batch in order, two at a time; lane l owns the
+// part's dimensions l, l + 64, ... and adds r x and r x^2 of them in fp64
+// (r x is exact), and r itself (N_k, every lane the same sum; lane 0 of the
+// first part writes it).
 template <int D64>
-__global__ __launch_bounds__(64 * sparse_waves(D64)) void k_stats_sparse(
+__global__ __launch_bounds__(64 * kSparseWaves) void k_stats_sparse(
     const float* __restrict__ x, int64_t n, int d, const SPair* __restrict__ list,
     const int64_t* __restrict__ goff, int nunit, int nparts, double* __restrict__ part) {
-  constexpr int NWV = sparse_waves(D64), T = 64 * NWV;
-  constexpr int C = sparse_cb(D64), CW = C / NWV;
-  static_assert(CW >= 1 && CW * NWV == C, "slots split evenly over the waves");
+  constexpr int NWV = kSparseWaves, T = 64 * NWV;
+  constexpr int C = sparse_cb(D64);
+  constexpr int DS = NWV > C ? NWV / C : 1;      // dimension parts per slot
+  constexpr int CW = C * DS / NWV;               // slots per wave
+  constexpr int DP = D64 / DS;                   // dimensions per part
+  static_assert(CW >= 1 && CW * NWV == C * DS && DP % 64 == 0, "slots and dimensions split evenly");
   constexpr int STRIDE = 1 + 2 * D64;
   // pairs per batch: as many as a wave has lanes up to 128 dimensions (one
   // record per lane), 16 from 512 dimensions (two batches of rows then take
@@ -2662,7 +2667,9 @@ __global__ __launch_bounds__(64 * sparse_waves(D64)) void k_stats_sparse(
   const int64_t a0 = lo + cnt * prt / nparts, a1 = lo + cnt * (prt + 1) / nparts;
   const int nbatch = (int)((a1 - a0 + NB - 1) / NB);
   const bool vec4 = (d & 3) == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0;
-  constexpr int NX = D64 / 64;                   // dimensions per lane
+  constexpr int NX = DP / 64;                    // dimensions per lane
+  // this wave: slots sb .. sb + CW - 1, dimensions dh DP .. dh DP + DP - 1
+  const int sb = (wave % (NWV / DS)) * CW, dh = wave / (NWV / DS);
   double accs[CW][NX], accq[CW][NX], accn[CW];
 #pragma unroll
   for (int j = 0; j < CW; ++j) {
@@ -2741,7 +2748,7 @@ __global__ __launch_bounds__(64 * sparse_waves(D64)) void k_stats_sparse(
     const int nbt = batch_len(t);
     int2 en = make_int2(0, 0);
     if (lane < nbt) en = rb[t & 7][lane];
-    const int cl = en.x - CW * wave;
+    const int cl = en.x - sb;
     // slot by slot (each slot's pairs in list order), two pairs at a time
 #pragma unroll
     for (int j = 0; j < CW; ++j) {
@@ -2751,8 +2758,8 @@ __global__ __launch_bounds__(64 * sparse_waves(D64)) void k_stats_sparse(
         own &= own - 1;
         const int e1 = own ? __ffsll(own) - 1 : -1;
         if (e1 >= 0) own &= own - 1;
-        const float* xr0 = xb[xbuf] + e0 * D64 + lane;
-        const float* xr1 = xb[xbuf] + (e1 >= 0 ? e1 : e0) * D64 + lane;
+        const float* xr0 = xb[xbuf] + e0 * D64 + dh * DP + lane;
+        const float* xr1 = xb[xbuf] + (e1 >= 0 ? e1 : e0) * D64 + dh * DP + lane;
         double x0[NX], x1[NX];
 #pragma unroll
         for (int u = 0; u < NX; ++u) {
@@ -2813,12 +2820,12 @@ __global__ __launch_bounds__(64 * sparse_waves(D64)) void k_stats_sparse(
   }
 #pragma unroll
   for (int j = 0; j < CW; ++j) {
-    double* out = part + ((size_t)blockIdx.x * C + CW * wave + j) * STRIDE;
-    if (lane == 0) out[0] = accn[j];
+    double* out = part + ((size_t)blockIdx.x * C + sb + j) * STRIDE;
+    if (lane == 0 && dh == 0) out[0] = accn[j];
 #pragma unroll
     for (int u = 0; u < NX; ++u) {
-      out[1 + lane + 64 * u] = accs[j][u];
-      out[1 + D64 + lane + 64 * u] = accq[j][u];
+      out[1 + dh * DP + lane + 64 * u] = accs[j][u];
+      out[1 + D64 + dh * DP + lane + 64 * u] = accq[j][u];
     }
   }
 }
@@ -4453,7 +4460,7 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
     hipLaunchKernelGGL(k_sparse_scatter, dim3((unsigned)L.nunit), dim3(64), scatter_lds(L.nb), st,
                        cslot, cr, n, L.upts, L.nb, L.lsbk, L.nunit, soff, slist);
     hipLaunchKernelGGL(k_stats_sparse<D64>, dim3((unsigned)(L.nb * L.nparts)),
-                       dim3(64 * sparse_waves(D64)), 0, st,
+                       dim3(64 * kSparseWaves), 0, st,
                        x, n, d, slist, soff, L.nunit, L.nparts, part_s);
   }
   tm = phase_mark(3, st) && tm;
@@ -4606,7 +4613,7 @@ int kmeans_impl(const Layout& L, const float* x, int n_iters, float var_floor, f
     hipLaunchKernelGGL(k_sparse_scatter, dim3((unsigned)L.nunit), dim3(64), scatter_lds(L.nb), st,
                        cslot, cr, n, L.upts, L.nb, L.lsbk, L.nunit, soff, slist);
     hipLaunchKernelGGL(k_stats_sparse<D64>, dim3((unsigned)(L.nb * L.nparts)),
-                       dim3(64 * sparse_waves(D64)), 0, st,
+                       dim3(64 * kSparseWaves), 0, st,
                        x, n, d, slist, soff, L.nunit, L.nparts, part_s);
     hipLaunchKernelGGL(k_km_reduce, dim3((unsigned)cdiv((int64_t)k * (1 + 2 * (int64_t)d), 256)),
                        dim3(256), 0, st, part_s, L.nparts, L.sbk, k, d, D64, fnk, fs, fq);
