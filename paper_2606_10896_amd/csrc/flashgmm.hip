@@ -2585,6 +2585,8 @@ __global__ __launch_bounds__(64) void k_sparse_scatter(
   const int64_t p0 = (int64_t)u * upts;
   const int64_t p1 = p0 + upts < n ? p0 + upts : n;
   const unsigned long long below = (1ull << lane) - 1ull;
+  int nbits = 0;                             // bits of the largest bucket index
+  while ((nb - 1) >> nbits) ++nbits;
   for (int64_t pb = p0; pb < p1; pb += 64) {
     const int64_t p = pb + lane;
     int sl[kT] = {-1, -1, -1, -1};
@@ -2603,6 +2605,30 @@ __global__ __launch_bounds__(64) void k_sparse_scatter(
     for (int j = 0; j < kT; ++j) {
       const bool valid = sl[j] >= 0;
       const int bk = valid ? (sl[j] >> lcb) : -1;
+      if (cached) {
+        // the lanes of each bucket found with one ballot per bit of the bucket
+        // index; a lane's place is its rank among them (lane order), as in
+        // the loop over buckets below
+        unsigned long long same = __ballot(valid);
+        for (int bb = 0; bb < nbits; ++bb) {
+          const bool bit = ((bk >> bb) & 1) != 0;
+          const unsigned long long m = __ballot(bit);
+          same &= bit ? m : ~m;
+        }
+        int64_t base = 0;
+        if (valid) {
+          base = cur[bk];
+          SPair e;
+          e.pt = p;
+          e.r = rr[j];
+          e.c = sl[j] & ((1 << lcb) - 1);
+          list[base + __popcll(same & below)] = e;
+        }
+        __builtin_amdgcn_wave_barrier();
+        if (valid && (same & below) == 0ull) cur[bk] = base + __popcll(same);
+        __builtin_amdgcn_wave_barrier();
+        continue;
+      }
       unsigned long long act = __ballot(valid);
       while (act) {
         const int leader = __ffsll(act) - 1;
