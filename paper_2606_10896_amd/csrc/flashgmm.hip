@@ -2775,37 +2775,34 @@ __global__ __launch_bounds__(64 * kSparseWaves) void k_stats_sparse(
     int2 en = make_int2(0, 0);
     if (lane < nbt) en = rb[t & 7][lane];
     const int cl = en.x - sb;
-    // slot by slot (each slot's pairs in list order), two pairs at a time
+    // slot by slot (each slot's pairs in list order), up to four pairs at a
+    // time (their rows read before the sums)
 #pragma unroll
     for (int j = 0; j < CW; ++j) {
       unsigned long long own = __ballot(lane < nbt && cl == j);
       while (own) {
-        const int e0 = __ffsll(own) - 1;
-        own &= own - 1;
-        const int e1 = own ? __ffsll(own) - 1 : -1;
-        if (e1 >= 0) own &= own - 1;
-        const float* xr0 = xb[xbuf] + e0 * D64 + dh * DP + lane;
-        const float* xr1 = xb[xbuf] + (e1 >= 0 ? e1 : e0) * D64 + dh * DP + lane;
-        double x0[NX], x1[NX];
+        int e[4];
 #pragma unroll
-        for (int u = 0; u < NX; ++u) {
-          x0[u] = (double)xr0[64 * u];
-          x1[u] = (double)xr1[64 * u];
+        for (int i = 0; i < 4; ++i) {
+          e[i] = own ? __ffsll(own) - 1 : -1;
+          if (e[i] >= 0) own &= own - 1;
         }
-        const double r0 = (double)__int_as_float(__builtin_amdgcn_readlane(en.y, e0));
-        accn[j] += r0;
+        double xv[4][NX];
 #pragma unroll
-        for (int u = 0; u < NX; ++u) {
-          accs[j][u] = fma(r0, x0[u], accs[j][u]);
-          accq[j][u] = fma(r0, x0[u] * x0[u], accq[j][u]);
+        for (int i = 0; i < 4; ++i) {
+          const float* xr = xb[xbuf] + (e[i] >= 0 ? e[i] : e[0]) * D64 + dh * DP + lane;
+#pragma unroll
+          for (int u = 0; u < NX; ++u) xv[i][u] = (double)xr[64 * u];
         }
-        if (e1 >= 0) {
-          const double r1 = (double)__int_as_float(__builtin_amdgcn_readlane(en.y, e1));
-          accn[j] += r1;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          if (e[i] < 0) break;
+          const double r = (double)__int_as_float(__builtin_amdgcn_readlane(en.y, e[i]));
+          accn[j] += r;
 #pragma unroll
           for (int u = 0; u < NX; ++u) {
-            accs[j][u] = fma(r1, x1[u], accs[j][u]);
-            accq[j][u] = fma(r1, x1[u] * x1[u], accq[j][u]);
+            accs[j][u] = fma(r, xv[i][u], accs[j][u]);
+            accq[j][u] = fma(r, xv[i][u] * xv[i][u], accq[j][u]);
           }
         }
       }
