@@ -2876,13 +2876,14 @@ __global__ __launch_bounds__(256) void k_stats_ill(
     const double* __restrict__ cdir, const int* __restrict__ counts,
     const double* __restrict__ logz2, const unsigned char* __restrict__ iflag,
     const unsigned char* __restrict__ lflag, const unsigned short* __restrict__ cslot,
-    const unsigned char* __restrict__ sflag, double* __restrict__ part) {
+    const int* __restrict__ small_pos, double* __restrict__ part) {
   constexpr int P = D64 + 4, NJ = D64 / 64, STRIDE = 1 + 2 * D64;
   constexpr int PT = ill_pt(D64), CW = ill_cw(D64), ICB = 4 * CW;
   constexpr int WIN = 16 * 256;                 // points scanned per queue window
   __shared__ __align__(16) float xs[PT * P];
   __shared__ float rs[ICB * PT];
   __shared__ double lzs[PT];
+  __shared__ int lsx[PT][kT];                   // light: list index of each stored pair, or -1
   __shared__ unsigned qpt[WIN + PT];            // queued points (offsets from the chunk start)
   __shared__ int qsum[4];
   const int n_ill = counts[1];
@@ -2906,10 +2907,12 @@ __global__ __launch_bounds__(256) void k_stats_ill(
   // of them (every point when iflag is null) are taken: windows of WIN points
   // are scanned, flagged points queued in order, and tiles of PT queued points
   // gathered (the queue's rest moves to its front).  For the light components
-  // (sflag given: their well slots flagged) a point is taken when the dense
-  // pass flagged it (lflag: a light component's dense log-density there came
-  // within 2^-72 of log2 Z) or one of its stored exact pairs is a light
-  // component: at every other point each of them has r < 2^-64.
+  // (small_pos given: each well slot's index in their list, or -1) a point is
+  // taken when the dense pass flagged it (lflag: a light component's dense
+  // log-density there came within 2^-72 of log2 Z), and the point's stored
+  // exact pairs are left out there: the exact-pair pass has summed them.  At
+  // every other point each light component is either stored or has
+  // r < 2^-64.
   int qn = 0;
   for (int64_t wb0 = p0; wb0 < p1; wb0 += WIN) {
     const int64_t we = wb0 + WIN < p1 ? wb0 + WIN : p1;
@@ -2921,14 +2924,7 @@ __global__ __launch_bounds__(256) void k_stats_ill(
         const int64_t pt = a + e;
         bool take = pt < we;
         if (take && iflag != nullptr) take = iflag[pt] != 0;
-        if (take && sflag != nullptr) {
-          bool hit = lflag[pt] != 0;
-          const ushort4 sl = *reinterpret_cast<const ushort4*>(cslot + pt * kT);
-          const int v4[4] = {sl.x, sl.y, sl.z, sl.w};
-#pragma unroll
-          for (int j = 0; j < kT; ++j) hit = hit || (v4[j] != kNoSlot && sflag[v4[j]] != 0);
-          take = hit;
-        }
+        if (take && small_pos != nullptr) take = lflag[pt] != 0;
         if (take) sel |= 1u << e;
       }
       const int cnt = __popc(sel);
@@ -2979,6 +2975,15 @@ __global__ __launch_bounds__(256) void k_stats_ill(
       if (tid < PT) {
         const int e = PT * ti + tid;
         lzs[tid] = e < qn ? logz2[p0 + qpt[e]] : INFINITY;
+        if (small_pos != nullptr) {
+          int v4[kT] = {kNoSlot, kNoSlot, kNoSlot, kNoSlot};
+          if (e < qn) {
+            const ushort4 sl = *reinterpret_cast<const ushort4*>(cslot + (p0 + qpt[e]) * kT);
+            v4[0] = sl.x; v4[1] = sl.y; v4[2] = sl.z; v4[3] = sl.w;
+          }
+#pragma unroll
+          for (int j = 0; j < kT; ++j) lsx[tid][j] = v4[j] != kNoSlot ? small_pos[v4[j]] : -1;
+        }
       }
     }
     __syncthreads();
@@ -2988,7 +2993,12 @@ __global__ __launch_bounds__(256) void k_stats_ill(
     for (int c = 0; c < CW; ++c) {
       const int ki = kb * ICB + wave * CW + c;
       float r = 0.0f;
-      if (ki < n_ill && lane < PT) {
+      bool stored = false;
+      if (small_pos != nullptr && lane < PT) {
+#pragma unroll
+        for (int j = 0; j < kT; ++j) stored = stored || lsx[lane][j] == ki;
+      }
+      if (ki < n_ill && lane < PT && !stored) {
         const int comp = ill_idx[ki];
         const double c0 = cdir[comp];
         // r < 2^-150 is 0 in fp32: such pairs are not finished
@@ -3747,9 +3757,10 @@ __device__ __forceinline__ double sum_strided(const double* __restrict__ p, int 
 // N_k).  Every well-conditioned component whose stored exact pairs hold less
 // than kSmallMass is therefore light: the dense pass leaves it out and flags
 // the points where its fp32 log-density comes within 2^-72 of log2 Z (eight
-// log2 units of slack over the 2^-64 cut for the dense pass's error), and its
-// statistics are computed at those points and at the points that store it,
-// in the direct form with fp64 sums (k_stats_ill).  A component with more
+// log2 units of slack over the 2^-64 cut for the dense pass's error); its
+// pairs at those points, except the stored ones, are computed in the direct
+// form with fp64 sums (k_stats_ill), and its stored pairs come from the
+// exact-pair pass as for every component.  A component with more
 // mass spreads its variance over enough pairs that their independent
 // rounding errors stay well inside the variance tolerance.
 constexpr double kSmallMass = 64.0;
@@ -3837,11 +3848,15 @@ __global__ __launch_bounds__(256) void k_reduce_stats(
     comp = well_idx[slot];
     const int xp = small_pos != nullptr ? small_pos[slot] : -1;
     if (xp >= 0) {
-      // a light component: its exact recomputation replaces the fast passes
+      // a light component: its exact recomputation at the flagged points
+      // replaces the dense pass; its stored pairs come from the exact-pair pass
       const int n_xkb = (small_cnt[1] + ibk - 1) / ibk;
       const int nchk = ill_chunks(grid_i, n_xkb, n, ipt);
       const double* p = part_x + ((size_t)(xp / ibk) * nchk * ibk + (xp % ibk)) * stride + off;
       acc = sum_strided(p, nchk, (size_t)ibk * stride, acc);
+      const double* ps =
+          part_s + ((size_t)(slot / sbk) * nparts * sbk + (slot % sbk)) * stride + off;
+      acc = sum_strided(ps, nparts, (size_t)sbk * stride, acc);
     } else {
       const double* p = part_w + ((size_t)(slot / wbk) * nch * wbk + (slot % wbk)) * stride + off;
       acc = sum_strided(p, nch, (size_t)wbk * stride, acc);
@@ -4527,7 +4542,7 @@ int estep_impl(const Layout& L, const float* x, const float* w, const float* mu,
                      part_i);
   if (L.refine)
     hipLaunchKernelGGL(k_stats_ill<D64>, dim3((unsigned)L.grid_i), dim3(256), 0, st, x, n, d,
-                       vec4, sidx, dmu, dh, cdir, scnt2, logz2, nullptr, lflag, cslot, sflag,
+                       vec4, sidx, dmu, dh, cdir, scnt2, logz2, nullptr, lflag, cslot, spos,
                        part_x);
   {
     const int64_t tot = 2 * (int64_t)k * (1 + 2 * (int64_t)d);
