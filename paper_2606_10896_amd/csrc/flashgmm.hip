@@ -4258,9 +4258,12 @@ bool make_layout(int64_t n, int d, int k, int m, Layout* L, size_t budget = 0) {
     if (u > cap) u = cap;
     L->nunit = (int)(u < 1 ? 1 : u);
     L->upts = cdiv(n, L->nunit);
-    // about 2048 workgroups for the exact pairs, but no more parts than a few
-    // hundred stored pairs each would fill
-    int64_t pp = 2048 / L->nb;
+    // about 8192 workgroups for the exact pairs (16384 for rows of more than
+    // 512 dimensions, one workgroup per compute unit), so that the parts of
+    // the buckets of popular components, whose lists are the longest, leave
+    // no long tail; but no more parts than a few hundred stored pairs each
+    // would fill
+    int64_t pp = (L->D64 > 512 ? 16384 : 8192) / L->nb;
     const int64_t by_pairs = cdiv(n * kT, (int64_t)L->nb * 256);
     if (pp > by_pairs) pp = by_pairs;
     L->nparts = (int)(pp < 1 ? 1 : pp);

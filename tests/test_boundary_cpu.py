@@ -52,7 +52,7 @@ def test_workspace_is_o_n_plus_o_kd(n, d, k):
     kpad = (k + 63) // 64 * 64
     row = 8 * (1 + 2 * dp)
     well_part = row * max(8 * kpad, 2048 * 64)
-    sparse_part = row * max(kpad, 2048 * 32)
+    sparse_part = row * max(kpad, 8192 * 32)
     ill_part = row * max(kpad + 32, 512 * 32)
     # the routed components' partials, and as many for the exact recomputation of the light
     # components (plus their flags, list positions and list: 9 bytes per component)
