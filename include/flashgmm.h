@@ -337,7 +337,7 @@ int gmm_estep_accumulate_static(const float* x, int64_t n, int32_t d, int32_t k,
  * (64-component block, chunk); a workgroup queues the chunk's points that
  * need its block, sums their statistics on fp32 MFMA and adds the fp32 sums
  * into fp64 partials every 4096 queued points; the partials are summed in
- * chunk order.  The library picks the chunk count from (n, d, k) (about 2048
+ * chunk order.  The library picks the chunk count from (n, d, k) (about 8192
  * workgroups); max_chunks > 0 caps it, 0 restores the automatic count.
  * Fewer, longer chunks change the results by rounding only (the split of the
  * fp32 runs moves) and never need a larger workspace.  The setting is

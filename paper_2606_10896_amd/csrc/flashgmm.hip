@@ -4226,17 +4226,17 @@ bool make_layout(int64_t n, int d, int k, int m, Layout* L, size_t budget = 0) {
   L->wbk = L->D64 >= 256 ? 16 : kWB;
   const int nwb = L->kpad / L->wbk;
   if (L->D64 < 256) {
-    // about 2048 workgroups (four rounds at two per CU) for k_stats_well: the
-    // blocks' shares of the points differ, and several rounds let the
-    // workgroups of the busy blocks spread over the chip
-    int maxc = 2048 / nwb;
+    // about 8192 workgroups (sixteen rounds at two per CU) for k_stats_well:
+    // the blocks' shares of the points differ, and many short rounds let the
+    // workgroups of the busy blocks spread over the chip and leave no long tail
+    int maxc = 8192 / nwb;
     if (maxc < 8) maxc = 8;
     int64_t c = cdiv(n, 1024);
     if (c > maxc) c = maxc;
     if (c >= 8) c = c / 8 * 8;
     L->nch = (int)(c < 1 ? 1 : c);
   } else {
-    int maxc = 2048 / nwb;
+    int maxc = 8192 / nwb;
     if (maxc < 1) maxc = 1;
     int64_t c = cdiv(n, 1024);
     if (c > maxc) c = maxc;

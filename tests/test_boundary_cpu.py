@@ -51,7 +51,7 @@ def test_workspace_is_o_n_plus_o_kd(n, d, k):
     dp = (d + 63) // 64 * 64 if d <= 256 else (d + 127) // 128 * 128
     kpad = (k + 63) // 64 * 64
     row = 8 * (1 + 2 * dp)
-    well_part = row * max(8 * kpad, 2048 * 64)
+    well_part = row * max(8 * kpad, 8192 * 64)
     sparse_part = row * max(kpad, 8192 * 32)
     ill_part = row * max(kpad + 32, 512 * 32)
     # the routed components' partials, and as many for the exact recomputation of the light
