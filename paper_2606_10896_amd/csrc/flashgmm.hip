@@ -4226,17 +4226,27 @@ bool make_layout(int64_t n, int d, int k, int m, Layout* L, size_t budget = 0) {
   L->wbk = L->D64 >= 256 ? 16 : kWB;
   const int nwb = L->kpad / L->wbk;
   if (L->D64 < 256) {
-    // about 8192 workgroups (sixteen rounds at two per CU) for k_stats_well:
-    // the blocks' shares of the points differ, and many short rounds let the
-    // workgroups of the busy blocks spread over the chip and leave no long tail
-    int maxc = 8192 / nwb;
+    // about 2048 workgroups (four rounds at two per CU) for k_stats_well, and
+    // up to 8192 while the chunks keep 65536 points or more: the blocks'
+    // shares of the points differ, and many short rounds let the workgroups
+    // of the busy blocks spread over the chip and leave no long tail, while
+    // a workgroup's fixed cost (its operands, its partial sums) stays small
+    int maxc = 2048 / nwb;
+    {
+      const int64_t more = cdiv(n, 65536) < 8192 / nwb ? cdiv(n, 65536) : 8192 / nwb;
+      if (more > maxc) maxc = (int)more;
+    }
     if (maxc < 8) maxc = 8;
     int64_t c = cdiv(n, 1024);
     if (c > maxc) c = maxc;
     if (c >= 8) c = c / 8 * 8;
     L->nch = (int)(c < 1 ? 1 : c);
   } else {
-    int maxc = 8192 / nwb;
+    int maxc = 2048 / nwb;
+    {
+      const int64_t more = cdiv(n, 65536) < 8192 / nwb ? cdiv(n, 65536) : 8192 / nwb;
+      if (more > maxc) maxc = (int)more;
+    }
     if (maxc < 1) maxc = 1;
     int64_t c = cdiv(n, 1024);
     if (c > maxc) c = maxc;
@@ -4261,11 +4271,13 @@ bool make_layout(int64_t n, int d, int k, int m, Layout* L, size_t budget = 0) {
     // about 8192 workgroups for the exact pairs (16384 for rows of more than
     // 512 dimensions, one workgroup per compute unit), so that the parts of
     // the buckets of popular components, whose lists are the longest, leave
-    // no long tail; but no more parts than a few hundred stored pairs each
-    // would fill
+    // no long tail; but the parts' partial sums (kpad pp rows of 1 + 2 D64
+    // doubles) no larger than a quarter of X, which they would outweigh at
+    // small n, unless that leaves fewer than about 1024 workgroups
     int64_t pp = (L->D64 > 512 ? 16384 : 8192) / L->nb;
-    const int64_t by_pairs = cdiv(n * kT, (int64_t)L->nb * 256);
-    if (pp > by_pairs) pp = by_pairs;
+    int64_t by_bytes = n * (int64_t)d / (8 * (int64_t)L->kpad * stride);
+    if (by_bytes < 1024 / L->nb) by_bytes = 1024 / L->nb;
+    if (pp > by_bytes) pp = by_bytes;
     L->nparts = (int)(pp < 1 ? 1 : pp);
   }
   L->ipt = L->D64 <= 256 ? 64 : (L->D64 <= 512 ? 32 : 16);

@@ -3,7 +3,7 @@ row N = 1M), against the fp64 checker on all 1e6 points.
 
 Teacher-forced at the random-point initialisation Theta_0 and at the checker's Theta_3, where
 components have started to narrow onto groups of points.  Each is checked twice: with the
-library's own chunking of the dense statistics pass (512 chunks of 1,954 points) and with 16
+library's own chunking of the dense statistics pass (128 chunks of 7,813 points) and with 16
 chunks of 62,500 points, whose busiest blocks queue well over 4096 points, so that the fp32
 runs of the dense statistics reach the length they have at N = 1e8."""
 import sys
