@@ -251,10 +251,12 @@ int gmm_estep_accumulate_ring(gmm_fill_fn fill, void* user, int64_t n, int32_t d
  * uniforms u[k] (fp64, device, 0 <= u < 1).  Centre 0 is row floor(u_0 n);
  * centre t is the first row whose running sum of D^2 (squared distance to the
  * nearest centre chosen so far) exceeds u_t times the total, the sums taken
- * in a fixed order: D^2 of a row as fp64 fused multiply-adds over the
- * dimensions in order; blocks of 4096 rows, each 256 runs of 16 consecutive
- * rows; runs add their rows, blocks their runs, the total its blocks, and
- * the search walks blocks, runs and rows in order.  Every choice is thus a
+ * in a fixed order: D^2 of a row as 16 fp64 partial sums of fused
+ * multiply-adds (partial l over the dimensions 4 (l + 16 j) + e, e = 0..3,
+ * j = 0, 1, ..., in that order) added pairwise; blocks of 1024 rows, each 64
+ * runs of 16 consecutive rows; runs add their rows, blocks their runs, 256
+ * consecutive stretches of blocks their blocks, the total the stretches, and
+ * the search walks stretches, blocks, runs and rows in order.  Every choice is thus a
  * pure function of (x, u).  When the total is 0 (every row on a centre),
  * centre t is row floor(u_t n).  idx[k] (int64, device) receives the rows,
  * centers[k*d] (fp32, device) their coordinates.  ws: device workspace of

@@ -3983,13 +3983,16 @@ __global__ __launch_bounds__(256) void k_mstep_iso(const double* __restrict__ nk
 // of D^2 (squared distance to the nearest chosen centre) exceeds u_t times
 // the total.  Every sum has a fixed order, so each choice is a pure function
 // of the data and u: D^2 of a row is 16 fp64 partial sums (partial l takes
-// dimensions l, l + 16, ... in order, fma(t, t, acc), t = x - c) combined
-// pairwise by xor 8, 4, 2, 1 (16 lanes per row, coalesced loads); a block of
-// kKppBlock rows is 256 runs of 16 consecutive rows; a run adds its rows in
-// order, a block its runs, the total its blocks, and the search walks
-// blocks, runs and rows in that order.
-constexpr int kKppBlock = 4096;
+// the dimensions 4 (l + 16 j) + e, e = 0..3, j = 0, 1, ..., in that order,
+// fma(t, t, acc), t = x - c) combined pairwise by xor 8, 4, 2, 1 (16 lanes per
+// row, float4 loads where the rows allow them, the same order otherwise); a
+// block of kKppBlock rows is kKppRuns runs of kKppRun consecutive rows; a run
+// adds its rows in order, a block its runs; the total is the sum, in order,
+// of 256 consecutive stretches of blocks, each summed in order, and the
+// search walks stretches, blocks, runs and rows in that order.
 constexpr int kKppRun = 16;
+constexpr int kKppRuns = 64;
+constexpr int kKppBlock = kKppRun * kKppRuns;
 
 __device__ __forceinline__ int64_t kpp_first(double u, int64_t n) {
   int64_t i = (int64_t)(u * (double)n);
@@ -3997,21 +4000,22 @@ __device__ __forceinline__ int64_t kpp_first(double u, int64_t n) {
 }
 
 // One workgroup per block: folds centre idx[t-1] into D^2 (first: D^2 is
-// that centre's distance) and writes the block's sum.  Wave w of the 16 takes
-// runs w, w + 16, ...; a run's 16 rows go 4 at a time, lane group g (16
+// that centre's distance) and writes the block's sum.  Wave w of the 4 takes
+// runs w, w + 4, ...; a run's 16 rows go 4 at a time, lane group g (16
 // lanes) forming the D^2 of row 4 s + g, and lane 0 adds the rows in order.
-__global__ __launch_bounds__(1024) void k_kpp_update(const float* __restrict__ x, int64_t n, int d,
-                                                    const int64_t* __restrict__ idx, int t,
-                                                    int first, double* __restrict__ dist,
-                                                    double* __restrict__ bsum) {
-  __shared__ double rsum[256];
-  __shared__ float cs[GMM_MAX_D];
+__global__ __launch_bounds__(256) void k_kpp_update(const float* __restrict__ x, int64_t n, int d,
+                                                   int vec4, const int64_t* __restrict__ idx,
+                                                   int t, int first, double* __restrict__ dist,
+                                                   double* __restrict__ bsum) {
+  __shared__ double rsum[kKppRuns];
+  __shared__ __align__(16) float cs[GMM_MAX_D];
   const int64_t b = blockIdx.x;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, g = lane >> 4, l16 = lane & 15;
   const float* c = x + idx[t - 1] * (int64_t)d;
-  for (int e = tid; e < d; e += 1024) cs[e] = c[e];
+  for (int e = tid; e < d; e += 256) cs[e] = c[e];
   __syncthreads();
-  for (int q = wave; q < 256; q += 16) {
+  const int nc4 = (d + 3) / 4;                  // chunks of four dimensions
+  for (int q = wave; q < kKppRuns; q += 4) {
     const int64_t r0 = b * kKppBlock + (int64_t)kKppRun * q;
     double rs = 0.0;
     for (int sub = 0; sub < kKppRun / 4; ++sub) {
@@ -4020,9 +4024,22 @@ __global__ __launch_bounds__(1024) void k_kpp_update(const float* __restrict__ x
       if (i < n) {
         const float* xr = x + i * (int64_t)d;
         double acc = 0.0;
-        for (int e = l16; e < d; e += 16) {
-          const double u = (double)xr[e] - (double)cs[e];
-          acc = fma(u, u, acc);
+        for (int c4 = l16; c4 < nc4; c4 += 16) {
+          float xv[4];
+          if (vec4) {
+            const float4 f = *reinterpret_cast<const float4*>(xr + 4 * c4);
+            xv[0] = f.x; xv[1] = f.y; xv[2] = f.z; xv[3] = f.w;
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) xv[e] = 4 * c4 + e < d ? xr[4 * c4 + e] : 0.0f;
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if (4 * c4 + e < d) {
+              const double u = (double)xv[e] - (double)cs[4 * c4 + e];
+              acc = fma(u, u, acc);
+            }
+          }
         }
         acc += __shfl_xor(acc, 8);
         acc += __shfl_xor(acc, 4);
@@ -4044,34 +4061,48 @@ __global__ __launch_bounds__(1024) void k_kpp_update(const float* __restrict__ x
   __syncthreads();
   if (tid == 0) {
     double sb = 0.0;
-    for (int q = 0; q < 256; ++q) sb += rsum[q];
+    for (int q = 0; q < kKppRuns; ++q) sb += rsum[q];
     bsum[b] = sb;
   }
 }
 
-// One workgroup: centre t (t = 0: floor(u_0 n)) into idx[t] and its row into centres.
+// One workgroup: centre t (t = 0: floor(u_0 n)) into idx[t] and its row into
+// centres.  The blocks are taken in 256 consecutive stretches, thread j
+// summing stretch j in order.
 __global__ __launch_bounds__(256) void k_kpp_select(const float* __restrict__ x, int64_t n, int d,
-                                                    const double* __restrict__ uu, int t,
-                                                    const double* __restrict__ dist,
-                                                    const double* __restrict__ bsum,
-                                                    int64_t nblk, int64_t* __restrict__ idx,
-                                                    float* __restrict__ centres) {
-  __shared__ double rsum[256];
+                                                   const double* __restrict__ uu, int t,
+                                                   const double* __restrict__ dist,
+                                                   const double* __restrict__ bsum,
+                                                   int64_t nblk, int64_t* __restrict__ idx,
+                                                   float* __restrict__ centres) {
+  __shared__ double ssum[256];
+  __shared__ double rsum[kKppRuns];
   __shared__ double sh[2];      // run (sum of the blocks before), target
   __shared__ int64_t sb[2];     // block, pick
   const int j = threadIdx.x;
+  const int64_t per = (nblk + 255) / 256;
+  if (t > 0) {
+    const int64_t s0 = per * j, s1 = s0 + per < nblk ? s0 + per : nblk;
+    double ss = 0.0;
+    for (int64_t b = s0; b < s1; ++b) ss += bsum[b];
+    ssum[j] = ss;
+  }
+  __syncthreads();
   if (j == 0) {
     int64_t pick = -1, blk = -1;
     const double u = uu[t];
     if (t > 0) {
       double total = 0.0;
-      for (int64_t b = 0; b < nblk; ++b) total += bsum[b];
+      for (int q = 0; q < 256; ++q) total += ssum[q];
       if (total > 0.0) {
         const double target = u * total;
         double run = 0.0;
-        int64_t b = 0;
-        while (b + 1 < nblk && !(run + bsum[b] > target)) run += bsum[b++];
-        blk = b;
+        int q = 0;
+        while (q + 1 < 256 && !(run + ssum[q] > target)) run += ssum[q++];
+        int64_t b = per * q;
+        const int64_t b1 = b + per < nblk ? b + per : nblk;
+        while (b + 1 < b1 && !(run + bsum[b] > target)) run += bsum[b++];
+        blk = b < nblk ? b : nblk - 1;
         sh[0] = run;
         sh[1] = target;
       }
@@ -4084,16 +4115,18 @@ __global__ __launch_bounds__(256) void k_kpp_select(const float* __restrict__ x,
   const int64_t blk = sb[0];
   if (blk >= 0) {
     // run sums of the block, as k_kpp_update formed them
-    const int64_t r0 = blk * kKppBlock + (int64_t)kKppRun * j;
-    double rs = 0.0;
-    for (int64_t i = r0; i < r0 + kKppRun && i < n; ++i) rs += dist[i];
-    rsum[j] = rs;
+    if (j < kKppRuns) {
+      const int64_t r0 = blk * kKppBlock + (int64_t)kKppRun * j;
+      double rs = 0.0;
+      for (int64_t i = r0; i < r0 + kKppRun && i < n; ++i) rs += dist[i];
+      rsum[j] = rs;
+    }
     __syncthreads();
     if (j == 0) {
       const double run = sh[0], target = sh[1];
       double bs = 0.0;
       int64_t pick = -1;
-      for (int q = 0; q < 256 && pick < 0; ++q) {
+      for (int q = 0; q < kKppRuns && pick < 0; ++q) {
         const int64_t q0 = blk * kKppBlock + (int64_t)kKppRun * q;
         if (q0 >= n) break;
         if (!(run + (bs + rsum[q]) > target)) {
@@ -5167,13 +5200,14 @@ int gmm_kmeanspp(const float* x, int64_t n, int32_t d, int32_t k, const double* 
       ws_bytes < gmm_kmeanspp_workspace_bytes(n))
     return GMM_ERR_WORKSPACE;
   const int64_t nblk = cdiv(n, kKppBlock);
+  const int vec4 = (d & 3) == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0;
   double* dist = static_cast<double*>(ws);
   double* bsum = at<double>(ws, align256((size_t)n * sizeof(double)));
   hipLaunchKernelGGL(k_kpp_select, dim3(1), dim3(256), 0, stream, x, n, d, u, 0, dist, bsum,
                      nblk, idx, centers);
   for (int t = 1; t < k; ++t) {
-    hipLaunchKernelGGL(k_kpp_update, dim3((unsigned)nblk), dim3(1024), 0, stream, x, n, d, idx, t,
-                       t == 1 ? 1 : 0, dist, bsum);
+    hipLaunchKernelGGL(k_kpp_update, dim3((unsigned)nblk), dim3(256), 0, stream, x, n, d, vec4,
+                       idx, t, t == 1 ? 1 : 0, dist, bsum);
     hipLaunchKernelGGL(k_kpp_select, dim3(1), dim3(256), 0, stream, x, n, d, u, t, dist, bsum,
                        nblk, idx, centers);
   }
