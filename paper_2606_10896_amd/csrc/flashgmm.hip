@@ -2661,7 +2661,7 @@ __global__ __launch_bounds__(64) void k_sparse_scatter(
 // end of batch t), so that no memory round trip is waited for within a
 // batch.  Each of the NWV waves owns CW slots of the bucket and one of DS
 // parts of the dimensions (DS = 2 for buckets of four slots, else 1) and
-// takes its slots' pairs of a batch in order, two at a time; lane l owns the
+// takes its slots' pairs of a batch in order, up to four at a time; lane l owns the
 // part's dimensions l, l + 64, ... and adds r x and r x^2 of them in fp64
 // (r x is exact), and r itself (N_k, every lane the same sum; lane 0 of the
 // first part writes it).
