@@ -1466,53 +1466,65 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
   // candidates: lane states whose maximum is within the window of the screening log2 Z
   float XT[16 * NT];                 // candidate mass per lane state, summed below
   unsigned cbits = 0u;               // this lane's candidate lane states, bit 16 blk + v
+  // every operand read and every exp2 taken without branches; the pass is
+  // compiled once per place of the thresholds (LDS or global memory), so that
+  // each read is a plain LDS or global load
+  auto cand_pass = [&](const float2* __restrict__ tsrc) {
 #pragma unroll
-  for (int v = 0; v < 16; ++v) {
-    const int p = 8 * (v >> 2) + 4 * h + (v & 3);
+    for (int v = 0; v < 16; ++v) {
+      const int p = 8 * (v >> 2) + 4 * h + (v & 3);
 #pragma unroll
-    for (int blk = 0; blk < NT; ++blk) {
-      const int pp = blk * 32 + p;
-      const float mv = blk ? m1[v] : m0[v];
-      const float sv = blk ? s1[v] : s0[v];
-      const int av = blk ? a1[v] : a0[v];
-      // refined: within the component's window, or among the point's four
-      // largest lane states (those fill the exact top-kT list); refined in full
-      // (every component of the lane state) when the screening error of its
-      // other components' mass (bound: that mass times the arg-max component's
-      // relative error bound) could exceed kFullErr of the point's total
-      const float rel = mv - lzm[pp];
-      const float2 tf = av >= 0 ? (thr_lds ? thr_s[av] : thr[av]) : make_float2(0.0f, 0.0f);
-      const bool full = REFINE && av >= 0 && (sv - 1.0f) * exp2_fast(rel) * tf.y > kFullErr;
-      const bool cand = av >= 0 && (full || rel > tf.x ||
-                                    (mv >= s4m[pp] && rel > -(float)kWideWindow));
-      if (cand) cbits |= 1u << (16 * blk + v);
-      XT[16 * blk + v] = cand ? (full ? sv : 1.0f) * exp2_fast(mv - stw[wave][pp].x) : 0.0f;
-      const bool sig = bmask != nullptr && av >= 0 && rel > -kDenseWindow;
-      const bool oth = sig && (sv - 1.0f) * exp2_fast(rel) > kDenseMass;
-      if constexpr (B16) {
-        // one flag byte per lane state (IllStage's space is free now); the
-        // (point, wave) masks are assembled from them below
-        unsigned char* fl = smem + IST_OFF;
-        fl[pp * 128 + wave * 32 + col] =
-            (unsigned char)((cand ? 1 : 0) | (full ? 2 : 0) | (sig ? 4 : 0) | (oth ? 8 : 0));
-      } else {
-        const unsigned long long bal = __ballot(cand);
-        const unsigned long long balf = __ballot(full);
-        if (col == 0) {
-          cmask[pp][wave] = (unsigned)(bal >> (32 * h));
-          fmask[pp][wave] = (unsigned)(balf >> (32 * h));
-        }
-        if (bmask != nullptr) {
-          const unsigned long long bals = __ballot(sig);
-          const unsigned long long balo = __ballot(oth);
+      for (int blk = 0; blk < NT; ++blk) {
+        const int pp = blk * 32 + p;
+        const float mv = blk ? m1[v] : m0[v];
+        const float sv = blk ? s1[v] : s0[v];
+        const int av = blk ? a1[v] : a0[v];
+        const bool valid = av >= 0;
+        // refined: within the component's window, or among the point's four
+        // largest lane states (those fill the exact top-kT list); refined in
+        // full (every component of the lane state) when the screening error of
+        // its other components' mass (bound: that mass times the arg-max
+        // component's relative error bound) could exceed kFullErr of the
+        // point's total
+        const float rel = mv - lzm[pp];
+        const float s4 = s4m[pp], swx = stw[wave][pp].x;
+        const float2 tr = tsrc[valid ? av : 0];
+        const float2 tf = valid ? tr : make_float2(0.0f, 0.0f);
+        const float er = exp2_fast(rel), ex = exp2_fast(mv - swx);
+        const bool full = REFINE & valid & ((sv - 1.0f) * er * tf.y > kFullErr);
+        const bool cand =
+            valid & (full | (rel > tf.x) | ((mv >= s4) & (rel > -(float)kWideWindow)));
+        if (cand) cbits |= 1u << (16 * blk + v);
+        XT[16 * blk + v] = cand ? (full ? sv : 1.0f) * ex : 0.0f;
+        const bool sig = (bmask != nullptr) & valid & (rel > -kDenseWindow);
+        const bool oth = sig & ((sv - 1.0f) * er > kDenseMass);
+        if constexpr (B16) {
+          // one flag byte per lane state (IllStage's space is free now); the
+          // (point, wave) masks are assembled from them below
+          unsigned char* fl = smem + IST_OFF;
+          fl[pp * 128 + wave * 32 + col] =
+              (unsigned char)((cand ? 1 : 0) | (full ? 2 : 0) | (sig ? 4 : 0) | (oth ? 8 : 0));
+        } else {
+          const unsigned long long bal = __ballot(cand);
+          const unsigned long long balf = __ballot(full);
           if (col == 0) {
-            smask[pp][wave] = (unsigned)(bals >> (32 * h));
-            omask[pp][wave] = (unsigned)(balo >> (32 * h));
+            cmask[pp][wave] = (unsigned)(bal >> (32 * h));
+            fmask[pp][wave] = (unsigned)(balf >> (32 * h));
+          }
+          if (bmask != nullptr) {
+            const unsigned long long bals = __ballot(sig);
+            const unsigned long long balo = __ballot(oth);
+            if (col == 0) {
+              smask[pp][wave] = (unsigned)(bals >> (32 * h));
+              omask[pp][wave] = (unsigned)(balo >> (32 * h));
+            }
           }
         }
       }
     }
-  }
+  };
+  if (thr_lds) cand_pass(thr_s);
+  else cand_pass(thr);
   xpose_levels<16 * NT>(col, [&](auto jc, auto hc, int off, bool up) {
     constexpr int j = decltype(jc)::value, half = decltype(hc)::value;
     const float kt = up ? XT[j + half] : XT[j], st = up ? XT[j] : XT[j + half];
@@ -1622,12 +1634,15 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
         if (B16 && vec4) {
           // kRefLanes lanes per entry: lane g of a group sums, in fp64, the float4
           // chunks g, g + kRefLanes, ... of the row (coalesced over the group),
-          // and the group adds its partial sums in a fixed butterfly order
+          // and the group adds its partial sums in a fixed butterfly order.
+          // Compiled once per place of the slots' components (LDS or global
+          // memory), so that each lookup is a plain LDS or global load.
           constexpr int G = kRefLanes, NCK = D64 / 4 / G;
           const int g = tid & (G - 1);
+          auto refine_entries = [&](const int* __restrict__ widx) {
           for (int j = lo + tid / G; j < hi; j += 256 / G) {
             const int e = rlist[j - lo], pp = e >> 16;
-            const int comp = thr_lds ? wid_s[e & 0xFFFF] : well_idx[e & 0xFFFF];
+            const int comp = widx[e & 0xFFFF];
             const float* xr = x + (n0 + pp) * d;
             const float* mu = dmu + (size_t)comp * D64;
             const double* hh = dh + (size_t)comp * D64;
@@ -1661,10 +1676,15 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
               rres[j - lo] = (float)((cd - acc) - ref);
             }
           }
+          };
+          if (thr_lds) refine_entries(wid_s);
+          else refine_entries(well_idx);
         } else {
           for (int j = lo + tid; j < hi; j += 256) {
             const int e = rlist[j - lo], pp = e >> 16;
-            const int comp = thr_lds ? wid_s[e & 0xFFFF] : well_idx[e & 0xFFFF];
+            int comp;
+            if (thr_lds) comp = wid_s[e & 0xFFFF];
+            else comp = well_idx[e & 0xFFFF];
             const double ref = lzm[pp] > -INFINITY ? (double)lzm[pp] : 0.0;
             const double l =
                 B16 ? ill_logit_gr(x + (n0 + pp) * d, d, vec4, dmu + (size_t)comp * D64,
