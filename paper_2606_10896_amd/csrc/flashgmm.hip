@@ -897,11 +897,12 @@ __device__ __forceinline__ void logz_group16(const float* xs, const bf16x8* __re
 // (NV = 32) or col / 2 (NV = 16): 31 merges per lane instead of 5 NV.
 // j and half reach comb as std::integral_constant, so that the register
 // arrays it indexes stay in registers.
-template <int J, int HALF, class Comb>
-__device__ __forceinline__ void xpose_pairs(Comb& comb, int off, bool up) {
+template <int J, int HALF, int OFF, class Comb>
+__device__ __forceinline__ void xpose_pairs(Comb& comb, bool up) {
   if constexpr (J < HALF) {
-    comb(std::integral_constant<int, J>{}, std::integral_constant<int, HALF>{}, off, up);
-    xpose_pairs<J + 1, HALF>(comb, off, up);
+    comb(std::integral_constant<int, J>{}, std::integral_constant<int, HALF>{},
+         std::integral_constant<int, OFF>{}, up);
+    xpose_pairs<J + 1, HALF, OFF>(comb, up);
   }
 }
 
@@ -910,11 +911,34 @@ __device__ __forceinline__ void xpose_levels(int col, Comb&& comb) {
   if constexpr (LVL < 5) {
     constexpr int off = 16 >> LVL, cnt = NV >> LVL;
     if constexpr (cnt > 1)
-      xpose_pairs<0, cnt / 2>(comb, off, (col & off) != 0);
+      xpose_pairs<0, cnt / 2, off>(comb, (col & off) != 0);
     else
-      comb(std::integral_constant<int, 0>{}, std::integral_constant<int, 0>{}, off, false);
+      comb(std::integral_constant<int, 0>{}, std::integral_constant<int, 0>{},
+           std::integral_constant<int, off>{}, false);
     xpose_levels<NV, LVL + 1>(col, comb);
   }
+}
+
+// v of lane (lane ^ OFF), OFF a constant: a DPP quad permutation for 1 and 2
+// (no data-share instruction), a swizzle within 32 lanes for 4, 8 and 16 (no
+// lane-index operand), a permute for 32.
+template <int OFF>
+__device__ __forceinline__ int xshfl_i(int v) {
+  if constexpr (OFF == 1) return __builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, false);
+  else if constexpr (OFF == 2) return __builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, false);
+  else if constexpr (OFF == 4 || OFF == 8 || OFF == 16)
+    return __builtin_amdgcn_ds_swizzle(v, 0x1F | (OFF << 10));
+  else return __shfl_xor(v, OFF);
+}
+template <int OFF>
+__device__ __forceinline__ float xshfl(float v) {
+  return __int_as_float(xshfl_i<OFF>(__float_as_int(v)));
+}
+template <int OFF>
+__device__ __forceinline__ double xshfl(double v) {
+  const long long b = __double_as_longlong(v);
+  const int lo = xshfl_i<OFF>((int)(b & 0xFFFFFFFFll)), hi = xshfl_i<OFF>((int)(b >> 32));
+  return __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
 }
 
 // The point whose reduction xpose_levels leaves in lane (h, col): value index
@@ -1280,14 +1304,15 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
         XB[16 + v] = kEmpty;
       }
     }
-    xpose_levels<NV>(col, [&](auto jc, auto hc, int off, bool up) {
+    xpose_levels<NV>(col, [&](auto jc, auto hc, auto oc, bool up) {
       constexpr int j = decltype(jc)::value, half = decltype(hc)::value;
+      constexpr int off = decltype(oc)::value;
       const float km = up ? XM[j + half] : XM[j], sm = up ? XM[j] : XM[j + half];
       const float ks = up ? XS[j + half] : XS[j], ss = up ? XS[j] : XS[j + half];
       const float ka = up ? XA[j + half] : XA[j], sa = up ? XA[j] : XA[j + half];
       const float kb = up ? XB[j + half] : XB[j], sb = up ? XB[j] : XB[j + half];
-      const float rm = __shfl_xor(sm, off), rs = __shfl_xor(ss, off);
-      const float ra = __shfl_xor(sa, off), rb = __shfl_xor(sb, off);
+      const float rm = xshfl<off>(sm), rs = xshfl<off>(ss);
+      const float ra = xshfl<off>(sa), rb = xshfl<off>(sb);
       float M = km, S = ks;
       lse_merge(M, S, rm, rs);
       XM[j] = M;
@@ -1525,10 +1550,11 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
   };
   if (thr_lds) cand_pass(thr_s);
   else cand_pass(thr);
-  xpose_levels<16 * NT>(col, [&](auto jc, auto hc, int off, bool up) {
+  xpose_levels<16 * NT>(col, [&](auto jc, auto hc, auto oc, bool up) {
     constexpr int j = decltype(jc)::value, half = decltype(hc)::value;
+    constexpr int off = decltype(oc)::value;
     const float kt = up ? XT[j + half] : XT[j], st = up ? XT[j] : XT[j + half];
-    XT[j] = kt + __shfl_xor(st, off);
+    XT[j] = kt + xshfl<off>(st);
   });
   if (NT == 2 || (col & 1) == 0) cms[wave][xpose_point<NT>(col, h)] = XT[0];
   __syncthreads();
@@ -1669,8 +1695,9 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_logz(
               u = (double)xv[t].z - (double)mv[t].z; acc = fma(u * u, g1[t].x, acc);
               u = (double)xv[t].w - (double)mv[t].w; acc = fma(u * u, g1[t].y, acc);
             }
-  #pragma unroll
-            for (int o = 1; o < G; o <<= 1) acc += __shfl_xor(acc, o);
+            static_assert(G == 4, "the butterfly below takes four lanes");
+            acc += xshfl<1>(acc);
+            acc += xshfl<2>(acc);
             if (g == 0) {
               const double ref = lzm[pp] > -INFINITY ? (double)lzm[pp] : 0.0;
               rres[j - lo] = (float)((cd - acc) - ref);
