@@ -3490,21 +3490,27 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_assign_collect
         return 0.0f;
       }
     };
+    // the sums take every value, a candidate's as -inf (which adds nothing);
+    // the rare candidates are pushed under a wave-uniform test, so that the
+    // common path has no branch between the MFMAs
     assign_screen<D64>(xs, xa, wp, wpb, cw, n_wkb, pre,
                        [&](int v, float l0, float l1, int slot, float bj) {
       const int p = 8 * (v >> 2) + 4 * h + (v & 3);
-      if (l0 >= th0[v] - bj && l0 > -INFINITY) {
-        const int pos = atomicAdd(&ccnt[p], 1);
-        if (pos < kACap) cand[p][pos] = slot;
-      } else {
-        lse_add_e(m0[v], s0[v], l0);
-      }
+      const bool c0 = (l0 >= th0[v] - bj) & (l0 > -INFINITY);
+      lse_add_e(m0[v], s0[v], c0 ? -INFINITY : l0);
+      bool c1 = false;
       if constexpr (NT == 2) {
-        if (l1 >= th1[v] - bj && l1 > -INFINITY) {
+        c1 = (l1 >= th1[v] - bj) & (l1 > -INFINITY);
+        lse_add_e(m1[v], s1[v], c1 ? -INFINITY : l1);
+      }
+      if (__ballot(c0 | c1) != 0ull) {
+        if (c0) {
+          const int pos = atomicAdd(&ccnt[p], 1);
+          if (pos < kACap) cand[p][pos] = slot;
+        }
+        if (c1) {
           const int pos = atomicAdd(&ccnt[32 + p], 1);
           if (pos < kACap) cand[32 + p][pos] = slot;
-        } else {
-          lse_add_e(m1[v], s1[v], l1);
         }
       }
     });
@@ -3513,10 +3519,16 @@ __global__ __launch_bounds__(256, screen_b16(D64) ? 2 : 1) void k_assign_collect
   for (int v = 0; v < 16; ++v) {
     const int p = 8 * (v >> 2) + 4 * h + (v & 3);
     float M0 = m0[v], S0 = s0[v], M1 = m1[v], S1 = s1[v];
-    for (int off = 16; off > 0; off >>= 1) {
-      lse_merge(M0, S0, __shfl_xor(M0, off), __shfl_xor(S0, off));
-      if constexpr (NT == 2) lse_merge(M1, S1, __shfl_xor(M1, off), __shfl_xor(S1, off));
-    }
+    auto merge = [&](auto oc) {
+      constexpr int off = decltype(oc)::value;
+      lse_merge(M0, S0, xshfl<off>(M0), xshfl<off>(S0));
+      if constexpr (NT == 2) lse_merge(M1, S1, xshfl<off>(M1), xshfl<off>(S1));
+    };
+    merge(std::integral_constant<int, 16>{});
+    merge(std::integral_constant<int, 8>{});
+    merge(std::integral_constant<int, 4>{});
+    merge(std::integral_constant<int, 2>{});
+    merge(std::integral_constant<int, 1>{});
     if (col == 0) {
       stw[wave][p] = make_float2(M0, S0);
       if constexpr (NT == 2) stw[wave][32 + p] = make_float2(M1, S1);
