@@ -40,10 +40,12 @@
 // component collapsing onto one point, beyond any fp32 accumulation.
 //
 // Results are bitwise reproducible run to run: every sum runs in a fixed
-// order.  The only atomics are LDS counters with which the assignment
-// kernels append candidates to per-point lists; a list is sorted before its
-// terms are summed, and the fallback's list of points only decides which
-// points a workgroup visits, each point's result being its own.
+// order.  The only atomics are LDS integer counters: the exact pairs' counts
+// per bucket (sums of ones, the same in any order) and the counters with
+// which the assignment kernels append candidates to per-point lists; a list
+// is sorted before its terms are summed, and the fallback's list of points
+// only decides which points a workgroup visits, each point's result being
+// its own.
 
 #include <hip/hip_runtime.h>
 
